@@ -1,0 +1,537 @@
+/*
+ * CPU oracle for one multi-signal iteration of a growing self-organizing network
+ * (Parigi, Stramieri, Pau, Piastra: "A Multi-signal Variant for the GPU-based
+ * Parallelization of Growing Self-Organizing Networks").
+ *
+ * TEST INFRASTRUCTURE, NOT PART OF THE PRODUCT.  These routines define the results the
+ * HIP path must reproduce.  They share no source, header, table or helper with the HIP
+ * path.  Only the test suite, the smoke check and the CPU-baseline leg of the benchmark
+ * load this library.
+ *
+ * Every step is a plain sequential loop written in the order the paper states the
+ * iteration (Sec. 2.1 "basic iteration", Sec. 2.2 "multi-signal variant"):
+ *
+ *   find winners   Sec. 2.1 step 2 / Sec. 2.2 step 2: exhaustive k = 2 nearest search.
+ *   resolve        Sec. 2.2, collision kinds and the implicit lock: among signals whose
+ *                  updates would touch a common unit, one survivor, the others discarded.
+ *   adapt          Sec. 2.1 step 3, Eq. (adaptation), with eta(i,b) = 1 iff connected.
+ *   update edges   Sec. 2.1 step 3: create or reset the winner-second connection, age
+ *                  the winner's connections (footnote: GNG aging), drop old ones.
+ *   grow           Sec. 2.1, insertion near the unit of largest accumulated error (GNG);
+ *                  removal of units left without connections.
+ *
+ * Readings of points the paper leaves open (all fixed here, the HIP path follows them):
+ *   - distance: squared Euclidean distance in IEEE binary32, computed exactly as
+ *       dx = sx - wx; dy = sy - wy; dz = sz - wz; d = (dx*dx + dy*dy) + dz*dz
+ *     with every operation rounded to nearest even, no fused multiply-add, no sqrt
+ *     (the square root is monotone, so the order of units is the same, but rounding
+ *     it could merge distinct values into ties);
+ *   - ties: the order is lexicographic on (d, unit index); the second winner is the
+ *     minimum over all units other than the winner;
+ *   - snapshot: all winners, all neighbourhoods and all conflicts are taken from the
+ *     state before the iteration;
+ *   - lock scope: a signal j claims L_j = {b_j, s_j} plus the pre-iteration neighbours
+ *     of b_j; its key is (bits(d1_j) << 32) | j; j survives iff no other signal with a
+ *     smaller key claims a unit of L_j (one round, no re-admission);
+ *   - adaptation step (the equation prints a norm where a vector is meant):
+ *       t = xi - w;  t = eps * t;  w = w + t   per component, binary32;
+ *     eps_b for b_j, eps_n for each unit of N(b_j) plus s_j (s_j moved once);
+ *   - order inside one accepted signal: age every edge at b_j by one, then set the
+ *     edge {b_j, s_j} to age 0 (creating it if absent), then remove the edges at b_j
+ *     whose age exceeds max_age;
+ *   - error: err[b_j] += d1_j for accepted signals, then err[i] *= beta for every unit
+ *     once per iteration;
+ *   - removal: a unit is removed (stable compaction) only if its last edge was removed
+ *     by aging since the last grow call; units that never had edges stay;
+ *   - insertion: q = argmax err, f = argmax err over N(q) (ties to the lower index),
+ *     w_r = (w_q + w_f) * 0.5, edge {q,f} replaced by {q,r} and {r,f} at age 0,
+ *     err_q *= alpha, err_f *= alpha, err_r = err_q; skipped when N(q) is empty.
+ *
+ * Build: gcc -O2 -ffp-contract=off -fopenmp -shared -fPIC (no -ffast-math, no -march).
+ */
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#include <math.h>
+
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define ORC_OK 0
+#define ORC_E_INVAL -1
+#define ORC_E_CAPACITY -2
+#define ORC_E_STATE -4
+
+typedef struct {
+  float eps_b;
+  float eps_n;
+  int32_t max_age;
+  float err_alpha;
+  float err_beta;
+  int32_t n_max;
+  int32_t e_max;
+  int32_t m_max;
+} orc_params;
+
+typedef struct {
+  orc_params p;
+  int32_t n;        /* live units */
+  int64_t n_edges;  /* undirected edges */
+  float *x, *y, *z, *err;
+  int32_t *deg;     /* neighbours per unit */
+  int32_t *cap;     /* allocated length of nb[u] / ag[u] */
+  int32_t **nb;     /* neighbour ids of u, ascending */
+  int32_t **ag;     /* age of edge {u, nb[u][k]} */
+  uint8_t *orphan;  /* 1: last edge removed by aging since the last grow call */
+  int32_t status;   /* sticky error */
+} orc_net;
+
+/* ------------------------------------------------------------------ adjacency --- */
+
+static int32_t edge_pos(const orc_net* g, int32_t u, int32_t v) {
+  for (int32_t k = 0; k < g->deg[u]; ++k)
+    if (g->nb[u][k] == v) return k;
+  return -1;
+}
+
+static int half_insert(orc_net* g, int32_t u, int32_t v, int32_t age) {
+  if (g->deg[u] == g->cap[u]) {
+    int32_t nc = g->cap[u] ? 2 * g->cap[u] : 8;
+    int32_t* nb = (int32_t*)realloc(g->nb[u], sizeof(int32_t) * (size_t)nc);
+    if (!nb) return ORC_E_CAPACITY;
+    g->nb[u] = nb;
+    int32_t* ag = (int32_t*)realloc(g->ag[u], sizeof(int32_t) * (size_t)nc);
+    if (!ag) return ORC_E_CAPACITY;
+    g->ag[u] = ag;
+    g->cap[u] = nc;
+  }
+  /* keep the row ascending by neighbour id */
+  int32_t k = g->deg[u];
+  while (k > 0 && g->nb[u][k - 1] > v) {
+    g->nb[u][k] = g->nb[u][k - 1];
+    g->ag[u][k] = g->ag[u][k - 1];
+    --k;
+  }
+  g->nb[u][k] = v;
+  g->ag[u][k] = age;
+  g->deg[u] += 1;
+  return ORC_OK;
+}
+
+static void half_remove(orc_net* g, int32_t u, int32_t v) {
+  int32_t k = edge_pos(g, u, v);
+  if (k < 0) return;
+  for (; k + 1 < g->deg[u]; ++k) {
+    g->nb[u][k] = g->nb[u][k + 1];
+    g->ag[u][k] = g->ag[u][k + 1];
+  }
+  g->deg[u] -= 1;
+}
+
+static int add_edge(orc_net* g, int32_t u, int32_t v, int32_t age) {
+  int rc = half_insert(g, u, v, age);
+  if (rc) return rc;
+  rc = half_insert(g, v, u, age);
+  if (rc) return rc;
+  g->n_edges += 1;
+  return ORC_OK;
+}
+
+static void remove_edge(orc_net* g, int32_t u, int32_t v) {
+  half_remove(g, u, v);
+  half_remove(g, v, u);
+  g->n_edges -= 1;
+}
+
+static void set_age(orc_net* g, int32_t u, int32_t v, int32_t age) {
+  int32_t k = edge_pos(g, u, v);
+  if (k >= 0) g->ag[u][k] = age;
+  k = edge_pos(g, v, u);
+  if (k >= 0) g->ag[v][k] = age;
+}
+
+static int32_t get_age(const orc_net* g, int32_t u, int32_t v) {
+  int32_t k = edge_pos(g, u, v);
+  return k >= 0 ? g->ag[u][k] : -1;
+}
+
+/* ------------------------------------------------------------- create/destroy --- */
+
+void orc_destroy(orc_net* g) {
+  if (!g) return;
+  if (g->nb)
+    for (int32_t u = 0; u < g->p.n_max; ++u) free(g->nb[u]);
+  if (g->ag)
+    for (int32_t u = 0; u < g->p.n_max; ++u) free(g->ag[u]);
+  free(g->nb); free(g->ag); free(g->deg); free(g->cap);
+  free(g->x); free(g->y); free(g->z); free(g->err); free(g->orphan);
+  free(g);
+}
+
+static int params_ok(const orc_params* p) {
+  if (!p) return 0;
+  if (!(p->eps_b >= 0.0f && p->eps_b <= 1.0f)) return 0;
+  if (!(p->eps_n >= 0.0f && p->eps_n <= 1.0f)) return 0;
+  if (p->max_age < 0) return 0;
+  if (p->n_max < 2 || p->e_max < 0 || p->m_max < 1) return 0;
+  return 1;
+}
+
+/* xyz: SoA [3][n0] binary32 (all x, then all y, then all z). */
+int orc_create(const orc_params* p, int32_t n0, const float* xyz, orc_net** out) {
+  if (!out) return ORC_E_INVAL;
+  *out = NULL;
+  if (!params_ok(p) || n0 < 0 || n0 > p->n_max || (n0 > 0 && !xyz)) return ORC_E_INVAL;
+  orc_net* g = (orc_net*)calloc(1, sizeof(orc_net));
+  if (!g) return ORC_E_CAPACITY;
+  g->p = *p;
+  size_t nm = (size_t)p->n_max;
+  g->x = (float*)calloc(nm, sizeof(float));
+  g->y = (float*)calloc(nm, sizeof(float));
+  g->z = (float*)calloc(nm, sizeof(float));
+  g->err = (float*)calloc(nm, sizeof(float));
+  g->deg = (int32_t*)calloc(nm, sizeof(int32_t));
+  g->cap = (int32_t*)calloc(nm, sizeof(int32_t));
+  g->nb = (int32_t**)calloc(nm, sizeof(int32_t*));
+  g->ag = (int32_t**)calloc(nm, sizeof(int32_t*));
+  g->orphan = (uint8_t*)calloc(nm, 1);
+  if (!g->x || !g->y || !g->z || !g->err || !g->deg || !g->cap || !g->nb || !g->ag ||
+      !g->orphan) {
+    orc_destroy(g);
+    return ORC_E_CAPACITY;
+  }
+  g->n = n0;
+  for (int32_t i = 0; i < n0; ++i) {
+    g->x[i] = xyz[i];
+    g->y[i] = xyz[(size_t)n0 + i];
+    g->z[i] = xyz[2 * (size_t)n0 + i];
+  }
+  *out = g;
+  return ORC_OK;
+}
+
+/* ---------------------------------------------------------------- find winners --- */
+
+/* (da, ia) < (db, ib) in the lexicographic order on (distance, unit index). */
+static int key_less(float da, int32_t ia, float db, int32_t ib) {
+  return da < db || (da == db && ia < ib);
+}
+
+/*
+ * For every signal j: b_j = the unit of smallest (d, index), s_j = the unit of smallest
+ * (d, index) among the others; d1_j, d2_j their distances.  sig: SoA [3][m].
+ * Signals are independent, so they may be shared out over threads; each signal's scan
+ * is the same sequential loop whatever the thread count.
+ */
+int orc_find_winners(const orc_net* g, const float* sig, int32_t m, int32_t* winner,
+                     int32_t* second, float* d1, float* d2, int32_t nthreads) {
+  if (!g || m < 0 || m > g->p.m_max) return ORC_E_INVAL;
+  if (g->n < 2) return ORC_E_INVAL;
+  if (m == 0) return ORC_OK;
+  if (!sig || !winner || !second || !d1 || !d2) return ORC_E_INVAL;
+  const int32_t n = g->n;
+  const float *x = g->x, *y = g->y, *z = g->z;
+#ifdef _OPENMP
+  if (nthreads < 1) nthreads = 1;
+#pragma omp parallel for num_threads(nthreads) schedule(dynamic, 16)
+#endif
+  for (int32_t j = 0; j < m; ++j) {
+    const float sx = sig[j], sy = sig[(size_t)m + j], sz = sig[2 * (size_t)m + j];
+    float bd = INFINITY, sd = INFINITY;
+    int32_t bi = -1, si = -1;
+    for (int32_t i = 0; i < n; ++i) {
+      float dx = sx - x[i];
+      float dy = sy - y[i];
+      float dz = sz - z[i];
+      float d = (dx * dx + dy * dy) + dz * dz;
+      if (bi < 0 || key_less(d, i, bd, bi)) {
+        sd = bd; si = bi;
+        bd = d; bi = i;
+      } else if (si < 0 || key_less(d, i, sd, si)) {
+        sd = d; si = i;
+      }
+    }
+    winner[j] = bi; second[j] = si; d1[j] = bd; d2[j] = sd;
+  }
+  (void)nthreads;
+  return ORC_OK;
+}
+
+/* ------------------------------------------------------------- resolve conflicts --- */
+
+static uint64_t signal_key(float d1, int32_t j) {
+  uint32_t bits;
+  memcpy(&bits, &d1, sizeof bits);
+  return ((uint64_t)bits << 32) | (uint32_t)j;
+}
+
+static int check_pair(const orc_net* g, int32_t b, int32_t s) {
+  return b >= 0 && b < g->n && s >= 0 && s < g->n && b != s;
+}
+
+/*
+ * L_j = {b_j, s_j} + N(b_j) on the pre-iteration graph.  owner[u] = the smallest key
+ * among the signals that claim u; j is accepted iff it owns every unit of L_j.
+ */
+int orc_resolve_conflicts(const orc_net* g, int32_t m, const int32_t* winner,
+                          const int32_t* second, const float* d1, uint8_t* accepted) {
+  if (!g || m < 0 || m > g->p.m_max) return ORC_E_INVAL;
+  if (m == 0) return ORC_OK;
+  if (!winner || !second || !d1 || !accepted) return ORC_E_INVAL;
+  for (int32_t j = 0; j < m; ++j)
+    if (!check_pair(g, winner[j], second[j])) return ORC_E_INVAL;
+  uint64_t* owner = (uint64_t*)malloc(sizeof(uint64_t) * (size_t)(g->n > 0 ? g->n : 1));
+  if (!owner) return ORC_E_CAPACITY;
+  for (int32_t u = 0; u < g->n; ++u) owner[u] = UINT64_MAX;
+  for (int32_t j = 0; j < m; ++j) {
+    const uint64_t key = signal_key(d1[j], j);
+    const int32_t b = winner[j], s = second[j];
+    if (key < owner[b]) owner[b] = key;
+    if (key < owner[s]) owner[s] = key;
+    for (int32_t k = 0; k < g->deg[b]; ++k) {
+      int32_t u = g->nb[b][k];
+      if (key < owner[u]) owner[u] = key;
+    }
+  }
+  for (int32_t j = 0; j < m; ++j) {
+    const uint64_t key = signal_key(d1[j], j);
+    const int32_t b = winner[j], s = second[j];
+    int ok = owner[b] == key && owner[s] == key;
+    for (int32_t k = 0; ok && k < g->deg[b]; ++k) ok = owner[g->nb[b][k]] == key;
+    accepted[j] = (uint8_t)ok;
+  }
+  free(owner);
+  return ORC_OK;
+}
+
+/* ---------------------------------------------------------------------- adapt --- */
+
+/* w <- w + eps * (xi - w), one rounding per operation, per component. */
+static void move_unit(orc_net* g, int32_t u, float eps, float sx, float sy, float sz) {
+  float t;
+  t = sx - g->x[u]; t = eps * t; g->x[u] = g->x[u] + t;
+  t = sy - g->y[u]; t = eps * t; g->y[u] = g->y[u] + t;
+  t = sz - g->z[u]; t = eps * t; g->z[u] = g->z[u] + t;
+}
+
+int orc_adapt(orc_net* g, const float* sig, int32_t m, const int32_t* winner,
+              const int32_t* second, const float* d1, const uint8_t* accepted) {
+  if (!g || m < 0 || m > g->p.m_max) return ORC_E_INVAL;
+  if (m > 0 && (!sig || !winner || !second || !d1 || !accepted)) return ORC_E_INVAL;
+  for (int32_t j = 0; j < m; ++j)
+    if (accepted[j] && !check_pair(g, winner[j], second[j])) return ORC_E_INVAL;
+  for (int32_t j = 0; j < m; ++j) {
+    if (!accepted[j]) continue;
+    const float sx = sig[j], sy = sig[(size_t)m + j], sz = sig[2 * (size_t)m + j];
+    const int32_t b = winner[j], s = second[j];
+    move_unit(g, b, g->p.eps_b, sx, sy, sz);
+    for (int32_t k = 0; k < g->deg[b]; ++k)
+      move_unit(g, g->nb[b][k], g->p.eps_n, sx, sy, sz);
+    if (edge_pos(g, b, s) < 0) move_unit(g, s, g->p.eps_n, sx, sy, sz);
+    g->err[b] = g->err[b] + d1[j];
+  }
+  for (int32_t i = 0; i < g->n; ++i) g->err[i] = g->err[i] * g->p.err_beta;
+  return ORC_OK;
+}
+
+/* --------------------------------------------------------------- update edges --- */
+
+int orc_update_edges(orc_net* g, int32_t m, const int32_t* winner, const int32_t* second,
+                     const uint8_t* accepted) {
+  if (!g || m < 0 || m > g->p.m_max) return ORC_E_INVAL;
+  if (m > 0 && (!winner || !second || !accepted)) return ORC_E_INVAL;
+  for (int32_t j = 0; j < m; ++j)
+    if (accepted[j] && !check_pair(g, winner[j], second[j])) return ORC_E_INVAL;
+  int32_t* tmp = NULL;
+  int32_t tmp_cap = 0;
+  for (int32_t j = 0; j < m; ++j) {
+    if (!accepted[j]) continue;
+    const int32_t b = winner[j], s = second[j];
+    /* 1. age every edge at b */
+    for (int32_t k = 0; k < g->deg[b]; ++k) {
+      int32_t v = g->nb[b][k];
+      set_age(g, b, v, g->ag[b][k] + 1);
+    }
+    /* 2. connect b and s at age 0 */
+    if (edge_pos(g, b, s) >= 0) {
+      set_age(g, b, s, 0);
+    } else {
+      int rc = add_edge(g, b, s, 0);
+      if (rc) { free(tmp); g->status = rc; return rc; }
+    }
+    /* 3. remove the edges at b older than max_age */
+    if (g->deg[b] > tmp_cap) {
+      tmp_cap = g->deg[b];
+      int32_t* t = (int32_t*)realloc(tmp, sizeof(int32_t) * (size_t)tmp_cap);
+      if (!t) { free(tmp); g->status = ORC_E_CAPACITY; return ORC_E_CAPACITY; }
+      tmp = t;
+    }
+    int32_t nd = 0;
+    for (int32_t k = 0; k < g->deg[b]; ++k)
+      if (g->ag[b][k] > g->p.max_age) tmp[nd++] = g->nb[b][k];
+    for (int32_t k = 0; k < nd; ++k) {
+      int32_t v = tmp[k];
+      remove_edge(g, b, v);
+      if (g->deg[v] == 0) g->orphan[v] = 1;
+    }
+  }
+  free(tmp);
+  if (g->n_edges > g->p.e_max) {
+    g->status = ORC_E_CAPACITY;
+    return ORC_E_CAPACITY;
+  }
+  return ORC_OK;
+}
+
+/* ---------------------------------------------------------------------- grow --- */
+
+static int remove_orphans(orc_net* g) {
+  int32_t* newid = (int32_t*)malloc(sizeof(int32_t) * (size_t)(g->n > 0 ? g->n : 1));
+  if (!newid) return ORC_E_CAPACITY;
+  int32_t kept = 0;
+  for (int32_t u = 0; u < g->n; ++u) {
+    int gone = g->orphan[u] && g->deg[u] == 0;
+    newid[u] = gone ? -1 : kept;
+    if (!gone) ++kept;
+  }
+  if (kept == g->n) {
+    free(newid);
+    memset(g->orphan, 0, (size_t)g->p.n_max);
+    return ORC_OK;
+  }
+  for (int32_t u = 0; u < g->n; ++u) {
+    int32_t t = newid[u];
+    if (t < 0) {
+      free(g->nb[u]); free(g->ag[u]);
+      g->nb[u] = NULL; g->ag[u] = NULL; g->cap[u] = 0; g->deg[u] = 0;
+      continue;
+    }
+    /* t <= u: moving downwards never overwrites a unit not yet visited */
+    g->x[t] = g->x[u]; g->y[t] = g->y[u]; g->z[t] = g->z[u]; g->err[t] = g->err[u];
+    if (t != u) {
+      g->nb[t] = g->nb[u]; g->ag[t] = g->ag[u];
+      g->deg[t] = g->deg[u]; g->cap[t] = g->cap[u];
+      g->nb[u] = NULL; g->ag[u] = NULL; g->deg[u] = 0; g->cap[u] = 0;
+    }
+    /* remapping is monotone, so rows stay ascending */
+    for (int32_t k = 0; k < g->deg[t]; ++k) g->nb[t][k] = newid[g->nb[t][k]];
+  }
+  for (int32_t u = kept; u < g->n; ++u) {
+    g->x[u] = 0.0f; g->y[u] = 0.0f; g->z[u] = 0.0f; g->err[u] = 0.0f;
+  }
+  g->n = kept;
+  memset(g->orphan, 0, (size_t)g->p.n_max);
+  free(newid);
+  return ORC_OK;
+}
+
+static int insert_unit(orc_net* g) {
+  if (g->n < 1 || g->n >= g->p.n_max) return ORC_OK;
+  int32_t q = 0;
+  for (int32_t i = 1; i < g->n; ++i)
+    if (g->err[i] > g->err[q]) q = i;
+  if (g->deg[q] == 0) return ORC_OK;
+  int32_t f = g->nb[q][0];
+  for (int32_t k = 1; k < g->deg[q]; ++k) {
+    int32_t v = g->nb[q][k];
+    if (g->err[v] > g->err[f] || (g->err[v] == g->err[f] && v < f)) f = v;
+  }
+  if (g->n_edges + 1 > g->p.e_max) {
+    g->status = ORC_E_CAPACITY;
+    return ORC_E_CAPACITY;
+  }
+  const int32_t r = g->n;
+  g->n += 1;
+  g->x[r] = (g->x[q] + g->x[f]) * 0.5f;
+  g->y[r] = (g->y[q] + g->y[f]) * 0.5f;
+  g->z[r] = (g->z[q] + g->z[f]) * 0.5f;
+  remove_edge(g, q, f);
+  int rc = add_edge(g, q, r, 0);
+  if (!rc) rc = add_edge(g, r, f, 0);
+  if (rc) { g->status = rc; return rc; }
+  g->err[q] = g->err[q] * g->p.err_alpha;
+  g->err[f] = g->err[f] * g->p.err_alpha;
+  g->err[r] = g->err[q];
+  return ORC_OK;
+}
+
+/* Remove orphaned units, then, when iteration % insert_every == 0, insert one unit. */
+int orc_grow(orc_net* g, int32_t iteration, int32_t insert_every) {
+  if (!g || insert_every < 0) return ORC_E_INVAL;
+  int rc = remove_orphans(g);
+  if (rc) return rc;
+  if (insert_every > 0 && iteration > 0 && iteration % insert_every == 0)
+    return insert_unit(g);
+  return ORC_OK;
+}
+
+/* ------------------------------------------------------------- state transfer --- */
+
+int orc_sizes(const orc_net* g, int32_t* n_units, int64_t* n_edges) {
+  if (!g) return ORC_E_INVAL;
+  if (n_units) *n_units = g->n;
+  if (n_edges) *n_edges = g->n_edges;
+  return ORC_OK;
+}
+
+int orc_status(const orc_net* g) { return g ? g->status : ORC_E_INVAL; }
+
+/*
+ * xyz: SoA [3][n]; err: [n]; edges: SoA [3][n_edges] = (u, v, age) with u < v,
+ * ascending by (u, v); orphan: [n].  Any output pointer may be NULL.
+ */
+int orc_export(const orc_net* g, float* xyz, float* err, int32_t* edges, uint8_t* orphan) {
+  if (!g) return ORC_E_INVAL;
+  const size_t n = (size_t)g->n, e = (size_t)g->n_edges;
+  if (xyz)
+    for (size_t i = 0; i < n; ++i) {
+      xyz[i] = g->x[i]; xyz[n + i] = g->y[i]; xyz[2 * n + i] = g->z[i];
+    }
+  if (err) memcpy(err, g->err, sizeof(float) * n);
+  if (orphan) memcpy(orphan, g->orphan, n);
+  if (edges) {
+    size_t t = 0;
+    for (int32_t u = 0; u < g->n; ++u)
+      for (int32_t k = 0; k < g->deg[u]; ++k) {
+        int32_t v = g->nb[u][k];
+        if (v > u) {
+          edges[t] = u; edges[e + t] = v; edges[2 * e + t] = g->ag[u][k];
+          ++t;
+        }
+      }
+  }
+  return ORC_OK;
+}
+
+/* Replace the whole state.  edges: SoA [3][n_edges] = (u, v, age), any order, u != v. */
+int orc_import(orc_net* g, int32_t n, const float* xyz, const float* err, int32_t n_edges,
+               const int32_t* edges) {
+  if (!g || n < 0 || n > g->p.n_max || n_edges < 0 || n_edges > g->p.e_max) return ORC_E_INVAL;
+  if ((n > 0 && !xyz) || (n_edges > 0 && !edges)) return ORC_E_INVAL;
+  for (int32_t k = 0; k < n_edges; ++k) {
+    int32_t u = edges[k], v = edges[n_edges + k], a = edges[2 * n_edges + k];
+    if (u < 0 || v < 0 || u >= n || v >= n || u == v || a < 0) return ORC_E_INVAL;
+  }
+  for (int32_t u = 0; u < g->p.n_max; ++u) g->deg[u] = 0;
+  g->n_edges = 0;
+  g->n = n;
+  for (int32_t i = 0; i < n; ++i) {
+    g->x[i] = xyz[i]; g->y[i] = xyz[(size_t)n + i]; g->z[i] = xyz[2 * (size_t)n + i];
+    g->err[i] = err ? err[i] : 0.0f;
+  }
+  for (int32_t i = n; i < g->p.n_max; ++i) {
+    g->x[i] = 0.0f; g->y[i] = 0.0f; g->z[i] = 0.0f; g->err[i] = 0.0f;
+  }
+  memset(g->orphan, 0, (size_t)g->p.n_max);
+  for (int32_t k = 0; k < n_edges; ++k) {
+    int32_t u = edges[k], v = edges[n_edges + k], a = edges[2 * n_edges + k];
+    if (edge_pos(g, u, v) >= 0) return ORC_E_INVAL;
+    int rc = add_edge(g, u, v, a);
+    if (rc) return rc;
+  }
+  g->status = ORC_OK;
+  return ORC_OK;
+}
+
+int orc_age(const orc_net* g, int32_t u, int32_t v) { return g ? get_age(g, u, v) : -1; }
