@@ -1,0 +1,212 @@
+"""Throughput of the multi-signal iteration on one MI355X.
+
+One step = one whole iteration (find winners -> resolve conflicts -> adapt -> update
+edges) over one batch of m signals, on the genus-3 workload (200,000 units, 16,384 signals
+per iteration, signals drawn from a 4,000,000-point cloud).  All signal batches are
+resident in HBM before the timed region starts.
+
+Prints one JSON line:
+  value            whole-iteration signal-unit distance evaluations per second (m*N/step)
+  signals_per_s    m per step time
+  fw_evals_per_s   m*N per find-winners call (HIP events around the call)
+  roofline         the find-winners scan kernel: algorithmic fp32 FLOP/s (8 per
+                   evaluation) from HIP events around each launch on the library's stream,
+                   against the fp32 vector peak; HBM traffic per launch from rocprofv3
+                   counters when a summary for the current kernel source exists
+  cpu_baseline     the CPU oracle timed on this host's cores on the first iterations of the
+                   same workload
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "signal-unit distance evals/s and signals/s at 1 GPU; % fp32 VALU peak"
+FP32_PEAK_TFLOPS = 157.3     # 256 CUs x 2.4 GHz x 256 fp32 flop/clk (packed FMA)
+FLOPS_PER_EVAL = 8           # 3 sub + 3 mul + 2 add of one squared distance
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "find_winners_genus3_200k_traffic.json")
+SCAN_SOURCE = os.path.join(ROOT, "paper_1503_08294_amd", "csrc", "find_winners.hip")
+
+
+def scan_source_hash() -> str:
+    with open(SCAN_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def load_traffic(launch_evals: int):
+    """Per-launch HBM bytes of the scan kernel from the committed counter summary, or None
+    if there is none or it was taken on another version of the kernel source."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    with open(TRAFFIC_FILE) as f:
+        t = json.load(f)
+    if t.get("source_sha256_16") != scan_source_hash() or t.get("launch_evals") != launch_evals:
+        return None
+    return t.get("bytes_per_launch")
+
+
+def cpu_baseline(wl, units, first_sig_batches, budget_s: float):
+    import oracle
+    threads = max(1, min(16, os.cpu_count() or 1))
+    cap = wl.capacity()
+    p = oracle.Params(wl.eps_b, wl.eps_n, wl.max_age, wl.err_alpha, wl.err_beta,
+                      cap["n_max"], cap["e_max"], cap["m_max"])
+    o = oracle.Oracle(p, units, threads=threads)
+    t0 = time.perf_counter()
+    done = 0
+    for sig in first_sig_batches:
+        o.iterate(sig)
+        done += 1
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    dt = time.perf_counter() - t0
+    evals = wl.m * units.shape[1] * done
+    return {"value": evals / dt, "unit": "evals/s", "cores": threads, "kind": "oracle",
+            "signals_per_s": wl.m * done / dt,
+            "sample": f"first {done} whole iterations of {wl.name} (N={units.shape[1]}, "
+                      f"m={wl.m}), oracle find-winners on {threads} threads",
+            "seconds": dt}
+
+
+def copy_calibration(nbytes: int, reps: int):
+    """A plain device copy of known size, for scaling FETCH_SIZE / WRITE_SIZE counters."""
+    import torch
+    a = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda").fill_(1.0)
+    b = torch.empty_like(a)
+    for _ in range(reps):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": nbytes, "reps": reps}), flush=True)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="genus3_200k")
+    ap.add_argument("--cpu-budget", type=float, default=10.0,
+                    help="seconds of CPU oracle work for the cpu_baseline leg (0 = skip)")
+    ap.add_argument("--copy-calibration", type=int, default=0,
+                    help="only run a plain device copy of this many bytes")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported "
+              "(the path shards by signals across GPUs by design, but only one GPU is used "
+              "here)", file=sys.stderr)
+        sys.exit(2)
+
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration, 5)
+        return
+
+    import numpy as np
+    import torch
+
+    from paper_1503_08294_amd import gsn
+    from paper_1503_08294_amd.clouds import WORKLOADS, SignalStream
+
+    wl = WORKLOADS[args.workload]
+    print(f"[bench] generating {wl.name}: {wl.n_points} cloud points, N={wl.n_units}, "
+          f"m={wl.m}", file=sys.stderr, flush=True)
+    cloud = wl.make_cloud()
+    units = wl.make_units(cloud)
+    stream = SignalStream(cloud, wl.signal_seed)
+    total = args.warmup + args.steps + 1
+    host_sig = np.stack([stream.next(wl.m) for _ in range(total)])      # (T, 3, m)
+    n, m = units.shape[1], wl.m
+
+    torch.cuda.set_device(0)
+    dev_sig = torch.from_numpy(host_sig).cuda()
+    cap = wl.capacity()
+    params = gsn.make_params(wl.eps_b, wl.eps_n, wl.max_age, wl.err_alpha, wl.err_beta,
+                             cap["n_max"], cap["e_max"], cap["m_max"])
+    net = gsn.Network(params, torch.from_numpy(units).cuda())
+
+    def step(t):
+        net.iterate(dev_sig[t])
+        if wl.grow:
+            net.grow(t + 1, wl.insert_every)
+
+    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
+    for t in range(args.warmup):
+        step(t)
+    torch.cuda.synchronize()
+    for w in range(5):
+        gsn.gsn_timing_read(net.h, w)
+    gsn.gsn_timing_enable(net.h, True)
+
+    print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for t in range(args.warmup, args.warmup + args.steps):
+        step(t)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    gsn.gsn_timing_enable(net.h, False)
+    phase = {}
+    for name, w in (("find_scan", gsn.GSN_T_FIND_SCAN), ("find", gsn.GSN_T_FIND),
+                    ("resolve", gsn.GSN_T_RESOLVE), ("adapt", gsn.GSN_T_ADAPT),
+                    ("edges", gsn.GSN_T_EDGES)):
+        ms, cnt = gsn.gsn_timing_read(net.h, w)
+        phase[name] = ms / max(cnt, 1)
+    if net.check() != 0:
+        raise SystemExit(f"device status {net.check()} after the timed steps")
+
+    # one more untimed iteration to report the conflict rate at this state
+    t_last = args.warmup + args.steps
+    acc = net.iterate(dev_sig[t_last])[4]
+    conflict_rate = 1.0 - float(acc.sum().item()) / m
+    n_units, n_edges = net.sizes()
+
+    ms_per_step = 1e3 * elapsed / args.steps
+    scan_s = phase["find_scan"] * 1e-3
+    achieved = FLOPS_PER_EVAL * m * n / scan_s / 1e12
+    traffic = load_traffic(m * n)
+    out = {
+        "metric": METRIC,
+        "value": m * n * args.steps / elapsed,
+        "unit": "evals/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "n_units": n, "m_signals": m,
+                   "cloud_points": wl.n_points, "cloud": "genus-3 tube surface",
+                   "iteration": "find+resolve+adapt+update_edges", "parallelism": "single"},
+        "signals_per_s": m * args.steps / elapsed,
+        "fw_evals_per_s": m * n / (phase["find"] * 1e-3),
+        "fw_frac_fp32_peak": FLOPS_PER_EVAL * m * n / (phase["find"] * 1e-3) / 1e12
+                             / FP32_PEAK_TFLOPS,
+        "phase_ms": phase,
+        "conflict_rate": conflict_rate,
+        "state_after": {"units": n_units, "edges": n_edges},
+        "roofline": {"bound": "alu", "kernel": "fw_scan", "achieved": achieved,
+                     "peak": FP32_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": achieved / FP32_PEAK_TFLOPS, "traffic": traffic,
+                     "flops_per_launch": FLOPS_PER_EVAL * m * n,
+                     "avg_launch_ms": phase["find_scan"]},
+        "cpu_baseline": None,
+    }
+    if args.cpu_budget > 0:
+        print(f"[bench] cpu baseline (~{args.cpu_budget:.0f} s)", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(wl, units, list(host_sig[:30]), args.cpu_budget)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,181 @@
+/*
+ * gsn.h — C ABI of libgsn, the multi-signal growing self-organizing network iteration
+ * on AMD MI355X (gfx950).
+ *
+ * Method: Parigi, Stramieri, Pau, Piastra, "A Multi-signal Variant for the GPU-based
+ * Parallelization of Growing Self-Organizing Networks".  One iteration of the
+ * multi-signal variant (Sec. 2.2) is: sample m signals (done by the caller), find the
+ * winner and second-nearest unit of every signal against the same snapshot of the
+ * network, then update the network for every signal, where signals whose updates would
+ * collide are discarded so that one survivor per collision takes effect.
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * Memory.   Every device buffer is allocated and owned by the caller (for example as a
+ *           torch tensor) and must outlive the handle.  The network state lives in one
+ *           caller-provided device workspace of gsn_workspace_bytes() bytes, aligned to
+ *           256 bytes.  The library allocates only the host-side handle.
+ * Layout.   Points are structure-of-arrays binary32: a buffer "SoA [3][k]" holds all k x
+ *           coordinates, then all y, then all z.  Unit indices are int32 in [0, N).
+ * Streams.  `stream` is a hipStream_t passed as void* (NULL = the default stream).  Calls
+ *           marked "async" only enqueue work on it and return; their device outputs are
+ *           valid once the stream reaches that point.  Calls marked "syncs" wait for the
+ *           stream before returning.
+ * Order.    Within an iteration the calls are gsn_find_winners -> gsn_resolve_conflicts
+ *           -> gsn_adapt -> gsn_update_edges; gsn_grow goes between iterations.  Find and
+ *           resolve may be repeated (they do not change the network); any other order
+ *           returns GSN_E_STATE and enqueues nothing.
+ * Errors.   Argument errors are detected on the host and returned at once, with nothing
+ *           enqueued.  Errors only the device can see (a winner index out of range in a
+ *           caller-supplied array, an edge or unit capacity overflow) set a sticky device
+ *           status that gsn_check() returns; after such an error the network state is
+ *           unspecified.  Nothing throws across the ABI and nothing is printed.
+ * Results.  Every output is a deterministic function of the inputs and the state: the
+ *           same on every run and for every launch configuration (see gsn_tune), and
+ *           equal, element by element, to the sequential definition of each step.
+ * Threads.  A handle serves one host thread at a time.
+ */
+#ifndef GSN_H
+#define GSN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  GSN_OK = 0,
+  GSN_E_INVAL = -1,     /* invalid argument (or, sticky: an invalid index on the device) */
+  GSN_E_CAPACITY = -2,  /* n_max, e_max, m_max or the workspace would be exceeded */
+  GSN_E_HIP = -3,       /* a HIP runtime call failed */
+  GSN_E_STATE = -4      /* call out of the order stated above */
+};
+
+typedef struct gsn_net gsn_net;
+
+/* Parameters.  Learning rates and eta follow Eq. (adaptation) of Sec. 2.1; aging follows
+ * the footnote on connection aging there; err_alpha / err_beta keep the accumulated error
+ * that GNG insertion uses (Sec. 2.1: periodic insertion next to the unit whose accumulated
+ * squared error is largest). */
+typedef struct gsn_params {
+  float eps_b;       /* winner learning rate, in [0, 1] */
+  float eps_n;       /* learning rate of the winner's neighbours and second, in [0, 1] */
+  int32_t max_age;   /* an edge at an accepted winner whose age exceeds this is removed, >= 0 */
+  float err_alpha;   /* error scale applied to q and f when a unit is inserted between them */
+  float err_beta;    /* error decay applied to every unit once per iteration */
+  int32_t n_max;     /* unit capacity, >= 2 */
+  int32_t e_max;     /* undirected edge capacity, >= 0 */
+  int32_t m_max;     /* signals per iteration capacity, >= 1 */
+} gsn_params;
+
+/* Bytes of device workspace a network with these parameters needs; 0 if the parameters
+ * are invalid.  Pure host computation. */
+size_t gsn_workspace_bytes(const gsn_params* params);
+
+/* Create a network of n0 units (0 <= n0 <= n_max) at init_xyz (SoA [3][n0] binary32, host
+ * or device memory), with no edges and zero accumulated error.  workspace: device memory
+ * of at least gsn_workspace_bytes(params) bytes, 256-byte aligned, owned by the caller and
+ * used by this handle only.  Syncs.  On success *out holds the handle. */
+int gsn_create(const gsn_params* params, void* workspace, size_t workspace_bytes, int32_t n0,
+               const float* init_xyz, void* stream, gsn_net** out);
+
+/* Find Winners (Sec. 2.1 step 2; Sec. 2.2 step 2).  For every signal j < m (sig: device
+ * SoA [3][m] binary32) and every unit i < N, the squared distance
+ *     d_ji = (dx*dx + dy*dy) + dz*dz,   dx = sig_x - w_x (likewise y, z),
+ * each operation one binary32 rounding to nearest even, no fused multiply-add.  winner[j]
+ * is the unit of smallest (d, index) in lexicographic order, second[j] the smallest among
+ * the others; d1[j], d2[j] are their distances.  Outputs: device int32[m], int32[m],
+ * float[m], float[m].  Requires N >= 2 and 0 <= m <= m_max (m = 0 does nothing).  Async. */
+int gsn_find_winners(gsn_net* net, const float* sig, int32_t m, int32_t* winner,
+                     int32_t* second, float* d1, float* d2, void* stream);
+
+/* Collision handling (Sec. 2.2: signals whose updates would move the same unit, change
+ * the same neighbourhood or add the same edge collide; an implicit lock lets one of them
+ * take effect and discards the others).  Signal j locks L_j = {winner[j], second[j]} plus the current
+ * neighbours of winner[j]; its key is (bits(d1[j]) << 32) | j.  accepted[j] = 1 iff no
+ * other signal with a smaller key locks a unit of L_j, else 0.  Accepted lock sets are
+ * pairwise disjoint, so the updates below commute.  Inputs: device arrays of length m as
+ * produced by gsn_find_winners (any values with 0 <= winner, second < N and
+ * winner != second; others are rejected and flag GSN_E_INVAL on the device).  Output:
+ * device uint8[m].  Async. */
+int gsn_resolve_conflicts(gsn_net* net, int32_t m, const int32_t* winner,
+                          const int32_t* second, const float* d1, uint8_t* accepted,
+                          void* stream);
+
+/* Adaptation (Sec. 2.1 step 3, Eq. (adaptation), eta(i, b) = 1 iff i and b are
+ * connected).  For every accepted j, with b = winner[j], s = second[j]:
+ *     w <- w + eps * (sig_j - w)   per component as t = sig - w; t = eps * t; w = w + t,
+ * with eps_b for b and eps_n for every current neighbour of b and for s (once).  The
+ * winner's error grows by d1[j]; afterwards every unit's error is multiplied by err_beta.
+ * Inputs as for gsn_resolve_conflicts plus sig (SoA [3][m]).  Async. */
+int gsn_adapt(gsn_net* net, const float* sig, int32_t m, const int32_t* winner,
+              const int32_t* second, const float* d1, const uint8_t* accepted, void* stream);
+
+/* Connection update (Sec. 2.1 step 3 and its footnote on aging).  For every accepted j:
+ * every edge at b = winner[j] ages by one, the edge {b, second[j]} is set to age 0 (and
+ * created if absent), then the edges at b older than max_age are removed; a unit left
+ * with no edge by such a removal is marked for removal by gsn_grow.  The adjacency is then
+ * rewritten as a compacted CSR with rows in ascending neighbour order.  Exceeding e_max
+ * sets GSN_E_CAPACITY on the device.  Async. */
+int gsn_update_edges(gsn_net* net, int32_t m, const int32_t* winner, const int32_t* second,
+                     const uint8_t* accepted, void* stream);
+
+/* Growth (Sec. 2.1: units may be added and removed during the update; GNG inserts next
+ * to the unit of largest accumulated error).  First removes, by stable
+ * compaction (indices shift down, edges are renumbered), every unit marked by
+ * gsn_update_edges that still has no edge.  Then, if insert_every > 0, iteration > 0,
+ * iteration % insert_every == 0 and N < n_max: q = argmax error, f = argmax error over the
+ * neighbours of q (ties to the lower index; nothing happens if q has none); a unit r = N
+ * is added at (w_q + w_f) * 0.5, the edge {q, f} is replaced by {q, r} and {r, f} at age
+ * 0, err_q and err_f are multiplied by err_alpha and err_r = err_q.  Syncs. */
+int gsn_grow(gsn_net* net, int32_t iteration, int32_t insert_every, void* stream);
+
+/* Current unit count N and undirected edge count.  Syncs. */
+int gsn_sizes(gsn_net* net, int32_t* n_units, int32_t* n_edges, void* stream);
+
+/* Copy the state out (any pointer may be NULL; host or device memory): xyz SoA [3][N],
+ * err [N], edges SoA [3][E] = (u, v, age) with u < v in ascending (u, v) order.  Sizes
+ * from gsn_sizes.  Syncs. */
+int gsn_export(gsn_net* net, float* xyz, float* err, int32_t* edges, void* stream);
+
+/* Replace the state: n units at xyz (SoA [3][n]), errors err (NULL = zeros), and n_edges
+ * edges (SoA [3][n_edges] = (u, v, age), any order, u != v, no duplicates, age >= 0).  Host
+ * or device memory.  Clears the removal marks and any sticky error.  Syncs. */
+int gsn_import(gsn_net* net, int32_t n, const float* xyz, const float* err, int32_t n_edges,
+               const int32_t* edges, void* stream);
+
+/* Sticky device status: GSN_OK, or the first GSN_E_INVAL / GSN_E_CAPACITY a kernel
+ * raised since creation or the last gsn_import.  Syncs. */
+int gsn_check(gsn_net* net, void* stream);
+
+/* Free the host handle (the workspace stays the caller's).  NULL is ignored. */
+void gsn_destroy(gsn_net* net);
+
+/* Launch-configuration knobs, for tests and measurement; results never depend on them.
+ *   GSN_TUNE_SPLIT    units are split into this many chunks scanned by separate
+ *                     workgroups and merged afterwards (0 = automatic, 1..GSN_MAX_SPLIT)
+ *   GSN_TUNE_VARIANT  find-winners kernel: 0 = automatic, 1 = direct scan
+ * Returns GSN_E_INVAL for an unknown key or value. */
+enum { GSN_TUNE_SPLIT = 1, GSN_TUNE_VARIANT = 2 };
+#define GSN_MAX_SPLIT 64
+int gsn_tune(gsn_net* net, int32_t key, int32_t value);
+
+/* Kernel timing with HIP events recorded on the caller's stream around each step, for
+ * measurement.  gsn_timing_enable(net, 1) starts recording; gsn_timing_read returns the
+ * summed duration in milliseconds and the number of launches recorded for one step since
+ * the last read, and clears them (syncs).
+ *   GSN_T_FIND_SCAN   the find-winners scan kernel alone
+ *   GSN_T_FIND        all of gsn_find_winners
+ *   GSN_T_RESOLVE, GSN_T_ADAPT, GSN_T_EDGES   all of the corresponding call */
+enum { GSN_T_FIND_SCAN = 0, GSN_T_FIND = 1, GSN_T_RESOLVE = 2, GSN_T_ADAPT = 3,
+       GSN_T_EDGES = 4, GSN_T_COUNT = 5 };
+int gsn_timing_enable(gsn_net* net, int32_t enable);
+int gsn_timing_read(gsn_net* net, int32_t which, double* total_ms, int32_t* launches);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GSN_H */

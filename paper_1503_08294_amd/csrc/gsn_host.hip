@@ -1,0 +1,501 @@
+// Host side of the C ABI declared in include/gsn.h: argument validation, workspace
+// carving, launch configuration, call ordering and event timing.  All device memory is the
+// caller's; this file allocates only the handle (and short-lived host vectors in the
+// synchronous export/import calls).
+#include <stdlib.h>
+#include <string.h>
+
+#include <new>
+#include <vector>
+
+#include "gsn_internal.h"
+
+namespace gsn {
+
+Layout layout_for(const gsn_params& p) {
+  Layout L{};
+  size_t o = 0;
+  int i = 0;
+  auto add = [&](size_t bytes) {
+    o = (o + 255) & ~static_cast<size_t>(255);
+    L.off[i++] = o;
+    o += bytes;
+  };
+  const size_t nm = static_cast<size_t>(p.n_max);
+  const size_t hc = 2 * static_cast<size_t>(p.e_max) + 2;
+  const size_t mm = static_cast<size_t>(p.m_max);
+  add(4 * nm);                 // 0 x
+  add(4 * nm);                 // 1 y
+  add(4 * nm);                 // 2 z
+  add(4 * nm);                 // 3 err
+  add(4 * (nm + 2));           // 4 rp0
+  add(4 * (nm + 2));           // 5 rp1
+  add(4 * hc);                 // 6 col0
+  add(4 * hc);                 // 7 col1
+  add(4 * hc);                 // 8 age0
+  add(4 * hc);                 // 9 age1
+  add(8 * nm);                 // 10 lock
+  add(4 * nm);                 // 11 ins
+  add(4 * nm);                 // 12 orphan
+  add(4 * nm);                 // 13 cnt
+  add(4 * (nm / kBlock + 2));  // 14 bsum
+  add(16 * nm);                // 15 tmp
+  add(4 * kStSlots);           // 16 status
+  add(8 * static_cast<size_t>(kMaxSplit) * 2 * mm);  // 17 part
+  L.total = (o + 255) & ~static_cast<size_t>(255);
+  return L;
+}
+
+void carve(const gsn_params& p, void* base, DevState* s) {
+  const Layout L = layout_for(p);
+  char* b = static_cast<char*>(base);
+  s->x = reinterpret_cast<float*>(b + L.off[0]);
+  s->y = reinterpret_cast<float*>(b + L.off[1]);
+  s->z = reinterpret_cast<float*>(b + L.off[2]);
+  s->err = reinterpret_cast<float*>(b + L.off[3]);
+  s->rp[0] = reinterpret_cast<int32_t*>(b + L.off[4]);
+  s->rp[1] = reinterpret_cast<int32_t*>(b + L.off[5]);
+  s->col[0] = reinterpret_cast<int32_t*>(b + L.off[6]);
+  s->col[1] = reinterpret_cast<int32_t*>(b + L.off[7]);
+  s->age[0] = reinterpret_cast<int32_t*>(b + L.off[8]);
+  s->age[1] = reinterpret_cast<int32_t*>(b + L.off[9]);
+  s->lock = reinterpret_cast<unsigned long long*>(b + L.off[10]);
+  s->ins = reinterpret_cast<int32_t*>(b + L.off[11]);
+  s->orphan = reinterpret_cast<int32_t*>(b + L.off[12]);
+  s->cnt = reinterpret_cast<int32_t*>(b + L.off[13]);
+  s->bsum = reinterpret_cast<int32_t*>(b + L.off[14]);
+  s->tmp = reinterpret_cast<float*>(b + L.off[15]);
+  s->status = reinterpret_cast<int32_t*>(b + L.off[16]);
+  s->part = reinterpret_cast<unsigned long long*>(b + L.off[17]);
+}
+
+}  // namespace gsn
+
+using gsn::DevState;
+
+enum Phase { kReady = 0, kFound = 1, kResolved = 2, kAdapted = 3 };
+
+struct gsn_net {
+  gsn_params p;
+  DevState s;
+  int32_t n;        // live units (host copy, changed only by grow/import)
+  int cur;          // current CSR buffer
+  int phase;
+  int cus;          // compute units of the device
+  int tune_split;
+  int tune_variant;
+  bool timing;
+  std::vector<hipEvent_t> pool;
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> rec[GSN_T_COUNT];
+};
+
+namespace {
+
+bool params_ok(const gsn_params* p) {
+  if (!p) return false;
+  if (!(p->eps_b >= 0.0f && p->eps_b <= 1.0f)) return false;
+  if (!(p->eps_n >= 0.0f && p->eps_n <= 1.0f)) return false;
+  if (p->max_age < 0) return false;
+  if (p->n_max < 2 || p->e_max < 0 || p->m_max < 1) return false;
+  // keep every derived index inside int32
+  if (static_cast<int64_t>(p->e_max) * 2 + 2 > INT32_MAX) return false;
+  if (static_cast<int64_t>(p->n_max) + 2 > INT32_MAX / 4) return false;
+  if (static_cast<int64_t>(p->m_max) * 2 * gsn::kMaxSplit > INT32_MAX) return false;
+  return true;
+}
+
+inline hipStream_t as_stream(void* st) { return static_cast<hipStream_t>(st); }
+
+inline int hip_ok(hipError_t e) { return e == hipSuccess ? GSN_OK : GSN_E_HIP; }
+
+hipEvent_t take_event(gsn_net* net) {
+  if (!net->pool.empty()) {
+    hipEvent_t e = net->pool.back();
+    net->pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+// Records an event pair around the launches made between begin() and end().
+struct TimedRegion {
+  gsn_net* net;
+  int which;
+  hipStream_t st;
+  hipEvent_t a = nullptr;
+  TimedRegion(gsn_net* n, int w, hipStream_t s) : net(n), which(w), st(s) {
+    if (net->timing) {
+      a = take_event(net);
+      if (a && hipEventRecord(a, st) != hipSuccess) {
+        net->pool.push_back(a);
+        a = nullptr;
+      }
+    }
+  }
+  void end() {
+    if (!a) return;
+    hipEvent_t b = take_event(net);
+    if (!b) {
+      net->pool.push_back(a);
+      a = nullptr;
+      return;
+    }
+    if (hipEventRecord(b, st) == hipSuccess) {
+      net->rec[which].emplace_back(a, b);
+    } else {
+      net->pool.push_back(a);
+      net->pool.push_back(b);
+    }
+    a = nullptr;
+  }
+};
+
+int read_status_slot(gsn_net* net, int slot, int32_t* out, hipStream_t st) {
+  if (hipMemcpyAsync(out, net->s.status + slot, sizeof(int32_t), hipMemcpyDeviceToHost, st) !=
+      hipSuccess)
+    return GSN_E_HIP;
+  return hip_ok(hipStreamSynchronize(st));
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t gsn_workspace_bytes(const gsn_params* params) {
+  if (!params_ok(params)) return 0;
+  return gsn::layout_for(*params).total;
+}
+
+int gsn_create(const gsn_params* params, void* workspace, size_t workspace_bytes, int32_t n0,
+               const float* init_xyz, void* stream, gsn_net** out) {
+  if (!out) return GSN_E_INVAL;
+  *out = nullptr;
+  if (!params_ok(params) || !workspace || n0 < 0 || n0 > params->n_max) return GSN_E_INVAL;
+  if (n0 > 0 && !init_xyz) return GSN_E_INVAL;
+  if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0) return GSN_E_INVAL;
+  if (workspace_bytes < gsn::layout_for(*params).total) return GSN_E_CAPACITY;
+  gsn_net* net = new (std::nothrow) gsn_net();
+  if (!net) return GSN_E_CAPACITY;
+  net->p = *params;
+  gsn::carve(*params, workspace, &net->s);
+  net->n = n0;
+  net->cur = 0;
+  net->phase = kReady;
+  net->tune_split = 0;
+  net->tune_variant = 0;
+  net->timing = false;
+  int dev = 0, cus = 256;
+  if (hipGetDevice(&dev) == hipSuccess &&
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess)
+    net->cus = cus;
+  else
+    net->cus = 256;
+  hipStream_t st = as_stream(stream);
+  hipError_t e = gsn::launch_init(net->s, 0, n0, params->n_max, st);
+  const size_t bytes = sizeof(float) * static_cast<size_t>(n0);
+  if (e == hipSuccess && n0 > 0) {
+    e = hipMemcpyAsync(net->s.x, init_xyz, bytes, hipMemcpyDefault, st);
+    if (e == hipSuccess)
+      e = hipMemcpyAsync(net->s.y, init_xyz + n0, bytes, hipMemcpyDefault, st);
+    if (e == hipSuccess)
+      e = hipMemcpyAsync(net->s.z, init_xyz + 2 * static_cast<size_t>(n0), bytes,
+                         hipMemcpyDefault, st);
+  }
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e != hipSuccess) {
+    delete net;
+    return GSN_E_HIP;
+  }
+  *out = net;
+  return GSN_OK;
+}
+
+int gsn_find_winners(gsn_net* net, const float* sig, int32_t m, int32_t* winner,
+                     int32_t* second, float* d1, float* d2, void* stream) {
+  if (!net || m < 0 || m > net->p.m_max) return GSN_E_INVAL;
+  if (net->phase != kReady && net->phase != kFound) return GSN_E_STATE;
+  if (net->n < 2) return GSN_E_INVAL;
+  if (m > 0 && (!sig || !winner || !second || !d1 || !d2)) return GSN_E_INVAL;
+  net->phase = kFound;
+  if (m == 0) return GSN_OK;
+  hipStream_t st = as_stream(stream);
+  const gsn::FindConfig cfg =
+      gsn::find_config(net->n, m, net->cus, net->tune_split, net->tune_variant);
+  TimedRegion all(net, GSN_T_FIND, st);
+  TimedRegion scan(net, GSN_T_FIND_SCAN, st);
+  hipError_t e = gsn::launch_find_scan(net->s, net->n, sig, m, cfg, winner, second, d1, d2, st);
+  scan.end();
+  if (e == hipSuccess) e = gsn::launch_find_merge(net->s, m, cfg, winner, second, d1, d2, st);
+  all.end();
+  return hip_ok(e);
+}
+
+int gsn_resolve_conflicts(gsn_net* net, int32_t m, const int32_t* winner,
+                          const int32_t* second, const float* d1, uint8_t* accepted,
+                          void* stream) {
+  if (!net || m < 0 || m > net->p.m_max) return GSN_E_INVAL;
+  if (net->phase != kFound && net->phase != kResolved) return GSN_E_STATE;
+  if (m > 0 && (!winner || !second || !d1 || !accepted)) return GSN_E_INVAL;
+  net->phase = kResolved;
+  if (m == 0) return GSN_OK;
+  hipStream_t st = as_stream(stream);
+  TimedRegion t(net, GSN_T_RESOLVE, st);
+  hipError_t e = gsn::launch_resolve(net->s, net->cur, net->n, m, winner, second, d1, accepted,
+                                     st);
+  t.end();
+  return hip_ok(e);
+}
+
+int gsn_adapt(gsn_net* net, const float* sig, int32_t m, const int32_t* winner,
+              const int32_t* second, const float* d1, const uint8_t* accepted, void* stream) {
+  if (!net || m < 0 || m > net->p.m_max) return GSN_E_INVAL;
+  if (net->phase != kResolved) return GSN_E_STATE;
+  if (m > 0 && (!sig || !winner || !second || !d1 || !accepted)) return GSN_E_INVAL;
+  net->phase = kAdapted;
+  hipStream_t st = as_stream(stream);
+  TimedRegion t(net, GSN_T_ADAPT, st);
+  hipError_t e = gsn::launch_adapt(net->s, net->cur, net->n, sig, m, winner, second, d1,
+                                   accepted, net->p.eps_b, net->p.eps_n, net->p.err_beta, st);
+  t.end();
+  return hip_ok(e);
+}
+
+int gsn_update_edges(gsn_net* net, int32_t m, const int32_t* winner, const int32_t* second,
+                     const uint8_t* accepted, void* stream) {
+  if (!net || m < 0 || m > net->p.m_max) return GSN_E_INVAL;
+  if (net->phase != kAdapted) return GSN_E_STATE;
+  if (m > 0 && (!winner || !second || !accepted)) return GSN_E_INVAL;
+  hipStream_t st = as_stream(stream);
+  TimedRegion t(net, GSN_T_EDGES, st);
+  hipError_t e = gsn::launch_edges(net->s, net->cur, net->n, m, winner, second, accepted,
+                                   net->p.max_age, 2 * static_cast<int64_t>(net->p.e_max), st);
+  t.end();
+  if (e != hipSuccess) return GSN_E_HIP;
+  net->cur ^= 1;
+  net->phase = kReady;
+  return GSN_OK;
+}
+
+int gsn_grow(gsn_net* net, int32_t iteration, int32_t insert_every, void* stream) {
+  if (!net || insert_every < 0) return GSN_E_INVAL;
+  if (net->phase != kReady) return GSN_E_STATE;
+  hipStream_t st = as_stream(stream);
+  int32_t orphans = 0;
+  int rc = read_status_slot(net, gsn::kStOrphans, &orphans, st);
+  if (rc) return rc;
+  if (orphans > 0) {
+    if (gsn::launch_remove(net->s, net->cur, net->n, net->p.n_max, st) != hipSuccess)
+      return GSN_E_HIP;
+    net->cur ^= 1;
+    int32_t kept = 0;
+    rc = read_status_slot(net, gsn::kStKept, &kept, st);
+    if (rc) return rc;
+    net->n = kept;
+  }
+  if (insert_every > 0 && iteration > 0 && iteration % insert_every == 0 && net->n >= 1 &&
+      net->n < net->p.n_max) {
+    if (gsn::launch_insert(net->s, net->cur, net->n, net->p.err_alpha,
+                           2 * static_cast<int64_t>(net->p.e_max), st) != hipSuccess)
+      return GSN_E_HIP;
+    int32_t inserted = 0;
+    rc = read_status_slot(net, gsn::kStInserted, &inserted, st);
+    if (rc) return rc;
+    net->n += inserted;
+  }
+  return GSN_OK;
+}
+
+int gsn_sizes(gsn_net* net, int32_t* n_units, int32_t* n_edges, void* stream) {
+  if (!net) return GSN_E_INVAL;
+  hipStream_t st = as_stream(stream);
+  int32_t half = 0;
+  if (hipMemcpyAsync(&half, net->s.rp[net->cur] + net->n, sizeof(int32_t),
+                     hipMemcpyDeviceToHost, st) != hipSuccess)
+    return GSN_E_HIP;
+  if (hipStreamSynchronize(st) != hipSuccess) return GSN_E_HIP;
+  if (n_units) *n_units = net->n;
+  if (n_edges) *n_edges = half / 2;
+  return GSN_OK;
+}
+
+int gsn_export(gsn_net* net, float* xyz, float* err, int32_t* edges, void* stream) {
+  if (!net) return GSN_E_INVAL;
+  hipStream_t st = as_stream(stream);
+  const size_t n = static_cast<size_t>(net->n);
+  try {
+    if (hipStreamSynchronize(st) != hipSuccess) return GSN_E_HIP;
+    if (xyz && n > 0) {
+      if (hipMemcpy(xyz, net->s.x, 4 * n, hipMemcpyDefault) != hipSuccess ||
+          hipMemcpy(xyz + n, net->s.y, 4 * n, hipMemcpyDefault) != hipSuccess ||
+          hipMemcpy(xyz + 2 * n, net->s.z, 4 * n, hipMemcpyDefault) != hipSuccess)
+        return GSN_E_HIP;
+    }
+    if (err && n > 0 && hipMemcpy(err, net->s.err, 4 * n, hipMemcpyDefault) != hipSuccess)
+      return GSN_E_HIP;
+    if (edges) {
+      std::vector<int32_t> rp(n + 1);
+      if (hipMemcpy(rp.data(), net->s.rp[net->cur], 4 * (n + 1), hipMemcpyDeviceToHost) !=
+          hipSuccess)
+        return GSN_E_HIP;
+      const size_t half = static_cast<size_t>(rp[n]);
+      std::vector<int32_t> col(half), age(half);
+      if (half > 0 &&
+          (hipMemcpy(col.data(), net->s.col[net->cur], 4 * half, hipMemcpyDeviceToHost) !=
+               hipSuccess ||
+           hipMemcpy(age.data(), net->s.age[net->cur], 4 * half, hipMemcpyDeviceToHost) !=
+               hipSuccess))
+        return GSN_E_HIP;
+      const size_t e = half / 2;
+      std::vector<int32_t> out(3 * e);
+      size_t t = 0;
+      for (size_t u = 0; u < n; ++u)
+        for (int32_t k = rp[u]; k < rp[u + 1]; ++k)
+          if (static_cast<size_t>(col[k]) > u && t < e) {
+            out[t] = static_cast<int32_t>(u);
+            out[e + t] = col[k];
+            out[2 * e + t] = age[k];
+            ++t;
+          }
+      if (e > 0 && hipMemcpy(edges, out.data(), 4 * 3 * e, hipMemcpyDefault) != hipSuccess)
+        return GSN_E_HIP;
+    }
+  } catch (const std::bad_alloc&) {
+    return GSN_E_CAPACITY;
+  }
+  return GSN_OK;
+}
+
+int gsn_import(gsn_net* net, int32_t n, const float* xyz, const float* err, int32_t n_edges,
+               const int32_t* edges, void* stream) {
+  if (!net || n < 0 || n > net->p.n_max || n_edges < 0) return GSN_E_INVAL;
+  if (n_edges > net->p.e_max) return GSN_E_CAPACITY;
+  if ((n > 0 && !xyz) || (n_edges > 0 && !edges)) return GSN_E_INVAL;
+  hipStream_t st = as_stream(stream);
+  try {
+    if (hipStreamSynchronize(st) != hipSuccess) return GSN_E_HIP;
+    const size_t nn = static_cast<size_t>(n), ne = static_cast<size_t>(n_edges);
+    std::vector<int32_t> ed(3 * ne);
+    if (ne > 0 && hipMemcpy(ed.data(), edges, 4 * 3 * ne, hipMemcpyDefault) != hipSuccess)
+      return GSN_E_HIP;
+    std::vector<int32_t> deg(nn + 1, 0);
+    for (size_t k = 0; k < ne; ++k) {
+      const int32_t u = ed[k], v = ed[ne + k], a = ed[2 * ne + k];
+      if (u < 0 || v < 0 || u >= n || v >= n || u == v || a < 0) return GSN_E_INVAL;
+      ++deg[u];
+      ++deg[v];
+    }
+    std::vector<int32_t> rp(nn + 1, 0);
+    for (size_t u = 0; u < nn; ++u) rp[u + 1] = rp[u] + deg[u];
+    std::vector<int32_t> fill(rp.begin(), rp.end() - 1);
+    std::vector<std::pair<int32_t, int32_t>> half(2 * ne);
+    for (size_t k = 0; k < ne; ++k) {
+      const int32_t u = ed[k], v = ed[ne + k], a = ed[2 * ne + k];
+      half[fill[u]++] = {v, a};
+      half[fill[v]++] = {u, a};
+    }
+    std::vector<int32_t> col(2 * ne), age(2 * ne);
+    for (size_t u = 0; u < nn; ++u) {
+      std::sort(half.begin() + rp[u], half.begin() + rp[u + 1]);
+      for (int32_t k = rp[u]; k < rp[u + 1]; ++k) {
+        if (k > rp[u] && half[k].first == half[k - 1].first) return GSN_E_INVAL;
+        col[k] = half[k].first;
+        age[k] = half[k].second;
+      }
+    }
+    net->cur = 0;
+    const DevState& s = net->s;
+    bool ok = true;
+    if (n > 0) {
+      ok = ok && hipMemcpy(s.x, xyz, 4 * nn, hipMemcpyDefault) == hipSuccess;
+      ok = ok && hipMemcpy(s.y, xyz + nn, 4 * nn, hipMemcpyDefault) == hipSuccess;
+      ok = ok && hipMemcpy(s.z, xyz + 2 * nn, 4 * nn, hipMemcpyDefault) == hipSuccess;
+      if (err) {
+        ok = ok && hipMemcpy(s.err, err, 4 * nn, hipMemcpyDefault) == hipSuccess;
+      } else {
+        ok = ok && hipMemset(s.err, 0, 4 * nn) == hipSuccess;
+      }
+    }
+    ok = ok && hipMemcpy(s.rp[0], rp.data(), 4 * (nn + 1), hipMemcpyHostToDevice) == hipSuccess;
+    if (ne > 0) {
+      ok = ok && hipMemcpy(s.col[0], col.data(), 8 * ne, hipMemcpyHostToDevice) == hipSuccess;
+      ok = ok && hipMemcpy(s.age[0], age.data(), 8 * ne, hipMemcpyHostToDevice) == hipSuccess;
+    }
+    const size_t nm = static_cast<size_t>(net->p.n_max);
+    ok = ok && hipMemset(s.ins, 0xff, 4 * nm) == hipSuccess;
+    ok = ok && hipMemset(s.orphan, 0, 4 * nm) == hipSuccess;
+    ok = ok && hipMemset(s.status, 0, 4 * gsn::kStSlots) == hipSuccess;
+    ok = ok && hipDeviceSynchronize() == hipSuccess;
+    if (!ok) return GSN_E_HIP;
+    net->n = n;
+    net->phase = kReady;
+  } catch (const std::bad_alloc&) {
+    return GSN_E_CAPACITY;
+  }
+  return GSN_OK;
+}
+
+int gsn_check(gsn_net* net, void* stream) {
+  if (!net) return GSN_E_INVAL;
+  int32_t code = 0;
+  int rc = read_status_slot(net, gsn::kStError, &code, as_stream(stream));
+  if (rc) return rc;
+  return code;
+}
+
+void gsn_destroy(gsn_net* net) {
+  if (!net) return;
+  for (auto& v : net->rec)
+    for (auto& pr : v) {
+      (void)hipEventDestroy(pr.first);
+      (void)hipEventDestroy(pr.second);
+    }
+  for (hipEvent_t e : net->pool) (void)hipEventDestroy(e);
+  delete net;
+}
+
+int gsn_tune(gsn_net* net, int32_t key, int32_t value) {
+  if (!net) return GSN_E_INVAL;
+  switch (key) {
+    case GSN_TUNE_SPLIT:
+      if (value < 0 || value > GSN_MAX_SPLIT) return GSN_E_INVAL;
+      net->tune_split = value;
+      return GSN_OK;
+    case GSN_TUNE_VARIANT:
+      if (value < 0 || value > 1) return GSN_E_INVAL;
+      net->tune_variant = value;
+      return GSN_OK;
+    default:
+      return GSN_E_INVAL;
+  }
+}
+
+int gsn_timing_enable(gsn_net* net, int32_t enable) {
+  if (!net) return GSN_E_INVAL;
+  net->timing = enable != 0;
+  return GSN_OK;
+}
+
+int gsn_timing_read(gsn_net* net, int32_t which, double* total_ms, int32_t* launches) {
+  if (!net || which < 0 || which >= GSN_T_COUNT) return GSN_E_INVAL;
+  double sum = 0.0;
+  int32_t cnt = 0;
+  int rc = GSN_OK;
+  for (auto& pr : net->rec[which]) {
+    float ms = 0.0f;
+    if (hipEventSynchronize(pr.second) != hipSuccess ||
+        hipEventElapsedTime(&ms, pr.first, pr.second) != hipSuccess)
+      rc = GSN_E_HIP;
+    sum += ms;
+    ++cnt;
+    net->pool.push_back(pr.first);
+    net->pool.push_back(pr.second);
+  }
+  net->rec[which].clear();
+  if (total_ms) *total_ms = sum;
+  if (launches) *launches = cnt;
+  return rc;
+}
+
+}  // extern "C"

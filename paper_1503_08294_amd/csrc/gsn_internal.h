@@ -1,0 +1,87 @@
+// Internal declarations shared by the HIP translation units of libgsn.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <algorithm>
+
+#include "../../include/gsn.h"
+
+namespace gsn {
+
+constexpr int kBlock = 256;            // threads per workgroup of the per-unit kernels
+constexpr int kMaxSplit = GSN_MAX_SPLIT;
+constexpr int32_t kDead = -1;          // age marking a half-edge removed this iteration
+
+// Sticky status word layout (int32 slots in the status area).
+enum StatusSlot {
+  kStError = 0,       // first error code raised by a kernel (0 = none)
+  kStOrphans = 1,     // units marked for removal since the last grow
+  kStAbort = 2,       // 1 once the CSR rewrite overflowed (rows are then not written)
+  kStInserted = 3,    // grow: 1 if the last insertion added a unit
+  kStKept = 4,        // grow: units kept by the last compaction
+  kStSlots = 16
+};
+
+// Device arrays carved out of the caller's workspace.
+struct DevState {
+  float *x, *y, *z, *err;          // [n_max]
+  int32_t* rp[2];                  // [n_max + 2]   row pointers, ping-pong
+  int32_t* col[2];                 // [2 e_max + 2] neighbour ids, ping-pong
+  int32_t* age[2];                 // [2 e_max + 2] ages, ping-pong
+  unsigned long long* lock;        // [n_max]       packed (d1 bits, signal) claims
+  int32_t* ins;                    // [n_max]       partner of a new edge, -1 = none
+  int32_t* orphan;                 // [n_max]       1 = last edge removed by aging
+  int32_t* cnt;                    // [n_max]       per-unit scratch counts / new ids
+  int32_t* bsum;                   // [n_max / kBlock + 2] per-block sums / offsets
+  float* tmp;                      // [4 n_max]     compaction staging
+  int32_t* status;                 // [kStSlots]
+  unsigned long long* part;        // [kMaxSplit][2][m_max] per-chunk top-2 keys
+};
+
+struct Layout {
+  size_t off[32];
+  size_t total;
+};
+
+Layout layout_for(const gsn_params& p);
+void carve(const gsn_params& p, void* base, DevState* s);
+
+// ---------------------------------------------------------------- launchers ----
+// Every launcher enqueues on `stream` and returns the hipGetLastError() of its launches.
+
+struct FindConfig {
+  int variant;   // 1 = direct scan
+  int split;     // unit chunks
+};
+FindConfig find_config(int32_t n, int32_t m, int cus, int want_split, int want_variant);
+
+hipError_t launch_find_scan(const DevState& s, int32_t n, const float* sig, int32_t m,
+                            const FindConfig& cfg, int32_t* winner, int32_t* second,
+                            float* d1, float* d2, hipStream_t st);
+hipError_t launch_find_merge(const DevState& s, int32_t m, const FindConfig& cfg,
+                             int32_t* winner, int32_t* second, float* d1, float* d2,
+                             hipStream_t st);
+
+hipError_t launch_resolve(const DevState& s, int cur, int32_t n, int32_t m,
+                          const int32_t* winner, const int32_t* second, const float* d1,
+                          uint8_t* accepted, hipStream_t st);
+hipError_t launch_adapt(const DevState& s, int cur, int32_t n, const float* sig, int32_t m,
+                        const int32_t* winner, const int32_t* second, const float* d1,
+                        const uint8_t* accepted, float eps_b, float eps_n, float beta,
+                        hipStream_t st);
+hipError_t launch_edges(const DevState& s, int cur, int32_t n, int32_t m,
+                        const int32_t* winner, const int32_t* second,
+                        const uint8_t* accepted, int32_t max_age, int64_t half_cap,
+                        hipStream_t st);
+hipError_t launch_scan_blocks(int32_t* bsum, int32_t nb, int64_t cap, int32_t* out_total,
+                              int32_t* status, int32_t slot, hipStream_t st);
+hipError_t launch_init(const DevState& s, int cur, int32_t n0, int32_t n_max,
+                       hipStream_t st);
+hipError_t launch_remove(const DevState& s, int cur, int32_t n, int32_t n_max,
+                         hipStream_t st);
+hipError_t launch_insert(const DevState& s, int cur, int32_t n, float alpha,
+                         int64_t half_cap, hipStream_t st);
+
+}  // namespace gsn

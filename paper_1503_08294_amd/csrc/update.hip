@@ -1,0 +1,356 @@
+// The update phase of the multi-signal iteration (Sec. 2.1 step 3, Sec. 2.2): conflict
+// resolution, adaptation and the connection update, all on the device.
+//
+// The paper updates sequentially on the host and leaves a parallel update as future work
+// because of collisions (Sec. 4).  Here every signal claims its lock set L_j = {b_j, s_j}
+// + N(b_j) with a 64-bit atomic minimum of its key, and survives iff it holds every unit
+// of L_j.  Surviving lock sets are pairwise disjoint, which makes the adaptation and the
+// edge update write-disjoint: one thread per signal, no atomics, and the result equals any
+// sequential order.  The adjacency is a symmetric CSR (row_ptr, col, age per half-edge),
+// rows ascending by neighbour; the edge update modifies ages in place, then rewrites a
+// compacted CSR into the other buffer (count -> scan -> scatter).
+#include "gsn_internal.h"
+
+namespace gsn {
+namespace {
+
+__device__ __forceinline__ void raise_error(int32_t* status, int32_t code) {
+  atomicCAS(&status[kStError], 0, code);
+}
+
+__device__ __forceinline__ bool pair_ok(int32_t b, int32_t s, int32_t n) {
+  return b >= 0 && b < n && s >= 0 && s < n && b != s;
+}
+
+__device__ __forceinline__ unsigned long long signal_key(float d1, int32_t j) {
+  return (static_cast<unsigned long long>(__float_as_uint(d1)) << 32) |
+         static_cast<uint32_t>(j);
+}
+
+// Position of neighbour v in the (ascending) row of u, or -1.
+__device__ __forceinline__ int32_t find_in_row(const int32_t* __restrict__ rp,
+                                               const int32_t* __restrict__ col, int32_t u,
+                                               int32_t v) {
+  int32_t lo = rp[u], hi = rp[u + 1];
+  while (lo < hi) {
+    const int32_t mid = (lo + hi) >> 1;
+    const int32_t c = col[mid];
+    if (c == v) return mid;
+    if (c < v) lo = mid + 1; else hi = mid;
+  }
+  return -1;
+}
+
+// ------------------------------------------------------------------ resolve ----
+
+__global__ void rs_clear(unsigned long long* __restrict__ lock, int32_t n) {
+  const int32_t i = blockIdx.x * kBlock + threadIdx.x;
+  if (i < n) lock[i] = ~0ull;
+}
+
+__global__ void rs_claim(int32_t m, int32_t n, const int32_t* __restrict__ winner,
+                         const int32_t* __restrict__ second, const float* __restrict__ d1,
+                         const int32_t* __restrict__ rp, const int32_t* __restrict__ col,
+                         unsigned long long* __restrict__ lock, int32_t* __restrict__ status) {
+  const int32_t j = blockIdx.x * kBlock + threadIdx.x;
+  if (j >= m) return;
+  const int32_t b = winner[j], s = second[j];
+  if (!pair_ok(b, s, n)) {
+    raise_error(status, GSN_E_INVAL);
+    return;
+  }
+  const unsigned long long key = signal_key(d1[j], j);
+  atomicMin(&lock[b], key);
+  atomicMin(&lock[s], key);
+  for (int32_t k = rp[b]; k < rp[b + 1]; ++k) atomicMin(&lock[col[k]], key);
+}
+
+__global__ void rs_check(int32_t m, int32_t n, const int32_t* __restrict__ winner,
+                         const int32_t* __restrict__ second, const float* __restrict__ d1,
+                         const int32_t* __restrict__ rp, const int32_t* __restrict__ col,
+                         const unsigned long long* __restrict__ lock,
+                         uint8_t* __restrict__ accepted) {
+  const int32_t j = blockIdx.x * kBlock + threadIdx.x;
+  if (j >= m) return;
+  const int32_t b = winner[j], s = second[j];
+  if (!pair_ok(b, s, n)) {
+    accepted[j] = 0;
+    return;
+  }
+  const unsigned long long key = signal_key(d1[j], j);
+  bool ok = lock[b] == key && lock[s] == key;
+  for (int32_t k = rp[b]; ok && k < rp[b + 1]; ++k) ok = lock[col[k]] == key;
+  accepted[j] = ok ? 1 : 0;
+}
+
+// -------------------------------------------------------------------- adapt ----
+
+// w <- w + eps (xi - w), one binary32 rounding per operation (no contraction).
+__device__ __forceinline__ void move_unit(float* __restrict__ x, float* __restrict__ y,
+                                          float* __restrict__ z, int32_t u, float eps,
+                                          float sx, float sy, float sz) {
+  float t;
+  t = sx - x[u]; t = eps * t; x[u] = x[u] + t;
+  t = sy - y[u]; t = eps * t; y[u] = y[u] + t;
+  t = sz - z[u]; t = eps * t; z[u] = z[u] + t;
+}
+
+__global__ void ad_move(const float* __restrict__ sig, int32_t m, int32_t n,
+                        const int32_t* __restrict__ winner, const int32_t* __restrict__ second,
+                        const float* __restrict__ d1, const uint8_t* __restrict__ accepted,
+                        const int32_t* __restrict__ rp, const int32_t* __restrict__ col,
+                        float* __restrict__ x, float* __restrict__ y, float* __restrict__ z,
+                        float* __restrict__ err, float eps_b, float eps_n) {
+  const int32_t j = blockIdx.x * kBlock + threadIdx.x;
+  if (j >= m || !accepted[j]) return;
+  const int32_t b = winner[j], s = second[j];
+  if (!pair_ok(b, s, n)) return;
+  const float sx = sig[j], sy = sig[m + j], sz = sig[2 * m + j];
+  move_unit(x, y, z, b, eps_b, sx, sy, sz);
+  bool s_is_nb = false;
+  for (int32_t k = rp[b]; k < rp[b + 1]; ++k) {
+    const int32_t v = col[k];
+    s_is_nb |= v == s;
+    move_unit(x, y, z, v, eps_n, sx, sy, sz);
+  }
+  if (!s_is_nb) move_unit(x, y, z, s, eps_n, sx, sy, sz);
+  err[b] = err[b] + d1[j];
+}
+
+__global__ void ad_decay(float* __restrict__ err, int32_t n, float beta) {
+  const int32_t i = blockIdx.x * kBlock + threadIdx.x;
+  if (i < n) err[i] = err[i] * beta;
+}
+
+// -------------------------------------------------------------------- edges ----
+
+// Per accepted signal: age the edges at b (both half-edges), reset or request the edge
+// {b, s}, then mark the edges at b older than max_age as dead and flag neighbours left
+// without a live edge.  Rows touched belong to L_j only, so threads never share a row.
+__global__ void ed_mark(int32_t m, int32_t n, const int32_t* __restrict__ winner,
+                        const int32_t* __restrict__ second,
+                        const uint8_t* __restrict__ accepted, const int32_t* __restrict__ rp,
+                        const int32_t* __restrict__ col, int32_t* __restrict__ age,
+                        int32_t* __restrict__ ins, int32_t* __restrict__ orphan,
+                        int32_t* __restrict__ status, int32_t max_age) {
+  const int32_t j = blockIdx.x * kBlock + threadIdx.x;
+  if (j >= m || !accepted[j]) return;
+  const int32_t b = winner[j], s = second[j];
+  if (!pair_ok(b, s, n)) return;
+  const int32_t r0 = rp[b], r1 = rp[b + 1];
+  bool found = false;
+  for (int32_t k = r0; k < r1; ++k) {
+    const int32_t v = col[k];
+    int32_t a = age[k] + 1;
+    if (v == s) {
+      a = 0;
+      found = true;
+    }
+    age[k] = a;
+    const int32_t rk = find_in_row(rp, col, v, b);
+    if (rk >= 0) age[rk] = a;
+  }
+  if (!found) {
+    ins[b] = s;
+    ins[s] = b;
+  }
+  for (int32_t k = r0; k < r1; ++k) {
+    if (age[k] <= max_age) continue;
+    const int32_t v = col[k];
+    age[k] = kDead;
+    const int32_t rk = find_in_row(rp, col, v, b);
+    if (rk >= 0) age[rk] = kDead;
+    bool live = ins[v] >= 0;
+    for (int32_t kk = rp[v]; !live && kk < rp[v + 1]; ++kk) live = age[kk] != kDead;
+    if (!live && !orphan[v]) {
+      orphan[v] = 1;
+      atomicAdd(&status[kStOrphans], 1);
+    }
+  }
+}
+
+// New degree of every unit (live half-edges + a requested new edge) and per-block sums.
+__global__ void ed_count(int32_t n, const int32_t* __restrict__ rp,
+                         const int32_t* __restrict__ age, const int32_t* __restrict__ ins,
+                         int32_t* __restrict__ cnt, int32_t* __restrict__ bsum) {
+  __shared__ int32_t red[kBlock];
+  const int32_t u = blockIdx.x * kBlock + threadIdx.x;
+  int32_t c = 0;
+  if (u < n) {
+    for (int32_t k = rp[u]; k < rp[u + 1]; ++k) c += age[k] != kDead;
+    c += ins[u] >= 0;
+    cnt[u] = c;
+  }
+  red[threadIdx.x] = c;
+  __syncthreads();
+  for (int w = kBlock / 2; w > 0; w >>= 1) {
+    if (threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) bsum[blockIdx.x] = red[0];
+}
+
+// Exclusive scan of the per-block sums in one workgroup; bsum[nb] receives the total.
+// If the total exceeds `cap`, the rewrite is aborted and a capacity error is raised;
+// `out_rp_n` (if not null) receives the total, or 0 once aborted, so that the rows written
+// afterwards always describe a valid adjacency.
+__global__ __launch_bounds__(1024) void scan_blocks(int32_t* __restrict__ bsum, int32_t nb,
+                                                    int64_t cap, int32_t* __restrict__ out_rp_n,
+                                                    int32_t* __restrict__ status,
+                                                    int32_t status_slot_total) {
+  __shared__ int32_t part[1024];
+  const int32_t t = threadIdx.x;
+  const int32_t per = (nb + 1023) / 1024;
+  const int32_t a = t * per, e = min(nb, a + per);
+  int32_t sum = 0;
+  for (int32_t i = a; i < e; ++i) sum += bsum[i];
+  part[t] = sum;
+  __syncthreads();
+  for (int off = 1; off < 1024; off <<= 1) {
+    const int32_t v = t >= off ? part[t - off] : 0;
+    __syncthreads();
+    part[t] += v;
+    __syncthreads();
+  }
+  int32_t run = part[t] - sum;  // exclusive prefix of this thread's slice
+  for (int32_t i = a; i < e; ++i) {
+    const int32_t v = bsum[i];
+    bsum[i] = run;
+    run += v;
+  }
+  if (t == 1023) {
+    const int32_t total = part[1023];
+    bsum[nb] = total;
+    const bool over = static_cast<int64_t>(total) > cap;
+    if (over) {
+      status[kStAbort] = 1;
+      atomicCAS(&status[kStError], 0, GSN_E_CAPACITY);
+    }
+    if (out_rp_n) *out_rp_n = over || status[kStAbort] ? 0 : total;
+    if (status_slot_total >= 0) status[status_slot_total] = total;
+  }
+}
+
+// Block-local exclusive scan of cnt, plus the block offset, gives each row's start; the
+// row is written as the live old entries merged with the requested new neighbour, in
+// ascending neighbour order.  Clears the request.
+__global__ void ed_write(int32_t n, const int32_t* __restrict__ rp,
+                         const int32_t* __restrict__ col, const int32_t* __restrict__ age,
+                         int32_t* __restrict__ ins, const int32_t* __restrict__ cnt,
+                         const int32_t* __restrict__ boff, int32_t* __restrict__ rp_new,
+                         int32_t* __restrict__ col_new, int32_t* __restrict__ age_new,
+                         const int32_t* __restrict__ status) {
+  __shared__ int32_t sc[kBlock];
+  const int32_t u = blockIdx.x * kBlock + threadIdx.x;
+  const int32_t c = u < n ? cnt[u] : 0;
+  sc[threadIdx.x] = c;
+  __syncthreads();
+  for (int off = 1; off < kBlock; off <<= 1) {
+    const int32_t v = threadIdx.x >= off ? sc[threadIdx.x - off] : 0;
+    __syncthreads();
+    sc[threadIdx.x] += v;
+    __syncthreads();
+  }
+  if (u >= n) return;
+  const int32_t start = boff[blockIdx.x] + sc[threadIdx.x] - c;
+  const int32_t extra = ins[u];
+  ins[u] = -1;
+  if (status[kStAbort]) {
+    // the rewrite did not fit: leave a valid, empty adjacency (state is flagged invalid)
+    rp_new[u] = 0;
+    return;
+  }
+  rp_new[u] = start;
+  int32_t o = start;
+  bool pending = extra >= 0;
+  for (int32_t k = rp[u]; k < rp[u + 1]; ++k) {
+    if (age[k] == kDead) continue;
+    const int32_t v = col[k];
+    if (pending && extra < v) {
+      col_new[o] = extra;
+      age_new[o] = 0;
+      ++o;
+      pending = false;
+    }
+    col_new[o] = v;
+    age_new[o] = age[k];
+    ++o;
+  }
+  if (pending) {
+    col_new[o] = extra;
+    age_new[o] = 0;
+  }
+}
+
+__global__ void init_state(float* __restrict__ err, int32_t* __restrict__ ins,
+                           int32_t* __restrict__ orphan, int32_t* __restrict__ rp,
+                           int32_t n_max, int32_t* __restrict__ status) {
+  const int32_t i = blockIdx.x * kBlock + threadIdx.x;
+  if (i < n_max) {
+    err[i] = 0.0f;
+    ins[i] = -1;
+    orphan[i] = 0;
+  }
+  if (i <= n_max) rp[i] = 0;
+  if (i < kStSlots) status[i] = 0;
+}
+
+inline int blocks(int64_t n) { return static_cast<int>((n + kBlock - 1) / kBlock); }
+
+}  // namespace
+
+hipError_t launch_init(const DevState& s, int cur, int32_t, int32_t n_max, hipStream_t st) {
+  const int64_t cover = std::max<int64_t>(static_cast<int64_t>(n_max) + 1, kStSlots);
+  init_state<<<blocks(cover), kBlock, 0, st>>>(s.err, s.ins, s.orphan, s.rp[cur], n_max,
+                                               s.status);
+  return hipGetLastError();
+}
+
+hipError_t launch_resolve(const DevState& s, int cur, int32_t n, int32_t m,
+                          const int32_t* winner, const int32_t* second, const float* d1,
+                          uint8_t* accepted, hipStream_t st) {
+  if (n > 0) rs_clear<<<blocks(n), kBlock, 0, st>>>(s.lock, n);
+  rs_claim<<<blocks(m), kBlock, 0, st>>>(m, n, winner, second, d1, s.rp[cur], s.col[cur],
+                                         s.lock, s.status);
+  rs_check<<<blocks(m), kBlock, 0, st>>>(m, n, winner, second, d1, s.rp[cur], s.col[cur],
+                                         s.lock, accepted);
+  return hipGetLastError();
+}
+
+hipError_t launch_adapt(const DevState& s, int cur, int32_t n, const float* sig, int32_t m,
+                        const int32_t* winner, const int32_t* second, const float* d1,
+                        const uint8_t* accepted, float eps_b, float eps_n, float beta,
+                        hipStream_t st) {
+  if (m > 0)
+    ad_move<<<blocks(m), kBlock, 0, st>>>(sig, m, n, winner, second, d1, accepted, s.rp[cur],
+                                          s.col[cur], s.x, s.y, s.z, s.err, eps_b, eps_n);
+  if (n > 0) ad_decay<<<blocks(n), kBlock, 0, st>>>(s.err, n, beta);
+  return hipGetLastError();
+}
+
+hipError_t launch_edges(const DevState& s, int cur, int32_t n, int32_t m,
+                        const int32_t* winner, const int32_t* second,
+                        const uint8_t* accepted, int32_t max_age, int64_t half_cap,
+                        hipStream_t st) {
+  const int nxt = cur ^ 1;
+  if (m > 0)
+    ed_mark<<<blocks(m), kBlock, 0, st>>>(m, n, winner, second, accepted, s.rp[cur],
+                                          s.col[cur], s.age[cur], s.ins, s.orphan, s.status,
+                                          max_age);
+  const int nb = blocks(n);
+  if (n > 0)
+    ed_count<<<nb, kBlock, 0, st>>>(n, s.rp[cur], s.age[cur], s.ins, s.cnt, s.bsum);
+  scan_blocks<<<1, 1024, 0, st>>>(s.bsum, nb, half_cap, s.rp[nxt] + n, s.status, -1);
+  if (n > 0)
+    ed_write<<<nb, kBlock, 0, st>>>(n, s.rp[cur], s.col[cur], s.age[cur], s.ins, s.cnt,
+                                    s.bsum, s.rp[nxt], s.col[nxt], s.age[nxt], s.status);
+  return hipGetLastError();
+}
+
+hipError_t launch_scan_blocks(int32_t* bsum, int32_t nb, int64_t cap, int32_t* out_total,
+                              int32_t* status, int32_t slot, hipStream_t st) {
+  scan_blocks<<<1, 1024, 0, st>>>(bsum, nb, cap, out_total, status, slot);
+  return hipGetLastError();
+}
+
+}  // namespace gsn

@@ -1,0 +1,82 @@
+"""Helpers that run the HIP path (through the C ABI binding) and the CPU oracle side by
+side on the same seeded inputs and compare them element by element.
+
+Bar: winner, second, acceptance and edge lists bit-exact; d1, d2 bit-exact (same binary32
+expression on both sides); positions within 1e-6 max abs (bit-exact expected: the update
+expressions are the same operations in the same order); errors likewise.
+"""
+from __future__ import annotations
+
+import os
+
+import numpy as np
+
+import oracle
+
+POS_TOL = 1e-6
+
+
+def oracle_threads() -> int:
+    return max(1, min(16, os.cpu_count() or 1))
+
+
+def params_pair(n_max, e_max, m_max, eps_b=0.05, eps_n=0.0006, max_age=50, err_alpha=0.5,
+                err_beta=0.995):
+    from paper_1503_08294_amd import gsn
+    g = gsn.make_params(eps_b, eps_n, max_age, err_alpha, err_beta, n_max, e_max, m_max)
+    o = oracle.Params(eps_b, eps_n, max_age, err_alpha, err_beta, n_max, e_max, m_max)
+    return g, o
+
+
+class Pair:
+    """A GPU network and an oracle network created from the same units and parameters."""
+
+    def __init__(self, units: np.ndarray, n_max=None, e_max=None, m_max=1024, **kw):
+        import torch
+        from paper_1503_08294_amd import gsn
+        n = units.shape[1]
+        n_max = n_max or n
+        e_max = e_max if e_max is not None else 4 * n_max + 16
+        gp, op = params_pair(n_max, e_max, m_max, **kw)
+        self.torch = torch
+        self.gsn = gsn
+        self.net = gsn.Network(gp, torch.from_numpy(np.ascontiguousarray(units)).cuda())
+        self.orc = oracle.Oracle(op, units, threads=oracle_threads())
+
+    def to_dev(self, a: np.ndarray):
+        return self.torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+    def find(self, sig: np.ndarray):
+        g = [t.cpu().numpy() for t in self.net.find_winners(self.to_dev(sig))]
+        o = self.orc.find_winners(sig)
+        return g, o
+
+    def iterate(self, sig: np.ndarray, it=0, insert_every=0, grow=False):
+        g = [t.cpu().numpy() for t in self.net.iterate(self.to_dev(sig))]
+        if grow:
+            self.net.grow(it, insert_every)
+        o = self.orc.iterate(sig, it, insert_every, grow)
+        return g, o
+
+    def compare_state(self, where=""):
+        gs = self.net.export()
+        os_ = self.orc.export()
+        assert self.net.sizes() == tuple(int(v) for v in self.orc.sizes()), where
+        np.testing.assert_array_equal(gs["edges"].numpy(), os_["edges"], err_msg=where)
+        np.testing.assert_allclose(gs["xyz"].numpy(), os_["xyz"], rtol=0, atol=POS_TOL,
+                                   err_msg=where)
+        np.testing.assert_allclose(gs["err"].numpy(), os_["err"], rtol=1e-6, atol=1e-12,
+                                   err_msg=where)
+        return gs, os_
+
+
+def assert_find_equal(g, o, where=""):
+    names = ("winner", "second", "d1", "d2")
+    for a, b, nm in zip(g, o, names):
+        np.testing.assert_array_equal(a, b, err_msg=f"{where} {nm}")
+
+
+def assert_iter_equal(g, o, where=""):
+    names = ("winner", "second", "d1", "d2", "accepted")
+    for a, b, nm in zip(g, o, names):
+        np.testing.assert_array_equal(a, b, err_msg=f"{where} {nm}")

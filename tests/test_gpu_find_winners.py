@@ -1,0 +1,72 @@
+"""GPU parity of find-winners against the oracle: winner, second, d1, d2 bit-exact, over
+sizes that span several tiles, chunks and a ragged tail, tie-heavy inputs, every split of
+the unit range, and the full 200k-unit x 16k-signal genus-3 workload."""
+import numpy as np
+import pytest
+
+from parity import Pair, assert_find_equal
+
+pytestmark = pytest.mark.gpu
+
+CASES = [(2, 1, 0), (3, 7, 1), (100, 33, 2), (1000, 256, 3), (1537, 1000, 4),
+         (4099, 2049, 5), (10_000, 2_048, 6), (50_000, 300, 7), (20_000, 8_192, 8),
+         (700, 20_000, 9)]
+
+
+@pytest.mark.parametrize("n,m,seed", CASES)
+def test_random_inputs(n, m, seed):
+    rng = np.random.default_rng(seed)
+    units = rng.standard_normal((3, n)).astype(np.float32)
+    sig = rng.standard_normal((3, m)).astype(np.float32)
+    pair = Pair(units, m_max=m)
+    g, o = pair.find(sig)
+    assert_find_equal(g, o, f"n={n} m={m}")
+
+
+@pytest.mark.parametrize("grid,n,m", [(1, 50, 500), (3, 3000, 4000), (2, 9, 64)])
+def test_ties_duplicates_and_signals_on_units(grid, n, m):
+    rng = np.random.default_rng(grid)
+    units = rng.integers(-grid, grid + 1, (3, n)).astype(np.float32)
+    sig = rng.integers(-grid, grid + 1, (3, m)).astype(np.float32)
+    sig[:, : min(m, n)] = units[:, : min(m, n)]
+    pair = Pair(units, m_max=m)
+    g, o = pair.find(sig)
+    assert_find_equal(g, o, f"grid={grid}")
+
+
+def test_every_split_gives_the_same_answer():
+    from paper_1503_08294_amd import gsn
+    rng = np.random.default_rng(21)
+    units = rng.standard_normal((3, 5000)).astype(np.float32)
+    units[:, 4000:] = units[:, :1000]                  # exact duplicates across chunks
+    sig = rng.standard_normal((3, 3000)).astype(np.float32)
+    pair = Pair(units, m_max=3000)
+    o = pair.orc.find_winners(sig)
+    for split in (1, 2, 3, 7, 16, 64, 0):
+        pair.net.tune(gsn.GSN_TUNE_SPLIT, split)
+        g = [t.cpu().numpy() for t in pair.net.find_winners(pair.to_dev(sig))]
+        assert_find_equal(g, o, f"split={split}")
+
+
+def test_zero_signals_and_repeat_calls():
+    rng = np.random.default_rng(4)
+    units = rng.standard_normal((3, 300)).astype(np.float32)
+    pair = Pair(units, m_max=64)
+    sig = rng.standard_normal((3, 64)).astype(np.float32)
+    a = [t.cpu().numpy().copy() for t in pair.net.find_winners(pair.to_dev(sig))]
+    pair.net.find_winners(pair.to_dev(np.zeros((3, 0), np.float32)))
+    b = [t.cpu().numpy() for t in pair.net.find_winners(pair.to_dev(sig))]
+    assert_find_equal(a, b, "repeat")
+
+
+def test_genus3_full_size():
+    """200,000 units and 16,384 signals from the 4M-point genus-3 cloud (the launch
+    configuration the benchmark times), every output compared."""
+    from paper_1503_08294_amd.clouds import WORKLOADS, SignalStream
+    wl = WORKLOADS["genus3_200k"]
+    cloud = wl.make_cloud()
+    units = wl.make_units(cloud)
+    sig = SignalStream(cloud, wl.signal_seed).next(wl.m)
+    pair = Pair(units, m_max=wl.m)
+    g, o = pair.find(sig)
+    assert_find_equal(g, o, "genus3_200k")

@@ -1,0 +1,82 @@
+"""GPU parity of whole iterations (find -> resolve -> adapt -> update_edges, plus grow
+where the workload grows) against the oracle on the seeded synthetic workloads: every
+iteration's winner, second, d1, d2 and acceptance bit-exact; edge lists bit-exact and
+positions within 1e-6 after the iterations stated."""
+import numpy as np
+import pytest
+
+from parity import Pair, assert_iter_equal
+
+pytestmark = pytest.mark.gpu
+
+
+def run_workload(name, iterations=None, compare_every=1, n_points=None, m=None,
+                 n_units=None, **over):
+    from paper_1503_08294_amd.clouds import WORKLOADS, SignalStream
+    wl = WORKLOADS[name]
+    cloud = wl.make_cloud(n_points)
+    units = wl.make_units(cloud, n_units)
+    m = m or wl.m
+    its = iterations or wl.iterations
+    cap = wl.capacity(m)
+    kw = dict(eps_b=wl.eps_b, eps_n=wl.eps_n, max_age=wl.max_age, err_alpha=wl.err_alpha,
+              err_beta=wl.err_beta)
+    kw.update(over)
+    pair = Pair(units, n_max=max(cap["n_max"], units.shape[1]), e_max=cap["e_max"], m_max=m,
+                **kw)
+    stream = SignalStream(cloud, wl.signal_seed)
+    rejected = 0
+    for t in range(1, its + 1):
+        sig = stream.next(m)
+        g, o = pair.iterate(sig, t, wl.insert_every, wl.grow)
+        assert_iter_equal(g, o, f"{name} iteration {t}")
+        rejected += int(m - o[4].sum())
+        if t % compare_every == 0 or t == its:
+            pair.compare_state(f"{name} iteration {t}")
+    assert pair.net.check() == 0
+    return pair, rejected / (its * m)
+
+
+def test_tiny_sphere_20_iterations():
+    pair, _ = run_workload("tiny_sphere")
+    n, e = pair.net.sizes()
+    assert n == 1000 and e > 0
+
+
+def test_torus_grow_100_iterations():
+    pair, _ = run_workload("torus_grow")
+    n, _ = pair.net.sizes()
+    assert n > 10_000          # insertions happened
+
+
+def test_pruning_removal_and_insertion():
+    """A dense small network with max_age 2: edges are pruned, units are orphaned and
+    removed, and a unit is inserted every 10 iterations."""
+    pair, _ = run_workload("torus_grow", iterations=60, n_points=50_000, n_units=1_500, m=1_024,
+                           max_age=2)
+    # the same state was reached; check that removal and insertion actually occurred
+    n, _ = pair.net.sizes()
+    assert n != 1_500
+
+
+def test_spheres_plane_200_iterations():
+    pair, _ = run_workload("spheres_plane_prune", compare_every=25)
+    assert pair.net.sizes()[0] != 50_000
+
+
+def test_genus3_3_iterations():
+    run_workload("genus3_200k", iterations=3)
+
+
+@pytest.mark.parametrize("m", [1, 64, 1_024, 16_384, 65_536])
+def test_torus_sweep_one_iteration_per_m(m):
+    _, rate = run_workload("torus_sweep", iterations=2, m=m)
+    assert 0.0 <= rate < 1.0
+
+
+def test_determinism_of_repeated_runs():
+    a, _ = run_workload("torus_grow", iterations=15)
+    b, _ = run_workload("torus_grow", iterations=15)
+    sa, sb = a.net.export(), b.net.export()
+    for k in ("xyz", "err", "edges"):
+        assert np.array_equal(sa[k].numpy(), sb[k].numpy()), k
