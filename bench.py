@@ -53,21 +53,28 @@ def load_traffic(launch_evals: int):
     return t.get("bytes_per_launch")
 
 
-def cpu_baseline(wl, units, first_sig_batches, budget_s: float):
+def cpu_baseline(wl, units, cloud, budget_s: float):
+    """The oracle on the same initial units and the same seeded signal batches as the GPU
+    run, whole iterations until about budget_s seconds have passed (at most 200)."""
     import oracle
+    from paper_1503_08294_amd.clouds import SignalStream
     threads = max(1, min(16, os.cpu_count() or 1))
     cap = wl.capacity()
     p = oracle.Params(wl.eps_b, wl.eps_n, wl.max_age, wl.err_alpha, wl.err_beta,
                       cap["n_max"], cap["e_max"], cap["m_max"])
     o = oracle.Oracle(p, units, threads=threads)
-    t0 = time.perf_counter()
+    stream = SignalStream(cloud, wl.signal_seed)
+    batches = [stream.next(wl.m) for _ in range(3)]
+    dt = 0.0
     done = 0
-    for sig in first_sig_batches:
+    while done < 200 and dt < budget_s:
+        sig = batches[done] if done < len(batches) else stream.next(wl.m)
+        t0 = time.perf_counter()
         o.iterate(sig)
+        if wl.grow:
+            o.grow(done + 1, wl.insert_every)
+        dt += time.perf_counter() - t0
         done += 1
-        if time.perf_counter() - t0 >= budget_s:
-            break
-    dt = time.perf_counter() - t0
     evals = wl.m * units.shape[1] * done
     return {"value": evals / dt, "unit": "evals/s", "cores": threads, "kind": "oracle",
             "signals_per_s": wl.m * done / dt,
@@ -204,7 +211,7 @@ def main():
     }
     if args.cpu_budget > 0:
         print(f"[bench] cpu baseline (~{args.cpu_budget:.0f} s)", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(wl, units, list(host_sig[:30]), args.cpu_budget)
+        out["cpu_baseline"] = cpu_baseline(wl, units, cloud, args.cpu_budget)
     print(json.dumps(out), flush=True)
 
 

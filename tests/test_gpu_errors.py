@@ -37,9 +37,13 @@ def test_call_order_is_enforced():
 
 def test_signal_capacity_and_empty_batch():
     from paper_1503_08294_amd import gsn
+    import torch
     pair, rng = small_pair(m_max=16)
-    with pytest.raises(gsn.GsnError) as e:
-        pair.net.find_winners(pair.to_dev(rng.standard_normal((3, 17)).astype(np.float32)))
+    sig = pair.to_dev(rng.standard_normal((3, 17)).astype(np.float32))
+    out = [torch.empty(17, dtype=dt, device="cuda")
+           for dt in (torch.int32, torch.int32, torch.float32, torch.float32)]
+    with pytest.raises(gsn.GsnError) as e:         # m = 17 > m_max = 16: rejected by the library
+        gsn.gsn_find_winners(pair.net.h, sig, 17, *out)
     assert e.value.code == gsn.GSN_E_INVAL
     empty = pair.to_dev(np.zeros((3, 0), np.float32))
     pair.net.iterate(empty)
