@@ -33,12 +33,16 @@ METRIC = "signal-unit distance evals/s and signals/s at 1 GPU; % fp32 VALU peak"
 FP32_PEAK_TFLOPS = 157.3     # 256 CUs x 2.4 GHz x 256 fp32 flop/clk (packed FMA)
 FLOPS_PER_EVAL = 8           # 3 sub + 3 mul + 2 add of one squared distance
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "find_winners_genus3_200k_traffic.json")
-SCAN_SOURCE = os.path.join(ROOT, "paper_1503_08294_amd", "csrc", "find_winners.hip")
+SCAN_SOURCES = [os.path.join(ROOT, "paper_1503_08294_amd", "csrc", f)
+                for f in ("find_winners.hip", "find_screened.hip")]
 
 
 def scan_source_hash() -> str:
-    with open(SCAN_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for path in SCAN_SOURCES:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def load_traffic(launch_evals: int):
@@ -202,7 +206,7 @@ def main():
         "phase_ms": phase,
         "conflict_rate": conflict_rate,
         "state_after": {"units": n_units, "edges": n_edges},
-        "roofline": {"bound": "alu", "kernel": "fw_scan", "achieved": achieved,
+        "roofline": {"bound": "alu", "kernel": "fs_scan", "achieved": achieved,
                      "peak": FP32_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / FP32_PEAK_TFLOPS, "traffic": traffic,
                      "flops_per_launch": FLOPS_PER_EVAL * m * n,

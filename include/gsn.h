@@ -156,7 +156,9 @@ void gsn_destroy(gsn_net* net);
 /* Launch-configuration knobs, for tests and measurement; results never depend on them.
  *   GSN_TUNE_SPLIT    units are split into this many chunks scanned by separate
  *                     workgroups and merged afterwards (0 = automatic, 1..GSN_MAX_SPLIT)
- *   GSN_TUNE_VARIANT  find-winners kernel: 0 = automatic, 1 = direct scan
+ *   GSN_TUNE_VARIANT  find-winners kernel: 0 = automatic (screened), 1 = direct scan of
+ *                     every distance, 2 = screened scan (expanded-form screen with a
+ *                     rigorous rounding margin, direct-form recheck of candidates)
  * Returns GSN_E_INVAL for an unknown key or value. */
 enum { GSN_TUNE_SPLIT = 1, GSN_TUNE_VARIANT = 2 };
 #define GSN_MAX_SPLIT 64

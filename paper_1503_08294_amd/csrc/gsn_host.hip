@@ -42,6 +42,7 @@ Layout layout_for(const gsn_params& p) {
   add(16 * nm);                // 15 tmp
   add(4 * kStSlots);           // 16 status
   add(8 * static_cast<size_t>(kMaxSplit) * 2 * mm);  // 17 part
+  add(stage_bytes(p.n_max, p.m_max));                 // 18 screened staging
   L.total = (o + 255) & ~static_cast<size_t>(255);
   return L;
 }
@@ -67,6 +68,7 @@ void carve(const gsn_params& p, void* base, DevState* s) {
   s->tmp = reinterpret_cast<float*>(b + L.off[15]);
   s->status = reinterpret_cast<int32_t*>(b + L.off[16]);
   s->part = reinterpret_cast<unsigned long long*>(b + L.off[17]);
+  s->scr = b + L.off[18];
 }
 
 }  // namespace gsn
@@ -74,6 +76,7 @@ void carve(const gsn_params& p, void* base, DevState* s) {
 using gsn::DevState;
 
 enum Phase { kReady = 0, kFound = 1, kResolved = 2, kAdapted = 3 };
+constexpr int kRebucketEvery = 16;
 
 struct gsn_net {
   gsn_params p;
@@ -85,6 +88,8 @@ struct gsn_net {
   int tune_split;
   int tune_variant;
   bool timing;
+  int32_t bucket_n;            // unit count at the last spatial bucketing (-1: none yet)
+  int32_t finds_since_bucket;
   std::vector<hipEvent_t> pool;
   std::vector<std::pair<hipEvent_t, hipEvent_t>> rec[GSN_T_COUNT];
 };
@@ -186,6 +191,8 @@ int gsn_create(const gsn_params* params, void* workspace, size_t workspace_bytes
   net->tune_split = 0;
   net->tune_variant = 0;
   net->timing = false;
+  net->bucket_n = -1;
+  net->finds_since_bucket = 0;
   int dev = 0, cus = 256;
   if (hipGetDevice(&dev) == hipSuccess &&
       hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess)
@@ -194,6 +201,8 @@ int gsn_create(const gsn_params* params, void* workspace, size_t workspace_bytes
     net->cus = 256;
   hipStream_t st = as_stream(stream);
   hipError_t e = gsn::launch_init(net->s, 0, n0, params->n_max, st);
+  if (e == hipSuccess)
+    e = gsn::launch_stage_init(gsn::carve_stage(net->s.scr, params->n_max, params->m_max), st);
   const size_t bytes = sizeof(float) * static_cast<size_t>(n0);
   if (e == hipSuccess && n0 > 0) {
     e = hipMemcpyAsync(net->s.x, init_xyz, bytes, hipMemcpyDefault, st);
@@ -224,10 +233,30 @@ int gsn_find_winners(gsn_net* net, const float* sig, int32_t m, int32_t* winner,
   const gsn::FindConfig cfg =
       gsn::find_config(net->n, m, net->cus, net->tune_split, net->tune_variant);
   TimedRegion all(net, GSN_T_FIND, st);
-  TimedRegion scan(net, GSN_T_FIND_SCAN, st);
-  hipError_t e = gsn::launch_find_scan(net->s, net->n, sig, m, cfg, winner, second, d1, d2, st);
-  scan.end();
-  if (e == hipSuccess) e = gsn::launch_find_merge(net->s, m, cfg, winner, second, d1, d2, st);
+  hipError_t e;
+  if (cfg.variant == 2) {
+    const gsn::StageBufs sb = gsn::carve_stage(net->s.scr, net->p.n_max, net->p.m_max);
+    // the unit order is rebuilt when the network changed and every kRebucketEvery calls
+    const bool rebucket = net->bucket_n != net->n || net->finds_since_bucket >= kRebucketEvery;
+    e = gsn::launch_stage(net->s, sb, net->n, sig, m, rebucket, st);
+    if (rebucket) {
+      net->bucket_n = net->n;
+      net->finds_since_bucket = 0;
+    }
+    ++net->finds_since_bucket;
+    if (e == hipSuccess) {
+      TimedRegion scan(net, GSN_T_FIND_SCAN, st);
+      e = gsn::launch_scan_screened(net->s, sb, net->n, sig, m, cfg.split, st);
+      scan.end();
+    }
+    if (e == hipSuccess)
+      e = gsn::launch_stage_merge(net->s, sb, m, cfg.split, winner, second, d1, d2, st);
+  } else {
+    TimedRegion scan(net, GSN_T_FIND_SCAN, st);
+    e = gsn::launch_find_scan(net->s, net->n, sig, m, cfg, winner, second, d1, d2, st);
+    scan.end();
+    if (e == hipSuccess) e = gsn::launch_find_merge(net->s, m, cfg, winner, second, d1, d2, st);
+  }
   all.end();
   return hip_ok(e);
 }
@@ -293,6 +322,7 @@ int gsn_grow(gsn_net* net, int32_t iteration, int32_t insert_every, void* stream
     rc = read_status_slot(net, gsn::kStKept, &kept, st);
     if (rc) return rc;
     net->n = kept;
+    net->bucket_n = -1;  // indices changed
   }
   if (insert_every > 0 && iteration > 0 && iteration % insert_every == 0 && net->n >= 1 &&
       net->n < net->p.n_max) {
@@ -303,6 +333,7 @@ int gsn_grow(gsn_net* net, int32_t iteration, int32_t insert_every, void* stream
     rc = read_status_slot(net, gsn::kStInserted, &inserted, st);
     if (rc) return rc;
     net->n += inserted;
+    if (inserted) net->bucket_n = -1;
   }
   return GSN_OK;
 }
@@ -426,10 +457,13 @@ int gsn_import(gsn_net* net, int32_t n, const float* xyz, const float* err, int3
     ok = ok && hipMemset(s.ins, 0xff, 4 * nm) == hipSuccess;
     ok = ok && hipMemset(s.orphan, 0, 4 * nm) == hipSuccess;
     ok = ok && hipMemset(s.status, 0, 4 * gsn::kStSlots) == hipSuccess;
+    ok = ok && gsn::launch_stage_init(gsn::carve_stage(s.scr, net->p.n_max, net->p.m_max),
+                                      nullptr) == hipSuccess;
     ok = ok && hipDeviceSynchronize() == hipSuccess;
     if (!ok) return GSN_E_HIP;
     net->n = n;
     net->phase = kReady;
+    net->bucket_n = -1;
   } catch (const std::bad_alloc&) {
     return GSN_E_CAPACITY;
   }
@@ -463,7 +497,7 @@ int gsn_tune(gsn_net* net, int32_t key, int32_t value) {
       net->tune_split = value;
       return GSN_OK;
     case GSN_TUNE_VARIANT:
-      if (value < 0 || value > 1) return GSN_E_INVAL;
+      if (value < 0 || value > 2) return GSN_E_INVAL;
       net->tune_variant = value;
       return GSN_OK;
     default:

@@ -38,6 +38,7 @@ struct DevState {
   float* tmp;                      // [4 n_max]     compaction staging
   int32_t* status;                 // [kStSlots]
   unsigned long long* part;        // [kMaxSplit][2][m_max] per-chunk top-2 keys
+  void* scr;                       // staging area of the screened scans (staging.hip)
 };
 
 struct Layout {
@@ -52,7 +53,7 @@ void carve(const gsn_params& p, void* base, DevState* s);
 // Every launcher enqueues on `stream` and returns the hipGetLastError() of its launches.
 
 struct FindConfig {
-  int variant;   // 1 = direct scan
+  int variant;   // 1 = direct scan, 2 = screened scan
   int split;     // unit chunks
 };
 FindConfig find_config(int32_t n, int32_t m, int cus, int want_split, int want_variant);
@@ -63,6 +64,33 @@ hipError_t launch_find_scan(const DevState& s, int32_t n, const float* sig, int3
 hipError_t launch_find_merge(const DevState& s, int32_t m, const FindConfig& cfg,
                              int32_t* winner, int32_t* second, float* d1, float* d2,
                              hipStream_t st);
+
+// Spatial staging of the screened scans (staging.hip).
+constexpr int kBuckets = 32 * 32 * 32;
+struct StageBufs {
+  float4* pu;       // [n_max] units in bucket order: (x, y, z, |w|^2)
+  int32_t* pidx;    // [n_max] original index of every sorted slot
+  int32_t* ukey;    // [n_max] bucket of every unit at the last bucketing
+  int32_t* skey;    // [m_max] bucket of every signal
+  int32_t* sperm;   // [m_max] original index of the signal at every sorted position
+  float* seed;      // [m_max] seed bound B at every sorted position
+  int32_t *hist_u, *off_u, *cur_u, *hist_s, *off_s, *cur_s;  // [kBuckets + 1] each
+  int32_t* acc;     // [16] bounding-box accumulators
+  float* bb;        // [8] grid of the last unit bucketing: lo.xyz, cells per length.xyz
+  int32_t* mag;     // [4] max |x|, |y|, |z|, |w|^2 of this call (float bits)
+  float* bmag;      // [n_max / kBlock + 1][4] per-block magnitude maxima
+};
+size_t stage_bytes(int32_t n_max, int32_t m_max);
+StageBufs carve_stage(void* base, int32_t n_max, int32_t m_max);
+hipError_t launch_stage_init(const StageBufs& b, hipStream_t st);
+hipError_t launch_stage(const DevState& s, const StageBufs& b, int32_t n, const float* sig,
+                        int32_t m, bool rebucket, hipStream_t st);
+hipError_t launch_stage_merge(const DevState& s, const StageBufs& b, int32_t m, int split,
+                              int32_t* winner, int32_t* second, float* d1, float* d2,
+                              hipStream_t st);
+int screened_split(int32_t n, int32_t m, int cus, int want);
+hipError_t launch_scan_screened(const DevState& s, const StageBufs& b, int32_t n,
+                                const float* sig, int32_t m, int split, hipStream_t st);
 
 hipError_t launch_resolve(const DevState& s, int cur, int32_t n, int32_t m,
                           const int32_t* winner, const int32_t* second, const float* d1,

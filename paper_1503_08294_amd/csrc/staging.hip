@@ -1,0 +1,475 @@
+// Spatial staging shared by the screened find-winners scans (see find_screened.hip for the
+// screen and its rounding bound).
+//
+// Unit order.  Units are counting-sorted by the Morton code of a 32^3 grid cell over their
+// bounding box, and every find call gathers the current positions into that order as
+// packed (x, y, z, |w|^2) records.  The order only affects speed (every unit is still
+// visited for every signal), so it is rebuilt only when the host asks for it: after the
+// network changed size or indices, and periodically as units drift.
+// Signal order.  Signals are counting-sorted into the same grid on every call, so that a
+// wave owns signals that are near each other.
+// Seed.  For every signal, the exact direct-form distances to a window of sorted units
+// around its cell give B, the second smallest of them: an upper bound on the signal's
+// second-winner distance, reached by two real units.
+// Merge.  Per-chunk top-2 keys (bits(d) << 32 | index) of the scan are merged per signal
+// and written at the signal's original position.
+#include "gsn_internal.h"
+
+namespace gsn {
+namespace {
+
+constexpr int kGrid = 32;
+constexpr int kSignalShift = 3;                        // signals ordered by bucket >> 3
+constexpr int kSignalBuckets = kBuckets >> kSignalShift;
+constexpr int kSeedWindow = 64;
+constexpr int kSeedLanes = 4;
+
+__device__ __forceinline__ int32_t ord(float f) {
+  const int32_t b = __float_as_int(f);
+  return b >= 0 ? b : b ^ 0x7fffffff;
+}
+__device__ __forceinline__ float unord(int32_t b) {
+  return __int_as_float(b >= 0 ? b : b ^ 0x7fffffff);
+}
+
+// identities of the bounding-box accumulators: [0..2] ord(min), [3..5] ord(max)
+__device__ __forceinline__ int32_t acc_identity(int t) {
+  return t < 3 ? ord(__builtin_huge_valf()) : ord(-__builtin_huge_valf());
+}
+
+__device__ __forceinline__ uint32_t spread5(uint32_t v) {
+  v &= 31u;
+  v = (v | (v << 8)) & 0x0300Fu;
+  v = (v | (v << 4)) & 0x030C3u;
+  v = (v | (v << 2)) & 0x09249u;
+  return v;
+}
+
+__device__ __forceinline__ uint32_t cell_of(float p, float lo, float inv) {
+  const float t = fminf(fmaxf((p - lo) * inv, 0.0f), static_cast<float>(kGrid - 1));
+  return static_cast<uint32_t>(t);
+}
+
+// bb: lo.x lo.y lo.z inv.x inv.y inv.z
+__device__ __forceinline__ int32_t bucket_of(float x, float y, float z, const float* bb) {
+  return static_cast<int32_t>(spread5(cell_of(x, bb[0], bb[3])) |
+                              (spread5(cell_of(y, bb[1], bb[4])) << 1) |
+                              (spread5(cell_of(z, bb[2], bb[5])) << 2));
+}
+
+__device__ __forceinline__ float norm2(float x, float y, float z) {
+  return (x * x + y * y) + z * z;
+}
+
+// block-wide reduction of up to 4 values with op, result valid in thread 0
+template <typename Op>
+__device__ void block_reduce4(float v[4], Op op) {
+  __shared__ float red[kBlock / 64][4];
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1)
+#pragma unroll
+    for (int k = 0; k < 4; ++k) v[k] = op(v[k], __shfl_xor(v[k], off));
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0)
+#pragma unroll
+    for (int k = 0; k < 4; ++k) red[w][k] = v[k];
+  __syncthreads();
+  if (threadIdx.x == 0)
+    for (int ww = 1; ww < kBlock / 64; ++ww)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) v[k] = op(v[k], red[ww][k]);
+}
+
+struct FMin { __device__ float operator()(float a, float b) const { return fminf(a, b); } };
+struct FMax { __device__ float operator()(float a, float b) const { return fmaxf(a, b); } };
+
+// every histogram, offset and cursor array cleared; accumulators at their identities
+__global__ __launch_bounds__(kBlock) void st_init(StageBufs b) {
+  const int32_t i = blockIdx.x * kBlock + threadIdx.x;
+  if (i <= kBuckets) {
+    b.hist_u[i] = 0;
+    b.hist_s[i] = 0;
+    b.off_u[i] = 0;
+    b.off_s[i] = 0;
+    b.cur_u[i] = 0;
+    b.cur_s[i] = 0;
+  }
+  if (i < 16) b.acc[i] = i < 6 ? acc_identity(i) : 0;
+  if (i < 8) b.bb[i] = 0.0f;
+}
+
+// ------------------------------------------------------- unit bucketing (rare) ----
+
+__global__ __launch_bounds__(kBlock) void st_bbox(const float* __restrict__ x,
+                                                  const float* __restrict__ y,
+                                                  const float* __restrict__ z, int32_t n,
+                                                  int32_t* __restrict__ acc) {
+  float lo[4] = {__builtin_huge_valf(), __builtin_huge_valf(), __builtin_huge_valf(), 0.0f};
+  float hi[4] = {-__builtin_huge_valf(), -__builtin_huge_valf(), -__builtin_huge_valf(), 0.0f};
+  for (int32_t i = blockIdx.x * kBlock + threadIdx.x; i < n; i += gridDim.x * kBlock) {
+    const float p[3] = {x[i], y[i], z[i]};
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+      lo[k] = fminf(lo[k], p[k]);
+      hi[k] = fmaxf(hi[k], p[k]);
+    }
+  }
+  block_reduce4(lo, FMin());
+  __syncthreads();
+  block_reduce4(hi, FMax());
+  if (threadIdx.x == 0)
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+      atomicMin(&acc[k], ord(lo[k]));
+      atomicMax(&acc[3 + k], ord(hi[k]));
+    }
+}
+
+// Grid of this bucketing from the bounding box (written to bb by block 0), bucket of every
+// unit, per-bucket counts.
+__global__ __launch_bounds__(kBlock) void st_hist_units(const float* __restrict__ x,
+                                                        const float* __restrict__ y,
+                                                        const float* __restrict__ z, int32_t n,
+                                                        const int32_t* __restrict__ acc,
+                                                        float* __restrict__ bb,
+                                                        int32_t* __restrict__ ukey,
+                                                        int32_t* __restrict__ hist_u) {
+  __shared__ float sbb[6];
+  if (threadIdx.x < 3) {
+    const float lo = unord(acc[threadIdx.x]);
+    const float hi = unord(acc[3 + threadIdx.x]);
+    sbb[threadIdx.x] = lo;
+    sbb[3 + threadIdx.x] = hi > lo ? static_cast<float>(kGrid) / (hi - lo) : 0.0f;
+    if (blockIdx.x == 0) {
+      bb[threadIdx.x] = sbb[threadIdx.x];
+      bb[3 + threadIdx.x] = sbb[3 + threadIdx.x];
+    }
+  }
+  __syncthreads();
+  const int32_t i = blockIdx.x * kBlock + threadIdx.x;
+  if (i < n) {
+    const int32_t k = bucket_of(x[i], y[i], z[i], sbb);
+    ukey[i] = k;
+    atomicAdd(&hist_u[k], 1);
+  }
+}
+
+// Inclusive prefix sum over a 1024-thread workgroup: wave shuffles, then the 16 wave
+// totals through LDS (two barriers).
+__device__ int32_t block_inclusive_scan(int32_t v, int32_t* total) {
+  __shared__ int32_t wsum[16];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int32_t a = __shfl_up(v, o);
+    if (lane >= o) v += a;
+  }
+  if (lane == 63) wsum[w] = v;
+  __syncthreads();
+  int32_t before = 0, all = 0;
+#pragma unroll
+  for (int k = 0; k < 16; ++k) {
+    const int32_t x = wsum[k];
+    before += k < w ? x : 0;
+    all += x;
+  }
+  __syncthreads();
+  *total = all;
+  return v + before;
+}
+
+// One workgroup: exclusive scan of a histogram of B entries into off[] (off[B] = total)
+// and cur[], clearing the histogram.  Units (mode 0) also reset the bounding-box
+// accumulators.  Signals (mode 1) also reduce the gather's per-block magnitude maxima
+// (nmag blocks) into mag[].
+template <int B>
+__global__ __launch_bounds__(1024) void st_scan_hist(int32_t* __restrict__ hist,
+                                                     int32_t* __restrict__ off,
+                                                     int32_t* __restrict__ cur,
+                                                     int32_t* __restrict__ acc,
+                                                     const float* __restrict__ bmag,
+                                                     int32_t nmag, int32_t* __restrict__ mag,
+                                                     int mode) {
+  constexpr int per = B / 1024;
+  const int t = threadIdx.x;
+  int32_t v[per];
+  int32_t sum = 0;
+#pragma unroll
+  for (int i = 0; i < per; ++i) {
+    v[i] = hist[t * per + i];
+    sum += v[i];
+  }
+  int32_t total;
+  int32_t run = block_inclusive_scan(sum, &total) - sum;
+#pragma unroll
+  for (int i = 0; i < per; ++i) {
+    off[t * per + i] = run;
+    cur[t * per + i] = run;
+    hist[t * per + i] = 0;
+    run += v[i];
+  }
+  if (t == 1023) off[B] = total;
+  if (mode == 0 && t < 6) acc[t] = acc_identity(t);
+  if (mode == 1) {
+    float mg[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    for (int32_t b = t; b < nmag; b += 1024)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) mg[k] = fmaxf(mg[k], bmag[4 * b + k]);
+    __shared__ float red[16][4];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) mg[k] = fmaxf(mg[k], __shfl_xor(mg[k], o));
+    if ((t & 63) == 0)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) red[t >> 6][k] = mg[k];
+    __syncthreads();
+    if (t < 4) {
+      float r = 0.0f;
+      for (int w = 0; w < 16; ++w) r = fmaxf(r, red[w][t]);
+      mag[t] = __float_as_int(r);
+    }
+  }
+}
+
+__global__ __launch_bounds__(kBlock) void st_scatter_units(int32_t n,
+                                                           const int32_t* __restrict__ ukey,
+                                                           int32_t* __restrict__ cur_u,
+                                                           int32_t* __restrict__ pidx) {
+  const int32_t i = blockIdx.x * kBlock + threadIdx.x;
+  if (i >= n) return;
+  const int32_t pos = atomicAdd(&cur_u[ukey[i]], 1);
+  if (pos >= 0 && pos < n) pidx[pos] = i;  // always true when counts match keys
+}
+
+// ------------------------------------------------------------- every call ----
+
+// Blocks [0, ub): gather the current positions into sorted order and write each block's
+// magnitude maxima (max |x|, |y|, |z|, |w|^2) to bmag.  Blocks [ub, ...): bucket of every
+// signal in the grid of the last unit bucketing, counted per group of 2^kSignalShift
+// buckets (the signal order only needs to be coarsely spatial).
+__global__ __launch_bounds__(kBlock) void st_gather(const float* __restrict__ x,
+                                                    const float* __restrict__ y,
+                                                    const float* __restrict__ z, int32_t n,
+                                                    const int32_t* __restrict__ pidx,
+                                                    float4* __restrict__ pu,
+                                                    const float* __restrict__ sig, int32_t m,
+                                                    int32_t ub, const float* __restrict__ bb,
+                                                    int32_t* __restrict__ skey,
+                                                    int32_t* __restrict__ hist_s,
+                                                    float* __restrict__ bmag) {
+  if (static_cast<int32_t>(blockIdx.x) < ub) {
+    const int32_t pos = blockIdx.x * kBlock + threadIdx.x;
+    float mg[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    if (pos < n) {
+      const int32_t i = min(max(pidx[pos], 0), n - 1);
+      const float a = x[i], b = y[i], c = z[i];
+      const float nn = norm2(a, b, c);
+      pu[pos] = make_float4(a, b, c, nn);
+      mg[0] = fabsf(a);
+      mg[1] = fabsf(b);
+      mg[2] = fabsf(c);
+      mg[3] = nn;
+    }
+    block_reduce4(mg, FMax());
+    if (threadIdx.x == 0)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) bmag[4 * blockIdx.x + k] = mg[k];
+  } else {
+    const int32_t j = (blockIdx.x - ub) * kBlock + threadIdx.x;
+    if (j < m) {
+      const int32_t k = bucket_of(sig[j], sig[m + j], sig[2 * m + j], bb);
+      skey[j] = k;
+      atomicAdd(&hist_s[k >> kSignalShift], 1);
+    }
+  }
+}
+
+__global__ __launch_bounds__(kBlock) void st_scatter_signals(int32_t m,
+                                                             const int32_t* __restrict__ skey,
+                                                             int32_t* __restrict__ cur_s,
+                                                             int32_t* __restrict__ sperm) {
+  const int32_t j = blockIdx.x * kBlock + threadIdx.x;
+  if (j >= m) return;
+  const int32_t pos = atomicAdd(&cur_s[skey[j] >> kSignalShift], 1);
+  if (pos >= 0 && pos < m) sperm[pos] = j;  // always true when counts match keys
+}
+
+__device__ __forceinline__ unsigned long long pack(float d, int32_t i) {
+  return (static_cast<unsigned long long>(__float_as_uint(d)) << 32) |
+         static_cast<uint32_t>(i);
+}
+
+// top-2 of two top-2 lists of distinct keys
+__device__ __forceinline__ void merge2(unsigned long long& a1, unsigned long long& a2,
+                                       unsigned long long b1, unsigned long long b2) {
+  const unsigned long long lo = min(a1, b1), hi = max(a1, b1);
+  a2 = min(hi, min(a2, b2));
+  a1 = lo;
+}
+
+// kSeedLanes lanes per signal each scan a strided part of the window and merge.
+__global__ __launch_bounds__(kBlock) void st_seed(const float4* __restrict__ pu,
+                                                  const int32_t* __restrict__ pidx, int32_t n,
+                                                  const float* __restrict__ sig, int32_t m,
+                                                  const int32_t* __restrict__ sperm,
+                                                  const int32_t* __restrict__ skey,
+                                                  const int32_t* __restrict__ off_u,
+                                                  float* __restrict__ seed) {
+  const int32_t t = blockIdx.x * kBlock + threadIdx.x;
+  const int32_t p = t / kSeedLanes;
+  const int q = t % kSeedLanes;
+  unsigned long long k1 = ~0ull, k2 = ~0ull;
+  if (p < m) {
+    const int32_t j = min(max(sperm[p], 0), m - 1);
+    const float sx = sig[j], sy = sig[m + j], sz = sig[2 * m + j];
+    const int32_t k = skey[j];
+    const int32_t b0 = off_u[k], b1 = off_u[k + 1];
+    int32_t lo = (b0 + b1) / 2 - kSeedWindow / 2;
+    lo = max(0, min(lo, n - kSeedWindow));
+    const int32_t hi = min(n, lo + kSeedWindow);
+    for (int32_t r = lo + q; r < hi; r += kSeedLanes) {
+      const float4 w = pu[r];
+      const float dx = sx - w.x, dy = sy - w.y, dz = sz - w.z;
+      const unsigned long long key = pack((dx * dx + dy * dy) + dz * dz, pidx[r]);
+      merge2(k1, k2, key, ~0ull);
+    }
+  }
+#pragma unroll
+  for (int off = 1; off < kSeedLanes; off <<= 1) {
+    const unsigned long long o1 = __shfl_xor(k1, off);
+    const unsigned long long o2 = __shfl_xor(k2, off);
+    merge2(k1, k2, o1, o2);
+  }
+  if (p < m && q == 0)
+    seed[p] = k2 != ~0ull ? __uint_as_float(static_cast<uint32_t>(k2 >> 32))
+                          : __builtin_huge_valf();
+}
+
+// 32 signals per workgroup, 8 groups of lanes split the partial rows, merged in LDS.
+__global__ __launch_bounds__(kBlock) void st_merge(const unsigned long long* __restrict__ part,
+                                                   int32_t rows, int32_t m,
+                                                   const int32_t* __restrict__ sperm,
+                                                   int32_t* __restrict__ winner,
+                                                   int32_t* __restrict__ second,
+                                                   float* __restrict__ d1,
+                                                   float* __restrict__ d2) {
+  __shared__ unsigned long long sa[8][32], sb[8][32];
+  const int c = threadIdx.x & 31, g = threadIdx.x >> 5;
+  const int32_t p = blockIdx.x * 32 + c;
+  unsigned long long a = ~0ull, b = ~0ull;
+  // Rows may repeat a sentinel key (a chunk with fewer than two units under the seed bound
+  // reports (B, sentinel)); real keys are unique.  insert() keeps the two smallest
+  // distinct keys.
+  auto insert = [&](unsigned long long k) {
+    if (k < a) {
+      b = a;
+      a = k;
+    } else if (k < b && k != a) {
+      b = k;
+    }
+  };
+  if (p < m)
+    for (int32_t q = g; q < rows; q += 8) insert(part[q * static_cast<size_t>(m) + p]);
+  sa[g][c] = a;
+  sb[g][c] = b;
+  __syncthreads();
+  if (g != 0 || p >= m) return;
+  for (int h = 1; h < 8; ++h) {
+    insert(sa[h][c]);
+    insert(sb[h][c]);
+  }
+  const int32_t j = min(max(sperm[p], 0), m - 1);
+  winner[j] = static_cast<int32_t>(static_cast<uint32_t>(a));
+  second[j] = static_cast<int32_t>(static_cast<uint32_t>(b));
+  d1[j] = __uint_as_float(static_cast<uint32_t>(a >> 32));
+  d2[j] = __uint_as_float(static_cast<uint32_t>(b >> 32));
+}
+
+inline int blocks(int64_t n) { return static_cast<int>((n + kBlock - 1) / kBlock); }
+
+}  // namespace
+
+size_t stage_bytes(int32_t n_max, int32_t m_max) {
+  size_t b = 0;
+  auto add = [&](size_t x) { b += (x + 255) & ~static_cast<size_t>(255); };
+  const size_t nm = static_cast<size_t>(n_max), mm = static_cast<size_t>(m_max);
+  const size_t hb = 4 * static_cast<size_t>(kBuckets + 1);
+  add(16 * nm);  // pu
+  add(4 * nm);   // pidx
+  add(4 * nm);   // ukey
+  add(4 * mm);   // skey
+  add(4 * mm);   // sperm
+  add(4 * mm);   // seed
+  for (int i = 0; i < 6; ++i) add(hb);  // hist/off/cur for units and signals
+  add(4 * 16);   // acc
+  add(4 * 8);    // bb
+  add(4 * 4);    // mag
+  add(16 * (nm / kBlock + 1));  // bmag
+  return b;
+}
+
+StageBufs carve_stage(void* base, int32_t n_max, int32_t m_max) {
+  StageBufs s;
+  char* b = static_cast<char*>(base);
+  size_t o = 0;
+  auto take = [&](size_t x) {
+    char* r = b + o;
+    o += (x + 255) & ~static_cast<size_t>(255);
+    return r;
+  };
+  const size_t nm = static_cast<size_t>(n_max), mm = static_cast<size_t>(m_max);
+  const size_t hb = 4 * static_cast<size_t>(kBuckets + 1);
+  s.pu = reinterpret_cast<float4*>(take(16 * nm));
+  s.pidx = reinterpret_cast<int32_t*>(take(4 * nm));
+  s.ukey = reinterpret_cast<int32_t*>(take(4 * nm));
+  s.skey = reinterpret_cast<int32_t*>(take(4 * mm));
+  s.sperm = reinterpret_cast<int32_t*>(take(4 * mm));
+  s.seed = reinterpret_cast<float*>(take(4 * mm));
+  s.hist_u = reinterpret_cast<int32_t*>(take(hb));
+  s.off_u = reinterpret_cast<int32_t*>(take(hb));
+  s.cur_u = reinterpret_cast<int32_t*>(take(hb));
+  s.hist_s = reinterpret_cast<int32_t*>(take(hb));
+  s.off_s = reinterpret_cast<int32_t*>(take(hb));
+  s.cur_s = reinterpret_cast<int32_t*>(take(hb));
+  s.acc = reinterpret_cast<int32_t*>(take(4 * 16));
+  s.bb = reinterpret_cast<float*>(take(4 * 8));
+  s.mag = reinterpret_cast<int32_t*>(take(4 * 4));
+  s.bmag = reinterpret_cast<float*>(take(16 * (nm / kBlock + 1)));
+  return s;
+}
+
+hipError_t launch_stage_init(const StageBufs& b, hipStream_t st) {
+  st_init<<<blocks(kBuckets + 1), kBlock, 0, st>>>(b);
+  return hipGetLastError();
+}
+
+hipError_t launch_stage(const DevState& s, const StageBufs& b, int32_t n, const float* sig,
+                        int32_t m, bool rebucket, hipStream_t st) {
+  const int nb_u = blocks(n);
+  if (rebucket) {
+    st_bbox<<<std::min(nb_u, 64), kBlock, 0, st>>>(s.x, s.y, s.z, n, b.acc);
+    st_hist_units<<<nb_u, kBlock, 0, st>>>(s.x, s.y, s.z, n, b.acc, b.bb, b.ukey, b.hist_u);
+    st_scan_hist<kBuckets><<<1, 1024, 0, st>>>(b.hist_u, b.off_u, b.cur_u, b.acc, nullptr, 0,
+                                              b.mag, 0);
+    st_scatter_units<<<nb_u, kBlock, 0, st>>>(n, b.ukey, b.cur_u, b.pidx);
+  }
+  st_gather<<<nb_u + blocks(m), kBlock, 0, st>>>(s.x, s.y, s.z, n, b.pidx, b.pu, sig, m, nb_u,
+                                                 b.bb, b.skey, b.hist_s, b.bmag);
+  st_scan_hist<kSignalBuckets><<<1, 1024, 0, st>>>(b.hist_s, b.off_s, b.cur_s, b.acc, b.bmag,
+                                                   nb_u, b.mag, 1);
+  st_scatter_signals<<<blocks(m), kBlock, 0, st>>>(m, b.skey, b.cur_s, b.sperm);
+  st_seed<<<blocks(static_cast<int64_t>(m) * kSeedLanes), kBlock, 0, st>>>(
+      b.pu, b.pidx, n, sig, m, b.sperm, b.skey, b.off_u, b.seed);
+  return hipGetLastError();
+}
+
+hipError_t launch_stage_merge(const DevState& s, const StageBufs& b, int32_t m, int split,
+                              int32_t* winner, int32_t* second, float* d1, float* d2,
+                              hipStream_t st) {
+  st_merge<<<(m + 31) / 32, kBlock, 0, st>>>(s.part, 2 * split, m, b.sperm, winner, second, d1,
+                                             d2);
+  return hipGetLastError();
+}
+
+}  // namespace gsn

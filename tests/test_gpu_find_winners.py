@@ -70,3 +70,54 @@ def test_genus3_full_size():
     pair = Pair(units, m_max=wl.m)
     g, o = pair.find(sig)
     assert_find_equal(g, o, "genus3_200k")
+
+
+@pytest.mark.parametrize("variant", [1, 2])
+@pytest.mark.parametrize("n,m,seed", [(2, 3, 0), (3, 1, 1), (257, 999, 2), (4000, 16_384, 3),
+                                      (30_000, 5_000, 4)])
+def test_both_kernel_variants(variant, n, m, seed):
+    from paper_1503_08294_amd import gsn
+    rng = np.random.default_rng(100 + seed)
+    units = rng.standard_normal((3, n)).astype(np.float32)
+    sig = rng.standard_normal((3, m)).astype(np.float32)
+    pair = Pair(units, m_max=m)
+    pair.net.tune(gsn.GSN_TUNE_VARIANT, variant)
+    g, o = pair.find(sig)
+    assert_find_equal(g, o, f"variant={variant} n={n} m={m}")
+
+
+@pytest.mark.parametrize("variant", [1, 2])
+def test_cancellation_and_near_ties_far_from_the_origin(variant):
+    """Units and signals around (1000, -1000, 1000) separated by ~1e-3: the expanded form
+    loses about 12 bits to cancellation here, and many distances differ by a few ulps, so a
+    screen without a correct rounding margin would drop true winners."""
+    from paper_1503_08294_amd import gsn
+    rng = np.random.default_rng(77)
+    c = np.array([1000.0, -1000.0, 1000.0])[:, None]
+    n, m = 6000, 4096
+    off = rng.standard_normal((3, n)) * 1e-3
+    units = (c + off).astype(np.float32)
+    # a shell of near-equidistant units around some signals
+    sig = (c + rng.standard_normal((3, m)) * 1e-3).astype(np.float32)
+    for j in range(0, m, 97):
+        dirs = rng.standard_normal((3, 8))
+        dirs /= np.linalg.norm(dirs, axis=0)
+        k = (j // 97) * 8 % (n - 8)
+        units[:, k:k + 8] = (sig[:, j:j + 1].astype(np.float64) + 2e-4 * dirs).astype(np.float32)
+    pair = Pair(units, m_max=m)
+    pair.net.tune(gsn.GSN_TUNE_VARIANT, variant)
+    g, o = pair.find(sig)
+    assert_find_equal(g, o, f"variant={variant}")
+
+
+def test_screened_variant_ties_on_a_grid():
+    from paper_1503_08294_amd import gsn
+    rng = np.random.default_rng(5)
+    units = rng.integers(-2, 3, (3, 2000)).astype(np.float32)
+    sig = rng.integers(-2, 3, (3, 9000)).astype(np.float32)
+    pair = Pair(units, m_max=9000)
+    pair.net.tune(gsn.GSN_TUNE_VARIANT, 2)
+    for split in (1, 5, 64):
+        pair.net.tune(gsn.GSN_TUNE_SPLIT, split)
+        g, o = pair.find(sig)
+        assert_find_equal(g, o, f"split={split}")
