@@ -156,9 +156,11 @@ void gsn_destroy(gsn_net* net);
 /* Launch-configuration knobs, for tests and measurement; results never depend on them.
  *   GSN_TUNE_SPLIT    units are split into this many chunks scanned by separate
  *                     workgroups and merged afterwards (0 = automatic, 1..GSN_MAX_SPLIT)
- *   GSN_TUNE_VARIANT  find-winners kernel: 0 = automatic (screened), 1 = direct scan of
- *                     every distance, 2 = screened scan (expanded-form screen with a
- *                     rigorous rounding margin, direct-form recheck of candidates)
+ *   GSN_TUNE_VARIANT  find-winners kernel: 0 = automatic (3), 1 = direct scan of every
+ *                     distance, 2 = screened scan with the screen on the vector unit,
+ *                     3 = screened scan with the screen on the matrix cores (both screens
+ *                     carry a rigorous rounding margin; candidates are rechecked in the
+ *                     direct form)
  * Returns GSN_E_INVAL for an unknown key or value. */
 enum { GSN_TUNE_SPLIT = 1, GSN_TUNE_VARIANT = 2 };
 #define GSN_MAX_SPLIT 64

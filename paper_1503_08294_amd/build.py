@@ -5,6 +5,9 @@ Flags:
                          operation in binary32; no multiply-add contraction;
   -Xclang -target-feature -Xclang -packed-fp32-ops
                          no packed fp32 instructions are generated;
+  -mllvm -amdgpu-mfma-vgpr-form
+                         matrix-core results are written to ordinary VGPRs, so the vector
+                         unit reads them without accumulator-register copies;
   no fast-math, IEEE denormals (default for gfx950 fp32).
 """
 import os
@@ -13,13 +16,14 @@ import subprocess
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libgsn.so")
-SOURCES = ["gsn_host.hip", "find_winners.hip", "staging.hip", "find_screened.hip", "update.hip",
-           "grow.hip"]
+SOURCES = ["gsn_host.hip", "find_winners.hip", "staging.hip", "find_screened.hip",
+           "find_mfma.hip", "update.hip", "grow.hip"]
 ARCH = "gfx950"
 
 FLAGS = ["-O3", "-std=c++17", f"--offload-arch={ARCH}", "-fPIC", "-shared",
          "-ffp-contract=off", "-fno-fast-math",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+         "-mllvm", "-amdgpu-mfma-vgpr-form",
          "-Wall", "-Wno-unused-result"]
 
 

@@ -53,7 +53,7 @@ void carve(const gsn_params& p, void* base, DevState* s);
 // Every launcher enqueues on `stream` and returns the hipGetLastError() of its launches.
 
 struct FindConfig {
-  int variant;   // 1 = direct scan, 2 = screened scan
+  int variant;   // 1 = direct scan, 2 = screened scan (VALU), 3 = screened scan (MFMA)
   int split;     // unit chunks
 };
 FindConfig find_config(int32_t n, int32_t m, int cus, int want_split, int want_variant);
@@ -78,7 +78,8 @@ struct StageBufs {
   int32_t* acc;     // [16] bounding-box accumulators
   float* bb;        // [8] grid of the last unit bucketing: lo.xyz, cells per length.xyz
   int32_t* mag;     // [4] max |x|, |y|, |z|, |w|^2 of this call (float bits)
-  float* bmag;      // [n_max / kBlock + 1][4] per-block magnitude maxima
+  float* bmag;      // [n_max / kBlock + 2][4] per-block magnitude maxima
+  float* pm;        // [ceil(n_max / 64) * 256] units in matrix-core operand order
 };
 size_t stage_bytes(int32_t n_max, int32_t m_max);
 StageBufs carve_stage(void* base, int32_t n_max, int32_t m_max);
@@ -91,6 +92,9 @@ hipError_t launch_stage_merge(const DevState& s, const StageBufs& b, int32_t m, 
 int screened_split(int32_t n, int32_t m, int cus, int want);
 hipError_t launch_scan_screened(const DevState& s, const StageBufs& b, int32_t n,
                                 const float* sig, int32_t m, int split, hipStream_t st);
+int mfma_split(int32_t n, int32_t m, int cus, int want);
+hipError_t launch_scan_mfma(const DevState& s, const StageBufs& b, int32_t n, const float* sig,
+                            int32_t m, int split, hipStream_t st);
 
 hipError_t launch_resolve(const DevState& s, int cur, int32_t n, int32_t m,
                           const int32_t* winner, const int32_t* second, const float* d1,

@@ -253,6 +253,7 @@ __global__ __launch_bounds__(kBlock) void st_gather(const float* __restrict__ x,
                                                     const float* __restrict__ z, int32_t n,
                                                     const int32_t* __restrict__ pidx,
                                                     float4* __restrict__ pu,
+                                                    float* __restrict__ pm,
                                                     const float* __restrict__ sig, int32_t m,
                                                     int32_t ub, const float* __restrict__ bb,
                                                     int32_t* __restrict__ skey,
@@ -261,15 +262,27 @@ __global__ __launch_bounds__(kBlock) void st_gather(const float* __restrict__ x,
   if (static_cast<int32_t>(blockIdx.x) < ub) {
     const int32_t pos = blockIdx.x * kBlock + threadIdx.x;
     float mg[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    float cv[4] = {0.0f, 0.0f, 0.0f, __builtin_huge_valf()};  // padding: never a candidate
     if (pos < n) {
       const int32_t i = min(max(pidx[pos], 0), n - 1);
       const float a = x[i], b = y[i], c = z[i];
       const float nn = norm2(a, b, c);
       pu[pos] = make_float4(a, b, c, nn);
+      cv[0] = a;
+      cv[1] = b;
+      cv[2] = c;
+      cv[3] = nn;
       mg[0] = fabsf(a);
       mg[1] = fabsf(b);
       mg[2] = fabsf(c);
       mg[3] = nn;
+    }
+    if (pos < ((n + 63) & ~63)) {
+      // matrix-core layout: batch t = pos / 64 holds 4 groups of 16 units; component k of
+      // the unit in row i of group e sits at pm[256 t + 4 (16 k + i) + e]
+      const int32_t t = pos >> 6, e = (pos >> 4) & 3, i = pos & 15;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) pm[256 * t + 4 * (16 * k + i) + e] = cv[k];
     }
     block_reduce4(mg, FMax());
     if (threadIdx.x == 0)
@@ -405,7 +418,8 @@ size_t stage_bytes(int32_t n_max, int32_t m_max) {
   add(4 * 16);   // acc
   add(4 * 8);    // bb
   add(4 * 4);    // mag
-  add(16 * (nm / kBlock + 1));  // bmag
+  add(16 * (nm / kBlock + 2));  // bmag
+  add(16 * ((nm + 63) / 64 * 64));  // pm
   return b;
 }
 
@@ -435,7 +449,8 @@ StageBufs carve_stage(void* base, int32_t n_max, int32_t m_max) {
   s.acc = reinterpret_cast<int32_t*>(take(4 * 16));
   s.bb = reinterpret_cast<float*>(take(4 * 8));
   s.mag = reinterpret_cast<int32_t*>(take(4 * 4));
-  s.bmag = reinterpret_cast<float*>(take(16 * (nm / kBlock + 1)));
+  s.bmag = reinterpret_cast<float*>(take(16 * (nm / kBlock + 2)));
+  s.pm = reinterpret_cast<float*>(take(16 * ((nm + 63) / 64 * 64)));
   return s;
 }
 
@@ -454,10 +469,11 @@ hipError_t launch_stage(const DevState& s, const StageBufs& b, int32_t n, const 
                                               b.mag, 0);
     st_scatter_units<<<nb_u, kBlock, 0, st>>>(n, b.ukey, b.cur_u, b.pidx);
   }
-  st_gather<<<nb_u + blocks(m), kBlock, 0, st>>>(s.x, s.y, s.z, n, b.pidx, b.pu, sig, m, nb_u,
-                                                 b.bb, b.skey, b.hist_s, b.bmag);
+  const int nb_g = blocks((static_cast<int64_t>(n) + 63) & ~static_cast<int64_t>(63));
+  st_gather<<<nb_g + blocks(m), kBlock, 0, st>>>(s.x, s.y, s.z, n, b.pidx, b.pu, b.pm, sig, m,
+                                                 nb_g, b.bb, b.skey, b.hist_s, b.bmag);
   st_scan_hist<kSignalBuckets><<<1, 1024, 0, st>>>(b.hist_s, b.off_s, b.cur_s, b.acc, b.bmag,
-                                                   nb_u, b.mag, 1);
+                                                   nb_g, b.mag, 1);
   st_scatter_signals<<<blocks(m), kBlock, 0, st>>>(m, b.skey, b.cur_s, b.sperm);
   st_seed<<<blocks(static_cast<int64_t>(m) * kSeedLanes), kBlock, 0, st>>>(
       b.pu, b.pidx, n, sig, m, b.sperm, b.skey, b.off_u, b.seed);
