@@ -47,19 +47,16 @@ __device__ __forceinline__ float norm2(float x, float y, float z) {
   return (x * x + y * y) + z * z;
 }
 
-// insert a key into a top-2 of distinct keys
+// insert a key into a top-2 of distinct keys (branch-free, so the per-block key arrays stay
+// in registers)
 __device__ __forceinline__ bool insert2(unsigned long long& k1, unsigned long long& k2,
                                         unsigned long long key) {
-  if (key < k1) {
-    k2 = k1;
-    k1 = key;
-    return true;
-  }
-  if (key < k2 && key != k1) {
-    k2 = key;
-    return true;
-  }
-  return false;
+  const bool lt1 = key < k1;
+  const bool lt2 = key < k2 && key != k1;
+  const unsigned long long n2 = lt1 ? k1 : (lt2 ? key : k2);
+  k1 = lt1 ? key : k1;
+  k2 = n2;
+  return lt1 || lt2;
 }
 
 __device__ __forceinline__ float theta_of(unsigned long long k2, float ss, float ee) {
@@ -108,11 +105,28 @@ __device__ __forceinline__ int32_t batch_min(const v4f (&d)[4][NB]) {
   return imin3(acc[0], acc[1], min(acc[2], acc[3]));
 }
 
-// Exact recheck of the lane's candidates in batch t: the unit of group e, row 4 g + r is
-// 64 t + 16 e + 4 g + r.  Returns true if a top-2 improved.
+// Candidates of a batch as one 16-bit mask per block: bit 4 e + r is set when the unit of
+// group e, row 4 g + r passes the screen for the lane's signal of block b.
 template <int NB>
-__device__ __forceinline__ bool batch_recheck(const v4f (&d)[4][NB], int32_t t, int g, int32_t n,
-                                              const float4* __restrict__ pu,
+__device__ __forceinline__ void batch_masks(const v4f (&d)[4][NB], uint32_t (&mk)[NB]) {
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    uint32_t x = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) x |= (bits(d[e][b][r]) <= 0 ? 1u : 0u) << (4 * e + r);
+    mk[b] = x;
+  }
+}
+
+// Exact recheck of the lane's candidates in batch t: the unit of group e, row i = 4 g + r
+// is 64 t + 16 e + i; its component k is slot[4 (16 k + i) + e] of the wave's LDS copy of
+// the batch.  The unit's index is read from pidx only when the distance can enter the
+// top-2.  Returns true if a top-2 improved.
+template <int NB>
+__device__ __forceinline__ bool batch_recheck(const uint32_t (&mk)[NB], int32_t t, int g,
+                                              int32_t n, const float* __restrict__ slot,
                                               const int32_t* __restrict__ pidx,
                                               const float (&sx)[NB], const float (&sy)[NB],
                                               const float (&sz)[NB],
@@ -120,21 +134,21 @@ __device__ __forceinline__ bool batch_recheck(const v4f (&d)[4][NB], int32_t t, 
                                               unsigned long long (&k2)[NB]) {
   bool improved = false;
 #pragma unroll
-  for (int e = 0; e < 4; ++e) {
-#pragma unroll
-    for (int b = 0; b < NB; ++b) {
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        if (bits(d[e][b][r]) > 0) continue;
-        const int32_t uu = 64 * t + 16 * e + 4 * g + r;
-        if (uu >= n) continue;  // padding
-        const float4 w = pu[uu];
-        const float dx = sx[b] - w.x;
-        const float dy = sy[b] - w.y;
-        const float dz = sz[b] - w.z;
-        const float dd = (dx * dx + dy * dy) + dz * dz;
-        improved |= insert2(k1[b], k2[b], pack(dd, pidx[uu]));
-      }
+  for (int b = 0; b < NB; ++b) {
+    uint32_t x = mk[b];
+    while (x) {
+      const int s = __builtin_ctz(x);
+      x &= x - 1;
+      const int e = s >> 2, i = 4 * g + (s & 3);
+      const int32_t uu = 64 * t + 16 * e + i;
+      if (uu >= n) continue;  // padding
+      const float dx = sx[b] - slot[4 * i + e];
+      const float dy = sy[b] - slot[4 * (16 + i) + e];
+      const float dz = sz[b] - slot[4 * (32 + i) + e];
+      const float dd = (dx * dx + dy * dy) + dz * dz;
+      // keys order by distance first: only a distance <= the current second can enter
+      if (__float_as_uint(dd) > static_cast<uint32_t>(k2[b] >> 32)) continue;
+      improved |= insert2(k1[b], k2[b], pack(dd, pidx[uu]));
     }
   }
   return improved;
@@ -143,8 +157,8 @@ __device__ __forceinline__ bool batch_recheck(const v4f (&d)[4][NB], int32_t t, 
 // Units arrive in batches of 64 (four groups of 16) in matrix-core operand order: lane
 // (j, g) finds component g of the unit in row j of groups 0..3 of batch t as the float4 at
 // pm[256 t + 4 (16 g + j)], so a wave's operands for a batch are one contiguous 1 KB load.
-// Waves are independent (no LDS, no barriers); each operand load is issued a batch ahead of
-// its use.  A candidate's coordinates and index are read from pu / pidx.  Thresholds are
+// Waves are independent (no barriers); each operand load is issued a batch ahead of its
+// use.  Thresholds are
 // refreshed from the lanes' top-2 states after every pair of batches (a stale, larger
 // threshold only admits extra candidates), so the C operands stay fixed inside the body.
 __global__ __launch_bounds__(256) void fm_scan(const float4* __restrict__ pu,
@@ -157,8 +171,10 @@ __global__ __launch_bounds__(256) void fm_scan(const float4* __restrict__ pu,
                                                const int32_t* __restrict__ mag,
                                                unsigned long long* __restrict__ part) {
   constexpr int NB = kBlocksPerWave;
+  __shared__ __attribute__((aligned(16))) float lds[4][256];   // one batch per wave
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int j = lane & 15, g = lane >> 4;
+  float* slot = lds[wave];
   const int32_t c = blockIdx.y;
   const int32_t n_batches = (n + 63) >> 6;
   const int32_t t_begin = c * chunk_batches;
@@ -195,18 +211,30 @@ __global__ __launch_bounds__(256) void fm_scan(const float4* __restrict__ pu,
   const float4* opnd = reinterpret_cast<const float4*>(pm) + 16 * g + j;
   float4 a0 = t_begin < t_end ? opnd[64 * t_begin] : make_float4(0.f, 0.f, 0.f, 0.f);
   float4 a1 = t_begin + 1 < t_end ? opnd[64 * (t_begin + 1)] : make_float4(0.f, 0.f, 0.f, 0.f);
+  // the wave's copy of a batch in LDS serves the candidates' exact rechecks
+  float4* my = reinterpret_cast<float4*>(slot) + 16 * g + j;
   for (int32_t t = t_begin; t < t_end; t += 2) {
     bool improved = false;
     v4f d[4][NB];
+    // every lane writes its part of the batch (uniform control flow): a lane's recheck
+    // reads rows that other lanes loaded
+    *my = a0;
     mfma_batch<NB>(a0, bop, cc, d);
+    if (batch_min<NB>(d) <= 0) {
+      uint32_t mk[NB];
+      batch_masks<NB>(d, mk);
+      improved |= batch_recheck<NB>(mk, t, g, n, slot, pidx, sx, sy, sz, k1, k2);
+    }
     if (t + 2 < t_end) a0 = opnd[64 * (t + 2)];
-    if (batch_min<NB>(d) <= 0)
-      improved |= batch_recheck<NB>(d, t, g, n, pu, pidx, sx, sy, sz, k1, k2);
     if (t + 1 < t_end) {
+      *my = a1;
       mfma_batch<NB>(a1, bop, cc, d);
+      if (batch_min<NB>(d) <= 0) {
+        uint32_t mk[NB];
+        batch_masks<NB>(d, mk);
+        improved |= batch_recheck<NB>(mk, t + 1, g, n, slot, pidx, sx, sy, sz, k1, k2);
+      }
       if (t + 3 < t_end) a1 = opnd[64 * (t + 3)];
-      if (batch_min<NB>(d) <= 0)
-        improved |= batch_recheck<NB>(d, t + 1, g, n, pu, pidx, sx, sy, sz, k1, k2);
     }
     if (improved) {
 #pragma unroll
@@ -228,18 +256,15 @@ __global__ __launch_bounds__(256) void fm_scan(const float4* __restrict__ pu,
       insert2(k1[b], k2[b], o2);
     }
   }
-  // lane (j, g) writes block g's signal j
-  unsigned long long w1 = k1[0], w2 = k2[0];
+  // lane (j, g) writes block g's signal j (one predicated store per block, so the
+  // per-block arrays are never indexed by a lane-dependent value)
 #pragma unroll
-  for (int b = 1; b < NB; ++b)
-    if (g == b) {
-      w1 = k1[b];
-      w2 = k2[b];
+  for (int b = 0; b < NB; ++b) {
+    const int32_t p = base + 16 * b + j;
+    if (g == b && p < m) {
+      part[(2 * c) * static_cast<size_t>(m) + p] = k1[b];
+      part[(2 * c + 1) * static_cast<size_t>(m) + p] = k2[b];
     }
-  const int32_t p = base + 16 * g + j;
-  if (g < NB && p < m) {
-    part[(2 * c) * static_cast<size_t>(m) + p] = w1;
-    part[(2 * c + 1) * static_cast<size_t>(m) + p] = w2;
   }
 }
 
