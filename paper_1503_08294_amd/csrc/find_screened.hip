@@ -31,6 +31,11 @@
 //   each at most u times a quantity bounded by T_j, S^ or B_j >= d2) covers the inequality.
 // The screen may admit extra candidates (they are then rejected exactly); it never drops
 // a unit of the true top-2.
+//
+// Range: the bound needs every quantity above to be finite.  A signal whose margin E_j
+// exceeds 2^90 (huge or non-finite coordinates of the signal or of some unit) is "open":
+// every unit is its candidate, i.e. it is scanned exactly in the direct form.  Below that
+// margin T_j, S^ and B_j are at most 2^110, so no product, sum or threshold overflows.
 #include "gsn_internal.h"
 
 namespace gsn {
@@ -75,6 +80,7 @@ __global__ __launch_bounds__(kBlock) void fs_scan(const float4* __restrict__ pu,
   const float nmx = __int_as_float(mag[3]);
 
   float ax[S], ay[S], az[S], sx[S], sy[S], sz[S], ss[S], ee[S], th[S];
+  bool op[S];  // open: the screen's range does not hold, every unit is a candidate
   float d1[S], d2[S];
   int32_t i1[S], i2[S];
   const int32_t p0 = blockIdx.x * (kBlock * S) + threadIdx.x;
@@ -93,6 +99,8 @@ __global__ __launch_bounds__(kBlock) void fs_scan(const float4* __restrict__ pu,
     const float B = live ? seed[p] : 0.0f;
     const float T = 2.0f * (fabsf(sx[s]) * xm + fabsf(sy[s]) * ym + fabsf(sz[s]) * zm) + nmx;
     ee[s] = 16.0f * u * (T + 2.0f * ss[s] + 2.0f * B) + 7.52316384526264e-37f;
+    // 2^90 = 0x6c800000; the integer test also catches inf and NaN
+    op[s] = (__float_as_uint(ee[s]) & 0x7fffffffu) > 0x6c800000u;
     d1[s] = B;
     d2[s] = B;
     i1[s] = kSentinel;
@@ -131,7 +139,7 @@ __global__ __launch_bounds__(kBlock) void fs_scan(const float4* __restrict__ pu,
         float mn = q[0];
 #pragma unroll
         for (int k = 1; k < kGroup; ++k) mn = fminf(mn, q[k]);
-        hs[s] = mn <= th[s];
+        hs[s] = mn <= th[s] || op[s];
         hit |= hs[s];
       }
       if (hit) {
@@ -141,7 +149,7 @@ __global__ __launch_bounds__(kBlock) void fs_scan(const float4* __restrict__ pu,
           for (int k = 0; k < kGroup; ++k) {
             const float q = __builtin_fmaf(
                 ax[s], w[k].x, __builtin_fmaf(ay[s], w[k].y, __builtin_fmaf(az[s], w[k].z, w[k].w)));
-            if (!(q <= th[s])) continue;
+            if (!(q <= th[s]) && !op[s]) continue;
             const int32_t id = tid[g * kGroup + k];
             if (id == kSentinel) continue;
             const float dx = sx[s] - w[k].x;

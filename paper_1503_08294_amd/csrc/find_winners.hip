@@ -72,8 +72,10 @@ __global__ __launch_bounds__(kBlock) void fw_scan_direct(
         const float dy = sy[s] - w.y;
         const float dz = sz[s] - w.z;
         const float d = (dx * dx + dy * dy) + dz * dz;
-        const bool c1 = d < d1[s];
-        const bool c2 = d < d2[s];
+        // an empty slot (index -1) admits any distance, +inf included; units arrive in
+        // increasing index order, so the strict test keeps the smaller index on ties
+        const bool c1 = d < d1[s] || i1[s] < 0;
+        const bool c2 = d < d2[s] || i2[s] < 0;
         d2[s] = c1 ? d1[s] : (c2 ? d : d2[s]);
         i2[s] = c1 ? i1[s] : (c2 ? idx : i2[s]);
         d1[s] = c1 ? d : d1[s];

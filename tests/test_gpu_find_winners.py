@@ -122,3 +122,51 @@ def test_screened_variants_ties_on_a_grid(variant):
         pair.net.tune(gsn.GSN_TUNE_SPLIT, split)
         g, o = pair.find(sig)
         assert_find_equal(g, o, f"split={split}")
+
+
+@pytest.mark.parametrize("variant", [1, 2, 3])
+@pytest.mark.parametrize("scale", [1e17, 1e20])
+def test_huge_signal_coordinates_are_scanned_exactly(variant, scale):
+    """Signals far outside the screen's range (margin above 2^90, distances near or past
+    binary32 overflow) beside ordinary ones: the screened variants scan such signals
+    exactly in the direct form; ties of overflowed distances go to the smaller index."""
+    from paper_1503_08294_amd import gsn
+    rng = np.random.default_rng(31)
+    units = rng.standard_normal((3, 3000)).astype(np.float32)
+    sig = rng.standard_normal((3, 1000)).astype(np.float32)
+    far = rng.choice(1000, 120, replace=False)
+    sig[:, far] = (rng.standard_normal((3, 120)) * scale).astype(np.float32)
+    pair = Pair(units, m_max=1000)
+    pair.net.tune(gsn.GSN_TUNE_VARIANT, variant)
+    g, o = pair.find(sig)
+    assert_find_equal(g, o, f"variant={variant} scale={scale:g}")
+
+
+@pytest.mark.parametrize("variant", [2, 3])
+def test_one_huge_unit_opens_every_signal(variant):
+    """A single unit at 1e19 makes the magnitude bounds overflow, so every signal is open
+    (scanned exactly); results still match the oracle."""
+    from paper_1503_08294_amd import gsn
+    rng = np.random.default_rng(32)
+    units = rng.standard_normal((3, 700)).astype(np.float32)
+    units[:, 123] = np.float32(1e19)
+    sig = rng.standard_normal((3, 300)).astype(np.float32)
+    pair = Pair(units, m_max=300)
+    pair.net.tune(gsn.GSN_TUNE_VARIANT, variant)
+    g, o = pair.find(sig)
+    assert_find_equal(g, o, f"variant={variant}")
+
+
+@pytest.mark.parametrize("variant", [2, 3])
+def test_everything_at_1e17_is_scanned_exactly(variant):
+    """Units and signals spread at the 1e17 scale: distances are finite and distinct but the
+    screen's margin exceeds its range for every signal, so all are scanned exactly."""
+    from paper_1503_08294_amd import gsn
+    rng = np.random.default_rng(33)
+    units = (rng.standard_normal((3, 900)) * 1e17).astype(np.float32)
+    sig = (rng.standard_normal((3, 400)) * 1e17).astype(np.float32)
+    pair = Pair(units, m_max=400)
+    pair.net.tune(gsn.GSN_TUNE_VARIANT, variant)
+    g, o = pair.find(sig)
+    assert len(np.unique(o[0])) > 100, "the case must not collapse into ties"
+    assert_find_equal(g, o, f"variant={variant}")
