@@ -201,6 +201,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
                                                int32_t chunk_batches,
                                                const float* __restrict__ sig, int32_t m,
                                                const int32_t* __restrict__ sperm,
+                                               const int32_t* __restrict__ skey,
+                                               const int32_t* __restrict__ off_u,
                                                const float* __restrict__ seed,
                                                const int32_t* __restrict__ mag,
                                                unsigned long long* __restrict__ part) {
@@ -210,8 +212,23 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
   __shared__ float sdata[4][kBlocksPerWave * kSigFields * 64];     // rare-path signal data
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int j = lane & 15, g = lane >> 4;
-  const int32_t c = blockIdx.y;
   const int32_t n_batches = (n + 63) >> 6;
+  // Chunk order: the signal block's candidates (and so its rare-path work) concentrate in the
+  // chunk holding the units of the same grid cells, its home chunk, found from the bucket of
+  // the block's middle signal.  Row y of the grid takes chunk home + 0, +1, -1, +2, -2, ...
+  // (mod split, a bijection), so the work-groups with the most rare-path work start first
+  // instead of forming the tail.
+  int32_t c;
+  {
+    const int32_t split = static_cast<int32_t>(gridDim.y);
+    const int32_t pm_ = min(blockIdx.x * kSignalsPerWG + kSignalsPerWG / 2, m - 1);
+    const int32_t key = min(max(skey[min(max(sperm[pm_], 0), m - 1)], 0), kBuckets - 1);
+    const int32_t pos = min(max(off_u[key], 0), n);
+    const int32_t home = min(pos / (64 * chunk_batches), split - 1);
+    const int32_t y = static_cast<int32_t>(blockIdx.y);
+    const int32_t d = (y & 1) ? (y + 1) / 2 : -(y / 2);
+    c = ((home + d) % split + split) % split;
+  }
   const int32_t t_begin = c * chunk_batches;
   const int32_t t_end = min(n_batches, t_begin + chunk_batches);
   const float u = 5.9604644775390625e-8f;
@@ -357,8 +374,8 @@ hipError_t launch_scan_mfma(const DevState& s, const StageBufs& b, int32_t n, co
   const int32_t n_batches = (n + 63) / 64;
   const int32_t chunk_batches = (n_batches + split - 1) / split;
   dim3 grid((m + kSignalsPerWG - 1) / kSignalsPerWG, split);
-  fm_scan<<<grid, 256, 0, st>>>(b.pu, b.pm, b.pidx, n, chunk_batches, sig, m, b.sperm, b.seed,
-                                b.mag, s.part);
+  fm_scan<<<grid, 256, 0, st>>>(b.pu, b.pm, b.pidx, n, chunk_batches, sig, m, b.sperm, b.skey,
+                                b.off_u, b.seed, b.mag, s.part);
   return hipGetLastError();
 }
 
