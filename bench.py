@@ -9,10 +9,12 @@ Prints one JSON line:
   value            whole-iteration signal-unit distance evaluations per second (m*N/step)
   signals_per_s    m per step time
   fw_evals_per_s   m*N per find-winners call (HIP events around the call)
-  roofline         the find-winners scan kernel: algorithmic fp32 FLOP/s (8 per
-                   evaluation) from HIP events around each launch on the library's stream,
-                   against the fp32 vector peak; HBM traffic per launch from rocprofv3
-                   counters when a summary for the current kernel source exists
+  roofline         the find-winners scan kernel (fm_scan, the screened scan on the matrix
+                   cores): algorithmic fp32 FLOP/s (8 per evaluation, which is also what
+                   its K = 4 products execute) from HIP events around each launch on the
+                   library's stream, against the fp32 peak (157.3 TFLOP/s, vector and
+                   matrix alike); HBM traffic per launch from rocprofv3 counters when a
+                   summary for the current kernel source exists
   cpu_baseline     the CPU oracle timed on this host's cores on the first iterations of the
                    same workload
 """
@@ -30,11 +32,12 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "signal-unit distance evals/s and signals/s at 1 GPU; % fp32 VALU peak"
-FP32_PEAK_TFLOPS = 157.3     # 256 CUs x 2.4 GHz x 256 fp32 flop/clk (packed FMA)
+FP32_PEAK_TFLOPS = 157.3     # 256 CUs x 2.4 GHz x 256 fp32 flop/clk; also the fp32 MFMA peak
 FLOPS_PER_EVAL = 8           # 3 sub + 3 mul + 2 add of one squared distance
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "find_winners_genus3_200k_traffic.json")
+SCAN_KERNEL = "fm_scan"
 SCAN_SOURCES = [os.path.join(ROOT, "paper_1503_08294_amd", "csrc", f)
-                for f in ("find_winners.hip", "find_screened.hip")]
+                for f in ("find_mfma.hip", "gsn_internal.h")]
 
 
 def scan_source_hash() -> str:
@@ -206,7 +209,7 @@ def main():
         "phase_ms": phase,
         "conflict_rate": conflict_rate,
         "state_after": {"units": n_units, "edges": n_edges},
-        "roofline": {"bound": "alu", "kernel": "fs_scan", "achieved": achieved,
+        "roofline": {"bound": "mfma", "kernel": SCAN_KERNEL, "achieved": achieved,
                      "peak": FP32_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / FP32_PEAK_TFLOPS, "traffic": traffic,
                      "flops_per_launch": FLOPS_PER_EVAL * m * n,
