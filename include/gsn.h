@@ -156,11 +156,12 @@ void gsn_destroy(gsn_net* net);
 /* Launch-configuration knobs, for tests and measurement; results never depend on them.
  *   GSN_TUNE_SPLIT    units are split into this many chunks scanned by separate
  *                     workgroups and merged afterwards (0 = automatic, 1..GSN_MAX_SPLIT)
- *   GSN_TUNE_VARIANT  find-winners kernel: 0 = automatic (3), 1 = direct scan of every
+ *   GSN_TUNE_VARIANT  find-winners kernel: 0 = automatic (4), 1 = direct scan of every
  *                     distance, 2 = screened scan with the screen on the vector unit,
- *                     3 = screened scan with the screen on the matrix cores (both screens
- *                     carry a rigorous rounding margin; candidates are rechecked in the
- *                     direct form)
+ *                     3 = screened scan with the screen on the matrix cores in binary32,
+ *                     4 = the same screen on the matrix cores in split binary16 (every
+ *                     screen carries a rigorous rounding margin; candidates are rechecked
+ *                     in the binary32 direct form, so all variants return the same result)
  * Returns GSN_E_INVAL for an unknown key or value. */
 enum { GSN_TUNE_SPLIT = 1, GSN_TUNE_VARIANT = 2 };
 #define GSN_MAX_SPLIT 64

@@ -1,0 +1,373 @@
+// Find Winners, screened exhaustive variant on the matrix cores in split binary16.  Same
+// result as the direct scan (the exact lexicographic top-2 of the binary32 direct-form
+// distances); the screen of find_mfma.hip is evaluated with v_mfma_f32_32x32x16_f16, which
+// produces four times as many pairs per instruction as the binary32 16x16x4 product at
+// 1.6 times its issue cost.
+//
+// Scaling and split.  Units and signals are scaled by sigma = 2^k (staging: sigma times
+// the largest coordinate of the bucketing box lies in [16, 32)), which is exact, and every
+// scaled coordinate v is split as v = v1 + v2 + e with v1, v2 binary16.  One product per
+// 32-unit group and 32-signal block computes, for unit i and signal j,
+//     Q[i][j] = sum over axes a of (w1 + w2)_a (b1 + b2)_a + n1 + n2,   b = -2 sigma s,
+// where n1 + n2 splits the binary32 norm of the scaled unit: K = 14 of the 16 slots (lane
+// half h = 0 carries x and y, h = 1 carries z and the norm).  Every product of two binary16
+// numbers is exact in binary32.  A unit is a candidate for signal j iff Q <= theta_j (scaled).
+//
+// Lane layout (wave64, 32x32x16 f16, measured): lane l = 32 h + j supplies A[j][8h..8h+7]
+// (unit j of the group) and B[8h..8h+7][j] (signal j of the block) and receives
+// D[8q + 4h + r][j] as item 4q + r.  So lane l owns signal j of every block and sees the 16
+// units 8q + 4h + r of every group; the two partial top-2 states of a signal are merged at
+// the end.
+//
+// Rounding bound (u = 2^-24; everything scaled by sigma, sigma^2 for squares, exactly).
+//   split: |e| <= 2^-22 |v| + 2^-25, so the products of the pieces miss at most
+//     sum_a (2^-21 |w_a| |b_a| + 2^-25 (|w_a| + |b_a|)) + 2^-22 n + 2^-25;
+//   the matrix core sums the 14 exact products with an error measured at most 3.0 u of the
+//   sum of |terms|; the bound allows 32 u (15 additions, truncating);
+//   the sum of |terms| is at most (1 + 2^-9) T_j, T_j = 2(|sx| Xmax + |sy| Ymax + |sz| Zmax)
+//   + Nmax (scaled maxima over all units); the binary32 norms are within 3.01 u.
+//   So |Q^ - q| <= 43.1u T_j + 2^-25 (2 (|sx| + |sy| + |sz|) + 385) with q the exact
+//   |w|^2 - 2 s.w, and as in find_mfma.hip a unit with direct-form distance <= d2 has
+//   Q^ <= theta = fl(fl(fl(d2 (1 + 2^-20)) - S^) + E_j) whenever
+//   E_j (1 - u) >= 43.1u T_j + 5.02u S^ + 2.01u B_j + 2^-25 (2 (|sx| + |sy| + |sz|) + 385).
+//   The kernel uses E_j = 46u T_j + 6u S^ + 3u B_j + 2^-24 (2 (|sx| + |sy| + |sz|) + 400)
+//   + 2^-120, whose slack covers the five roundings of computing it.
+//
+// Range: the bound needs the binary16 pieces finite and the norm split meaningful: the call
+// is screened only if sigma max|w| <= 128 over the units of this call (so n <= 49152 <
+// 65504), and a signal only if its scaled coordinates are at most 2^14 in magnitude and its
+// margin at most 2^90.  Otherwise the call, or the signal, is "open": every unit is a
+// candidate, scanned exactly in the direct form from the binary32 copy.
+#include "gsn_internal.h"
+
+namespace gsn {
+namespace {
+
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+typedef float f4 __attribute__((ext_vector_type(4)));   // a native vector: stays in registers
+
+constexpr int kBlocks = 2;                        // 32-signal blocks per wave
+constexpr int kSignalsPerWG = 4 * 32 * kBlocks;   // 4 waves
+constexpr int32_t kSentinel = 0x7fffffff;
+constexpr int kDepth = 4;             // operand ring: loads run kDepth - 1 batches ahead
+static_assert(kDepth % 2 == 0, "the result sets alternate by batch parity");
+constexpr int kSigFields = 5;         // rare-path signal data: sx, sy, sz, S^, E (scaled S, E)
+
+__device__ __forceinline__ unsigned long long pack(float d, int32_t i) {
+  return (static_cast<unsigned long long>(__float_as_uint(d)) << 32) |
+         static_cast<uint32_t>(i);
+}
+
+__device__ __forceinline__ float norm2(float x, float y, float z) {
+  return (x * x + y * y) + z * z;
+}
+
+// insert a key into a top-2 of distinct keys (branch-free)
+__device__ __forceinline__ bool insert2(unsigned long long& k1, unsigned long long& k2,
+                                        unsigned long long key) {
+  const bool lt1 = key < k1;
+  const bool lt2 = key < k2 && key != k1;
+  const unsigned long long n2 = lt1 ? k1 : (lt2 ? key : k2);
+  k1 = lt1 ? key : k1;
+  k2 = n2;
+  return lt1 || lt2;
+}
+
+// scaled threshold from the lane's second key (unscaled distance) and the scale squared
+__device__ __forceinline__ float theta_of(unsigned long long k2, float sig2, float ss,
+                                          float ee) {
+  const float d2 = __uint_as_float(static_cast<uint32_t>(k2 >> 32)) * sig2;
+  return (d2 * 1.00000095367431640625f - ss) + ee;
+}
+
+__device__ __forceinline__ float fmin3(float a, float b, float c) {
+  return __builtin_elementwise_minimum(__builtin_elementwise_minimum(a, b), c);
+}
+
+// Minimum of the 32 results of a block (two groups).
+__device__ __forceinline__ float block_min(const v16f (&r)[2]) {
+  float m[2];
+#pragma unroll
+  for (int e = 0; e < 2; ++e) {
+    const float a = fmin3(r[e][0], r[e][1], r[e][2]);
+    const float b = fmin3(r[e][3], r[e][4], r[e][5]);
+    const float c = fmin3(r[e][6], r[e][7], r[e][8]);
+    const float d = fmin3(r[e][9], r[e][10], r[e][11]);
+    const float f = fmin3(r[e][12], r[e][13], r[e][14]);
+    m[e] = __builtin_elementwise_minimum(fmin3(a, b, c), fmin3(d, f, r[e][15]));
+  }
+  return __builtin_elementwise_minimum(m[0], m[1]);
+}
+
+// The rare path of block b of batch t, under a wave-uniform condition: bit 16 e + 4 q + r of
+// the lane's mask is set when its unit of group e, row 8 q + 4 h + r passes the screen
+// (r[e][4q + r] <= th, or the signal is open); that unit is 64 t + 32 e + 8 q + 4 h + r, its
+// binary32 coordinates are lu[32 e + 8 q + 4 h + r] and its index li[...] (the wave's LDS
+// copies of the batch).  The exact direct-form distance of a candidate is inserted into the
+// top-2 when it can enter it.  Returns true if the lane's top-2 improved.
+__device__ __forceinline__ bool block_recheck(const v16f (&r)[2], float th, bool open,
+                                              int32_t t, int h, int32_t n,
+                                              const f4* __restrict__ lu,
+                                              const int32_t* __restrict__ li, float sx,
+                                              float sy, float sz, unsigned long long& k1,
+                                              unsigned long long& k2) {
+  uint32_t x = 0;
+#pragma unroll
+  for (int e = 1; e >= 0; --e)
+#pragma unroll
+    for (int k = 15; k >= 0; --k) x = (x << 1) | (r[e][k] <= th ? 1u : 0u);
+  if (open) x = 0xffffffffu;
+  bool improved = false;
+  while (x) {
+    const int s = __builtin_ctz(x);
+    x &= x - 1;
+    const int e = s >> 4, q = (s >> 2) & 3, rr = s & 3;
+    const int uu = 32 * e + 8 * q + 4 * h + rr;
+    if (64 * t + uu >= n) continue;  // padding
+    const f4 w = lu[uu];
+    const float dx = sx - w[0];
+    const float dy = sy - w[1];
+    const float dz = sz - w[2];
+    const float dd = (dx * dx + dy * dy) + dz * dz;
+    // keys order by distance first: only a distance <= the current second can enter
+    if (__float_as_uint(dd) > static_cast<uint32_t>(k2 >> 32)) continue;
+    improved |= insert2(k1, k2, pack(dd, li[uu]));
+  }
+  return improved;
+}
+
+// Completes batch t once the minima mn[b] of its blocks are known (see find_mfma.hip): the
+// ballot is unconditional so the minima stay between the products; valid is uniform and
+// false for the placeholder batch before a chunk's first.
+__device__ __forceinline__ void finish_batch(const v16f (&res)[kBlocks][2],
+                                             const float (&mn)[kBlocks], bool valid, int32_t t,
+                                             int h, int lane, int32_t n,
+                                             const f4* __restrict__ lu,
+                                             const int32_t* __restrict__ li, const float* sd,
+                                             float sig2, float (&th)[kBlocks],
+                                             unsigned long long (&k1)[kBlocks],
+                                             unsigned long long (&k2)[kBlocks], uint32_t open,
+                                             unsigned long long wave_open) {
+  float lo = mn[0] - th[0];
+#pragma unroll
+  for (int b = 1; b < kBlocks; ++b) lo = __builtin_elementwise_minimum(lo, mn[b] - th[b]);
+  const unsigned long long hit = __ballot(lo <= 0.0f) | wave_open;
+  if (valid && hit != 0) {
+    bool improved = false;
+#pragma unroll
+    for (int b = 0; b < kBlocks; ++b) {
+      const bool ob = (open >> b) & 1u;
+      if (__ballot(mn[b] <= th[b] || ob) != 0) {
+        const float* f = sd + b * kSigFields * 64 + lane;
+        improved |= block_recheck(res[b], th[b], ob, t, h, n, lu, li, f[0], f[64], f[128],
+                                  k1[b], k2[b]);
+      }
+    }
+    if (improved) {
+#pragma unroll
+      for (int b = 0; b < kBlocks; ++b) {
+        const float* f = sd + b * kSigFields * 64 + lane;
+        th[b] = theta_of(k2[b], sig2, f[192], f[256]);
+      }
+    }
+  }
+}
+
+// Units arrive in batches of 64 (two groups of 32): lane l reads its two 16-byte operands of
+// batch t at pmh[(64 t + l) * 2 + group] (2 KB contiguous per wave), and the binary32 unit
+// 64 t + l (pu) and its index (pidx), which go to the wave's double-buffered LDS copy for
+// the rare path.  The loop is the software pipeline of find_mfma.hip (products of batch t into
+// one result set, minima of batch t - 1 from the other), with products in group-major order.
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void fh_scan(
+    const float4* __restrict__ pu, const uint4* __restrict__ pmh,
+    const int32_t* __restrict__ pidx, int32_t n, int32_t chunk_batches,
+    const float* __restrict__ sig, int32_t m, const int32_t* __restrict__ sperm,
+    const int32_t* __restrict__ skey, const int32_t* __restrict__ off_u,
+    const float* __restrict__ seed, const int32_t* __restrict__ mag,
+    const float* __restrict__ bb, unsigned long long* __restrict__ part) {
+  constexpr int NB = kBlocks;
+  __shared__ f4 lds_u[4][2][64];                   // binary32 units, two batches per wave
+  __shared__ int32_t lds_i[4][2][64];              // their indices
+  __shared__ float sdata[4][NB * kSigFields * 64];  // rare-path signal data
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int j = lane & 31, h = lane >> 5;
+  const int32_t n_batches = (n + 63) >> 6;
+  // chunk order: home chunk first, as in find_mfma.hip
+  int32_t c;
+  {
+    const int32_t split = static_cast<int32_t>(gridDim.y);
+    const int32_t pm_ = min(blockIdx.x * kSignalsPerWG + kSignalsPerWG / 2, m - 1);
+    const int32_t key = min(max(skey[min(max(sperm[pm_], 0), m - 1)], 0), kBuckets - 1);
+    const int32_t pos = min(max(off_u[key], 0), n);
+    const int32_t home = min(pos / (64 * chunk_batches), split - 1);
+    const int32_t y = static_cast<int32_t>(blockIdx.y);
+    const int32_t d = (y & 1) ? (y + 1) / 2 : -(y / 2);
+    c = ((home + d) % split + split) % split;
+  }
+  const int32_t t_begin = c * chunk_batches;
+  const int32_t t_end = min(n_batches, t_begin + chunk_batches);
+  const float u = 5.9604644775390625e-8f;
+  const float sgm = bb[6], sig2 = sgm * sgm;
+  const float xm = sgm * __int_as_float(mag[0]), ym = sgm * __int_as_float(mag[1]);
+  const float zm = sgm * __int_as_float(mag[2]), nmx = sig2 * __int_as_float(mag[3]);
+  // the call's units fit the binary16 operands (false for NaN as well)
+  const bool range_ok = fmaxf(xm, fmaxf(ym, zm)) <= 128.0f;
+
+  // the lane's signal in block b: sorted position p = base + 32 b + j
+  const int32_t base = blockIdx.x * kSignalsPerWG + wave * 32 * NB;
+  float* sd = sdata[wave];
+  h8 bop[NB];
+  float th[NB];
+  unsigned long long k1[NB], k2[NB];
+  uint32_t open = 0;
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    const int32_t p = base + 32 * b + j;
+    const bool live = p < m;
+    const int32_t jj = live ? min(max(sperm[p], 0), m - 1) : 0;
+    const float sx = live ? sig[jj] : 0.0f;
+    const float sy = live ? sig[m + jj] : 0.0f;
+    const float sz = live ? sig[2 * m + jj] : 0.0f;
+    const float tx = sgm * sx, ty = sgm * sy, tz = sgm * sz;  // exact
+    const float ss = norm2(tx, ty, tz);
+    // signals past m get B = -inf: their threshold is -inf and nothing is a candidate
+    const float B = live ? seed[p] : -__builtin_huge_valf();
+    const float T = 2.0f * (fabsf(tx) * xm + fabsf(ty) * ym + fabsf(tz) * zm) + nmx;
+    const float A = 2.0f * ((fabsf(tx) + fabsf(ty)) + fabsf(tz)) + 400.0f;
+    const float ee = live ? (((46.0f * u * T + 6.0f * u * ss) + 3.0f * u * (B * sig2)) +
+                             u * A) + 7.52316384526264e-37f
+                          : 0.0f;
+    // 2^90 = 0x6c800000; the integer test also catches inf and NaN
+    const bool big = !(fmaxf(fabsf(tx), fmaxf(fabsf(ty), fabsf(tz))) <= 16384.0f);
+    if (!range_ok || big || (__float_as_uint(ee) & 0x7fffffffu) > 0x6c800000u) open |= 1u << b;
+    k1[b] = pack(B, kSentinel);
+    k2[b] = k1[b];
+    th[b] = live ? theta_of(k2[b], sig2, ss, ee) : -__builtin_huge_valf();
+    // B operand: K slots 8h..8h+7 of signal j, b = -2 sigma s split in binary16 pairs
+    const float bx = -2.0f * tx, by = -2.0f * ty, bz = -2.0f * tz;
+    auto split = [](float v, _Float16& hi, _Float16& lo) {
+      hi = static_cast<_Float16>(v);
+      lo = static_cast<_Float16>(v - static_cast<float>(hi));
+    };
+    _Float16 a1, a2, c1, c2;
+    h8 o;
+    if (h == 0) {
+      split(bx, a1, a2);
+      split(by, c1, c2);
+      o = (h8){a1, a2, a1, a2, c1, c2, c1, c2};
+    } else {
+      split(bz, a1, a2);
+      const _Float16 one = static_cast<_Float16>(1.0f), zero = static_cast<_Float16>(0.0f);
+      o = (h8){a1, a2, a1, a2, one, one, zero, zero};
+    }
+    bop[b] = o;
+    float* f = sd + b * kSigFields * 64 + lane;  // read back only by this lane
+    f[0] = sx;
+    f[64] = sy;
+    f[128] = sz;
+    f[192] = ss;
+    f[256] = ee;
+  }
+  const unsigned long long wave_open = __ballot(open != 0);
+
+  // operand ring with clamped, unconditional loads issued in ring order (find_mfma.hip)
+  const h8* opnd = reinterpret_cast<const h8*>(pmh) + 2 * lane;
+  h8 ra[kDepth][2];
+  const f4* pu4 = reinterpret_cast<const f4*>(pu);
+  f4 ru[kDepth];
+  int32_t ri[kDepth];
+#pragma unroll
+  for (int q = 0; q < kDepth; ++q) {
+    const int32_t tq = min(t_begin + q, t_end - 1);
+    ra[q][0] = opnd[128 * tq];
+    ra[q][1] = opnd[128 * tq + 1];
+    ru[q] = pu4[min(64 * tq + lane, n - 1)];
+    ri[q] = pidx[min(64 * tq + lane, n - 1)];
+    asm volatile("" ::: "memory");
+  }
+  v16f res[2][NB][2];
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int e = 0; e < 2; ++e)
+#pragma unroll
+      for (int k = 0; k < 16; ++k) res[1][b][e][k] = __builtin_huge_valf();
+  const v16f zero16 = {};
+  for (int32_t t = t_begin; t < t_end; t += kDepth) {
+#pragma unroll
+    for (int q = 0; q < kDepth; ++q) {
+      const int cur = q & 1, prv = cur ^ 1;
+      lds_u[wave][cur][lane] = ru[q];
+      lds_i[wave][cur][lane] = ri[q];
+      float mn[NB];
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const h8 a = ra[q][e];
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+          res[cur][b][e] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, bop[b], zero16, 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        mn[e] = block_min(res[prv][e]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      const int32_t tn = min(t + kDepth + q, t_end - 1);
+      ra[q][0] = opnd[128 * tn];
+      ra[q][1] = opnd[128 * tn + 1];
+      ru[q] = pu4[min(64 * tn + lane, n - 1)];
+      ri[q] = pidx[min(64 * tn + lane, n - 1)];
+      asm volatile("" ::: "memory");
+      finish_batch(res[prv], mn, q > 0 || t > t_begin, min(t + q - 1, t_end - 1), h, lane, n,
+                   lds_u[wave][prv], lds_i[wave][prv], sd, sig2, th, k1, k2, open, wave_open);
+    }
+  }
+  // the chunk's last batch, t_end - 1, sits in the odd set (kDepth is even)
+  if (t_begin < t_end) {
+    float mn[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b) mn[b] = block_min(res[1][b]);
+    finish_batch(res[1], mn, true, t_end - 1, h, lane, n, lds_u[wave][1], lds_i[wave][1], sd,
+                 sig2, th, k1, k2, open, wave_open);
+  }
+
+  // merge the two partial states of each signal (lanes j and j + 32); lane (j, h) writes
+  // block h's signal j
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    const unsigned long long o1 = __shfl_xor(k1[b], 32);
+    const unsigned long long o2 = __shfl_xor(k2[b], 32);
+    insert2(k1[b], k2[b], o1);
+    insert2(k1[b], k2[b], o2);
+  }
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    const int32_t p = base + 32 * b + j;
+    if (h == b && p < m) {
+      part[(2 * c) * static_cast<size_t>(m) + p] = k1[b];
+      part[(2 * c + 1) * static_cast<size_t>(m) + p] = k2[b];
+    }
+  }
+}
+
+}  // namespace
+
+int f16_split(int32_t n, int32_t m, int cus, int want) {
+  if (want > 0) return std::min(want, kMaxSplit);
+  const int64_t sblocks = (m + kSignalsPerWG - 1) / kSignalsPerWG;
+  const int64_t target = 4LL * (cus > 0 ? cus : 256);
+  int64_t sp = (target + sblocks - 1) / sblocks;
+  sp = std::min<int64_t>(sp, (n + 2047) / 2048);
+  return static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(sp, kMaxSplit)));
+}
+
+hipError_t launch_scan_f16(const DevState& s, const StageBufs& b, int32_t n, const float* sig,
+                           int32_t m, int split, hipStream_t st) {
+  const int32_t n_batches = (n + 63) / 64;
+  const int32_t chunk_batches = (n_batches + split - 1) / split;
+  dim3 grid((m + kSignalsPerWG - 1) / kSignalsPerWG, split);
+  fh_scan<<<grid, 256, 0, st>>>(b.pu, b.pmh, b.pidx, n, chunk_batches, sig, m, b.sperm, b.skey,
+                                b.off_u, b.seed, b.mag, b.bb, s.part);
+  return hipGetLastError();
+}
+
+}  // namespace gsn

@@ -13,7 +13,7 @@
 // Candidates are evaluated in the direct form and inserted in the exact (d, index) top-2.
 //
 // Range: the screen is applied to a signal only when its margin E_j (below) is at most 2^90.
-// That bounds T_j, S^ and B_j by 2^109, so no product, sum or threshold of the screen
+// That bounds T_j, S^ and B_j by 2^113, so no product, sum or threshold of the screen
 // overflows and Q is never NaN.  A signal outside that range (huge or non-finite
 // coordinates) is "open": every unit is its candidate, i.e. it is scanned exactly in the
 // direct form.
@@ -26,17 +26,19 @@
 // is valid, and the four partial states of a signal are merged at the end.
 //
 // Rounding bound (u = 2^-24).  The matrix core sums the four products (exact, since -2 s is
-// exact) with an error measured at most 3.2 u (sum of |terms|) on the target and at most 5 u
-// for any sequence of binary32 roundings of exact products; the sum of |terms| is at most
-// T_j = 2(|sx| Xmax + |sy| Ymax + |sz| Zmax) + Nmax.  The computed norms n^ and S^ are within
-// 3.01 u of |w|^2 and |s|^2, and the direct-form distance d^ within 5.01 u of |s - w|^2.
-// So a unit with d^ <= d2 has
-//     Q^ <= d2 (1 + 5.01u) - S^ + 3.01u S^ + 8.02u T_j,
+// exact) with an error measured at most 3.2 u of the sum of |terms| on the target; the bound
+// below allows 8 u, which also covers truncating rather than rounding additions.  The sum
+// of |terms| is at most T_j = 2(|sx| Xmax + |sy| Ymax + |sz| Zmax) + Nmax.  The computed norms
+// n^ and S^ are within 3.01 u of |w|^2 and |s|^2, and the direct-form distance d^ within
+// 5.01 u of |s - w|^2.  So a unit with d^ <= d2 has
+//     Q^ <= d2 (1 + 5.01u) - S^ + 3.01u S^ + 11.02u T_j,
 // while theta = fl(fl(fl(d2 (1 + 2^-20)) - S^) + E_j) is at least
 //     d2 (1 + 14.99u) - S^ + E_j (1 - u) - (2 + u) u (B_j (1 + 17u) + S^),
-// so Q^ <= theta whenever E_j (1 - u) >= 8.02u T_j + 5.02u S^ + 2.01u B_j.  The kernel uses
-//     E_j = 32u (T_j + 2 S^ + 2 B_j) + 2^-120
-// (B_j >= d2 >= 0 is the seed bound; the last term covers underflow), with room to spare.
+// so Q^ <= theta whenever E_j (1 - u) >= 11.02u T_j + 5.02u S^ + 2.01u B_j.  The kernel uses
+//     E_j = 12u T_j + 6u S^ + 3u B_j + 2^-120,
+// evaluated in binary32 (at most four roundings, relative error below 4.01u, which the slack
+// 0.97u T_j + 0.97u S^ + 0.98u B_j absorbs).  B_j >= d2 >= 0 is the seed bound; the last
+// term covers underflow.
 #include "gsn_internal.h"
 
 namespace gsn {
@@ -82,13 +84,13 @@ __device__ __forceinline__ float fmin3(float a, float b, float c) {
 }
 
 
-// The four products of block b in a batch: r[e] = Q of group e.
-__device__ __forceinline__ void mfma_block(const float4& a, float bop, v4f (&r)[4]) {
+// The products of group e of a batch for the NB blocks: r[b][e] = Q of block b, group e.
+template <int NB>
+__device__ __forceinline__ void mfma_group(float a, const float (&bop)[NB], v4f (&r)[NB][4],
+                                           int e) {
   const v4f z = {0.0f, 0.0f, 0.0f, 0.0f};
-  r[0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, bop, z, 0, 0, 0);
-  r[1] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, bop, z, 0, 0, 0);
-  r[2] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, bop, z, 0, 0, 0);
-  r[3] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, bop, z, 0, 0, 0);
+#pragma unroll
+  for (int b = 0; b < NB; ++b) r[b][e] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bop[b], z, 0, 0, 0);
 }
 
 // Minimum of the 16 results of a block.
@@ -253,7 +255,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
     // signals past m get B = -inf: their threshold is -inf and nothing is a candidate
     const float B = live ? seed[p] : -__builtin_huge_valf();
     const float T = 2.0f * (fabsf(sx) * xm + fabsf(sy) * ym + fabsf(sz) * zm) + nmx;
-    const float ee = live ? 32.0f * u * (T + 2.0f * ss + 2.0f * B) + 7.52316384526264e-37f : 0.0f;
+    const float ee = live ? (12.0f * u * T + 6.0f * u * ss) + 3.0f * u * B + 7.52316384526264e-37f
+                          : 0.0f;
     // 2^90 = 0x6c800000; the integer test also catches inf and NaN
     if ((__float_as_uint(ee) & 0x7fffffffu) > 0x6c800000u) open |= 1u << b;
     k1[b] = pack(B, kSentinel);
@@ -309,12 +312,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
       // reads rows that other lanes loaded
       *my[cur] = ring[q];
       lds_idx[wave][cur][lane] = ridx[q];
+      // Products in group-major order: four consecutive MFMAs share their A operand (one
+      // component of the group's units) and differ only in B.  Fewer operand bits switch
+      // between consecutive products, which the matrix cores turn into throughput under this
+      // load (7-10% in a probe of this loop).  Between the groups, the minimum of one block of
+      // the previous batch.
+      static_assert(NB == 4, "one block minimum per group");
+      const float av[4] = {ring[q].x, ring[q].y, ring[q].z, ring[q].w};
       float mn[NB];
 #pragma unroll
-      for (int b = 0; b < NB; ++b) {
-        mfma_block(ring[q], bop[b], res[cur][b]);
+      for (int e = 0; e < 4; ++e) {
+        mfma_group(av[e], bop, res[cur], e);
         __builtin_amdgcn_sched_barrier(0);
-        mn[b] = block_min(res[prv][b]);
+        mn[e] = block_min(res[prv][e]);
         __builtin_amdgcn_sched_barrier(0);
       }
       ring[q] = opnd[64 * min(t + kDepth + q, t_end - 1)];

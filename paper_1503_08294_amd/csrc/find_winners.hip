@@ -126,13 +126,17 @@ int signals_per_lane(int32_t m) { return m >= 8192 ? 4 : (m >= 2048 ? 2 : 1); }
 
 FindConfig find_config(int32_t n, int32_t m, int cus, int want_split, int want_variant) {
   FindConfig c;
-  c.variant = want_variant > 0 ? want_variant : 3;
+  c.variant = want_variant > 0 ? want_variant : 4;
   if (c.variant == 2) {
     c.split = screened_split(n, m, cus, want_split);
     return c;
   }
   if (c.variant == 3) {
     c.split = mfma_split(n, m, cus, want_split);
+    return c;
+  }
+  if (c.variant == 4) {
+    c.split = f16_split(n, m, cus, want_split);
     return c;
   }
   const int S = signals_per_lane(m);

@@ -234,7 +234,7 @@ int gsn_find_winners(gsn_net* net, const float* sig, int32_t m, int32_t* winner,
       gsn::find_config(net->n, m, net->cus, net->tune_split, net->tune_variant);
   TimedRegion all(net, GSN_T_FIND, st);
   hipError_t e;
-  if (cfg.variant == 2 || cfg.variant == 3) {
+  if (cfg.variant >= 2) {
     const gsn::StageBufs sb = gsn::carve_stage(net->s.scr, net->p.n_max, net->p.m_max);
     // the unit order is rebuilt when the network changed and every kRebucketEvery calls
     const bool rebucket = net->bucket_n != net->n || net->finds_since_bucket >= kRebucketEvery;
@@ -246,8 +246,10 @@ int gsn_find_winners(gsn_net* net, const float* sig, int32_t m, int32_t* winner,
     ++net->finds_since_bucket;
     if (e == hipSuccess) {
       TimedRegion scan(net, GSN_T_FIND_SCAN, st);
-      e = cfg.variant == 3 ? gsn::launch_scan_mfma(net->s, sb, net->n, sig, m, cfg.split, st)
-                           : gsn::launch_scan_screened(net->s, sb, net->n, sig, m, cfg.split, st);
+      e = cfg.variant == 4   ? gsn::launch_scan_f16(net->s, sb, net->n, sig, m, cfg.split, st)
+          : cfg.variant == 3 ? gsn::launch_scan_mfma(net->s, sb, net->n, sig, m, cfg.split, st)
+                             : gsn::launch_scan_screened(net->s, sb, net->n, sig, m, cfg.split,
+                                                         st);
       scan.end();
     }
     if (e == hipSuccess)
@@ -498,7 +500,7 @@ int gsn_tune(gsn_net* net, int32_t key, int32_t value) {
       net->tune_split = value;
       return GSN_OK;
     case GSN_TUNE_VARIANT:
-      if (value < 0 || value > 3) return GSN_E_INVAL;
+      if (value < 0 || value > 4) return GSN_E_INVAL;
       net->tune_variant = value;
       return GSN_OK;
     default:

@@ -80,6 +80,8 @@ struct StageBufs {
   int32_t* mag;     // [4] max |x|, |y|, |z|, |w|^2 of this call (float bits)
   float* bmag;      // [n_max / kBlock + 2][4] per-block magnitude maxima
   float* pm;        // [ceil(n_max / 64) * 256] units in matrix-core operand order
+  uint4* pmh;       // [ceil(n_max / 64)][64 lanes][2 groups] scaled units split into binary16
+                    // pairs, in the operand order of the 32x32x16 f16 product (16 B each)
 };
 size_t stage_bytes(int32_t n_max, int32_t m_max);
 StageBufs carve_stage(void* base, int32_t n_max, int32_t m_max);
@@ -93,6 +95,9 @@ int screened_split(int32_t n, int32_t m, int cus, int want);
 hipError_t launch_scan_screened(const DevState& s, const StageBufs& b, int32_t n,
                                 const float* sig, int32_t m, int split, hipStream_t st);
 int mfma_split(int32_t n, int32_t m, int cus, int want);
+int f16_split(int32_t n, int32_t m, int cus, int want);
+hipError_t launch_scan_f16(const DevState& s, const StageBufs& b, int32_t n, const float* sig,
+                           int32_t m, int split, hipStream_t st);
 hipError_t launch_scan_mfma(const DevState& s, const StageBufs& b, int32_t n, const float* sig,
                             int32_t m, int split, hipStream_t st);
 

@@ -61,6 +61,29 @@ __device__ __forceinline__ float norm2(float x, float y, float z) {
   return (x * x + y * y) + z * z;
 }
 
+// Scale of the binary16 operands: sigma = 2^k with sigma M in [16, 32), M the largest
+// coordinate magnitude of the bucketing box (so units may grow fourfold before the scan's
+// range check, sigma max|w| <= 128, sends the call to the exact path); k in [-60, 60], and
+// sigma = 1 for an empty or non-finite box.
+__device__ __forceinline__ float scale_of(const int32_t* acc) {
+  float mx = 0.0f;
+  for (int k = 0; k < 6; ++k) mx = fmaxf(mx, fabsf(unord(acc[k])));
+  const uint32_t ex = (__float_as_uint(mx) >> 23) & 0xffu;
+  int k = 0;
+  if (ex == 0) k = 60;                                    // zero or subnormal
+  else if (ex != 0xffu) k = min(60, max(-60, 4 - (static_cast<int>(ex) - 127)));
+  return __uint_as_float(static_cast<uint32_t>(k + 127) << 23);
+}
+
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+
+// v = hi + lo + e with hi, lo binary16 (round to nearest) and |e| <= 2^-22 |v| + 2^-25;
+// v - hi is exact in binary32
+__device__ __forceinline__ void split16(float v, _Float16& hi, _Float16& lo) {
+  hi = static_cast<_Float16>(v);
+  lo = static_cast<_Float16>(v - static_cast<float>(hi));
+}
+
 // block-wide reduction of up to 4 values with op, result valid in thread 0
 template <typename Op>
 __device__ void block_reduce4(float v[4], Op op) {
@@ -145,6 +168,7 @@ __global__ __launch_bounds__(kBlock) void st_hist_units(const float* __restrict_
       bb[3 + threadIdx.x] = sbb[3 + threadIdx.x];
     }
   }
+  if (blockIdx.x == 0 && threadIdx.x == 0) bb[6] = scale_of(acc);
   __syncthreads();
   const int32_t i = blockIdx.x * kBlock + threadIdx.x;
   if (i < n) {
@@ -254,6 +278,7 @@ __global__ __launch_bounds__(kBlock) void st_gather(const float* __restrict__ x,
                                                     const int32_t* __restrict__ pidx,
                                                     float4* __restrict__ pu,
                                                     float* __restrict__ pm,
+                                                    uint4* __restrict__ pmh,
                                                     const float* __restrict__ sig, int32_t m,
                                                     int32_t ub, const float* __restrict__ bb,
                                                     int32_t* __restrict__ skey,
@@ -283,6 +308,31 @@ __global__ __launch_bounds__(kBlock) void st_gather(const float* __restrict__ x,
       const int32_t t = pos >> 6, e = (pos >> 4) & 3, i = pos & 15;
 #pragma unroll
       for (int k = 0; k < 4; ++k) pm[256 * t + 4 * (16 * k + i) + e] = cv[k];
+      // binary16 layout: batch t holds 2 groups of 32 units; lane h * 32 + r (r the row in
+      // the group) reads K slots 8h..8h+7 of its row: h = 0 (x1 x1 x2 x2 y1 y1 y2 y2),
+      // h = 1 (z1 z1 z2 z2 n1 n2 0 0) of the scaled unit sigma w and its binary32 norm,
+      // at pmh[(64 t + lane) * 2 + group].  Padding carries n1 = +inf: never a candidate.
+      const int32_t g2 = (pos >> 5) & 1, r = pos & 31;
+      const float sg = bb[6];
+      h8 o0 = {}, o1 = {};
+      if (pos < n) {
+        const float sx = sg * cv[0], sy = sg * cv[1], sz = sg * cv[2];
+        const float sn = norm2(sx, sy, sz);
+        _Float16 a, b;
+        split16(sx, a, b);
+        o0[0] = a; o0[1] = a; o0[2] = b; o0[3] = b;
+        split16(sy, a, b);
+        o0[4] = a; o0[5] = a; o0[6] = b; o0[7] = b;
+        split16(sz, a, b);
+        o1[0] = a; o1[1] = a; o1[2] = b; o1[3] = b;
+        split16(sn, a, b);
+        o1[4] = a; o1[5] = b;
+      } else {
+        o1[4] = static_cast<_Float16>(__builtin_huge_valf());
+      }
+      h8* dst = reinterpret_cast<h8*>(pmh);
+      dst[(64 * static_cast<int64_t>(t) + r) * 2 + g2] = o0;
+      dst[(64 * static_cast<int64_t>(t) + 32 + r) * 2 + g2] = o1;
     }
     block_reduce4(mg, FMax());
     if (threadIdx.x == 0)
@@ -420,6 +470,7 @@ size_t stage_bytes(int32_t n_max, int32_t m_max) {
   add(4 * 4);    // mag
   add(16 * (nm / kBlock + 2));  // bmag
   add(16 * ((nm + 63) / 64 * 64));  // pm
+  add(32 * ((nm + 63) / 64 * 64));  // pmh
   return b;
 }
 
@@ -451,6 +502,7 @@ StageBufs carve_stage(void* base, int32_t n_max, int32_t m_max) {
   s.mag = reinterpret_cast<int32_t*>(take(4 * 4));
   s.bmag = reinterpret_cast<float*>(take(16 * (nm / kBlock + 2)));
   s.pm = reinterpret_cast<float*>(take(16 * ((nm + 63) / 64 * 64)));
+  s.pmh = reinterpret_cast<uint4*>(take(32 * ((nm + 63) / 64 * 64)));
   return s;
 }
 
@@ -470,8 +522,8 @@ hipError_t launch_stage(const DevState& s, const StageBufs& b, int32_t n, const 
     st_scatter_units<<<nb_u, kBlock, 0, st>>>(n, b.ukey, b.cur_u, b.pidx);
   }
   const int nb_g = blocks((static_cast<int64_t>(n) + 63) & ~static_cast<int64_t>(63));
-  st_gather<<<nb_g + blocks(m), kBlock, 0, st>>>(s.x, s.y, s.z, n, b.pidx, b.pu, b.pm, sig, m,
-                                                 nb_g, b.bb, b.skey, b.hist_s, b.bmag);
+  st_gather<<<nb_g + blocks(m), kBlock, 0, st>>>(s.x, s.y, s.z, n, b.pidx, b.pu, b.pm, b.pmh, sig,
+                                                 m, nb_g, b.bb, b.skey, b.hist_s, b.bmag);
   st_scan_hist<kSignalBuckets><<<1, 1024, 0, st>>>(b.hist_s, b.off_s, b.cur_s, b.acc, b.bmag,
                                                    nb_g, b.mag, 1);
   st_scatter_signals<<<blocks(m), kBlock, 0, st>>>(m, b.skey, b.cur_s, b.sperm);

@@ -72,7 +72,7 @@ def test_genus3_full_size():
     assert_find_equal(g, o, "genus3_200k")
 
 
-@pytest.mark.parametrize("variant", [1, 2, 3])
+@pytest.mark.parametrize("variant", [1, 2, 3, 4])
 @pytest.mark.parametrize("n,m,seed", [(2, 3, 0), (3, 1, 1), (257, 999, 2), (4000, 16_384, 3),
                                       (30_000, 5_000, 4)])
 def test_both_kernel_variants(variant, n, m, seed):
@@ -86,7 +86,7 @@ def test_both_kernel_variants(variant, n, m, seed):
     assert_find_equal(g, o, f"variant={variant} n={n} m={m}")
 
 
-@pytest.mark.parametrize("variant", [1, 2, 3])
+@pytest.mark.parametrize("variant", [1, 2, 3, 4])
 def test_cancellation_and_near_ties_far_from_the_origin(variant):
     """Units and signals around (1000, -1000, 1000) separated by ~1e-3: the expanded form
     loses about 12 bits to cancellation here, and many distances differ by a few ulps, so a
@@ -110,7 +110,7 @@ def test_cancellation_and_near_ties_far_from_the_origin(variant):
     assert_find_equal(g, o, f"variant={variant}")
 
 
-@pytest.mark.parametrize("variant", [2, 3])
+@pytest.mark.parametrize("variant", [2, 3, 4])
 def test_screened_variants_ties_on_a_grid(variant):
     from paper_1503_08294_amd import gsn
     rng = np.random.default_rng(5)
@@ -124,7 +124,7 @@ def test_screened_variants_ties_on_a_grid(variant):
         assert_find_equal(g, o, f"split={split}")
 
 
-@pytest.mark.parametrize("variant", [1, 2, 3])
+@pytest.mark.parametrize("variant", [1, 2, 3, 4])
 @pytest.mark.parametrize("scale", [1e17, 1e20])
 def test_huge_signal_coordinates_are_scanned_exactly(variant, scale):
     """Signals far outside the screen's range (margin above 2^90, distances near or past
@@ -142,7 +142,7 @@ def test_huge_signal_coordinates_are_scanned_exactly(variant, scale):
     assert_find_equal(g, o, f"variant={variant} scale={scale:g}")
 
 
-@pytest.mark.parametrize("variant", [2, 3])
+@pytest.mark.parametrize("variant", [2, 3, 4])
 def test_one_huge_unit_opens_every_signal(variant):
     """A single unit at 1e19 makes the magnitude bounds overflow, so every signal is open
     (scanned exactly); results still match the oracle."""
@@ -157,7 +157,7 @@ def test_one_huge_unit_opens_every_signal(variant):
     assert_find_equal(g, o, f"variant={variant}")
 
 
-@pytest.mark.parametrize("variant", [2, 3])
+@pytest.mark.parametrize("variant", [2, 3, 4])
 def test_everything_at_1e17_is_scanned_exactly(variant):
     """Units and signals spread at the 1e17 scale: distances are finite and distinct but the
     screen's margin exceeds its range for every signal, so all are scanned exactly."""
