@@ -9,12 +9,13 @@ Prints one JSON line:
   value            whole-iteration signal-unit distance evaluations per second (m*N/step)
   signals_per_s    m per step time
   fw_evals_per_s   m*N per find-winners call (HIP events around the call)
-  roofline         the find-winners scan kernel (fm_scan, the screened scan on the matrix
-                   cores): algorithmic fp32 FLOP/s (8 per evaluation, which is also what
-                   its K = 4 products execute) from HIP events around each launch on the
-                   library's stream, against the fp32 peak (157.3 TFLOP/s, vector and
-                   matrix alike); HBM traffic per launch from rocprofv3 counters when a
-                   summary for the current kernel source exists
+  roofline         the find-winners scan kernel (fh_scan, the screened scan on the matrix
+                   cores in split binary16): algorithmic FLOP/s (8 per evaluation) from HIP
+                   events around each launch on the library's stream, against the peak of
+                   the contraction's type (binary16 dense, 2.5 PFLOP/s); also the matrix
+                   cores' executed rate (32 flops per pair: 32x32x16 products, K = 16) and
+                   the algorithmic rate against the fp32 peak; HBM traffic per launch from
+                   rocprofv3 counters when a summary for the current kernel source exists
   cpu_baseline     the CPU oracle timed on this host's cores on the first iterations of the
                    same workload
 """
@@ -33,11 +34,13 @@ if ROOT not in sys.path:
 
 METRIC = "signal-unit distance evals/s and signals/s at 1 GPU; % fp32 VALU peak"
 FP32_PEAK_TFLOPS = 157.3     # 256 CUs x 2.4 GHz x 256 fp32 flop/clk; also the fp32 MFMA peak
+F16_PEAK_TFLOPS = 2500.0     # dense binary16 matrix-core peak
+EXECUTED_FLOPS_PER_PAIR = 32  # one 32x32x16 product (32768 flops) per 1,024 pairs
 FLOPS_PER_EVAL = 8           # 3 sub + 3 mul + 2 add of one squared distance
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "find_winners_genus3_200k_traffic.json")
-SCAN_KERNEL = "fm_scan"
+SCAN_KERNEL = "fh_scan"
 SCAN_SOURCES = [os.path.join(ROOT, "paper_1503_08294_amd", "csrc", f)
-                for f in ("find_mfma.hip", "gsn_internal.h")]
+                for f in ("find_f16.hip", "gsn_internal.h")]
 
 
 def scan_source_hash() -> str:
@@ -209,11 +212,15 @@ def main():
         "phase_ms": phase,
         "conflict_rate": conflict_rate,
         "state_after": {"units": n_units, "edges": n_edges},
-        "roofline": {"bound": "mfma", "kernel": SCAN_KERNEL, "achieved": achieved,
-                     "peak": FP32_PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / FP32_PEAK_TFLOPS, "traffic": traffic,
+        "roofline": {"bound": "mfma", "kernel": SCAN_KERNEL, "dtype": "f16",
+                     "achieved": achieved, "peak": F16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": achieved / F16_PEAK_TFLOPS, "traffic": traffic,
                      "flops_per_launch": FLOPS_PER_EVAL * m * n,
-                     "avg_launch_ms": phase["find_scan"]},
+                     "avg_launch_ms": phase["find_scan"],
+                     "executed_mfma_tflops": EXECUTED_FLOPS_PER_PAIR * m * n / scan_s / 1e12,
+                     "executed_mfma_frac": EXECUTED_FLOPS_PER_PAIR * m * n / scan_s / 1e12
+                                           / F16_PEAK_TFLOPS,
+                     "achieved_vs_fp32_peak": achieved / FP32_PEAK_TFLOPS},
         "cpu_baseline": None,
     }
     if args.cpu_budget > 0:
