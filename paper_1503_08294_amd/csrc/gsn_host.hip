@@ -87,6 +87,7 @@ struct gsn_net {
   int cus;          // compute units of the device
   int tune_split;
   int tune_variant;
+  int stage_parity;  // which set of signal histogram and cursors the next call uses
   bool timing;
   int32_t bucket_n;            // unit count at the last spatial bucketing (-1: none yet)
   int32_t finds_since_bucket;
@@ -190,6 +191,7 @@ int gsn_create(const gsn_params* params, void* workspace, size_t workspace_bytes
   net->phase = kReady;
   net->tune_split = 0;
   net->tune_variant = 0;
+  net->stage_parity = 0;
   net->timing = false;
   net->bucket_n = -1;
   net->finds_since_bucket = 0;
@@ -238,7 +240,8 @@ int gsn_find_winners(gsn_net* net, const float* sig, int32_t m, int32_t* winner,
     const gsn::StageBufs sb = gsn::carve_stage(net->s.scr, net->p.n_max, net->p.m_max);
     // the unit order is rebuilt when the network changed and every kRebucketEvery calls
     const bool rebucket = net->bucket_n != net->n || net->finds_since_bucket >= kRebucketEvery;
-    e = gsn::launch_stage(net->s, sb, net->n, sig, m, rebucket, st);
+    e = gsn::launch_stage(net->s, sb, net->n, sig, m, rebucket, net->stage_parity, st);
+    net->stage_parity ^= 1;
     if (rebucket) {
       net->bucket_n = net->n;
       net->finds_since_bucket = 0;

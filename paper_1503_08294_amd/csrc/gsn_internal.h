@@ -74,7 +74,8 @@ struct StageBufs {
   int32_t* skey;    // [m_max] bucket of every signal
   int32_t* sperm;   // [m_max] original index of the signal at every sorted position
   float* seed;      // [m_max] seed bound B at every sorted position
-  int32_t *hist_u, *off_u, *cur_u, *hist_s, *off_s, *cur_s;  // [kBuckets + 1] each
+  int32_t *hist_u, *off_u, *cur_u, *hist_s, *off_s, *cur_s;  // [kBuckets + 1] each; the
+                    // signal histogram and cursors use two sets of kBuckets / 8 in hist_s, cur_s
   int32_t* acc;     // [16] bounding-box accumulators
   float* bb;        // [8] grid of the last unit bucketing: lo.xyz, cells per length.xyz
   int32_t* mag;     // [4] max |x|, |y|, |z|, |w|^2 of this call (float bits)
@@ -86,8 +87,9 @@ struct StageBufs {
 size_t stage_bytes(int32_t n_max, int32_t m_max);
 StageBufs carve_stage(void* base, int32_t n_max, int32_t m_max);
 hipError_t launch_stage_init(const StageBufs& b, hipStream_t st);
+// parity alternates between calls (two sets of signal histogram and cursors)
 hipError_t launch_stage(const DevState& s, const StageBufs& b, int32_t n, const float* sig,
-                        int32_t m, bool rebucket, hipStream_t st);
+                        int32_t m, bool rebucket, int parity, hipStream_t st);
 hipError_t launch_stage_merge(const DevState& s, const StageBufs& b, int32_t m, int split,
                               int32_t* winner, int32_t* second, float* d1, float* d2,
                               hipStream_t st);

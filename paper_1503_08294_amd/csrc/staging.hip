@@ -283,6 +283,8 @@ __global__ __launch_bounds__(kBlock) void st_gather(const float* __restrict__ x,
                                                     int32_t ub, const float* __restrict__ bb,
                                                     int32_t* __restrict__ skey,
                                                     int32_t* __restrict__ hist_s,
+                                                    int32_t* __restrict__ clear_a,
+                                                    int32_t* __restrict__ clear_b,
                                                     float* __restrict__ bmag) {
   if (static_cast<int32_t>(blockIdx.x) < ub) {
     const int32_t pos = blockIdx.x * kBlock + threadIdx.x;
@@ -345,18 +347,16 @@ __global__ __launch_bounds__(kBlock) void st_gather(const float* __restrict__ x,
       skey[j] = k;
       atomicAdd(&hist_s[k >> kSignalShift], 1);
     }
+    // the first signal workgroup zeroes the other parity's histogram and cursors, which
+    // the next call uses
+    if (static_cast<int32_t>(blockIdx.x) == ub)
+      for (int32_t i = threadIdx.x; i < kSignalBuckets; i += kBlock) {
+        clear_a[i] = 0;
+        clear_b[i] = 0;
+      }
   }
 }
 
-__global__ __launch_bounds__(kBlock) void st_scatter_signals(int32_t m,
-                                                             const int32_t* __restrict__ skey,
-                                                             int32_t* __restrict__ cur_s,
-                                                             int32_t* __restrict__ sperm) {
-  const int32_t j = blockIdx.x * kBlock + threadIdx.x;
-  if (j >= m) return;
-  const int32_t pos = atomicAdd(&cur_s[skey[j] >> kSignalShift], 1);
-  if (pos >= 0 && pos < m) sperm[pos] = j;  // always true when counts match keys
-}
 
 __device__ __forceinline__ unsigned long long pack(float d, int32_t i) {
   return (static_cast<unsigned long long>(__float_as_uint(d)) << 32) |
@@ -371,20 +371,82 @@ __device__ __forceinline__ void merge2(unsigned long long& a1, unsigned long lon
   a1 = lo;
 }
 
-// kSeedLanes lanes per signal each scan a strided part of the window and merge.
-__global__ __launch_bounds__(kBlock) void st_seed(const float4* __restrict__ pu,
-                                                  const int32_t* __restrict__ pidx, int32_t n,
-                                                  const float* __restrict__ sig, int32_t m,
-                                                  const int32_t* __restrict__ sperm,
-                                                  const int32_t* __restrict__ skey,
-                                                  const int32_t* __restrict__ off_u,
-                                                  float* __restrict__ seed) {
-  const int32_t t = blockIdx.x * kBlock + threadIdx.x;
-  const int32_t p = t / kSeedLanes;
+// Places the signals in bucket order and computes their seed bounds, in one launch.  Every
+// workgroup scans the signal histogram (kSignalBuckets bins, zeroed by the previous call) in
+// LDS itself, so the bins' offsets need no launch of their own; a signal's sorted position is
+// its bin's offset plus a ticket from the bin's cursor (atomics; the order inside a bin is
+// immaterial).  Workgroup 0 also reduces the per-block unit magnitudes of this call.
+// kSeedLanes lanes per signal then scan a strided part of the kSeedWindow units around the
+// signal's unit bucket in the sorted order; the second smallest direct-form distance over
+// these distinct units is the seed bound B >= the signal's true second-best distance.
+__global__ __launch_bounds__(kBlock) void st_place_seed(
+    const int32_t* __restrict__ hist_s, int32_t* __restrict__ cur_s,
+    const int32_t* __restrict__ skey, const float* __restrict__ sig, int32_t m,
+    const float4* __restrict__ pu, const int32_t* __restrict__ pidx, int32_t n,
+    const int32_t* __restrict__ off_u, int32_t* __restrict__ sperm, float* __restrict__ seed,
+    const float* __restrict__ bmag, int32_t nmag, int32_t* __restrict__ mag) {
+  static_assert(kBlock == 256 && kSignalBuckets % kBlock == 0, "four waves, whole bins");
+  constexpr int per = kSignalBuckets / kBlock;
+  __shared__ int32_t soff[kSignalBuckets];
+  __shared__ int32_t wsum[kBlock / 64];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  {
+    int32_t v[per], sum = 0;
+#pragma unroll
+    for (int i = 0; i < per; ++i) {
+      v[i] = hist_s[tid * per + i];
+      sum += v[i];
+    }
+    int32_t inc = sum;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int32_t a = __shfl_up(inc, o);
+      if (lane >= o) inc += a;
+    }
+    if (lane == 63) wsum[w] = inc;
+    __syncthreads();
+    int32_t run = inc - sum;
+    for (int k = 0; k < w; ++k) run += wsum[k];
+#pragma unroll
+    for (int i = 0; i < per; ++i) {
+      soff[tid * per + i] = run;
+      run += v[i];
+    }
+  }
+  if (blockIdx.x == 0) {
+    float mg[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    for (int32_t b = tid; b < nmag; b += kBlock)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) mg[k] = fmaxf(mg[k], bmag[4 * b + k]);
+    __shared__ float red[kBlock / 64][4];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) mg[k] = fmaxf(mg[k], __shfl_xor(mg[k], o));
+    if (lane == 0)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) red[w][k] = mg[k];
+    __syncthreads();
+    if (tid < 4) {
+      float r = 0.0f;
+      for (int q = 0; q < kBlock / 64; ++q) r = fmaxf(r, red[q][tid]);
+      mag[tid] = __float_as_int(r);
+    }
+  }
+  __syncthreads();
+
+  const int32_t t = blockIdx.x * kBlock + tid;
+  const int32_t j = t / kSeedLanes;
   const int q = t % kSeedLanes;
+  int32_t pos = -1;
+  if (j < m && q == 0) {
+    const int32_t bin = skey[j] >> kSignalShift;
+    pos = soff[bin] + atomicAdd(&cur_s[bin], 1);
+    if (pos >= 0 && pos < m) sperm[pos] = j;  // always true when counts match keys
+  }
+  pos = __shfl(pos, lane & ~(kSeedLanes - 1));  // the signal's lanes are consecutive
   unsigned long long k1 = ~0ull, k2 = ~0ull;
-  if (p < m) {
-    const int32_t j = min(max(sperm[p], 0), m - 1);
+  if (j < m) {
     const float sx = sig[j], sy = sig[m + j], sz = sig[2 * m + j];
     const int32_t k = skey[j];
     const int32_t b0 = off_u[k], b1 = off_u[k + 1];
@@ -392,8 +454,8 @@ __global__ __launch_bounds__(kBlock) void st_seed(const float4* __restrict__ pu,
     lo = max(0, min(lo, n - kSeedWindow));
     const int32_t hi = min(n, lo + kSeedWindow);
     for (int32_t r = lo + q; r < hi; r += kSeedLanes) {
-      const float4 w = pu[r];
-      const float dx = sx - w.x, dy = sy - w.y, dz = sz - w.z;
+      const float4 wu = pu[r];
+      const float dx = sx - wu.x, dy = sy - wu.y, dz = sz - wu.z;
       const unsigned long long key = pack((dx * dx + dy * dy) + dz * dz, pidx[r]);
       merge2(k1, k2, key, ~0ull);
     }
@@ -404,9 +466,9 @@ __global__ __launch_bounds__(kBlock) void st_seed(const float4* __restrict__ pu,
     const unsigned long long o2 = __shfl_xor(k2, off);
     merge2(k1, k2, o1, o2);
   }
-  if (p < m && q == 0)
-    seed[p] = k2 != ~0ull ? __uint_as_float(static_cast<uint32_t>(k2 >> 32))
-                          : __builtin_huge_valf();
+  if (j < m && q == 0 && pos >= 0 && pos < m)
+    seed[pos] = k2 != ~0ull ? __uint_as_float(static_cast<uint32_t>(k2 >> 32))
+                            : __builtin_huge_valf();
 }
 
 // 32 signals per workgroup, 8 groups of lanes split the partial rows, merged in LDS.
@@ -512,7 +574,7 @@ hipError_t launch_stage_init(const StageBufs& b, hipStream_t st) {
 }
 
 hipError_t launch_stage(const DevState& s, const StageBufs& b, int32_t n, const float* sig,
-                        int32_t m, bool rebucket, hipStream_t st) {
+                        int32_t m, bool rebucket, int parity, hipStream_t st) {
   const int nb_u = blocks(n);
   if (rebucket) {
     st_bbox<<<std::min(nb_u, 64), kBlock, 0, st>>>(s.x, s.y, s.z, n, b.acc);
@@ -522,13 +584,18 @@ hipError_t launch_stage(const DevState& s, const StageBufs& b, int32_t n, const 
     st_scatter_units<<<nb_u, kBlock, 0, st>>>(n, b.ukey, b.cur_u, b.pidx);
   }
   const int nb_g = blocks((static_cast<int64_t>(n) + 63) & ~static_cast<int64_t>(63));
+  // signal histogram and cursors alternate between two sets by call parity; each call's
+  // gather zeroes the other set for the next call
+  int32_t* hist = b.hist_s + parity * kSignalBuckets;
+  int32_t* cur = b.cur_s + parity * kSignalBuckets;
+  int32_t* hist_next = b.hist_s + (parity ^ 1) * kSignalBuckets;
+  int32_t* cur_next = b.cur_s + (parity ^ 1) * kSignalBuckets;
   st_gather<<<nb_g + blocks(m), kBlock, 0, st>>>(s.x, s.y, s.z, n, b.pidx, b.pu, b.pm, b.pmh, sig,
-                                                 m, nb_g, b.bb, b.skey, b.hist_s, b.bmag);
-  st_scan_hist<kSignalBuckets><<<1, 1024, 0, st>>>(b.hist_s, b.off_s, b.cur_s, b.acc, b.bmag,
-                                                   nb_g, b.mag, 1);
-  st_scatter_signals<<<blocks(m), kBlock, 0, st>>>(m, b.skey, b.cur_s, b.sperm);
-  st_seed<<<blocks(static_cast<int64_t>(m) * kSeedLanes), kBlock, 0, st>>>(
-      b.pu, b.pidx, n, sig, m, b.sperm, b.skey, b.off_u, b.seed);
+                                                 m, nb_g, b.bb, b.skey, hist, hist_next,
+                                                 cur_next, b.bmag);
+  st_place_seed<<<blocks(static_cast<int64_t>(m) * kSeedLanes), kBlock, 0, st>>>(
+      hist, cur, b.skey, sig, m, b.pu, b.pidx, n, b.off_u, b.sperm, b.seed, b.bmag, nb_g,
+      b.mag);
   return hipGetLastError();
 }
 
