@@ -271,19 +271,32 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
   }
   const unsigned long long wave_open = __ballot(open != 0);
 
-  // operand ring with clamped, unconditional loads issued in ring order (find_mfma.hip)
-  const h8* opnd = reinterpret_cast<const h8*>(pmh) + 2 * lane;
+  // Operand ring with clamped, unconditional loads issued in ring order (find_mfma.hip).  Each
+  // load is a uniform batch base plus a per-lane offset that never changes, so no vector
+  // instruction computes addresses; pu and pidx cover whole batches (the slots past n hold
+  // stale values that the rare path skips).
+  // The loads are raw buffer loads from a per-workgroup base at batch tb0 (the chunk's first,
+  // or the last batch for an empty chunk): the lane's offset sits in the vector offset and
+  // the batch's in the scalar offset.  Every access is in bounds by construction (batches
+  // are clamped to the chunk, the host keeps chunk offsets below 2^31).
+  const int32_t tb0 = min(t_begin, n_batches - 1);
+  const __amdgpu_buffer_rsrc_t rh = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint4*>(pmh) + 128 * static_cast<int64_t>(tb0), 0, 0x7fffffff, 0x00020000);
+  const __amdgpu_buffer_rsrc_t ru_ = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float4*>(pu) + 64 * static_cast<int64_t>(tb0), 0, 0x7fffffff, 0x00020000);
+  const __amdgpu_buffer_rsrc_t ri_ = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<int32_t*>(pidx) + 64 * static_cast<int64_t>(tb0), 0, 0x7fffffff, 0x00020000);
+  const int32_t vh = 32 * lane, vu = 16 * lane, vi = 4 * lane;
   h8 ra[kDepth][2];
-  const f4* pu4 = reinterpret_cast<const f4*>(pu);
   f4 ru[kDepth];
   int32_t ri[kDepth];
 #pragma unroll
   for (int q = 0; q < kDepth; ++q) {
-    const int32_t tq = min(t_begin + q, t_end - 1);
-    ra[q][0] = opnd[128 * tq];
-    ra[q][1] = opnd[128 * tq + 1];
-    ru[q] = pu4[min(64 * tq + lane, n - 1)];
-    ri[q] = pidx[min(64 * tq + lane, n - 1)];
+    const int32_t tq = min(t_begin + q, t_end - 1) - tb0;
+    ra[q][0] = __builtin_bit_cast(h8, __builtin_amdgcn_raw_buffer_load_b128(rh, vh, 2048 * tq, 0));
+    ra[q][1] = __builtin_bit_cast(h8, __builtin_amdgcn_raw_buffer_load_b128(rh, vh + 16, 2048 * tq, 0));
+    ru[q] = __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(ru_, vu, 1024 * tq, 0));
+    ri[q] = static_cast<int32_t>(__builtin_amdgcn_raw_buffer_load_b32(ri_, vi, 256 * tq, 0));
     asm volatile("" ::: "memory");
   }
   v16f res[2][NB][2];
@@ -311,11 +324,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
         mn[e] = block_min(res[prv][e]);
         __builtin_amdgcn_sched_barrier(0);
       }
-      const int32_t tn = min(t + kDepth + q, t_end - 1);
-      ra[q][0] = opnd[128 * tn];
-      ra[q][1] = opnd[128 * tn + 1];
-      ru[q] = pu4[min(64 * tn + lane, n - 1)];
-      ri[q] = pidx[min(64 * tn + lane, n - 1)];
+      const int32_t tn = min(t + kDepth + q, t_end - 1) - tb0;
+      ra[q][0] = __builtin_bit_cast(h8, __builtin_amdgcn_raw_buffer_load_b128(rh, vh, 2048 * tn, 0));
+      ra[q][1] = __builtin_bit_cast(h8, __builtin_amdgcn_raw_buffer_load_b128(rh, vh + 16, 2048 * tn, 0));
+      ru[q] = __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(ru_, vu, 1024 * tn, 0));
+      ri[q] = static_cast<int32_t>(__builtin_amdgcn_raw_buffer_load_b32(ri_, vi, 256 * tn, 0));
       asm volatile("" ::: "memory");
       finish_batch(res[prv], mn, q > 0 || t > t_begin, min(t + q - 1, t_end - 1), h, lane, n,
                    lds_u[wave][prv], lds_i[wave][prv], sd, sig2, th, k1, k2, open, wave_open);
@@ -354,7 +367,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
 int f16_split(int32_t n, int32_t m, int cus, int want) {
   if (want > 0) return std::min(want, kMaxSplit);
   const int64_t sblocks = (m + kSignalsPerWG - 1) / kSignalsPerWG;
-  const int64_t target = 4LL * (cus > 0 ? cus : 256);
+  // about four rounds of work-groups at two per CU: the dynamic dispatch then evens out the
+  // work-groups whose chunk holds their signals' neighbours (most rare-path work)
+  const int64_t target = 8LL * (cus > 0 ? cus : 256);
   int64_t sp = (target + sblocks - 1) / sblocks;
   sp = std::min<int64_t>(sp, (n + 2047) / 2048);
   return static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(sp, kMaxSplit)));
@@ -364,6 +379,8 @@ hipError_t launch_scan_f16(const DevState& s, const StageBufs& b, int32_t n, con
                            int32_t m, int split, hipStream_t st) {
   const int32_t n_batches = (n + 63) / 64;
   const int32_t chunk_batches = (n_batches + split - 1) / split;
+  // buffer offsets within a chunk are 32-bit: 2 KB per batch
+  if (static_cast<int64_t>(chunk_batches) * 2048 >= (1LL << 31)) return hipErrorInvalidValue;
   dim3 grid((m + kSignalsPerWG - 1) / kSignalsPerWG, split);
   fh_scan<<<grid, 256, 0, st>>>(b.pu, b.pmh, b.pidx, n, chunk_batches, sig, m, b.sperm, b.skey,
                                 b.off_u, b.seed, b.mag, b.bb, s.part);

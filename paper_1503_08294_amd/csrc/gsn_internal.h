@@ -68,8 +68,9 @@ hipError_t launch_find_merge(const DevState& s, int32_t m, const FindConfig& cfg
 // Spatial staging of the screened scans (staging.hip).
 constexpr int kBuckets = 32 * 32 * 32;
 struct StageBufs {
-  float4* pu;       // [n_max] units in bucket order: (x, y, z, |w|^2)
-  int32_t* pidx;    // [n_max] original index of every sorted slot
+  float4* pu;       // [ceil64(n_max)] units in bucket order: (x, y, z, |w|^2); slots from n
+                    // to the end of the last batch hold stale values
+  int32_t* pidx;    // [ceil64(n_max)] original index of every sorted slot (same padding)
   int32_t* ukey;    // [n_max] bucket of every unit at the last bucketing
   int32_t* skey;    // [m_max] bucket of every signal
   int32_t* sperm;   // [m_max] original index of the signal at every sorted position

@@ -520,8 +520,9 @@ size_t stage_bytes(int32_t n_max, int32_t m_max) {
   auto add = [&](size_t x) { b += (x + 255) & ~static_cast<size_t>(255); };
   const size_t nm = static_cast<size_t>(n_max), mm = static_cast<size_t>(m_max);
   const size_t hb = 4 * static_cast<size_t>(kBuckets + 1);
-  add(16 * nm);  // pu
-  add(4 * nm);   // pidx
+  const size_t nb64 = (nm + 63) / 64 * 64;  // pu and pidx cover whole batches of 64 units
+  add(16 * nb64);  // pu
+  add(4 * nb64);   // pidx
   add(4 * nm);   // ukey
   add(4 * mm);   // skey
   add(4 * mm);   // sperm
@@ -547,8 +548,9 @@ StageBufs carve_stage(void* base, int32_t n_max, int32_t m_max) {
   };
   const size_t nm = static_cast<size_t>(n_max), mm = static_cast<size_t>(m_max);
   const size_t hb = 4 * static_cast<size_t>(kBuckets + 1);
-  s.pu = reinterpret_cast<float4*>(take(16 * nm));
-  s.pidx = reinterpret_cast<int32_t*>(take(4 * nm));
+  const size_t nb64 = (nm + 63) / 64 * 64;
+  s.pu = reinterpret_cast<float4*>(take(16 * nb64));
+  s.pidx = reinterpret_cast<int32_t*>(take(4 * nb64));
   s.ukey = reinterpret_cast<int32_t*>(take(4 * nm));
   s.skey = reinterpret_cast<int32_t*>(take(4 * mm));
   s.sperm = reinterpret_cast<int32_t*>(take(4 * mm));
