@@ -494,8 +494,17 @@ __global__ __launch_bounds__(kBlock) void st_merge(const unsigned long long* __r
       b = k;
     }
   };
+  // four rows per step, loaded before any is inserted, so the loads overlap (rows beyond
+  // the last read the all-ones key, which changes nothing)
   if (p < m)
-    for (int32_t q = g; q < rows; q += 8) insert(part[q * static_cast<size_t>(m) + p]);
+    for (int32_t q = g; q < rows; q += 32) {
+      unsigned long long k[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        k[i] = q + 8 * i < rows ? part[(q + 8 * i) * static_cast<size_t>(m) + p] : ~0ull;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) insert(k[i]);
+    }
   sa[g][c] = a;
   sb[g][c] = b;
   __syncthreads();
