@@ -35,6 +35,8 @@ class _Params(ctypes.Structure):
         ("n_max", ctypes.c_int32),
         ("e_max", ctypes.c_int32),
         ("m_max", ctypes.c_int32),
+        ("lock_mode", ctypes.c_int32),
+        ("key_mode", ctypes.c_int32),
     ]
 
 
@@ -49,10 +51,12 @@ class Params:
     n_max: int = 1024
     e_max: int = 4096
     m_max: int = 1024
+    lock_mode: int = 0   # 0: lock set {b, s} + N(b); 1: winner only, sequential update
+    key_mode: int = 0    # 0: (bits(d1) << 32) | j; 1: j (arrival order)
 
     def c(self) -> _Params:
         return _Params(self.eps_b, self.eps_n, self.max_age, self.err_alpha, self.err_beta,
-                       self.n_max, self.e_max, self.m_max)
+                       self.n_max, self.e_max, self.m_max, self.lock_mode, self.key_mode)
 
 
 _lib = None

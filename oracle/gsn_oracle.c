@@ -47,6 +47,17 @@
  *     w_r = (w_q + w_f) * 0.5, edge {q,f} replaced by {q,r} and {r,f} at age 0,
  *     err_q *= alpha, err_f *= alpha, err_r = err_q; skipped when N(q) is empty.
  *
+ * The paper's own collision rule is a second mode (lock_mode = 1, key_mode = 1 for its
+ * arrival order): the lock covers the winner only (Sec. 2.2, "implicit lock on the winner
+ * unit"), so the survivor of each winner unit is its signal of smallest key and all other
+ * signals with that winner are discarded; the survivors then update the network one after
+ * another in ascending key order, each with the complete single-signal step of Sec. 2.1
+ * (age, connect, move the winner and its neighbours as they are at that moment plus the
+ * second, drop old edges, err[b] += d1) on the network left by the survivors before it;
+ * winners and seconds stay those of the snapshot.  err *= beta once after all survivors.
+ * In this mode adapt performs the whole update and update_edges has nothing left to do.
+ * key_mode 1 keys a signal by its index alone (arrival order), 0 by (bits(d1) << 32) | j.
+ *
  * Build: gcc -O2 -ffp-contract=off -fopenmp -shared -fPIC (no -ffast-math, no -march).
  */
 #include <stdint.h>
@@ -72,6 +83,8 @@ typedef struct {
   int32_t n_max;
   int32_t e_max;
   int32_t m_max;
+  int32_t lock_mode;  /* 0: lock set {b, s} + N(b); 1: the winner only, sequential update */
+  int32_t key_mode;   /* 0: (bits(d1) << 32) | j; 1: j */
 } orc_params;
 
 typedef struct {
@@ -175,6 +188,7 @@ static int params_ok(const orc_params* p) {
   if (!(p->eps_n >= 0.0f && p->eps_n <= 1.0f)) return 0;
   if (p->max_age < 0) return 0;
   if (p->n_max < 2 || p->e_max < 0 || p->m_max < 1) return 0;
+  if (p->lock_mode < 0 || p->lock_mode > 1 || p->key_mode < 0 || p->key_mode > 1) return 0;
   return 1;
 }
 
@@ -260,7 +274,8 @@ int orc_find_winners(const orc_net* g, const float* sig, int32_t m, int32_t* win
 
 /* ------------------------------------------------------------- resolve conflicts --- */
 
-static uint64_t signal_key(float d1, int32_t j) {
+static uint64_t signal_key(const orc_net* g, float d1, int32_t j) {
+  if (g->p.key_mode == 1) return (uint64_t)(uint32_t)j;
   uint32_t bits;
   memcpy(&bits, &d1, sizeof bits);
   return ((uint64_t)bits << 32) | (uint32_t)j;
@@ -271,8 +286,9 @@ static int check_pair(const orc_net* g, int32_t b, int32_t s) {
 }
 
 /*
- * L_j = {b_j, s_j} + N(b_j) on the pre-iteration graph.  owner[u] = the smallest key
- * among the signals that claim u; j is accepted iff it owns every unit of L_j.
+ * L_j = {b_j, s_j} + N(b_j) on the pre-iteration graph (lock_mode 0) or {b_j} (lock_mode
+ * 1).  owner[u] = the smallest key among the signals that claim u; j is accepted iff it
+ * owns every unit of L_j.
  */
 int orc_resolve_conflicts(const orc_net* g, int32_t m, const int32_t* winner,
                           const int32_t* second, const float* d1, uint8_t* accepted) {
@@ -284,10 +300,12 @@ int orc_resolve_conflicts(const orc_net* g, int32_t m, const int32_t* winner,
   uint64_t* owner = (uint64_t*)malloc(sizeof(uint64_t) * (size_t)(g->n > 0 ? g->n : 1));
   if (!owner) return ORC_E_CAPACITY;
   for (int32_t u = 0; u < g->n; ++u) owner[u] = UINT64_MAX;
+  const int whole = g->p.lock_mode == 0;
   for (int32_t j = 0; j < m; ++j) {
-    const uint64_t key = signal_key(d1[j], j);
+    const uint64_t key = signal_key(g, d1[j], j);
     const int32_t b = winner[j], s = second[j];
     if (key < owner[b]) owner[b] = key;
+    if (!whole) continue;
     if (key < owner[s]) owner[s] = key;
     for (int32_t k = 0; k < g->deg[b]; ++k) {
       int32_t u = g->nb[b][k];
@@ -295,10 +313,13 @@ int orc_resolve_conflicts(const orc_net* g, int32_t m, const int32_t* winner,
     }
   }
   for (int32_t j = 0; j < m; ++j) {
-    const uint64_t key = signal_key(d1[j], j);
+    const uint64_t key = signal_key(g, d1[j], j);
     const int32_t b = winner[j], s = second[j];
-    int ok = owner[b] == key && owner[s] == key;
-    for (int32_t k = 0; ok && k < g->deg[b]; ++k) ok = owner[g->nb[b][k]] == key;
+    int ok = owner[b] == key;
+    if (whole) {
+      ok = ok && owner[s] == key;
+      for (int32_t k = 0; ok && k < g->deg[b]; ++k) ok = owner[g->nb[b][k]] == key;
+    }
     accepted[j] = (uint8_t)ok;
   }
   free(owner);
@@ -315,12 +336,16 @@ static void move_unit(orc_net* g, int32_t u, float eps, float sx, float sy, floa
   t = sz - g->z[u]; t = eps * t; g->z[u] = g->z[u] + t;
 }
 
+static int sequential_update(orc_net* g, const float* sig, int32_t m, const int32_t* winner,
+                             const int32_t* second, const float* d1, const uint8_t* accepted);
+
 int orc_adapt(orc_net* g, const float* sig, int32_t m, const int32_t* winner,
               const int32_t* second, const float* d1, const uint8_t* accepted) {
   if (!g || m < 0 || m > g->p.m_max) return ORC_E_INVAL;
   if (m > 0 && (!sig || !winner || !second || !d1 || !accepted)) return ORC_E_INVAL;
   for (int32_t j = 0; j < m; ++j)
     if (accepted[j] && !check_pair(g, winner[j], second[j])) return ORC_E_INVAL;
+  if (g->p.lock_mode == 1) return sequential_update(g, sig, m, winner, second, d1, accepted);
   for (int32_t j = 0; j < m; ++j) {
     if (!accepted[j]) continue;
     const float sx = sig[j], sy = sig[(size_t)m + j], sz = sig[2 * (size_t)m + j];
@@ -343,6 +368,7 @@ int orc_update_edges(orc_net* g, int32_t m, const int32_t* winner, const int32_t
   if (m > 0 && (!winner || !second || !accepted)) return ORC_E_INVAL;
   for (int32_t j = 0; j < m; ++j)
     if (accepted[j] && !check_pair(g, winner[j], second[j])) return ORC_E_INVAL;
+  if (g->p.lock_mode == 1) return ORC_OK;  /* adapt performed the whole update */
   int32_t* tmp = NULL;
   int32_t tmp_cap = 0;
   for (int32_t j = 0; j < m; ++j) {
@@ -381,6 +407,78 @@ int orc_update_edges(orc_net* g, int32_t m, const int32_t* winner, const int32_t
     g->status = ORC_E_CAPACITY;
     return ORC_E_CAPACITY;
   }
+  return ORC_OK;
+}
+
+/* ------------------------------------------------- sequential update (lock_mode 1) --- */
+
+static const orc_net* sort_net;   /* the comparator's context (the oracle is not reentrant) */
+static const float* sort_d1;
+
+static int by_key(const void* a, const void* b) {
+  const int32_t i = *(const int32_t*)a, j = *(const int32_t*)b;
+  const uint64_t ki = signal_key(sort_net, sort_d1[i], i), kj = signal_key(sort_net, sort_d1[j], j);
+  return ki < kj ? -1 : (ki > kj ? 1 : 0);
+}
+
+/* The survivors in ascending key order, each with the complete single-signal step of
+ * Sec. 2.1 on the current network (see the header); then err *= beta once. */
+static int sequential_update(orc_net* g, const float* sig, int32_t m, const int32_t* winner,
+                             const int32_t* second, const float* d1, const uint8_t* accepted) {
+  int32_t* order = (int32_t*)malloc(sizeof(int32_t) * (size_t)(m > 0 ? m : 1));
+  if (!order) return ORC_E_CAPACITY;
+  int32_t ns = 0;
+  for (int32_t j = 0; j < m; ++j)
+    if (accepted[j]) order[ns++] = j;
+  sort_net = g;
+  sort_d1 = d1;
+  qsort(order, (size_t)ns, sizeof(int32_t), by_key);
+  int32_t* tmp = NULL;
+  int32_t tmp_cap = 0;
+  int rc = ORC_OK;
+  for (int32_t q = 0; q < ns && rc == ORC_OK; ++q) {
+    const int32_t j = order[q];
+    const int32_t b = winner[j], s = second[j];
+    const float sx = sig[j], sy = sig[(size_t)m + j], sz = sig[2 * (size_t)m + j];
+    /* neighbours of b before this step; s moves once, as a neighbour or on its own */
+    if (g->deg[b] > tmp_cap) {
+      tmp_cap = g->deg[b] + 1;
+      int32_t* t = (int32_t*)realloc(tmp, sizeof(int32_t) * (size_t)tmp_cap);
+      if (!t) { rc = ORC_E_CAPACITY; break; }
+      tmp = t;
+    }
+    const int32_t nb0 = g->deg[b];
+    memcpy(tmp, g->nb[b], sizeof(int32_t) * (size_t)nb0);
+    const int s_was_nb = edge_pos(g, b, s) >= 0;
+    /* 1. age every edge at b; 2. connect b and s at age 0 */
+    for (int32_t k = 0; k < g->deg[b]; ++k) set_age(g, b, g->nb[b][k], g->ag[b][k] + 1);
+    if (s_was_nb) {
+      set_age(g, b, s, 0);
+    } else if ((rc = add_edge(g, b, s, 0)) != ORC_OK) {
+      break;
+    }
+    /* 3. move the winner, its neighbours and the second */
+    move_unit(g, b, g->p.eps_b, sx, sy, sz);
+    for (int32_t k = 0; k < nb0; ++k) move_unit(g, tmp[k], g->p.eps_n, sx, sy, sz);
+    if (!s_was_nb) move_unit(g, s, g->p.eps_n, sx, sy, sz);
+    /* 4. remove the edges at b older than max_age */
+    int32_t nd = 0;
+    for (int32_t k = 0; k < g->deg[b]; ++k)
+      if (g->ag[b][k] > g->p.max_age) tmp[nd++] = g->nb[b][k];
+    for (int32_t k = 0; k < nd; ++k) {
+      remove_edge(g, b, tmp[k]);
+      if (g->deg[tmp[k]] == 0) g->orphan[tmp[k]] = 1;
+    }
+    g->err[b] = g->err[b] + d1[j];
+  }
+  free(tmp);
+  free(order);
+  if (rc == ORC_OK && g->n_edges > g->p.e_max) rc = ORC_E_CAPACITY;
+  if (rc != ORC_OK) {
+    g->status = rc;
+    return rc;
+  }
+  for (int32_t i = 0; i < g->n; ++i) g->err[i] = g->err[i] * g->p.err_beta;
   return ORC_OK;
 }
 

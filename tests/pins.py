@@ -69,6 +69,12 @@ class SingleSignalGNG:
              + (xi[2] - self.w[i, 2]) * (xi[2] - self.w[i, 2]) for i in range(n)]
         order = sorted(range(n), key=lambda i: (d[i], i))
         b, s = order[0], order[1]
+        self.apply(b, s, xi)
+        return b, s, d[b]
+
+    def apply(self, b, s, xi):
+        """The update half of the step for a given winner b and second s."""
+        xi = np.asarray(xi, np.float32)
         nb_before = self.nbrs(b)
         for v in nb_before:
             self.age[frozenset((b, v))] += 1
@@ -81,7 +87,6 @@ class SingleSignalGNG:
         old = [e for e, a in self.age.items() if b in e and a > self.max_age]
         for e in old:
             del self.age[e]
-        return b, s, d[b]
 
     def edges(self):
         out = sorted((min(e), max(e), a) for e, a in self.age.items())
