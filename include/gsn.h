@@ -68,7 +68,26 @@ typedef struct gsn_params {
   int32_t n_max;     /* unit capacity, >= 2 */
   int32_t e_max;     /* undirected edge capacity, >= 0 */
   int32_t m_max;     /* signals per iteration capacity, >= 1 */
+  int32_t lock_mode; /* collision rule: GSN_LOCK_SET (0) or GSN_LOCK_WINNER (1), see below */
+  int32_t key_mode;  /* survivor priority: GSN_KEY_DIST_INDEX (0) or GSN_KEY_INDEX (1) */
 } gsn_params;
+
+/* Collision rules (Sec. 2.2).  The key of signal j orders the signals that collide:
+ *   GSN_KEY_DIST_INDEX  key = (bits(d1[j]) << 32) | j: the signal nearest to its winner
+ *                       survives, ties to the lower index;
+ *   GSN_KEY_INDEX       key = j: the first signal of the batch survives, as with signals
+ *                       that arrive in order.
+ *   GSN_LOCK_SET        signal j locks L_j = {winner, second} + N(winner); survivors have
+ *                       pairwise disjoint lock sets and update in parallel (one pass).
+ *   GSN_LOCK_WINNER     the paper's rule: only the winner unit is locked, so the first
+ *                       signal (smallest key) of every winner survives and the others are
+ *                       discarded; the survivors then take the whole single-signal step of
+ *                       Sec. 2.1 (aging, the edge to the second, adaptation, pruning) one
+ *                       after another in ascending key order, each on the network its
+ *                       predecessors left.  gsn_adapt performs that whole update and
+ *                       gsn_update_edges does nothing. */
+enum { GSN_LOCK_SET = 0, GSN_LOCK_WINNER = 1 };
+enum { GSN_KEY_DIST_INDEX = 0, GSN_KEY_INDEX = 1 };
 
 /* Bytes of device workspace a network with these parameters needs; 0 if the parameters
  * are invalid.  Pure host computation. */
@@ -93,9 +112,10 @@ int gsn_find_winners(gsn_net* net, const float* sig, int32_t m, int32_t* winner,
 
 /* Collision handling (Sec. 2.2: signals whose updates would move the same unit, change
  * the same neighbourhood or add the same edge collide; an implicit lock lets one of them
- * take effect and discards the others).  Signal j locks L_j = {winner[j], second[j]} plus the current
- * neighbours of winner[j]; its key is (bits(d1[j]) << 32) | j.  accepted[j] = 1 iff no
- * other signal with a smaller key locks a unit of L_j, else 0.  Accepted lock sets are
+ * take effect and discards the others).  With GSN_LOCK_SET, signal j locks L_j =
+ * {winner[j], second[j]} plus the current neighbours of winner[j]; with GSN_LOCK_WINNER,
+ * L_j = {winner[j]}.  Keys follow key_mode.  accepted[j] = 1 iff no other signal with a
+ * smaller key locks a unit of L_j, else 0.  With GSN_LOCK_SET, accepted lock sets are
  * pairwise disjoint, so the updates below commute.  Inputs: device arrays of length m as
  * produced by gsn_find_winners (any values with 0 <= winner, second < N and
  * winner != second; others are rejected and flag GSN_E_INVAL on the device).  Output:
@@ -109,11 +129,21 @@ int gsn_resolve_conflicts(gsn_net* net, int32_t m, const int32_t* winner,
  *     w <- w + eps * (sig_j - w)   per component as t = sig - w; t = eps * t; w = w + t,
  * with eps_b for b and eps_n for every current neighbour of b and for s (once).  The
  * winner's error grows by d1[j]; afterwards every unit's error is multiplied by err_beta.
- * Inputs as for gsn_resolve_conflicts plus sig (SoA [3][m]).  Async. */
+ * Inputs as for gsn_resolve_conflicts plus sig (SoA [3][m]).  Async with GSN_LOCK_SET.
+ * With GSN_LOCK_WINNER it performs, for the accepted signals in ascending key order, the
+ * whole single-signal step: every edge at b ages by one, {b, s} is set to age 0 (created if
+ * absent), b, its neighbours before that step and s (once) move as above, the edges at b
+ * older than max_age are removed (a unit left with no edge is marked for gsn_grow) and
+ * err[b] grows by d1[j]; then err *= err_beta.  Any accepted set is valid (signals sharing
+ * a winner are applied in key order too); more than e_max edges at the end set
+ * GSN_E_CAPACITY on the device.  It runs in rounds (every pending signal whose units
+ * {b, s} + N(b) no pending signal of smaller key touches goes in the same round) and syncs
+ * once every few rounds to see whether signals are left. */
 int gsn_adapt(gsn_net* net, const float* sig, int32_t m, const int32_t* winner,
               const int32_t* second, const float* d1, const uint8_t* accepted, void* stream);
 
-/* Connection update (Sec. 2.1 step 3 and its footnote on aging).  For every accepted j:
+/* Connection update (Sec. 2.1 step 3 and its footnote on aging); with GSN_LOCK_WINNER
+ * gsn_adapt has done it and this call only ends the iteration.  For every accepted j:
  * every edge at b = winner[j] ages by one, the edge {b, second[j]} is set to age 0 (and
  * created if absent), then the edges at b older than max_age are removed; a unit left
  * with no edge by such a removal is marked for removal by gsn_grow.  The adjacency is then
@@ -178,6 +208,14 @@ enum { GSN_T_FIND_SCAN = 0, GSN_T_FIND = 1, GSN_T_RESOLVE = 2, GSN_T_ADAPT = 3,
        GSN_T_EDGES = 4, GSN_T_COUNT = 5 };
 int gsn_timing_enable(gsn_net* net, int32_t enable);
 int gsn_timing_read(gsn_net* net, int32_t which, double* total_ms, int32_t* launches);
+
+/* Counters of the last call, for measurement (host values, no sync).
+ *   GSN_STAT_ROUNDS   rounds the last gsn_adapt with GSN_LOCK_WINNER took to apply every
+ *                     accepted signal (0 in GSN_LOCK_SET mode or when none was accepted)
+ *   GSN_STAT_LAUNCHED rounds it launched (rounds are launched a few at a time; those after
+ *                     the last one return at once) */
+enum { GSN_STAT_ROUNDS = 0, GSN_STAT_LAUNCHED = 1 };
+int gsn_stat(gsn_net* net, int32_t key, int64_t* value);
 
 #ifdef __cplusplus
 }

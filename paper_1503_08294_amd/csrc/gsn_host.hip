@@ -22,8 +22,10 @@ Layout layout_for(const gsn_params& p) {
     o += bytes;
   };
   const size_t nm = static_cast<size_t>(p.n_max);
-  const size_t hc = 2 * static_cast<size_t>(p.e_max) + 2;
   const size_t mm = static_cast<size_t>(p.m_max);
+  // the winner-lock update works on a copy of the adjacency with room for one insertion
+  // per survivor at its winner and one at its second
+  const size_t hc = 2 * (static_cast<size_t>(p.e_max) + (p.lock_mode == 1 ? mm : 0)) + 2;
   add(4 * nm);                 // 0 x
   add(4 * nm);                 // 1 y
   add(4 * nm);                 // 2 z
@@ -43,6 +45,10 @@ Layout layout_for(const gsn_params& p) {
   add(4 * kStSlots);           // 16 status
   add(8 * static_cast<size_t>(kMaxSplit) * 2 * mm);  // 17 part
   add(stage_bytes(p.n_max, p.m_max));                 // 18 screened staging
+  add(mm);                     // 19 pend
+  add(4 * nm);                 // 20 len
+  add(4 * nm);                 // 21 extra
+  add(4 * (kRing + 1));        // 22 rem
   L.total = (o + 255) & ~static_cast<size_t>(255);
   return L;
 }
@@ -69,6 +75,10 @@ void carve(const gsn_params& p, void* base, DevState* s) {
   s->status = reinterpret_cast<int32_t*>(b + L.off[16]);
   s->part = reinterpret_cast<unsigned long long*>(b + L.off[17]);
   s->scr = b + L.off[18];
+  s->pend = reinterpret_cast<uint8_t*>(b + L.off[19]);
+  s->len = reinterpret_cast<int32_t*>(b + L.off[20]);
+  s->extra = reinterpret_cast<int32_t*>(b + L.off[21]);
+  s->rem = reinterpret_cast<int32_t*>(b + L.off[22]);
 }
 
 }  // namespace gsn
@@ -77,6 +87,7 @@ using gsn::DevState;
 
 enum Phase { kReady = 0, kFound = 1, kResolved = 2, kAdapted = 3 };
 constexpr int kRebucketEvery = 16;
+constexpr int kFirstRoundBatch = 8;  // rounds of the winner-lock update before the first read
 
 struct gsn_net {
   gsn_params p;
@@ -91,6 +102,7 @@ struct gsn_net {
   bool timing;
   int32_t bucket_n;            // unit count at the last spatial bucketing (-1: none yet)
   int32_t finds_since_bucket;
+  int64_t stat[2];             // GSN_STAT_ROUNDS, GSN_STAT_LAUNCHED of the last adapt
   std::vector<hipEvent_t> pool;
   std::vector<std::pair<hipEvent_t, hipEvent_t>> rec[GSN_T_COUNT];
 };
@@ -103,8 +115,10 @@ bool params_ok(const gsn_params* p) {
   if (!(p->eps_n >= 0.0f && p->eps_n <= 1.0f)) return false;
   if (p->max_age < 0) return false;
   if (p->n_max < 2 || p->e_max < 0 || p->m_max < 1) return false;
+  if (p->lock_mode < 0 || p->lock_mode > 1 || p->key_mode < 0 || p->key_mode > 1) return false;
   // keep every derived index inside int32
-  if (static_cast<int64_t>(p->e_max) * 2 + 2 > INT32_MAX) return false;
+  const int64_t slack = p->lock_mode == 1 ? p->m_max : 0;
+  if ((static_cast<int64_t>(p->e_max) + slack) * 2 + 2 > INT32_MAX) return false;
   if (static_cast<int64_t>(p->n_max) + 2 > INT32_MAX / 4) return false;
   if (static_cast<int64_t>(p->m_max) * 2 * gsn::kMaxSplit > INT32_MAX) return false;
   return true;
@@ -165,6 +179,45 @@ int read_status_slot(gsn_net* net, int slot, int32_t* out, hipStream_t st) {
   return hip_ok(hipStreamSynchronize(st));
 }
 
+// The winner-lock update: survivors go in rounds (update_winner.hip); the pending counts
+// are read back after every batch of rounds, and the batches grow so that long chains of
+// colliding survivors cost few reads.
+int adapt_sequential(gsn_net* net, const float* sig, int32_t m, const int32_t* winner,
+                     const int32_t* second, const float* d1, const uint8_t* accepted,
+                     hipStream_t st) {
+  const gsn::DevState& s = net->s;
+  const int64_t slack_cap = 2 * (static_cast<int64_t>(net->p.e_max) + net->p.m_max);
+  hipError_t e = gsn::launch_winner_prologue(s, net->cur, net->n, m, winner, second, accepted,
+                                             slack_cap, st);
+  int32_t h[gsn::kRing + 1];
+  int64_t t = 0, rounds = -1;
+  int batch = kFirstRoundBatch;
+  while (e == hipSuccess && rounds < 0) {
+    e = gsn::launch_winner_rounds(s, net->cur, net->n, sig, m, winner, second, d1,
+                                  net->p.key_mode, net->p.eps_b, net->p.eps_n, net->p.max_age,
+                                  t, batch, st);
+    if (e != hipSuccess) break;
+    e = hipMemcpyAsync(h, s.rem, sizeof(h), hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e != hipSuccess) break;
+    for (int64_t i = t; i < t + batch; ++i)
+      if (h[i % gsn::kRing] == 0) {
+        rounds = h[gsn::kRingSurvivors] > 0 ? i + 1 : 0;
+        break;
+      }
+    t += batch;
+    // every round applies the pending survivor of smallest key, so m rounds always suffice
+    if (rounds < 0 && t > static_cast<int64_t>(m) + gsn::kRing) return GSN_E_HIP;
+    batch = std::min(2 * batch, gsn::kRing - 1);
+  }
+  if (e == hipSuccess)
+    e = gsn::launch_winner_epilogue(s, net->cur, net->n, net->p.err_beta,
+                                    2 * static_cast<int64_t>(net->p.e_max), st);
+  net->stat[0] = rounds < 0 ? 0 : rounds;
+  net->stat[1] = t;
+  return hip_ok(e);
+}
+
 }  // namespace
 
 extern "C" {
@@ -195,6 +248,7 @@ int gsn_create(const gsn_params* params, void* workspace, size_t workspace_bytes
   net->timing = false;
   net->bucket_n = -1;
   net->finds_since_bucket = 0;
+  net->stat[0] = net->stat[1] = 0;
   int dev = 0, cus = 256;
   if (hipGetDevice(&dev) == hipSuccess &&
       hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess)
@@ -278,7 +332,7 @@ int gsn_resolve_conflicts(gsn_net* net, int32_t m, const int32_t* winner,
   hipStream_t st = as_stream(stream);
   TimedRegion t(net, GSN_T_RESOLVE, st);
   hipError_t e = gsn::launch_resolve(net->s, net->cur, net->n, m, winner, second, d1, accepted,
-                                     st);
+                                     net->p.lock_mode, net->p.key_mode, st);
   t.end();
   return hip_ok(e);
 }
@@ -291,10 +345,14 @@ int gsn_adapt(gsn_net* net, const float* sig, int32_t m, const int32_t* winner,
   net->phase = kAdapted;
   hipStream_t st = as_stream(stream);
   TimedRegion t(net, GSN_T_ADAPT, st);
-  hipError_t e = gsn::launch_adapt(net->s, net->cur, net->n, sig, m, winner, second, d1,
-                                   accepted, net->p.eps_b, net->p.eps_n, net->p.err_beta, st);
+  int rc = net->p.lock_mode == 1 && m > 0 && net->n > 0
+               ? adapt_sequential(net, sig, m, winner, second, d1, accepted, st)
+               : hip_ok(gsn::launch_adapt(net->s, net->cur, net->n, sig, m, winner, second, d1,
+                                          accepted, net->p.eps_b, net->p.eps_n,
+                                          net->p.err_beta, st));
+  if (net->p.lock_mode != 1 || m == 0 || net->n == 0) net->stat[0] = net->stat[1] = 0;
   t.end();
-  return hip_ok(e);
+  return rc;
 }
 
 int gsn_update_edges(gsn_net* net, int32_t m, const int32_t* winner, const int32_t* second,
@@ -303,6 +361,10 @@ int gsn_update_edges(gsn_net* net, int32_t m, const int32_t* winner, const int32
   if (net->phase != kAdapted) return GSN_E_STATE;
   if (m > 0 && (!winner || !second || !accepted)) return GSN_E_INVAL;
   hipStream_t st = as_stream(stream);
+  if (net->p.lock_mode == 1) {  // gsn_adapt has updated the edges
+    net->phase = kReady;
+    return GSN_OK;
+  }
   TimedRegion t(net, GSN_T_EDGES, st);
   hipError_t e = gsn::launch_edges(net->s, net->cur, net->n, m, winner, second, accepted,
                                    net->p.max_age, 2 * static_cast<int64_t>(net->p.e_max), st);
@@ -462,6 +524,9 @@ int gsn_import(gsn_net* net, int32_t n, const float* xyz, const float* err, int3
     const size_t nm = static_cast<size_t>(net->p.n_max);
     ok = ok && hipMemset(s.ins, 0xff, 4 * nm) == hipSuccess;
     ok = ok && hipMemset(s.orphan, 0, 4 * nm) == hipSuccess;
+    ok = ok && hipMemset(s.lock, 0xff, 8 * nm) == hipSuccess;
+    ok = ok && hipMemset(s.extra, 0, 4 * nm) == hipSuccess;
+    ok = ok && hipMemset(s.rem, 0, 4 * (gsn::kRing + 1)) == hipSuccess;
     ok = ok && hipMemset(s.status, 0, 4 * gsn::kStSlots) == hipSuccess;
     ok = ok && gsn::launch_stage_init(gsn::carve_stage(s.scr, net->p.n_max, net->p.m_max),
                                       nullptr) == hipSuccess;
@@ -509,6 +574,12 @@ int gsn_tune(gsn_net* net, int32_t key, int32_t value) {
     default:
       return GSN_E_INVAL;
   }
+}
+
+int gsn_stat(gsn_net* net, int32_t key, int64_t* value) {
+  if (!net || !value || key < 0 || key > GSN_STAT_LAUNCHED) return GSN_E_INVAL;
+  *value = net->stat[key];
+  return GSN_OK;
 }
 
 int gsn_timing_enable(gsn_net* net, int32_t enable) {

@@ -24,12 +24,44 @@ enum StatusSlot {
   kStSlots = 16
 };
 
+// Rounds of the sequential-survivor update: counters live in a ring of kRing slots (slot
+// t % kRing counts the signals still pending after round t) plus one slot that counts the
+// survivors of the call.  At most kRing - 1 rounds are launched between two host reads.
+constexpr int kRing = 64;
+constexpr int kRingSurvivors = kRing;
+
+__device__ __forceinline__ void raise_error(int32_t* status, int32_t code) {
+  atomicCAS(&status[kStError], 0, code);
+}
+
+__device__ __forceinline__ bool pair_ok(int32_t b, int32_t s, int32_t n) {
+  return b >= 0 && b < n && s >= 0 && s < n && b != s;
+}
+
+// Priority of signal j among the signals that collide (smaller wins): key_mode 0 orders by
+// the winner distance, then the index; key_mode 1 by the index alone.
+__device__ __forceinline__ unsigned long long signal_key(float d1, int32_t j, int key_mode) {
+  const unsigned long long lo = static_cast<uint32_t>(j);
+  if (key_mode == 1) return lo;
+  return (static_cast<unsigned long long>(__float_as_uint(d1)) << 32) | lo;
+}
+
+// w <- w + eps (xi - w), one binary32 rounding per operation (no contraction).
+__device__ __forceinline__ void move_unit(float* __restrict__ x, float* __restrict__ y,
+                                          float* __restrict__ z, int32_t u, float eps,
+                                          float sx, float sy, float sz) {
+  float t;
+  t = sx - x[u]; t = eps * t; x[u] = x[u] + t;
+  t = sy - y[u]; t = eps * t; y[u] = y[u] + t;
+  t = sz - z[u]; t = eps * t; z[u] = z[u] + t;
+}
+
 // Device arrays carved out of the caller's workspace.
 struct DevState {
   float *x, *y, *z, *err;          // [n_max]
   int32_t* rp[2];                  // [n_max + 2]   row pointers, ping-pong
-  int32_t* col[2];                 // [2 e_max + 2] neighbour ids, ping-pong
-  int32_t* age[2];                 // [2 e_max + 2] ages, ping-pong
+  int32_t* col[2];                 // [2 e_max + 2] neighbour ids, ping-pong (2 (e_max +
+  int32_t* age[2];                 //  m_max) + 2 with the winner lock); ages, ping-pong
   unsigned long long* lock;        // [n_max]       packed (d1 bits, signal) claims
   int32_t* ins;                    // [n_max]       partner of a new edge, -1 = none
   int32_t* orphan;                 // [n_max]       1 = last edge removed by aging
@@ -39,6 +71,11 @@ struct DevState {
   int32_t* status;                 // [kStSlots]
   unsigned long long* part;        // [kMaxSplit][2][m_max] per-chunk top-2 keys
   void* scr;                       // staging area of the screened scans (staging.hip)
+  // sequential-survivor update (winner lock)
+  uint8_t* pend;                   // [m_max]       0 done, 1 pending, 2 applies this round
+  int32_t* len;                    // [n_max]       live length of every row of the slack CSR
+  int32_t* extra;                  // [n_max]       insertions a row may receive (kept zero)
+  int32_t* rem;                    // [kRing + 1]   per-round pending counts, survivors
 };
 
 struct Layout {
@@ -104,9 +141,11 @@ hipError_t launch_scan_f16(const DevState& s, const StageBufs& b, int32_t n, con
 hipError_t launch_scan_mfma(const DevState& s, const StageBufs& b, int32_t n, const float* sig,
                             int32_t m, int split, hipStream_t st);
 
+// lock_mode: 0 = lock set {b, s} + N(b), 1 = the winner alone; key_mode: 0 = (d1 bits,
+// index), 1 = index
 hipError_t launch_resolve(const DevState& s, int cur, int32_t n, int32_t m,
                           const int32_t* winner, const int32_t* second, const float* d1,
-                          uint8_t* accepted, hipStream_t st);
+                          uint8_t* accepted, int lock_mode, int key_mode, hipStream_t st);
 hipError_t launch_adapt(const DevState& s, int cur, int32_t n, const float* sig, int32_t m,
                         const int32_t* winner, const int32_t* second, const float* d1,
                         const uint8_t* accepted, float eps_b, float eps_n, float beta,
@@ -115,6 +154,18 @@ hipError_t launch_edges(const DevState& s, int cur, int32_t n, int32_t m,
                         const int32_t* winner, const int32_t* second,
                         const uint8_t* accepted, int32_t max_age, int64_t half_cap,
                         hipStream_t st);
+// The sequential-survivor update (update_winner.hip).  Prologue: the slack copy of the CSR
+// in buffer cur ^ 1; rounds [t0, t0 + count); epilogue: the compact CSR back in buffer cur
+// and the error decay.  half_cap bounds the compact adjacency, slack_cap the slack copy.
+hipError_t launch_winner_prologue(const DevState& s, int cur, int32_t n, int32_t m,
+                                  const int32_t* winner, const int32_t* second,
+                                  const uint8_t* accepted, int64_t slack_cap, hipStream_t st);
+hipError_t launch_winner_rounds(const DevState& s, int cur, int32_t n, const float* sig,
+                                int32_t m, const int32_t* winner, const int32_t* second,
+                                const float* d1, int key_mode, float eps_b, float eps_n,
+                                int32_t max_age, int64_t t0, int count, hipStream_t st);
+hipError_t launch_winner_epilogue(const DevState& s, int cur, int32_t n, float beta,
+                                  int64_t half_cap, hipStream_t st);
 hipError_t launch_scan_blocks(int32_t* bsum, int32_t nb, int64_t cap, int32_t* out_total,
                               int32_t* status, int32_t slot, hipStream_t st);
 hipError_t launch_init(const DevState& s, int cur, int32_t n0, int32_t n_max,

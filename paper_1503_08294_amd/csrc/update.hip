@@ -14,19 +14,6 @@
 namespace gsn {
 namespace {
 
-__device__ __forceinline__ void raise_error(int32_t* status, int32_t code) {
-  atomicCAS(&status[kStError], 0, code);
-}
-
-__device__ __forceinline__ bool pair_ok(int32_t b, int32_t s, int32_t n) {
-  return b >= 0 && b < n && s >= 0 && s < n && b != s;
-}
-
-__device__ __forceinline__ unsigned long long signal_key(float d1, int32_t j) {
-  return (static_cast<unsigned long long>(__float_as_uint(d1)) << 32) |
-         static_cast<uint32_t>(j);
-}
-
 // Position of neighbour v in the (ascending) row of u, or -1.
 __device__ __forceinline__ int32_t find_in_row(const int32_t* __restrict__ rp,
                                                const int32_t* __restrict__ col, int32_t u,
@@ -48,10 +35,12 @@ __global__ void rs_clear(unsigned long long* __restrict__ lock, int32_t n) {
   if (i < n) lock[i] = ~0ull;
 }
 
+// winner_only: L_j = {b}, else L_j = {b, s} + N(b).
 __global__ void rs_claim(int32_t m, int32_t n, const int32_t* __restrict__ winner,
                          const int32_t* __restrict__ second, const float* __restrict__ d1,
                          const int32_t* __restrict__ rp, const int32_t* __restrict__ col,
-                         unsigned long long* __restrict__ lock, int32_t* __restrict__ status) {
+                         unsigned long long* __restrict__ lock, int32_t* __restrict__ status,
+                         int winner_only, int key_mode) {
   const int32_t j = blockIdx.x * kBlock + threadIdx.x;
   if (j >= m) return;
   const int32_t b = winner[j], s = second[j];
@@ -59,17 +48,21 @@ __global__ void rs_claim(int32_t m, int32_t n, const int32_t* __restrict__ winne
     raise_error(status, GSN_E_INVAL);
     return;
   }
-  const unsigned long long key = signal_key(d1[j], j);
+  const unsigned long long key = signal_key(d1[j], j, key_mode);
   atomicMin(&lock[b], key);
+  if (winner_only) return;
   atomicMin(&lock[s], key);
   for (int32_t k = rp[b]; k < rp[b + 1]; ++k) atomicMin(&lock[col[k]], key);
 }
 
+// With the winner alone locked, the survivor also releases its lock (the other claimants
+// compare with their own keys, which differ from both values), so the lock array is back
+// to all ones afterwards.
 __global__ void rs_check(int32_t m, int32_t n, const int32_t* __restrict__ winner,
                          const int32_t* __restrict__ second, const float* __restrict__ d1,
                          const int32_t* __restrict__ rp, const int32_t* __restrict__ col,
-                         const unsigned long long* __restrict__ lock,
-                         uint8_t* __restrict__ accepted) {
+                         unsigned long long* __restrict__ lock,
+                         uint8_t* __restrict__ accepted, int winner_only, int key_mode) {
   const int32_t j = blockIdx.x * kBlock + threadIdx.x;
   if (j >= m) return;
   const int32_t b = winner[j], s = second[j];
@@ -77,23 +70,19 @@ __global__ void rs_check(int32_t m, int32_t n, const int32_t* __restrict__ winne
     accepted[j] = 0;
     return;
   }
-  const unsigned long long key = signal_key(d1[j], j);
-  bool ok = lock[b] == key && lock[s] == key;
+  const unsigned long long key = signal_key(d1[j], j, key_mode);
+  bool ok = lock[b] == key;
+  if (winner_only) {
+    if (ok) lock[b] = ~0ull;
+    accepted[j] = ok ? 1 : 0;
+    return;
+  }
+  ok = ok && lock[s] == key;
   for (int32_t k = rp[b]; ok && k < rp[b + 1]; ++k) ok = lock[col[k]] == key;
   accepted[j] = ok ? 1 : 0;
 }
 
 // -------------------------------------------------------------------- adapt ----
-
-// w <- w + eps (xi - w), one binary32 rounding per operation (no contraction).
-__device__ __forceinline__ void move_unit(float* __restrict__ x, float* __restrict__ y,
-                                          float* __restrict__ z, int32_t u, float eps,
-                                          float sx, float sy, float sz) {
-  float t;
-  t = sx - x[u]; t = eps * t; x[u] = x[u] + t;
-  t = sy - y[u]; t = eps * t; y[u] = y[u] + t;
-  t = sz - z[u]; t = eps * t; z[u] = z[u] + t;
-}
 
 __global__ void ad_move(const float* __restrict__ sig, int32_t m, int32_t n,
                         const int32_t* __restrict__ winner, const int32_t* __restrict__ second,
@@ -284,15 +273,20 @@ __global__ void ed_write(int32_t n, const int32_t* __restrict__ rp,
 
 __global__ void init_state(float* __restrict__ err, int32_t* __restrict__ ins,
                            int32_t* __restrict__ orphan, int32_t* __restrict__ rp,
-                           int32_t n_max, int32_t* __restrict__ status) {
+                           unsigned long long* __restrict__ lock, int32_t* __restrict__ extra,
+                           int32_t* __restrict__ rem, int32_t n_max,
+                           int32_t* __restrict__ status) {
   const int32_t i = blockIdx.x * kBlock + threadIdx.x;
   if (i < n_max) {
     err[i] = 0.0f;
     ins[i] = -1;
     orphan[i] = 0;
+    lock[i] = ~0ull;
+    extra[i] = 0;
   }
   if (i <= n_max) rp[i] = 0;
   if (i < kStSlots) status[i] = 0;
+  if (i <= kRing) rem[i] = 0;
 }
 
 inline int blocks(int64_t n) { return static_cast<int>((n + kBlock - 1) / kBlock); }
@@ -300,20 +294,23 @@ inline int blocks(int64_t n) { return static_cast<int>((n + kBlock - 1) / kBlock
 }  // namespace
 
 hipError_t launch_init(const DevState& s, int cur, int32_t, int32_t n_max, hipStream_t st) {
-  const int64_t cover = std::max<int64_t>(static_cast<int64_t>(n_max) + 1, kStSlots);
-  init_state<<<blocks(cover), kBlock, 0, st>>>(s.err, s.ins, s.orphan, s.rp[cur], n_max,
-                                               s.status);
+  const int64_t cover =
+      std::max<int64_t>(static_cast<int64_t>(n_max) + 1, std::max<int>(kStSlots, kRing + 1));
+  init_state<<<blocks(cover), kBlock, 0, st>>>(s.err, s.ins, s.orphan, s.rp[cur], s.lock,
+                                               s.extra, s.rem, n_max, s.status);
   return hipGetLastError();
 }
 
 hipError_t launch_resolve(const DevState& s, int cur, int32_t n, int32_t m,
                           const int32_t* winner, const int32_t* second, const float* d1,
-                          uint8_t* accepted, hipStream_t st) {
-  if (n > 0) rs_clear<<<blocks(n), kBlock, 0, st>>>(s.lock, n);
+                          uint8_t* accepted, int lock_mode, int key_mode, hipStream_t st) {
+  const int wo = lock_mode == 1;
+  // the winner-lock mode keeps the lock array at all ones between calls
+  if (!wo && n > 0) rs_clear<<<blocks(n), kBlock, 0, st>>>(s.lock, n);
   rs_claim<<<blocks(m), kBlock, 0, st>>>(m, n, winner, second, d1, s.rp[cur], s.col[cur],
-                                         s.lock, s.status);
+                                         s.lock, s.status, wo, key_mode);
   rs_check<<<blocks(m), kBlock, 0, st>>>(m, n, winner, second, d1, s.rp[cur], s.col[cur],
-                                         s.lock, accepted);
+                                         s.lock, accepted, wo, key_mode);
   return hipGetLastError();
 }
 

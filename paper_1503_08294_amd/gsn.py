@@ -35,6 +35,14 @@ GSN_T_RESOLVE = 2
 GSN_T_ADAPT = 3
 GSN_T_EDGES = 4
 
+GSN_LOCK_SET = 0
+GSN_LOCK_WINNER = 1
+GSN_KEY_DIST_INDEX = 0
+GSN_KEY_INDEX = 1
+
+GSN_STAT_ROUNDS = 0
+GSN_STAT_LAUNCHED = 1
+
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
                       "(hipcc --offload-arch=gfx950); there is no fallback path")
@@ -52,6 +60,8 @@ class gsn_params(ctypes.Structure):
         ("n_max", ctypes.c_int32),
         ("e_max", ctypes.c_int32),
         ("m_max", ctypes.c_int32),
+        ("lock_mode", ctypes.c_int32),
+        ("key_mode", ctypes.c_int32),
     ]
 
 
@@ -75,6 +85,7 @@ _sig = {
     "gsn_timing_enable": (ctypes.c_int, [_P, _I]),
     "gsn_timing_read": (ctypes.c_int, [_P, _I, ctypes.POINTER(ctypes.c_double),
                                        ctypes.POINTER(_I)]),
+    "gsn_stat": (ctypes.c_int, [_P, _I, ctypes.POINTER(ctypes.c_int64)]),
 }
 for _name, (_res, _args) in _sig.items():
     _f = getattr(_lib, _name)
@@ -117,8 +128,10 @@ def _dev(t: torch.Tensor | None, dtype, n: int | None = None, what: str = "tenso
 
 
 def make_params(eps_b=0.05, eps_n=0.0006, max_age=50, err_alpha=0.5, err_beta=0.995,
-                n_max=1024, e_max=4096, m_max=1024) -> gsn_params:
-    return gsn_params(eps_b, eps_n, max_age, err_alpha, err_beta, n_max, e_max, m_max)
+                n_max=1024, e_max=4096, m_max=1024, lock_mode=GSN_LOCK_SET,
+                key_mode=GSN_KEY_DIST_INDEX) -> gsn_params:
+    return gsn_params(eps_b, eps_n, max_age, err_alpha, err_beta, n_max, e_max, m_max,
+                      lock_mode, key_mode)
 
 
 # ------------------------------------------------------------- C-named calls ----
@@ -227,6 +240,12 @@ def gsn_timing_read(net, which: int):
     return ms.value, cnt.value
 
 
+def gsn_stat(net, key: int) -> int:
+    v = ctypes.c_int64()
+    _check(_lib.gsn_stat(net, key, ctypes.byref(v)), "gsn_stat")
+    return v.value
+
+
 # ------------------------------------------------------------------ convenience ----
 
 @dataclass
@@ -329,3 +348,6 @@ class Network:
 
     def tune(self, key: int, value: int):
         gsn_tune(self.h, key, value)
+
+    def stat(self, key: int) -> int:
+        return gsn_stat(self.h, key)

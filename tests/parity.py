@@ -21,10 +21,12 @@ def oracle_threads() -> int:
 
 
 def params_pair(n_max, e_max, m_max, eps_b=0.05, eps_n=0.0006, max_age=50, err_alpha=0.5,
-                err_beta=0.995):
+                err_beta=0.995, lock_mode=0, key_mode=0):
     from paper_1503_08294_amd import gsn
-    g = gsn.make_params(eps_b, eps_n, max_age, err_alpha, err_beta, n_max, e_max, m_max)
-    o = oracle.Params(eps_b, eps_n, max_age, err_alpha, err_beta, n_max, e_max, m_max)
+    g = gsn.make_params(eps_b, eps_n, max_age, err_alpha, err_beta, n_max, e_max, m_max,
+                        lock_mode, key_mode)
+    o = oracle.Params(eps_b, eps_n, max_age, err_alpha, err_beta, n_max, e_max, m_max,
+                      lock_mode=lock_mode, key_mode=key_mode)
     return g, o
 
 
@@ -80,3 +82,30 @@ def assert_iter_equal(g, o, where=""):
     names = ("winner", "second", "d1", "d2", "accepted")
     for a, b, nm in zip(g, o, names):
         np.testing.assert_array_equal(a, b, err_msg=f"{where} {nm}")
+
+
+def run_workload(name, iterations=None, compare_every=1, n_points=None, m=None,
+                 n_units=None, **over):
+    from paper_1503_08294_amd.clouds import WORKLOADS, SignalStream
+    wl = WORKLOADS[name]
+    cloud = wl.make_cloud(n_points)
+    units = wl.make_units(cloud, n_units)
+    m = m or wl.m
+    its = iterations or wl.iterations
+    cap = wl.capacity(m)
+    kw = dict(eps_b=wl.eps_b, eps_n=wl.eps_n, max_age=wl.max_age, err_alpha=wl.err_alpha,
+              err_beta=wl.err_beta)
+    kw.update(over)
+    pair = Pair(units, n_max=max(cap["n_max"], units.shape[1]), e_max=cap["e_max"], m_max=m,
+                **kw)
+    stream = SignalStream(cloud, wl.signal_seed)
+    rejected = 0
+    for t in range(1, its + 1):
+        sig = stream.next(m)
+        g, o = pair.iterate(sig, t, wl.insert_every, wl.grow)
+        assert_iter_equal(g, o, f"{name} iteration {t}")
+        rejected += int(m - o[4].sum())
+        if t % compare_every == 0 or t == its:
+            pair.compare_state(f"{name} iteration {t}")
+    assert pair.net.check() == 0
+    return pair, rejected / (its * m)

@@ -48,8 +48,14 @@ def test_host_side_validation(lib):
     good = make_params(n_max=1000, e_max=4000, m_max=256)
     size = lib.gsn_workspace_bytes(ctypes.byref(good))
     assert size > 12 * 1000 and size % 256 == 0
+    # the winner lock needs room for one insertion at the winner and one at the second of
+    # every survivor in both adjacency buffers (col and age)
+    winner = make_params(n_max=1000, e_max=4000, m_max=256, lock_mode=1)
+    assert lib.gsn_workspace_bytes(ctypes.byref(winner)) >= size + 4 * 4 * 2 * 256
     for bad in (make_params(eps_b=1.5), make_params(eps_n=-0.1), make_params(max_age=-1),
-                make_params(n_max=1), make_params(m_max=0), make_params(e_max=-1)):
+                make_params(n_max=1), make_params(m_max=0), make_params(e_max=-1),
+                make_params(lock_mode=2), make_params(key_mode=-1),
+                make_params(lock_mode=1, e_max=2**30 - 1, m_max=2**20)):
         assert lib.gsn_workspace_bytes(ctypes.byref(bad)) == 0
     P = ctypes.c_void_p
     lib.gsn_create.argtypes = [ctypes.POINTER(gsn_params), P, ctypes.c_size_t, ctypes.c_int32,

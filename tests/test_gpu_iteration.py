@@ -5,36 +5,9 @@ positions within 1e-6 after the iterations stated."""
 import numpy as np
 import pytest
 
-from parity import Pair, assert_iter_equal
+from parity import run_workload
 
 pytestmark = pytest.mark.gpu
-
-
-def run_workload(name, iterations=None, compare_every=1, n_points=None, m=None,
-                 n_units=None, **over):
-    from paper_1503_08294_amd.clouds import WORKLOADS, SignalStream
-    wl = WORKLOADS[name]
-    cloud = wl.make_cloud(n_points)
-    units = wl.make_units(cloud, n_units)
-    m = m or wl.m
-    its = iterations or wl.iterations
-    cap = wl.capacity(m)
-    kw = dict(eps_b=wl.eps_b, eps_n=wl.eps_n, max_age=wl.max_age, err_alpha=wl.err_alpha,
-              err_beta=wl.err_beta)
-    kw.update(over)
-    pair = Pair(units, n_max=max(cap["n_max"], units.shape[1]), e_max=cap["e_max"], m_max=m,
-                **kw)
-    stream = SignalStream(cloud, wl.signal_seed)
-    rejected = 0
-    for t in range(1, its + 1):
-        sig = stream.next(m)
-        g, o = pair.iterate(sig, t, wl.insert_every, wl.grow)
-        assert_iter_equal(g, o, f"{name} iteration {t}")
-        rejected += int(m - o[4].sum())
-        if t % compare_every == 0 or t == its:
-            pair.compare_state(f"{name} iteration {t}")
-    assert pair.net.check() == 0
-    return pair, rejected / (its * m)
 
 
 def test_tiny_sphere_20_iterations():
