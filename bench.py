@@ -63,7 +63,7 @@ def load_traffic(launch_evals: int):
     return t.get("bytes_per_launch")
 
 
-def cpu_baseline(wl, units, cloud, budget_s: float):
+def cpu_baseline(wl, units, cloud, budget_s: float, lock_mode: int = 0, key_mode: int = 0):
     """The oracle on the same initial units and the same seeded signal batches as the GPU
     run, whole iterations until about budget_s seconds have passed (at most 200)."""
     import oracle
@@ -71,7 +71,8 @@ def cpu_baseline(wl, units, cloud, budget_s: float):
     threads = max(1, min(16, os.cpu_count() or 1))
     cap = wl.capacity()
     p = oracle.Params(wl.eps_b, wl.eps_n, wl.max_age, wl.err_alpha, wl.err_beta,
-                      cap["n_max"], cap["e_max"], cap["m_max"])
+                      cap["n_max"], cap["e_max"], cap["m_max"], lock_mode=lock_mode,
+                      key_mode=key_mode)
     o = oracle.Oracle(p, units, threads=threads)
     stream = SignalStream(cloud, wl.signal_seed)
     batches = [stream.next(wl.m) for _ in range(3)]
@@ -114,6 +115,11 @@ def main():
                     help="seconds of CPU oracle work for the cpu_baseline leg (0 = skip)")
     ap.add_argument("--copy-calibration", type=int, default=0,
                     help="only run a plain device copy of this many bytes")
+    ap.add_argument("--lock", choices=("set", "winner"), default="set",
+                    help="collision rule: lock set {b, s} + N(b) with one parallel update, "
+                         "or the winner alone with the survivors applied in key order")
+    ap.add_argument("--key", choices=("dist", "index"), default="dist",
+                    help="survivor priority: (winner distance, index) or the index alone")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -145,8 +151,10 @@ def main():
     torch.cuda.set_device(0)
     dev_sig = torch.from_numpy(host_sig).cuda()
     cap = wl.capacity()
+    lock_mode = gsn.GSN_LOCK_WINNER if args.lock == "winner" else gsn.GSN_LOCK_SET
+    key_mode = gsn.GSN_KEY_INDEX if args.key == "index" else gsn.GSN_KEY_DIST_INDEX
     params = gsn.make_params(wl.eps_b, wl.eps_n, wl.max_age, wl.err_alpha, wl.err_beta,
-                             cap["n_max"], cap["e_max"], cap["m_max"])
+                             cap["n_max"], cap["e_max"], cap["m_max"], lock_mode, key_mode)
     net = gsn.Network(params, torch.from_numpy(units).cuda())
 
     def step(t):
@@ -164,12 +172,16 @@ def main():
 
     print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
+    net.stat(gsn.GSN_STAT_CLEAR)
     t0 = time.perf_counter()
     for t in range(args.warmup, args.warmup + args.steps):
         step(t)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     gsn.gsn_timing_enable(net.h, False)
+    updates = net.stat(gsn.GSN_STAT_UPDATES)
+    rounds = ({"mean": net.stat(gsn.GSN_STAT_ROUNDS) / updates,
+               "max": net.stat(gsn.GSN_STAT_ROUNDS_MAX)} if updates else None)
     phase = {}
     for name, w in (("find_scan", gsn.GSN_T_FIND_SCAN), ("find", gsn.GSN_T_FIND),
                     ("resolve", gsn.GSN_T_RESOLVE), ("adapt", gsn.GSN_T_ADAPT),
@@ -204,7 +216,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "n_units": n, "m_signals": m,
                    "cloud_points": wl.n_points, "cloud": "genus-3 tube surface",
-                   "iteration": "find+resolve+adapt+update_edges", "parallelism": "single"},
+                   "iteration": "find+resolve+adapt+update_edges", "parallelism": "single",
+                   "collision": {"lock": args.lock, "key": args.key}},
         "signals_per_s": m * args.steps / elapsed,
         "fw_evals_per_s": m * n / (phase["find"] * 1e-3),
         "fw_frac_fp32_peak": FLOPS_PER_EVAL * m * n / (phase["find"] * 1e-3) / 1e12
@@ -212,6 +225,7 @@ def main():
         "phase_ms": phase,
         "conflict_rate": conflict_rate,
         "state_after": {"units": n_units, "edges": n_edges},
+        "update_rounds": rounds,
         "roofline": {"bound": "mfma", "kernel": SCAN_KERNEL, "dtype": "f16",
                      "achieved": achieved, "peak": F16_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / F16_PEAK_TFLOPS, "traffic": traffic,
@@ -225,7 +239,8 @@ def main():
     }
     if args.cpu_budget > 0:
         print(f"[bench] cpu baseline (~{args.cpu_budget:.0f} s)", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(wl, units, cloud, args.cpu_budget)
+        out["cpu_baseline"] = cpu_baseline(wl, units, cloud, args.cpu_budget, lock_mode,
+                                           key_mode)
     print(json.dumps(out), flush=True)
 
 

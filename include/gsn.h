@@ -137,8 +137,9 @@ int gsn_resolve_conflicts(gsn_net* net, int32_t m, const int32_t* winner,
  * err[b] grows by d1[j]; then err *= err_beta.  Any accepted set is valid (signals sharing
  * a winner are applied in key order too); more than e_max edges at the end set
  * GSN_E_CAPACITY on the device.  It runs in rounds (every pending signal whose units
- * {b, s} + N(b) no pending signal of smaller key touches goes in the same round) and syncs
- * once every few rounds to see whether signals are left. */
+ * {b, s} + N(b) no pending signal of smaller key touches goes in the same round); the
+ * first rounds are grid-wide launches (GSN_TUNE_GRID_ROUNDS), the rest run inside one
+ * workgroup, so the call stays async. */
 int gsn_adapt(gsn_net* net, const float* sig, int32_t m, const int32_t* winner,
               const int32_t* second, const float* d1, const uint8_t* accepted, void* stream);
 
@@ -177,7 +178,8 @@ int gsn_import(gsn_net* net, int32_t n, const float* xyz, const float* err, int3
                const int32_t* edges, void* stream);
 
 /* Sticky device status: GSN_OK, or the first GSN_E_INVAL / GSN_E_CAPACITY a kernel
- * raised since creation or the last gsn_import.  Syncs. */
+ * raised since creation or the last gsn_import (GSN_E_STATE if the winner-lock update
+ * found its lock words not cleared, which only a corrupted workspace causes).  Syncs. */
 int gsn_check(gsn_net* net, void* stream);
 
 /* Free the host handle (the workspace stays the caller's).  NULL is ignored. */
@@ -192,8 +194,11 @@ void gsn_destroy(gsn_net* net);
  *                     4 = the same screen on the matrix cores in split binary16 (every
  *                     screen carries a rigorous rounding margin; candidates are rechecked
  *                     in the binary32 direct form, so all variants return the same result)
+ *   GSN_TUNE_GRID_ROUNDS  rounds of the GSN_LOCK_WINNER update launched over the whole
+ *                     device before the remaining ones run in a single workgroup (0..16,
+ *                     default 6)
  * Returns GSN_E_INVAL for an unknown key or value. */
-enum { GSN_TUNE_SPLIT = 1, GSN_TUNE_VARIANT = 2 };
+enum { GSN_TUNE_SPLIT = 1, GSN_TUNE_VARIANT = 2, GSN_TUNE_GRID_ROUNDS = 3 };
 #define GSN_MAX_SPLIT 64
 int gsn_tune(gsn_net* net, int32_t key, int32_t value);
 
@@ -209,13 +214,16 @@ enum { GSN_T_FIND_SCAN = 0, GSN_T_FIND = 1, GSN_T_RESOLVE = 2, GSN_T_ADAPT = 3,
 int gsn_timing_enable(gsn_net* net, int32_t enable);
 int gsn_timing_read(gsn_net* net, int32_t which, double* total_ms, int32_t* launches);
 
-/* Counters of the last call, for measurement (host values, no sync).
- *   GSN_STAT_ROUNDS   rounds the last gsn_adapt with GSN_LOCK_WINNER took to apply every
- *                     accepted signal (0 in GSN_LOCK_SET mode or when none was accepted)
- *   GSN_STAT_LAUNCHED rounds it launched (rounds are launched a few at a time; those after
- *                     the last one return at once) */
-enum { GSN_STAT_ROUNDS = 0, GSN_STAT_LAUNCHED = 1 };
-int gsn_stat(gsn_net* net, int32_t key, int64_t* value);
+/* Statistics of the GSN_LOCK_WINNER updates, accumulated on the device since creation or
+ * the last GSN_STAT_CLEAR, for measurement.  Syncs.
+ *   GSN_STAT_ROUNDS      rounds summed over the updates (a round applies every pending
+ *                        survivor whose units no pending survivor of smaller key touches)
+ *   GSN_STAT_ROUNDS_MAX  the most rounds one update took
+ *   GSN_STAT_UPDATES     gsn_adapt calls that applied the winner-lock update
+ *   GSN_STAT_CLEAR       sets the three to zero (value may be NULL) */
+enum { GSN_STAT_ROUNDS = 0, GSN_STAT_ROUNDS_MAX = 1, GSN_STAT_UPDATES = 2,
+       GSN_STAT_CLEAR = 3 };
+int gsn_stat(gsn_net* net, int32_t key, int64_t* value, void* stream);
 
 #ifdef __cplusplus
 }

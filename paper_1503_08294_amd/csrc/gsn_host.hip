@@ -48,7 +48,8 @@ Layout layout_for(const gsn_params& p) {
   add(mm);                     // 19 pend
   add(4 * nm);                 // 20 len
   add(4 * nm);                 // 21 extra
-  add(4 * (kRing + 1));        // 22 rem
+  add(4 * kRmSlots);           // 22 rem
+  add(8 * mm);                 // 23 list
   L.total = (o + 255) & ~static_cast<size_t>(255);
   return L;
 }
@@ -79,6 +80,7 @@ void carve(const gsn_params& p, void* base, DevState* s) {
   s->len = reinterpret_cast<int32_t*>(b + L.off[20]);
   s->extra = reinterpret_cast<int32_t*>(b + L.off[21]);
   s->rem = reinterpret_cast<int32_t*>(b + L.off[22]);
+  s->list = reinterpret_cast<int32_t*>(b + L.off[23]);
 }
 
 }  // namespace gsn
@@ -87,7 +89,7 @@ using gsn::DevState;
 
 enum Phase { kReady = 0, kFound = 1, kResolved = 2, kAdapted = 3 };
 constexpr int kRebucketEvery = 16;
-constexpr int kFirstRoundBatch = 8;  // rounds of the winner-lock update before the first read
+constexpr int kDefaultGridRounds = 6;
 
 struct gsn_net {
   gsn_params p;
@@ -102,7 +104,7 @@ struct gsn_net {
   bool timing;
   int32_t bucket_n;            // unit count at the last spatial bucketing (-1: none yet)
   int32_t finds_since_bucket;
-  int64_t stat[2];             // GSN_STAT_ROUNDS, GSN_STAT_LAUNCHED of the last adapt
+  int grid_rounds;             // grid-wide rounds of the winner-lock update
   std::vector<hipEvent_t> pool;
   std::vector<std::pair<hipEvent_t, hipEvent_t>> rec[GSN_T_COUNT];
 };
@@ -179,45 +181,6 @@ int read_status_slot(gsn_net* net, int slot, int32_t* out, hipStream_t st) {
   return hip_ok(hipStreamSynchronize(st));
 }
 
-// The winner-lock update: survivors go in rounds (update_winner.hip); the pending counts
-// are read back after every batch of rounds, and the batches grow so that long chains of
-// colliding survivors cost few reads.
-int adapt_sequential(gsn_net* net, const float* sig, int32_t m, const int32_t* winner,
-                     const int32_t* second, const float* d1, const uint8_t* accepted,
-                     hipStream_t st) {
-  const gsn::DevState& s = net->s;
-  const int64_t slack_cap = 2 * (static_cast<int64_t>(net->p.e_max) + net->p.m_max);
-  hipError_t e = gsn::launch_winner_prologue(s, net->cur, net->n, m, winner, second, accepted,
-                                             slack_cap, st);
-  int32_t h[gsn::kRing + 1];
-  int64_t t = 0, rounds = -1;
-  int batch = kFirstRoundBatch;
-  while (e == hipSuccess && rounds < 0) {
-    e = gsn::launch_winner_rounds(s, net->cur, net->n, sig, m, winner, second, d1,
-                                  net->p.key_mode, net->p.eps_b, net->p.eps_n, net->p.max_age,
-                                  t, batch, st);
-    if (e != hipSuccess) break;
-    e = hipMemcpyAsync(h, s.rem, sizeof(h), hipMemcpyDeviceToHost, st);
-    if (e == hipSuccess) e = hipStreamSynchronize(st);
-    if (e != hipSuccess) break;
-    for (int64_t i = t; i < t + batch; ++i)
-      if (h[i % gsn::kRing] == 0) {
-        rounds = h[gsn::kRingSurvivors] > 0 ? i + 1 : 0;
-        break;
-      }
-    t += batch;
-    // every round applies the pending survivor of smallest key, so m rounds always suffice
-    if (rounds < 0 && t > static_cast<int64_t>(m) + gsn::kRing) return GSN_E_HIP;
-    batch = std::min(2 * batch, gsn::kRing - 1);
-  }
-  if (e == hipSuccess)
-    e = gsn::launch_winner_epilogue(s, net->cur, net->n, net->p.err_beta,
-                                    2 * static_cast<int64_t>(net->p.e_max), st);
-  net->stat[0] = rounds < 0 ? 0 : rounds;
-  net->stat[1] = t;
-  return hip_ok(e);
-}
-
 }  // namespace
 
 extern "C" {
@@ -248,7 +211,7 @@ int gsn_create(const gsn_params* params, void* workspace, size_t workspace_bytes
   net->timing = false;
   net->bucket_n = -1;
   net->finds_since_bucket = 0;
-  net->stat[0] = net->stat[1] = 0;
+  net->grid_rounds = kDefaultGridRounds;
   int dev = 0, cus = 256;
   if (hipGetDevice(&dev) == hipSuccess &&
       hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess)
@@ -345,14 +308,19 @@ int gsn_adapt(gsn_net* net, const float* sig, int32_t m, const int32_t* winner,
   net->phase = kAdapted;
   hipStream_t st = as_stream(stream);
   TimedRegion t(net, GSN_T_ADAPT, st);
-  int rc = net->p.lock_mode == 1 && m > 0 && net->n > 0
-               ? adapt_sequential(net, sig, m, winner, second, d1, accepted, st)
-               : hip_ok(gsn::launch_adapt(net->s, net->cur, net->n, sig, m, winner, second, d1,
-                                          accepted, net->p.eps_b, net->p.eps_n,
-                                          net->p.err_beta, st));
-  if (net->p.lock_mode != 1 || m == 0 || net->n == 0) net->stat[0] = net->stat[1] = 0;
+  hipError_t e;
+  if (net->p.lock_mode == 1 && m > 0 && net->n > 0) {
+    gsn::WinnerStep w{sig, m, winner, second, d1, accepted, net->p.key_mode, net->p.eps_b,
+                      net->p.eps_n, net->p.err_beta, net->p.max_age, net->grid_rounds,
+                      2 * (static_cast<int64_t>(net->p.e_max) + net->p.m_max),
+                      2 * static_cast<int64_t>(net->p.e_max)};
+    e = gsn::launch_winner_update(net->s, net->cur, net->n, w, st);
+  } else {
+    e = gsn::launch_adapt(net->s, net->cur, net->n, sig, m, winner, second, d1, accepted,
+                          net->p.eps_b, net->p.eps_n, net->p.err_beta, st);
+  }
   t.end();
-  return rc;
+  return hip_ok(e);
 }
 
 int gsn_update_edges(gsn_net* net, int32_t m, const int32_t* winner, const int32_t* second,
@@ -526,7 +494,7 @@ int gsn_import(gsn_net* net, int32_t n, const float* xyz, const float* err, int3
     ok = ok && hipMemset(s.orphan, 0, 4 * nm) == hipSuccess;
     ok = ok && hipMemset(s.lock, 0xff, 8 * nm) == hipSuccess;
     ok = ok && hipMemset(s.extra, 0, 4 * nm) == hipSuccess;
-    ok = ok && hipMemset(s.rem, 0, 4 * (gsn::kRing + 1)) == hipSuccess;
+    ok = ok && hipMemset(s.rem, 0, 4 * gsn::kRmSlots) == hipSuccess;
     ok = ok && hipMemset(s.status, 0, 4 * gsn::kStSlots) == hipSuccess;
     ok = ok && gsn::launch_stage_init(gsn::carve_stage(s.scr, net->p.n_max, net->p.m_max),
                                       nullptr) == hipSuccess;
@@ -571,14 +539,31 @@ int gsn_tune(gsn_net* net, int32_t key, int32_t value) {
       if (value < 0 || value > 4) return GSN_E_INVAL;
       net->tune_variant = value;
       return GSN_OK;
+    case GSN_TUNE_GRID_ROUNDS:
+      if (value < 0 || value > gsn::kMaxGridRounds) return GSN_E_INVAL;
+      net->grid_rounds = value;
+      return GSN_OK;
     default:
       return GSN_E_INVAL;
   }
 }
 
-int gsn_stat(gsn_net* net, int32_t key, int64_t* value) {
-  if (!net || !value || key < 0 || key > GSN_STAT_LAUNCHED) return GSN_E_INVAL;
-  *value = net->stat[key];
+int gsn_stat(gsn_net* net, int32_t key, int64_t* value, void* stream) {
+  if (!net || key < 0 || key > GSN_STAT_CLEAR) return GSN_E_INVAL;
+  if (key != GSN_STAT_CLEAR && !value) return GSN_E_INVAL;
+  hipStream_t st = as_stream(stream);
+  int32_t* slots = net->s.rem + gsn::kRmRounds;
+  if (key == GSN_STAT_CLEAR) {
+    const int32_t zero[3] = {0, 0, 0};
+    if (hipMemcpyAsync(slots, zero, sizeof(zero), hipMemcpyHostToDevice, st) != hipSuccess)
+      return GSN_E_HIP;
+    return hip_ok(hipStreamSynchronize(st));
+  }
+  int32_t h[3];
+  if (hipMemcpyAsync(h, slots, sizeof(h), hipMemcpyDeviceToHost, st) != hipSuccess)
+    return GSN_E_HIP;
+  if (hipStreamSynchronize(st) != hipSuccess) return GSN_E_HIP;
+  *value = key == GSN_STAT_ROUNDS ? h[0] : key == GSN_STAT_ROUNDS_MAX ? h[1] : h[2];
   return GSN_OK;
 }
 

@@ -24,11 +24,17 @@ enum StatusSlot {
   kStSlots = 16
 };
 
-// Rounds of the sequential-survivor update: counters live in a ring of kRing slots (slot
-// t % kRing counts the signals still pending after round t) plus one slot that counts the
-// survivors of the call.  At most kRing - 1 rounds are launched between two host reads.
-constexpr int kRing = 64;
-constexpr int kRingSurvivors = kRing;
+// Counters of the sequential-survivor update (int32 slots of DevState::rem): the signals
+// still pending after each grid-wide round, the survivors of the current call, and round
+// statistics accumulated until the host clears them.
+constexpr int kMaxGridRounds = 16;
+enum RoundSlot {
+  kRmSurvivors = kMaxGridRounds,
+  kRmRounds,       // rounds summed over the updates since the last clear
+  kRmRoundsMax,    // the most rounds one update took
+  kRmUpdates,      // updates since the last clear
+  kRmSlots
+};
 
 __device__ __forceinline__ void raise_error(int32_t* status, int32_t code) {
   atomicCAS(&status[kStError], 0, code);
@@ -72,10 +78,11 @@ struct DevState {
   unsigned long long* part;        // [kMaxSplit][2][m_max] per-chunk top-2 keys
   void* scr;                       // staging area of the screened scans (staging.hip)
   // sequential-survivor update (winner lock)
-  uint8_t* pend;                   // [m_max]       0 done, 1 pending, 2 applies this round
+  uint8_t* pend;                   // [m_max]       1 pending survivor, 0 otherwise
   int32_t* len;                    // [n_max]       live length of every row of the slack CSR
   int32_t* extra;                  // [n_max]       insertions a row may receive (kept zero)
-  int32_t* rem;                    // [kRing + 1]   per-round pending counts, survivors
+  int32_t* rem;                    // [kRmSlots]    round counters (RoundSlot)
+  int32_t* list;                   // [2 m_max]     pending signals of the last rounds
 };
 
 struct Layout {
@@ -154,18 +161,25 @@ hipError_t launch_edges(const DevState& s, int cur, int32_t n, int32_t m,
                         const int32_t* winner, const int32_t* second,
                         const uint8_t* accepted, int32_t max_age, int64_t half_cap,
                         hipStream_t st);
-// The sequential-survivor update (update_winner.hip).  Prologue: the slack copy of the CSR
-// in buffer cur ^ 1; rounds [t0, t0 + count); epilogue: the compact CSR back in buffer cur
-// and the error decay.  half_cap bounds the compact adjacency, slack_cap the slack copy.
-hipError_t launch_winner_prologue(const DevState& s, int cur, int32_t n, int32_t m,
-                                  const int32_t* winner, const int32_t* second,
-                                  const uint8_t* accepted, int64_t slack_cap, hipStream_t st);
-hipError_t launch_winner_rounds(const DevState& s, int cur, int32_t n, const float* sig,
-                                int32_t m, const int32_t* winner, const int32_t* second,
-                                const float* d1, int key_mode, float eps_b, float eps_n,
-                                int32_t max_age, int64_t t0, int count, hipStream_t st);
-hipError_t launch_winner_epilogue(const DevState& s, int cur, int32_t n, float beta,
-                                  int64_t half_cap, hipStream_t st);
+// The sequential-survivor update (update_winner.hip), all enqueued without a host sync:
+// the slack copy of the CSR in buffer cur ^ 1, grid_rounds grid-wide rounds, the remaining
+// rounds in one workgroup, and the compact CSR back in buffer cur with the error decay.
+// half_cap bounds the compact adjacency, slack_cap the slack copy.
+struct WinnerStep {
+  const float* sig;
+  int32_t m;
+  const int32_t* winner;
+  const int32_t* second;
+  const float* d1;
+  const uint8_t* accepted;
+  int key_mode;
+  float eps_b, eps_n, beta;
+  int32_t max_age;
+  int grid_rounds;   // 0..kMaxGridRounds
+  int64_t slack_cap, half_cap;
+};
+hipError_t launch_winner_update(const DevState& s, int cur, int32_t n, const WinnerStep& w,
+                                hipStream_t st);
 hipError_t launch_scan_blocks(int32_t* bsum, int32_t nb, int64_t cap, int32_t* out_total,
                               int32_t* status, int32_t slot, hipStream_t st);
 hipError_t launch_init(const DevState& s, int cur, int32_t n0, int32_t n_max,

@@ -17,7 +17,10 @@
 //
 // The rows are edited in place: before the rounds the CSR is copied with room for every
 // insertion the survivors can make (one per survivor at its winner and one at its second),
-// and afterwards compacted back, so no round rewrites the adjacency.
+// and afterwards compacted back, so no round rewrites the adjacency.  The first rounds,
+// which hold most of the survivors, are grid-wide launches; the few survivors left then go
+// through the remaining rounds inside one workgroup, so that the whole update is enqueued
+// without the host waiting to learn how many rounds it takes.
 #include "gsn_internal.h"
 
 namespace gsn {
@@ -100,18 +103,22 @@ __global__ void wl_prepare(int32_t m, int32_t n, const int32_t* __restrict__ win
       atomicAdd(&extra[s], 1);
     }
   }
-  wave_count(ok, &rem[kRingSurvivors]);
+  wave_count(ok, &rem[kRmSurvivors]);
 }
 
 // Row sizes for a rewrite: the live length (len, or the CSR row length when len is null)
-// plus the room asked in extra (when not null; it is cleared), and per-block sums.
+// plus the room asked in extra (when not null; it is cleared), and per-block sums.  Also
+// sets the lock words to all ones when lock is not null (they are all ones after a
+// complete update already; this keeps them so after an update that stopped on an error).
 __global__ void wl_count(int32_t n, const int32_t* __restrict__ rp,
                          const int32_t* __restrict__ len, int32_t* __restrict__ extra,
-                         int32_t* __restrict__ cnt, int32_t* __restrict__ bsum) {
+                         unsigned long long* __restrict__ lock, int32_t* __restrict__ cnt,
+                         int32_t* __restrict__ bsum) {
   __shared__ int32_t red[kBlock];
   const int32_t u = blockIdx.x * kBlock + threadIdx.x;
   int32_t c = 0;
   if (u < n) {
+    if (lock) lock[u] = ~0ull;
     c = len ? len[u] : rp[u + 1] - rp[u];
     if (extra) {
       c += extra[u];
@@ -169,173 +176,249 @@ __global__ void wl_write(int32_t n, const int32_t* __restrict__ rp,
 }
 
 // ------------------------------------------------------------------- rounds ----
-// Round t writes slot t % kRing of rem (pending after the round) and reads slot
-// (t - 1) % kRing: once a round leaves nothing pending, the later ones return at once.
 
-__global__ void wl_claim(int32_t m, const int32_t* __restrict__ winner,
-                         const int32_t* __restrict__ second, const float* __restrict__ d1,
-                         int key_mode, const uint8_t* __restrict__ pend,
-                         const int32_t* __restrict__ rp, const int32_t* __restrict__ len,
-                         const int32_t* __restrict__ col, unsigned long long* __restrict__ lock,
-                         int32_t* __restrict__ rem, int32_t slot, int32_t prev, int force) {
-  if (blockIdx.x == 0 && threadIdx.x == 0) rem[slot] = 0;
-  if (!force && rem[prev] == 0) return;
-  const int32_t j = blockIdx.x * kBlock + threadIdx.x;
-  if (j >= m || pend[j] != 1) return;
-  const int32_t b = winner[j], s = second[j];
-  const unsigned long long key = signal_key(d1[j], j, key_mode);
-  atomicMin(&lock[b], key);
-  atomicMin(&lock[s], key);
-  const int32_t r0 = rp[b], r1 = r0 + len[b];
-  for (int32_t k = r0; k < r1; ++k) atomicMin(&lock[col[k]], key);
+constexpr int kRoundBlock = 64;    // threads per workgroup of the grid-wide rounds
+constexpr int kTailBlock = 1024;   // threads of the single workgroup of the last rounds
+
+// The lock words are read and released with agent-scope atomics: the last rounds run in
+// one workgroup whose claims and checks are separated by barriers, not by kernel ends.
+__device__ __forceinline__ unsigned long long lock_read(unsigned long long* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void lock_release(unsigned long long* p) {
+  __hip_atomic_store(p, ~0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Every claimant visits each unit of F_j once and releases the units it holds; the others
-// compare the lock with their own keys, which differ from the holder's key and from all
-// ones in the index half, so the release order does not matter and the lock array is all
-// ones again afterwards.
-__global__ void wl_check(int32_t m, const int32_t* __restrict__ winner,
-                         const int32_t* __restrict__ second, const float* __restrict__ d1,
-                         int key_mode, uint8_t* __restrict__ pend,
-                         const int32_t* __restrict__ rp, const int32_t* __restrict__ len,
-                         const int32_t* __restrict__ col, unsigned long long* __restrict__ lock,
-                         int32_t* __restrict__ rem, int32_t slot, int32_t prev, int force) {
-  if (!force && rem[prev] == 0) return;
-  const int32_t j = blockIdx.x * kBlock + threadIdx.x;
-  bool left = false;
-  if (j < m && pend[j] == 1) {
-    const int32_t b = winner[j], s = second[j];
-    const unsigned long long key = signal_key(d1[j], j, key_mode);
-    bool ok = true;
-    if (lock[b] == key) lock[b] = ~0ull; else ok = false;
-    bool s_nb = false;
-    const int32_t r0 = rp[b], r1 = r0 + len[b];
-    for (int32_t k = r0; k < r1; ++k) {
-      const int32_t v = col[k];
-      s_nb |= v == s;
-      if (lock[v] == key) lock[v] = ~0ull; else ok = false;
-    }
-    if (!s_nb) {
-      if (lock[s] == key) lock[s] = ~0ull; else ok = false;
-    }
-    if (ok) pend[j] = 2;
-    left = !ok;
-  }
-  wave_count(left, &rem[slot]);
+struct RoundArgs {
+  const float* sig;
+  int32_t m;
+  const int32_t* winner;
+  const int32_t* second;
+  const float* d1;
+  int key_mode;
+  uint8_t* pend;
+  const int32_t* rp;
+  int32_t* len;
+  int32_t* col;
+  int32_t* age;
+  unsigned long long* lock;
+  float *x, *y, *z, *err;
+  int32_t* orphan;
+  int32_t* status;
+  float eps_b, eps_n;
+  int32_t max_age;
+  int32_t* rem;
+  int32_t* list;
+};
+
+// Claim F_j = {b, s} + N(b) with the key of j.
+__device__ void claim(const RoundArgs& a, int32_t j) {
+  const int32_t b = a.winner[j], s = a.second[j];
+  const unsigned long long key = signal_key(a.d1[j], j, a.key_mode);
+  atomicMin(&a.lock[b], key);
+  atomicMin(&a.lock[s], key);
+  const int32_t r0 = a.rp[b], r1 = r0 + a.len[b];
+  for (int32_t k = r0; k < r1; ++k) atomicMin(&a.lock[a.col[k]], key);
 }
 
-// The single-signal step of every survivor that holds its units (pend = 2).
-__global__ void wl_apply(const float* __restrict__ sig, int32_t m,
-                         const int32_t* __restrict__ winner,
-                         const int32_t* __restrict__ second, const float* __restrict__ d1,
-                         uint8_t* __restrict__ pend, const int32_t* __restrict__ rp,
-                         int32_t* __restrict__ len, int32_t* __restrict__ col,
-                         int32_t* __restrict__ age, float* __restrict__ x,
-                         float* __restrict__ y, float* __restrict__ z,
-                         float* __restrict__ err, int32_t* __restrict__ orphan,
-                         int32_t* __restrict__ status, float eps_b, float eps_n,
-                         int32_t max_age, const int32_t* __restrict__ rem, int32_t prev,
-                         int force) {
-  if (!force && rem[prev] == 0) return;
-  const int32_t j = blockIdx.x * kBlock + threadIdx.x;
-  if (j >= m || pend[j] != 2) return;
-  pend[j] = 0;
-  const int32_t b = winner[j], s = second[j];
-  const float sx = sig[j], sy = sig[m + j], sz = sig[2 * m + j];
+__device__ void apply(const RoundArgs& a, int32_t j);
+
+// Applies the step of j if j holds every unit of F_j; returns whether it did.  The winner
+// is checked first, and the row of b_j is read only if j holds b_j: a survivor that goes in
+// this round edits the rows of its own units only, so the row of a unit that j holds stays
+// as claimed.  A survivor that goes releases its units before its step (the others compare
+// with their own keys, which differ from the holder's and from all ones in the index half).
+// A signal that does not go keeps what it holds: those units stay in its F, because F_j
+// loses only winners of survivors that go, which j does not hold, so it claims them again
+// with the same key in the next round, and releases them when it goes.
+__device__ bool try_apply(const RoundArgs& a, int32_t j) {
+  const int32_t b = a.winner[j], s = a.second[j];
+  const unsigned long long key = signal_key(a.d1[j], j, a.key_mode);
+  if (lock_read(&a.lock[b]) != key) return false;
+  bool ok = lock_read(&a.lock[s]) == key;
+  const int32_t r0 = a.rp[b], r1 = r0 + a.len[b];
+  for (int32_t k = r0; ok && k < r1; ++k) ok = lock_read(&a.lock[a.col[k]]) == key;
+  if (!ok) return false;
+  lock_release(&a.lock[b]);
+  lock_release(&a.lock[s]);
+  for (int32_t k = r0; k < r1; ++k) lock_release(&a.lock[a.col[k]]);
+  apply(a, j);
+  return true;
+}
+
+// The single-signal step of j on the current network.
+__device__ void apply(const RoundArgs& a, int32_t j) {
+  const int32_t b = a.winner[j], s = a.second[j];
+  const int32_t m = a.m;
+  const float sx = a.sig[j], sy = a.sig[m + j], sz = a.sig[2 * m + j];
+  const int32_t* rp = a.rp;
+  int32_t* len = a.len;
+  int32_t* col = a.col;
+  int32_t* age = a.age;
   const int32_t r0 = rp[b];
   int32_t l = len[b];
   // adaptation: the winner, its neighbours before this step, and the second once
-  move_unit(x, y, z, b, eps_b, sx, sy, sz);
+  move_unit(a.x, a.y, a.z, b, a.eps_b, sx, sy, sz);
   bool s_nb = false;
   for (int32_t k = r0; k < r0 + l; ++k) {
     const int32_t v = col[k];
     s_nb |= v == s;
-    move_unit(x, y, z, v, eps_n, sx, sy, sz);
+    move_unit(a.x, a.y, a.z, v, a.eps_n, sx, sy, sz);
   }
-  if (!s_nb) move_unit(x, y, z, s, eps_n, sx, sy, sz);
+  if (!s_nb) move_unit(a.x, a.y, a.z, s, a.eps_n, sx, sy, sz);
   // aging of the edges at b, the edge {b, s} at age 0
   for (int32_t k = r0; k < r0 + l; ++k) {
     const int32_t v = col[k];
-    const int32_t a = v == s ? 0 : age[k] + 1;
-    age[k] = a;
+    const int32_t g = v == s ? 0 : age[k] + 1;
+    age[k] = g;
     const int32_t rk = slice_find(col, rp[v], rp[v] + len[v], b);
-    if (rk >= 0) age[rk] = a;
+    if (rk >= 0) age[rk] = g;
   }
   if (!s_nb) {
     if (!row_insert(rp, len, col, age, b, s, 0) || !row_insert(rp, len, col, age, s, b, 0))
-      raise_error(status, GSN_E_CAPACITY);
+      raise_error(a.status, GSN_E_CAPACITY);
   }
   // removal of the edges at b older than max_age
   l = len[b];
   int32_t w = r0;
   for (int32_t k = r0; k < r0 + l; ++k) {
     const int32_t v = col[k];
-    const int32_t a = age[k];
-    if (a > max_age) {
-      if (row_remove(rp, len, col, age, v, b) == 0 && !orphan[v]) {
-        orphan[v] = 1;
-        atomicAdd(&status[kStOrphans], 1);
+    const int32_t g = age[k];
+    if (g > a.max_age) {
+      if (row_remove(rp, len, col, age, v, b) == 0 && !a.orphan[v]) {
+        a.orphan[v] = 1;
+        atomicAdd(&a.status[kStOrphans], 1);
       }
     } else {
       col[w] = v;
-      age[w] = a;
+      age[w] = g;
       ++w;
     }
   }
   len[b] = w - r0;
-  err[b] = err[b] + d1[j];
+  a.err[b] = a.err[b] + a.d1[j];
+}
+
+// Grid-wide round t: rem[t] counts the signals left pending; a round after one that left
+// none returns at once.
+__global__ void wl_claim(RoundArgs a, int32_t t) {
+  if (blockIdx.x == 0 && threadIdx.x == 0) a.rem[t] = 0;
+  if (t > 0 && a.rem[t - 1] == 0) return;
+  const int32_t j = blockIdx.x * kRoundBlock + threadIdx.x;
+  if (j < a.m && a.pend[j] == 1) claim(a, j);
+}
+
+__global__ void wl_step(RoundArgs a, int32_t t) {
+  if (t > 0 && a.rem[t - 1] == 0) return;
+  const int32_t j = blockIdx.x * kRoundBlock + threadIdx.x;
+  bool left = false;
+  if (j < a.m && a.pend[j] == 1) {
+    if (try_apply(a, j)) a.pend[j] = 0; else left = true;
+  }
+  wave_count(left, &a.rem[t]);
+}
+
+// The remaining rounds in one workgroup: the pending signals are gathered into a list, and
+// every round claims, applies where it may and re-gathers them, with a device-scope fence
+// and a barrier between the phases.  Each round applies at least the pending signal of smallest
+// key, so the loop ends after at most as many rounds as signals were pending; a round
+// without progress ends it with an error.  Also adds this update's round count to the
+// statistics and clears the survivor count.
+__global__ __launch_bounds__(kTailBlock) void wl_tail(RoundArgs a, int32_t grid_rounds) {
+  __shared__ int32_t s_n, s_next, s_rounds;
+  const int tid = threadIdx.x;
+  if (tid == 0) {
+    const int32_t survivors = a.rem[kRmSurvivors];
+    int32_t g = 0;
+    for (int32_t t = 0; t < grid_rounds; ++t) g += (t == 0 ? survivors : a.rem[t - 1]) > 0;
+    s_rounds = g;
+    s_n = 0;
+    s_next = 0;
+  }
+  __syncthreads();
+  const bool any = grid_rounds == 0 || a.rem[grid_rounds - 1] > 0;
+  int32_t* cur = a.list;
+  int32_t* nxt = a.list + a.m;
+  if (any)
+    for (int32_t j = tid; j < a.m; j += kTailBlock)
+      if (a.pend[j] == 1) cur[atomicAdd(&s_n, 1)] = j;
+  __threadfence();
+  __syncthreads();
+  for (;;) {
+    const int32_t n = s_n;
+    if (n == 0) break;
+    for (int32_t i = tid; i < n; i += kTailBlock) claim(a, cur[i]);
+    __threadfence();
+    __syncthreads();
+    for (int32_t i = tid; i < n; i += kTailBlock) {
+      const int32_t j = cur[i];
+      if (try_apply(a, j)) a.pend[j] = 0;
+    }
+    __threadfence();
+    __syncthreads();
+    for (int32_t i = tid; i < n; i += kTailBlock) {
+      const int32_t j = cur[i];
+      if (a.pend[j] == 1) nxt[atomicAdd(&s_next, 1)] = j;
+    }
+    __threadfence();
+    __syncthreads();
+    if (tid == 0) {
+      // no progress means the lock words were not all ones on entry (a corrupted
+      // workspace): stop with an error rather than loop
+      if (s_next == n) {
+        raise_error(a.status, GSN_E_STATE);
+        s_next = 0;
+      }
+      s_n = s_next;
+      s_next = 0;
+      ++s_rounds;
+    }
+    __syncthreads();
+    int32_t* t = cur;
+    cur = nxt;
+    nxt = t;
+  }
+  if (tid == 0) {
+    a.rem[kRmSurvivors] = 0;
+    a.rem[kRmRounds] += s_rounds;
+    a.rem[kRmRoundsMax] = max(a.rem[kRmRoundsMax], s_rounds);
+    a.rem[kRmUpdates] += 1;
+  }
 }
 
 }  // namespace
 
-hipError_t launch_winner_prologue(const DevState& s, int cur, int32_t n, int32_t m,
-                                  const int32_t* winner, const int32_t* second,
-                                  const uint8_t* accepted, int64_t slack_cap, hipStream_t st) {
+hipError_t launch_winner_update(const DevState& s, int cur, int32_t n, const WinnerStep& w,
+                                hipStream_t st) {
   const int nxt = cur ^ 1;
-  wl_prepare<<<blocks(m), kBlock, 0, st>>>(m, n, winner, second, accepted, s.pend, s.extra,
-                                           s.rem, s.status);
+  const int32_t m = w.m;
   const int nb = blocks(n);
-  wl_count<<<nb, kBlock, 0, st>>>(n, s.rp[cur], nullptr, s.extra, s.cnt, s.bsum);
-  hipError_t e = launch_scan_blocks(s.bsum, nb, slack_cap, s.rp[nxt] + n, s.status, -1, st);
+  // slack copy of the adjacency
+  wl_prepare<<<blocks(m), kBlock, 0, st>>>(m, n, w.winner, w.second, w.accepted, s.pend,
+                                           s.extra, s.rem, s.status);
+  wl_count<<<nb, kBlock, 0, st>>>(n, s.rp[cur], nullptr, s.extra, nullptr, s.cnt, s.bsum);
+  hipError_t e = launch_scan_blocks(s.bsum, nb, w.slack_cap, s.rp[nxt] + n, s.status, -1, st);
   if (e != hipSuccess) return e;
   wl_write<<<nb, kBlock, 0, st>>>(n, s.rp[cur], nullptr, s.col[cur], s.age[cur], s.cnt, s.bsum,
                                   s.rp[nxt], s.col[nxt], s.age[nxt], s.len, nullptr, 1.0f,
                                   s.status);
-  return hipGetLastError();
-}
-
-hipError_t launch_winner_rounds(const DevState& s, int cur, int32_t n, const float* sig,
-                                int32_t m, const int32_t* winner, const int32_t* second,
-                                const float* d1, int key_mode, float eps_b, float eps_n,
-                                int32_t max_age, int64_t t0, int count, hipStream_t st) {
-  (void)n;
-  const int nxt = cur ^ 1;
-  const int g = blocks(m);
-  for (int i = 0; i < count; ++i) {
-    const int64_t t = t0 + i;
-    const int32_t slot = static_cast<int32_t>(t % kRing);
-    const int32_t prev = static_cast<int32_t>((t + kRing - 1) % kRing);
-    const int force = t == 0;
-    wl_claim<<<g, kBlock, 0, st>>>(m, winner, second, d1, key_mode, s.pend, s.rp[nxt], s.len,
-                                   s.col[nxt], s.lock, s.rem, slot, prev, force);
-    wl_check<<<g, kBlock, 0, st>>>(m, winner, second, d1, key_mode, s.pend, s.rp[nxt], s.len,
-                                   s.col[nxt], s.lock, s.rem, slot, prev, force);
-    wl_apply<<<g, kBlock, 0, st>>>(sig, m, winner, second, d1, s.pend, s.rp[nxt], s.len,
-                                   s.col[nxt], s.age[nxt], s.x, s.y, s.z, s.err, s.orphan,
-                                   s.status, eps_b, eps_n, max_age, s.rem, prev, force);
+  // rounds
+  RoundArgs a{w.sig,  m,          w.winner,   w.second,  w.d1,    w.key_mode, s.pend,
+              s.rp[nxt], s.len,   s.col[nxt], s.age[nxt], s.lock, s.x,        s.y,
+              s.z,    s.err,      s.orphan,   s.status,  w.eps_b, w.eps_n,    w.max_age,
+              s.rem,  s.list};
+  const int g = static_cast<int>((m + kRoundBlock - 1) / kRoundBlock);
+  for (int32_t t = 0; t < w.grid_rounds; ++t) {
+    wl_claim<<<g, kRoundBlock, 0, st>>>(a, t);
+    wl_step<<<g, kRoundBlock, 0, st>>>(a, t);
   }
-  return hipGetLastError();
-}
-
-hipError_t launch_winner_epilogue(const DevState& s, int cur, int32_t n, float beta,
-                                  int64_t half_cap, hipStream_t st) {
-  const int nxt = cur ^ 1;
-  const int nb = blocks(n);
-  wl_count<<<nb, kBlock, 0, st>>>(n, s.rp[nxt], s.len, nullptr, s.cnt, s.bsum);
-  hipError_t e = launch_scan_blocks(s.bsum, nb, half_cap, s.rp[cur] + n, s.status, -1, st);
+  wl_tail<<<1, kTailBlock, 0, st>>>(a, w.grid_rounds);
+  // compact adjacency and error decay
+  wl_count<<<nb, kBlock, 0, st>>>(n, s.rp[nxt], s.len, nullptr, s.lock, s.cnt, s.bsum);
+  e = launch_scan_blocks(s.bsum, nb, w.half_cap, s.rp[cur] + n, s.status, -1, st);
   if (e != hipSuccess) return e;
   wl_write<<<nb, kBlock, 0, st>>>(n, s.rp[nxt], s.len, s.col[nxt], s.age[nxt], s.cnt, s.bsum,
-                                  s.rp[cur], s.col[cur], s.age[cur], nullptr, s.err, beta,
+                                  s.rp[cur], s.col[cur], s.age[cur], nullptr, s.err, w.beta,
                                   s.status);
   return hipGetLastError();
 }

@@ -27,6 +27,7 @@ GSN_E_STATE = -4
 
 GSN_TUNE_SPLIT = 1
 GSN_TUNE_VARIANT = 2
+GSN_TUNE_GRID_ROUNDS = 3
 GSN_MAX_SPLIT = 64
 
 GSN_T_FIND_SCAN = 0
@@ -41,7 +42,9 @@ GSN_KEY_DIST_INDEX = 0
 GSN_KEY_INDEX = 1
 
 GSN_STAT_ROUNDS = 0
-GSN_STAT_LAUNCHED = 1
+GSN_STAT_ROUNDS_MAX = 1
+GSN_STAT_UPDATES = 2
+GSN_STAT_CLEAR = 3
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
@@ -85,7 +88,7 @@ _sig = {
     "gsn_timing_enable": (ctypes.c_int, [_P, _I]),
     "gsn_timing_read": (ctypes.c_int, [_P, _I, ctypes.POINTER(ctypes.c_double),
                                        ctypes.POINTER(_I)]),
-    "gsn_stat": (ctypes.c_int, [_P, _I, ctypes.POINTER(ctypes.c_int64)]),
+    "gsn_stat": (ctypes.c_int, [_P, _I, ctypes.POINTER(ctypes.c_int64), _P]),
 }
 for _name, (_res, _args) in _sig.items():
     _f = getattr(_lib, _name)
@@ -240,9 +243,9 @@ def gsn_timing_read(net, which: int):
     return ms.value, cnt.value
 
 
-def gsn_stat(net, key: int) -> int:
+def gsn_stat(net, key: int, stream=None) -> int:
     v = ctypes.c_int64()
-    _check(_lib.gsn_stat(net, key, ctypes.byref(v)), "gsn_stat")
+    _check(_lib.gsn_stat(net, key, ctypes.byref(v), _stream(stream)), "gsn_stat")
     return v.value
 
 
@@ -350,4 +353,4 @@ class Network:
         gsn_tune(self.h, key, value)
 
     def stat(self, key: int) -> int:
-        return gsn_stat(self.h, key)
+        return gsn_stat(self.h, key, self.stream)

@@ -29,12 +29,15 @@ def random_graph(rng, n, e):
     return np.array([[p[0] for p in pairs], [p[1] for p in pairs], ages], np.int32)
 
 
-def dense_pair(seed, n, e, m, key_mode, max_age=3, e_max=None):
+def dense_pair(seed, n, e, m, key_mode, max_age=3, e_max=None, grid_rounds=None):
+    from paper_1503_08294_amd import gsn
     rng = np.random.default_rng(seed)
     units = rng.standard_normal((3, n)).astype(np.float32)
     pair = Pair(units, n_max=n + 16, e_max=e_max if e_max is not None else 8 * n + 64,
                 m_max=m, eps_b=0.2, eps_n=0.05, max_age=max_age, lock_mode=WINNER,
                 key_mode=key_mode)
+    if grid_rounds is not None:
+        pair.net.tune(gsn.GSN_TUNE_GRID_ROUNDS, grid_rounds)
     edges = random_graph(rng, n, e)
     import torch
     pair.net.import_state(torch.from_numpy(units), None, torch.from_numpy(edges))
@@ -42,21 +45,26 @@ def dense_pair(seed, n, e, m, key_mode, max_age=3, e_max=None):
     return pair, rng
 
 
+@pytest.mark.parametrize("grid_rounds", [None, 0, 1, 16])
 @pytest.mark.parametrize("key_mode", [0, 1])
 @pytest.mark.parametrize("seed,n,e,m", [(0, 30, 40, 200), (1, 200, 500, 1_000),
                                         (2, 1_000, 2_500, 4_096), (3, 12, 0, 64)])
-def test_colliding_survivors_match_the_sequential_order(key_mode, seed, n, e, m):
-    """Few units, many signals: long chains of survivors whose units overlap."""
+def test_colliding_survivors_match_the_sequential_order(key_mode, seed, n, e, m,
+                                                        grid_rounds):
+    """Few units, many signals: long chains of survivors whose units overlap; every split
+    between grid-wide rounds and rounds inside one workgroup."""
     from paper_1503_08294_amd import gsn
-    pair, rng = dense_pair(seed, n, e, m, key_mode)
+    pair, rng = dense_pair(seed, n, e, m, key_mode, grid_rounds=grid_rounds)
     rounds = []
     for t in range(1, 9):
+        pair.net.stat(gsn.GSN_STAT_CLEAR)
         sig = rng.standard_normal((3, m)).astype(np.float32)
         g, o = pair.iterate(sig, t, 4, True)
         assert_iter_equal(g, o, f"iteration {t}")
         exact_state(pair, f"iteration {t}")
+        assert pair.net.stat(gsn.GSN_STAT_UPDATES) == 1
         rounds.append(pair.net.stat(gsn.GSN_STAT_ROUNDS))
-        assert pair.net.stat(gsn.GSN_STAT_LAUNCHED) >= rounds[-1]
+        assert pair.net.stat(gsn.GSN_STAT_ROUNDS_MAX) == rounds[-1]
     assert pair.net.check() == 0
     assert max(rounds) >= 2            # survivors did collide
 
@@ -82,7 +90,8 @@ def test_genus3_200k_3_iterations(key_mode):
                               key_mode=key_mode)
     exact_state(pair, "genus3 end")
     assert 0.0 < rate < 0.5
-    assert pair.net.stat(gsn.GSN_STAT_ROUNDS) >= 1
+    assert pair.net.stat(gsn.GSN_STAT_UPDATES) == 3
+    assert pair.net.stat(gsn.GSN_STAT_ROUNDS) >= 3
 
 
 def test_index_keys_with_the_lock_set_rule():
