@@ -308,12 +308,99 @@ __global__ void wl_claim(RoundArgs a, int32_t t) {
   if (j < a.m && a.pend[j] == 1) claim(a, j);
 }
 
+// The same with a group of kGroup lanes of one wave per signal: lane q takes the q-th
+// neighbour of b (ownership, release, its move, the mirror age or its removal), and the
+// row of b is rebuilt from ballots over the group.  Rows longer than kGroup go through
+// try_apply on the group's first lane.  Every lane of the group calls it with the same j;
+// the result is the same on all of them.
+constexpr int kGroup = 8;
+
+__device__ __forceinline__ uint32_t group_bits(unsigned long long wave_mask) {
+  const int base = static_cast<int>(threadIdx.x & 63) & ~(kGroup - 1);
+  return static_cast<uint32_t>(wave_mask >> base) & ((1u << kGroup) - 1);
+}
+
+__device__ bool group_try_apply(const RoundArgs& a, int32_t j, int q) {
+  const int32_t b = a.winner[j], s = a.second[j];
+  const unsigned long long key = signal_key(a.d1[j], j, a.key_mode);
+  if (lock_read(&a.lock[b]) != key) return false;
+  const int32_t r0 = a.rp[b], l = a.len[b];
+  if (l > kGroup) {
+    int applied = 0;
+    if (q == 0) applied = try_apply(a, j);
+    return __shfl(applied, static_cast<int>(threadIdx.x & 63) & ~(kGroup - 1)) != 0;
+  }
+  const bool has = q < l;
+  int32_t v = -1, a_old = 0;
+  if (has) {
+    v = a.col[r0 + q];
+    a_old = a.age[r0 + q];
+  }
+  bool mine = !has || lock_read(&a.lock[v]) == key;
+  if (q == 0) mine = mine && lock_read(&a.lock[s]) == key;
+  if (group_bits(__ballot(!mine)) != 0) return false;
+  // j holds F_j: release it, then the step
+  if (has) lock_release(&a.lock[v]);
+  if (q == 0) {
+    lock_release(&a.lock[b]);
+    lock_release(&a.lock[s]);
+  }
+  const int32_t m = a.m;
+  const float sx = a.sig[j], sy = a.sig[m + j], sz = a.sig[2 * m + j];
+  const bool is_s = has && v == s;
+  const bool new_s = group_bits(__ballot(is_s)) == 0;
+  if (q == 0) {
+    move_unit(a.x, a.y, a.z, b, a.eps_b, sx, sy, sz);
+    if (new_s) move_unit(a.x, a.y, a.z, s, a.eps_n, sx, sy, sz);
+  }
+  if (has) move_unit(a.x, a.y, a.z, v, a.eps_n, sx, sy, sz);
+  const int32_t g = is_s ? 0 : a_old + 1;
+  const bool keep = has && g <= a.max_age;
+  if (keep) {
+    const int32_t rk = slice_find(a.col, a.rp[v], a.rp[v] + a.len[v], b);
+    if (rk >= 0) a.age[rk] = g;
+  } else if (has) {
+    if (row_remove(a.rp, a.len, a.col, a.age, v, b) == 0 && !a.orphan[v]) {
+      a.orphan[v] = 1;
+      atomicAdd(&a.status[kStOrphans], 1);
+    }
+  }
+  // the row of b: kept entries in order, with s at its place if the edge is new
+  const uint32_t kept_mask = group_bits(__ballot(keep));
+  const uint32_t below_s = group_bits(__ballot(keep && v < s));
+  const int32_t kept = __popc(kept_mask);
+  const bool ins = new_s && kept + 1 <= a.rp[b + 1] - r0;
+  if (keep) {
+    const int32_t pos = __popc(kept_mask & ((1u << q) - 1)) + (ins && s < v ? 1 : 0);
+    a.col[r0 + pos] = v;
+    a.age[r0 + pos] = g;
+  }
+  if (q == 0) {
+    if (ins) {
+      const int32_t ps = __popc(below_s);
+      a.col[r0 + ps] = s;
+      a.age[r0 + ps] = 0;
+    }
+    if (new_s && (!ins || !row_insert(a.rp, a.len, a.col, a.age, s, b, 0)))
+      raise_error(a.status, GSN_E_CAPACITY);
+    a.len[b] = kept + (ins ? 1 : 0);
+    a.err[b] = a.err[b] + a.d1[j];
+  }
+  return true;
+}
+
 __global__ void wl_step(RoundArgs a, int32_t t) {
   if (t > 0 && a.rem[t - 1] == 0) return;
-  const int32_t j = blockIdx.x * kRoundBlock + threadIdx.x;
+  const int32_t gt = blockIdx.x * kRoundBlock + threadIdx.x;
+  const int32_t j = gt / kGroup;
+  const int q = gt % kGroup;
   bool left = false;
   if (j < a.m && a.pend[j] == 1) {
-    if (try_apply(a, j)) a.pend[j] = 0; else left = true;
+    if (group_try_apply(a, j, q)) {
+      if (q == 0) a.pend[j] = 0;
+    } else {
+      left = q == 0;
+    }
   }
   wave_count(left, &a.rem[t]);
 }
@@ -350,9 +437,9 @@ __global__ __launch_bounds__(kTailBlock) void wl_tail(RoundArgs a, int32_t grid_
     for (int32_t i = tid; i < n; i += kTailBlock) claim(a, cur[i]);
     __threadfence();
     __syncthreads();
-    for (int32_t i = tid; i < n; i += kTailBlock) {
+    for (int32_t i = tid / kGroup; i < n; i += kTailBlock / kGroup) {
       const int32_t j = cur[i];
-      if (try_apply(a, j)) a.pend[j] = 0;
+      if (group_try_apply(a, j, tid % kGroup) && tid % kGroup == 0) a.pend[j] = 0;
     }
     __threadfence();
     __syncthreads();
@@ -408,9 +495,11 @@ hipError_t launch_winner_update(const DevState& s, int cur, int32_t n, const Win
               s.z,    s.err,      s.orphan,   s.status,  w.eps_b, w.eps_n,    w.max_age,
               s.rem,  s.list};
   const int g = static_cast<int>((m + kRoundBlock - 1) / kRoundBlock);
+  const int gs = static_cast<int>((static_cast<int64_t>(m) * kGroup + kRoundBlock - 1) /
+                                  kRoundBlock);
   for (int32_t t = 0; t < w.grid_rounds; ++t) {
     wl_claim<<<g, kRoundBlock, 0, st>>>(a, t);
-    wl_step<<<g, kRoundBlock, 0, st>>>(a, t);
+    wl_step<<<gs, kRoundBlock, 0, st>>>(a, t);
   }
   wl_tail<<<1, kTailBlock, 0, st>>>(a, w.grid_rounds);
   // compact adjacency and error decay
