@@ -84,13 +84,17 @@ __device__ __forceinline__ void wave_count(bool pred, int32_t* ctr) {
 
 // ----------------------------------------------------------------- prologue ----
 
-// Survivors (pend = 1), the insertions each row may receive, and the survivor count.
+// Survivors (pend = 1), the insertions each row may receive, the survivor count, and the
+// claims of the first round, made on the compact rows (the slack copy holds the same rows).
 __global__ void wl_prepare(int32_t m, int32_t n, const int32_t* __restrict__ winner,
-                           const int32_t* __restrict__ second,
-                           const uint8_t* __restrict__ accepted, uint8_t* __restrict__ pend,
+                           const int32_t* __restrict__ second, const float* __restrict__ d1,
+                           const uint8_t* __restrict__ accepted, int key_mode,
+                           const int32_t* __restrict__ rp, const int32_t* __restrict__ col,
+                           unsigned long long* __restrict__ lock, uint8_t* __restrict__ pend,
                            int32_t* __restrict__ extra, int32_t* __restrict__ rem,
                            int32_t* __restrict__ status) {
   const int32_t j = blockIdx.x * kBlock + threadIdx.x;
+  if (j == 0) rem[0] = 0;
   bool ok = false;
   if (j < m) {
     const bool a = accepted[j] != 0;
@@ -101,6 +105,10 @@ __global__ void wl_prepare(int32_t m, int32_t n, const int32_t* __restrict__ win
     if (ok) {
       atomicAdd(&extra[b], 1);
       atomicAdd(&extra[s], 1);
+      const unsigned long long key = signal_key(d1[j], j, key_mode);
+      atomicMin(&lock[b], key);
+      atomicMin(&lock[s], key);
+      for (int32_t k = rp[b]; k < rp[b + 1]; ++k) atomicMin(&lock[col[k]], key);
     }
   }
   wave_count(ok, &rem[kRmSurvivors]);
@@ -481,7 +489,8 @@ hipError_t launch_winner_update(const DevState& s, int cur, int32_t n, const Win
   const int32_t m = w.m;
   const int nb = blocks(n);
   // slack copy of the adjacency
-  wl_prepare<<<blocks(m), kBlock, 0, st>>>(m, n, w.winner, w.second, w.accepted, s.pend,
+  wl_prepare<<<blocks(m), kBlock, 0, st>>>(m, n, w.winner, w.second, w.d1, w.accepted,
+                                           w.key_mode, s.rp[cur], s.col[cur], s.lock, s.pend,
                                            s.extra, s.rem, s.status);
   wl_count<<<nb, kBlock, 0, st>>>(n, s.rp[cur], nullptr, s.extra, nullptr, s.cnt, s.bsum);
   hipError_t e = launch_scan_blocks(s.bsum, nb, w.slack_cap, s.rp[nxt] + n, s.status, -1, st);
@@ -498,7 +507,8 @@ hipError_t launch_winner_update(const DevState& s, int cur, int32_t n, const Win
   const int gs = static_cast<int>((static_cast<int64_t>(m) * kGroup + kRoundBlock - 1) /
                                   kRoundBlock);
   for (int32_t t = 0; t < w.grid_rounds; ++t) {
-    wl_claim<<<g, kRoundBlock, 0, st>>>(a, t);
+    // the first round's claims were made with the survivors
+    if (t > 0) wl_claim<<<g, kRoundBlock, 0, st>>>(a, t);
     wl_step<<<gs, kRoundBlock, 0, st>>>(a, t);
   }
   wl_tail<<<1, kTailBlock, 0, st>>>(a, w.grid_rounds);
