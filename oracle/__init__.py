@@ -59,6 +59,48 @@ class Params:
                        self.n_max, self.e_max, self.m_max, self.lock_mode, self.key_mode)
 
 
+class _Schedule(ctypes.Structure):
+    _fields_ = [
+        ("m_cap", ctypes.c_int32),
+        ("fixed_m", ctypes.c_int32),
+        ("insert_every", ctypes.c_int64),
+        ("qe_window", ctypes.c_int64),
+        ("max_signals", ctypes.c_int64),
+        ("qe_threshold", ctypes.c_float),
+        ("seed", ctypes.c_uint64),
+    ]
+
+
+class _ScheduleResult(ctypes.Structure):
+    _fields_ = [
+        ("iterations", ctypes.c_int64),
+        ("signals", ctypes.c_int64),
+        ("accepted", ctypes.c_int64),
+        ("inserted", ctypes.c_int64),
+        ("qe", ctypes.c_double),
+        ("converged", ctypes.c_int32),
+        ("n_units", ctypes.c_int32),
+        ("n_edges", ctypes.c_int64),
+    ]
+
+
+@dataclass
+class Schedule:
+    """The growing-network schedule (Sec. 3.1 level of parallelism, GNG insertion, stop on
+    the quantization error); see the header of gsn_oracle.c."""
+    m_cap: int = 8192
+    fixed_m: int = 0
+    insert_every: int = 100
+    qe_window: int = 8192
+    max_signals: int = 1 << 20
+    qe_threshold: float = 0.0
+    seed: int = 0
+
+    def c(self) -> _Schedule:
+        return _Schedule(self.m_cap, self.fixed_m, self.insert_every, self.qe_window,
+                         self.max_signals, self.qe_threshold, self.seed)
+
+
 _lib = None
 
 
@@ -85,12 +127,28 @@ def _load():
     lib.orc_export.argtypes = [P, P, P, P, P]
     lib.orc_import.argtypes = [P, i32, P, P, i32, P]
     lib.orc_age.argtypes = [P, i32, i32]
+    lib.orc_splitmix64.argtypes = [ctypes.c_uint64, ctypes.c_uint64]
+    lib.orc_splitmix64.restype = ctypes.c_uint64
+    lib.orc_schedule_m.argtypes = [i32, i32, i32]
+    lib.orc_schedule_m.restype = i32
+    lib.orc_run_schedule.argtypes = [P, P, ctypes.c_int64, ctypes.POINTER(_Schedule),
+                                     ctypes.POINTER(_ScheduleResult), i32]
+    lib.orc_run_schedule.restype = ctypes.c_int
     for f in ("orc_create", "orc_find_winners", "orc_resolve_conflicts", "orc_adapt",
               "orc_update_edges", "orc_grow", "orc_sizes", "orc_status", "orc_export",
               "orc_import", "orc_age"):
         getattr(lib, f).restype = ctypes.c_int
     _lib = lib
     return lib
+
+
+def splitmix64(seed: int, counter: int) -> int:
+    """Output number `counter` (1, 2, ...) of SplitMix64 started at `seed`."""
+    return int(_load().orc_splitmix64(seed & (2**64 - 1), counter & (2**64 - 1)))
+
+
+def schedule_m(n: int, m_cap: int, fixed_m: int = 0) -> int:
+    return int(_load().orc_schedule_m(n, m_cap, fixed_m))
 
 
 def _ptr(a: np.ndarray | None):
@@ -229,3 +287,12 @@ class Oracle:
 
     def age(self, u: int, v: int) -> int:
         return _load().orc_age(self._h, int(u), int(v))
+
+    def run_schedule(self, cloud, schedule: Schedule) -> dict:
+        """Whole iterations under the growing-network schedule from the current state."""
+        c = _soa(cloud)
+        r = _ScheduleResult()
+        _check(_load().orc_run_schedule(self._h, _ptr(c), c.shape[1],
+                                        ctypes.byref(schedule.c()), ctypes.byref(r),
+                                        self.threads), "orc_run_schedule")
+        return {f: getattr(r, f) for f, _ in _ScheduleResult._fields_}

@@ -58,6 +58,22 @@
  * In this mode adapt performs the whole update and update_edges has nothing left to do.
  * key_mode 1 keys a signal by its index alone (arrival order), 0 by (bits(d1) << 32) | j.
  *
+ * The growing-network schedule (orc_run_schedule) drives whole iterations the way the
+ * paper's runs do (Sec. 3.1): starting from the current network, the level of parallelism
+ * of every iteration is the smallest power of two greater than the number of units, capped;
+ * units are inserted GNG-style every insert_every signals (Sec. 2.1: insertion at regular
+ * intervals near the unit of largest error), several in one iteration when it drew that
+ * many signals; the run stops on a threshold on the quantization error, the mean squared
+ * distance between the signals and their winners (Sec. 2.1, convergence criterion).
+ * Readings: signals are drawn from a point cloud by SplitMix64 (a counter-based generator
+ * with a published definition: output c of seed s mixes s + c * 0x9E3779B97F4A7C15), the
+ * c-th signal of the run (c = 1, 2, ...) takes point ((output_c >> 32) * P) >> 32; the
+ * error is tested on windows of at least qe_window signals (whole iterations), each d1
+ * counted as the integer floor(d1 * 2^32) (capped at 2^44 for d1 >= 4096) so that the sum
+ * is exact and does not depend on its order; a window's mean is
+ * (double)sum * 2^-32 / (double)count.  Per iteration: draw, find, resolve, adapt, update
+ * edges, accumulate, remove orphaned units, insert, then the window test and the signal cap.
+ *
  * Build: gcc -O2 -ffp-contract=off -fopenmp -shared -fPIC (no -ffast-math, no -march).
  */
 #include <stdint.h>
@@ -633,3 +649,117 @@ int orc_import(orc_net* g, int32_t n, const float* xyz, const float* err, int32_
 }
 
 int orc_age(const orc_net* g, int32_t u, int32_t v) { return g ? get_age(g, u, v) : -1; }
+
+/* ---------------------------------------------------------------- schedule --- */
+
+typedef struct {
+  int32_t m_cap;         /* largest level of parallelism */
+  int32_t fixed_m;       /* > 0: this m every iteration instead of the power-of-two rule */
+  int64_t insert_every;  /* signals between two insertions; 0 = none */
+  int64_t qe_window;     /* signals per stop test */
+  int64_t max_signals;   /* stop once this many signals were drawn */
+  float qe_threshold;    /* stop when a window's mean is below it */
+  uint64_t seed;
+} orc_schedule;
+
+typedef struct {
+  int64_t iterations, signals, accepted, inserted;
+  double qe;             /* the last complete window's mean (the partial one if none) */
+  int32_t converged, n_units;
+  int64_t n_edges;
+} orc_schedule_result;
+
+/* Output number `counter` (1, 2, ...) of SplitMix64 started at `seed`. */
+uint64_t orc_splitmix64(uint64_t seed, uint64_t counter) {
+  uint64_t z = seed + counter * 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+/* The smallest power of two greater than n, capped at m_cap (Sec. 3.1); fixed_m if > 0. */
+int32_t orc_schedule_m(int32_t n, int32_t m_cap, int32_t fixed_m) {
+  if (fixed_m > 0) return fixed_m;
+  int64_t m = 1;
+  while (m <= n) m *= 2;
+  return m > m_cap ? m_cap : (int32_t)m;
+}
+
+static uint64_t qe_units(float d1) {
+  if (d1 < 4096.0f) return (uint64_t)(d1 * 4294967296.0f);
+  return (uint64_t)1 << 44;  /* also +inf and NaN */
+}
+
+int orc_run_schedule(orc_net* g, const float* cloud, int64_t n_points, const orc_schedule* s,
+                     orc_schedule_result* r, int threads) {
+  if (!g || !cloud || !s || !r) return ORC_E_INVAL;
+  if (n_points < 1 || n_points > 0xFFFFFFFFll) return ORC_E_INVAL;
+  if (s->m_cap < 1 || s->m_cap > g->p.m_max || s->fixed_m < 0 || s->fixed_m > g->p.m_max)
+    return ORC_E_INVAL;
+  if (s->insert_every < 0 || s->qe_window < 1 || s->max_signals < 1) return ORC_E_INVAL;
+  const int32_t mm = s->fixed_m > 0 ? s->fixed_m : s->m_cap;
+  if (s->qe_window + mm > ((int64_t)1 << 19)) return ORC_E_INVAL;
+  memset(r, 0, sizeof(*r));
+  const size_t cap = (size_t)mm;
+  float* sig = (float*)malloc(sizeof(float) * 3 * cap);
+  int32_t* w = (int32_t*)malloc(sizeof(int32_t) * cap);
+  int32_t* sc = (int32_t*)malloc(sizeof(int32_t) * cap);
+  float* d1 = (float*)malloc(sizeof(float) * cap);
+  float* d2 = (float*)malloc(sizeof(float) * cap);
+  uint8_t* acc = (uint8_t*)malloc(cap);
+  int rc = ORC_OK;
+  if (!sig || !w || !sc || !d1 || !d2 || !acc) rc = ORC_E_CAPACITY;
+  uint64_t wsum = 0;
+  int64_t wcount = 0;
+  int have_qe = 0;
+  while (rc == ORC_OK) {
+    if (g->n < 2) { rc = ORC_E_STATE; break; }
+    const int32_t m = orc_schedule_m(g->n, s->m_cap, s->fixed_m);
+    for (int32_t j = 0; j < m; ++j) {
+      const uint64_t z = orc_splitmix64(s->seed, (uint64_t)(r->signals + j + 1));
+      const int64_t i = (int64_t)(((z >> 32) * (uint64_t)n_points) >> 32);
+      sig[j] = cloud[i];
+      sig[m + j] = cloud[n_points + i];
+      sig[2 * (size_t)m + j] = cloud[2 * n_points + i];
+    }
+    if ((rc = orc_find_winners(g, sig, m, w, sc, d1, d2, threads)) != ORC_OK) break;
+    if ((rc = orc_resolve_conflicts(g, m, w, sc, d1, acc)) != ORC_OK) break;
+    if ((rc = orc_adapt(g, sig, m, w, sc, d1, acc)) != ORC_OK) break;
+    if ((rc = orc_update_edges(g, m, w, sc, acc)) != ORC_OK) break;
+    for (int32_t j = 0; j < m; ++j) {
+      wsum += qe_units(d1[j]);
+      r->accepted += acc[j];
+    }
+    r->signals += m;
+    wcount += m;
+    r->iterations += 1;
+    if ((rc = remove_orphans(g)) != ORC_OK) break;
+    const int64_t k = s->insert_every > 0
+                          ? r->signals / s->insert_every - (r->signals - m) / s->insert_every
+                          : 0;
+    for (int64_t i = 0; i < k && rc == ORC_OK; ++i) {
+      const int32_t before = g->n;
+      rc = insert_unit(g);
+      if (g->n == before) break;
+      r->inserted += 1;
+    }
+    if (rc != ORC_OK) break;
+    if (wcount >= s->qe_window) {
+      r->qe = (double)wsum * 0x1p-32 / (double)wcount;
+      have_qe = 1;
+      wsum = 0;
+      wcount = 0;
+      if (r->qe < (double)s->qe_threshold) {
+        r->converged = 1;
+        break;
+      }
+    }
+    if (r->signals >= s->max_signals) break;
+  }
+  if (rc == ORC_OK && !have_qe && wcount > 0) r->qe = (double)wsum * 0x1p-32 / (double)wcount;
+  r->n_units = g->n;
+  r->n_edges = g->n_edges;
+  free(sig); free(w); free(sc); free(d1); free(d2); free(acc);
+  if (rc != ORC_OK && rc != ORC_E_STATE) g->status = rc;
+  return rc;
+}
