@@ -163,6 +163,47 @@ int gsn_update_edges(gsn_net* net, int32_t m, const int32_t* winner, const int32
  * 0, err_q and err_f are multiplied by err_alpha and err_r = err_q.  Syncs. */
 int gsn_grow(gsn_net* net, int32_t iteration, int32_t insert_every, void* stream);
 
+/* Growing-network schedule: whole iterations the way the paper's runs drive them (Sec.
+ * 3.1: the level of parallelism m of every iteration is the smallest power of two greater
+ * than the current N, capped at m_cap, the paper's cap being 8192; Sec. 2.1: GNG insertion
+ * at regular intervals, stop on a threshold on the quantization error, the mean squared
+ * distance between signals and their winners).  Per iteration, on the device: draw m
+ * signals from the cloud, find winners, resolve, adapt, update edges (the handle's collision
+ * rule), add the winners' squared distances to the error window, remove orphaned units, and
+ * insert k units one after another (GNG rule of gsn_grow), where k is the number of
+ * multiples of insert_every passed by the signal count in this iteration.  Then, once the
+ * window holds at least qe_window signals, its mean is tested against qe_threshold and the
+ * window restarts; the run also stops once max_signals signals were drawn.
+ * Signals: the c-th signal of the run (c = 1, 2, ...) is cloud point
+ * ((z >> 32) * n_points) >> 32 with z = SplitMix64 output c of `seed` (the mix of
+ * seed + c * 0x9E3779B97F4A7C15, Steele, Lea and Flood, 2014).  The error window counts
+ * each d1 as the integer floor(d1 * 2^32) (2^44 from d1 >= 4096 on, also for inf and NaN),
+ * so its sum is exact in any order; its mean is (double)sum * 2^-32 / (double)count. */
+typedef struct gsn_schedule {
+  int32_t m_cap;          /* largest m, 1..m_max */
+  int32_t fixed_m;        /* 0: the power-of-two rule; > 0 (<= m_max): this m every iteration */
+  int64_t insert_every;   /* signals between two insertions, >= 0 (0: no insertion) */
+  int64_t qe_window;      /* signals per stop test, >= 1; qe_window + largest m <= 2^19 */
+  int64_t max_signals;    /* >= 1 */
+  float qe_threshold;     /* stop at the first window whose mean is below it */
+  uint64_t seed;
+} gsn_schedule;
+
+typedef struct gsn_schedule_result {
+  int64_t iterations, signals, accepted, inserted;
+  double qe;              /* mean of the last complete window (of the partial one if none) */
+  int32_t converged;      /* 1 if the run stopped on the threshold */
+  int32_t n_units;
+  int64_t n_edges;
+} gsn_schedule_result;
+
+/* Runs the schedule from the current network (N >= 2) on cloud (device SoA [3][n_points]
+ * binary32, 1 <= n_points < 2^32), continuing the handle's state; the per-iteration buffers
+ * are in the workspace.  Must be called between iterations (GSN_E_STATE otherwise, or if N
+ * falls below 2).  Syncs (every iteration: growth reads the unit count). */
+int gsn_run_schedule(gsn_net* net, const float* cloud, int64_t n_points,
+                     const gsn_schedule* schedule, gsn_schedule_result* result, void* stream);
+
 /* Current unit count N and undirected edge count.  Syncs. */
 int gsn_sizes(gsn_net* net, int32_t* n_units, int32_t* n_edges, void* stream);
 
@@ -214,15 +255,18 @@ enum { GSN_T_FIND_SCAN = 0, GSN_T_FIND = 1, GSN_T_RESOLVE = 2, GSN_T_ADAPT = 3,
 int gsn_timing_enable(gsn_net* net, int32_t enable);
 int gsn_timing_read(gsn_net* net, int32_t which, double* total_ms, int32_t* launches);
 
-/* Statistics of the GSN_LOCK_WINNER updates, accumulated on the device since creation or
- * the last GSN_STAT_CLEAR, for measurement.  Syncs.
- *   GSN_STAT_ROUNDS      rounds summed over the updates (a round applies every pending
- *                        survivor whose units no pending survivor of smaller key touches)
- *   GSN_STAT_ROUNDS_MAX  the most rounds one update took
+/* Statistics accumulated on the device since creation or the last GSN_STAT_CLEAR, for
+ * measurement.  Syncs.
+ *   GSN_STAT_ROUNDS      rounds summed over the GSN_LOCK_WINNER updates (a round applies
+ *                        every pending survivor whose units no pending survivor of smaller
+ *                        key touches)
+ *   GSN_STAT_ROUNDS_MAX  the most rounds one such update took
  *   GSN_STAT_UPDATES     gsn_adapt calls that applied the winner-lock update
- *   GSN_STAT_CLEAR       sets the three to zero (value may be NULL) */
+ *   GSN_STAT_CLEAR       sets every statistic to zero (value may be NULL)
+ *   GSN_STAT_RESOLVED    signals that went through gsn_resolve_conflicts
+ *   GSN_STAT_ACCEPTED    of those, the accepted ones */
 enum { GSN_STAT_ROUNDS = 0, GSN_STAT_ROUNDS_MAX = 1, GSN_STAT_UPDATES = 2,
-       GSN_STAT_CLEAR = 3 };
+       GSN_STAT_CLEAR = 3, GSN_STAT_RESOLVED = 4, GSN_STAT_ACCEPTED = 5 };
 int gsn_stat(gsn_net* net, int32_t key, int64_t* value, void* stream);
 
 #ifdef __cplusplus

@@ -118,44 +118,15 @@ __device__ void replace_in_row(const int32_t* __restrict__ rp, int32_t* __restri
   age[r1 - 1] = 0;
 }
 
-__global__ __launch_bounds__(1024) void gr_insert(int32_t n, float alpha, int64_t half_cap,
-                                                  int32_t* __restrict__ rp,
-                                                  int32_t* __restrict__ col,
-                                                  int32_t* __restrict__ age,
-                                                  float* __restrict__ x, float* __restrict__ y,
-                                                  float* __restrict__ z,
-                                                  float* __restrict__ err,
-                                                  int32_t* __restrict__ status) {
-  __shared__ float be[1024];
-  __shared__ int32_t bi[1024];
-  const int32_t t = threadIdx.x;
-  float e = -__builtin_huge_valf();
-  int32_t idx = -1;
-  for (int32_t i = t; i < n; i += 1024) {
-    const float v = err[i];
-    if (idx < 0 || v > e) {  // ascending i per lane: strict > keeps the lower index
-      e = v;
-      idx = i;
-    }
-  }
-  be[t] = e;
-  bi[t] = idx;
-  __syncthreads();
-  for (int w = 512; w > 0; w >>= 1) {
-    if (t < w) {
-      const float oe = be[t + w];
-      const int32_t oi = bi[t + w];
-      if (oi >= 0 && (bi[t] < 0 || oe > be[t] || (oe == be[t] && oi < bi[t]))) {
-        be[t] = oe;
-        bi[t] = oi;
-      }
-    }
-    __syncthreads();
-  }
-  if (t != 0) return;
-  status[kStInserted] = 0;
-  const int32_t q = bi[0];
-  if (q < 0 || rp[q + 1] == rp[q]) return;
+// One GNG insertion at unit index n (thread 0 only): q = argmax err (given), f = argmax err
+// over the neighbours of q, r = n at the midpoint, {q, f} replaced by {q, r} and {r, f}.
+// Returns 1 if a unit was added.
+__device__ int insert_one(int32_t n, int32_t q, float alpha, int64_t half_cap,
+                          int32_t* __restrict__ rp, int32_t* __restrict__ col,
+                          int32_t* __restrict__ age, float* __restrict__ x,
+                          float* __restrict__ y, float* __restrict__ z,
+                          float* __restrict__ err, int32_t* __restrict__ status) {
+  if (q < 0 || rp[q + 1] == rp[q]) return 0;
   int32_t f = col[rp[q]];
   for (int32_t k = rp[q] + 1; k < rp[q + 1]; ++k) {
     const int32_t v = col[k];
@@ -164,7 +135,7 @@ __global__ __launch_bounds__(1024) void gr_insert(int32_t n, float alpha, int64_
   const int32_t e2 = rp[n];
   if (static_cast<int64_t>(e2) + 2 > half_cap) {
     atomicCAS(&status[kStError], 0, GSN_E_CAPACITY);
-    return;
+    return 0;
   }
   const int32_t r = n;
   x[r] = (x[q] + x[f]) * 0.5f;
@@ -180,7 +151,60 @@ __global__ __launch_bounds__(1024) void gr_insert(int32_t n, float alpha, int64_
   err[q] = err[q] * alpha;
   err[f] = err[f] * alpha;
   err[r] = err[q];
-  status[kStInserted] = 1;
+  return 1;
+}
+
+// Up to `count` insertions one after another (each sees the errors and edges the previous
+// one left), while N < n_max and the unit of largest error has a neighbour.  One workgroup:
+// the argmax is a block reduction, the edge surgery runs on thread 0, and a device-scope
+// fence and a barrier separate the insertions.
+__global__ __launch_bounds__(1024) void gr_insert(int32_t n0, int32_t count, int32_t n_max,
+                                                  float alpha, int64_t half_cap,
+                                                  int32_t* __restrict__ rp,
+                                                  int32_t* __restrict__ col,
+                                                  int32_t* __restrict__ age,
+                                                  float* __restrict__ x, float* __restrict__ y,
+                                                  float* __restrict__ z,
+                                                  float* __restrict__ err,
+                                                  int32_t* __restrict__ status) {
+  __shared__ float be[1024];
+  __shared__ int32_t bi[1024];
+  __shared__ int32_t added;
+  const int32_t t = threadIdx.x;
+  int32_t n = n0;
+  int32_t done = 0;
+  for (int32_t it = 0; it < count && n < n_max; ++it) {
+    float e = -__builtin_huge_valf();
+    int32_t idx = -1;
+    for (int32_t i = t; i < n; i += 1024) {
+      const float v = err[i];
+      if (idx < 0 || v > e) {  // ascending i per lane: strict > keeps the lower index
+        e = v;
+        idx = i;
+      }
+    }
+    be[t] = e;
+    bi[t] = idx;
+    __syncthreads();
+    for (int w = 512; w > 0; w >>= 1) {
+      if (t < w) {
+        const float oe = be[t + w];
+        const int32_t oi = bi[t + w];
+        if (oi >= 0 && (bi[t] < 0 || oe > be[t] || (oe == be[t] && oi < bi[t]))) {
+          be[t] = oe;
+          bi[t] = oi;
+        }
+      }
+      __syncthreads();
+    }
+    if (t == 0) added = insert_one(n, bi[0], alpha, half_cap, rp, col, age, x, y, z, err, status);
+    __threadfence();
+    __syncthreads();
+    if (!added) break;
+    ++n;
+    ++done;
+  }
+  if (t == 0) status[kStInserted] = done;
 }
 
 }  // namespace
@@ -201,10 +225,10 @@ hipError_t launch_remove(const DevState& s, int cur, int32_t n, int32_t n_max,
   return hipGetLastError();
 }
 
-hipError_t launch_insert(const DevState& s, int cur, int32_t n, float alpha, int64_t half_cap,
-                         hipStream_t st) {
-  gr_insert<<<1, 1024, 0, st>>>(n, alpha, half_cap, s.rp[cur], s.col[cur], s.age[cur], s.x,
-                                s.y, s.z, s.err, s.status);
+hipError_t launch_insert(const DevState& s, int cur, int32_t n, int32_t count, float alpha,
+                         int32_t n_max, int64_t half_cap, hipStream_t st) {
+  gr_insert<<<1, 1024, 0, st>>>(n, count, n_max, alpha, half_cap, s.rp[cur], s.col[cur],
+                                s.age[cur], s.x, s.y, s.z, s.err, s.status);
   return hipGetLastError();
 }
 

@@ -50,6 +50,13 @@ Layout layout_for(const gsn_params& p) {
   add(4 * nm);                 // 21 extra
   add(4 * kRmSlots);           // 22 rem
   add(8 * mm);                 // 23 list
+  add(12 * mm);                // 24 schedule signals
+  add(4 * mm);                 // 25 schedule winners
+  add(4 * mm);                 // 26 schedule seconds
+  add(4 * mm);                 // 27 schedule d1
+  add(4 * mm);                 // 28 schedule d2
+  add(mm);                     // 29 schedule acceptance
+  add(8 * kA64Slots);          // 30 64-bit accumulators
   L.total = (o + 255) & ~static_cast<size_t>(255);
   return L;
 }
@@ -81,6 +88,13 @@ void carve(const gsn_params& p, void* base, DevState* s) {
   s->extra = reinterpret_cast<int32_t*>(b + L.off[21]);
   s->rem = reinterpret_cast<int32_t*>(b + L.off[22]);
   s->list = reinterpret_cast<int32_t*>(b + L.off[23]);
+  s->ssig = reinterpret_cast<float*>(b + L.off[24]);
+  s->swin = reinterpret_cast<int32_t*>(b + L.off[25]);
+  s->ssec = reinterpret_cast<int32_t*>(b + L.off[26]);
+  s->sd1 = reinterpret_cast<float*>(b + L.off[27]);
+  s->sd2 = reinterpret_cast<float*>(b + L.off[28]);
+  s->sacc = reinterpret_cast<uint8_t*>(b + L.off[29]);
+  s->acc64 = reinterpret_cast<unsigned long long*>(b + L.off[30]);
 }
 
 }  // namespace gsn
@@ -179,6 +193,46 @@ int read_status_slot(gsn_net* net, int slot, int32_t* out, hipStream_t st) {
       hipSuccess)
     return GSN_E_HIP;
   return hip_ok(hipStreamSynchronize(st));
+}
+
+int read_acc64(gsn_net* net, int slot, int64_t* out, hipStream_t st) {
+  unsigned long long v = 0;
+  if (hipMemcpyAsync(&v, net->s.acc64 + slot, sizeof(v), hipMemcpyDeviceToHost, st) !=
+      hipSuccess)
+    return GSN_E_HIP;
+  if (hipStreamSynchronize(st) != hipSuccess) return GSN_E_HIP;
+  *out = static_cast<int64_t>(v);
+  return GSN_OK;
+}
+
+// Between iterations: remove the units orphaned since the last call, then up to `count` GNG
+// insertions one after another (while N < n_max).  Syncs to learn the new unit count.
+int grow_step(gsn_net* net, int32_t count, int32_t* inserted_out, hipStream_t st) {
+  int32_t orphans = 0;
+  int rc = read_status_slot(net, gsn::kStOrphans, &orphans, st);
+  if (rc) return rc;
+  if (orphans > 0) {
+    if (gsn::launch_remove(net->s, net->cur, net->n, net->p.n_max, st) != hipSuccess)
+      return GSN_E_HIP;
+    net->cur ^= 1;
+    int32_t kept = 0;
+    rc = read_status_slot(net, gsn::kStKept, &kept, st);
+    if (rc) return rc;
+    net->n = kept;
+    net->bucket_n = -1;  // indices changed
+  }
+  int32_t inserted = 0;
+  if (count > 0 && net->n >= 1 && net->n < net->p.n_max) {
+    if (gsn::launch_insert(net->s, net->cur, net->n, count, net->p.err_alpha, net->p.n_max,
+                           2 * static_cast<int64_t>(net->p.e_max), st) != hipSuccess)
+      return GSN_E_HIP;
+    rc = read_status_slot(net, gsn::kStInserted, &inserted, st);
+    if (rc) return rc;
+    net->n += inserted;
+    if (inserted) net->bucket_n = -1;
+  }
+  if (inserted_out) *inserted_out = inserted;
+  return GSN_OK;
 }
 
 }  // namespace
@@ -346,31 +400,83 @@ int gsn_update_edges(gsn_net* net, int32_t m, const int32_t* winner, const int32
 int gsn_grow(gsn_net* net, int32_t iteration, int32_t insert_every, void* stream) {
   if (!net || insert_every < 0) return GSN_E_INVAL;
   if (net->phase != kReady) return GSN_E_STATE;
+  const bool insert = insert_every > 0 && iteration > 0 && iteration % insert_every == 0;
+  return grow_step(net, insert ? 1 : 0, nullptr, as_stream(stream));
+}
+
+int gsn_run_schedule(gsn_net* net, const float* cloud, int64_t n_points,
+                     const gsn_schedule* sc, gsn_schedule_result* res, void* stream) {
+  if (!net || !cloud || !sc || !res) return GSN_E_INVAL;
+  if (n_points < 1 || n_points > static_cast<int64_t>(UINT32_MAX)) return GSN_E_INVAL;
+  if (sc->m_cap < 1 || sc->m_cap > net->p.m_max || sc->fixed_m < 0 ||
+      sc->fixed_m > net->p.m_max)
+    return GSN_E_INVAL;
+  if (sc->insert_every < 0 || sc->qe_window < 1 || sc->max_signals < 1) return GSN_E_INVAL;
+  const int32_t m_big = sc->fixed_m > 0 ? sc->fixed_m : sc->m_cap;
+  if (sc->qe_window + m_big > (int64_t{1} << 19)) return GSN_E_INVAL;
+  if (net->phase != kReady || net->n < 2) return GSN_E_STATE;
   hipStream_t st = as_stream(stream);
-  int32_t orphans = 0;
-  int rc = read_status_slot(net, gsn::kStOrphans, &orphans, st);
+  const gsn::DevState& s = net->s;
+  *res = gsn_schedule_result{};
+  int64_t accepted0 = 0, accepted1 = 0;
+  int rc = read_acc64(net, gsn::kA64Accepted, &accepted0, st);
   if (rc) return rc;
-  if (orphans > 0) {
-    if (gsn::launch_remove(net->s, net->cur, net->n, net->p.n_max, st) != hipSuccess)
+  if (hipMemsetAsync(s.acc64 + gsn::kA64Window, 0, 8, st) != hipSuccess) return GSN_E_HIP;
+  int64_t wcount = 0;
+  bool have_qe = false;
+  for (;;) {
+    if (net->n < 2) return GSN_E_STATE;
+    int32_t m = sc->fixed_m;
+    if (m == 0) {
+      int64_t p2 = 1;
+      while (p2 <= net->n) p2 *= 2;  // the smallest power of two greater than N
+      m = static_cast<int32_t>(std::min<int64_t>(p2, sc->m_cap));
+    }
+    if (gsn::launch_draw(cloud, n_points, sc->seed, res->signals, m, s.ssig, st) != hipSuccess)
       return GSN_E_HIP;
-    net->cur ^= 1;
-    int32_t kept = 0;
-    rc = read_status_slot(net, gsn::kStKept, &kept, st);
-    if (rc) return rc;
-    net->n = kept;
-    net->bucket_n = -1;  // indices changed
-  }
-  if (insert_every > 0 && iteration > 0 && iteration % insert_every == 0 && net->n >= 1 &&
-      net->n < net->p.n_max) {
-    if (gsn::launch_insert(net->s, net->cur, net->n, net->p.err_alpha,
-                           2 * static_cast<int64_t>(net->p.e_max), st) != hipSuccess)
-      return GSN_E_HIP;
+    if ((rc = gsn_find_winners(net, s.ssig, m, s.swin, s.ssec, s.sd1, s.sd2, stream))) return rc;
+    if ((rc = gsn_resolve_conflicts(net, m, s.swin, s.ssec, s.sd1, s.sacc, stream))) return rc;
+    if ((rc = gsn_adapt(net, s.ssig, m, s.swin, s.ssec, s.sd1, s.sacc, stream))) return rc;
+    if ((rc = gsn_update_edges(net, m, s.swin, s.ssec, s.sacc, stream))) return rc;
+    if (gsn::launch_qe(s.sd1, m, s.acc64 + gsn::kA64Window, st) != hipSuccess) return GSN_E_HIP;
+    res->signals += m;
+    res->iterations += 1;
+    wcount += m;
+    const int64_t k = sc->insert_every > 0 ? res->signals / sc->insert_every -
+                                                 (res->signals - m) / sc->insert_every
+                                           : 0;
     int32_t inserted = 0;
-    rc = read_status_slot(net, gsn::kStInserted, &inserted, st);
-    if (rc) return rc;
-    net->n += inserted;
-    if (inserted) net->bucket_n = -1;
+    if ((rc = grow_step(net, static_cast<int32_t>(std::min<int64_t>(k, INT32_MAX)), &inserted,
+                        st)))
+      return rc;
+    res->inserted += inserted;
+    if (wcount >= sc->qe_window) {
+      int64_t sum = 0;
+      if ((rc = read_acc64(net, gsn::kA64Window, &sum, st))) return rc;
+      if (hipMemsetAsync(s.acc64 + gsn::kA64Window, 0, 8, st) != hipSuccess) return GSN_E_HIP;
+      res->qe = static_cast<double>(static_cast<uint64_t>(sum)) * 0x1p-32 /
+                static_cast<double>(wcount);
+      have_qe = true;
+      wcount = 0;
+      if (res->qe < static_cast<double>(sc->qe_threshold)) {
+        res->converged = 1;
+        break;
+      }
+    }
+    if (res->signals >= sc->max_signals) break;
   }
+  if (!have_qe && wcount > 0) {
+    int64_t sum = 0;
+    if ((rc = read_acc64(net, gsn::kA64Window, &sum, st))) return rc;
+    res->qe = static_cast<double>(static_cast<uint64_t>(sum)) * 0x1p-32 /
+              static_cast<double>(wcount);
+  }
+  if ((rc = read_acc64(net, gsn::kA64Accepted, &accepted1, st))) return rc;
+  res->accepted = accepted1 - accepted0;
+  int32_t nu = 0, ne = 0;
+  if ((rc = gsn_sizes(net, &nu, &ne, stream))) return rc;
+  res->n_units = nu;
+  res->n_edges = ne;
   return GSN_OK;
 }
 
@@ -549,16 +655,23 @@ int gsn_tune(gsn_net* net, int32_t key, int32_t value) {
 }
 
 int gsn_stat(gsn_net* net, int32_t key, int64_t* value, void* stream) {
-  if (!net || key < 0 || key > GSN_STAT_CLEAR) return GSN_E_INVAL;
+  if (!net || key < 0 || key > GSN_STAT_ACCEPTED) return GSN_E_INVAL;
   if (key != GSN_STAT_CLEAR && !value) return GSN_E_INVAL;
   hipStream_t st = as_stream(stream);
   int32_t* slots = net->s.rem + gsn::kRmRounds;
   if (key == GSN_STAT_CLEAR) {
     const int32_t zero[3] = {0, 0, 0};
-    if (hipMemcpyAsync(slots, zero, sizeof(zero), hipMemcpyHostToDevice, st) != hipSuccess)
+    const unsigned long long zero64[2] = {0, 0};
+    if (hipMemcpyAsync(slots, zero, sizeof(zero), hipMemcpyHostToDevice, st) != hipSuccess ||
+        hipMemcpyAsync(net->s.acc64 + gsn::kA64Resolved, zero64, sizeof(zero64),
+                       hipMemcpyHostToDevice, st) != hipSuccess)
       return GSN_E_HIP;
     return hip_ok(hipStreamSynchronize(st));
   }
+  if (key == GSN_STAT_RESOLVED)
+    return read_acc64(net, gsn::kA64Resolved, value, st);
+  if (key == GSN_STAT_ACCEPTED)
+    return read_acc64(net, gsn::kA64Accepted, value, st);
   int32_t h[3];
   if (hipMemcpyAsync(h, slots, sizeof(h), hipMemcpyDeviceToHost, st) != hipSuccess)
     return GSN_E_HIP;

@@ -36,6 +36,14 @@ enum RoundSlot {
   kRmSlots
 };
 
+// 64-bit accumulators (DevState::acc64).
+enum Acc64Slot {
+  kA64Window = 0,    // error window of the schedule: sum of floor(d1 * 2^32)
+  kA64Resolved = 1,  // signals through resolve since the last statistics clear
+  kA64Accepted = 2,  // of those, accepted
+  kA64Slots = 4
+};
+
 __device__ __forceinline__ void raise_error(int32_t* status, int32_t code) {
   atomicCAS(&status[kStError], 0, code);
 }
@@ -50,6 +58,22 @@ __device__ __forceinline__ unsigned long long signal_key(float d1, int32_t j, in
   const unsigned long long lo = static_cast<uint32_t>(j);
   if (key_mode == 1) return lo;
   return (static_cast<unsigned long long>(__float_as_uint(d1)) << 32) | lo;
+}
+
+// Adds the lanes of this wave for which `pred` holds to *ctr with one atomic.
+__device__ __forceinline__ void wave_count(bool pred, int32_t* ctr) {
+  const unsigned long long mask = __ballot(pred);
+  if (mask == 0) return;
+  const int lane = static_cast<int>(threadIdx.x & 63);
+  if (lane == __ffsll(static_cast<long long>(mask)) - 1)
+    atomicAdd(ctr, static_cast<int32_t>(__popcll(mask)));
+}
+__device__ __forceinline__ void wave_count(bool pred, unsigned long long* ctr) {
+  const unsigned long long mask = __ballot(pred);
+  if (mask == 0) return;
+  const int lane = static_cast<int>(threadIdx.x & 63);
+  if (lane == __ffsll(static_cast<long long>(mask)) - 1)
+    atomicAdd(ctr, static_cast<unsigned long long>(__popcll(mask)));
 }
 
 // w <- w + eps (xi - w), one binary32 rounding per operation (no contraction).
@@ -83,6 +107,12 @@ struct DevState {
   int32_t* extra;                  // [n_max]       insertions a row may receive (kept zero)
   int32_t* rem;                    // [kRmSlots]    round counters (RoundSlot)
   int32_t* list;                   // [2 m_max]     pending signals of the last rounds
+  // growing-network schedule
+  float* ssig;                     // [3 m_max]     signals of the iteration, SoA
+  int32_t *swin, *ssec;            // [m_max]
+  float *sd1, *sd2;                // [m_max]
+  uint8_t* sacc;                   // [m_max]
+  unsigned long long* acc64;       // [kA64Slots]   64-bit accumulators (Acc64Slot)
 };
 
 struct Layout {
@@ -186,7 +216,13 @@ hipError_t launch_init(const DevState& s, int cur, int32_t n0, int32_t n_max,
                        hipStream_t st);
 hipError_t launch_remove(const DevState& s, int cur, int32_t n, int32_t n_max,
                          hipStream_t st);
-hipError_t launch_insert(const DevState& s, int cur, int32_t n, float alpha,
-                         int64_t half_cap, hipStream_t st);
+// Schedule kernels (schedule.hip): draw m signals (signal numbers c0 + 1 .. c0 + m) from
+// the cloud, and add the winners' distances of m signals to the error window.
+hipError_t launch_draw(const float* cloud, int64_t n_points, uint64_t seed, int64_t c0,
+                       int32_t m, float* sig, hipStream_t st);
+hipError_t launch_qe(const float* d1, int32_t m, unsigned long long* acc, hipStream_t st);
+// Up to `count` GNG insertions one after another; status[kStInserted] receives how many.
+hipError_t launch_insert(const DevState& s, int cur, int32_t n, int32_t count, float alpha,
+                         int32_t n_max, int64_t half_cap, hipStream_t st);
 
 }  // namespace gsn

@@ -58,28 +58,31 @@ __global__ void rs_claim(int32_t m, int32_t n, const int32_t* __restrict__ winne
 // With the winner alone locked, the survivor also releases its lock (the other claimants
 // compare with their own keys, which differ from both values), so the lock array is back
 // to all ones afterwards.
+// Also counts the signals and the accepted ones into the 64-bit statistics.
 __global__ void rs_check(int32_t m, int32_t n, const int32_t* __restrict__ winner,
                          const int32_t* __restrict__ second, const float* __restrict__ d1,
                          const int32_t* __restrict__ rp, const int32_t* __restrict__ col,
                          unsigned long long* __restrict__ lock,
-                         uint8_t* __restrict__ accepted, int winner_only, int key_mode) {
+                         uint8_t* __restrict__ accepted, int winner_only, int key_mode,
+                         unsigned long long* __restrict__ acc64) {
   const int32_t j = blockIdx.x * kBlock + threadIdx.x;
-  if (j >= m) return;
-  const int32_t b = winner[j], s = second[j];
-  if (!pair_ok(b, s, n)) {
-    accepted[j] = 0;
-    return;
-  }
-  const unsigned long long key = signal_key(d1[j], j, key_mode);
-  bool ok = lock[b] == key;
-  if (winner_only) {
-    if (ok) lock[b] = ~0ull;
+  bool ok = false;
+  if (j < m) {
+    const int32_t b = winner[j], s = second[j];
+    if (pair_ok(b, s, n)) {
+      const unsigned long long key = signal_key(d1[j], j, key_mode);
+      ok = lock[b] == key;
+      if (winner_only) {
+        if (ok) lock[b] = ~0ull;
+      } else {
+        ok = ok && lock[s] == key;
+        for (int32_t k = rp[b]; ok && k < rp[b + 1]; ++k) ok = lock[col[k]] == key;
+      }
+    }
     accepted[j] = ok ? 1 : 0;
-    return;
   }
-  ok = ok && lock[s] == key;
-  for (int32_t k = rp[b]; ok && k < rp[b + 1]; ++k) ok = lock[col[k]] == key;
-  accepted[j] = ok ? 1 : 0;
+  wave_count(j < m, &acc64[kA64Resolved]);
+  wave_count(ok, &acc64[kA64Accepted]);
 }
 
 // -------------------------------------------------------------------- adapt ----
@@ -274,8 +277,8 @@ __global__ void ed_write(int32_t n, const int32_t* __restrict__ rp,
 __global__ void init_state(float* __restrict__ err, int32_t* __restrict__ ins,
                            int32_t* __restrict__ orphan, int32_t* __restrict__ rp,
                            unsigned long long* __restrict__ lock, int32_t* __restrict__ extra,
-                           int32_t* __restrict__ rem, int32_t n_max,
-                           int32_t* __restrict__ status) {
+                           int32_t* __restrict__ rem, unsigned long long* __restrict__ acc64,
+                           int32_t n_max, int32_t* __restrict__ status) {
   const int32_t i = blockIdx.x * kBlock + threadIdx.x;
   if (i < n_max) {
     err[i] = 0.0f;
@@ -287,6 +290,7 @@ __global__ void init_state(float* __restrict__ err, int32_t* __restrict__ ins,
   if (i <= n_max) rp[i] = 0;
   if (i < kStSlots) status[i] = 0;
   if (i < kRmSlots) rem[i] = 0;
+  if (i < kA64Slots) acc64[i] = 0;
 }
 
 inline int blocks(int64_t n) { return static_cast<int>((n + kBlock - 1) / kBlock); }
@@ -297,7 +301,7 @@ hipError_t launch_init(const DevState& s, int cur, int32_t, int32_t n_max, hipSt
   const int64_t cover =
       std::max<int64_t>(static_cast<int64_t>(n_max) + 1, std::max<int>(kStSlots, kRmSlots));
   init_state<<<blocks(cover), kBlock, 0, st>>>(s.err, s.ins, s.orphan, s.rp[cur], s.lock,
-                                               s.extra, s.rem, n_max, s.status);
+                                               s.extra, s.rem, s.acc64, n_max, s.status);
   return hipGetLastError();
 }
 
@@ -310,7 +314,7 @@ hipError_t launch_resolve(const DevState& s, int cur, int32_t n, int32_t m,
   rs_claim<<<blocks(m), kBlock, 0, st>>>(m, n, winner, second, d1, s.rp[cur], s.col[cur],
                                          s.lock, s.status, wo, key_mode);
   rs_check<<<blocks(m), kBlock, 0, st>>>(m, n, winner, second, d1, s.rp[cur], s.col[cur],
-                                         s.lock, accepted, wo, key_mode);
+                                         s.lock, accepted, wo, key_mode, s.acc64);
   return hipGetLastError();
 }
 

@@ -73,15 +73,6 @@ __device__ int32_t row_remove(const int32_t* __restrict__ rp, int32_t* __restric
   return l - 1;
 }
 
-// Adds the lanes of this wave for which `pred` holds to *ctr with one atomic.
-__device__ __forceinline__ void wave_count(bool pred, int32_t* ctr) {
-  const unsigned long long mask = __ballot(pred);
-  if (mask == 0) return;
-  const int lane = static_cast<int>(threadIdx.x & 63);
-  if (lane == __ffsll(static_cast<long long>(mask)) - 1)
-    atomicAdd(ctr, static_cast<int32_t>(__popcll(mask)));
-}
-
 // ----------------------------------------------------------------- prologue ----
 
 // Survivors (pend = 1), the insertions each row may receive, the survivor count, and the

@@ -45,6 +45,8 @@ GSN_STAT_ROUNDS = 0
 GSN_STAT_ROUNDS_MAX = 1
 GSN_STAT_UPDATES = 2
 GSN_STAT_CLEAR = 3
+GSN_STAT_RESOLVED = 4
+GSN_STAT_ACCEPTED = 5
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
@@ -68,6 +70,31 @@ class gsn_params(ctypes.Structure):
     ]
 
 
+class gsn_schedule(ctypes.Structure):
+    _fields_ = [
+        ("m_cap", ctypes.c_int32),
+        ("fixed_m", ctypes.c_int32),
+        ("insert_every", ctypes.c_int64),
+        ("qe_window", ctypes.c_int64),
+        ("max_signals", ctypes.c_int64),
+        ("qe_threshold", ctypes.c_float),
+        ("seed", ctypes.c_uint64),
+    ]
+
+
+class gsn_schedule_result(ctypes.Structure):
+    _fields_ = [
+        ("iterations", ctypes.c_int64),
+        ("signals", ctypes.c_int64),
+        ("accepted", ctypes.c_int64),
+        ("inserted", ctypes.c_int64),
+        ("qe", ctypes.c_double),
+        ("converged", ctypes.c_int32),
+        ("n_units", ctypes.c_int32),
+        ("n_edges", ctypes.c_int64),
+    ]
+
+
 _P = ctypes.c_void_p
 _I = ctypes.c_int32
 _sig = {
@@ -79,6 +106,8 @@ _sig = {
     "gsn_adapt": (ctypes.c_int, [_P, _P, _I, _P, _P, _P, _P, _P]),
     "gsn_update_edges": (ctypes.c_int, [_P, _I, _P, _P, _P, _P]),
     "gsn_grow": (ctypes.c_int, [_P, _I, _I, _P]),
+    "gsn_run_schedule": (ctypes.c_int, [_P, _P, ctypes.c_int64, ctypes.POINTER(gsn_schedule),
+                                        ctypes.POINTER(gsn_schedule_result), _P]),
     "gsn_sizes": (ctypes.c_int, [_P, ctypes.POINTER(_I), ctypes.POINTER(_I), _P]),
     "gsn_export": (ctypes.c_int, [_P, _P, _P, _P, _P]),
     "gsn_import": (ctypes.c_int, [_P, _I, _P, _P, _I, _P, _P]),
@@ -243,6 +272,23 @@ def gsn_timing_read(net, which: int):
     return ms.value, cnt.value
 
 
+def make_schedule(m_cap=8192, fixed_m=0, insert_every=100, qe_window=8192,
+                  max_signals=1 << 20, qe_threshold=0.0, seed=0) -> gsn_schedule:
+    return gsn_schedule(m_cap, fixed_m, insert_every, qe_window, max_signals, qe_threshold,
+                        seed)
+
+
+def gsn_run_schedule(net, cloud: torch.Tensor, schedule: gsn_schedule, stream=None) -> dict:
+    """cloud: device SoA (3, P) float32.  Returns the result fields as a dict."""
+    if cloud.dim() != 2 or cloud.shape[0] != 3:
+        raise ValueError("cloud must be (3, P)")
+    p = _dev(cloud, torch.float32, what="cloud")
+    r = gsn_schedule_result()
+    _check(_lib.gsn_run_schedule(net, p, cloud.shape[1], ctypes.byref(schedule),
+                                 ctypes.byref(r), _stream(stream)), "gsn_run_schedule")
+    return {f: getattr(r, f) for f, _ in gsn_schedule_result._fields_}
+
+
 def gsn_stat(net, key: int, stream=None) -> int:
     v = ctypes.c_int64()
     _check(_lib.gsn_stat(net, key, ctypes.byref(v), _stream(stream)), "gsn_stat")
@@ -354,3 +400,6 @@ class Network:
 
     def stat(self, key: int) -> int:
         return gsn_stat(self.h, key, self.stream)
+
+    def run_schedule(self, cloud: torch.Tensor, schedule: gsn_schedule) -> dict:
+        return gsn_run_schedule(self.h, cloud.contiguous(), schedule, self.stream)
