@@ -94,6 +94,99 @@ def cpu_baseline(wl, units, cloud, budget_s: float, lock_mode: int = 0, key_mode
             "seconds": dt}
 
 
+# The growing-network run: genus-3 cloud (4,000,000 points), two initial cloud points,
+# m = smallest power of two above N capped at 8192, one GNG insertion every 100 signals,
+# stop when a window of 65,536 signals has a mean squared winner distance below 1.5e-5.
+SCHEDULE = dict(m_cap=8192, insert_every=100, qe_window=65536, max_signals=40_000_000,
+                qe_threshold=1.5e-5, seed=3)
+SCHEDULE_N_MAX = 200_000
+SCHEDULE_CPU_SIGNALS = 2_000_000
+
+
+def run_schedule_bench(args):
+    import numpy as np
+    import torch
+
+    from paper_1503_08294_amd import gsn
+    from paper_1503_08294_amd.clouds import WORKLOADS, initial_units
+
+    wl = WORKLOADS["genus3_200k"]
+    print(f"[bench] generating the genus-3 cloud ({wl.n_points} points)", file=sys.stderr,
+          flush=True)
+    cloud = wl.make_cloud()
+    units = initial_units(cloud, 2, wl.unit_seed)
+    soa = np.ascontiguousarray(cloud.T)
+    torch.cuda.set_device(0)
+    dev_cloud = torch.from_numpy(soa).cuda()
+    lock_mode = gsn.GSN_LOCK_WINNER if args.lock == "winner" else gsn.GSN_LOCK_SET
+    key_mode = gsn.GSN_KEY_INDEX if args.key == "index" else gsn.GSN_KEY_DIST_INDEX
+    n_max = SCHEDULE_N_MAX
+    params = gsn.make_params(wl.eps_b, wl.eps_n, wl.max_age, wl.err_alpha, wl.err_beta,
+                             n_max, 4 * n_max + 16, SCHEDULE["m_cap"], lock_mode, key_mode)
+
+    def one_run(max_signals):
+        net = gsn.Network(params, torch.from_numpy(units).cuda())
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        r = net.run_schedule(dev_cloud, gsn.make_schedule(**dict(SCHEDULE,
+                                                                 max_signals=max_signals)))
+        torch.cuda.synchronize()
+        el = time.perf_counter() - t0
+        if net.check() != 0:
+            raise SystemExit(f"device status {net.check()} after the run")
+        net.close()
+        return r, el
+
+    print("[bench] warmup run (first 1M signals)", file=sys.stderr, flush=True)
+    one_run(1_000_000)
+    print("[bench] timed run", file=sys.stderr, flush=True)
+    r, el = one_run(SCHEDULE["max_signals"])
+    out = {
+        "metric": "growing-network run to the quantization-error threshold: signals/s",
+        "value": r["signals"] / el,
+        "unit": "signals/s",
+        "n_gpus": 1,
+        "steps": r["iterations"],
+        "warmup": 1,
+        "ms_per_step": 1e3 * el / r["iterations"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "genus3_schedule", "cloud_points": wl.n_points,
+                   "initial_units": 2, "n_max": n_max, **SCHEDULE,
+                   "collision": {"lock": args.lock, "key": args.key},
+                   "parallelism": "single"},
+        "seconds": el,
+        "result": r,
+        "accepted_per_s": r["accepted"] / el,
+        "cpu_baseline": None,
+    }
+    if args.cpu_budget > 0:
+        import oracle
+        print(f"[bench] cpu baseline (first {SCHEDULE_CPU_SIGNALS} signals)", file=sys.stderr,
+              flush=True)
+        threads = max(1, min(16, os.cpu_count() or 1))
+        o = oracle.Oracle(oracle.Params(wl.eps_b, wl.eps_n, wl.max_age, wl.err_alpha,
+                                        wl.err_beta, n_max, 4 * n_max + 16,
+                                        SCHEDULE["m_cap"], lock_mode=lock_mode,
+                                        key_mode=key_mode), units, threads=threads)
+        t0 = time.perf_counter()
+        ro = o.run_schedule(soa, oracle.Schedule(**dict(SCHEDULE,
+                                                        max_signals=SCHEDULE_CPU_SIGNALS)))
+        dt = time.perf_counter() - t0
+        out["cpu_baseline"] = {"value": ro["signals"] / dt, "unit": "signals/s",
+                               "cores": threads, "kind": "oracle",
+                               "sample": f"the first {ro['signals']} signals of the same run "
+                                         f"(N 2 -> {ro['n_units']}), oracle find-winners on "
+                                         f"{threads} threads", "seconds": dt}
+        r1, el1 = one_run(SCHEDULE_CPU_SIGNALS)
+        out["gpu_same_sample"] = {"signals_per_s": r1["signals"] / el1, "seconds": el1,
+                                  "n_units": r1["n_units"]}
+    print(json.dumps(out), flush=True)
+
+
 def copy_calibration(nbytes: int, reps: int):
     """A plain device copy of known size, for scaling FETCH_SIZE / WRITE_SIZE counters."""
     import torch
@@ -120,6 +213,10 @@ def main():
                          "or the winner alone with the survivors applied in key order")
     ap.add_argument("--key", choices=("dist", "index"), default="dist",
                     help="survivor priority: (winner distance, index) or the index alone")
+    ap.add_argument("--schedule", action="store_true",
+                    help="instead of fixed-size steps, time one growing-network run "
+                         "(gsn_run_schedule) from two units to the quantization-error "
+                         "threshold on the genus-3 cloud")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -130,6 +227,10 @@ def main():
 
     if args.copy_calibration:
         copy_calibration(args.copy_calibration, 5)
+        return
+
+    if args.schedule:
+        run_schedule_bench(args)
         return
 
     import numpy as np

@@ -14,7 +14,8 @@
  * Memory.   Every device buffer is allocated and owned by the caller (for example as a
  *           torch tensor) and must outlive the handle.  The network state lives in one
  *           caller-provided device workspace of gsn_workspace_bytes() bytes, aligned to
- *           256 bytes.  The library allocates only the host-side handle.
+ *           256 bytes.  The library allocates only the host-side handle (with a few bytes
+ *           of pinned host memory in it).
  * Layout.   Points are structure-of-arrays binary32: a buffer "SoA [3][k]" holds all k x
  *           coordinates, then all y, then all z.  Unit indices are int32 in [0, N).
  * Streams.  `stream` is a hipStream_t passed as void* (NULL = the default stream).  Calls
@@ -96,7 +97,8 @@ size_t gsn_workspace_bytes(const gsn_params* params);
 /* Create a network of n0 units (0 <= n0 <= n_max) at init_xyz (SoA [3][n0] binary32, host
  * or device memory), with no edges and zero accumulated error.  workspace: device memory
  * of at least gsn_workspace_bytes(params) bytes, 256-byte aligned, owned by the caller and
- * used by this handle only.  Syncs.  On success *out holds the handle. */
+ * used by this handle only.  The handle itself holds a few bytes of pinned host memory
+ * (launch feedback of the winner-lock update).  Syncs.  On success *out holds the handle. */
 int gsn_create(const gsn_params* params, void* workspace, size_t workspace_bytes, int32_t n0,
                const float* init_xyz, void* stream, gsn_net** out);
 
@@ -236,8 +238,10 @@ void gsn_destroy(gsn_net* net);
  *                     screen carries a rigorous rounding margin; candidates are rechecked
  *                     in the binary32 direct form, so all variants return the same result)
  *   GSN_TUNE_GRID_ROUNDS  rounds of the GSN_LOCK_WINNER update launched over the whole
- *                     device before the remaining ones run in a single workgroup (0..16,
- *                     default 6)
+ *                     device (each skipped once fewer than 256 signals are pending) before
+ *                     the remaining ones run in a single workgroup: 1..16, or 0 =
+ *                     automatic (one more than the previous update used, from a pinned
+ *                     host copy of its count)
  * Returns GSN_E_INVAL for an unknown key or value. */
 enum { GSN_TUNE_SPLIT = 1, GSN_TUNE_VARIANT = 2, GSN_TUNE_GRID_ROUNDS = 3 };
 #define GSN_MAX_SPLIT 64

@@ -102,64 +102,143 @@ __global__ void gr_copyback(int32_t n, int32_t n_max, const float* __restrict__ 
   }
 }
 
-// Remove neighbour `gone` from the ascending row of u and append `added` (larger than
-// every id in the row) at age 0.  The row keeps its length.
-__device__ void replace_in_row(const int32_t* __restrict__ rp, int32_t* __restrict__ col,
-                               int32_t* __restrict__ age, int32_t u, int32_t gone,
-                               int32_t added) {
-  const int32_t r0 = rp[u], r1 = rp[u + 1];
-  int32_t k = r0;
-  while (k < r1 && col[k] != gone) ++k;
-  for (; k + 1 < r1; ++k) {
-    col[k] = col[k + 1];
-    age[k] = age[k + 1];
-  }
-  col[r1 - 1] = added;
-  age[r1 - 1] = 0;
+// ------------------------------------------------------------------ insertion ----
+// GNG insertion (Sec. 2.1): q = the unit of largest error, f = the neighbour of q of
+// largest error (ties to the lower index for both), a unit r = N at their midpoint, the edge
+// {q, f} replaced by {q, r} and {r, f} at age 0, err_q and err_f scaled by alpha, and
+// err_r = err_q.  Several insertions run one after another in one workgroup; the argmax
+// over all units goes over per-segment maxima held in LDS, and after every insertion only
+// the segments of q, f and r are rescanned.
+
+constexpr int kMaxSeg = 4096;  // segments held in LDS
+
+// Order key for the argmax: larger error first, then the lower index (errors are >= +0, so
+// their bits order like their values).  0 means "no unit".
+__device__ __forceinline__ unsigned long long err_key(float e, int32_t i) {
+  return (static_cast<unsigned long long>(__float_as_uint(e)) << 32) |
+         (0xFFFFFFFFu - static_cast<uint32_t>(i));
+}
+__device__ __forceinline__ int32_t key_index(unsigned long long k) {
+  return static_cast<int32_t>(0xFFFFFFFFu - static_cast<uint32_t>(k));
 }
 
-// One GNG insertion at unit index n (thread 0 only): q = argmax err (given), f = argmax err
-// over the neighbours of q, r = n at the midpoint, {q, f} replaced by {q, r} and {r, f}.
-// Returns 1 if a unit was added.
-__device__ int insert_one(int32_t n, int32_t q, float alpha, int64_t half_cap,
-                          int32_t* __restrict__ rp, int32_t* __restrict__ col,
-                          int32_t* __restrict__ age, float* __restrict__ x,
-                          float* __restrict__ y, float* __restrict__ z,
-                          float* __restrict__ err, int32_t* __restrict__ status) {
-  if (q < 0 || rp[q + 1] == rp[q]) return 0;
-  int32_t f = col[rp[q]];
-  for (int32_t k = rp[q] + 1; k < rp[q + 1]; ++k) {
-    const int32_t v = col[k];
-    if (err[v] > err[f]) f = v;  // ascending row: ties keep the lower index
+__device__ __forceinline__ unsigned long long wave_max(unsigned long long v) {
+  for (int off = 32; off > 0; off >>= 1) {
+    const unsigned long long o = __shfl_xor(v, off);
+    v = o > v ? o : v;
   }
+  return v;
+}
+
+// Key of the best unit of segment sg (units [sg len, sg len + len) below n), by one wave.
+__device__ unsigned long long segment_key(const float* __restrict__ err, int32_t n, int32_t sg,
+                                          int32_t len) {
+  const int lane = static_cast<int>(threadIdx.x & 63);
+  unsigned long long best = 0;
+  const int32_t end = min(n, (sg + 1) * len);
+  for (int32_t i = sg * len + lane; i < end; i += 64) {
+    const unsigned long long k = err_key(err[i], i);
+    best = k > best ? k : best;
+  }
+  return wave_max(best);
+}
+
+__global__ void gr_segmax(int32_t n, int32_t len, int32_t nseg, const float* __restrict__ err,
+                          unsigned long long* __restrict__ seg) {
+  const int32_t sg = (blockIdx.x * kBlock + threadIdx.x) >> 6;
+  if (sg >= nseg) return;  // whole waves
+  const unsigned long long k = segment_key(err, n, sg, len);
+  if ((threadIdx.x & 63) == 0) seg[sg] = k;
+}
+
+// Remove `gone` from the ascending row of u and append `added` (larger than every id in the
+// row) at age 0, by one wave: lanes hold the entries, the ones after `gone` move down.
+__device__ void wave_replace(const int32_t* __restrict__ rp, int32_t* __restrict__ col,
+                             int32_t* __restrict__ age, int32_t u, int32_t gone,
+                             int32_t added) {
+  const int lane = static_cast<int>(threadIdx.x & 63);
+  const int32_t r0 = rp[u], r1 = rp[u + 1], l = r1 - r0;
+  if (l > 64) {
+    if (lane == 0) {
+      int32_t k = r0;
+      while (k < r1 && col[k] != gone) ++k;
+      for (; k + 1 < r1; ++k) {
+        col[k] = col[k + 1];
+        age[k] = age[k + 1];
+      }
+      col[r1 - 1] = added;
+      age[r1 - 1] = 0;
+    }
+    return;
+  }
+  int32_t c = -1, a = 0;
+  if (lane < l) {
+    c = col[r0 + lane];
+    a = age[r0 + lane];
+  }
+  const unsigned long long at = __ballot(lane < l && c == gone);
+  const int pos = at ? __ffsll(static_cast<long long>(at)) - 1 : l;
+  if (lane < l && lane > pos) {
+    col[r0 + lane - 1] = c;
+    age[r0 + lane - 1] = a;
+  }
+  if (lane == 0) {
+    col[r1 - 1] = added;
+    age[r1 - 1] = 0;
+  }
+}
+
+// One insertion at r = n with q given, by one wave; returns 1 if a unit was added and the
+// chosen f in *f_out.
+__device__ int wave_insert(int32_t n, int32_t q, float alpha, int64_t half_cap,
+                           int32_t* __restrict__ rp, int32_t* __restrict__ col,
+                           int32_t* __restrict__ age, float* __restrict__ x,
+                           float* __restrict__ y, float* __restrict__ z,
+                           float* __restrict__ err, int32_t* __restrict__ status,
+                           int32_t* f_out) {
+  const int lane = static_cast<int>(threadIdx.x & 63);
+  if (q < 0) return 0;
+  const int32_t r0 = rp[q], r1 = rp[q + 1];
+  if (r1 == r0) return 0;
+  unsigned long long best = 0;
+  for (int32_t k = r0 + lane; k < r1; k += 64) {
+    const int32_t v = col[k];
+    const unsigned long long kk = err_key(err[v], v);
+    best = kk > best ? kk : best;
+  }
+  const int32_t f = key_index(wave_max(best));
   const int32_t e2 = rp[n];
   if (static_cast<int64_t>(e2) + 2 > half_cap) {
-    atomicCAS(&status[kStError], 0, GSN_E_CAPACITY);
+    if (lane == 0) atomicCAS(&status[kStError], 0, GSN_E_CAPACITY);
     return 0;
   }
   const int32_t r = n;
-  x[r] = (x[q] + x[f]) * 0.5f;
-  y[r] = (y[q] + y[f]) * 0.5f;
-  z[r] = (z[q] + z[f]) * 0.5f;
-  replace_in_row(rp, col, age, q, f, r);
-  replace_in_row(rp, col, age, f, q, r);
-  col[e2] = min(q, f);
-  col[e2 + 1] = max(q, f);
-  age[e2] = 0;
-  age[e2 + 1] = 0;
-  rp[r + 1] = e2 + 2;
-  err[q] = err[q] * alpha;
-  err[f] = err[f] * alpha;
-  err[r] = err[q];
+  wave_replace(rp, col, age, q, f, r);
+  wave_replace(rp, col, age, f, q, r);
+  if (lane == 0) {
+    x[r] = (x[q] + x[f]) * 0.5f;
+    y[r] = (y[q] + y[f]) * 0.5f;
+    z[r] = (z[q] + z[f]) * 0.5f;
+    col[e2] = min(q, f);
+    col[e2 + 1] = max(q, f);
+    age[e2] = 0;
+    age[e2 + 1] = 0;
+    rp[r + 1] = e2 + 2;
+    err[q] = err[q] * alpha;
+    err[f] = err[f] * alpha;
+    err[r] = err[q];
+  }
+  *f_out = f;
   return 1;
 }
 
 // Up to `count` insertions one after another (each sees the errors and edges the previous
-// one left), while N < n_max and the unit of largest error has a neighbour.  One workgroup:
-// the argmax is a block reduction, the edge surgery runs on thread 0, and a device-scope
-// fence and a barrier separate the insertions.
+// one left), while N < n_max and the unit of largest error has a neighbour.  seg holds the
+// segment keys of the n0 units on entry (gr_segmax).  A barrier separates the phases of an
+// insertion (one workgroup: its ordering covers what the waves share).
 __global__ __launch_bounds__(1024) void gr_insert(int32_t n0, int32_t count, int32_t n_max,
-                                                  float alpha, int64_t half_cap,
+                                                  int32_t len, float alpha, int64_t half_cap,
+                                                  const unsigned long long* __restrict__ seg,
                                                   int32_t* __restrict__ rp,
                                                   int32_t* __restrict__ col,
                                                   int32_t* __restrict__ age,
@@ -167,42 +246,50 @@ __global__ __launch_bounds__(1024) void gr_insert(int32_t n0, int32_t count, int
                                                   float* __restrict__ z,
                                                   float* __restrict__ err,
                                                   int32_t* __restrict__ status) {
-  __shared__ float be[1024];
-  __shared__ int32_t bi[1024];
-  __shared__ int32_t added;
-  const int32_t t = threadIdx.x;
+  __shared__ unsigned long long sk[kMaxSeg];
+  __shared__ unsigned long long red[16];
+  __shared__ int32_t s_q, s_f, s_added;
+  const int t = threadIdx.x, w = t >> 6, lane = t & 63;
+  int32_t nseg = (n0 + len - 1) / len;
+  for (int32_t i = t; i < nseg; i += 1024) sk[i] = seg[i];
+  __syncthreads();
   int32_t n = n0;
   int32_t done = 0;
   for (int32_t it = 0; it < count && n < n_max; ++it) {
-    float e = -__builtin_huge_valf();
-    int32_t idx = -1;
-    for (int32_t i = t; i < n; i += 1024) {
-      const float v = err[i];
-      if (idx < 0 || v > e) {  // ascending i per lane: strict > keeps the lower index
-        e = v;
-        idx = i;
+    // q: the best segment key
+    unsigned long long best = 0;
+    for (int32_t i = t; i < nseg; i += 1024) best = sk[i] > best ? sk[i] : best;
+    best = wave_max(best);
+    if (lane == 0) red[w] = best;
+    __syncthreads();
+    if (w == 0) {
+      unsigned long long b = lane < 16 ? red[lane] : 0;
+      b = wave_max(b);
+      if (lane == 0) s_q = b ? key_index(b) : -1;
+    }
+    __syncthreads();
+    if (w == 0) {
+      int32_t f = -1;
+      const int a = wave_insert(n, s_q, alpha, half_cap, rp, col, age, x, y, z, err, status,
+                                &f);
+      if (lane == 0) {
+        s_added = a;
+        s_f = f;
       }
     }
-    be[t] = e;
-    bi[t] = idx;
     __syncthreads();
-    for (int w = 512; w > 0; w >>= 1) {
-      if (t < w) {
-        const float oe = be[t + w];
-        const int32_t oi = bi[t + w];
-        if (oi >= 0 && (bi[t] < 0 || oe > be[t] || (oe == be[t] && oi < bi[t]))) {
-          be[t] = oe;
-          bi[t] = oi;
-        }
-      }
-      __syncthreads();
-    }
-    if (t == 0) added = insert_one(n, bi[0], alpha, half_cap, rp, col, age, x, y, z, err, status);
-    __threadfence();
-    __syncthreads();
-    if (!added) break;
+    if (!s_added) break;
+    // rescan the segments of q, f and r (waves 0, 1, 2; equal segments give equal keys)
+    const int32_t r = n;
     ++n;
     ++done;
+    if (w < 3) {
+      const int32_t u = w == 0 ? s_q : (w == 1 ? s_f : r);
+      const unsigned long long k = segment_key(err, n, u / len, len);
+      if (lane == 0) sk[u / len] = k;
+    }
+    nseg = (n + len - 1) / len;
+    __syncthreads();
   }
   if (t == 0) status[kStInserted] = done;
 }
@@ -227,8 +314,16 @@ hipError_t launch_remove(const DevState& s, int cur, int32_t n, int32_t n_max,
 
 hipError_t launch_insert(const DevState& s, int cur, int32_t n, int32_t count, float alpha,
                          int32_t n_max, int64_t half_cap, hipStream_t st) {
-  gr_insert<<<1, 1024, 0, st>>>(n, count, n_max, alpha, half_cap, s.rp[cur], s.col[cur],
-                                s.age[cur], s.x, s.y, s.z, s.err, s.status);
+  // segment length: whole waves, at most kMaxSeg segments over n_max units
+  const int32_t waves = (n_max + 63) / 64;
+  const int32_t len = 64 * ((waves + kMaxSeg - 1) / kMaxSeg);
+  const int32_t nseg = (n + len - 1) / len;
+  // the per-unit count array is free between iterations; it holds the segment keys
+  unsigned long long* seg = reinterpret_cast<unsigned long long*>(s.cnt);
+  if (nseg > 0)
+    gr_segmax<<<(nseg * 64 + kBlock - 1) / kBlock, kBlock, 0, st>>>(n, len, nseg, s.err, seg);
+  gr_insert<<<1, 1024, 0, st>>>(n, count, n_max, len, alpha, half_cap, seg, s.rp[cur],
+                                s.col[cur], s.age[cur], s.x, s.y, s.z, s.err, s.status);
   return hipGetLastError();
 }
 

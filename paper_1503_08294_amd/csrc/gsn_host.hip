@@ -103,7 +103,7 @@ using gsn::DevState;
 
 enum Phase { kReady = 0, kFound = 1, kResolved = 2, kAdapted = 3 };
 constexpr int kRebucketEvery = 16;
-constexpr int kDefaultGridRounds = 6;
+constexpr int kDefaultGridRounds = 6;  // before any update has reported back
 
 struct gsn_net {
   gsn_params p;
@@ -118,7 +118,8 @@ struct gsn_net {
   bool timing;
   int32_t bucket_n;            // unit count at the last spatial bucketing (-1: none yet)
   int32_t finds_since_bucket;
-  int grid_rounds;             // grid-wide rounds of the winner-lock update
+  int grid_rounds;             // grid-wide rounds of the winner-lock update (0: automatic)
+  int32_t* feedback;           // pinned host copy of the last update's grid rounds used
   std::vector<hipEvent_t> pool;
   std::vector<std::pair<hipEvent_t, hipEvent_t>> rec[GSN_T_COUNT];
 };
@@ -265,7 +266,13 @@ int gsn_create(const gsn_params* params, void* workspace, size_t workspace_bytes
   net->timing = false;
   net->bucket_n = -1;
   net->finds_since_bucket = 0;
-  net->grid_rounds = kDefaultGridRounds;
+  net->grid_rounds = 0;
+  net->feedback = nullptr;
+  if (hipHostMalloc(reinterpret_cast<void**>(&net->feedback), sizeof(int32_t)) != hipSuccess) {
+    delete net;
+    return GSN_E_HIP;
+  }
+  *net->feedback = kDefaultGridRounds - 1;
   int dev = 0, cus = 256;
   if (hipGetDevice(&dev) == hipSuccess &&
       hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess)
@@ -364,11 +371,19 @@ int gsn_adapt(gsn_net* net, const float* sig, int32_t m, const int32_t* winner,
   TimedRegion t(net, GSN_T_ADAPT, st);
   hipError_t e;
   if (net->p.lock_mode == 1 && m > 0 && net->n > 0) {
+    // automatic: one grid round more than the last update used (read from the pinned copy
+    // of its count; a stale value only changes the split, never the result)
+    int g = net->grid_rounds;
+    if (g == 0) g = std::clamp(*static_cast<volatile int32_t*>(net->feedback) + 1, 1,
+                               gsn::kMaxGridRounds);
     gsn::WinnerStep w{sig, m, winner, second, d1, accepted, net->p.key_mode, net->p.eps_b,
-                      net->p.eps_n, net->p.err_beta, net->p.max_age, net->grid_rounds,
+                      net->p.eps_n, net->p.err_beta, net->p.max_age, g,
                       2 * (static_cast<int64_t>(net->p.e_max) + net->p.m_max),
                       2 * static_cast<int64_t>(net->p.e_max)};
     e = gsn::launch_winner_update(net->s, net->cur, net->n, w, st);
+    if (e == hipSuccess)
+      e = hipMemcpyAsync(net->feedback, net->s.rem + gsn::kRmGridUsed, sizeof(int32_t),
+                         hipMemcpyDeviceToHost, st);
   } else {
     e = gsn::launch_adapt(net->s, net->cur, net->n, sig, m, winner, second, d1, accepted,
                           net->p.eps_b, net->p.eps_n, net->p.err_beta, st);
@@ -631,6 +646,7 @@ void gsn_destroy(gsn_net* net) {
       (void)hipEventDestroy(pr.second);
     }
   for (hipEvent_t e : net->pool) (void)hipEventDestroy(e);
+  if (net->feedback) (void)hipHostFree(net->feedback);
   delete net;
 }
 
@@ -646,7 +662,7 @@ int gsn_tune(gsn_net* net, int32_t key, int32_t value) {
       net->tune_variant = value;
       return GSN_OK;
     case GSN_TUNE_GRID_ROUNDS:
-      if (value < 0 || value > gsn::kMaxGridRounds) return GSN_E_INVAL;
+      if (value < 0 || value > gsn::kMaxGridRounds) return GSN_E_INVAL;  // 0: automatic
       net->grid_rounds = value;
       return GSN_OK;
     default:

@@ -33,8 +33,12 @@ enum RoundSlot {
   kRmRounds,       // rounds summed over the updates since the last clear
   kRmRoundsMax,    // the most rounds one update took
   kRmUpdates,      // updates since the last clear
+  kRmGridUsed,     // grid-wide rounds that did work in the last update
   kRmSlots
 };
+// A grid-wide round is skipped, and its signals left to the single-workgroup rounds, once
+// fewer than this many survivors are pending.
+constexpr int kTailMin = 128;
 
 // 64-bit accumulators (DevState::acc64).
 enum Acc64Slot {

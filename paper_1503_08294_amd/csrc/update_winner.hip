@@ -179,8 +179,10 @@ __global__ void wl_write(int32_t n, const int32_t* __restrict__ rp,
 constexpr int kRoundBlock = 64;    // threads per workgroup of the grid-wide rounds
 constexpr int kTailBlock = 1024;   // threads of the single workgroup of the last rounds
 
-// The lock words are read and released with agent-scope atomics: the last rounds run in
-// one workgroup whose claims and checks are separated by barriers, not by kernel ends.
+// The lock words are read and released with agent-scope atomics (at L2): the grid-wide
+// rounds of several workgroups and the claims (atomic minima) meet there.  The last rounds
+// run in one workgroup whose phases are separated by barriers, not by kernel ends; the
+// barrier's workgroup-scope ordering covers the rows and flags its waves share.
 __device__ __forceinline__ unsigned long long lock_read(unsigned long long* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -299,10 +301,11 @@ __device__ void apply(const RoundArgs& a, int32_t j) {
 }
 
 // Grid-wide round t: rem[t] counts the signals left pending; a round after one that left
-// none returns at once.
+// fewer than kTailMin returns at once (the single-workgroup rounds take them), and so do
+// the later ones (their counts stay zero).
 __global__ void wl_claim(RoundArgs a, int32_t t) {
   if (blockIdx.x == 0 && threadIdx.x == 0) a.rem[t] = 0;
-  if (t > 0 && a.rem[t - 1] == 0) return;
+  if (t > 0 && a.rem[t - 1] < kTailMin) return;
   const int32_t j = blockIdx.x * kRoundBlock + threadIdx.x;
   if (j < a.m && a.pend[j] == 1) claim(a, j);
 }
@@ -389,7 +392,7 @@ __device__ bool group_try_apply(const RoundArgs& a, int32_t j, int q) {
 }
 
 __global__ void wl_step(RoundArgs a, int32_t t) {
-  if (t > 0 && a.rem[t - 1] == 0) return;
+  if (t > 0 && a.rem[t - 1] < kTailMin) return;
   const int32_t gt = blockIdx.x * kRoundBlock + threadIdx.x;
   const int32_t j = gt / kGroup;
   const int q = gt % kGroup;
@@ -405,8 +408,8 @@ __global__ void wl_step(RoundArgs a, int32_t t) {
 }
 
 // The remaining rounds in one workgroup: the pending signals are gathered into a list, and
-// every round claims, applies where it may and re-gathers them, with a device-scope fence
-// and a barrier between the phases.  Each round applies at least the pending signal of smallest
+// every round claims, applies where it may and re-gathers them, with a barrier between the
+// phases.  Each round applies at least the pending signal of smallest
 // key, so the loop ends after at most as many rounds as signals were pending; a round
 // without progress ends it with an error.  Also adds this update's round count to the
 // statistics and clears the survivor count.
@@ -414,39 +417,35 @@ __global__ __launch_bounds__(kTailBlock) void wl_tail(RoundArgs a, int32_t grid_
   __shared__ int32_t s_n, s_next, s_rounds;
   const int tid = threadIdx.x;
   if (tid == 0) {
-    const int32_t survivors = a.rem[kRmSurvivors];
-    int32_t g = 0;
-    for (int32_t t = 0; t < grid_rounds; ++t) g += (t == 0 ? survivors : a.rem[t - 1]) > 0;
-    s_rounds = g;
+    // grid rounds that ran: the first, then each one after a round that left kTailMin or
+    // more; those that applied something: the ones that found survivors pending
+    int32_t ran = grid_rounds > 0 ? 1 : 0;
+    while (ran < grid_rounds && a.rem[ran - 1] >= kTailMin) ++ran;
+    s_rounds = ran > 0 && a.rem[kRmSurvivors] > 0 ? ran : 0;
+    a.rem[kRmGridUsed] = ran;
     s_n = 0;
     s_next = 0;
   }
   __syncthreads();
-  const bool any = grid_rounds == 0 || a.rem[grid_rounds - 1] > 0;
   int32_t* cur = a.list;
   int32_t* nxt = a.list + a.m;
-  if (any)
-    for (int32_t j = tid; j < a.m; j += kTailBlock)
-      if (a.pend[j] == 1) cur[atomicAdd(&s_n, 1)] = j;
-  __threadfence();
+  for (int32_t j = tid; j < a.m; j += kTailBlock)
+    if (a.pend[j] == 1) cur[atomicAdd(&s_n, 1)] = j;
   __syncthreads();
   for (;;) {
     const int32_t n = s_n;
     if (n == 0) break;
     for (int32_t i = tid; i < n; i += kTailBlock) claim(a, cur[i]);
-    __threadfence();
     __syncthreads();
     for (int32_t i = tid / kGroup; i < n; i += kTailBlock / kGroup) {
       const int32_t j = cur[i];
       if (group_try_apply(a, j, tid % kGroup) && tid % kGroup == 0) a.pend[j] = 0;
     }
-    __threadfence();
     __syncthreads();
     for (int32_t i = tid; i < n; i += kTailBlock) {
       const int32_t j = cur[i];
       if (a.pend[j] == 1) nxt[atomicAdd(&s_next, 1)] = j;
     }
-    __threadfence();
     __syncthreads();
     if (tid == 0) {
       // no progress means the lock words were not all ones on entry (a corrupted
