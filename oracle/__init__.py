@@ -101,6 +101,19 @@ class Schedule:
                          self.max_signals, self.qe_threshold, self.seed)
 
 
+class _Grid(ctypes.Structure):
+    _fields_ = [("lo", ctypes.c_float * 3), ("h", ctypes.c_float), ("dims", ctypes.c_int32 * 3)]
+
+
+def _grid(lo, h, dims) -> _Grid:
+    g = _Grid()
+    for a in range(3):
+        g.lo[a] = float(lo[a])
+        g.dims[a] = int(dims[a])
+    g.h = float(h)
+    return g
+
+
 _lib = None
 
 
@@ -134,6 +147,11 @@ def _load():
     lib.orc_run_schedule.argtypes = [P, P, ctypes.c_int64, ctypes.POINTER(_Schedule),
                                      ctypes.POINTER(_ScheduleResult), i32]
     lib.orc_run_schedule.restype = ctypes.c_int
+    lib.orc_grid_cell.argtypes = [ctypes.POINTER(_Grid), ctypes.c_float, ctypes.c_float,
+                                  ctypes.c_float, P]
+    lib.orc_grid_cell.restype = None
+    lib.orc_find_winners_grid.argtypes = [P, ctypes.POINTER(_Grid), P, i32, P, P, P, P, P, i32]
+    lib.orc_find_winners_grid.restype = ctypes.c_int
     for f in ("orc_create", "orc_find_winners", "orc_resolve_conflicts", "orc_adapt",
               "orc_update_edges", "orc_grow", "orc_sizes", "orc_status", "orc_export",
               "orc_import", "orc_age"):
@@ -149,6 +167,14 @@ def splitmix64(seed: int, counter: int) -> int:
 
 def schedule_m(n: int, m_cap: int, fixed_m: int = 0) -> int:
     return int(_load().orc_schedule_m(n, m_cap, fixed_m))
+
+
+def grid_cell(lo, h, dims, point) -> tuple:
+    """Cell coordinates of a point in the index grid (see gsn_oracle.c)."""
+    c = np.zeros(3, np.int32)
+    _load().orc_grid_cell(ctypes.byref(_grid(lo, h, dims)), float(point[0]), float(point[1]),
+                          float(point[2]), ctypes.c_void_p(c.ctypes.data))
+    return tuple(int(v) for v in c)
 
 
 def _ptr(a: np.ndarray | None):
@@ -216,6 +242,23 @@ class Oracle:
         _check(_load().orc_find_winners(self._h, _ptr(s), m, _ptr(w), _ptr(sc), _ptr(d1),
                                         _ptr(d2), self.threads), "orc_find_winners")
         return w, sc, d1, d2
+
+    def find_winners_grid(self, sig, lo, h, dims):
+        """The indexed search of the paper's "Indexed" implementation on every signal.
+        Returns winner, second, d1, d2 and the number of signals that fell back to the
+        exhaustive search."""
+        s = _soa(sig)
+        m = s.shape[1]
+        w = np.empty(m, np.int32)
+        sc = np.empty(m, np.int32)
+        d1 = np.empty(m, np.float32)
+        d2 = np.empty(m, np.float32)
+        fb = ctypes.c_int32()
+        _check(_load().orc_find_winners_grid(self._h, ctypes.byref(_grid(lo, h, dims)), _ptr(s),
+                                             m, _ptr(w), _ptr(sc), _ptr(d1), _ptr(d2),
+                                             ctypes.byref(fb), self.threads),
+               "orc_find_winners_grid")
+        return w, sc, d1, d2, fb.value
 
     def resolve_conflicts(self, winner, second, d1):
         w = np.ascontiguousarray(winner, np.int32)

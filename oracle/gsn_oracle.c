@@ -74,6 +74,18 @@
  * (double)sum * 2^-32 / (double)count.  Per iteration: draw, find, resolve, adapt, update
  * edges, accumulate, remove orphaned units, insert, then the window test and the signal cap.
  *
+ * Indexed find winners (orc_find_winners_grid) is the hash index of the paper's "Indexed"
+ * implementation (Sec. 3.1) applied to every signal of the batch: a grid of cubes of side h
+ * over an axis-parallel box that holds the input signals; the winner and the second are
+ * searched among the units of the signal's cube and its 26 neighbours, and the exhaustive
+ * search is used when that search fails (fewer than two units there).  Readings: the cell
+ * of a point p is c_a = floor((p_a - lo_a) * inv_h) per axis, inv_h = 1 / h rounded to
+ * binary32 and every operation in binary32, clamped to [0, dims_a - 1] (so points outside
+ * the box fall into its border cells); candidates are the units whose cell differs from
+ * the signal's by at most one on every axis; among them the order is the same (d, index)
+ * order as the exhaustive search.  The result can differ from the exhaustive one when a
+ * unit outside the 27 cubes is nearer than the second found inside, as the paper notes.
+ *
  * Build: gcc -O2 -ffp-contract=off -fopenmp -shared -fPIC (no -ffast-math, no -march).
  */
 #include <stdint.h>
@@ -762,4 +774,84 @@ int orc_run_schedule(orc_net* g, const float* cloud, int64_t n_points, const orc
   free(sig); free(w); free(sc); free(d1); free(d2); free(acc);
   if (rc != ORC_OK && rc != ORC_E_STATE) g->status = rc;
   return rc;
+}
+
+/* ------------------------------------------------------------ indexed search --- */
+
+typedef struct {
+  float lo[3];     /* corner of the box */
+  float h;         /* side of a cube, > 0 */
+  int32_t dims[3]; /* cubes per axis, >= 1 */
+} orc_grid;
+
+static int32_t grid_axis(float p, float lo, float inv_h, int32_t dim) {
+  const float t = (p - lo) * inv_h;
+  if (!(t >= 0.0f)) return 0;          /* below the box (also NaN) */
+  if (t >= (float)dim) return dim - 1;  /* beyond it */
+  const int32_t c = (int32_t)floorf(t);
+  return c < dim ? c : dim - 1;
+}
+
+/* Cell coordinates of a point (the reading in the header). */
+void orc_grid_cell(const orc_grid* gr, float x, float y, float z, int32_t* c) {
+  const float inv_h = 1.0f / gr->h;
+  c[0] = grid_axis(x, gr->lo[0], inv_h, gr->dims[0]);
+  c[1] = grid_axis(y, gr->lo[1], inv_h, gr->dims[1]);
+  c[2] = grid_axis(z, gr->lo[2], inv_h, gr->dims[2]);
+}
+
+int orc_find_winners_grid(const orc_net* g, const orc_grid* gr, const float* sig, int32_t m,
+                          int32_t* winner, int32_t* second, float* d1, float* d2,
+                          int32_t* fell_back, int threads) {
+  if (!g || !gr || m < 0 || g->n < 2) return ORC_E_INVAL;
+  if (!(gr->h > 0.0f) || gr->dims[0] < 1 || gr->dims[1] < 1 || gr->dims[2] < 1)
+    return ORC_E_INVAL;
+  if (m > 0 && (!sig || !winner || !second || !d1 || !d2)) return ORC_E_INVAL;
+  const int32_t n = g->n;
+  int32_t* ucell = (int32_t*)malloc(sizeof(int32_t) * 3 * (size_t)n);
+  if (!ucell) return ORC_E_CAPACITY;
+  for (int32_t i = 0; i < n; ++i) orc_grid_cell(gr, g->x[i], g->y[i], g->z[i], &ucell[3 * i]);
+  int32_t fb = 0;
+#ifdef _OPENMP
+#pragma omp parallel for schedule(dynamic, 64) num_threads(threads > 0 ? threads : 1) reduction(+ : fb)
+#endif
+  for (int32_t j = 0; j < m; ++j) {
+    const float sx = sig[j], sy = sig[(size_t)m + j], sz = sig[2 * (size_t)m + j];
+    int32_t c[3];
+    orc_grid_cell(gr, sx, sy, sz, c);
+    float bd = 0.0f, sd = 0.0f;
+    int32_t bi = -1, si = -1, found = 0;
+    for (int32_t i = 0; i < n; ++i) {
+      const int32_t* u = &ucell[3 * i];
+      if (abs(u[0] - c[0]) > 1 || abs(u[1] - c[1]) > 1 || abs(u[2] - c[2]) > 1) continue;
+      ++found;
+      const float dx = sx - g->x[i], dy = sy - g->y[i], dz = sz - g->z[i];
+      const float d = (dx * dx + dy * dy) + dz * dz;
+      if (bi < 0 || key_less(d, i, bd, bi)) {
+        si = bi; sd = bd;
+        bi = i; bd = d;
+      } else if (si < 0 || key_less(d, i, sd, si)) {
+        si = i; sd = d;
+      }
+    }
+    if (found < 2) {
+      /* the search failed: the exhaustive search */
+      ++fb;
+      bi = si = -1;
+      for (int32_t i = 0; i < n; ++i) {
+        const float dx = sx - g->x[i], dy = sy - g->y[i], dz = sz - g->z[i];
+        const float d = (dx * dx + dy * dy) + dz * dz;
+        if (bi < 0 || key_less(d, i, bd, bi)) {
+          si = bi; sd = bd;
+          bi = i; bd = d;
+        } else if (si < 0 || key_less(d, i, sd, si)) {
+          si = i; sd = d;
+        }
+      }
+    }
+    winner[j] = bi; second[j] = si; d1[j] = bd; d2[j] = sd;
+  }
+  free(ucell);
+  if (fell_back) *fell_back = fb;
+  return ORC_OK;
 }
