@@ -112,6 +112,30 @@ int gsn_create(const gsn_params* params, void* workspace, size_t workspace_bytes
 int gsn_find_winners(gsn_net* net, const float* sig, int32_t m, int32_t* winner,
                      int32_t* second, float* d1, float* d2, void* stream);
 
+/* Indexed find winners: the hash index of the paper's "Indexed" implementation (Sec. 3.1)
+ * applied to every signal of the batch.  A grid of cubes of side h covers the axis-parallel
+ * box with corner lo (the box should hold the input signals); the cube of a point p is
+ * c_a = floor((p_a - lo_a) * inv_h), inv_h = 1/h rounded to binary32, each operation in
+ * binary32, clamped to [0, dims_a - 1].  For every signal, winner, second, d1 and d2 are
+ * those of gsn_find_winners restricted to the units whose cube is within one cube of the
+ * signal's on every axis (the signal's cube and its 26 neighbours); when fewer than two
+ * units are there, the exhaustive search is used.  Like the paper's index this is
+ * approximate: a unit outside the 27 cubes can be nearer than the second found.
+ * grid_ws: device memory of gsn_grid_workspace_bytes() bytes (256-byte aligned, the
+ * caller's, reused across calls; any contents).  Same order rules and outputs as
+ * gsn_find_winners; GSN_E_INVAL for an invalid grid, GSN_E_CAPACITY for a small workspace.
+ * Async. */
+typedef struct gsn_grid {
+  float lo[3];       /* box corner, finite */
+  float h;           /* side of a cube, finite, > 0 */
+  int32_t dims[3];   /* cubes per axis, >= 1, product <= GSN_MAX_GRID_CELLS */
+} gsn_grid;
+#define GSN_MAX_GRID_CELLS (1 << 24)
+size_t gsn_grid_workspace_bytes(const gsn_grid* grid, int32_t n_max, int32_t m_max);
+int gsn_find_winners_grid(gsn_net* net, const gsn_grid* grid, void* grid_ws,
+                          size_t grid_ws_bytes, const float* sig, int32_t m, int32_t* winner,
+                          int32_t* second, float* d1, float* d2, void* stream);
+
 /* Collision handling (Sec. 2.2: signals whose updates would move the same unit, change
  * the same neighbourhood or add the same edge collide; an implicit lock lets one of them
  * take effect and discards the others).  With GSN_LOCK_SET, signal j locks L_j =

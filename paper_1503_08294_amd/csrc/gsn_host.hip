@@ -5,6 +5,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <cmath>
 #include <new>
 #include <vector>
 
@@ -142,6 +143,20 @@ bool params_ok(const gsn_params* p) {
 }
 
 inline hipStream_t as_stream(void* st) { return static_cast<hipStream_t>(st); }
+
+bool grid_ok(const gsn_grid* g, int64_t* cells) {
+  if (!g) return false;
+  if (!(g->h > 0.0f) || !std::isfinite(g->h)) return false;
+  if (!std::isfinite(1.0f / g->h)) return false;
+  int64_t c = 1;
+  for (int a = 0; a < 3; ++a) {
+    if (!std::isfinite(g->lo[a]) || g->dims[a] < 1) return false;
+    c *= g->dims[a];
+    if (c > GSN_MAX_GRID_CELLS) return false;
+  }
+  *cells = c;
+  return true;
+}
 
 inline int hip_ok(hipError_t e) { return e == hipSuccess ? GSN_OK : GSN_E_HIP; }
 
@@ -342,6 +357,41 @@ int gsn_find_winners(gsn_net* net, const float* sig, int32_t m, int32_t* winner,
     if (e == hipSuccess) e = gsn::launch_find_merge(net->s, m, cfg, winner, second, d1, d2, st);
   }
   all.end();
+  return hip_ok(e);
+}
+
+size_t gsn_grid_workspace_bytes(const gsn_grid* grid, int32_t n_max, int32_t m_max) {
+  int64_t cells = 0;
+  if (!grid_ok(grid, &cells) || n_max < 2 || m_max < 1) return 0;
+  return gsn::grid_bytes(cells, n_max, m_max);
+}
+
+int gsn_find_winners_grid(gsn_net* net, const gsn_grid* grid, void* grid_ws,
+                          size_t grid_ws_bytes, const float* sig, int32_t m, int32_t* winner,
+                          int32_t* second, float* d1, float* d2, void* stream) {
+  if (!net || m < 0 || m > net->p.m_max) return GSN_E_INVAL;
+  if (net->phase != kReady && net->phase != kFound) return GSN_E_STATE;
+  int64_t cells = 0;
+  if (!grid_ok(grid, &cells) || !grid_ws) return GSN_E_INVAL;
+  if (reinterpret_cast<uintptr_t>(grid_ws) % 256 != 0) return GSN_E_INVAL;
+  if (grid_ws_bytes < gsn::grid_bytes(cells, net->p.n_max, net->p.m_max)) return GSN_E_CAPACITY;
+  if (net->n < 2) return GSN_E_INVAL;
+  if (m > 0 && (!sig || !winner || !second || !d1 || !d2)) return GSN_E_INVAL;
+  net->phase = kFound;
+  if (m == 0) return GSN_OK;
+  hipStream_t st = as_stream(stream);
+  gsn::GridSpec spec{};
+  for (int a = 0; a < 3; ++a) {
+    spec.lo[a] = grid->lo[a];
+    spec.dims[a] = grid->dims[a];
+  }
+  spec.inv_h = 1.0f / grid->h;
+  spec.cells = cells;
+  const gsn::GridBufs gb = gsn::carve_grid(grid_ws, cells, net->p.n_max, net->p.m_max);
+  TimedRegion t(net, GSN_T_FIND, st);
+  hipError_t e = gsn::launch_find_grid(net->s, gb, spec, net->n, sig, m, winner, second, d1,
+                                       d2, st);
+  t.end();
   return hip_ok(e);
 }
 

@@ -220,6 +220,28 @@ hipError_t launch_init(const DevState& s, int cur, int32_t n0, int32_t n_max,
                        hipStream_t st);
 hipError_t launch_remove(const DevState& s, int cur, int32_t n, int32_t n_max,
                          hipStream_t st);
+// Indexed find winners (find_grid.hip): the grid and the caller's grid workspace.
+struct GridSpec {
+  float lo[3];
+  float inv_h;       // 1 / h rounded to binary32 (the cell function multiplies by it)
+  int32_t dims[3];
+  int64_t cells;
+};
+struct GridBufs {
+  int32_t* cnt;      // [cells + 1] units per cube, then scatter cursors
+  int32_t* start;    // [cells + 1] first sorted slot of every cube
+  int32_t* bsum;     // [cells / kBlock + 2]
+  float4* sorted;    // [n_max] units by cube: (x, y, z, index bits)
+  int32_t* ucell;    // [n_max] cube of every unit
+  int32_t* fb_list;  // [m_max] signals that fell back to the exhaustive search
+  int32_t* nfb;      // their count
+};
+size_t grid_bytes(int64_t cells, int32_t n_max, int32_t m_max);
+GridBufs carve_grid(void* base, int64_t cells, int32_t n_max, int32_t m_max);
+hipError_t launch_find_grid(const DevState& s, const GridBufs& gb, const GridSpec& spec,
+                            int32_t n, const float* sig, int32_t m, int32_t* winner,
+                            int32_t* second, float* d1, float* d2, hipStream_t st);
+
 // Schedule kernels (schedule.hip): draw m signals (signal numbers c0 + 1 .. c0 + m) from
 // the cloud, and add the winners' distances of m signals to the error window.
 hipError_t launch_draw(const float* cloud, int64_t n_points, uint64_t seed, int64_t c0,

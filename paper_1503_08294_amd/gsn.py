@@ -70,6 +70,19 @@ class gsn_params(ctypes.Structure):
     ]
 
 
+class gsn_grid(ctypes.Structure):
+    _fields_ = [("lo", ctypes.c_float * 3), ("h", ctypes.c_float), ("dims", ctypes.c_int32 * 3)]
+
+
+def make_grid(lo, h, dims) -> gsn_grid:
+    g = gsn_grid()
+    for a in range(3):
+        g.lo[a] = float(lo[a])
+        g.dims[a] = int(dims[a])
+    g.h = float(h)
+    return g
+
+
 class gsn_schedule(ctypes.Structure):
     _fields_ = [
         ("m_cap", ctypes.c_int32),
@@ -102,6 +115,9 @@ _sig = {
     "gsn_create": (ctypes.c_int, [ctypes.POINTER(gsn_params), _P, ctypes.c_size_t, _I, _P, _P,
                                   ctypes.POINTER(_P)]),
     "gsn_find_winners": (ctypes.c_int, [_P, _P, _I, _P, _P, _P, _P, _P]),
+    "gsn_grid_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(gsn_grid), _I, _I]),
+    "gsn_find_winners_grid": (ctypes.c_int, [_P, ctypes.POINTER(gsn_grid), _P, ctypes.c_size_t,
+                                             _P, _I, _P, _P, _P, _P, _P]),
     "gsn_resolve_conflicts": (ctypes.c_int, [_P, _I, _P, _P, _P, _P, _P]),
     "gsn_adapt": (ctypes.c_int, [_P, _P, _I, _P, _P, _P, _P, _P]),
     "gsn_update_edges": (ctypes.c_int, [_P, _I, _P, _P, _P, _P]),
@@ -272,6 +288,21 @@ def gsn_timing_read(net, which: int):
     return ms.value, cnt.value
 
 
+def gsn_grid_workspace_bytes(grid: gsn_grid, n_max: int, m_max: int) -> int:
+    return int(_lib.gsn_grid_workspace_bytes(ctypes.byref(grid), n_max, m_max))
+
+
+def gsn_find_winners_grid(net, grid: gsn_grid, grid_ws: torch.Tensor, sig: torch.Tensor, m: int,
+                          winner, second, d1, d2, stream=None):
+    _check(_lib.gsn_find_winners_grid(net, ctypes.byref(grid), _dev(grid_ws, torch.uint8),
+                                      grid_ws.numel(), _dev(sig, torch.float32, 3 * m, "sig"),
+                                      m, _dev(winner, torch.int32, m, "winner"),
+                                      _dev(second, torch.int32, m, "second"),
+                                      _dev(d1, torch.float32, m, "d1"),
+                                      _dev(d2, torch.float32, m, "d2"), _stream(stream)),
+           "gsn_find_winners_grid")
+
+
 def make_schedule(m_cap=8192, fixed_m=0, insert_every=100, qe_window=8192,
                   max_signals=1 << 20, qe_threshold=0.0, seed=0) -> gsn_schedule:
     return gsn_schedule(m_cap, fixed_m, insert_every, qe_window, max_signals, qe_threshold,
@@ -348,6 +379,24 @@ class Network:
         m = sig.shape[1]
         b = self.buf
         gsn_find_winners(self.h, sig, m, b.winner, b.second, b.d1, b.d2, self.stream)
+        return b.winner[:m], b.second[:m], b.d1[:m], b.d2[:m]
+
+    def grid_workspace(self, grid: gsn_grid) -> torch.Tensor:
+        """A 256-byte aligned device buffer for gsn_find_winners_grid with this grid."""
+        size = gsn_grid_workspace_bytes(grid, self.params.n_max, self.params.m_max)
+        if size == 0:
+            raise GsnError(GSN_E_INVAL, "gsn_grid_workspace_bytes")
+        raw = torch.empty(size + 256, dtype=torch.uint8, device=self.device)
+        off = (-raw.data_ptr()) % 256
+        ws = raw[off:off + size]
+        ws._raw = raw  # keep the allocation alive with the view
+        return ws
+
+    def find_winners_grid(self, sig: torch.Tensor, grid: gsn_grid, grid_ws: torch.Tensor):
+        m = sig.shape[1]
+        b = self.buf
+        gsn_find_winners_grid(self.h, grid, grid_ws, sig, m, b.winner, b.second, b.d1, b.d2,
+                              self.stream)
         return b.winner[:m], b.second[:m], b.d1[:m], b.d2[:m]
 
     def resolve_conflicts(self, m, winner=None, second=None, d1=None):
