@@ -213,6 +213,9 @@ def main():
                          "or the winner alone with the survivors applied in key order")
     ap.add_argument("--key", choices=("dist", "index"), default="dist",
                     help="survivor priority: (winner distance, index) or the index alone")
+    ap.add_argument("--grid-cell", type=float, default=0.0,
+                    help="find winners with the paper's hash index (cubes of this side over "
+                         "the cloud's box) instead of the exhaustive search; 0 = exhaustive")
     ap.add_argument("--schedule", action="store_true",
                     help="instead of fixed-size steps, time one growing-network run "
                          "(gsn_run_schedule) from two units to the quantization-error "
@@ -257,9 +260,22 @@ def main():
     params = gsn.make_params(wl.eps_b, wl.eps_n, wl.max_age, wl.err_alpha, wl.err_beta,
                              cap["n_max"], cap["e_max"], cap["m_max"], lock_mode, key_mode)
     net = gsn.Network(params, torch.from_numpy(units).cuda())
+    grid = grid_ws = None
+    if args.grid_cell > 0:
+        lo = cloud.min(axis=0) - np.float32(1e-3)
+        hi = cloud.max(axis=0) + np.float32(1e-3)
+        dims = [int(np.ceil((hi[a] - lo[a]) / args.grid_cell)) for a in range(3)]
+        grid = gsn.make_grid([float(v) for v in lo], args.grid_cell, dims)
+        grid_ws = net.grid_workspace(grid)
 
     def step(t):
-        net.iterate(dev_sig[t])
+        if grid is None:
+            net.iterate(dev_sig[t])
+        else:
+            net.find_winners_grid(dev_sig[t], grid, grid_ws)
+            net.resolve_conflicts(m)
+            net.adapt(dev_sig[t])
+            net.update_edges(m)
         if wl.grow:
             net.grow(t + 1, wl.insert_every)
 
@@ -294,12 +310,36 @@ def main():
 
     # one more untimed iteration to report the conflict rate at this state
     t_last = args.warmup + args.steps
-    acc = net.iterate(dev_sig[t_last])[4]
+    index_stats = None
+    if grid is not None:
+        # the index against the exhaustive search on this state and batch
+        gw, gs_, gd1, _ = [t.clone() for t in net.find_winners_grid(dev_sig[t_last], grid,
+                                                                    grid_ws)]
+        ew, es, ed1, _ = net.find_winners(dev_sig[t_last])
+        index_stats = {"cell": args.grid_cell, "dims": list(grid.dims),
+                       "winner_differs": float((gw != ew).float().mean().item()),
+                       "second_differs": float((gs_ != es).float().mean().item()),
+                       "d1_excess_mean": float((gd1 - ed1).double().mean().item()),
+                       "exhaustive_find_ms_same_state": None}
+        gsn.gsn_timing_enable(net.h, True)
+        for _ in range(10):
+            net.find_winners(dev_sig[t_last])
+        torch.cuda.synchronize()
+        gsn.gsn_timing_enable(net.h, False)
+        ms_ex, cnt_ex = gsn.gsn_timing_read(net.h, gsn.GSN_T_FIND)
+        gsn.gsn_timing_read(net.h, gsn.GSN_T_FIND_SCAN)
+        index_stats["exhaustive_find_ms_same_state"] = ms_ex / max(cnt_ex, 1)
+        net.resolve_conflicts(m)
+        net.adapt(dev_sig[t_last])
+        net.update_edges(m)
+        acc = net.buf.accepted[:m]
+    else:
+        acc = net.iterate(dev_sig[t_last])[4]
     conflict_rate = 1.0 - float(acc.sum().item()) / m
     n_units, n_edges = net.sizes()
 
     ms_per_step = 1e3 * elapsed / args.steps
-    scan_s = phase["find_scan"] * 1e-3
+    scan_s = max(phase["find_scan"], 1e-9) * 1e-3
     achieved = FLOPS_PER_EVAL * m * n / scan_s / 1e12
     traffic = load_traffic(m * n)
     out = {
@@ -318,6 +358,8 @@ def main():
         "config": {"workload": wl.name, "n_units": n, "m_signals": m,
                    "cloud_points": wl.n_points, "cloud": "genus-3 tube surface",
                    "iteration": "find+resolve+adapt+update_edges", "parallelism": "single",
+                   "find": ("exhaustive" if grid is None else
+                            f"hash index, cubes of side {args.grid_cell}"),
                    "collision": {"lock": args.lock, "key": args.key}},
         "signals_per_s": m * args.steps / elapsed,
         "fw_evals_per_s": m * n / (phase["find"] * 1e-3),
@@ -327,6 +369,7 @@ def main():
         "conflict_rate": conflict_rate,
         "state_after": {"units": n_units, "edges": n_edges},
         "update_rounds": rounds,
+        "index": index_stats,
         "roofline": {"bound": "mfma", "kernel": SCAN_KERNEL, "dtype": "f16",
                      "achieved": achieved, "peak": F16_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / F16_PEAK_TFLOPS, "traffic": traffic,
@@ -338,6 +381,8 @@ def main():
                      "achieved_vs_fp32_peak": achieved / FP32_PEAK_TFLOPS},
         "cpu_baseline": None,
     }
+    if grid is not None:
+        out["roofline"] = None   # the scan kernel does not run; see "index"
     if args.cpu_budget > 0:
         print(f"[bench] cpu baseline (~{args.cpu_budget:.0f} s)", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(wl, units, cloud, args.cpu_budget, lock_mode,
