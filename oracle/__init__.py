@@ -51,7 +51,8 @@ class Params:
     n_max: int = 1024
     e_max: int = 4096
     m_max: int = 1024
-    lock_mode: int = 0   # 0: lock set {b, s} + N(b); 1: winner only, sequential update
+    lock_mode: int = 0   # 0: lock set {b, s} + N(b); 1: winner only, sequential update;
+    #                      2: lock set, greedy in key order
     key_mode: int = 0    # 0: (bits(d1) << 32) | j; 1: j (arrival order)
 
     def c(self) -> _Params:

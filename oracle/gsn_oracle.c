@@ -74,6 +74,12 @@
  * (double)sum * 2^-32 / (double)count.  Per iteration: draw, find, resolve, adapt, update
  * edges, accumulate, remove orphaned units, insert, then the window test and the signal cap.
  *
+ * A third collision rule (lock_mode = 2) keeps the lock sets of lock_mode 0 but takes the
+ * signals greedily in key order: a signal is accepted iff its lock set is disjoint from the
+ * lock set of every signal accepted before it (signals whose blockers were themselves
+ * rejected are re-admitted); accepted lock sets are still pairwise disjoint, so adapt and
+ * the edge update are those of lock_mode 0.
+ *
  * Indexed find winners (orc_find_winners_grid) is the hash index of the paper's "Indexed"
  * implementation (Sec. 3.1) applied to every signal of the batch: a grid of cubes of side h
  * over an axis-parallel box that holds the input signals; the winner and the second are
@@ -111,7 +117,8 @@ typedef struct {
   int32_t n_max;
   int32_t e_max;
   int32_t m_max;
-  int32_t lock_mode;  /* 0: lock set {b, s} + N(b); 1: the winner only, sequential update */
+  int32_t lock_mode;  /* 0: lock set {b, s} + N(b), one round; 1: the winner only,
+                         sequential update; 2: lock set, greedy in key order */
   int32_t key_mode;   /* 0: (bits(d1) << 32) | j; 1: j */
 } orc_params;
 
@@ -216,7 +223,7 @@ static int params_ok(const orc_params* p) {
   if (!(p->eps_n >= 0.0f && p->eps_n <= 1.0f)) return 0;
   if (p->max_age < 0) return 0;
   if (p->n_max < 2 || p->e_max < 0 || p->m_max < 1) return 0;
-  if (p->lock_mode < 0 || p->lock_mode > 1 || p->key_mode < 0 || p->key_mode > 1) return 0;
+  if (p->lock_mode < 0 || p->lock_mode > 2 || p->key_mode < 0 || p->key_mode > 1) return 0;
   return 1;
 }
 
@@ -318,6 +325,9 @@ static int check_pair(const orc_net* g, int32_t b, int32_t s) {
  * 1).  owner[u] = the smallest key among the signals that claim u; j is accepted iff it
  * owns every unit of L_j.
  */
+static int resolve_greedy(const orc_net* g, int32_t m, const int32_t* winner,
+                          const int32_t* second, const float* d1, uint8_t* accepted);
+
 int orc_resolve_conflicts(const orc_net* g, int32_t m, const int32_t* winner,
                           const int32_t* second, const float* d1, uint8_t* accepted) {
   if (!g || m < 0 || m > g->p.m_max) return ORC_E_INVAL;
@@ -325,6 +335,7 @@ int orc_resolve_conflicts(const orc_net* g, int32_t m, const int32_t* winner,
   if (!winner || !second || !d1 || !accepted) return ORC_E_INVAL;
   for (int32_t j = 0; j < m; ++j)
     if (!check_pair(g, winner[j], second[j])) return ORC_E_INVAL;
+  if (g->p.lock_mode == 2) return resolve_greedy(g, m, winner, second, d1, accepted);
   uint64_t* owner = (uint64_t*)malloc(sizeof(uint64_t) * (size_t)(g->n > 0 ? g->n : 1));
   if (!owner) return ORC_E_CAPACITY;
   for (int32_t u = 0; u < g->n; ++u) owner[u] = UINT64_MAX;
@@ -435,6 +446,44 @@ int orc_update_edges(orc_net* g, int32_t m, const int32_t* winner, const int32_t
     g->status = ORC_E_CAPACITY;
     return ORC_E_CAPACITY;
   }
+  return ORC_OK;
+}
+
+/* ----------------------------------------------------- greedy resolve (lock_mode 2) --- */
+
+static const orc_net* greedy_net;   /* the comparator's context (the oracle is not reentrant) */
+static const float* greedy_d1;
+
+static int by_key_greedy(const void* a, const void* b) {
+  const int32_t i = *(const int32_t*)a, j = *(const int32_t*)b;
+  const uint64_t ki = signal_key(greedy_net, greedy_d1[i], i);
+  const uint64_t kj = signal_key(greedy_net, greedy_d1[j], j);
+  return ki < kj ? -1 : (ki > kj ? 1 : 0);
+}
+
+/* The signals in ascending key order; each is accepted iff its lock set {b, s} + N(b) (the
+ * pre-iteration graph) shares no unit with the lock set of a signal accepted before it. */
+static int resolve_greedy(const orc_net* g, int32_t m, const int32_t* winner,
+                          const int32_t* second, const float* d1, uint8_t* accepted) {
+  int32_t* order = (int32_t*)malloc(sizeof(int32_t) * (size_t)m);
+  uint8_t* taken = (uint8_t*)calloc((size_t)(g->n > 0 ? g->n : 1), 1);
+  if (!order || !taken) { free(order); free(taken); return ORC_E_CAPACITY; }
+  for (int32_t j = 0; j < m; ++j) order[j] = j;
+  greedy_net = g;
+  greedy_d1 = d1;
+  qsort(order, (size_t)m, sizeof(int32_t), by_key_greedy);
+  for (int32_t q = 0; q < m; ++q) {
+    const int32_t j = order[q], b = winner[j], s = second[j];
+    int free_set = !taken[b] && !taken[s];
+    for (int32_t k = 0; free_set && k < g->deg[b]; ++k) free_set = !taken[g->nb[b][k]];
+    accepted[j] = (uint8_t)free_set;
+    if (!free_set) continue;
+    taken[b] = 1;
+    taken[s] = 1;
+    for (int32_t k = 0; k < g->deg[b]; ++k) taken[g->nb[b][k]] = 1;
+  }
+  free(order);
+  free(taken);
   return ORC_OK;
 }
 

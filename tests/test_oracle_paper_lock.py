@@ -124,6 +124,6 @@ def test_disjoint_lock_sets_give_the_lock_set_result():
 
 def test_modes_are_validated():
     units = np.zeros((3, 4), np.float32)
-    for bad in (dict(lock_mode=2), dict(key_mode=-1)):
+    for bad in (dict(lock_mode=3), dict(key_mode=-1)):
         with pytest.raises(oracle.OracleError):
             oracle.Oracle(oracle.Params(n_max=8, e_max=8, m_max=4, **bad), units)
