@@ -118,7 +118,8 @@ def run_schedule_bench(args):
     soa = np.ascontiguousarray(cloud.T)
     torch.cuda.set_device(0)
     dev_cloud = torch.from_numpy(soa).cuda()
-    lock_mode = gsn.GSN_LOCK_WINNER if args.lock == "winner" else gsn.GSN_LOCK_SET
+    lock_mode = {"set": gsn.GSN_LOCK_SET, "winner": gsn.GSN_LOCK_WINNER,
+                 "greedy": gsn.GSN_LOCK_SET_GREEDY}[args.lock]
     key_mode = gsn.GSN_KEY_INDEX if args.key == "index" else gsn.GSN_KEY_DIST_INDEX
     n_max = SCHEDULE_N_MAX
     params = gsn.make_params(wl.eps_b, wl.eps_n, wl.max_age, wl.err_alpha, wl.err_beta,
@@ -208,9 +209,10 @@ def main():
                     help="seconds of CPU oracle work for the cpu_baseline leg (0 = skip)")
     ap.add_argument("--copy-calibration", type=int, default=0,
                     help="only run a plain device copy of this many bytes")
-    ap.add_argument("--lock", choices=("set", "winner"), default="set",
+    ap.add_argument("--lock", choices=("set", "winner", "greedy"), default="set",
                     help="collision rule: lock set {b, s} + N(b) with one parallel update, "
-                         "or the winner alone with the survivors applied in key order")
+                         "the winner alone with the survivors applied in key order, or the "
+                         "lock sets taken greedily in key order")
     ap.add_argument("--key", choices=("dist", "index"), default="dist",
                     help="survivor priority: (winner distance, index) or the index alone")
     ap.add_argument("--grid-cell", type=float, default=0.0,
@@ -255,7 +257,8 @@ def main():
     torch.cuda.set_device(0)
     dev_sig = torch.from_numpy(host_sig).cuda()
     cap = wl.capacity()
-    lock_mode = gsn.GSN_LOCK_WINNER if args.lock == "winner" else gsn.GSN_LOCK_SET
+    lock_mode = {"set": gsn.GSN_LOCK_SET, "winner": gsn.GSN_LOCK_WINNER,
+                 "greedy": gsn.GSN_LOCK_SET_GREEDY}[args.lock]
     key_mode = gsn.GSN_KEY_INDEX if args.key == "index" else gsn.GSN_KEY_DIST_INDEX
     params = gsn.make_params(wl.eps_b, wl.eps_n, wl.max_age, wl.err_alpha, wl.err_beta,
                              cap["n_max"], cap["e_max"], cap["m_max"], lock_mode, key_mode)
@@ -296,6 +299,8 @@ def main():
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     gsn.gsn_timing_enable(net.h, False)
+    resolved = net.stat(gsn.GSN_STAT_RESOLVED)
+    accepted_timed = net.stat(gsn.GSN_STAT_ACCEPTED)
     updates = net.stat(gsn.GSN_STAT_UPDATES)
     rounds = ({"mean": net.stat(gsn.GSN_STAT_ROUNDS) / updates,
                "max": net.stat(gsn.GSN_STAT_ROUNDS_MAX)} if updates else None)
@@ -362,6 +367,8 @@ def main():
                             f"hash index, cubes of side {args.grid_cell}"),
                    "collision": {"lock": args.lock, "key": args.key}},
         "signals_per_s": m * args.steps / elapsed,
+        "accepted_per_s": accepted_timed / elapsed,
+        "accepted_fraction": accepted_timed / max(resolved, 1),
         "fw_evals_per_s": m * n / (phase["find"] * 1e-3),
         "fw_frac_fp32_peak": FLOPS_PER_EVAL * m * n / (phase["find"] * 1e-3) / 1e12
                              / FP32_PEAK_TFLOPS,

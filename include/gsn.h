@@ -69,7 +69,8 @@ typedef struct gsn_params {
   int32_t n_max;     /* unit capacity, >= 2 */
   int32_t e_max;     /* undirected edge capacity, >= 0 */
   int32_t m_max;     /* signals per iteration capacity, >= 1 */
-  int32_t lock_mode; /* collision rule: GSN_LOCK_SET (0) or GSN_LOCK_WINNER (1), see below */
+  int32_t lock_mode; /* collision rule: GSN_LOCK_SET (0), GSN_LOCK_WINNER (1) or
+                        GSN_LOCK_SET_GREEDY (2), see below */
   int32_t key_mode;  /* survivor priority: GSN_KEY_DIST_INDEX (0) or GSN_KEY_INDEX (1) */
 } gsn_params;
 
@@ -86,8 +87,14 @@ typedef struct gsn_params {
  *                       Sec. 2.1 (aging, the edge to the second, adaptation, pruning) one
  *                       after another in ascending key order, each on the network its
  *                       predecessors left.  gsn_adapt performs that whole update and
- *                       gsn_update_edges does nothing. */
-enum { GSN_LOCK_SET = 0, GSN_LOCK_WINNER = 1 };
+ *                       gsn_update_edges does nothing.
+ *   GSN_LOCK_SET_GREEDY the lock sets of GSN_LOCK_SET taken in key order: a signal is
+ *                       accepted iff its lock set is disjoint from the lock sets accepted
+ *                       before it (a signal whose blockers were all rejected is accepted);
+ *                       the accepted sets are pairwise disjoint and the update is that of
+ *                       GSN_LOCK_SET.  Resolve runs in rounds (grid-wide, then one
+ *                       workgroup) and stays async. */
+enum { GSN_LOCK_SET = 0, GSN_LOCK_WINNER = 1, GSN_LOCK_SET_GREEDY = 2 };
 enum { GSN_KEY_DIST_INDEX = 0, GSN_KEY_INDEX = 1 };
 
 /* Bytes of device workspace a network with these parameters needs; 0 if the parameters
@@ -138,11 +145,12 @@ int gsn_find_winners_grid(gsn_net* net, const gsn_grid* grid, void* grid_ws,
 
 /* Collision handling (Sec. 2.2: signals whose updates would move the same unit, change
  * the same neighbourhood or add the same edge collide; an implicit lock lets one of them
- * take effect and discards the others).  With GSN_LOCK_SET, signal j locks L_j =
- * {winner[j], second[j]} plus the current neighbours of winner[j]; with GSN_LOCK_WINNER,
- * L_j = {winner[j]}.  Keys follow key_mode.  accepted[j] = 1 iff no other signal with a
- * smaller key locks a unit of L_j, else 0.  With GSN_LOCK_SET, accepted lock sets are
- * pairwise disjoint, so the updates below commute.  Inputs: device arrays of length m as
+ * take effect and discards the others).  With GSN_LOCK_SET (and _GREEDY), signal j locks
+ * L_j = {winner[j], second[j]} plus the current neighbours of winner[j]; with
+ * GSN_LOCK_WINNER, L_j = {winner[j]}.  Keys follow key_mode.  accepted[j] = 1 iff no other
+ * signal with a smaller key locks a unit of L_j (with GSN_LOCK_SET_GREEDY: no accepted
+ * one), else 0.  With the lock sets, accepted lock sets are pairwise disjoint, so the
+ * updates below commute.  Inputs: device arrays of length m as
  * produced by gsn_find_winners (any values with 0 <= winner, second < N and
  * winner != second; others are rejected and flag GSN_E_INVAL on the device).  Output:
  * device uint8[m].  Async. */

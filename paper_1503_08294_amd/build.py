@@ -18,7 +18,7 @@ CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libgsn.so")
 SOURCES = ["gsn_host.hip", "find_winners.hip", "staging.hip", "find_screened.hip",
            "find_mfma.hip", "find_f16.hip", "update.hip", "update_winner.hip", "grow.hip",
-           "schedule.hip", "find_grid.hip"]
+           "schedule.hip", "find_grid.hip", "resolve_greedy.hip"]
 ARCH = "gfx950"
 
 FLAGS = ["-O3", "-std=c++17", f"--offload-arch={ARCH}", "-fPIC", "-shared",

@@ -105,6 +105,7 @@ using gsn::DevState;
 enum Phase { kReady = 0, kFound = 1, kResolved = 2, kAdapted = 3 };
 constexpr int kRebucketEvery = 16;
 constexpr int kDefaultGridRounds = 6;  // before any update has reported back
+constexpr int kGreedyGridRounds = 4;   // grid-wide rounds of the greedy lock-set resolve
 
 struct gsn_net {
   gsn_params p;
@@ -133,7 +134,7 @@ bool params_ok(const gsn_params* p) {
   if (!(p->eps_n >= 0.0f && p->eps_n <= 1.0f)) return false;
   if (p->max_age < 0) return false;
   if (p->n_max < 2 || p->e_max < 0 || p->m_max < 1) return false;
-  if (p->lock_mode < 0 || p->lock_mode > 1 || p->key_mode < 0 || p->key_mode > 1) return false;
+  if (p->lock_mode < 0 || p->lock_mode > 2 || p->key_mode < 0 || p->key_mode > 1) return false;
   // keep every derived index inside int32
   const int64_t slack = p->lock_mode == 1 ? p->m_max : 0;
   if ((static_cast<int64_t>(p->e_max) + slack) * 2 + 2 > INT32_MAX) return false;
@@ -405,8 +406,14 @@ int gsn_resolve_conflicts(gsn_net* net, int32_t m, const int32_t* winner,
   if (m == 0) return GSN_OK;
   hipStream_t st = as_stream(stream);
   TimedRegion t(net, GSN_T_RESOLVE, st);
-  hipError_t e = gsn::launch_resolve(net->s, net->cur, net->n, m, winner, second, d1, accepted,
-                                     net->p.lock_mode, net->p.key_mode, st);
+  hipError_t e =
+      net->p.lock_mode == 2
+          ? gsn::launch_resolve_greedy(net->s, net->cur, net->n, m, winner, second, d1,
+                                       accepted, net->p.key_mode,
+                                       net->grid_rounds ? net->grid_rounds : kGreedyGridRounds,
+                                       st)
+          : gsn::launch_resolve(net->s, net->cur, net->n, m, winner, second, d1, accepted,
+                                net->p.lock_mode, net->p.key_mode, st);
   t.end();
   return hip_ok(e);
 }

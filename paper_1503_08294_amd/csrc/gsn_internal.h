@@ -195,6 +195,14 @@ hipError_t launch_edges(const DevState& s, int cur, int32_t n, int32_t m,
                         const int32_t* winner, const int32_t* second,
                         const uint8_t* accepted, int32_t max_age, int64_t half_cap,
                         hipStream_t st);
+// Greedy lock-set resolve (resolve_greedy.hip): rounds of claims over L_j = {b, s} + N(b),
+// grid_rounds grid-wide, the rest in one workgroup.  Uses lock, extra (as the taken marks),
+// pend (signal states), rem and list.
+hipError_t launch_resolve_greedy(const DevState& s, int cur, int32_t n, int32_t m,
+                                 const int32_t* winner, const int32_t* second, const float* d1,
+                                 uint8_t* accepted, int key_mode, int grid_rounds,
+                                 hipStream_t st);
+
 // The sequential-survivor update (update_winner.hip), all enqueued without a host sync:
 // the slack copy of the CSR in buffer cur ^ 1, grid_rounds grid-wide rounds, the remaining
 // rounds in one workgroup, and the compact CSR back in buffer cur with the error decay.

@@ -1,0 +1,170 @@
+// Greedy lock-set resolve (lock_mode 2): the lock sets L_j = {b_j, s_j} + N(b_j) of the
+// lock-set reading of Sec. 2.2, with the signals taken in key order: j is accepted iff L_j
+// is disjoint from the lock sets accepted before it.  Computed in rounds: every pending
+// signal claims L_j with a 64-bit atomic minimum of its key; a signal that finds a unit of
+// L_j taken by an accepted signal is rejected; one that holds all of L_j is accepted and
+// marks its units taken; the others stay pending.  A signal is settled once every signal of
+// smaller key whose lock set meets L_j is settled, exactly as in the sequential greedy
+// order, so the result is that order's; the pending signal of smallest key is always
+// settled, so every round makes progress.  The first rounds are grid-wide launches, the
+// rest run in one workgroup (as for the winner-lock update).
+#include "gsn_internal.h"
+
+namespace gsn {
+namespace {
+
+constexpr int kRoundBlock = 256;
+constexpr int kTailBlock = 1024;
+
+inline int blocks(int64_t n) { return static_cast<int>((n + kBlock - 1) / kBlock); }
+
+__device__ __forceinline__ unsigned long long lock_read(unsigned long long* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void lock_release(unsigned long long* p) {
+  __hip_atomic_store(p, ~0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+struct GreedyArgs {
+  int32_t m, n;
+  const int32_t* winner;
+  const int32_t* second;
+  const float* d1;
+  int key_mode;
+  const int32_t* rp;
+  const int32_t* col;
+  unsigned long long* lock;
+  int32_t* taken;      // 1: unit of an accepted lock set
+  uint8_t* state;      // 0 rejected, 1 pending, 2 accepted
+  int32_t* rem;
+  int32_t* list;
+  int32_t* status;
+};
+
+__device__ void g_claim(const GreedyArgs& a, int32_t j) {
+  const int32_t b = a.winner[j], s = a.second[j];
+  const unsigned long long key = signal_key(a.d1[j], j, a.key_mode);
+  atomicMin(&a.lock[b], key);
+  atomicMin(&a.lock[s], key);
+  for (int32_t k = a.rp[b]; k < a.rp[b + 1]; ++k) atomicMin(&a.lock[a.col[k]], key);
+}
+
+// Visits every unit of L_j once (s skipped when it is a neighbour of b), releases the ones
+// j holds, and settles j: 0 rejected, 2 accepted (its units marked taken), 1 pending.
+__device__ uint8_t g_check(const GreedyArgs& a, int32_t j) {
+  const int32_t b = a.winner[j], s = a.second[j];
+  const unsigned long long key = signal_key(a.d1[j], j, a.key_mode);
+  bool blocked = false, holds = true;
+  auto visit = [&](int32_t u) {
+    blocked |= a.taken[u] != 0;
+    if (lock_read(&a.lock[u]) == key) lock_release(&a.lock[u]); else holds = false;
+  };
+  visit(b);
+  bool s_nb = false;
+  for (int32_t k = a.rp[b]; k < a.rp[b + 1]; ++k) {
+    const int32_t v = a.col[k];
+    s_nb |= v == s;
+    visit(v);
+  }
+  if (!s_nb) visit(s);
+  if (blocked) return 0;
+  if (!holds) return 1;
+  a.taken[b] = 1;
+  a.taken[s] = 1;
+  for (int32_t k = a.rp[b]; k < a.rp[b + 1]; ++k) a.taken[a.col[k]] = 1;
+  return 2;
+}
+
+__global__ void rg_init(GreedyArgs a) {
+  const int32_t i = blockIdx.x * kBlock + threadIdx.x;
+  if (i < a.n) {
+    a.lock[i] = ~0ull;
+    a.taken[i] = 0;
+  }
+  if (i < a.m) {
+    const bool ok = pair_ok(a.winner[i], a.second[i], a.n);
+    if (!ok) raise_error(a.status, GSN_E_INVAL);
+    a.state[i] = ok ? 1 : 0;
+  }
+}
+
+// Grid-wide round t; rem[t] counts the signals left pending; rounds after one that left
+// fewer than kTailMin return at once.
+__global__ void rg_claim(GreedyArgs a, int32_t t) {
+  if (blockIdx.x == 0 && threadIdx.x == 0) a.rem[t] = 0;
+  if (t > 0 && a.rem[t - 1] < kTailMin) return;
+  const int32_t j = blockIdx.x * kRoundBlock + threadIdx.x;
+  if (j < a.m && a.state[j] == 1) g_claim(a, j);
+}
+
+__global__ void rg_check(GreedyArgs a, int32_t t) {
+  if (t > 0 && a.rem[t - 1] < kTailMin) return;
+  const int32_t j = blockIdx.x * kRoundBlock + threadIdx.x;
+  bool left = false;
+  if (j < a.m && a.state[j] == 1) {
+    const uint8_t st = g_check(a, j);
+    a.state[j] = st;
+    left = st == 1;
+  }
+  wave_count(left, &a.rem[t]);
+}
+
+// The remaining rounds in one workgroup, then the acceptance flags of all signals.
+__global__ __launch_bounds__(kTailBlock) void rg_tail(GreedyArgs a, uint8_t* accepted) {
+  __shared__ int32_t s_n, s_next;
+  const int tid = threadIdx.x;
+  if (tid == 0) {
+    s_n = 0;
+    s_next = 0;
+  }
+  __syncthreads();
+  int32_t* cur = a.list;
+  int32_t* nxt = a.list + a.m;
+  for (int32_t j = tid; j < a.m; j += kTailBlock)
+    if (a.state[j] == 1) cur[atomicAdd(&s_n, 1)] = j;
+  __syncthreads();
+  for (;;) {
+    const int32_t n = s_n;
+    if (n == 0) break;
+    for (int32_t i = tid; i < n; i += kTailBlock) g_claim(a, cur[i]);
+    __syncthreads();
+    for (int32_t i = tid; i < n; i += kTailBlock) a.state[cur[i]] = g_check(a, cur[i]);
+    __syncthreads();
+    for (int32_t i = tid; i < n; i += kTailBlock)
+      if (a.state[cur[i]] == 1) nxt[atomicAdd(&s_next, 1)] = cur[i];
+    __syncthreads();
+    if (tid == 0) {
+      if (s_next == n) {  // no progress: the lock words were not cleared on entry
+        raise_error(a.status, GSN_E_STATE);
+        s_next = 0;
+      }
+      s_n = s_next;
+      s_next = 0;
+    }
+    __syncthreads();
+    int32_t* t = cur;
+    cur = nxt;
+    nxt = t;
+  }
+  for (int32_t j = tid; j < a.m; j += kTailBlock) accepted[j] = a.state[j] == 2 ? 1 : 0;
+}
+
+}  // namespace
+
+hipError_t launch_resolve_greedy(const DevState& s, int cur, int32_t n, int32_t m,
+                                 const int32_t* winner, const int32_t* second, const float* d1,
+                                 uint8_t* accepted, int key_mode, int grid_rounds,
+                                 hipStream_t st) {
+  GreedyArgs a{m, n, winner, second, d1, key_mode, s.rp[cur], s.col[cur], s.lock,
+               s.extra, s.pend, s.rem, s.list, s.status};
+  rg_init<<<blocks(std::max(n, m)), kBlock, 0, st>>>(a);
+  const int g = static_cast<int>((m + kRoundBlock - 1) / kRoundBlock);
+  for (int32_t t = 0; t < grid_rounds; ++t) {
+    rg_claim<<<g, kRoundBlock, 0, st>>>(a, t);
+    rg_check<<<g, kRoundBlock, 0, st>>>(a, t);
+  }
+  rg_tail<<<1, kTailBlock, 0, st>>>(a, accepted);
+  return hipGetLastError();
+}
+
+}  // namespace gsn

@@ -38,6 +38,7 @@ GSN_T_EDGES = 4
 
 GSN_LOCK_SET = 0
 GSN_LOCK_WINNER = 1
+GSN_LOCK_SET_GREEDY = 2
 GSN_KEY_DIST_INDEX = 0
 GSN_KEY_INDEX = 1
 

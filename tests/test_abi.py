@@ -54,7 +54,7 @@ def test_host_side_validation(lib):
     assert lib.gsn_workspace_bytes(ctypes.byref(winner)) >= size + 4 * 4 * 2 * 256
     for bad in (make_params(eps_b=1.5), make_params(eps_n=-0.1), make_params(max_age=-1),
                 make_params(n_max=1), make_params(m_max=0), make_params(e_max=-1),
-                make_params(lock_mode=2), make_params(key_mode=-1),
+                make_params(lock_mode=3), make_params(key_mode=-1),
                 make_params(lock_mode=1, e_max=2**30 - 1, m_max=2**20)):
         assert lib.gsn_workspace_bytes(ctypes.byref(bad)) == 0
     P = ctypes.c_void_p

@@ -1,0 +1,67 @@
+"""GPU parity of the greedy lock-set rule (GSN_LOCK_SET_GREEDY: the lock sets {b, s} + N(b)
+taken in key order, a signal accepted iff its lock set is disjoint from those accepted
+before it) against the oracle: acceptance bit-exact every iteration, final networks
+bit-exact, in both key orders and for every split between grid-wide and single-workgroup
+rounds."""
+import numpy as np
+import pytest
+
+from parity import Pair, assert_iter_equal, run_workload
+
+pytestmark = pytest.mark.gpu
+
+GREEDY = 2
+
+
+def random_graph(rng, n, e):
+    pairs = set()
+    while len(pairs) < e:
+        u, v = rng.integers(0, n, 2)
+        if u != v:
+            pairs.add((min(u, v), max(u, v)))
+    pairs = sorted(pairs)
+    ages = rng.integers(0, 6, len(pairs))
+    return np.array([[p[0] for p in pairs], [p[1] for p in pairs], ages], np.int32)
+
+
+def exact_state(pair, where):
+    gs, os_ = pair.compare_state(where)
+    np.testing.assert_array_equal(gs["xyz"].numpy(), os_["xyz"], err_msg=where)
+    np.testing.assert_array_equal(gs["err"].numpy(), os_["err"], err_msg=where)
+
+
+@pytest.mark.parametrize("grid_rounds", [0, 1, 16])
+@pytest.mark.parametrize("key_mode", [0, 1])
+@pytest.mark.parametrize("seed,n,e,m", [(0, 30, 40, 200), (1, 300, 700, 1_000),
+                                        (2, 2_000, 5_000, 4_096), (3, 12, 0, 64)])
+def test_dense_collisions(seed, n, e, m, key_mode, grid_rounds):
+    import torch
+    from paper_1503_08294_amd import gsn
+    rng = np.random.default_rng(seed)
+    units = rng.standard_normal((3, n)).astype(np.float32)
+    pair = Pair(units, n_max=n + 16, e_max=8 * n + 64, m_max=m, eps_b=0.2, eps_n=0.05,
+                max_age=3, lock_mode=GREEDY, key_mode=key_mode)
+    if grid_rounds:
+        pair.net.tune(gsn.GSN_TUNE_GRID_ROUNDS, grid_rounds)
+    edges = random_graph(rng, n, e)
+    pair.net.import_state(torch.from_numpy(units), None, torch.from_numpy(edges))
+    pair.orc.import_state(units, None, edges)
+    for t in range(1, 7):
+        sig = rng.standard_normal((3, m)).astype(np.float32)
+        g, o = pair.iterate(sig, t, 3, True)
+        assert_iter_equal(g, o, f"iteration {t}")
+        exact_state(pair, f"iteration {t}")
+    assert pair.net.check() == 0
+
+
+@pytest.mark.parametrize("key_mode", [0, 1])
+def test_torus_grow_with_pruning(key_mode):
+    pair, rate = run_workload("torus_grow", iterations=40, n_points=50_000, n_units=1_500,
+                              m=1_024, max_age=2, lock_mode=GREEDY, key_mode=key_mode)
+    exact_state(pair, "torus end")
+
+
+def test_genus3_200k_accepts_more_than_one_round():
+    _, rate_greedy = run_workload("genus3_200k", iterations=3, lock_mode=GREEDY)
+    _, rate_one = run_workload("genus3_200k", iterations=3, lock_mode=0)
+    assert rate_greedy < rate_one
