@@ -39,6 +39,7 @@ struct GreedyArgs {
   int32_t* rem;
   int32_t* list;
   int32_t* status;
+  unsigned long long* acc64;
 };
 
 __device__ void g_claim(const GreedyArgs& a, int32_t j) {
@@ -109,7 +110,8 @@ __global__ void rg_check(GreedyArgs a, int32_t t) {
   wave_count(left, &a.rem[t]);
 }
 
-// The remaining rounds in one workgroup, then the acceptance flags of all signals.
+// The remaining rounds in one workgroup, then the acceptance flags of all signals (and
+// their counts in the statistics).
 __global__ __launch_bounds__(kTailBlock) void rg_tail(GreedyArgs a, uint8_t* accepted) {
   __shared__ int32_t s_n, s_next;
   const int tid = threadIdx.x;
@@ -146,7 +148,12 @@ __global__ __launch_bounds__(kTailBlock) void rg_tail(GreedyArgs a, uint8_t* acc
     cur = nxt;
     nxt = t;
   }
-  for (int32_t j = tid; j < a.m; j += kTailBlock) accepted[j] = a.state[j] == 2 ? 1 : 0;
+  for (int32_t j = tid; j < a.m; j += kTailBlock) {
+    const bool acc = a.state[j] == 2;
+    accepted[j] = acc ? 1 : 0;
+    wave_count(true, &a.acc64[kA64Resolved]);
+    wave_count(acc, &a.acc64[kA64Accepted]);
+  }
 }
 
 }  // namespace
@@ -156,7 +163,7 @@ hipError_t launch_resolve_greedy(const DevState& s, int cur, int32_t n, int32_t 
                                  uint8_t* accepted, int key_mode, int grid_rounds,
                                  hipStream_t st) {
   GreedyArgs a{m, n, winner, second, d1, key_mode, s.rp[cur], s.col[cur], s.lock,
-               s.extra, s.pend, s.rem, s.list, s.status};
+               s.extra, s.pend, s.rem, s.list, s.status, s.acc64};
   rg_init<<<blocks(std::max(n, m)), kBlock, 0, st>>>(a);
   const int g = static_cast<int>((m + kRoundBlock - 1) / kRoundBlock);
   for (int32_t t = 0; t < grid_rounds; ++t) {

@@ -62,6 +62,12 @@ def test_torus_grow_with_pruning(key_mode):
 
 
 def test_genus3_200k_accepts_more_than_one_round():
-    _, rate_greedy = run_workload("genus3_200k", iterations=3, lock_mode=GREEDY)
+    from paper_1503_08294_amd import gsn
+    pair, rate_greedy = run_workload("genus3_200k", iterations=3, lock_mode=GREEDY)
     _, rate_one = run_workload("genus3_200k", iterations=3, lock_mode=0)
     assert rate_greedy < rate_one
+    # the device statistics count the greedy acceptance too
+    resolved = pair.net.stat(gsn.GSN_STAT_RESOLVED)
+    accepted = pair.net.stat(gsn.GSN_STAT_ACCEPTED)
+    assert resolved == 3 * 16_384
+    assert abs(accepted / resolved - (1.0 - rate_greedy)) < 1e-12
