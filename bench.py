@@ -218,6 +218,9 @@ def main():
     ap.add_argument("--grid-cell", type=float, default=0.0,
                     help="find winners with the paper's hash index (cubes of this side over "
                          "the cloud's box) instead of the exhaustive search; 0 = exhaustive")
+    ap.add_argument("--grid-exact", action="store_true",
+                    help="with --grid-cell: certify the index's result per signal and use the "
+                         "exhaustive search where it cannot be certified (exact results)")
     ap.add_argument("--schedule", action="store_true",
                     help="instead of fixed-size steps, time one growing-network run "
                          "(gsn_run_schedule) from two units to the quantization-error "
@@ -268,7 +271,8 @@ def main():
         lo = cloud.min(axis=0) - np.float32(1e-3)
         hi = cloud.max(axis=0) + np.float32(1e-3)
         dims = [int(np.ceil((hi[a] - lo[a]) / args.grid_cell)) for a in range(3)]
-        grid = gsn.make_grid([float(v) for v in lo], args.grid_cell, dims)
+        grid = gsn.make_grid([float(v) for v in lo], args.grid_cell, dims,
+                             exact=args.grid_exact)
         grid_ws = net.grid_workspace(grid)
 
     def step(t):
@@ -364,7 +368,8 @@ def main():
                    "cloud_points": wl.n_points, "cloud": "genus-3 tube surface",
                    "iteration": "find+resolve+adapt+update_edges", "parallelism": "single",
                    "find": ("exhaustive" if grid is None else
-                            f"hash index, cubes of side {args.grid_cell}"),
+                            f"hash index, cubes of side {args.grid_cell}" +
+                            (", certified exact" if args.grid_exact else "")),
                    "collision": {"lock": args.lock, "key": args.key}},
         "signals_per_s": m * args.steps / elapsed,
         "accepted_per_s": accepted_timed / elapsed,

@@ -128,6 +128,11 @@ int gsn_find_winners(gsn_net* net, const float* sig, int32_t m, int32_t* winner,
  * signal's on every axis (the signal's cube and its 26 neighbours); when fewer than two
  * units are there, the exhaustive search is used.  Like the paper's index this is
  * approximate: a unit outside the 27 cubes can be nearer than the second found.
+ * With exact = 1 the result is instead certified: the two found are kept only when a
+ * rigorous lower bound on the distance from the signal to any unit outside its 27 cubes
+ * (from the signal's position in its cube, with the rounding of the cell function and of
+ * the distances accounted for) exceeds the second's distance; every other signal gets the
+ * exhaustive search, so the outputs equal gsn_find_winners' bit for bit.
  * grid_ws: device memory of gsn_grid_workspace_bytes() bytes (256-byte aligned, the
  * caller's, reused across calls; any contents).  Same order rules and outputs as
  * gsn_find_winners; GSN_E_INVAL for an invalid grid, GSN_E_CAPACITY for a small workspace.
@@ -136,6 +141,7 @@ typedef struct gsn_grid {
   float lo[3];       /* box corner, finite */
   float h;           /* side of a cube, finite, > 0 */
   int32_t dims[3];   /* cubes per axis, >= 1, product <= GSN_MAX_GRID_CELLS */
+  int32_t exact;     /* 0: the paper's index (approximate); 1: certified, exact */
 } gsn_grid;
 #define GSN_MAX_GRID_CELLS (1 << 24)
 size_t gsn_grid_workspace_bytes(const gsn_grid* grid, int32_t n_max, int32_t m_max);

@@ -5,7 +5,8 @@
 // neighbours, one lane per cube (a group of 32 lanes per signal, the lanes' top-2 keys
 // merged by shuffles), and signals whose 27 cubes hold fewer than two units get the
 // exhaustive search.  Results equal the oracle's indexed search bit for bit: the same cell
-// function, the same direct-form distance, the same (d, index) order.
+// function, the same direct-form distance, the same (d, index) order.  In exact mode the
+// 27-cube result is kept only where it is certified to be the exhaustive one.
 #include "gsn_internal.h"
 
 namespace gsn {
@@ -13,7 +14,7 @@ namespace {
 
 constexpr int kGroupLanes = 32;            // lanes per signal (27 cubes, 5 idle)
 constexpr int kQueryBlock = 256;           // 8 signals per workgroup
-constexpr int kFallbackBlocks = 64;
+constexpr int kFallbackBlocks = 256;
 constexpr unsigned long long kNoKey = ~0ull;
 
 inline int blocks(int64_t n) { return static_cast<int>((n + kBlock - 1) / kBlock); }
@@ -29,6 +30,7 @@ __device__ __forceinline__ int32_t grid_axis(float p, float lo, float inv_h, int
 struct GridArgs {
   float lo0, lo1, lo2, inv_h;
   int32_t d0, d1, d2;
+  int exact;
 };
 
 __device__ __forceinline__ void cell_of(const GridArgs& g, float x, float y, float z,
@@ -47,6 +49,35 @@ __device__ __forceinline__ float direct_d(float sx, float sy, float sz, float wx
                                           float wz) {
   const float dx = sx - wx, dy = sy - wy, dz = sz - wz;
   return (dx * dx + dy * dy) + dz * dz;
+}
+
+// Certification of a signal's 27-cube result (exact mode).  With t = fl(fl(p - lo) inv_h)
+// and x = (p - lo) inv_h exactly, t = x (1 + eta), |eta| <= 2u + u^2.  A unit in a cube two
+// or more above the signal's on axis a has t_w >= c + 2, so x_w >= (c + 2) / (1 + |eta|);
+// the signal has t_s < c + 1 (or t_s < 0), so x_s <= max(t_s, 0) / (1 - |eta|); below
+// likewise with x_w < (c - 1) / (1 - |eta|) and x_s >= t_s / (1 + |eta|).  Every unit outside
+// the 27 cubes is outside on some axis, so its true distance is at least r = the least of
+// these gaps divided by inv_h (gaps computed in binary64 with a relative margin of 3e-7 >
+// 2.01 u per factor and an absolute one for subnormal differences).  Its computed binary32
+// distance is at least (1 - 5u) times the true one, so if d2 < r^2 (1 - 4e-7) every outside
+// unit's computed distance exceeds d2 and the 27-cube top-2 is the exhaustive one.
+__device__ bool certified(const GridArgs& g, float sx, float sy, float sz, const int32_t* c,
+                          float d2) {
+  const double up = 1.0 + 3e-7, dn = 1.0 - 3e-7;
+  const float p[3] = {sx, sy, sz};
+  const float lo[3] = {g.lo0, g.lo1, g.lo2};
+  const int32_t dims[3] = {g.d0, g.d1, g.d2};
+  double gap = __builtin_huge_val();  // in cells
+  for (int a = 0; a < 3; ++a) {
+    const double t = static_cast<double>((p[a] - lo[a]) * g.inv_h);
+    if (c[a] + 2 <= dims[a] - 1) gap = fmin(gap, (c[a] + 2) * dn - fmax(t, 0.0) * up);
+    if (c[a] - 2 >= 0) gap = fmin(gap, t * dn - (c[a] - 1) * up);
+  }
+  if (gap == __builtin_huge_val()) return d2 < __builtin_huge_valf();  // the cubes hold all
+  gap -= 1e-30;
+  if (!(gap > 0.0)) return false;
+  const double r = gap / static_cast<double>(g.inv_h) * (1.0 - 1e-12);
+  return static_cast<double>(d2) < r * r * (1.0 - 4e-7);
 }
 
 __device__ __forceinline__ void top2_insert(unsigned long long k, unsigned long long& k1,
@@ -123,7 +154,8 @@ __global__ void gx_scatter(int32_t n, const float* __restrict__ x, const float* 
 
 // 32 lanes per signal: lane q < 27 scans cube (cx + q % 3 - 1, cy + (q / 3) % 3 - 1,
 // cz + q / 9 - 1).  The lanes' top-2 keys and candidate counts are merged by shuffles
-// within the 32 lanes; fewer than two candidates sends the signal to the fallback list.
+// within the 32 lanes; fewer than two candidates (or, in exact mode, a result that cannot
+// be certified) sends the signal to the fallback list.
 __global__ void gx_query(const float* __restrict__ sig, int32_t m, GridArgs g,
                          const int32_t* __restrict__ start, const float4* __restrict__ sorted,
                          int32_t* __restrict__ winner, int32_t* __restrict__ second,
@@ -161,7 +193,8 @@ __global__ void gx_query(const float* __restrict__ sig, int32_t m, GridArgs g,
     k2 = hi < rest ? hi : rest;
   }
   if (q != 0) return;
-  if (found < 2) {
+  if (found < 2 ||
+      (g.exact && !certified(g, sx, sy, sz, c, __uint_as_float(static_cast<uint32_t>(k2 >> 32))))) {
     fb_list[atomicAdd(nfb, 1)] = j;
     return;
   }
@@ -253,7 +286,7 @@ hipError_t launch_find_grid(const DevState& s, const GridBufs& gb, const GridSpe
                             int32_t* second, float* d1, float* d2, hipStream_t st) {
   const int32_t cells = static_cast<int32_t>(spec.cells);
   const GridArgs g{spec.lo[0], spec.lo[1], spec.lo[2], spec.inv_h,
-                   spec.dims[0], spec.dims[1], spec.dims[2]};
+                   spec.dims[0], spec.dims[1], spec.dims[2], spec.exact};
   gx_clear<<<std::min(blocks(cells), 1024), kBlock, 0, st>>>(gb.cnt, cells, gb.nfb);
   gx_count<<<blocks(n), kBlock, 0, st>>>(n, s.x, s.y, s.z, g, gb.ucell, gb.cnt);
   const int nb = blocks(cells);

@@ -155,6 +155,7 @@ bool grid_ok(const gsn_grid* g, int64_t* cells) {
     c *= g->dims[a];
     if (c > GSN_MAX_GRID_CELLS) return false;
   }
+  if (g->exact != 0 && g->exact != 1) return false;
   *cells = c;
   return true;
 }
@@ -388,6 +389,7 @@ int gsn_find_winners_grid(gsn_net* net, const gsn_grid* grid, void* grid_ws,
   }
   spec.inv_h = 1.0f / grid->h;
   spec.cells = cells;
+  spec.exact = grid->exact;
   const gsn::GridBufs gb = gsn::carve_grid(grid_ws, cells, net->p.n_max, net->p.m_max);
   TimedRegion t(net, GSN_T_FIND, st);
   hipError_t e = gsn::launch_find_grid(net->s, gb, spec, net->n, sig, m, winner, second, d1,

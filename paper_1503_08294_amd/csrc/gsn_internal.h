@@ -234,6 +234,7 @@ struct GridSpec {
   float inv_h;       // 1 / h rounded to binary32 (the cell function multiplies by it)
   int32_t dims[3];
   int64_t cells;
+  int exact;         // certify the 27-cube result, else the exhaustive search
 };
 struct GridBufs {
   int32_t* cnt;      // [cells + 1] units per cube, then scatter cursors

@@ -72,15 +72,17 @@ class gsn_params(ctypes.Structure):
 
 
 class gsn_grid(ctypes.Structure):
-    _fields_ = [("lo", ctypes.c_float * 3), ("h", ctypes.c_float), ("dims", ctypes.c_int32 * 3)]
+    _fields_ = [("lo", ctypes.c_float * 3), ("h", ctypes.c_float), ("dims", ctypes.c_int32 * 3),
+                ("exact", ctypes.c_int32)]
 
 
-def make_grid(lo, h, dims) -> gsn_grid:
+def make_grid(lo, h, dims, exact=False) -> gsn_grid:
     g = gsn_grid()
     for a in range(3):
         g.lo[a] = float(lo[a])
         g.dims[a] = int(dims[a])
     g.h = float(h)
+    g.exact = 1 if exact else 0
     return g
 
 

@@ -137,3 +137,59 @@ def test_grid_arguments_are_checked():
     with pytest.raises(gsn.GsnError) as e:        # workspace sized for the small grid
         g.find_winners_grid(sig, big, ws)
     assert e.value.code == gsn.GSN_E_CAPACITY
+
+
+# ------------------------------------------------------------------ exact mode ----
+# With exact = 1 the 27-cube result is kept only where it is certified; the outputs must
+# equal the exhaustive search's (the oracle's find_winners) bit for bit.
+
+def compare_exact(g, o, sig, lo, h, dims, where=""):
+    import torch
+    from paper_1503_08294_amd import gsn
+    grid = gsn.make_grid(lo, h, dims, exact=True)
+    ws = g.grid_workspace(grid)
+    got = [t.cpu().numpy() for t in g.find_winners_grid(torch.from_numpy(sig).cuda(), grid, ws)]
+    want = o.find_winners(sig)
+    for a, b, nm in zip(got, want, ("winner", "second", "d1", "d2")):
+        np.testing.assert_array_equal(a, b, err_msg=f"{where} {nm}")
+
+
+@pytest.mark.parametrize("seed,n,m,h", [(10, 500, 700, 0.3), (11, 3000, 4096, 0.12),
+                                        (12, 40, 300, 0.5), (13, 2, 64, 0.25),
+                                        (14, 20000, 10000, 0.05), (15, 20000, 4000, 0.01),
+                                        (16, 5000, 3000, 0.2)])
+def test_exact_mode_random_inputs(seed, n, m, h):
+    rng = np.random.default_rng(seed)
+    units = rng.uniform(-1, 1, (3, n)).astype(np.float32)
+    sig = rng.uniform(-1.3, 1.3, (3, m)).astype(np.float32)   # some outside the box
+    g, o = setup(units, m)
+    dims = tuple(int(np.ceil(2.0 / h)) for _ in range(3))
+    compare_exact(g, o, sig, (-1.0, -1.0, -1.0), h, dims, f"seed {seed}")
+
+
+def test_exact_mode_on_cube_faces():
+    """Units and signals on and next to cube faces, on a lattice: distances tie often, and
+    the nearest outside unit sits right behind the block's faces."""
+    rng = np.random.default_rng(17)
+    h = 0.125
+    ax = np.arange(-1.0, 1.0001, h / 2, dtype=np.float32)
+    grid_pts = np.stack(np.meshgrid(ax, ax, ax[:5], indexing="ij")).reshape(3, -1)
+    units = grid_pts[:, rng.choice(grid_pts.shape[1], 3000, replace=False)].astype(np.float32)
+    jitter = rng.choice(np.array([0.0, 1e-6, -1e-6, h / 4], np.float32), size=(3, 2000))
+    sig = (grid_pts[:, rng.choice(grid_pts.shape[1], 2000)] + jitter).astype(np.float32)
+    g, o = setup(units, 2000)
+    compare_exact(g, o, sig, (-1.0, -1.0, -1.0), h, (16, 16, 3), "lattice")
+
+
+@pytest.mark.parametrize("h", [0.005, 0.01, 0.02])
+def test_exact_mode_genus3(h):
+    from paper_1503_08294_amd.clouds import WORKLOADS, SignalStream
+    wl = WORKLOADS["genus3_200k"]
+    cloud = wl.make_cloud()
+    units = wl.make_units(cloud)
+    sig = SignalStream(cloud, wl.signal_seed).next(wl.m)
+    g, o = setup(units, wl.m)
+    lo = cloud.min(axis=0) - np.float32(1e-3)
+    hi = cloud.max(axis=0) + np.float32(1e-3)
+    dims = tuple(int(np.ceil((hi[a] - lo[a]) / h)) for a in range(3))
+    compare_exact(g, o, sig, tuple(float(v) for v in lo), h, dims, f"genus3 h={h}")
