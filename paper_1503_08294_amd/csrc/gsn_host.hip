@@ -311,7 +311,7 @@ int gsn_create(const gsn_params* params, void* workspace, size_t workspace_bytes
   }
   if (e == hipSuccess) e = hipStreamSynchronize(st);
   if (e != hipSuccess) {
-    delete net;
+    gsn_destroy(net);  // frees the pinned feedback word with the handle
     return GSN_E_HIP;
   }
   *out = net;

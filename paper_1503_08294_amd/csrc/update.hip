@@ -30,11 +30,6 @@ __device__ __forceinline__ int32_t find_in_row(const int32_t* __restrict__ rp,
 
 // ------------------------------------------------------------------ resolve ----
 
-__global__ void rs_clear(unsigned long long* __restrict__ lock, int32_t n) {
-  const int32_t i = blockIdx.x * kBlock + threadIdx.x;
-  if (i < n) lock[i] = ~0ull;
-}
-
 // winner_only: L_j = {b}, else L_j = {b, s} + N(b).
 __global__ void rs_claim(int32_t m, int32_t n, const int32_t* __restrict__ winner,
                          const int32_t* __restrict__ second, const float* __restrict__ d1,
@@ -58,7 +53,11 @@ __global__ void rs_claim(int32_t m, int32_t n, const int32_t* __restrict__ winne
 // With the winner alone locked, the survivor also releases its lock (the other claimants
 // compare with their own keys, which differ from both values), so the lock array is back
 // to all ones afterwards.
-// Also counts the signals and the accepted ones into the 64-bit statistics.
+// Every claimant visits each unit of its lock set once and releases the units it holds
+// (the others compare with their own keys, which differ from the holder's and from all
+// ones in the index half), so the lock words are all ones again afterwards and the next
+// resolve needs no clearing pass.  Also counts the signals and the accepted ones into the
+// 64-bit statistics.
 __global__ void rs_check(int32_t m, int32_t n, const int32_t* __restrict__ winner,
                          const int32_t* __restrict__ second, const float* __restrict__ d1,
                          const int32_t* __restrict__ rp, const int32_t* __restrict__ col,
@@ -71,12 +70,19 @@ __global__ void rs_check(int32_t m, int32_t n, const int32_t* __restrict__ winne
     const int32_t b = winner[j], s = second[j];
     if (pair_ok(b, s, n)) {
       const unsigned long long key = signal_key(d1[j], j, key_mode);
-      ok = lock[b] == key;
-      if (winner_only) {
-        if (ok) lock[b] = ~0ull;
-      } else {
-        ok = ok && lock[s] == key;
-        for (int32_t k = rp[b]; ok && k < rp[b + 1]; ++k) ok = lock[col[k]] == key;
+      ok = true;
+      auto visit = [&](int32_t u) {
+        if (lock[u] == key) lock[u] = ~0ull; else ok = false;
+      };
+      visit(b);
+      if (!winner_only) {
+        bool s_nb = false;
+        for (int32_t k = rp[b]; k < rp[b + 1]; ++k) {
+          const int32_t v = col[k];
+          s_nb |= v == s;
+          visit(v);
+        }
+        if (!s_nb) visit(s);
       }
     }
     accepted[j] = ok ? 1 : 0;
@@ -309,8 +315,8 @@ hipError_t launch_resolve(const DevState& s, int cur, int32_t n, int32_t m,
                           const int32_t* winner, const int32_t* second, const float* d1,
                           uint8_t* accepted, int lock_mode, int key_mode, hipStream_t st) {
   const int wo = lock_mode == 1;
-  // the winner-lock mode keeps the lock array at all ones between calls
-  if (!wo && n > 0) rs_clear<<<blocks(n), kBlock, 0, st>>>(s.lock, n);
+  // the lock words are all ones between calls (set at creation and import, released by
+  // their holders in every check)
   rs_claim<<<blocks(m), kBlock, 0, st>>>(m, n, winner, second, d1, s.rp[cur], s.col[cur],
                                          s.lock, s.status, wo, key_mode);
   rs_check<<<blocks(m), kBlock, 0, st>>>(m, n, winner, second, d1, s.rp[cur], s.col[cur],
