@@ -193,17 +193,46 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int j = lane & 31, h = lane >> 5;
   const int32_t n_batches = (n + 63) >> 6;
-  // chunk order: home chunk first, as in find_mfma.hip
-  int32_t c;
+  // Work-group -> (signal block sb, chunk c).  Work-groups go to the 8 XCDs round-robin by
+  // linear id; when the split is a multiple of 8, XCD r gets the chunks c = r (mod 8) only,
+  // so its L2 holds a quarter-or-less of the operand array instead of all of it.  Within an
+  // XCD, the signal blocks take their chunks nearest to the home chunk (the one holding
+  // their signals' cells) first; otherwise the home chunk first, then alternately above and
+  // below it.
+  int32_t c, sb;
   {
     const int32_t split = static_cast<int32_t>(gridDim.y);
-    const int32_t pm_ = min(blockIdx.x * kSignalsPerWG + kSignalsPerWG / 2, m - 1);
+    const int32_t sblocks = static_cast<int32_t>(gridDim.x);
+    const int32_t id = static_cast<int32_t>(blockIdx.x) + static_cast<int32_t>(blockIdx.y) * sblocks;
+    const bool xcd = split % 8 == 0;
+    const int32_t r = id % 8, k = id / 8;
+    sb = xcd ? k % sblocks : static_cast<int32_t>(blockIdx.x);
+    const int32_t pm_ = min(sb * kSignalsPerWG + kSignalsPerWG / 2, m - 1);
     const int32_t key = min(max(skey[min(max(sperm[pm_], 0), m - 1)], 0), kBuckets - 1);
     const int32_t pos = min(max(off_u[key], 0), n);
     const int32_t home = min(pos / (64 * chunk_batches), split - 1);
-    const int32_t y = static_cast<int32_t>(blockIdx.y);
-    const int32_t d = (y & 1) ? (y + 1) / 2 : -(y / 2);
-    c = ((home + d) % split + split) % split;
+    if (xcd) {
+      // the rank-th nearest (ring distance, then lower q) of the chunks r + 8q
+      const int32_t per = split / 8, rank = k / sblocks;
+      auto ring = [&](int32_t cc) {
+        const int32_t a = cc > home ? cc - home : home - cc;
+        return min(a, split - a);
+      };
+      c = r;
+      for (int32_t q = 0; q < per; ++q) {
+        const int32_t cq = r + 8 * q, dq = ring(cq);
+        int32_t before = 0;
+        for (int32_t p = 0; p < per; ++p) {
+          const int32_t dp = ring(r + 8 * p);
+          before += dp < dq || (dp == dq && p < q);
+        }
+        if (before == rank) c = cq;
+      }
+    } else {
+      const int32_t y = static_cast<int32_t>(blockIdx.y);
+      const int32_t d = (y & 1) ? (y + 1) / 2 : -(y / 2);
+      c = ((home + d) % split + split) % split;
+    }
   }
   const int32_t t_begin = c * chunk_batches;
   const int32_t t_end = min(n_batches, t_begin + chunk_batches);
@@ -215,7 +244,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
   const bool range_ok = fmaxf(xm, fmaxf(ym, zm)) <= 128.0f;
 
   // the lane's signal in block b: sorted position p = base + 32 b + j
-  const int32_t base = blockIdx.x * kSignalsPerWG + wave * 32 * NB;
+  const int32_t base = sb * kSignalsPerWG + wave * 32 * NB;
   float* sd = sdata[wave];
   h8 bop[NB];
   float th[NB];
