@@ -1,9 +1,10 @@
 """Throughput of the multi-signal iteration on one MI355X.
 
 One step = one whole iteration (find winners -> resolve conflicts -> adapt -> update
-edges) over one batch of m signals, on the genus-3 workload (200,000 units, 16,384 signals
-per iteration, signals drawn from a 4,000,000-point cloud).  All signal batches are
-resident in HBM before the timed region starts.
+edges, one gsn_iterate call: the lock-set update runs fused) over one batch of m signals,
+on the genus-3 workload (200,000 units, 16,384 signals per iteration, signals drawn from a
+4,000,000-point cloud).  All signal batches are resident in HBM before the timed region
+starts.
 
 Prints one JSON line:
   value            whole-iteration signal-unit distance evaluations per second (m*N/step)
@@ -290,7 +291,7 @@ def main():
     for t in range(args.warmup):
         step(t)
     torch.cuda.synchronize()
-    for w in range(5):
+    for w in range(6):
         gsn.gsn_timing_read(net.h, w)
     gsn.gsn_timing_enable(net.h, True)
 
@@ -311,7 +312,7 @@ def main():
     phase = {}
     for name, w in (("find_scan", gsn.GSN_T_FIND_SCAN), ("find", gsn.GSN_T_FIND),
                     ("resolve", gsn.GSN_T_RESOLVE), ("adapt", gsn.GSN_T_ADAPT),
-                    ("edges", gsn.GSN_T_EDGES)):
+                    ("edges", gsn.GSN_T_EDGES), ("update_fused", gsn.GSN_T_UPDATE)):
         ms, cnt = gsn.gsn_timing_read(net.h, w)
         phase[name] = ms / max(cnt, 1)
     if net.check() != 0:

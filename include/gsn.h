@@ -193,6 +193,16 @@ int gsn_adapt(gsn_net* net, const float* sig, int32_t m, const int32_t* winner,
 int gsn_update_edges(gsn_net* net, int32_t m, const int32_t* winner, const int32_t* second,
                      const uint8_t* accepted, void* stream);
 
+/* One whole iteration (Sec. 2.2: find winners, resolve, adapt, update edges) in one call:
+ * the outputs and the state afterwards are those of the four calls above in order (same
+ * order rules: it starts like gsn_find_winners and leaves the handle ready for gsn_grow).
+ * With GSN_LOCK_SET the update runs fused: resolve's check applies each accepted signal's
+ * adaptation and edge marks at once (accepted lock sets are disjoint) and the error decay
+ * rides on the degree count, five launches instead of eight.  The other rules run the
+ * four steps.  Outputs: device arrays of length m.  Async. */
+int gsn_iterate(gsn_net* net, const float* sig, int32_t m, int32_t* winner, int32_t* second,
+                float* d1, float* d2, uint8_t* accepted, void* stream);
+
 /* Growth (Sec. 2.1: units may be added and removed during the update; GNG inserts next
  * to the unit of largest accumulated error).  First removes, by stable
  * compaction (indices shift down, edges are renumbered), every unit marked by
@@ -291,9 +301,10 @@ int gsn_tune(gsn_net* net, int32_t key, int32_t value);
  * the last read, and clears them (syncs).
  *   GSN_T_FIND_SCAN   the find-winners scan kernel alone
  *   GSN_T_FIND        all of gsn_find_winners
- *   GSN_T_RESOLVE, GSN_T_ADAPT, GSN_T_EDGES   all of the corresponding call */
+ *   GSN_T_RESOLVE, GSN_T_ADAPT, GSN_T_EDGES   all of the corresponding call
+ *   GSN_T_UPDATE      the fused update of gsn_iterate (resolve, adapt and edges) */
 enum { GSN_T_FIND_SCAN = 0, GSN_T_FIND = 1, GSN_T_RESOLVE = 2, GSN_T_ADAPT = 3,
-       GSN_T_EDGES = 4, GSN_T_COUNT = 5 };
+       GSN_T_EDGES = 4, GSN_T_UPDATE = 5, GSN_T_COUNT = 6 };
 int gsn_timing_enable(gsn_net* net, int32_t enable);
 int gsn_timing_read(gsn_net* net, int32_t which, double* total_ms, int32_t* launches);
 

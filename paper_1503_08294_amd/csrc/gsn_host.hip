@@ -471,6 +471,31 @@ int gsn_update_edges(gsn_net* net, int32_t m, const int32_t* winner, const int32
   return GSN_OK;
 }
 
+int gsn_iterate(gsn_net* net, const float* sig, int32_t m, int32_t* winner, int32_t* second,
+                float* d1, float* d2, uint8_t* accepted, void* stream) {
+  if (!net || m < 0 || m > net->p.m_max) return GSN_E_INVAL;
+  if (net->phase != kReady && net->phase != kFound) return GSN_E_STATE;
+  if (m > 0 && !accepted) return GSN_E_INVAL;
+  int rc = gsn_find_winners(net, sig, m, winner, second, d1, d2, stream);
+  if (rc) return rc;
+  if (net->p.lock_mode != 0) {
+    if ((rc = gsn_resolve_conflicts(net, m, winner, second, d1, accepted, stream))) return rc;
+    if ((rc = gsn_adapt(net, sig, m, winner, second, d1, accepted, stream))) return rc;
+    return gsn_update_edges(net, m, winner, second, accepted, stream);
+  }
+  hipStream_t st = as_stream(stream);
+  TimedRegion t(net, GSN_T_UPDATE, st);
+  const hipError_t e = gsn::launch_iterate_set(
+      net->s, net->cur, net->n, sig, m, winner, second, d1, accepted, net->p.key_mode,
+      net->p.eps_b, net->p.eps_n, net->p.err_beta, net->p.max_age,
+      2 * static_cast<int64_t>(net->p.e_max), st);
+  t.end();
+  if (e != hipSuccess) return GSN_E_HIP;
+  net->cur ^= 1;
+  net->phase = kReady;
+  return GSN_OK;
+}
+
 int gsn_grow(gsn_net* net, int32_t iteration, int32_t insert_every, void* stream) {
   if (!net || insert_every < 0) return GSN_E_INVAL;
   if (net->phase != kReady) return GSN_E_STATE;

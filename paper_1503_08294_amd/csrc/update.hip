@@ -93,6 +93,26 @@ __global__ void rs_check(int32_t m, int32_t n, const int32_t* __restrict__ winne
 
 // -------------------------------------------------------------------- adapt ----
 
+// The adaptation of one accepted signal j (winner b, second s).
+__device__ __forceinline__ void adapt_signal(const float* __restrict__ sig, int32_t m,
+                                             int32_t j, int32_t b, int32_t s, float d1j,
+                                             const int32_t* __restrict__ rp,
+                                             const int32_t* __restrict__ col,
+                                             float* __restrict__ x, float* __restrict__ y,
+                                             float* __restrict__ z, float* __restrict__ err,
+                                             float eps_b, float eps_n) {
+  const float sx = sig[j], sy = sig[m + j], sz = sig[2 * m + j];
+  move_unit(x, y, z, b, eps_b, sx, sy, sz);
+  bool s_is_nb = false;
+  for (int32_t k = rp[b]; k < rp[b + 1]; ++k) {
+    const int32_t v = col[k];
+    s_is_nb |= v == s;
+    move_unit(x, y, z, v, eps_n, sx, sy, sz);
+  }
+  if (!s_is_nb) move_unit(x, y, z, s, eps_n, sx, sy, sz);
+  err[b] = err[b] + d1j;
+}
+
 __global__ void ad_move(const float* __restrict__ sig, int32_t m, int32_t n,
                         const int32_t* __restrict__ winner, const int32_t* __restrict__ second,
                         const float* __restrict__ d1, const uint8_t* __restrict__ accepted,
@@ -103,16 +123,7 @@ __global__ void ad_move(const float* __restrict__ sig, int32_t m, int32_t n,
   if (j >= m || !accepted[j]) return;
   const int32_t b = winner[j], s = second[j];
   if (!pair_ok(b, s, n)) return;
-  const float sx = sig[j], sy = sig[m + j], sz = sig[2 * m + j];
-  move_unit(x, y, z, b, eps_b, sx, sy, sz);
-  bool s_is_nb = false;
-  for (int32_t k = rp[b]; k < rp[b + 1]; ++k) {
-    const int32_t v = col[k];
-    s_is_nb |= v == s;
-    move_unit(x, y, z, v, eps_n, sx, sy, sz);
-  }
-  if (!s_is_nb) move_unit(x, y, z, s, eps_n, sx, sy, sz);
-  err[b] = err[b] + d1[j];
+  adapt_signal(sig, m, j, b, s, d1[j], rp, col, x, y, z, err, eps_b, eps_n);
 }
 
 __global__ void ad_decay(float* __restrict__ err, int32_t n, float beta) {
@@ -125,16 +136,13 @@ __global__ void ad_decay(float* __restrict__ err, int32_t n, float beta) {
 // Per accepted signal: age the edges at b (both half-edges), reset or request the edge
 // {b, s}, then mark the edges at b older than max_age as dead and flag neighbours left
 // without a live edge.  Rows touched belong to L_j only, so threads never share a row.
-__global__ void ed_mark(int32_t m, int32_t n, const int32_t* __restrict__ winner,
-                        const int32_t* __restrict__ second,
-                        const uint8_t* __restrict__ accepted, const int32_t* __restrict__ rp,
-                        const int32_t* __restrict__ col, int32_t* __restrict__ age,
-                        int32_t* __restrict__ ins, int32_t* __restrict__ orphan,
-                        int32_t* __restrict__ status, int32_t max_age) {
-  const int32_t j = blockIdx.x * kBlock + threadIdx.x;
-  if (j >= m || !accepted[j]) return;
-  const int32_t b = winner[j], s = second[j];
-  if (!pair_ok(b, s, n)) return;
+// The connection update of one accepted signal (winner b, second s) on its own rows.
+__device__ __forceinline__ void mark_signal(int32_t b, int32_t s,
+                                            const int32_t* __restrict__ rp,
+                                            const int32_t* __restrict__ col,
+                                            int32_t* __restrict__ age, int32_t* __restrict__ ins,
+                                            int32_t* __restrict__ orphan,
+                                            int32_t* __restrict__ status, int32_t max_age) {
   const int32_t r0 = rp[b], r1 = rp[b + 1];
   bool found = false;
   for (int32_t k = r0; k < r1; ++k) {
@@ -167,14 +175,87 @@ __global__ void ed_mark(int32_t m, int32_t n, const int32_t* __restrict__ winner
   }
 }
 
-// New degree of every unit (live half-edges + a requested new edge) and per-block sums.
+
+__global__ void ed_mark(int32_t m, int32_t n, const int32_t* __restrict__ winner,
+                        const int32_t* __restrict__ second,
+                        const uint8_t* __restrict__ accepted, const int32_t* __restrict__ rp,
+                        const int32_t* __restrict__ col, int32_t* __restrict__ age,
+                        int32_t* __restrict__ ins, int32_t* __restrict__ orphan,
+                        int32_t* __restrict__ status, int32_t max_age) {
+  const int32_t j = blockIdx.x * kBlock + threadIdx.x;
+  if (j >= m || !accepted[j]) return;
+  const int32_t b = winner[j], s = second[j];
+  if (!pair_ok(b, s, n)) return;
+  mark_signal(b, s, rp, col, age, ins, orphan, status, max_age);
+}
+
+// The lock-set resolve of rs_check fused with the update of the accepted signals (the
+// adaptation of ad_move and the marks of ed_mark): an accepted lock set is held by its
+// signal alone, and the other threads of this kernel read only lock words and row layouts,
+// which the update leaves alone, so each accepted signal applies its update at once.
+struct FusedArgs {
+  const float* sig;
+  int32_t m, n;
+  const int32_t* winner;
+  const int32_t* second;
+  const float* d1;
+  int key_mode;
+  const int32_t* rp;
+  const int32_t* col;
+  unsigned long long* lock;
+  uint8_t* accepted;
+  unsigned long long* acc64;
+  float *x, *y, *z, *err;
+  float eps_b, eps_n;
+  int32_t* age;
+  int32_t* ins;
+  int32_t* orphan;
+  int32_t* status;
+  int32_t max_age;
+};
+
+__global__ void fu_check_apply(FusedArgs a) {
+  const int32_t j = blockIdx.x * kBlock + threadIdx.x;
+  bool ok = false;
+  if (j < a.m) {
+    const int32_t b = a.winner[j], s = a.second[j];
+    if (pair_ok(b, s, a.n)) {
+      const unsigned long long key = signal_key(a.d1[j], j, a.key_mode);
+      ok = true;
+      auto visit = [&](int32_t u) {
+        if (a.lock[u] == key) a.lock[u] = ~0ull; else ok = false;
+      };
+      visit(b);
+      bool s_nb = false;
+      for (int32_t k = a.rp[b]; k < a.rp[b + 1]; ++k) {
+        const int32_t v = a.col[k];
+        s_nb |= v == s;
+        visit(v);
+      }
+      if (!s_nb) visit(s);
+      if (ok) {
+        adapt_signal(a.sig, a.m, j, b, s, a.d1[j], a.rp, a.col, a.x, a.y, a.z, a.err, a.eps_b,
+                     a.eps_n);
+        mark_signal(b, s, a.rp, a.col, a.age, a.ins, a.orphan, a.status, a.max_age);
+      }
+    }
+    a.accepted[j] = ok ? 1 : 0;
+  }
+  wave_count(j < a.m, &a.acc64[kA64Resolved]);
+  wave_count(ok, &a.acc64[kA64Accepted]);
+}
+
+// New degree of every unit (live half-edges + a requested new edge) and per-block sums;
+// with err not null also the error decay of the fused iteration.
 __global__ void ed_count(int32_t n, const int32_t* __restrict__ rp,
                          const int32_t* __restrict__ age, const int32_t* __restrict__ ins,
-                         int32_t* __restrict__ cnt, int32_t* __restrict__ bsum) {
+                         int32_t* __restrict__ cnt, int32_t* __restrict__ bsum,
+                         float* __restrict__ err, float beta) {
   __shared__ int32_t red[kBlock];
   const int32_t u = blockIdx.x * kBlock + threadIdx.x;
   int32_t c = 0;
   if (u < n) {
+    if (err) err[u] = err[u] * beta;
     for (int32_t k = rp[u]; k < rp[u + 1]; ++k) c += age[k] != kDead;
     c += ins[u] >= 0;
     cnt[u] = c;
@@ -346,7 +427,34 @@ hipError_t launch_edges(const DevState& s, int cur, int32_t n, int32_t m,
                                           max_age);
   const int nb = blocks(n);
   if (n > 0)
-    ed_count<<<nb, kBlock, 0, st>>>(n, s.rp[cur], s.age[cur], s.ins, s.cnt, s.bsum);
+    ed_count<<<nb, kBlock, 0, st>>>(n, s.rp[cur], s.age[cur], s.ins, s.cnt, s.bsum, nullptr,
+                                    1.0f);
+  scan_blocks<<<1, 1024, 0, st>>>(s.bsum, nb, half_cap, s.rp[nxt] + n, s.status, -1);
+  if (n > 0)
+    ed_write<<<nb, kBlock, 0, st>>>(n, s.rp[cur], s.col[cur], s.age[cur], s.ins, s.cnt,
+                                    s.bsum, s.rp[nxt], s.col[nxt], s.age[nxt], s.status);
+  return hipGetLastError();
+}
+
+hipError_t launch_iterate_set(const DevState& s, int cur, int32_t n, const float* sig,
+                              int32_t m, const int32_t* winner, const int32_t* second,
+                              const float* d1, uint8_t* accepted, int key_mode, float eps_b,
+                              float eps_n, float beta, int32_t max_age, int64_t half_cap,
+                              hipStream_t st) {
+  const int nxt = cur ^ 1;
+  if (m > 0) {
+    rs_claim<<<blocks(m), kBlock, 0, st>>>(m, n, winner, second, d1, s.rp[cur], s.col[cur],
+                                           s.lock, s.status, 0, key_mode);
+    FusedArgs a{sig,      m,          n,          winner,  second,   d1,     key_mode,
+                s.rp[cur], s.col[cur], s.lock,     accepted, s.acc64, s.x,    s.y,
+                s.z,      s.err,      eps_b,      eps_n,   s.age[cur], s.ins, s.orphan,
+                s.status, max_age};
+    fu_check_apply<<<blocks(m), kBlock, 0, st>>>(a);
+  }
+  const int nb = blocks(n);
+  if (n > 0)
+    ed_count<<<nb, kBlock, 0, st>>>(n, s.rp[cur], s.age[cur], s.ins, s.cnt, s.bsum, s.err,
+                                    beta);
   scan_blocks<<<1, 1024, 0, st>>>(s.bsum, nb, half_cap, s.rp[nxt] + n, s.status, -1);
   if (n > 0)
     ed_write<<<nb, kBlock, 0, st>>>(n, s.rp[cur], s.col[cur], s.age[cur], s.ins, s.cnt,

@@ -35,6 +35,7 @@ GSN_T_FIND = 1
 GSN_T_RESOLVE = 2
 GSN_T_ADAPT = 3
 GSN_T_EDGES = 4
+GSN_T_UPDATE = 5
 
 GSN_LOCK_SET = 0
 GSN_LOCK_WINNER = 1
@@ -124,6 +125,7 @@ _sig = {
     "gsn_resolve_conflicts": (ctypes.c_int, [_P, _I, _P, _P, _P, _P, _P]),
     "gsn_adapt": (ctypes.c_int, [_P, _P, _I, _P, _P, _P, _P, _P]),
     "gsn_update_edges": (ctypes.c_int, [_P, _I, _P, _P, _P, _P]),
+    "gsn_iterate": (ctypes.c_int, [_P, _P, _I, _P, _P, _P, _P, _P, _P]),
     "gsn_grow": (ctypes.c_int, [_P, _I, _I, _P]),
     "gsn_run_schedule": (ctypes.c_int, [_P, _P, ctypes.c_int64, ctypes.POINTER(gsn_schedule),
                                         ctypes.POINTER(gsn_schedule_result), _P]),
@@ -306,6 +308,16 @@ def gsn_find_winners_grid(net, grid: gsn_grid, grid_ws: torch.Tensor, sig: torch
            "gsn_find_winners_grid")
 
 
+def gsn_iterate(net, sig: torch.Tensor, m: int, winner, second, d1, d2, accepted,
+                stream=None):
+    _check(_lib.gsn_iterate(net, _dev(sig, torch.float32, 3 * m, "sig"), m,
+                            _dev(winner, torch.int32, m, "winner"),
+                            _dev(second, torch.int32, m, "second"),
+                            _dev(d1, torch.float32, m, "d1"), _dev(d2, torch.float32, m, "d2"),
+                            _dev(accepted, torch.uint8, m, "accepted"), _stream(stream)),
+           "gsn_iterate")
+
+
 def make_schedule(m_cap=8192, fixed_m=0, insert_every=100, qe_window=8192,
                   max_signals=1 << 20, qe_threshold=0.0, seed=0) -> gsn_schedule:
     return gsn_schedule(m_cap, fixed_m, insert_every, qe_window, max_signals, qe_threshold,
@@ -423,7 +435,15 @@ class Network:
                          b.accepted if accepted is None else accepted, self.stream)
 
     def iterate(self, sig: torch.Tensor):
-        """find -> resolve -> adapt -> update_edges on one batch (device SoA (3, m))."""
+        """find -> resolve -> adapt -> update_edges on one batch (device SoA (3, m)), in one
+        gsn_iterate call."""
+        m = sig.shape[1]
+        b = self.buf
+        gsn_iterate(self.h, sig, m, b.winner, b.second, b.d1, b.d2, b.accepted, self.stream)
+        return b.winner[:m], b.second[:m], b.d1[:m], b.d2[:m], b.accepted[:m]
+
+    def iterate_steps(self, sig: torch.Tensor):
+        """The same iteration through the four separate calls."""
         m = sig.shape[1]
         self.find_winners(sig)
         self.resolve_conflicts(m)

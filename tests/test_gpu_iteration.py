@@ -53,3 +53,33 @@ def test_determinism_of_repeated_runs():
     sa, sb = a.net.export(), b.net.export()
     for k in ("xyz", "err", "edges"):
         assert np.array_equal(sa[k].numpy(), sb[k].numpy()), k
+
+
+@pytest.mark.parametrize("lock_mode", [0, 1, 2])
+def test_fused_iteration_equals_the_four_calls(lock_mode):
+    """gsn_iterate (fused update for the lock-set rule) against find, resolve, adapt and
+    update_edges called one by one, on two networks from the same state: every output and
+    the whole state bit for bit, with pruning, removal and insertion."""
+    import torch
+    from paper_1503_08294_amd import gsn
+    from paper_1503_08294_amd.clouds import WORKLOADS, SignalStream
+    wl = WORKLOADS["torus_grow"]
+    cloud = wl.make_cloud(50_000)
+    units = torch.from_numpy(wl.make_units(cloud, 1_500)).cuda()
+    p = gsn.make_params(wl.eps_b, wl.eps_n, 2, wl.err_alpha, wl.err_beta, 1_700, 8_000, 1_024,
+                        lock_mode, 0)
+    a, b = gsn.Network(p, units), gsn.Network(p, units)
+    stream = SignalStream(cloud, wl.signal_seed)
+    for t in range(1, 41):
+        sig = torch.from_numpy(stream.next(1_024)).cuda()
+        ra = [x.clone() for x in a.iterate(sig)]
+        rb = [x.clone() for x in b.iterate_steps(sig)]
+        for x, y in zip(ra, rb):
+            assert torch.equal(x, y), f"iteration {t}"
+        a.grow(t, 10)
+        b.grow(t, 10)
+    sa, sb = a.export(), b.export()
+    for k in ("xyz", "err", "edges"):
+        assert torch.equal(sa[k], sb[k]), k
+    assert a.sizes() == b.sizes() and a.sizes()[0] != 1_500
+    assert a.check() == 0 and b.check() == 0
