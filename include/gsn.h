@@ -285,11 +285,12 @@ void gsn_destroy(gsn_net* net);
  *                     4 = the same screen on the matrix cores in split binary16 (every
  *                     screen carries a rigorous rounding margin; candidates are rechecked
  *                     in the binary32 direct form, so all variants return the same result)
- *   GSN_TUNE_GRID_ROUNDS  rounds of the GSN_LOCK_WINNER update launched over the whole
- *                     device (each skipped once fewer than 256 signals are pending) before
- *                     the remaining ones run in a single workgroup: 1..16, or 0 =
- *                     automatic (one more than the previous update used, from a pinned
- *                     host copy of its count)
+ *   GSN_TUNE_GRID_ROUNDS  rounds of the GSN_LOCK_WINNER update and of the
+ *                     GSN_LOCK_SET_GREEDY resolve launched over the whole device (each
+ *                     skipped once fewer than 128 signals are pending) before the remaining
+ *                     ones run in a single workgroup: 1..16, or 0 = automatic (winner lock:
+ *                     one more than the previous update used, from a pinned host copy of its
+ *                     count; greedy resolve: 4)
  * Returns GSN_E_INVAL for an unknown key or value. */
 enum { GSN_TUNE_SPLIT = 1, GSN_TUNE_VARIANT = 2, GSN_TUNE_GRID_ROUNDS = 3 };
 #define GSN_MAX_SPLIT 64
