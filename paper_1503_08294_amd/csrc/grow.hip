@@ -235,7 +235,12 @@ __device__ int wave_insert(int32_t n, int32_t q, float alpha, int64_t half_cap,
 // Up to `count` insertions one after another (each sees the errors and edges the previous
 // one left), while N < n_max and the unit of largest error has a neighbour.  seg holds the
 // segment keys of the n0 units on entry (gr_segmax).  A barrier separates the phases of an
-// insertion (one workgroup: its ordering covers what the waves share).
+// insertion (one workgroup: its ordering covers what the waves share).  Per insertion, wave
+// 0 takes q (the best segment key), then in three dependent rounds of loads q's row bounds,
+// position and error; q's row; every neighbour's error, row bounds and position, so that
+// f's come with the choice of f.  It writes the three new errors, and while waves 1-3
+// rescan the segments of q, f and r, it rewrites the rows of q and f (one more round of
+// loads, f's row) and adds r.  Rows longer than 64 entries take the one-lane path.
 __global__ __launch_bounds__(1024) void gr_insert(int32_t n0, int32_t count, int32_t n_max,
                                                   int32_t len, float alpha, int64_t half_cap,
                                                   const unsigned long long* __restrict__ seg,
@@ -248,7 +253,7 @@ __global__ __launch_bounds__(1024) void gr_insert(int32_t n0, int32_t count, int
                                                   int32_t* __restrict__ status) {
   __shared__ unsigned long long sk[kMaxSeg];
   __shared__ unsigned long long red[16];
-  __shared__ int32_t s_q, s_f, s_added;
+  __shared__ int32_t s_q, s_f, s_added, s_long;
   const int t = threadIdx.x, w = t >> 6, lane = t & 63;
   int32_t nseg = (n0 + len - 1) / len;
   for (int32_t i = t; i < nseg; i += 1024) sk[i] = seg[i];
@@ -268,25 +273,137 @@ __global__ __launch_bounds__(1024) void gr_insert(int32_t n0, int32_t count, int
       if (lane == 0) s_q = b ? key_index(b) : -1;
     }
     __syncthreads();
+    const int32_t q = s_q, r = n;
+    // wave 0: choose f, write the new errors (registers keep q's row for the surgery)
+    int32_t r0 = 0, r1 = 0, e2 = 0, l = 0, v = -1, av = 0, kf = 0, f = -1, f0 = 0, f1 = 0;
+    float xq = 0.0f, yq = 0.0f, zq = 0.0f, xf = 0.0f, yf = 0.0f, zf = 0.0f;
     if (w == 0) {
-      int32_t f = -1;
-      const int a = wave_insert(n, s_q, alpha, half_cap, rp, col, age, x, y, z, err, status,
-                                &f);
+      int added = 0, longrow = 0;
+      if (q >= 0) {
+        r0 = rp[q];
+        r1 = rp[q + 1];
+        e2 = rp[n];
+        xq = x[q];
+        yq = y[q];
+        zq = z[q];
+        const float eq = err[q];
+        l = r1 - r0;
+        if (l > 64) {
+          longrow = 1;
+        } else if (l > 0) {
+          if (static_cast<int64_t>(e2) + 2 > half_cap) {
+            if (lane == 0) atomicCAS(&status[kStError], 0, GSN_E_CAPACITY);
+          } else {
+            float ev = 0.0f, xv = 0.0f, yv = 0.0f, zv = 0.0f;
+            int32_t rv0 = 0, rv1 = 0;
+            unsigned long long kv = 0;
+            if (lane < l) {
+              v = col[r0 + lane];
+              av = age[r0 + lane];
+            }
+            if (lane < l) {
+              ev = err[v];
+              rv0 = rp[v];
+              rv1 = rp[v + 1];
+              xv = x[v];
+              yv = y[v];
+              zv = z[v];
+              kv = err_key(ev, v);
+            }
+            f = key_index(wave_max(kv));
+            kf = __ffsll(static_cast<long long>(__ballot(lane < l && v == f))) - 1;
+            f0 = __shfl(rv0, kf);
+            f1 = __shfl(rv1, kf);
+            xf = __shfl(xv, kf);
+            yf = __shfl(yv, kf);
+            zf = __shfl(zv, kf);
+            const float ef = __shfl(ev, kf);
+            if (lane == 0) {
+              err[q] = eq * alpha;
+              err[f] = ef * alpha;
+              err[r] = eq * alpha;
+            }
+            added = 1;
+          }
+        }
+      }
       if (lane == 0) {
-        s_added = a;
+        s_added = added;
+        s_long = longrow;
         s_f = f;
       }
     }
     __syncthreads();
+    if (s_long) {
+      // a row longer than 64 entries: the whole insertion on one wave as before
+      if (w == 0) {
+        int32_t ff = -1;
+        const int a = wave_insert(n, q, alpha, half_cap, rp, col, age, x, y, z, err, status,
+                                  &ff);
+        if (lane == 0) {
+          s_added = a;
+          s_f = ff;
+        }
+      }
+      __syncthreads();
+    }
     if (!s_added) break;
-    // rescan the segments of q, f and r (waves 0, 1, 2; equal segments give equal keys)
-    const int32_t r = n;
     ++n;
     ++done;
-    if (w < 3) {
-      const int32_t u = w == 0 ? s_q : (w == 1 ? s_f : r);
+    if (w >= 1 && w <= 3) {
+      // rescan the segments of q, f and r (equal segments give equal keys)
+      const int32_t u = w == 1 ? q : (w == 2 ? s_f : r);
       const unsigned long long k = segment_key(err, n, u / len, len);
       if (lane == 0) sk[u / len] = k;
+    } else if (w == 0 && !s_long) {
+      // rows of q (f -> r) and f (q -> r), and the new unit r
+      if (lane < l && lane > kf) {
+        col[r0 + lane - 1] = v;
+        age[r0 + lane - 1] = av;
+      }
+      if (lane == 0) {
+        col[r1 - 1] = r;
+        age[r1 - 1] = 0;
+      }
+      const int32_t lf = f1 - f0;
+      if (lf > 64) {
+        if (lane == 0) {
+          int32_t k = f0;
+          while (k < f1 && col[k] != q) ++k;
+          for (; k + 1 < f1; ++k) {
+            col[k] = col[k + 1];
+            age[k] = age[k + 1];
+          }
+          col[f1 - 1] = r;
+          age[f1 - 1] = 0;
+        }
+      } else {
+        int32_t c = -1, a = 0;
+        if (lane < lf) {
+          c = col[f0 + lane];
+          a = age[f0 + lane];
+        }
+        const unsigned long long at = __ballot(lane < lf && c == q);
+        const int pos = at ? __ffsll(static_cast<long long>(at)) - 1 : lf;
+        if (lane < lf && lane > pos) {
+          col[f0 + lane - 1] = c;
+          age[f0 + lane - 1] = a;
+        }
+        if (lane == 0) {
+          col[f1 - 1] = r;
+          age[f1 - 1] = 0;
+        }
+      }
+      if (lane == 0) {
+        x[r] = (xq + xf) * 0.5f;
+        y[r] = (yq + yf) * 0.5f;
+        z[r] = (zq + zf) * 0.5f;
+        col[e2] = min(q, f);
+        col[e2 + 1] = max(q, f);
+        age[e2] = 0;
+        age[e2 + 1] = 0;
+        rp[r + 1] = e2 + 2;
+      }
     }
     nseg = (n + len - 1) / len;
     __syncthreads();
