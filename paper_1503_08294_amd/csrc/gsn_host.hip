@@ -533,10 +533,8 @@ int gsn_run_schedule(gsn_net* net, const float* cloud, int64_t n_points,
     }
     if (gsn::launch_draw(cloud, n_points, sc->seed, res->signals, m, s.ssig, st) != hipSuccess)
       return GSN_E_HIP;
-    if ((rc = gsn_find_winners(net, s.ssig, m, s.swin, s.ssec, s.sd1, s.sd2, stream))) return rc;
-    if ((rc = gsn_resolve_conflicts(net, m, s.swin, s.ssec, s.sd1, s.sacc, stream))) return rc;
-    if ((rc = gsn_adapt(net, s.ssig, m, s.swin, s.ssec, s.sd1, s.sacc, stream))) return rc;
-    if ((rc = gsn_update_edges(net, m, s.swin, s.ssec, s.sacc, stream))) return rc;
+    if ((rc = gsn_iterate(net, s.ssig, m, s.swin, s.ssec, s.sd1, s.sd2, s.sacc, stream)))
+      return rc;
     if (gsn::launch_qe(s.sd1, m, s.acc64 + gsn::kA64Window, st) != hipSuccess) return GSN_E_HIP;
     res->signals += m;
     res->iterations += 1;
