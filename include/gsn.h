@@ -299,7 +299,9 @@ int gsn_tune(gsn_net* net, int32_t key, int32_t value);
 /* Kernel timing with HIP events recorded on the caller's stream around each step, for
  * measurement.  gsn_timing_enable(net, 1) starts recording; gsn_timing_read returns the
  * summed duration in milliseconds and the number of launches recorded for one step since
- * the last read, and clears them (syncs).
+ * the last read, and clears them (syncs).  The events are made without the system-scope
+ * memory fence (hipEventDisableSystemFence): they time the work, they publish nothing to
+ * the host, and recording them does not stall the stream.
  *   GSN_T_FIND_SCAN   the find-winners scan kernel alone
  *   GSN_T_FIND        all of gsn_find_winners
  *   GSN_T_RESOLVE, GSN_T_ADAPT, GSN_T_EDGES   all of the corresponding call

@@ -168,8 +168,10 @@ hipEvent_t take_event(gsn_net* net) {
     net->pool.pop_back();
     return e;
   }
+  // timing only: no system-scope fence at the record (the default one writes back and
+  // invalidates the caches, which stalls the stream for several microseconds per record)
   hipEvent_t e = nullptr;
-  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return nullptr;
   return e;
 }
 
@@ -335,7 +337,8 @@ int gsn_find_winners(gsn_net* net, const float* sig, int32_t m, int32_t* winner,
     const gsn::StageBufs sb = gsn::carve_stage(net->s.scr, net->p.n_max, net->p.m_max);
     // the unit order is rebuilt when the network changed and every kRebucketEvery calls
     const bool rebucket = net->bucket_n != net->n || net->finds_since_bucket >= kRebucketEvery;
-    e = gsn::launch_stage(net->s, sb, net->n, sig, m, rebucket, net->stage_parity, st);
+    e = gsn::launch_stage(net->s, sb, net->n, sig, m, rebucket, net->stage_parity,
+                          cfg.variant, st);
     net->stage_parity ^= 1;
     if (rebucket) {
       net->bucket_n = net->n;

@@ -80,6 +80,19 @@ __device__ __forceinline__ void wave_count(bool pred, unsigned long long* ctr) {
     atomicAdd(ctr, static_cast<unsigned long long>(__popcll(mask)));
 }
 
+// Adds the threads of this workgroup for which `pred` holds to *ctr with one atomic per
+// workgroup (same-address atomics from thousands of waves queue up at the cache).  Every
+// thread of the workgroup calls it (it holds a barrier); `acc` is an LDS word that was
+// zeroed before an earlier barrier.
+template <typename T>
+__device__ __forceinline__ void block_count(bool pred, T* ctr, int32_t* acc) {
+  const unsigned long long mask = __ballot(pred);
+  if ((threadIdx.x & 63) == 0 && mask != 0)
+    atomicAdd(acc, static_cast<int32_t>(__popcll(mask)));
+  __syncthreads();
+  if (threadIdx.x == 0 && *acc != 0) atomicAdd(ctr, static_cast<T>(*acc));
+}
+
 // w <- w + eps (xi - w), one binary32 rounding per operation (no contraction).
 __device__ __forceinline__ void move_unit(float* __restrict__ x, float* __restrict__ y,
                                           float* __restrict__ z, int32_t u, float eps,
@@ -168,7 +181,7 @@ StageBufs carve_stage(void* base, int32_t n_max, int32_t m_max);
 hipError_t launch_stage_init(const StageBufs& b, hipStream_t st);
 // parity alternates between calls (two sets of signal histogram and cursors)
 hipError_t launch_stage(const DevState& s, const StageBufs& b, int32_t n, const float* sig,
-                        int32_t m, bool rebucket, int parity, hipStream_t st);
+                        int32_t m, bool rebucket, int parity, int variant, hipStream_t st);
 hipError_t launch_stage_merge(const DevState& s, const StageBufs& b, int32_t m, int split,
                               int32_t* winner, int32_t* second, float* d1, float* d2,
                               hipStream_t st);

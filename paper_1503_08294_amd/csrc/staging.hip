@@ -22,7 +22,11 @@ constexpr int kGrid = 32;
 constexpr int kSignalShift = 3;                        // signals ordered by bucket >> 3
 constexpr int kSignalBuckets = kBuckets >> kSignalShift;
 constexpr int kSeedWindow = 64;
-constexpr int kSeedLanes = 4;
+// operand layouts the gather writes besides the packed records: the binary32 matrix-core
+// one (read by the binary32 product scan) and the binary16 one (the split-binary16 scan)
+constexpr int kLayoutF32 = 1;
+constexpr int kLayoutF16 = 2;
+constexpr int kSeedLanes = 16;
 
 __device__ __forceinline__ int32_t ord(float f) {
   const int32_t b = __float_as_int(f);
@@ -285,7 +289,7 @@ __global__ __launch_bounds__(kBlock) void st_gather(const float* __restrict__ x,
                                                     int32_t* __restrict__ hist_s,
                                                     int32_t* __restrict__ clear_a,
                                                     int32_t* __restrict__ clear_b,
-                                                    float* __restrict__ bmag) {
+                                                    float* __restrict__ bmag, int layouts) {
   if (static_cast<int32_t>(blockIdx.x) < ub) {
     const int32_t pos = blockIdx.x * kBlock + threadIdx.x;
     float mg[4] = {0.0f, 0.0f, 0.0f, 0.0f};
@@ -308,33 +312,36 @@ __global__ __launch_bounds__(kBlock) void st_gather(const float* __restrict__ x,
       // matrix-core layout: batch t = pos / 64 holds 4 groups of 16 units; component k of
       // the unit in row i of group e sits at pm[256 t + 4 (16 k + i) + e]
       const int32_t t = pos >> 6, e = (pos >> 4) & 3, i = pos & 15;
+      if (layouts & kLayoutF32)
 #pragma unroll
-      for (int k = 0; k < 4; ++k) pm[256 * t + 4 * (16 * k + i) + e] = cv[k];
+        for (int k = 0; k < 4; ++k) pm[256 * t + 4 * (16 * k + i) + e] = cv[k];
       // binary16 layout: batch t holds 2 groups of 32 units; lane h * 32 + r (r the row in
       // the group) reads K slots 8h..8h+7 of its row: h = 0 (x1 x1 x2 x2 y1 y1 y2 y2),
       // h = 1 (z1 z1 z2 z2 n1 n2 0 0) of the scaled unit sigma w and its binary32 norm,
       // at pmh[(64 t + lane) * 2 + group].  Padding carries n1 = +inf: never a candidate.
-      const int32_t g2 = (pos >> 5) & 1, r = pos & 31;
-      const float sg = bb[6];
-      h8 o0 = {}, o1 = {};
-      if (pos < n) {
-        const float sx = sg * cv[0], sy = sg * cv[1], sz = sg * cv[2];
-        const float sn = norm2(sx, sy, sz);
-        _Float16 a, b;
-        split16(sx, a, b);
-        o0[0] = a; o0[1] = a; o0[2] = b; o0[3] = b;
-        split16(sy, a, b);
-        o0[4] = a; o0[5] = a; o0[6] = b; o0[7] = b;
-        split16(sz, a, b);
-        o1[0] = a; o1[1] = a; o1[2] = b; o1[3] = b;
-        split16(sn, a, b);
-        o1[4] = a; o1[5] = b;
-      } else {
-        o1[4] = static_cast<_Float16>(__builtin_huge_valf());
+      if (layouts & kLayoutF16) {
+        const int32_t g2 = (pos >> 5) & 1, r = pos & 31;
+        const float sg = bb[6];
+        h8 o0 = {}, o1 = {};
+        if (pos < n) {
+          const float sx = sg * cv[0], sy = sg * cv[1], sz = sg * cv[2];
+          const float sn = norm2(sx, sy, sz);
+          _Float16 a, b;
+          split16(sx, a, b);
+          o0[0] = a; o0[1] = a; o0[2] = b; o0[3] = b;
+          split16(sy, a, b);
+          o0[4] = a; o0[5] = a; o0[6] = b; o0[7] = b;
+          split16(sz, a, b);
+          o1[0] = a; o1[1] = a; o1[2] = b; o1[3] = b;
+          split16(sn, a, b);
+          o1[4] = a; o1[5] = b;
+        } else {
+          o1[4] = static_cast<_Float16>(__builtin_huge_valf());
+        }
+        h8* dst = reinterpret_cast<h8*>(pmh);
+        dst[(64 * static_cast<int64_t>(t) + r) * 2 + g2] = o0;
+        dst[(64 * static_cast<int64_t>(t) + 32 + r) * 2 + g2] = o1;
       }
-      h8* dst = reinterpret_cast<h8*>(pmh);
-      dst[(64 * static_cast<int64_t>(t) + r) * 2 + g2] = o0;
-      dst[(64 * static_cast<int64_t>(t) + 32 + r) * 2 + g2] = o1;
     }
     block_reduce4(mg, FMax());
     if (threadIdx.x == 0)
@@ -585,7 +592,8 @@ hipError_t launch_stage_init(const StageBufs& b, hipStream_t st) {
 }
 
 hipError_t launch_stage(const DevState& s, const StageBufs& b, int32_t n, const float* sig,
-                        int32_t m, bool rebucket, int parity, hipStream_t st) {
+                        int32_t m, bool rebucket, int parity, int variant, hipStream_t st) {
+  const int layouts = variant == 3 ? kLayoutF32 : variant == 4 ? kLayoutF16 : 0;
   const int nb_u = blocks(n);
   if (rebucket) {
     st_bbox<<<std::min(nb_u, 64), kBlock, 0, st>>>(s.x, s.y, s.z, n, b.acc);
@@ -603,7 +611,7 @@ hipError_t launch_stage(const DevState& s, const StageBufs& b, int32_t n, const 
   int32_t* cur_next = b.cur_s + (parity ^ 1) * kSignalBuckets;
   st_gather<<<nb_g + blocks(m), kBlock, 0, st>>>(s.x, s.y, s.z, n, b.pidx, b.pu, b.pm, b.pmh, sig,
                                                  m, nb_g, b.bb, b.skey, hist, hist_next,
-                                                 cur_next, b.bmag);
+                                                 cur_next, b.bmag, layouts);
   st_place_seed<<<blocks(static_cast<int64_t>(m) * kSeedLanes), kBlock, 0, st>>>(
       hist, cur, b.skey, sig, m, b.pu, b.pidx, n, b.off_u, b.sperm, b.seed, b.bmag, nb_g,
       b.mag);

@@ -214,35 +214,112 @@ struct FusedArgs {
   int32_t max_age;
 };
 
+// The fused kernels give each signal a group of kGroup lanes of one wave: lane q takes the
+// neighbours k = q, q + kGroup, ... of the row of b (its claim, its lock word, its move, the
+// age of its edge and the mirror half-edge, its removal), lane 0 also the winner and the
+// second, and the group agrees on the outcome by ballots.  The neighbours' dependent loads
+// (lock word, position, mirror search) then run side by side instead of one after another.
+constexpr int kGroup = 8;
+
+__device__ __forceinline__ uint32_t group_bits(unsigned long long wave_mask) {
+  const int base = static_cast<int>(threadIdx.x & 63) & ~(kGroup - 1);
+  return static_cast<uint32_t>(wave_mask >> base) & ((1u << kGroup) - 1);
+}
+
+// Claims of the lock sets L_j = {b, s} + N(b), as rs_claim.
+__global__ void fu_claim(int32_t m, int32_t n, const int32_t* __restrict__ winner,
+                         const int32_t* __restrict__ second, const float* __restrict__ d1,
+                         const int32_t* __restrict__ rp, const int32_t* __restrict__ col,
+                         unsigned long long* __restrict__ lock, int32_t* __restrict__ status,
+                         int key_mode) {
+  const int32_t gt = blockIdx.x * kBlock + threadIdx.x;
+  const int32_t j = gt / kGroup;
+  const int q = gt % kGroup;
+  if (j >= m) return;
+  const int32_t b = winner[j], s = second[j];
+  if (!pair_ok(b, s, n)) {
+    if (q == 0) raise_error(status, GSN_E_INVAL);
+    return;
+  }
+  const unsigned long long key = signal_key(d1[j], j, key_mode);
+  if (q == 0) {
+    atomicMin(&lock[b], key);
+    atomicMin(&lock[s], key);
+  }
+  for (int32_t k = rp[b] + q; k < rp[b + 1]; k += kGroup) atomicMin(&lock[col[k]], key);
+}
+
+// The check of rs_check and, for an accepted signal, the adaptation of adapt_signal and
+// the marks of mark_signal, with the same result: each unit of L_j is moved once with the
+// same expression, every edge at b is aged (or reset, for {b, s}) and, if older than
+// max_age, marked dead on both half-edges, and a neighbour left without a live edge or a
+// requested one is flagged.  The lane of neighbour v alone writes the row of v, so its
+// orphan test sees that row complete.
 __global__ void fu_check_apply(FusedArgs a) {
-  const int32_t j = blockIdx.x * kBlock + threadIdx.x;
+  __shared__ int32_t s_acc;
+  if (threadIdx.x == 0) s_acc = 0;
+  __syncthreads();
+  const int32_t gt = blockIdx.x * kBlock + threadIdx.x;
+  const int32_t j = gt / kGroup;
+  const int q = gt % kGroup;
   bool ok = false;
   if (j < a.m) {
     const int32_t b = a.winner[j], s = a.second[j];
     if (pair_ok(b, s, a.n)) {
       const unsigned long long key = signal_key(a.d1[j], j, a.key_mode);
-      ok = true;
+      const int32_t r0 = a.rp[b], r1 = a.rp[b + 1];
+      bool mine = true, is_s = false;
       auto visit = [&](int32_t u) {
-        if (a.lock[u] == key) a.lock[u] = ~0ull; else ok = false;
+        if (a.lock[u] == key) a.lock[u] = ~0ull; else mine = false;
       };
-      visit(b);
-      bool s_nb = false;
-      for (int32_t k = a.rp[b]; k < a.rp[b + 1]; ++k) {
+      for (int32_t k = r0 + q; k < r1; k += kGroup) {
         const int32_t v = a.col[k];
-        s_nb |= v == s;
+        is_s |= v == s;
         visit(v);
       }
-      if (!s_nb) visit(s);
+      const bool s_nb = group_bits(__ballot(is_s)) != 0;
+      if (q == 0) {
+        visit(b);
+        if (!s_nb) visit(s);
+      }
+      ok = group_bits(__ballot(!mine)) == 0;
       if (ok) {
-        adapt_signal(a.sig, a.m, j, b, s, a.d1[j], a.rp, a.col, a.x, a.y, a.z, a.err, a.eps_b,
-                     a.eps_n);
-        mark_signal(b, s, a.rp, a.col, a.age, a.ins, a.orphan, a.status, a.max_age);
+        const float sx = a.sig[j], sy = a.sig[a.m + j], sz = a.sig[2 * a.m + j];
+        if (q == 0) {
+          move_unit(a.x, a.y, a.z, b, a.eps_b, sx, sy, sz);
+          if (!s_nb) {
+            move_unit(a.x, a.y, a.z, s, a.eps_n, sx, sy, sz);
+            a.ins[b] = s;
+            a.ins[s] = b;
+          }
+          a.err[b] = a.err[b] + a.d1[j];
+        }
+        for (int32_t k = r0 + q; k < r1; k += kGroup) {
+          const int32_t v = a.col[k];
+          move_unit(a.x, a.y, a.z, v, a.eps_n, sx, sy, sz);
+          const int32_t g = v == s ? 0 : a.age[k] + 1;
+          const int32_t rk = find_in_row(a.rp, a.col, v, b);
+          if (g <= a.max_age) {
+            a.age[k] = g;
+            if (rk >= 0) a.age[rk] = g;
+            continue;
+          }
+          a.age[k] = kDead;
+          if (rk >= 0) a.age[rk] = kDead;
+          bool live = a.ins[v] >= 0;
+          for (int32_t kk = a.rp[v]; !live && kk < a.rp[v + 1]; ++kk) live = a.age[kk] != kDead;
+          if (!live && !a.orphan[v]) {
+            a.orphan[v] = 1;
+            atomicAdd(&a.status[kStOrphans], 1);
+          }
+        }
       }
     }
-    a.accepted[j] = ok ? 1 : 0;
+    if (q == 0) a.accepted[j] = ok ? 1 : 0;
   }
-  wave_count(j < a.m, &a.acc64[kA64Resolved]);
-  wave_count(ok, &a.acc64[kA64Accepted]);
+  if (blockIdx.x == 0 && threadIdx.x == 0)
+    atomicAdd(&a.acc64[kA64Resolved], static_cast<unsigned long long>(a.m));
+  block_count(ok && q == 0, &a.acc64[kA64Accepted], &s_acc);
 }
 
 // New degree of every unit (live half-edges + a requested new edge) and per-block sums;
@@ -443,13 +520,14 @@ hipError_t launch_iterate_set(const DevState& s, int cur, int32_t n, const float
                               hipStream_t st) {
   const int nxt = cur ^ 1;
   if (m > 0) {
-    rs_claim<<<blocks(m), kBlock, 0, st>>>(m, n, winner, second, d1, s.rp[cur], s.col[cur],
-                                           s.lock, s.status, 0, key_mode);
+    const int gb = blocks(static_cast<int64_t>(m) * kGroup);
+    fu_claim<<<gb, kBlock, 0, st>>>(m, n, winner, second, d1, s.rp[cur], s.col[cur], s.lock,
+                                    s.status, key_mode);
     FusedArgs a{sig,      m,          n,          winner,  second,   d1,     key_mode,
                 s.rp[cur], s.col[cur], s.lock,     accepted, s.acc64, s.x,    s.y,
                 s.z,      s.err,      eps_b,      eps_n,   s.age[cur], s.ins, s.orphan,
                 s.status, max_age};
-    fu_check_apply<<<blocks(m), kBlock, 0, st>>>(a);
+    fu_check_apply<<<gb, kBlock, 0, st>>>(a);
   }
   const int nb = blocks(n);
   if (n > 0)

@@ -176,7 +176,8 @@ __global__ void wl_write(int32_t n, const int32_t* __restrict__ rp,
 
 // ------------------------------------------------------------------- rounds ----
 
-constexpr int kRoundBlock = 64;    // threads per workgroup of the grid-wide rounds
+constexpr int kRoundBlock = 64;    // threads per workgroup of the grid-wide claims
+constexpr int kStepBlock = 256;    // threads per workgroup of the grid-wide steps
 constexpr int kTailBlock = 1024;   // threads of the single workgroup of the last rounds
 
 // The lock words are read and released with agent-scope atomics (at L2): the grid-wide
@@ -391,9 +392,12 @@ __device__ bool group_try_apply(const RoundArgs& a, int32_t j, int q) {
   return true;
 }
 
-__global__ void wl_step(RoundArgs a, int32_t t) {
+__global__ __launch_bounds__(kStepBlock) void wl_step(RoundArgs a, int32_t t) {
+  __shared__ int32_t s_left;
   if (t > 0 && a.rem[t - 1] < kTailMin) return;
-  const int32_t gt = blockIdx.x * kRoundBlock + threadIdx.x;
+  if (threadIdx.x == 0) s_left = 0;
+  __syncthreads();
+  const int32_t gt = blockIdx.x * kStepBlock + threadIdx.x;
   const int32_t j = gt / kGroup;
   const int q = gt % kGroup;
   bool left = false;
@@ -404,7 +408,7 @@ __global__ void wl_step(RoundArgs a, int32_t t) {
       left = q == 0;
     }
   }
-  wave_count(left, &a.rem[t]);
+  block_count(left, &a.rem[t], &s_left);
 }
 
 // The remaining rounds in one workgroup: the pending signals are gathered into a list, and
@@ -494,12 +498,12 @@ hipError_t launch_winner_update(const DevState& s, int cur, int32_t n, const Win
               s.z,    s.err,      s.orphan,   s.status,  w.eps_b, w.eps_n,    w.max_age,
               s.rem,  s.list};
   const int g = static_cast<int>((m + kRoundBlock - 1) / kRoundBlock);
-  const int gs = static_cast<int>((static_cast<int64_t>(m) * kGroup + kRoundBlock - 1) /
-                                  kRoundBlock);
+  const int gs = static_cast<int>((static_cast<int64_t>(m) * kGroup + kStepBlock - 1) /
+                                  kStepBlock);
   for (int32_t t = 0; t < w.grid_rounds; ++t) {
     // the first round's claims were made with the survivors
     if (t > 0) wl_claim<<<g, kRoundBlock, 0, st>>>(a, t);
-    wl_step<<<gs, kRoundBlock, 0, st>>>(a, t);
+    wl_step<<<gs, kStepBlock, 0, st>>>(a, t);
   }
   wl_tail<<<1, kTailBlock, 0, st>>>(a, w.grid_rounds);
   // compact adjacency and error decay
