@@ -143,9 +143,10 @@ __device__ __forceinline__ bool block_recheck(const v16f (&r)[2], float th, bool
 __device__ __forceinline__ void finish_batch(const v16f (&res)[kBlocks][2],
                                              const float (&mn)[kBlocks], bool valid, int32_t t,
                                              int h, int lane, int32_t n,
-                                             const f4* __restrict__ lu,
-                                             const int32_t* __restrict__ li, const float* sd,
-                                             float sig2, float (&th)[kBlocks],
+                                             __amdgpu_buffer_rsrc_t ru_,
+                                             __amdgpu_buffer_rsrc_t ri_, int32_t tb0,
+                                             f4* __restrict__ lu, int32_t* __restrict__ li,
+                                             const float* sd, float sig2, float (&th)[kBlocks],
                                              unsigned long long (&k1)[kBlocks],
                                              unsigned long long (&k2)[kBlocks], uint32_t open,
                                              unsigned long long wave_open) {
@@ -154,6 +155,14 @@ __device__ __forceinline__ void finish_batch(const v16f (&res)[kBlocks][2],
   for (int b = 1; b < kBlocks; ++b) lo = __builtin_elementwise_minimum(lo, mn[b] - th[b]);
   const unsigned long long hit = __ballot(lo <= 0.0f) | wave_open;
   if (valid && hit != 0) {
+    // the batch's binary32 units and indices, for the candidates' exact distances: each
+    // lane fetches one unit into the wave's LDS copy (the slots past n get stale values,
+    // which the recheck skips)
+    const int32_t tq = t - tb0;
+    lu[lane] = __builtin_bit_cast(
+        f4, __builtin_amdgcn_raw_buffer_load_b128(ru_, 16 * lane, 1024 * tq, 0));
+    li[lane] = static_cast<int32_t>(
+        __builtin_amdgcn_raw_buffer_load_b32(ri_, 4 * lane, 256 * tq, 0));
     bool improved = false;
 #pragma unroll
     for (int b = 0; b < kBlocks; ++b) {
@@ -187,8 +196,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
     const float* __restrict__ seed, const int32_t* __restrict__ mag,
     const float* __restrict__ bb, unsigned long long* __restrict__ part) {
   constexpr int NB = kBlocks;
-  __shared__ f4 lds_u[4][2][64];                   // binary32 units, two batches per wave
-  __shared__ int32_t lds_i[4][2][64];              // their indices
+  __shared__ f4 lds_u[4][64];                      // binary32 units of a batch, per wave
+  __shared__ int32_t lds_i[4][64];                 // their indices
   __shared__ float sdata[4][NB * kSigFields * 64];  // rare-path signal data
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int j = lane & 31, h = lane >> 5;
@@ -315,17 +324,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
       const_cast<float4*>(pu) + 64 * static_cast<int64_t>(tb0), 0, 0x7fffffff, 0x00020000);
   const __amdgpu_buffer_rsrc_t ri_ = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<int32_t*>(pidx) + 64 * static_cast<int64_t>(tb0), 0, 0x7fffffff, 0x00020000);
-  const int32_t vh = 32 * lane, vu = 16 * lane, vi = 4 * lane;
+  const int32_t vh = 32 * lane;
   h8 ra[kDepth][2];
-  f4 ru[kDepth];
-  int32_t ri[kDepth];
 #pragma unroll
   for (int q = 0; q < kDepth; ++q) {
     const int32_t tq = min(t_begin + q, t_end - 1) - tb0;
     ra[q][0] = __builtin_bit_cast(h8, __builtin_amdgcn_raw_buffer_load_b128(rh, vh, 2048 * tq, 0));
     ra[q][1] = __builtin_bit_cast(h8, __builtin_amdgcn_raw_buffer_load_b128(rh, vh + 16, 2048 * tq, 0));
-    ru[q] = __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(ru_, vu, 1024 * tq, 0));
-    ri[q] = static_cast<int32_t>(__builtin_amdgcn_raw_buffer_load_b32(ri_, vi, 256 * tq, 0));
     asm volatile("" ::: "memory");
   }
   v16f res[2][NB][2];
@@ -340,8 +345,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
 #pragma unroll
     for (int q = 0; q < kDepth; ++q) {
       const int cur = q & 1, prv = cur ^ 1;
-      lds_u[wave][cur][lane] = ru[q];
-      lds_i[wave][cur][lane] = ri[q];
       float mn[NB];
 #pragma unroll
       for (int e = 0; e < 2; ++e) {
@@ -356,11 +359,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
       const int32_t tn = min(t + kDepth + q, t_end - 1) - tb0;
       ra[q][0] = __builtin_bit_cast(h8, __builtin_amdgcn_raw_buffer_load_b128(rh, vh, 2048 * tn, 0));
       ra[q][1] = __builtin_bit_cast(h8, __builtin_amdgcn_raw_buffer_load_b128(rh, vh + 16, 2048 * tn, 0));
-      ru[q] = __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(ru_, vu, 1024 * tn, 0));
-      ri[q] = static_cast<int32_t>(__builtin_amdgcn_raw_buffer_load_b32(ri_, vi, 256 * tn, 0));
       asm volatile("" ::: "memory");
       finish_batch(res[prv], mn, q > 0 || t > t_begin, min(t + q - 1, t_end - 1), h, lane, n,
-                   lds_u[wave][prv], lds_i[wave][prv], sd, sig2, th, k1, k2, open, wave_open);
+                   ru_, ri_, tb0, lds_u[wave], lds_i[wave], sd, sig2, th, k1, k2, open,
+                   wave_open);
     }
   }
   // the chunk's last batch, t_end - 1, sits in the odd set (kDepth is even)
@@ -368,8 +370,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
     float mn[NB];
 #pragma unroll
     for (int b = 0; b < NB; ++b) mn[b] = block_min(res[1][b]);
-    finish_batch(res[1], mn, true, t_end - 1, h, lane, n, lds_u[wave][1], lds_i[wave][1], sd,
-                 sig2, th, k1, k2, open, wave_open);
+    finish_batch(res[1], mn, true, t_end - 1, h, lane, n, ru_, ri_, tb0, lds_u[wave],
+                 lds_i[wave], sd, sig2, th, k1, k2, open, wave_open);
   }
 
   // merge the two partial states of each signal (lanes j and j + 32); lane (j, h) writes
