@@ -10,9 +10,13 @@ Prints one JSON line:
   value            whole-iteration signal-unit distance evaluations per second (m*N/step)
   signals_per_s    m per step time
   fw_evals_per_s   m*N per find-winners call (HIP events around the call)
+  phase_ms         per-call times of the steps, from phase_steps further iterations run
+                   after the timed ones with every timer on (inside the timed steps only
+                   the scan kernel carries an event pair)
   roofline         the find-winners scan kernel (fh_scan, the screened scan on the matrix
                    cores in split binary16): algorithmic FLOP/s (8 per evaluation) from HIP
-                   events around each launch on the library's stream, against the peak of
+                   events around each of its launches in the timed steps, on the library's
+                   stream, against the peak of
                    the contraction's type (binary16 dense, 2.5 PFLOP/s); also the matrix
                    cores' executed rate (32 flops per pair: 32x32x16 products, K = 16) and
                    the algorithmic rate against the fp32 peak; HBM traffic per launch from
@@ -254,7 +258,10 @@ def main():
     cloud = wl.make_cloud()
     units = wl.make_units(cloud)
     stream = SignalStream(cloud, wl.signal_seed)
-    total = args.warmup + args.steps + 1
+    # the timed steps, then a few more with every phase timer on, then one for the
+    # conflict rate
+    phase_steps = min(args.steps, 20)
+    total = args.warmup + args.steps + phase_steps + 1
     host_sig = np.stack([stream.next(wl.m) for _ in range(total)])      # (T, 3, m)
     n, m = units.shape[1], wl.m
 
@@ -291,8 +298,12 @@ def main():
     for t in range(args.warmup):
         step(t)
     torch.cuda.synchronize()
-    for w in range(6):
+    for w in range(gsn.GSN_T_COUNT):
         gsn.gsn_timing_read(net.h, w)
+    # inside the timed steps only the scan kernel carries an event pair (its average launch
+    # duration is the roofline's denominator); each further event pair costs the stream a
+    # few microseconds, so the per-phase times come from the steps after them
+    gsn.gsn_timing_select(net.h, 1 << gsn.GSN_T_FIND_SCAN)
     gsn.gsn_timing_enable(net.h, True)
 
     print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
@@ -304,11 +315,24 @@ def main():
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     gsn.gsn_timing_enable(net.h, False)
+    scan_ms_sum, scan_launches = gsn.gsn_timing_read(net.h, gsn.GSN_T_FIND_SCAN)
+    scan_ms = scan_ms_sum / max(scan_launches, 1)
     resolved = net.stat(gsn.GSN_STAT_RESOLVED)
     accepted_timed = net.stat(gsn.GSN_STAT_ACCEPTED)
     updates = net.stat(gsn.GSN_STAT_UPDATES)
     rounds = ({"mean": net.stat(gsn.GSN_STAT_ROUNDS) / updates,
                "max": net.stat(gsn.GSN_STAT_ROUNDS_MAX)} if updates else None)
+    if net.check() != 0:
+        raise SystemExit(f"device status {net.check()} after the timed steps")
+
+    print(f"[bench] phase timers over {phase_steps} more steps", file=sys.stderr, flush=True)
+    gsn.gsn_timing_select(net.h, (1 << gsn.GSN_T_COUNT) - 1)
+    gsn.gsn_timing_enable(net.h, True)
+    t_phase = args.warmup + args.steps
+    for t in range(t_phase, t_phase + phase_steps):
+        step(t)
+    torch.cuda.synchronize()
+    gsn.gsn_timing_enable(net.h, False)
     phase = {}
     for name, w in (("find_scan", gsn.GSN_T_FIND_SCAN), ("find", gsn.GSN_T_FIND),
                     ("resolve", gsn.GSN_T_RESOLVE), ("adapt", gsn.GSN_T_ADAPT),
@@ -316,10 +340,10 @@ def main():
         ms, cnt = gsn.gsn_timing_read(net.h, w)
         phase[name] = ms / max(cnt, 1)
     if net.check() != 0:
-        raise SystemExit(f"device status {net.check()} after the timed steps")
+        raise SystemExit(f"device status {net.check()} after the phase steps")
 
     # one more untimed iteration to report the conflict rate at this state
-    t_last = args.warmup + args.steps
+    t_last = t_phase + phase_steps
     index_stats = None
     if grid is not None:
         # the index against the exhaustive search on this state and batch
@@ -349,7 +373,7 @@ def main():
     n_units, n_edges = net.sizes()
 
     ms_per_step = 1e3 * elapsed / args.steps
-    scan_s = max(phase["find_scan"], 1e-9) * 1e-3
+    scan_s = max(scan_ms, 1e-9) * 1e-3
     achieved = FLOPS_PER_EVAL * m * n / scan_s / 1e12
     traffic = load_traffic(m * n)
     out = {
@@ -379,6 +403,7 @@ def main():
         "fw_frac_fp32_peak": FLOPS_PER_EVAL * m * n / (phase["find"] * 1e-3) / 1e12
                              / FP32_PEAK_TFLOPS,
         "phase_ms": phase,
+        "phase_steps": phase_steps,
         "conflict_rate": conflict_rate,
         "state_after": {"units": n_units, "edges": n_edges},
         "update_rounds": rounds,
@@ -387,7 +412,8 @@ def main():
                      "achieved": achieved, "peak": F16_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / F16_PEAK_TFLOPS, "traffic": traffic,
                      "flops_per_launch": FLOPS_PER_EVAL * m * n,
-                     "avg_launch_ms": phase["find_scan"],
+                     "avg_launch_ms": scan_ms,
+                     "launches_timed": scan_launches,
                      "executed_mfma_tflops": EXECUTED_FLOPS_PER_PAIR * m * n / scan_s / 1e12,
                      "executed_mfma_frac": EXECUTED_FLOPS_PER_PAIR * m * n / scan_s / 1e12
                                            / F16_PEAK_TFLOPS,

@@ -310,6 +310,10 @@ enum { GSN_T_FIND_SCAN = 0, GSN_T_FIND = 1, GSN_T_RESOLVE = 2, GSN_T_ADAPT = 3,
        GSN_T_EDGES = 4, GSN_T_UPDATE = 5, GSN_T_COUNT = 6 };
 int gsn_timing_enable(gsn_net* net, int32_t enable);
 int gsn_timing_read(gsn_net* net, int32_t which, double* total_ms, int32_t* launches);
+/* Restricts the timers that record while timing is enabled to the bits set in mask (bit w
+ * for GSN_T_w; all of them after gsn_create), so that a measurement can time one kernel
+ * with a single event pair per call.  GSN_E_INVAL for bits beyond GSN_T_COUNT. */
+int gsn_timing_select(gsn_net* net, uint32_t mask);
 
 /* Statistics accumulated on the device since creation or the last GSN_STAT_CLEAR, for
  * measurement.  Syncs.

@@ -118,6 +118,7 @@ struct gsn_net {
   int tune_variant;
   int stage_parity;  // which set of signal histogram and cursors the next call uses
   bool timing;
+  uint32_t timing_mask;  // timers that record while timing is on (bit GSN_T_*)
   int32_t bucket_n;            // unit count at the last spatial bucketing (-1: none yet)
   int32_t finds_since_bucket;
   int grid_rounds;             // grid-wide rounds of the winner-lock update (0: automatic)
@@ -182,7 +183,7 @@ struct TimedRegion {
   hipStream_t st;
   hipEvent_t a = nullptr;
   TimedRegion(gsn_net* n, int w, hipStream_t s) : net(n), which(w), st(s) {
-    if (net->timing) {
+    if (net->timing && ((net->timing_mask >> w) & 1u)) {
       a = take_event(net);
       if (a && hipEventRecord(a, st) != hipSuccess) {
         net->pool.push_back(a);
@@ -283,6 +284,7 @@ int gsn_create(const gsn_params* params, void* workspace, size_t workspace_bytes
   net->tune_variant = 0;
   net->stage_parity = 0;
   net->timing = false;
+  net->timing_mask = (1u << GSN_T_COUNT) - 1;
   net->bucket_n = -1;
   net->finds_since_bucket = 0;
   net->grid_rounds = 0;
@@ -784,6 +786,12 @@ int gsn_stat(gsn_net* net, int32_t key, int64_t* value, void* stream) {
 int gsn_timing_enable(gsn_net* net, int32_t enable) {
   if (!net) return GSN_E_INVAL;
   net->timing = enable != 0;
+  return GSN_OK;
+}
+
+int gsn_timing_select(gsn_net* net, uint32_t mask) {
+  if (!net || (mask >> GSN_T_COUNT) != 0) return GSN_E_INVAL;
+  net->timing_mask = mask;
   return GSN_OK;
 }
 

@@ -36,6 +36,7 @@ GSN_T_RESOLVE = 2
 GSN_T_ADAPT = 3
 GSN_T_EDGES = 4
 GSN_T_UPDATE = 5
+GSN_T_COUNT = 6
 
 GSN_LOCK_SET = 0
 GSN_LOCK_WINNER = 1
@@ -136,6 +137,7 @@ _sig = {
     "gsn_destroy": (None, [_P]),
     "gsn_tune": (ctypes.c_int, [_P, _I, _I]),
     "gsn_timing_enable": (ctypes.c_int, [_P, _I]),
+    "gsn_timing_select": (ctypes.c_int, [_P, ctypes.c_uint32]),
     "gsn_timing_read": (ctypes.c_int, [_P, _I, ctypes.POINTER(ctypes.c_double),
                                        ctypes.POINTER(_I)]),
     "gsn_stat": (ctypes.c_int, [_P, _I, ctypes.POINTER(ctypes.c_int64), _P]),
@@ -283,6 +285,10 @@ def gsn_tune(net, key: int, value: int):
 
 def gsn_timing_enable(net, enable: bool):
     return _check(_lib.gsn_timing_enable(net, 1 if enable else 0), "gsn_timing_enable")
+
+
+def gsn_timing_select(net, mask: int):
+    return _check(_lib.gsn_timing_select(net, mask), "gsn_timing_select")
 
 
 def gsn_timing_read(net, which: int):
