@@ -49,6 +49,7 @@ typedef float f4 __attribute__((ext_vector_type(4)));   // a native vector: stay
 
 constexpr int kBlocks = 2;                        // 32-signal blocks per wave
 constexpr int kSignalsPerWG = 4 * 32 * kBlocks;   // 4 waves
+static_assert(kSignalsPerWG == kScanBlock, "the staging finds the home chunk per work-group");
 constexpr int32_t kSentinel = 0x7fffffff;
 constexpr int kDepth = 4;             // operand ring: loads run kDepth - 1 batches ahead
 static_assert(kDepth % 2 == 0, "the result sets alternate by batch parity");
@@ -191,8 +192,7 @@ __device__ __forceinline__ void finish_batch(const v16f (&res)[kBlocks][2],
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void fh_scan(
     const float4* __restrict__ pu, const uint4* __restrict__ pmh,
     const int32_t* __restrict__ pidx, int32_t n, int32_t chunk_batches,
-    const float* __restrict__ sig, int32_t m, const int32_t* __restrict__ sperm,
-    const int32_t* __restrict__ skey, const int32_t* __restrict__ off_u,
+    const float* __restrict__ ssig, int32_t m, const int32_t* __restrict__ sbpos,
     const float* __restrict__ seed, const int32_t* __restrict__ mag,
     const float* __restrict__ bb, unsigned long long* __restrict__ part) {
   constexpr int NB = kBlocks;
@@ -216,9 +216,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
     const bool xcd = split % 8 == 0;
     const int32_t r = id % 8, k = id / 8;
     sb = xcd ? k % sblocks : static_cast<int32_t>(blockIdx.x);
-    const int32_t pm_ = min(sb * kSignalsPerWG + kSignalsPerWG / 2, m - 1);
-    const int32_t key = min(max(skey[min(max(sperm[pm_], 0), m - 1)], 0), kBuckets - 1);
-    const int32_t pos = min(max(off_u[key], 0), n);
+    const int32_t pos = min(max(sbpos[sb], 0), n);
     const int32_t home = min(pos / (64 * chunk_batches), split - 1);
     if (xcd) {
       // the rank-th nearest (ring distance, then lower q) of the chunks r + 8q
@@ -263,10 +261,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
   for (int b = 0; b < NB; ++b) {
     const int32_t p = base + 32 * b + j;
     const bool live = p < m;
-    const int32_t jj = live ? min(max(sperm[p], 0), m - 1) : 0;
-    const float sx = live ? sig[jj] : 0.0f;
-    const float sy = live ? sig[m + jj] : 0.0f;
-    const float sz = live ? sig[2 * m + jj] : 0.0f;
+    const float sx = live ? ssig[p] : 0.0f;
+    const float sy = live ? ssig[m + p] : 0.0f;
+    const float sz = live ? ssig[2 * m + p] : 0.0f;
     const float tx = sgm * sx, ty = sgm * sy, tz = sgm * sz;  // exact
     const float ss = norm2(tx, ty, tz);
     // signals past m get B = -inf: their threshold is -inf and nothing is a candidate
@@ -413,8 +410,8 @@ hipError_t launch_scan_f16(const DevState& s, const StageBufs& b, int32_t n, con
   // buffer offsets within a chunk are 32-bit: 2 KB per batch
   if (static_cast<int64_t>(chunk_batches) * 2048 >= (1LL << 31)) return hipErrorInvalidValue;
   dim3 grid((m + kSignalsPerWG - 1) / kSignalsPerWG, split);
-  fh_scan<<<grid, 256, 0, st>>>(b.pu, b.pmh, b.pidx, n, chunk_batches, sig, m, b.sperm, b.skey,
-                                b.off_u, b.seed, b.mag, b.bb, s.part);
+  fh_scan<<<grid, 256, 0, st>>>(b.pu, b.pmh, b.pidx, n, chunk_batches, b.ssig, m, b.sbpos,
+                                b.seed, b.mag, b.bb, s.part);
   return hipGetLastError();
 }
 

@@ -48,6 +48,26 @@ def test_every_split_gives_the_same_answer():
         assert_find_equal(g, o, f"split={split}")
 
 
+def test_larger_network_every_split():
+    """40,037 units (a ragged last batch) and 2,999 signals (a ragged last signal block):
+    chunks of several dozen batches, the XCD order of chunks for splits that are multiples of
+    8, exact duplicates in different chunks and signals on top of units."""
+    from paper_1503_08294_amd import gsn
+    rng = np.random.default_rng(22)
+    n, m = 40037, 2999
+    units = rng.standard_normal((3, n)).astype(np.float32)
+    units[:, 30000:31000] = units[:, :1000]
+    units[:, 20000:20300] = units[:, 20300:20600]
+    sig = rng.standard_normal((3, m)).astype(np.float32)
+    sig[:, :500] = units[:, 29500:30000]
+    pair = Pair(units, m_max=m)
+    o = pair.orc.find_winners(sig)
+    for split in (16, 24, 40, 56, 64, 0):
+        pair.net.tune(gsn.GSN_TUNE_SPLIT, split)
+        g = [t.cpu().numpy() for t in pair.net.find_winners(pair.to_dev(sig))]
+        assert_find_equal(g, o, f"split={split}")
+
+
 def test_zero_signals_and_repeat_calls():
     rng = np.random.default_rng(4)
     units = rng.standard_normal((3, 300)).astype(np.float32)
