@@ -93,6 +93,59 @@ __device__ __forceinline__ void block_count(bool pred, T* ctr, int32_t* acc) {
   if (threadIdx.x == 0 && *acc != 0) atomicAdd(ctr, static_cast<T>(*acc));
 }
 
+// A rewrite of per-row counts into offsets (count -> scan of the per-workgroup sums ->
+// write) can skip the single-workgroup scan when it has at most kFoldBlocks workgroups:
+// each writing workgroup sums the block sums before its own and all of them itself.
+constexpr int kFoldBlocks = 2048;
+
+// The sum of bsum[0, blockIdx.x) and of bsum[0, nb).  Every thread of the workgroup calls
+// it (it holds a barrier); red is LDS for 2 ints per wave.
+__device__ __forceinline__ void fold_offsets(const int32_t* __restrict__ bsum, int32_t nb,
+                                             int32_t* red, int32_t* before, int32_t* total) {
+  int32_t a = 0, t = 0;
+  const int32_t me = static_cast<int32_t>(blockIdx.x);
+  for (int32_t i = threadIdx.x; i < nb; i += blockDim.x) {
+    const int32_t v = bsum[i];
+    t += v;
+    a += i < me ? v : 0;
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    a += __shfl_xor(a, o);
+    t += __shfl_xor(t, o);
+  }
+  const int w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    red[w] = a;
+    red[nw + w] = t;
+  }
+  __syncthreads();
+  a = 0;
+  t = 0;
+  for (int k = 0; k < nw; ++k) {
+    a += red[k];
+    t += red[nw + k];
+  }
+  *before = a;
+  *total = t;
+}
+
+// The capacity decision of a folded rewrite, the same in every workgroup: a total above cap
+// (or an abort flagged earlier) aborts it; workgroup 0 records the error and writes the
+// total, or 0 once aborted, to *out_total (if not null), as the block-sum scan would.
+__device__ __forceinline__ bool fold_abort(int32_t total, int64_t cap, int32_t* status,
+                                           int32_t* out_total) {
+  const bool over = static_cast<int64_t>(total) > cap;
+  const bool abort = over || status[kStAbort] != 0;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    if (over) {
+      status[kStAbort] = 1;
+      atomicCAS(&status[kStError], 0, GSN_E_CAPACITY);
+    }
+    if (out_total) *out_total = abort ? 0 : total;
+  }
+  return abort;
+}
+
 // w <- w + eps (xi - w), one binary32 rounding per operation (no contraction).
 __device__ __forceinline__ void move_unit(float* __restrict__ x, float* __restrict__ y,
                                           float* __restrict__ z, int32_t u, float eps,

@@ -389,16 +389,29 @@ __global__ __launch_bounds__(1024) void scan_blocks(int32_t* __restrict__ bsum, 
 
 // Block-local exclusive scan of cnt, plus the block offset, gives each row's start; the
 // row is written as the live old entries merged with the requested new neighbour, in
-// ascending neighbour order.  Clears the request.
+// ascending neighbour order.  Clears the request.  With fold the block offsets and the
+// capacity check come from the raw block sums (fold_offsets, fold_abort: cap and out_total
+// as for scan_blocks); otherwise bsum holds the scanned offsets.
 __global__ void ed_write(int32_t n, const int32_t* __restrict__ rp,
                          const int32_t* __restrict__ col, const int32_t* __restrict__ age,
                          int32_t* __restrict__ ins, const int32_t* __restrict__ cnt,
-                         const int32_t* __restrict__ boff, int32_t* __restrict__ rp_new,
+                         const int32_t* __restrict__ bsum, int32_t* __restrict__ rp_new,
                          int32_t* __restrict__ col_new, int32_t* __restrict__ age_new,
-                         const int32_t* __restrict__ status) {
+                         int32_t* __restrict__ status, int fold, int32_t nb, int64_t cap,
+                         int32_t* __restrict__ out_total) {
   __shared__ int32_t sc[kBlock];
+  __shared__ int32_t red[2 * kBlock / 64];
   const int32_t u = blockIdx.x * kBlock + threadIdx.x;
   const int32_t c = u < n ? cnt[u] : 0;
+  int32_t boff, abort;
+  if (fold) {
+    int32_t total;
+    fold_offsets(bsum, nb, red, &boff, &total);
+    abort = fold_abort(total, cap, status, out_total);
+  } else {
+    boff = bsum[blockIdx.x];
+    abort = status[kStAbort];
+  }
   sc[threadIdx.x] = c;
   __syncthreads();
   for (int off = 1; off < kBlock; off <<= 1) {
@@ -408,10 +421,10 @@ __global__ void ed_write(int32_t n, const int32_t* __restrict__ rp,
     __syncthreads();
   }
   if (u >= n) return;
-  const int32_t start = boff[blockIdx.x] + sc[threadIdx.x] - c;
+  const int32_t start = boff + sc[threadIdx.x] - c;
   const int32_t extra = ins[u];
   ins[u] = -1;
-  if (status[kStAbort]) {
+  if (abort) {
     // the rewrite did not fit: leave a valid, empty adjacency (state is flagged invalid)
     rp_new[u] = 0;
     return;
@@ -503,13 +516,15 @@ hipError_t launch_edges(const DevState& s, int cur, int32_t n, int32_t m,
                                           s.col[cur], s.age[cur], s.ins, s.orphan, s.status,
                                           max_age);
   const int nb = blocks(n);
+  const int fold = nb > 0 && nb <= kFoldBlocks;
   if (n > 0)
     ed_count<<<nb, kBlock, 0, st>>>(n, s.rp[cur], s.age[cur], s.ins, s.cnt, s.bsum, nullptr,
                                     1.0f);
-  scan_blocks<<<1, 1024, 0, st>>>(s.bsum, nb, half_cap, s.rp[nxt] + n, s.status, -1);
+  if (!fold) scan_blocks<<<1, 1024, 0, st>>>(s.bsum, nb, half_cap, s.rp[nxt] + n, s.status, -1);
   if (n > 0)
     ed_write<<<nb, kBlock, 0, st>>>(n, s.rp[cur], s.col[cur], s.age[cur], s.ins, s.cnt,
-                                    s.bsum, s.rp[nxt], s.col[nxt], s.age[nxt], s.status);
+                                    s.bsum, s.rp[nxt], s.col[nxt], s.age[nxt], s.status, fold,
+                                    nb, half_cap, s.rp[nxt] + n);
   return hipGetLastError();
 }
 
@@ -530,13 +545,15 @@ hipError_t launch_iterate_set(const DevState& s, int cur, int32_t n, const float
     fu_check_apply<<<gb, kBlock, 0, st>>>(a);
   }
   const int nb = blocks(n);
+  const int fold = nb > 0 && nb <= kFoldBlocks;
   if (n > 0)
     ed_count<<<nb, kBlock, 0, st>>>(n, s.rp[cur], s.age[cur], s.ins, s.cnt, s.bsum, s.err,
                                     beta);
-  scan_blocks<<<1, 1024, 0, st>>>(s.bsum, nb, half_cap, s.rp[nxt] + n, s.status, -1);
+  if (!fold) scan_blocks<<<1, 1024, 0, st>>>(s.bsum, nb, half_cap, s.rp[nxt] + n, s.status, -1);
   if (n > 0)
     ed_write<<<nb, kBlock, 0, st>>>(n, s.rp[cur], s.col[cur], s.age[cur], s.ins, s.cnt,
-                                    s.bsum, s.rp[nxt], s.col[nxt], s.age[nxt], s.status);
+                                    s.bsum, s.rp[nxt], s.col[nxt], s.age[nxt], s.status, fold,
+                                    nb, half_cap, s.rp[nxt] + n);
   return hipGetLastError();
 }
 

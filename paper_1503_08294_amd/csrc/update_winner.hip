@@ -137,16 +137,29 @@ __global__ void wl_count(int32_t n, const int32_t* __restrict__ rp,
 // Copies every row (len[u] entries, or the CSR row when len is null) to the offsets given
 // by the block-local scan of cnt plus the block offsets; dst_len (if not null) receives the
 // copied length; err (if not null) is multiplied by beta on the way.  Rows stay ascending.
+// With fold the block offsets and the capacity check come from the raw block sums
+// (fold_offsets, fold_abort); otherwise bsum holds the scanned offsets.
 __global__ void wl_write(int32_t n, const int32_t* __restrict__ rp,
                          const int32_t* __restrict__ len, const int32_t* __restrict__ col,
                          const int32_t* __restrict__ age, const int32_t* __restrict__ cnt,
-                         const int32_t* __restrict__ boff, int32_t* __restrict__ dst_rp,
+                         const int32_t* __restrict__ bsum, int32_t* __restrict__ dst_rp,
                          int32_t* __restrict__ dst_col, int32_t* __restrict__ dst_age,
                          int32_t* __restrict__ dst_len, float* __restrict__ err, float beta,
-                         const int32_t* __restrict__ status) {
+                         int32_t* __restrict__ status, int fold, int32_t nb, int64_t cap,
+                         int32_t* __restrict__ out_total) {
   __shared__ int32_t sc[kBlock];
+  __shared__ int32_t red[2 * kBlock / 64];
   const int32_t u = blockIdx.x * kBlock + threadIdx.x;
   const int32_t c = u < n ? cnt[u] : 0;
+  int32_t boff, abort;
+  if (fold) {
+    int32_t total;
+    fold_offsets(bsum, nb, red, &boff, &total);
+    abort = fold_abort(total, cap, status, out_total);
+  } else {
+    boff = bsum[blockIdx.x];
+    abort = status[kStAbort];
+  }
   sc[threadIdx.x] = c;
   __syncthreads();
   for (int off = 1; off < kBlock; off <<= 1) {
@@ -157,13 +170,13 @@ __global__ void wl_write(int32_t n, const int32_t* __restrict__ rp,
   }
   if (u >= n) return;
   if (err) err[u] = err[u] * beta;
-  if (status[kStAbort]) {
+  if (abort) {
     // the rewrite did not fit: leave a valid, empty adjacency (the state is flagged invalid)
     dst_rp[u] = 0;
     if (dst_len) dst_len[u] = 0;
     return;
   }
-  const int32_t start = boff[blockIdx.x] + sc[threadIdx.x] - c;
+  const int32_t start = boff + sc[threadIdx.x] - c;
   const int32_t r0 = rp[u];
   const int32_t l = len ? len[u] : rp[u + 1] - r0;
   dst_rp[u] = start;
@@ -486,12 +499,16 @@ hipError_t launch_winner_update(const DevState& s, int cur, int32_t n, const Win
   wl_prepare<<<blocks(m), kBlock, 0, st>>>(m, n, w.winner, w.second, w.d1, w.accepted,
                                            w.key_mode, s.rp[cur], s.col[cur], s.lock, s.pend,
                                            s.extra, s.rem, s.status);
+  const int fold = nb <= kFoldBlocks;
   wl_count<<<nb, kBlock, 0, st>>>(n, s.rp[cur], nullptr, s.extra, nullptr, s.cnt, s.bsum);
-  hipError_t e = launch_scan_blocks(s.bsum, nb, w.slack_cap, s.rp[nxt] + n, s.status, -1, st);
-  if (e != hipSuccess) return e;
+  hipError_t e = hipSuccess;
+  if (!fold) {
+    e = launch_scan_blocks(s.bsum, nb, w.slack_cap, s.rp[nxt] + n, s.status, -1, st);
+    if (e != hipSuccess) return e;
+  }
   wl_write<<<nb, kBlock, 0, st>>>(n, s.rp[cur], nullptr, s.col[cur], s.age[cur], s.cnt, s.bsum,
                                   s.rp[nxt], s.col[nxt], s.age[nxt], s.len, nullptr, 1.0f,
-                                  s.status);
+                                  s.status, fold, nb, w.slack_cap, s.rp[nxt] + n);
   // rounds
   RoundArgs a{w.sig,  m,          w.winner,   w.second,  w.d1,    w.key_mode, s.pend,
               s.rp[nxt], s.len,   s.col[nxt], s.age[nxt], s.lock, s.x,        s.y,
@@ -508,11 +525,13 @@ hipError_t launch_winner_update(const DevState& s, int cur, int32_t n, const Win
   wl_tail<<<1, kTailBlock, 0, st>>>(a, w.grid_rounds);
   // compact adjacency and error decay
   wl_count<<<nb, kBlock, 0, st>>>(n, s.rp[nxt], s.len, nullptr, s.lock, s.cnt, s.bsum);
-  e = launch_scan_blocks(s.bsum, nb, w.half_cap, s.rp[cur] + n, s.status, -1, st);
-  if (e != hipSuccess) return e;
+  if (!fold) {
+    e = launch_scan_blocks(s.bsum, nb, w.half_cap, s.rp[cur] + n, s.status, -1, st);
+    if (e != hipSuccess) return e;
+  }
   wl_write<<<nb, kBlock, 0, st>>>(n, s.rp[nxt], s.len, s.col[nxt], s.age[nxt], s.cnt, s.bsum,
                                   s.rp[cur], s.col[cur], s.age[cur], nullptr, s.err, w.beta,
-                                  s.status);
+                                  s.status, fold, nb, w.half_cap, s.rp[cur] + n);
   return hipGetLastError();
 }
 

@@ -83,3 +83,33 @@ def test_fused_iteration_equals_the_four_calls(lock_mode):
         assert torch.equal(sa[k], sb[k]), k
     assert a.sizes() == b.sizes() and a.sizes()[0] != 1_500
     assert a.check() == 0 and b.check() == 0
+
+
+@pytest.mark.parametrize("lock_mode", [0, 1])
+def test_network_beyond_the_folded_rewrite(lock_mode):
+    """600,000 units: the edge rewrites take more than 2,048 workgroups, so the block
+    offsets come from the single-workgroup scan instead of being summed by every writing
+    workgroup (the path the smaller workloads never take).  Edges: a path through all units
+    plus chords, ages 0-5, max_age 4 so that edges are pruned; signals on top of units, so
+    that lock sets collide."""
+    import torch
+    from parity import Pair, assert_iter_equal
+    rng = np.random.default_rng(31)
+    n, m = 600_000, 4_096
+    units = rng.standard_normal((3, n)).astype(np.float32)
+    units /= np.linalg.norm(units, axis=0).astype(np.float32)
+    u = np.concatenate([np.arange(n - 1), np.arange(0, n - 7, 3)])
+    v = np.concatenate([np.arange(1, n), np.arange(7, n, 3)])
+    order = np.lexsort((v, u))
+    edges = np.stack([u[order], v[order], rng.integers(0, 6, len(u))]).astype(np.int32)
+    pair = Pair(units, e_max=2 * edges.shape[1] + 4 * m, m_max=m, max_age=4,
+                lock_mode=lock_mode)
+    pair.net.import_state(torch.from_numpy(units), None, torch.from_numpy(edges))
+    pair.orc.import_state(units, None, edges)
+    for t in range(1, 4):
+        pick = rng.integers(0, n, m)
+        sig = (units[:, pick] + 1e-3 * rng.standard_normal((3, m))).astype(np.float32)
+        g, o = pair.iterate(sig, t, 0, False)
+        assert_iter_equal(g, o, f"iteration {t}")
+        pair.compare_state(f"iteration {t}")
+    assert pair.net.check() == 0
