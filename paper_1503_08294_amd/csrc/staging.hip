@@ -522,16 +522,18 @@ __global__ __launch_bounds__(kBlock) void st_merge(const unsigned long long* __r
       b = k;
     }
   };
-  // four rows per step, loaded before any is inserted, so the loads overlap (rows beyond
+  // the output position first, then eight rows per step, all loaded before any is
+  // inserted, so the loads overlap (64 rows, the usual count, take one step; rows beyond
   // the last read the all-ones key, which changes nothing)
+  const int32_t jp = g == 0 && p < m ? sperm[p] : 0;
   if (p < m)
-    for (int32_t q = g; q < rows; q += 32) {
-      unsigned long long k[4];
+    for (int32_t q = g; q < rows; q += 64) {
+      unsigned long long k[8];
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < 8; ++i)
         k[i] = q + 8 * i < rows ? part[(q + 8 * i) * static_cast<size_t>(m) + p] : ~0ull;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) insert(k[i]);
+      for (int i = 0; i < 8; ++i) insert(k[i]);
     }
   sa[g][c] = a;
   sb[g][c] = b;
@@ -541,7 +543,7 @@ __global__ __launch_bounds__(kBlock) void st_merge(const unsigned long long* __r
     insert(sa[h][c]);
     insert(sb[h][c]);
   }
-  const int32_t j = min(max(sperm[p], 0), m - 1);
+  const int32_t j = min(max(jp, 0), m - 1);
   winner[j] = static_cast<int32_t>(static_cast<uint32_t>(a));
   second[j] = static_cast<int32_t>(static_cast<uint32_t>(b));
   d1[j] = __uint_as_float(static_cast<uint32_t>(a >> 32));
