@@ -322,8 +322,17 @@ int gsn_create(const gsn_params* params, void* workspace, size_t workspace_bytes
   return GSN_OK;
 }
 
-int gsn_find_winners(gsn_net* net, const float* sig, int32_t m, int32_t* winner,
-                     int32_t* second, float* d1, float* d2, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// gsn_find_winners; with claim not null the merge of the staged scans also makes the
+// lock-set claims of every signal, and *claimed says whether it did (the direct scan's
+// merge does not).
+int find_impl(gsn_net* net, const float* sig, int32_t m, int32_t* winner, int32_t* second,
+              float* d1, float* d2, void* stream, const gsn::ClaimArgs* claim,
+              bool* claimed) {
+  if (claimed) *claimed = false;
   if (!net || m < 0 || m > net->p.m_max) return GSN_E_INVAL;
   if (net->phase != kReady && net->phase != kFound) return GSN_E_STATE;
   if (net->n < 2) return GSN_E_INVAL;
@@ -355,8 +364,10 @@ int gsn_find_winners(gsn_net* net, const float* sig, int32_t m, int32_t* winner,
                                                          st);
       scan.end();
     }
-    if (e == hipSuccess)
-      e = gsn::launch_stage_merge(net->s, sb, m, cfg.split, winner, second, d1, d2, st);
+    if (e == hipSuccess) {
+      e = gsn::launch_stage_merge(net->s, sb, m, cfg.split, winner, second, d1, d2, claim, st);
+      if (claimed) *claimed = claim != nullptr;
+    }
   } else {
     TimedRegion scan(net, GSN_T_FIND_SCAN, st);
     e = gsn::launch_find_scan(net->s, net->n, sig, m, cfg, winner, second, d1, d2, st);
@@ -365,6 +376,15 @@ int gsn_find_winners(gsn_net* net, const float* sig, int32_t m, int32_t* winner,
   }
   all.end();
   return hip_ok(e);
+}
+
+}  // namespace
+
+extern "C" {
+
+int gsn_find_winners(gsn_net* net, const float* sig, int32_t m, int32_t* winner,
+                     int32_t* second, float* d1, float* d2, void* stream) {
+  return find_impl(net, sig, m, winner, second, d1, d2, stream, nullptr, nullptr);
 }
 
 size_t gsn_grid_workspace_bytes(const gsn_grid* grid, int32_t n_max, int32_t m_max) {
@@ -481,19 +501,25 @@ int gsn_iterate(gsn_net* net, const float* sig, int32_t m, int32_t* winner, int3
   if (!net || m < 0 || m > net->p.m_max) return GSN_E_INVAL;
   if (net->phase != kReady && net->phase != kFound) return GSN_E_STATE;
   if (m > 0 && !accepted) return GSN_E_INVAL;
-  int rc = gsn_find_winners(net, sig, m, winner, second, d1, d2, stream);
-  if (rc) return rc;
   if (net->p.lock_mode != 0) {
+    int rc = gsn_find_winners(net, sig, m, winner, second, d1, d2, stream);
+    if (rc) return rc;
     if ((rc = gsn_resolve_conflicts(net, m, winner, second, d1, accepted, stream))) return rc;
     if ((rc = gsn_adapt(net, sig, m, winner, second, d1, accepted, stream))) return rc;
     return gsn_update_edges(net, m, winner, second, accepted, stream);
   }
+  // the lock-set rule: the merge makes the claims where it can, then the fused update
+  const gsn::ClaimArgs claim{net->n, net->s.rp[net->cur], net->s.col[net->cur], net->s.lock,
+                             net->s.status, net->p.key_mode};
+  bool claimed = false;
+  int rc = find_impl(net, sig, m, winner, second, d1, d2, stream, &claim, &claimed);
+  if (rc) return rc;
   hipStream_t st = as_stream(stream);
   TimedRegion t(net, GSN_T_UPDATE, st);
   const hipError_t e = gsn::launch_iterate_set(
       net->s, net->cur, net->n, sig, m, winner, second, d1, accepted, net->p.key_mode,
       net->p.eps_b, net->p.eps_n, net->p.err_beta, net->p.max_age,
-      2 * static_cast<int64_t>(net->p.e_max), st);
+      2 * static_cast<int64_t>(net->p.e_max), claimed, st);
   t.end();
   if (e != hipSuccess) return GSN_E_HIP;
   net->cur ^= 1;

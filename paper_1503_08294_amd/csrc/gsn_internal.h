@@ -241,9 +241,19 @@ hipError_t launch_stage_init(const StageBufs& b, hipStream_t st);
 // parity alternates between calls (two sets of signal histogram and cursors)
 hipError_t launch_stage(const DevState& s, const StageBufs& b, int32_t n, const float* sig,
                         int32_t m, bool rebucket, int parity, int variant, hipStream_t st);
+// The lock-set claims of the fused iteration, made by the merge once a signal's winner and
+// second are known (claim = nullptr: the merge only merges).
+struct ClaimArgs {
+  int32_t n;
+  const int32_t* rp;
+  const int32_t* col;
+  unsigned long long* lock;
+  int32_t* status;
+  int key_mode;
+};
 hipError_t launch_stage_merge(const DevState& s, const StageBufs& b, int32_t m, int split,
                               int32_t* winner, int32_t* second, float* d1, float* d2,
-                              hipStream_t st);
+                              const ClaimArgs* claim, hipStream_t st);
 int screened_split(int32_t n, int32_t m, int cus, int want);
 hipError_t launch_scan_screened(const DevState& s, const StageBufs& b, int32_t n,
                                 const float* sig, int32_t m, int split, hipStream_t st);
@@ -301,7 +311,7 @@ hipError_t launch_iterate_set(const DevState& s, int cur, int32_t n, const float
                               int32_t m, const int32_t* winner, const int32_t* second,
                               const float* d1, uint8_t* accepted, int key_mode, float eps_b,
                               float eps_n, float beta, int32_t max_age, int64_t half_cap,
-                              hipStream_t st);
+                              bool claimed, hipStream_t st);
 hipError_t launch_scan_blocks(int32_t* bsum, int32_t nb, int64_t cap, int32_t* out_total,
                               int32_t* status, int32_t slot, hipStream_t st);
 hipError_t launch_init(const DevState& s, int cur, int32_t n0, int32_t n_max,

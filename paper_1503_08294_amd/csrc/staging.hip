@@ -500,14 +500,19 @@ __global__ __launch_bounds__(kBlock) void st_place_seed(
 }
 
 // 32 signals per workgroup, 8 groups of lanes split the partial rows, merged in LDS.
+// With claim set (the fused lock-set iteration), the merge then makes the claims of each
+// signal's lock set {b, s} + N(b): its eight threads (one per group) take the neighbours
+// k = g, g + 8, ... of b's row, the first also b and s, each an atomic minimum of the key.
 __global__ __launch_bounds__(kBlock) void st_merge(const unsigned long long* __restrict__ part,
                                                    int32_t rows, int32_t m,
                                                    const int32_t* __restrict__ sperm,
                                                    int32_t* __restrict__ winner,
                                                    int32_t* __restrict__ second,
                                                    float* __restrict__ d1,
-                                                   float* __restrict__ d2) {
+                                                   float* __restrict__ d2, ClaimArgs claim,
+                                                   int do_claim) {
   __shared__ unsigned long long sa[8][32], sb[8][32];
+  __shared__ int32_t sj[32];
   const int c = threadIdx.x & 31, g = threadIdx.x >> 5;
   const int32_t p = blockIdx.x * 32 + c;
   unsigned long long a = ~0ull, b = ~0ull;
@@ -538,16 +543,38 @@ __global__ __launch_bounds__(kBlock) void st_merge(const unsigned long long* __r
   sa[g][c] = a;
   sb[g][c] = b;
   __syncthreads();
-  if (g != 0 || p >= m) return;
-  for (int h = 1; h < 8; ++h) {
-    insert(sa[h][c]);
-    insert(sb[h][c]);
+  if (g == 0 && p < m) {
+    for (int h = 1; h < 8; ++h) {
+      insert(sa[h][c]);
+      insert(sb[h][c]);
+    }
+    const int32_t j = min(max(jp, 0), m - 1);
+    winner[j] = static_cast<int32_t>(static_cast<uint32_t>(a));
+    second[j] = static_cast<int32_t>(static_cast<uint32_t>(b));
+    d1[j] = __uint_as_float(static_cast<uint32_t>(a >> 32));
+    d2[j] = __uint_as_float(static_cast<uint32_t>(b >> 32));
+    sa[0][c] = a;
+    sb[0][c] = b;
+    sj[c] = j;
   }
-  const int32_t j = min(max(jp, 0), m - 1);
-  winner[j] = static_cast<int32_t>(static_cast<uint32_t>(a));
-  second[j] = static_cast<int32_t>(static_cast<uint32_t>(b));
-  d1[j] = __uint_as_float(static_cast<uint32_t>(a >> 32));
-  d2[j] = __uint_as_float(static_cast<uint32_t>(b >> 32));
+  if (!do_claim) return;
+  __syncthreads();
+  if (p >= m) return;
+  const unsigned long long ka = sa[0][c];
+  const int32_t bw = static_cast<int32_t>(static_cast<uint32_t>(ka));
+  const int32_t sw = static_cast<int32_t>(static_cast<uint32_t>(sb[0][c]));
+  if (!pair_ok(bw, sw, claim.n)) {
+    if (g == 0) raise_error(claim.status, GSN_E_INVAL);
+    return;
+  }
+  const unsigned long long key =
+      signal_key(__uint_as_float(static_cast<uint32_t>(ka >> 32)), sj[c], claim.key_mode);
+  if (g == 0) {
+    atomicMin(&claim.lock[bw], key);
+    atomicMin(&claim.lock[sw], key);
+  }
+  for (int32_t k = claim.rp[bw] + g; k < claim.rp[bw + 1]; k += 8)
+    atomicMin(&claim.lock[claim.col[k]], key);
 }
 
 inline int blocks(int64_t n) { return static_cast<int>((n + kBlock - 1) / kBlock); }
@@ -647,9 +674,10 @@ hipError_t launch_stage(const DevState& s, const StageBufs& b, int32_t n, const 
 
 hipError_t launch_stage_merge(const DevState& s, const StageBufs& b, int32_t m, int split,
                               int32_t* winner, int32_t* second, float* d1, float* d2,
-                              hipStream_t st) {
+                              const ClaimArgs* claim, hipStream_t st) {
+  const ClaimArgs none{};
   st_merge<<<(m + 31) / 32, kBlock, 0, st>>>(s.part, 2 * split, m, b.sperm, winner, second, d1,
-                                             d2);
+                                             d2, claim ? *claim : none, claim ? 1 : 0);
   return hipGetLastError();
 }
 

@@ -532,12 +532,13 @@ hipError_t launch_iterate_set(const DevState& s, int cur, int32_t n, const float
                               int32_t m, const int32_t* winner, const int32_t* second,
                               const float* d1, uint8_t* accepted, int key_mode, float eps_b,
                               float eps_n, float beta, int32_t max_age, int64_t half_cap,
-                              hipStream_t st) {
+                              bool claimed, hipStream_t st) {
   const int nxt = cur ^ 1;
   if (m > 0) {
     const int gb = blocks(static_cast<int64_t>(m) * kGroup);
-    fu_claim<<<gb, kBlock, 0, st>>>(m, n, winner, second, d1, s.rp[cur], s.col[cur], s.lock,
-                                    s.status, key_mode);
+    if (!claimed)
+      fu_claim<<<gb, kBlock, 0, st>>>(m, n, winner, second, d1, s.rp[cur], s.col[cur], s.lock,
+                                      s.status, key_mode);
     FusedArgs a{sig,      m,          n,          winner,  second,   d1,     key_mode,
                 s.rp[cur], s.col[cur], s.lock,     accepted, s.acc64, s.x,    s.y,
                 s.z,      s.err,      eps_b,      eps_n,   s.age[cur], s.ins, s.orphan,
