@@ -64,8 +64,9 @@ typedef struct gsn_params {
   float eps_b;       /* winner learning rate, in [0, 1] */
   float eps_n;       /* learning rate of the winner's neighbours and second, in [0, 1] */
   int32_t max_age;   /* an edge at an accepted winner whose age exceeds this is removed, >= 0 */
-  float err_alpha;   /* error scale applied to q and f when a unit is inserted between them */
-  float err_beta;    /* error decay applied to every unit once per iteration */
+  float err_alpha;   /* error scale applied to q and f when a unit is inserted between them,
+                        in [0, 1] */
+  float err_beta;    /* error decay applied to every unit once per iteration, in [0, 1] */
   int32_t n_max;     /* unit capacity, >= 2 */
   int32_t e_max;     /* undirected edge capacity, >= 0 */
   int32_t m_max;     /* signals per iteration capacity, >= 1 */

@@ -133,6 +133,9 @@ bool params_ok(const gsn_params* p) {
   if (!p) return false;
   if (!(p->eps_b >= 0.0f && p->eps_b <= 1.0f)) return false;
   if (!(p->eps_n >= 0.0f && p->eps_n <= 1.0f)) return false;
+  // errors stay >= +0 and only shrink under the two factors (the argmax keys rely on it)
+  if (!(p->err_alpha >= 0.0f && p->err_alpha <= 1.0f)) return false;
+  if (!(p->err_beta >= 0.0f && p->err_beta <= 1.0f)) return false;
   if (p->max_age < 0) return false;
   if (p->n_max < 2 || p->e_max < 0 || p->m_max < 1) return false;
   if (p->lock_mode < 0 || p->lock_mode > 2 || p->key_mode < 0 || p->key_mode > 1) return false;

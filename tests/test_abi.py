@@ -55,6 +55,8 @@ def test_host_side_validation(lib):
     for bad in (make_params(eps_b=1.5), make_params(eps_n=-0.1), make_params(max_age=-1),
                 make_params(n_max=1), make_params(m_max=0), make_params(e_max=-1),
                 make_params(lock_mode=3), make_params(key_mode=-1),
+                make_params(err_alpha=1.5), make_params(err_alpha=-0.5),
+                make_params(err_beta=1.01), make_params(err_beta=float("nan")),
                 make_params(lock_mode=1, e_max=2**30 - 1, m_max=2**20)):
         assert lib.gsn_workspace_bytes(ctypes.byref(bad)) == 0
     P = ctypes.c_void_p
