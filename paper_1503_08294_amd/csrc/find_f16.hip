@@ -185,10 +185,11 @@ __device__ __forceinline__ void finish_batch(const v16f (&res)[kBlocks][2],
 }
 
 // Units arrive in batches of 64 (two groups of 32): lane l reads its two 16-byte operands of
-// batch t at pmh[(64 t + l) * 2 + group] (2 KB contiguous per wave), and the binary32 unit
-// 64 t + l (pu) and its index (pidx), which go to the wave's double-buffered LDS copy for
-// the rare path.  The loop is the software pipeline of find_mfma.hip (products of batch t into
-// one result set, minima of batch t - 1 from the other), with products in group-major order.
+// batch t at pmh[(64 t + l) * 2 + group] (2 KB contiguous per wave).  The binary32 units and
+// their indices are read only for a batch in which some lane has a candidate: lane l then
+// fetches unit 64 t + l (pu) and its index (pidx) into the wave's LDS copy (finish_batch).
+// The loop is the software pipeline of find_mfma.hip (products of batch t into one result
+// set, minima of batch t - 1 from the other), with products in group-major order.
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void fh_scan(
     const float4* __restrict__ pu, const uint4* __restrict__ pmh,
     const int32_t* __restrict__ pidx, int32_t n, int32_t chunk_batches,

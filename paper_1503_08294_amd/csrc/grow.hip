@@ -6,9 +6,10 @@
 // Removed rows are empty, so the half-edge arrays keep their positions; only the row
 // pointers are compacted and the column ids remapped.
 //
-// Insertion is a single small edit done by one workgroup: an argmax reduction over the
-// errors, then one lane rewrites the rows of q and f in place and appends the row of the
-// new unit r = N (its index is the largest, so appending keeps every row ascending).
+// Insertion runs in one workgroup, one unit after another: the argmax over per-segment
+// maxima of the errors held in LDS, the rows of q and f rewritten in place and the row of
+// the new unit r = N appended (its index is the largest, so every row stays ascending);
+// only the segments of q, f and r are rescanned after an insertion.
 #include "gsn_internal.h"
 
 namespace gsn {

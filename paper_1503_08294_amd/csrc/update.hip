@@ -5,8 +5,9 @@
 // because of collisions (Sec. 4).  Here every signal claims its lock set L_j = {b_j, s_j}
 // + N(b_j) with a 64-bit atomic minimum of its key, and survives iff it holds every unit
 // of L_j.  Surviving lock sets are pairwise disjoint, which makes the adaptation and the
-// edge update write-disjoint: one thread per signal, no atomics, and the result equals any
-// sequential order.  The adjacency is a symmetric CSR (row_ptr, col, age per half-edge),
+// edge update write-disjoint: no atomics on positions, errors or rows, and the result
+// equals any sequential order (one thread per signal in the separate calls, a group of
+// eight lanes per signal in the fused iteration).  The adjacency is a symmetric CSR (row_ptr, col, age per half-edge),
 // rows ascending by neighbour; the edge update modifies ages in place, then rewrites a
 // compacted CSR into the other buffer (count -> scan -> scatter).
 #include "gsn_internal.h"
