@@ -122,7 +122,8 @@ struct gsn_net {
   int32_t bucket_n;            // unit count at the last spatial bucketing (-1: none yet)
   int32_t finds_since_bucket;
   int grid_rounds;             // grid-wide rounds of the winner-lock update (0: automatic)
-  int32_t* feedback;           // pinned host copy of the last update's grid rounds used
+  int32_t* feedback;           // pinned host word: the last update's grid rounds used
+  int32_t* feedback_dev;       // its device address, stored by the update's last kernel
   std::vector<hipEvent_t> pool;
   std::vector<std::pair<hipEvent_t, hipEvent_t>> rec[GSN_T_COUNT];
 };
@@ -297,6 +298,12 @@ int gsn_create(const gsn_params* params, void* workspace, size_t workspace_bytes
     return GSN_E_HIP;
   }
   *net->feedback = kDefaultGridRounds - 1;
+  net->feedback_dev = nullptr;
+  if (hipHostGetDevicePointer(reinterpret_cast<void**>(&net->feedback_dev), net->feedback, 0) !=
+      hipSuccess) {
+    gsn_destroy(net);
+    return GSN_E_HIP;
+  }
   int dev = 0, cus = 256;
   if (hipGetDevice(&dev) == hipSuccess &&
       hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess)
@@ -466,11 +473,8 @@ int gsn_adapt(gsn_net* net, const float* sig, int32_t m, const int32_t* winner,
     gsn::WinnerStep w{sig, m, winner, second, d1, accepted, net->p.key_mode, net->p.eps_b,
                       net->p.eps_n, net->p.err_beta, net->p.max_age, g,
                       2 * (static_cast<int64_t>(net->p.e_max) + net->p.m_max),
-                      2 * static_cast<int64_t>(net->p.e_max)};
+                      2 * static_cast<int64_t>(net->p.e_max), net->feedback_dev};
     e = gsn::launch_winner_update(net->s, net->cur, net->n, w, st);
-    if (e == hipSuccess)
-      e = hipMemcpyAsync(net->feedback, net->s.rem + gsn::kRmGridUsed, sizeof(int32_t),
-                         hipMemcpyDeviceToHost, st);
   } else {
     e = gsn::launch_adapt(net->s, net->cur, net->n, sig, m, winner, second, d1, accepted,
                           net->p.eps_b, net->p.eps_n, net->p.err_beta, st);

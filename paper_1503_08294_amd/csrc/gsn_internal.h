@@ -301,6 +301,7 @@ struct WinnerStep {
   int32_t max_age;
   int grid_rounds;   // 0..kMaxGridRounds
   int64_t slack_cap, half_cap;
+  int32_t* feedback; // pinned host word (device address) that receives the grid rounds used
 };
 hipError_t launch_winner_update(const DevState& s, int cur, int32_t n, const WinnerStep& w,
                                 hipStream_t st);

@@ -58,12 +58,27 @@ __device__ bool row_insert(const int32_t* __restrict__ rp, int32_t* __restrict__
   return true;
 }
 
+// Position of v in the ascending slice col[r0, r0 + l), or -1: rows of up to 8 entries
+// (nearly all of them) are read in one batch of loads rather than by a binary search.
+__device__ __forceinline__ int32_t row_find(const int32_t* __restrict__ col, int32_t r0,
+                                            int32_t l, int32_t v) {
+  if (l > 8) return slice_find(col, r0, r0 + l, v);
+  int32_t c[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) c[k] = k < l ? col[r0 + k] : -1;
+  int32_t at = -1;
+#pragma unroll
+  for (int k = 7; k >= 0; --k)
+    if (c[k] == v) at = r0 + k;
+  return at;
+}
+
 // Remove v from the row of u if present; returns the new length.
 __device__ int32_t row_remove(const int32_t* __restrict__ rp, int32_t* __restrict__ len,
                               int32_t* __restrict__ col, int32_t* __restrict__ age, int32_t u,
                               int32_t v) {
   const int32_t r0 = rp[u], l = len[u];
-  const int32_t k = slice_find(col, r0, r0 + l, v);
+  const int32_t k = row_find(col, r0, l, v);
   if (k < 0) return l;
   for (int32_t q = k; q + 1 < r0 + l; ++q) {
     col[q] = col[q + 1];
@@ -224,6 +239,7 @@ struct RoundArgs {
   int32_t max_age;
   int32_t* rem;
   int32_t* list;
+  int32_t* feedback;  // pinned host word for the grid rounds used, or null
 };
 
 // Claim F_j = {b, s} + N(b) with the key of j.
@@ -339,8 +355,10 @@ __device__ __forceinline__ uint32_t group_bits(unsigned long long wave_mask) {
 __device__ bool group_try_apply(const RoundArgs& a, int32_t j, int q) {
   const int32_t b = a.winner[j], s = a.second[j];
   const unsigned long long key = signal_key(a.d1[j], j, a.key_mode);
-  if (lock_read(&a.lock[b]) != key) return false;
+  // the row bounds of b are read with its lock word: they are used only if j holds b, and
+  // then nobody else edits that row during the round
   const int32_t r0 = a.rp[b], l = a.len[b];
+  if (lock_read(&a.lock[b]) != key) return false;
   if (l > kGroup) {
     int applied = 0;
     if (q == 0) applied = try_apply(a, j);
@@ -373,7 +391,7 @@ __device__ bool group_try_apply(const RoundArgs& a, int32_t j, int q) {
   const int32_t g = is_s ? 0 : a_old + 1;
   const bool keep = has && g <= a.max_age;
   if (keep) {
-    const int32_t rk = slice_find(a.col, a.rp[v], a.rp[v] + a.len[v], b);
+    const int32_t rk = row_find(a.col, a.rp[v], a.len[v], b);
     if (rk >= 0) a.age[rk] = g;
   } else if (has) {
     if (row_remove(a.rp, a.len, a.col, a.age, v, b) == 0 && !a.orphan[v]) {
@@ -440,6 +458,9 @@ __global__ __launch_bounds__(kTailBlock) void wl_tail(RoundArgs a, int32_t grid_
     while (ran < grid_rounds && a.rem[ran - 1] >= kTailMin) ++ran;
     s_rounds = ran > 0 && a.rem[kRmSurvivors] > 0 ? ran : 0;
     a.rem[kRmGridUsed] = ran;
+    // the host reads it when it enqueues a later update (a stale value only changes how
+    // the rounds are split); a store straight to its pinned word spares the stream a copy
+    if (a.feedback) __hip_atomic_store(a.feedback, ran, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
     s_n = 0;
     s_next = 0;
   }
@@ -513,7 +534,7 @@ hipError_t launch_winner_update(const DevState& s, int cur, int32_t n, const Win
   RoundArgs a{w.sig,  m,          w.winner,   w.second,  w.d1,    w.key_mode, s.pend,
               s.rp[nxt], s.len,   s.col[nxt], s.age[nxt], s.lock, s.x,        s.y,
               s.z,    s.err,      s.orphan,   s.status,  w.eps_b, w.eps_n,    w.max_age,
-              s.rem,  s.list};
+              s.rem,  s.list,     w.feedback};
   const int g = static_cast<int>((m + kRoundBlock - 1) / kRoundBlock);
   const int gs = static_cast<int>((static_cast<int64_t>(m) * kGroup + kStepBlock - 1) /
                                   kStepBlock);
