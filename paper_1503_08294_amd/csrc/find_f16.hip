@@ -51,8 +51,7 @@ constexpr int kBlocks = 2;                        // 32-signal blocks per wave
 constexpr int kSignalsPerWG = 4 * 32 * kBlocks;   // 4 waves
 static_assert(kSignalsPerWG == kScanBlock, "the staging finds the home chunk per work-group");
 constexpr int32_t kSentinel = 0x7fffffff;
-constexpr int kDepth = 4;             // operand ring: loads run kDepth - 1 batches ahead
-static_assert(kDepth % 2 == 0, "the result sets alternate by batch parity");
+constexpr int kDepth = 2;             // operand ring: loads run kDepth - 1 batches ahead
 constexpr int kSigFields = 5;         // rare-path signal data: sx, sy, sz, S^, E (scaled S, E)
 
 __device__ __forceinline__ unsigned long long pack(float d, int32_t i) {
@@ -139,8 +138,7 @@ __device__ __forceinline__ bool block_recheck(const v16f (&r)[2], float th, bool
 }
 
 // Completes batch t once the minima mn[b] of its blocks are known (see find_mfma.hip): the
-// ballot is unconditional so the minima stay between the products; valid is uniform and
-// false for the placeholder batch before a chunk's first.
+// ballot is unconditional; valid is uniform (false skips the batch).
 __device__ __forceinline__ void finish_batch(const v16f (&res)[kBlocks][2],
                                              const float (&mn)[kBlocks], bool valid, int32_t t,
                                              int h, int lane, int32_t n,
@@ -188,9 +186,11 @@ __device__ __forceinline__ void finish_batch(const v16f (&res)[kBlocks][2],
 // batch t at pmh[(64 t + l) * 2 + group] (2 KB contiguous per wave).  The binary32 units and
 // their indices are read only for a batch in which some lane has a candidate: lane l then
 // fetches unit 64 t + l (pu) and its index (pidx) into the wave's LDS copy (finish_batch).
-// The loop is the software pipeline of find_mfma.hip (products of batch t into one result
-// set, minima of batch t - 1 from the other), with products in group-major order.
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void fh_scan(
+// One result set: the minima of a batch follow its own products, and the other waves of the
+// SIMD cover their latency (119 VGPRs, four waves per SIMD; measured faster than the
+// two-set pipeline of find_mfma.hip at two waves per SIMD, whose 200 VGPRs allow no more).
+// Products in group-major order.
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void fh_scan(
     const float4* __restrict__ pu, const uint4* __restrict__ pmh,
     const int32_t* __restrict__ pidx, int32_t n, int32_t chunk_batches,
     const float* __restrict__ ssig, int32_t m, const int32_t* __restrict__ sbpos,
@@ -331,45 +331,28 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
     ra[q][1] = __builtin_bit_cast(h8, __builtin_amdgcn_raw_buffer_load_b128(rh, vh + 16, 2048 * tq, 0));
     asm volatile("" ::: "memory");
   }
-  v16f res[2][NB][2];
-#pragma unroll
-  for (int b = 0; b < NB; ++b)
-#pragma unroll
-    for (int e = 0; e < 2; ++e)
-#pragma unroll
-      for (int k = 0; k < 16; ++k) res[1][b][e][k] = __builtin_huge_valf();
+  v16f res[NB][2];
   const v16f zero16 = {};
   for (int32_t t = t_begin; t < t_end; t += kDepth) {
 #pragma unroll
     for (int q = 0; q < kDepth; ++q) {
-      const int cur = q & 1, prv = cur ^ 1;
-      float mn[NB];
 #pragma unroll
       for (int e = 0; e < 2; ++e) {
         const h8 a = ra[q][e];
 #pragma unroll
         for (int b = 0; b < NB; ++b)
-          res[cur][b][e] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, bop[b], zero16, 0, 0, 0);
-        __builtin_amdgcn_sched_barrier(0);
-        mn[e] = block_min(res[prv][e]);
-        __builtin_amdgcn_sched_barrier(0);
+          res[b][e] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, bop[b], zero16, 0, 0, 0);
       }
       const int32_t tn = min(t + kDepth + q, t_end - 1) - tb0;
       ra[q][0] = __builtin_bit_cast(h8, __builtin_amdgcn_raw_buffer_load_b128(rh, vh, 2048 * tn, 0));
       ra[q][1] = __builtin_bit_cast(h8, __builtin_amdgcn_raw_buffer_load_b128(rh, vh + 16, 2048 * tn, 0));
       asm volatile("" ::: "memory");
-      finish_batch(res[prv], mn, q > 0 || t > t_begin, min(t + q - 1, t_end - 1), h, lane, n,
-                   ru_, ri_, tb0, lds_u[wave], lds_i[wave], sd, sig2, th, k1, k2, open,
-                   wave_open);
-    }
-  }
-  // the chunk's last batch, t_end - 1, sits in the odd set (kDepth is even)
-  if (t_begin < t_end) {
-    float mn[NB];
+      float mn[NB];
 #pragma unroll
-    for (int b = 0; b < NB; ++b) mn[b] = block_min(res[1][b]);
-    finish_batch(res[1], mn, true, t_end - 1, h, lane, n, ru_, ri_, tb0, lds_u[wave],
-                 lds_i[wave], sd, sig2, th, k1, k2, open, wave_open);
+      for (int b = 0; b < NB; ++b) mn[b] = block_min(res[b]);
+      finish_batch(res, mn, true, min(t + q, t_end - 1), h, lane, n, ru_, ri_, tb0,
+                   lds_u[wave], lds_i[wave], sd, sig2, th, k1, k2, open, wave_open);
+    }
   }
 
   // merge the two partial states of each signal (lanes j and j + 32); lane (j, h) writes
