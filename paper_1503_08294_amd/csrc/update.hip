@@ -29,6 +29,22 @@ __device__ __forceinline__ int32_t find_in_row(const int32_t* __restrict__ rp,
   return -1;
 }
 
+// The same for rows of up to 8 entries (nearly all of them), read in one batch of loads.
+__device__ __forceinline__ int32_t find_in_short_row(const int32_t* __restrict__ rp,
+                                                     const int32_t* __restrict__ col,
+                                                     int32_t u, int32_t v) {
+  const int32_t r0 = rp[u], l = rp[u + 1] - r0;
+  if (l > 8) return find_in_row(rp, col, u, v);
+  int32_t c[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) c[k] = k < l ? col[r0 + k] : -1;
+  int32_t at = -1;
+#pragma unroll
+  for (int k = 7; k >= 0; --k)
+    if (c[k] == v) at = r0 + k;
+  return at;
+}
+
 // ------------------------------------------------------------------ resolve ----
 
 // winner_only: L_j = {b}, else L_j = {b, s} + N(b).
@@ -299,7 +315,7 @@ __global__ void fu_check_apply(FusedArgs a) {
           const int32_t v = a.col[k];
           move_unit(a.x, a.y, a.z, v, a.eps_n, sx, sy, sz);
           const int32_t g = v == s ? 0 : a.age[k] + 1;
-          const int32_t rk = find_in_row(a.rp, a.col, v, b);
+          const int32_t rk = find_in_short_row(a.rp, a.col, v, b);
           if (g <= a.max_age) {
             a.age[k] = g;
             if (rk >= 0) a.age[rk] = g;
