@@ -253,8 +253,19 @@ int grow_step(gsn_net* net, int32_t count, int32_t* inserted_out, hipStream_t st
       return GSN_E_HIP;
     rc = read_status_slot(net, gsn::kStInserted, &inserted, st);
     if (rc) return rc;
+    const int32_t n_before = net->n;
     net->n += inserted;
-    if (inserted) net->bucket_n = -1;
+    if (inserted) {
+      // new units take the next indices: they join the spatial order at its end (the
+      // periodic rebucketing restores locality); after a removal the order is rebuilt
+      if (net->bucket_n == n_before) {
+        const gsn::StageBufs sb = gsn::carve_stage(net->s.scr, net->p.n_max, net->p.m_max);
+        if (gsn::launch_stage_append(sb, n_before, net->n, st) != hipSuccess) return GSN_E_HIP;
+        net->bucket_n = net->n;
+      } else {
+        net->bucket_n = -1;
+      }
+    }
   }
   if (inserted_out) *inserted_out = inserted;
   return GSN_OK;

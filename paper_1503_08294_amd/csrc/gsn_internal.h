@@ -238,6 +238,8 @@ struct StageBufs {
 size_t stage_bytes(int32_t n_max, int32_t m_max);
 StageBufs carve_stage(void* base, int32_t n_max, int32_t m_max);
 hipError_t launch_stage_init(const StageBufs& b, hipStream_t st);
+// units n0 .. n1 - 1 appended to the spatial order (older indices unchanged)
+hipError_t launch_stage_append(const StageBufs& b, int32_t n0, int32_t n1, hipStream_t st);
 // parity alternates between calls (two sets of signal histogram and cursors)
 hipError_t launch_stage(const DevState& s, const StageBufs& b, int32_t n, const float* sig,
                         int32_t m, bool rebucket, int parity, int variant, hipStream_t st);

@@ -270,6 +270,15 @@ __global__ __launch_bounds__(kBlock) void st_scatter_units(int32_t n,
   if (pos >= 0 && pos < n) pidx[pos] = i;  // always true when counts match keys
 }
 
+// Units added at the end (indices n0 .. n1 - 1, every older index unchanged) join the
+// order at its end: the scan still visits every unit, only their place is not spatial until
+// the next bucketing.
+__global__ __launch_bounds__(kBlock) void st_append(int32_t n0, int32_t n1,
+                                                    int32_t* __restrict__ pidx) {
+  const int32_t i = n0 + blockIdx.x * kBlock + threadIdx.x;
+  if (i < n1) pidx[i] = i;
+}
+
 // ------------------------------------------------------------- every call ----
 
 // Blocks [0, ub): gather the current positions into sorted order and write each block's
@@ -638,6 +647,12 @@ StageBufs carve_stage(void* base, int32_t n_max, int32_t m_max) {
   s.pm = reinterpret_cast<float*>(take(16 * ((nm + 63) / 64 * 64)));
   s.pmh = reinterpret_cast<uint4*>(take(32 * ((nm + 63) / 64 * 64)));
   return s;
+}
+
+hipError_t launch_stage_append(const StageBufs& b, int32_t n0, int32_t n1, hipStream_t st) {
+  if (n1 <= n0) return hipSuccess;
+  st_append<<<blocks(n1 - n0), kBlock, 0, st>>>(n0, n1, b.pidx);
+  return hipGetLastError();
 }
 
 hipError_t launch_stage_init(const StageBufs& b, hipStream_t st) {
