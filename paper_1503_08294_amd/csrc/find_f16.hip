@@ -85,19 +85,19 @@ __device__ __forceinline__ float fmin3(float a, float b, float c) {
   return __builtin_elementwise_minimum(__builtin_elementwise_minimum(a, b), c);
 }
 
-// Minimum of the 32 results of a block (two groups).
+// Minimum of the 32 results of a block (two groups): fifteen three-input minima leave two
+// values, one two-input minimum joins them (31 reductions in 16 instructions).
 __device__ __forceinline__ float block_min(const v16f (&r)[2]) {
-  float m[2];
+  float x[10];
 #pragma unroll
-  for (int e = 0; e < 2; ++e) {
-    const float a = fmin3(r[e][0], r[e][1], r[e][2]);
-    const float b = fmin3(r[e][3], r[e][4], r[e][5]);
-    const float c = fmin3(r[e][6], r[e][7], r[e][8]);
-    const float d = fmin3(r[e][9], r[e][10], r[e][11]);
-    const float f = fmin3(r[e][12], r[e][13], r[e][14]);
-    m[e] = __builtin_elementwise_minimum(fmin3(a, b, c), fmin3(d, f, r[e][15]));
-  }
-  return __builtin_elementwise_minimum(m[0], m[1]);
+  for (int e = 0; e < 2; ++e)
+#pragma unroll
+    for (int i = 0; i < 5; ++i) x[5 * e + i] = fmin3(r[e][3 * i], r[e][3 * i + 1], r[e][3 * i + 2]);
+  const float y0 = fmin3(x[0], x[1], x[2]);
+  const float y1 = fmin3(x[3], x[4], r[0][15]);
+  const float y2 = fmin3(x[5], x[6], x[7]);
+  const float y3 = fmin3(x[8], x[9], r[1][15]);
+  return __builtin_elementwise_minimum(fmin3(y0, y1, y2), y3);
 }
 
 // The rare path of block b of batch t, under a wave-uniform condition: bit 16 e + 4 q + r of
@@ -149,10 +149,10 @@ __device__ __forceinline__ void finish_batch(const v16f (&res)[kBlocks][2],
                                              unsigned long long (&k1)[kBlocks],
                                              unsigned long long (&k2)[kBlocks], uint32_t open,
                                              unsigned long long wave_open) {
-  float lo = mn[0] - th[0];
+  // one ballot per block: each compare then writes its lane mask directly
+  unsigned long long hit = wave_open;
 #pragma unroll
-  for (int b = 1; b < kBlocks; ++b) lo = __builtin_elementwise_minimum(lo, mn[b] - th[b]);
-  const unsigned long long hit = __ballot(lo <= 0.0f) | wave_open;
+  for (int b = 0; b < kBlocks; ++b) hit |= __ballot(mn[b] <= th[b]);
   if (valid && hit != 0) {
     // the batch's binary32 units and indices, for the candidates' exact distances: each
     // lane fetches one unit into the wave's LDS copy (the slots past n get stale values,
@@ -187,7 +187,7 @@ __device__ __forceinline__ void finish_batch(const v16f (&res)[kBlocks][2],
 // their indices are read only for a batch in which some lane has a candidate: lane l then
 // fetches unit 64 t + l (pu) and its index (pidx) into the wave's LDS copy (finish_batch).
 // One result set: the minima of a batch follow its own products, and the other waves of the
-// SIMD cover their latency (119 VGPRs, four waves per SIMD; measured faster than the
+// SIMD cover their latency (122 VGPRs, four waves per SIMD; measured faster than the
 // two-set pipeline of find_mfma.hip at two waves per SIMD, whose 200 VGPRs allow no more).
 // Products in group-major order.
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void fh_scan(
