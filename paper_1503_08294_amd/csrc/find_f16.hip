@@ -49,7 +49,6 @@ typedef float f4 __attribute__((ext_vector_type(4)));   // a native vector: stay
 
 constexpr int kBlocks = 2;                        // 32-signal blocks per wave
 constexpr int kSignalsPerWG = 4 * 32 * kBlocks;   // 4 waves
-static_assert(kSignalsPerWG == kScanBlock, "the staging finds the home chunk per work-group");
 constexpr int32_t kSentinel = 0x7fffffff;
 constexpr int kDepth = 2;             // operand ring: loads run kDepth - 1 batches ahead
 constexpr int kSigFields = 5;         // rare-path signal data: sx, sy, sz, S^, E (scaled S, E)
@@ -137,13 +136,14 @@ __device__ __forceinline__ bool block_recheck(const v16f (&r)[2], float th, bool
   return improved;
 }
 
-// Completes batch t once the minima mn[b] of its blocks are known (see find_mfma.hip): the
-// ballot is unconditional; valid is uniform (false skips the batch).
+// Completes batch t (tq batches past the work-group's first) once the minima mn[b] of its
+// blocks are known (see find_mfma.hip): the ballot is unconditional; valid is uniform (false
+// skips the batch).
 __device__ __forceinline__ void finish_batch(const v16f (&res)[kBlocks][2],
                                              const float (&mn)[kBlocks], bool valid, int32_t t,
                                              int h, int lane, int32_t n,
                                              __amdgpu_buffer_rsrc_t ru_,
-                                             __amdgpu_buffer_rsrc_t ri_, int32_t tb0,
+                                             __amdgpu_buffer_rsrc_t ri_, int32_t tq,
                                              f4* __restrict__ lu, int32_t* __restrict__ li,
                                              const float* sd, float sig2, float (&th)[kBlocks],
                                              unsigned long long (&k1)[kBlocks],
@@ -157,7 +157,6 @@ __device__ __forceinline__ void finish_batch(const v16f (&res)[kBlocks][2],
     // the batch's binary32 units and indices, for the candidates' exact distances: each
     // lane fetches one unit into the wave's LDS copy (the slots past n get stale values,
     // which the recheck skips)
-    const int32_t tq = t - tb0;
     lu[lane] = __builtin_bit_cast(
         f4, __builtin_amdgcn_raw_buffer_load_b128(ru_, 16 * lane, 1024 * tq, 0));
     li[lane] = static_cast<int32_t>(
@@ -192,8 +191,7 @@ __device__ __forceinline__ void finish_batch(const v16f (&res)[kBlocks][2],
 // Products in group-major order.
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void fh_scan(
     const float4* __restrict__ pu, const uint4* __restrict__ pmh,
-    const int32_t* __restrict__ pidx, int32_t n, int32_t chunk_batches,
-    const float* __restrict__ ssig, int32_t m, const int32_t* __restrict__ sbpos,
+    const int32_t* __restrict__ pidx, int32_t n, const float* __restrict__ ssig, int32_t m,
     const float* __restrict__ seed, const int32_t* __restrict__ mag,
     const float* __restrict__ bb, unsigned long long* __restrict__ part) {
   constexpr int NB = kBlocks;
@@ -203,47 +201,27 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int j = lane & 31, h = lane >> 5;
   const int32_t n_batches = (n + 63) >> 6;
-  // Work-group -> (signal block sb, chunk c).  Work-groups go to the 8 XCDs round-robin by
+  // Work-group -> (signal block sb, chunk c).  Chunk c holds the batches t = c (mod split),
+  // so every chunk samples the whole spatial order evenly: the few batches near a block's
+  // signals, where its candidates and so its rare-path work lie, spread over all of its
+  // work-groups instead of weighing on one.  Work-groups go to the 8 XCDs round-robin by
   // linear id; when the split is a multiple of 8, XCD r gets the chunks c = r (mod 8) only,
-  // so its L2 holds a quarter-or-less of the operand array instead of all of it.  Within an
-  // XCD, the signal blocks take their chunks nearest to the home chunk (the one holding
-  // their signals' cells) first; otherwise the home chunk first, then alternately above and
-  // below it.
+  // so its L2 holds an eighth of the operand array (the batches t = r (mod 8)).
+  const int32_t split = static_cast<int32_t>(gridDim.y);
   int32_t c, sb;
-  {
-    const int32_t split = static_cast<int32_t>(gridDim.y);
+  if (split % 8 == 0) {
     const int32_t sblocks = static_cast<int32_t>(gridDim.x);
     const int32_t id = static_cast<int32_t>(blockIdx.x) + static_cast<int32_t>(blockIdx.y) * sblocks;
-    const bool xcd = split % 8 == 0;
-    const int32_t r = id % 8, k = id / 8;
-    sb = xcd ? k % sblocks : static_cast<int32_t>(blockIdx.x);
-    const int32_t pos = min(max(sbpos[sb], 0), n);
-    const int32_t home = min(pos / (64 * chunk_batches), split - 1);
-    if (xcd) {
-      // the rank-th nearest (ring distance, then lower q) of the chunks r + 8q
-      const int32_t per = split / 8, rank = k / sblocks;
-      auto ring = [&](int32_t cc) {
-        const int32_t a = cc > home ? cc - home : home - cc;
-        return min(a, split - a);
-      };
-      c = r;
-      for (int32_t q = 0; q < per; ++q) {
-        const int32_t cq = r + 8 * q, dq = ring(cq);
-        int32_t before = 0;
-        for (int32_t p = 0; p < per; ++p) {
-          const int32_t dp = ring(r + 8 * p);
-          before += dp < dq || (dp == dq && p < q);
-        }
-        if (before == rank) c = cq;
-      }
-    } else {
-      const int32_t y = static_cast<int32_t>(blockIdx.y);
-      const int32_t d = (y & 1) ? (y + 1) / 2 : -(y / 2);
-      c = ((home + d) % split + split) % split;
-    }
+    const int32_t k = id / 8;
+    sb = k % sblocks;
+    c = id % 8 + 8 * (k / sblocks);
+  } else {
+    sb = static_cast<int32_t>(blockIdx.x);
+    c = static_cast<int32_t>(blockIdx.y);
   }
-  const int32_t t_begin = c * chunk_batches;
-  const int32_t t_end = min(n_batches, t_begin + chunk_batches);
+  // batches c + split i, i < cnt, of the chunk (none when c >= n_batches)
+  const int32_t cnt = c < n_batches ? (n_batches - 1 - c) / split + 1 : 0;
+  const int32_t last = max(cnt - 1, 0);
   const float u = 5.9604644775390625e-8f;
   const float sgm = bb[6], sig2 = sgm * sgm;
   const float xm = sgm * __int_as_float(mag[0]), ym = sgm * __int_as_float(mag[1]);
@@ -315,7 +293,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
   // or the last batch for an empty chunk): the lane's offset sits in the vector offset and
   // the batch's in the scalar offset.  Every access is in bounds by construction (batches
   // are clamped to the chunk, the host keeps chunk offsets below 2^31).
-  const int32_t tb0 = min(t_begin, n_batches - 1);
+  const int32_t tb0 = min(c, n_batches - 1);
+  const int32_t stride = 2048 * split;  // operand bytes from one batch of the chunk to the next
   const __amdgpu_buffer_rsrc_t rh = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint4*>(pmh) + 128 * static_cast<int64_t>(tb0), 0, 0x7fffffff, 0x00020000);
   const __amdgpu_buffer_rsrc_t ru_ = __builtin_amdgcn_make_buffer_rsrc(
@@ -326,14 +305,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
   h8 ra[kDepth][2];
 #pragma unroll
   for (int q = 0; q < kDepth; ++q) {
-    const int32_t tq = min(t_begin + q, t_end - 1) - tb0;
-    ra[q][0] = __builtin_bit_cast(h8, __builtin_amdgcn_raw_buffer_load_b128(rh, vh, 2048 * tq, 0));
-    ra[q][1] = __builtin_bit_cast(h8, __builtin_amdgcn_raw_buffer_load_b128(rh, vh + 16, 2048 * tq, 0));
+    const int32_t iq = min(q, last);
+    ra[q][0] = __builtin_bit_cast(h8, __builtin_amdgcn_raw_buffer_load_b128(rh, vh, stride * iq, 0));
+    ra[q][1] = __builtin_bit_cast(h8, __builtin_amdgcn_raw_buffer_load_b128(rh, vh + 16, stride * iq, 0));
     asm volatile("" ::: "memory");
   }
   v16f res[NB][2];
   const v16f zero16 = {};
-  for (int32_t t = t_begin; t < t_end; t += kDepth) {
+  for (int32_t i = 0; i < cnt; i += kDepth) {
 #pragma unroll
     for (int q = 0; q < kDepth; ++q) {
 #pragma unroll
@@ -343,14 +322,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
         for (int b = 0; b < NB; ++b)
           res[b][e] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, bop[b], zero16, 0, 0, 0);
       }
-      const int32_t tn = min(t + kDepth + q, t_end - 1) - tb0;
-      ra[q][0] = __builtin_bit_cast(h8, __builtin_amdgcn_raw_buffer_load_b128(rh, vh, 2048 * tn, 0));
-      ra[q][1] = __builtin_bit_cast(h8, __builtin_amdgcn_raw_buffer_load_b128(rh, vh + 16, 2048 * tn, 0));
+      const int32_t in = min(i + kDepth + q, last);
+      ra[q][0] = __builtin_bit_cast(h8, __builtin_amdgcn_raw_buffer_load_b128(rh, vh, stride * in, 0));
+      ra[q][1] = __builtin_bit_cast(h8, __builtin_amdgcn_raw_buffer_load_b128(rh, vh + 16, stride * in, 0));
       asm volatile("" ::: "memory");
       float mn[NB];
 #pragma unroll
       for (int b = 0; b < NB; ++b) mn[b] = block_min(res[b]);
-      finish_batch(res, mn, true, min(t + q, t_end - 1), h, lane, n, ru_, ri_, tb0,
+      const int32_t ic = min(i + q, last);
+      finish_batch(res, mn, true, c + split * ic, h, lane, n, ru_, ri_, split * ic,
                    lds_u[wave], lds_i[wave], sd, sig2, th, k1, k2, open, wave_open);
     }
   }
@@ -390,11 +370,10 @@ int f16_split(int32_t n, int32_t m, int cus, int want) {
 hipError_t launch_scan_f16(const DevState& s, const StageBufs& b, int32_t n, const float* sig,
                            int32_t m, int split, hipStream_t st) {
   const int32_t n_batches = (n + 63) / 64;
-  const int32_t chunk_batches = (n_batches + split - 1) / split;
-  // buffer offsets within a chunk are 32-bit: 2 KB per batch
-  if (static_cast<int64_t>(chunk_batches) * 2048 >= (1LL << 31)) return hipErrorInvalidValue;
+  // buffer offsets from a chunk's first batch are 32-bit: 2 KB per batch
+  if (static_cast<int64_t>(n_batches) * 2048 >= (1LL << 31)) return hipErrorInvalidValue;
   dim3 grid((m + kSignalsPerWG - 1) / kSignalsPerWG, split);
-  fh_scan<<<grid, 256, 0, st>>>(b.pu, b.pmh, b.pidx, n, chunk_batches, b.ssig, m, b.sbpos,
+  fh_scan<<<grid, 256, 0, st>>>(b.pu, b.pmh, b.pidx, n, b.ssig, m,
                                 b.seed, b.mag, b.bb, s.part);
   return hipGetLastError();
 }

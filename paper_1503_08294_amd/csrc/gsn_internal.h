@@ -211,8 +211,6 @@ hipError_t launch_find_merge(const DevState& s, int32_t m, const FindConfig& cfg
 
 // Spatial staging of the screened scans (staging.hip).
 constexpr int kBuckets = 32 * 32 * 32;
-// signals per work-group of the binary16 scan (its home chunk is found per such block)
-constexpr int kScanBlock = 256;
 
 struct StageBufs {
   float4* pu;       // [ceil64(n_max)] units in bucket order: (x, y, z, |w|^2); slots from n
@@ -223,8 +221,6 @@ struct StageBufs {
   int32_t* sperm;   // [m_max] original index of the signal at every sorted position
   float* seed;      // [m_max] seed bound B at every sorted position
   float* ssig;      // [3][m] the signals in sorted order (x, y, z rows of stride m)
-  int32_t* sbpos;   // [m_max / kScanBlock + 1] sorted unit position of the grid bin that
-                    // holds the middle signal of every block of kScanBlock sorted signals
   int32_t *hist_u, *off_u, *cur_u, *hist_s, *off_s, *cur_s;  // [kBuckets + 1] each; the
                     // signal histogram and cursors use two sets of kBuckets / 8 in hist_s, cur_s
   int32_t* acc;     // [16] bounding-box accumulators

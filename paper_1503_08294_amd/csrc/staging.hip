@@ -392,8 +392,7 @@ __device__ __forceinline__ void merge2(unsigned long long& a1, unsigned long lon
 // LDS itself, so the bins' offsets need no launch of their own; a signal's sorted position is
 // its bin's offset plus a ticket from the bin's cursor (atomics; the order inside a bin is
 // immaterial).  The signal's index and coordinates are written at that position (sperm,
-// ssig), and every block of kScanBlock sorted positions gets the unit position of its
-// middle bin (sbpos), so the scan's prologue reads its signals and its chunk order directly.
+// ssig), so the scan's prologue reads its signals directly.
 // Workgroup 0 also reduces the per-block unit magnitudes of this call.
 // kSeedLanes lanes per signal then scan a strided part of the kSeedWindow units around the
 // signal's unit bucket in the sorted order; the second smallest direct-form distance over
@@ -403,7 +402,7 @@ __global__ __launch_bounds__(kBlock) void st_place_seed(
     const int32_t* __restrict__ skey, const float* __restrict__ sig, int32_t m,
     const float4* __restrict__ pu, const int32_t* __restrict__ pidx, int32_t n,
     const int32_t* __restrict__ off_u, int32_t* __restrict__ sperm, float* __restrict__ seed,
-    float* __restrict__ ssig, int32_t* __restrict__ sbpos, const float* __restrict__ bmag,
+    float* __restrict__ ssig, const float* __restrict__ bmag,
     int32_t nmag, int32_t* __restrict__ mag) {
   static_assert(kBlock == 256 && kSignalBuckets % kBlock == 0, "four waves, whole bins");
   constexpr int per = kSignalBuckets / kBlock;
@@ -456,18 +455,6 @@ __global__ __launch_bounds__(kBlock) void st_place_seed(
   __syncthreads();
 
   const int32_t t = blockIdx.x * kBlock + tid;
-  // for every block of kScanBlock sorted signals: the sorted unit position of the bin that
-  // holds its middle signal (the last bin whose offset is at most that position), from which
-  // the scan orders its chunks
-  if (t < (m + kScanBlock - 1) / kScanBlock) {
-    const int32_t mid = min(t * kScanBlock + kScanBlock / 2, m - 1);
-    int32_t lo = 0, hi = kSignalBuckets;
-    while (lo < hi) {
-      const int32_t md = (lo + hi) >> 1;
-      if (soff[md] <= mid) lo = md + 1; else hi = md;
-    }
-    sbpos[t] = off_u[max(lo - 1, 0) << kSignalShift];
-  }
   const int32_t j = t / kSeedLanes;
   const int q = t % kSeedLanes;
   int32_t pos = -1;
@@ -603,7 +590,6 @@ size_t stage_bytes(int32_t n_max, int32_t m_max) {
   add(4 * mm);   // sperm
   add(4 * mm);   // seed
   add(12 * mm);  // ssig
-  add(4 * (mm / kScanBlock + 1));  // sbpos
   for (int i = 0; i < 6; ++i) add(hb);  // hist/off/cur for units and signals
   add(4 * 16);   // acc
   add(4 * 8);    // bb
@@ -633,7 +619,6 @@ StageBufs carve_stage(void* base, int32_t n_max, int32_t m_max) {
   s.sperm = reinterpret_cast<int32_t*>(take(4 * mm));
   s.seed = reinterpret_cast<float*>(take(4 * mm));
   s.ssig = reinterpret_cast<float*>(take(12 * mm));
-  s.sbpos = reinterpret_cast<int32_t*>(take(4 * (mm / kScanBlock + 1)));
   s.hist_u = reinterpret_cast<int32_t*>(take(hb));
   s.off_u = reinterpret_cast<int32_t*>(take(hb));
   s.cur_u = reinterpret_cast<int32_t*>(take(hb));
@@ -682,7 +667,7 @@ hipError_t launch_stage(const DevState& s, const StageBufs& b, int32_t n, const 
                                                  m, nb_g, b.bb, b.skey, hist, hist_next,
                                                  cur_next, b.bmag, layouts);
   st_place_seed<<<blocks(static_cast<int64_t>(m) * kSeedLanes), kBlock, 0, st>>>(
-      hist, cur, b.skey, sig, m, b.pu, b.pidx, n, b.off_u, b.sperm, b.seed, b.ssig, b.sbpos,
+      hist, cur, b.skey, sig, m, b.pu, b.pidx, n, b.off_u, b.sperm, b.seed, b.ssig,
       b.bmag, nb_g, b.mag);
   return hipGetLastError();
 }
