@@ -58,6 +58,7 @@ Layout layout_for(const gsn_params& p) {
   add(4 * mm);                 // 28 schedule d2
   add(mm);                     // 29 schedule acceptance
   add(8 * kA64Slots);          // 30 64-bit accumulators
+  add(4 * (mm / 32 + 2));      // 31 accepted signals per workgroup of the fused check
   L.total = (o + 255) & ~static_cast<size_t>(255);
   return L;
 }
@@ -96,6 +97,7 @@ void carve(const gsn_params& p, void* base, DevState* s) {
   s->sd2 = reinterpret_cast<float*>(b + L.off[28]);
   s->sacc = reinterpret_cast<uint8_t*>(b + L.off[29]);
   s->acc64 = reinterpret_cast<unsigned long long*>(b + L.off[30]);
+  s->apart = reinterpret_cast<int32_t*>(b + L.off[31]);
 }
 
 }  // namespace gsn

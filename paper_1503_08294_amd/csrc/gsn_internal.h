@@ -183,6 +183,8 @@ struct DevState {
   float *sd1, *sd2;                // [m_max]
   uint8_t* sacc;                   // [m_max]
   unsigned long long* acc64;       // [kA64Slots]   64-bit accumulators (Acc64Slot)
+  int32_t* apart;                  // [m_max / 32 + 2] accepted signals per workgroup of the
+                                   // fused check, added to acc64 by the next degree count
 };
 
 struct Layout {

@@ -515,13 +515,12 @@ __global__ __launch_bounds__(kBlock) void st_merge(const unsigned long long* __r
   // Rows may repeat a sentinel key (a chunk with fewer than two units under the seed bound
   // reports (B, sentinel)); real keys are unique.  insert() keeps the two smallest
   // distinct keys.
+  // (branch-free: a wave's lanes see different rows)
   auto insert = [&](unsigned long long k) {
-    if (k < a) {
-      b = a;
-      a = k;
-    } else if (k < b && k != a) {
-      b = k;
-    }
+    const bool lt1 = k < a;
+    const bool lt2 = k < b && k != a;
+    b = lt1 ? a : (lt2 ? k : b);
+    a = lt1 ? k : a;
   };
   // the output position first, then eight rows per step, all loaded before any is
   // inserted, so the loads overlap (64 rows, the usual count, take one step; rows beyond

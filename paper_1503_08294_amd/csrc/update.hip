@@ -15,11 +15,9 @@
 namespace gsn {
 namespace {
 
-// Position of neighbour v in the (ascending) row of u, or -1.
-__device__ __forceinline__ int32_t find_in_row(const int32_t* __restrict__ rp,
-                                               const int32_t* __restrict__ col, int32_t u,
-                                               int32_t v) {
-  int32_t lo = rp[u], hi = rp[u + 1];
+// Position of neighbour v in the ascending row col[lo, hi), or -1.
+__device__ __forceinline__ int32_t find_in_span(const int32_t* __restrict__ col, int32_t lo,
+                                                int32_t hi, int32_t v) {
   while (lo < hi) {
     const int32_t mid = (lo + hi) >> 1;
     const int32_t c = col[mid];
@@ -29,19 +27,29 @@ __device__ __forceinline__ int32_t find_in_row(const int32_t* __restrict__ rp,
   return -1;
 }
 
-// The same for rows of up to 8 entries (nearly all of them), read in one batch of loads.
-__device__ __forceinline__ int32_t find_in_short_row(const int32_t* __restrict__ rp,
-                                                     const int32_t* __restrict__ col,
-                                                     int32_t u, int32_t v) {
-  const int32_t r0 = rp[u], l = rp[u + 1] - r0;
-  if (l > 8) return find_in_row(rp, col, u, v);
+// Position of neighbour v in the row of u, or -1.
+__device__ __forceinline__ int32_t find_in_row(const int32_t* __restrict__ rp,
+                                               const int32_t* __restrict__ col, int32_t u,
+                                               int32_t v) {
+  return find_in_span(col, rp[u], rp[u + 1], v);
+}
+
+// The same for a row col[r0, r1) of up to 8 entries (nearly all of them), read in one batch
+// of loads.
+__device__ __forceinline__ int32_t find_in_short_span(const int32_t* __restrict__ col,
+                                                      int32_t r0, int32_t r1, int32_t v) {
+  const int32_t l = r1 - r0;
+  if (l > 8) return find_in_span(col, r0, r1, v);
+  if (l <= 0) return -1;
+  // every load in the row (slots past its end repeat the last entry), so none waits on a
+  // bounds test
   int32_t c[8];
 #pragma unroll
-  for (int k = 0; k < 8; ++k) c[k] = k < l ? col[r0 + k] : -1;
+  for (int k = 0; k < 8; ++k) c[k] = col[r0 + min(k, l - 1)];
   int32_t at = -1;
 #pragma unroll
   for (int k = 7; k >= 0; --k)
-    if (c[k] == v) at = r0 + k;
+    if (k < l && c[k] == v) at = r0 + k;
   return at;
 }
 
@@ -229,6 +237,7 @@ struct FusedArgs {
   int32_t* orphan;
   int32_t* status;
   int32_t max_age;
+  int32_t* apart;  // accepted signals of each workgroup (plain stores)
 };
 
 // The fused kernels give each signal a group of kGroup lanes of one wave: lane q takes the
@@ -272,6 +281,12 @@ __global__ void fu_claim(int32_t m, int32_t n, const int32_t* __restrict__ winne
 // max_age, marked dead on both half-edges, and a neighbour left without a live edge or a
 // requested one is flagged.  The lane of neighbour v alone writes the row of v, so its
 // orphan test sees that row complete.
+// What the update reads (the signal, the positions of b, s and the lane's first neighbour
+// v0, b's error, v0's edge age, row bounds and row) is loaded beside the check rather than
+// after it: a lock set that passes the check is its signal's alone, so no other thread of
+// this launch writes those words, and the check's own reads of lock words taken early
+// decide the same (another signal only ever clears a word holding its own key).  The
+// dependent loads then form a chain of five rounds instead of about nine.
 __global__ void fu_check_apply(FusedArgs a) {
   __shared__ int32_t s_acc;
   if (threadIdx.x == 0) s_acc = 0;
@@ -282,40 +297,81 @@ __global__ void fu_check_apply(FusedArgs a) {
   bool ok = false;
   if (j < a.m) {
     const int32_t b = a.winner[j], s = a.second[j];
+    const float dj = a.d1[j];
+    const float sx = a.sig[j], sy = a.sig[a.m + j], sz = a.sig[2 * a.m + j];
+    // the five loads above are issued together before any of them is waited for
+    __builtin_amdgcn_sched_barrier(0);
     if (pair_ok(b, s, a.n)) {
-      const unsigned long long key = signal_key(a.d1[j], j, a.key_mode);
+      const unsigned long long key = signal_key(dj, j, a.key_mode);
       const int32_t r0 = a.rp[b], r1 = a.rp[b + 1];
+      // lane 0: the lock words, positions and error of b and s
+      unsigned long long lb = 0, ls = 0;
+      float bx = 0.0f, by = 0.0f, bz = 0.0f, be = 0.0f, tx = 0.0f, ty = 0.0f, tz = 0.0f;
+      if (q == 0) {
+        lb = a.lock[b];
+        ls = a.lock[s];
+        bx = a.x[b]; by = a.y[b]; bz = a.z[b];
+        be = a.err[b];
+        tx = a.x[s]; ty = a.y[s]; tz = a.z[s];
+      }
+      // the lane's first neighbour (a row of up to kGroup entries gives each lane at most one)
+      const int32_t k0 = r0 + q;
+      const bool has0 = k0 < r1;
+      int32_t v0 = -1, g0 = 0, w0 = 0, w1 = 0;
+      unsigned long long l0 = 0;
+      float vx = 0.0f, vy = 0.0f, vz = 0.0f;
+      if (has0) {
+        v0 = a.col[k0];
+        g0 = a.age[k0];
+        l0 = a.lock[v0];
+        vx = a.x[v0]; vy = a.y[v0]; vz = a.z[v0];
+        w0 = a.rp[v0];
+        w1 = a.rp[v0 + 1];
+      }
+      const int32_t rk0 = has0 ? find_in_short_span(a.col, w0, w1, b) : -1;
       bool mine = true, is_s = false;
-      auto visit = [&](int32_t u) {
-        if (a.lock[u] == key) a.lock[u] = ~0ull; else mine = false;
+      auto visit = [&](int32_t u, unsigned long long word) {
+        if (word == key) a.lock[u] = ~0ull; else mine = false;
       };
-      for (int32_t k = r0 + q; k < r1; k += kGroup) {
+      if (has0) {
+        is_s |= v0 == s;
+        visit(v0, l0);
+      }
+      for (int32_t k = k0 + kGroup; k < r1; k += kGroup) {
         const int32_t v = a.col[k];
         is_s |= v == s;
-        visit(v);
+        visit(v, a.lock[v]);
       }
       const bool s_nb = group_bits(__ballot(is_s)) != 0;
       if (q == 0) {
-        visit(b);
-        if (!s_nb) visit(s);
+        visit(b, lb);
+        if (!s_nb) visit(s, ls);
       }
       ok = group_bits(__ballot(!mine)) == 0;
       if (ok) {
-        const float sx = a.sig[j], sy = a.sig[a.m + j], sz = a.sig[2 * a.m + j];
+        // move_unit's expression on positions already loaded
+        auto move = [&](int32_t u, float eps, float px, float py, float pz) {
+          float t;
+          t = sx - px; t = eps * t; a.x[u] = px + t;
+          t = sy - py; t = eps * t; a.y[u] = py + t;
+          t = sz - pz; t = eps * t; a.z[u] = pz + t;
+        };
         if (q == 0) {
-          move_unit(a.x, a.y, a.z, b, a.eps_b, sx, sy, sz);
+          move(b, a.eps_b, bx, by, bz);
           if (!s_nb) {
-            move_unit(a.x, a.y, a.z, s, a.eps_n, sx, sy, sz);
+            move(s, a.eps_n, tx, ty, tz);
             a.ins[b] = s;
             a.ins[s] = b;
           }
-          a.err[b] = a.err[b] + a.d1[j];
+          a.err[b] = be + dj;
         }
-        for (int32_t k = r0 + q; k < r1; k += kGroup) {
-          const int32_t v = a.col[k];
-          move_unit(a.x, a.y, a.z, v, a.eps_n, sx, sy, sz);
-          const int32_t g = v == s ? 0 : a.age[k] + 1;
-          const int32_t rk = find_in_short_row(a.rp, a.col, v, b);
+        for (int32_t k = k0; k < r1; k += kGroup) {
+          const bool first = k == k0;
+          const int32_t v = first ? v0 : a.col[k];
+          if (first) move(v, a.eps_n, vx, vy, vz);
+          else move(v, a.eps_n, a.x[v], a.y[v], a.z[v]);
+          const int32_t g = v == s ? 0 : (first ? g0 : a.age[k]) + 1;
+          const int32_t rk = first ? rk0 : find_in_row(a.rp, a.col, v, b);
           if (g <= a.max_age) {
             a.age[k] = g;
             if (rk >= 0) a.age[rk] = g;
@@ -336,16 +392,39 @@ __global__ void fu_check_apply(FusedArgs a) {
   }
   if (blockIdx.x == 0 && threadIdx.x == 0)
     atomicAdd(&a.acc64[kA64Resolved], static_cast<unsigned long long>(a.m));
-  block_count(ok && q == 0, &a.acc64[kA64Accepted], &s_acc);
+  // the workgroup's accepted count goes to its own word; the degree count that follows
+  // adds them with one atomic (hundreds of same-address atomics at the end of this launch
+  // would queue at the cache)
+  const unsigned long long acc_mask = __ballot(ok && q == 0);
+  if ((threadIdx.x & 63) == 0 && acc_mask != 0)
+    atomicAdd(&s_acc, static_cast<int32_t>(__popcll(acc_mask)));
+  __syncthreads();
+  if (threadIdx.x == 0) a.apart[blockIdx.x] = s_acc;
 }
 
 // New degree of every unit (live half-edges + a requested new edge) and per-block sums;
-// with err not null also the error decay of the fused iteration.
+// with err not null also the error decay of the fused iteration, and with apart not null
+// workgroup 0 adds the napart per-workgroup counts of the fused check to *acc.
 __global__ void ed_count(int32_t n, const int32_t* __restrict__ rp,
                          const int32_t* __restrict__ age, const int32_t* __restrict__ ins,
                          int32_t* __restrict__ cnt, int32_t* __restrict__ bsum,
-                         float* __restrict__ err, float beta) {
+                         float* __restrict__ err, float beta,
+                         const int32_t* __restrict__ apart, int32_t napart,
+                         unsigned long long* __restrict__ acc) {
   __shared__ int32_t red[kBlock];
+  if (apart != nullptr && blockIdx.x == 0) {
+    int32_t v = 0;
+    for (int32_t i = threadIdx.x; i < napart; i += kBlock) v += apart[i];
+    red[threadIdx.x] = v;
+    __syncthreads();
+    for (int w = kBlock / 2; w > 0; w >>= 1) {
+      if (threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+      __syncthreads();
+    }
+    if (threadIdx.x == 0 && red[0] != 0)
+      atomicAdd(acc, static_cast<unsigned long long>(red[0]));
+    __syncthreads();  // red[] is reused below
+  }
   const int32_t u = blockIdx.x * kBlock + threadIdx.x;
   int32_t c = 0;
   if (u < n) {
@@ -536,7 +615,7 @@ hipError_t launch_edges(const DevState& s, int cur, int32_t n, int32_t m,
   const int fold = nb > 0 && nb <= kFoldBlocks;
   if (n > 0)
     ed_count<<<nb, kBlock, 0, st>>>(n, s.rp[cur], s.age[cur], s.ins, s.cnt, s.bsum, nullptr,
-                                    1.0f);
+                                    1.0f, nullptr, 0, nullptr);
   if (!fold) scan_blocks<<<1, 1024, 0, st>>>(s.bsum, nb, half_cap, s.rp[nxt] + n, s.status, -1);
   if (n > 0)
     ed_write<<<nb, kBlock, 0, st>>>(n, s.rp[cur], s.col[cur], s.age[cur], s.ins, s.cnt,
@@ -559,14 +638,17 @@ hipError_t launch_iterate_set(const DevState& s, int cur, int32_t n, const float
     FusedArgs a{sig,      m,          n,          winner,  second,   d1,     key_mode,
                 s.rp[cur], s.col[cur], s.lock,     accepted, s.acc64, s.x,    s.y,
                 s.z,      s.err,      eps_b,      eps_n,   s.age[cur], s.ins, s.orphan,
-                s.status, max_age};
+                s.status, max_age, s.apart};
     fu_check_apply<<<gb, kBlock, 0, st>>>(a);
   }
   const int nb = blocks(n);
   const int fold = nb > 0 && nb <= kFoldBlocks;
+  // (with no units no signal is accepted, so skipping the count loses nothing)
   if (n > 0)
     ed_count<<<nb, kBlock, 0, st>>>(n, s.rp[cur], s.age[cur], s.ins, s.cnt, s.bsum, s.err,
-                                    beta);
+                                    beta, m > 0 ? s.apart : nullptr,
+                                    blocks(static_cast<int64_t>(m) * kGroup),
+                                    s.acc64 + kA64Accepted);
   if (!fold) scan_blocks<<<1, 1024, 0, st>>>(s.bsum, nb, half_cap, s.rp[nxt] + n, s.status, -1);
   if (n > 0)
     ed_write<<<nb, kBlock, 0, st>>>(n, s.rp[cur], s.col[cur], s.age[cur], s.ins, s.cnt,

@@ -63,13 +63,16 @@ __device__ bool row_insert(const int32_t* __restrict__ rp, int32_t* __restrict__
 __device__ __forceinline__ int32_t row_find(const int32_t* __restrict__ col, int32_t r0,
                                             int32_t l, int32_t v) {
   if (l > 8) return slice_find(col, r0, r0 + l, v);
+  if (l <= 0) return -1;
+  // every load in the row (slots past its end repeat the last entry), so none waits on a
+  // bounds test
   int32_t c[8];
 #pragma unroll
-  for (int k = 0; k < 8; ++k) c[k] = k < l ? col[r0 + k] : -1;
+  for (int k = 0; k < 8; ++k) c[k] = col[r0 + min(k, l - 1)];
   int32_t at = -1;
 #pragma unroll
   for (int k = 7; k >= 0; --k)
-    if (c[k] == v) at = r0 + k;
+    if (k < l && c[k] == v) at = r0 + k;
   return at;
 }
 

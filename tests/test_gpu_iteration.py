@@ -69,15 +69,23 @@ def test_fused_iteration_equals_the_four_calls(lock_mode):
     p = gsn.make_params(wl.eps_b, wl.eps_n, 2, wl.err_alpha, wl.err_beta, 1_700, 8_000, 1_024,
                         lock_mode, 0)
     a, b = gsn.Network(p, units), gsn.Network(p, units)
+    a.stat(gsn.GSN_STAT_CLEAR)
+    b.stat(gsn.GSN_STAT_CLEAR)
     stream = SignalStream(cloud, wl.signal_seed)
+    accepted = 0
     for t in range(1, 41):
         sig = torch.from_numpy(stream.next(1_024)).cuda()
         ra = [x.clone() for x in a.iterate(sig)]
         rb = [x.clone() for x in b.iterate_steps(sig)]
         for x, y in zip(ra, rb):
             assert torch.equal(x, y), f"iteration {t}"
+        accepted += int(ra[4].sum().item())
         a.grow(t, 10)
         b.grow(t, 10)
+    # the statistics count every resolved and accepted signal on both paths
+    for net in (a, b):
+        assert net.stat(gsn.GSN_STAT_RESOLVED) == 40 * 1_024
+        assert net.stat(gsn.GSN_STAT_ACCEPTED) == accepted
     sa, sb = a.export(), b.export()
     for k in ("xyz", "err", "edges"):
         assert torch.equal(sa[k], sb[k]), k
