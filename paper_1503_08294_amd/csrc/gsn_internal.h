@@ -104,10 +104,25 @@ __device__ __forceinline__ void fold_offsets(const int32_t* __restrict__ bsum, i
                                              int32_t* red, int32_t* before, int32_t* total) {
   int32_t a = 0, t = 0;
   const int32_t me = static_cast<int32_t>(blockIdx.x);
-  for (int32_t i = threadIdx.x; i < nb; i += blockDim.x) {
-    const int32_t v = bsum[i];
-    t += v;
-    a += i < me ? v : 0;
+  const int32_t bd = static_cast<int32_t>(blockDim.x), tid = static_cast<int32_t>(threadIdx.x);
+  if (nb > 0 && nb <= 8 * bd) {
+    // up to eight sums per thread in one batch of loads (indices past nb repeat the last)
+    int32_t v[8];
+#pragma unroll
+    for (int r = 0; r < 8; ++r) v[r] = bsum[min(tid + r * bd, nb - 1)];
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      const int32_t i = tid + r * bd;
+      const int32_t x = i < nb ? v[r] : 0;
+      t += x;
+      a += i < me ? x : 0;
+    }
+  } else {
+    for (int32_t i = tid; i < nb; i += bd) {
+      const int32_t v = bsum[i];
+      t += v;
+      a += i < me ? v : 0;
+    }
   }
   for (int o = 32; o > 0; o >>= 1) {
     a += __shfl_xor(a, o);

@@ -477,11 +477,26 @@ __global__ __launch_bounds__(kBlock) void st_place_seed(
     int32_t lo = (b0 + b1) / 2 - kSeedWindow / 2;
     lo = max(0, min(lo, n - kSeedWindow));
     const int32_t hi = min(n, lo + kSeedWindow);
-    for (int32_t r = lo + q; r < hi; r += kSeedLanes) {
-      const float4 wu = pu[r];
-      const float dx = sx - wu.x, dy = sy - wu.y, dz = sz - wu.z;
-      const unsigned long long key = pack((dx * dx + dy * dy) + dz * dz, pidx[r]);
-      merge2(k1, k2, key, ~0ull);
+    // the lane's kSeedWindow / kSeedLanes units in one batch of loads (indices past hi
+    // repeat the last unit and enter as the all-ones key, which changes nothing)
+    constexpr int kPer = kSeedWindow / kSeedLanes;
+    if (hi > lo) {
+      float4 wu[kPer];
+      int32_t wi[kPer];
+#pragma unroll
+      for (int i = 0; i < kPer; ++i) {
+        const int32_t r = min(lo + q + i * kSeedLanes, hi - 1);
+        wu[i] = pu[r];
+        wi[i] = pidx[r];
+      }
+#pragma unroll
+      for (int i = 0; i < kPer; ++i) {
+        const float dx = sx - wu[i].x, dy = sy - wu[i].y, dz = sz - wu[i].z;
+        const unsigned long long key = lo + q + i * kSeedLanes < hi
+                                           ? pack((dx * dx + dy * dy) + dz * dz, wi[i])
+                                           : ~0ull;
+        merge2(k1, k2, key, ~0ull);
+      }
     }
   }
 #pragma unroll

@@ -15,6 +15,9 @@
 namespace gsn {
 namespace {
 
+// Rows of up to this many entries (nearly all of them) are read in one batch of loads.
+constexpr int kShortRow = 8;
+
 // Position of neighbour v in the ascending row col[lo, hi), or -1.
 __device__ __forceinline__ int32_t find_in_span(const int32_t* __restrict__ col, int32_t lo,
                                                 int32_t hi, int32_t v) {
@@ -428,10 +431,21 @@ __global__ void ed_count(int32_t n, const int32_t* __restrict__ rp,
   const int32_t u = blockIdx.x * kBlock + threadIdx.x;
   int32_t c = 0;
   if (u < n) {
-    if (err) err[u] = err[u] * beta;
-    for (int32_t k = rp[u]; k < rp[u + 1]; ++k) c += age[k] != kDead;
+    const float e = err ? err[u] : 0.0f;  // loaded beside the row, stored after it
+    const int32_t r0 = rp[u], r1 = rp[u + 1], l = r1 - r0;
+    if (l > 0 && l <= kShortRow) {
+      // one batch of loads (slots past the row's end repeat its last entry)
+      int32_t g[kShortRow];
+#pragma unroll
+      for (int k = 0; k < kShortRow; ++k) g[k] = age[r0 + min(k, l - 1)];
+#pragma unroll
+      for (int k = 0; k < kShortRow; ++k) c += k < l && g[k] != kDead;
+    } else {
+      for (int32_t k = r0; k < r1; ++k) c += age[k] != kDead;
+    }
     c += ins[u] >= 0;
     cnt[u] = c;
+    if (err) err[u] = e * beta;
   }
   red[threadIdx.x] = c;
   __syncthreads();
@@ -528,9 +542,10 @@ __global__ void ed_write(int32_t n, const int32_t* __restrict__ rp,
   rp_new[u] = start;
   int32_t o = start;
   bool pending = extra >= 0;
-  for (int32_t k = rp[u]; k < rp[u + 1]; ++k) {
-    if (age[k] == kDead) continue;
-    const int32_t v = col[k];
+  // one live entry (v, g) in ascending order, with the requested neighbour placed before
+  // the first larger one
+  auto put = [&](int32_t v, int32_t g) {
+    if (g == kDead) return;
     if (pending && extra < v) {
       col_new[o] = extra;
       age_new[o] = 0;
@@ -538,8 +553,23 @@ __global__ void ed_write(int32_t n, const int32_t* __restrict__ rp,
       pending = false;
     }
     col_new[o] = v;
-    age_new[o] = age[k];
+    age_new[o] = g;
     ++o;
+  };
+  const int32_t r0 = rp[u], r1 = rp[u + 1], l = r1 - r0;
+  if (l > 0 && l <= kShortRow) {
+    // one batch of loads (slots past the row's end repeat its last entry)
+    int32_t cv[kShortRow], gv[kShortRow];
+#pragma unroll
+    for (int k = 0; k < kShortRow; ++k) {
+      cv[k] = col[r0 + min(k, l - 1)];
+      gv[k] = age[r0 + min(k, l - 1)];
+    }
+#pragma unroll
+    for (int k = 0; k < kShortRow; ++k)
+      if (k < l) put(cv[k], gv[k]);
+  } else {
+    for (int32_t k = r0; k < r1; ++k) put(col[k], age[k]);
   }
   if (pending) {
     col_new[o] = extra;
