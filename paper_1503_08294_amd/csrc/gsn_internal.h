@@ -64,22 +64,6 @@ __device__ __forceinline__ unsigned long long signal_key(float d1, int32_t j, in
   return (static_cast<unsigned long long>(__float_as_uint(d1)) << 32) | lo;
 }
 
-// Adds the lanes of this wave for which `pred` holds to *ctr with one atomic.
-__device__ __forceinline__ void wave_count(bool pred, int32_t* ctr) {
-  const unsigned long long mask = __ballot(pred);
-  if (mask == 0) return;
-  const int lane = static_cast<int>(threadIdx.x & 63);
-  if (lane == __ffsll(static_cast<long long>(mask)) - 1)
-    atomicAdd(ctr, static_cast<int32_t>(__popcll(mask)));
-}
-__device__ __forceinline__ void wave_count(bool pred, unsigned long long* ctr) {
-  const unsigned long long mask = __ballot(pred);
-  if (mask == 0) return;
-  const int lane = static_cast<int>(threadIdx.x & 63);
-  if (lane == __ffsll(static_cast<long long>(mask)) - 1)
-    atomicAdd(ctr, static_cast<unsigned long long>(__popcll(mask)));
-}
-
 // Adds the threads of this workgroup for which `pred` holds to *ctr with one atomic per
 // workgroup (same-address atomics from thousands of waves queue up at the cache).  Every
 // thread of the workgroup calls it (it holds a barrier); `acc` is an LDS word that was

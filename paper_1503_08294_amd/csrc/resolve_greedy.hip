@@ -99,7 +99,11 @@ __global__ void rg_claim(GreedyArgs a, int32_t t) {
 }
 
 __global__ void rg_check(GreedyArgs a, int32_t t) {
+  // (the same for every thread: the word was written by an earlier launch)
   if (t > 0 && a.rem[t - 1] < kTailMin) return;
+  __shared__ int32_t s_left;
+  if (threadIdx.x == 0) s_left = 0;
+  __syncthreads();
   const int32_t j = blockIdx.x * kRoundBlock + threadIdx.x;
   bool left = false;
   if (j < a.m && a.state[j] == 1) {
@@ -107,7 +111,7 @@ __global__ void rg_check(GreedyArgs a, int32_t t) {
     a.state[j] = st;
     left = st == 1;
   }
-  wave_count(left, &a.rem[t]);
+  block_count(left, &a.rem[t], &s_left);
 }
 
 // The remaining rounds in one workgroup, then the acceptance flags of all signals (and
@@ -148,11 +152,23 @@ __global__ __launch_bounds__(kTailBlock) void rg_tail(GreedyArgs a, uint8_t* acc
     cur = nxt;
     nxt = t;
   }
+  // the counts with one atomic each (hundreds of same-address atomics would queue at the
+  // cache)
+  __shared__ int32_t s_acc;
+  if (tid == 0) s_acc = 0;
+  __syncthreads();
+  int32_t mine = 0;
   for (int32_t j = tid; j < a.m; j += kTailBlock) {
     const bool acc = a.state[j] == 2;
     accepted[j] = acc ? 1 : 0;
-    wave_count(true, &a.acc64[kA64Resolved]);
-    wave_count(acc, &a.acc64[kA64Accepted]);
+    mine += acc;
+  }
+  for (int o = 32; o > 0; o >>= 1) mine += __shfl_xor(mine, o);
+  if ((tid & 63) == 0 && mine != 0) atomicAdd(&s_acc, mine);
+  __syncthreads();
+  if (tid == 0) {
+    atomicAdd(&a.acc64[kA64Resolved], static_cast<unsigned long long>(a.m));
+    if (s_acc != 0) atomicAdd(&a.acc64[kA64Accepted], static_cast<unsigned long long>(s_acc));
   }
 }
 

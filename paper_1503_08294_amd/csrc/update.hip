@@ -92,6 +92,9 @@ __global__ void rs_check(int32_t m, int32_t n, const int32_t* __restrict__ winne
                          unsigned long long* __restrict__ lock,
                          uint8_t* __restrict__ accepted, int winner_only, int key_mode,
                          unsigned long long* __restrict__ acc64) {
+  __shared__ int32_t s_acc;
+  if (threadIdx.x == 0) s_acc = 0;
+  __syncthreads();
   const int32_t j = blockIdx.x * kBlock + threadIdx.x;
   bool ok = false;
   if (j < m) {
@@ -115,8 +118,9 @@ __global__ void rs_check(int32_t m, int32_t n, const int32_t* __restrict__ winne
     }
     accepted[j] = ok ? 1 : 0;
   }
-  wave_count(j < m, &acc64[kA64Resolved]);
-  wave_count(ok, &acc64[kA64Accepted]);
+  if (blockIdx.x == 0 && threadIdx.x == 0)
+    atomicAdd(&acc64[kA64Resolved], static_cast<unsigned long long>(m));
+  block_count(ok, &acc64[kA64Accepted], &s_acc);
 }
 
 // -------------------------------------------------------------------- adapt ----

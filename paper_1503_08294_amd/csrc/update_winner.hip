@@ -102,6 +102,9 @@ __global__ void wl_prepare(int32_t m, int32_t n, const int32_t* __restrict__ win
                            unsigned long long* __restrict__ lock, uint8_t* __restrict__ pend,
                            int32_t* __restrict__ extra, int32_t* __restrict__ rem,
                            int32_t* __restrict__ status) {
+  __shared__ int32_t s_ok;
+  if (threadIdx.x == 0) s_ok = 0;
+  __syncthreads();
   const int32_t j = blockIdx.x * kBlock + threadIdx.x;
   if (j == 0) rem[0] = 0;
   bool ok = false;
@@ -120,7 +123,7 @@ __global__ void wl_prepare(int32_t m, int32_t n, const int32_t* __restrict__ win
       for (int32_t k = rp[b]; k < rp[b + 1]; ++k) atomicMin(&lock[col[k]], key);
     }
   }
-  wave_count(ok, &rem[kRmSurvivors]);
+  block_count(ok, &rem[kRmSurvivors], &s_ok);
 }
 
 // Row sizes for a rewrite: the live length (len, or the CSR row length when len is null)
