@@ -18,6 +18,34 @@ namespace {
 // Rows of up to this many entries (nearly all of them) are read in one batch of loads.
 constexpr int kShortRow = 8;
 
+// Sum of v over a kBlock workgroup, valid in every thread: wave shuffles, then the wave
+// totals through LDS (wt holds kBlock / 64 words; one barrier before it may be reused).
+__device__ __forceinline__ int32_t block_sum(int32_t v, int32_t* wt) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  if ((threadIdx.x & 63) == 0) wt[threadIdx.x >> 6] = v;
+  __syncthreads();
+  int32_t t = 0;
+#pragma unroll
+  for (int w = 0; w < kBlock / 64; ++w) t += wt[w];
+  return t;
+}
+
+// Inclusive prefix sum of v over a kBlock workgroup in thread order: a shuffle scan per
+// wave, then the totals of the earlier waves through LDS (one barrier).
+__device__ __forceinline__ int32_t block_inclusive_scan(int32_t v, int32_t* wt) {
+  const int lane = static_cast<int>(threadIdx.x & 63), w = static_cast<int>(threadIdx.x >> 6);
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int32_t x = __shfl_up(v, o);
+    if (lane >= o) v += x;
+  }
+  if (lane == 63) wt[w] = v;
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < kBlock / 64; ++k) v += k < w ? wt[k] : 0;
+  return v;
+}
+
 // Position of neighbour v in the ascending row col[lo, hi), or -1.
 __device__ __forceinline__ int32_t find_in_span(const int32_t* __restrict__ col, int32_t lo,
                                                 int32_t hi, int32_t v) {
@@ -418,19 +446,12 @@ __global__ void ed_count(int32_t n, const int32_t* __restrict__ rp,
                          float* __restrict__ err, float beta,
                          const int32_t* __restrict__ apart, int32_t napart,
                          unsigned long long* __restrict__ acc) {
-  __shared__ int32_t red[kBlock];
+  __shared__ int32_t wt[2][kBlock / 64];
   if (apart != nullptr && blockIdx.x == 0) {
     int32_t v = 0;
     for (int32_t i = threadIdx.x; i < napart; i += kBlock) v += apart[i];
-    red[threadIdx.x] = v;
-    __syncthreads();
-    for (int w = kBlock / 2; w > 0; w >>= 1) {
-      if (threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
-      __syncthreads();
-    }
-    if (threadIdx.x == 0 && red[0] != 0)
-      atomicAdd(acc, static_cast<unsigned long long>(red[0]));
-    __syncthreads();  // red[] is reused below
+    v = block_sum(v, wt[0]);
+    if (threadIdx.x == 0 && v != 0) atomicAdd(acc, static_cast<unsigned long long>(v));
   }
   const int32_t u = blockIdx.x * kBlock + threadIdx.x;
   int32_t c = 0;
@@ -451,13 +472,8 @@ __global__ void ed_count(int32_t n, const int32_t* __restrict__ rp,
     cnt[u] = c;
     if (err) err[u] = e * beta;
   }
-  red[threadIdx.x] = c;
-  __syncthreads();
-  for (int w = kBlock / 2; w > 0; w >>= 1) {
-    if (threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
-    __syncthreads();
-  }
-  if (threadIdx.x == 0) bsum[blockIdx.x] = red[0];
+  c = block_sum(c, wt[1]);
+  if (threadIdx.x == 0) bsum[blockIdx.x] = c;
 }
 
 // Exclusive scan of the per-block sums in one workgroup; bsum[nb] receives the total.
@@ -513,7 +529,7 @@ __global__ void ed_write(int32_t n, const int32_t* __restrict__ rp,
                          int32_t* __restrict__ col_new, int32_t* __restrict__ age_new,
                          int32_t* __restrict__ status, int fold, int32_t nb, int64_t cap,
                          int32_t* __restrict__ out_total) {
-  __shared__ int32_t sc[kBlock];
+  __shared__ int32_t wt[kBlock / 64];
   __shared__ int32_t red[2 * kBlock / 64];
   const int32_t u = blockIdx.x * kBlock + threadIdx.x;
   const int32_t c = u < n ? cnt[u] : 0;
@@ -526,16 +542,9 @@ __global__ void ed_write(int32_t n, const int32_t* __restrict__ rp,
     boff = bsum[blockIdx.x];
     abort = status[kStAbort];
   }
-  sc[threadIdx.x] = c;
-  __syncthreads();
-  for (int off = 1; off < kBlock; off <<= 1) {
-    const int32_t v = threadIdx.x >= off ? sc[threadIdx.x - off] : 0;
-    __syncthreads();
-    sc[threadIdx.x] += v;
-    __syncthreads();
-  }
+  const int32_t inc = block_inclusive_scan(c, wt);
   if (u >= n) return;
-  const int32_t start = boff + sc[threadIdx.x] - c;
+  const int32_t start = boff + inc - c;
   const int32_t extra = ins[u];
   ins[u] = -1;
   if (abort) {
