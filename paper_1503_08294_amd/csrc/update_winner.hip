@@ -360,24 +360,48 @@ __device__ __forceinline__ uint32_t group_bits(unsigned long long wave_mask) {
 
 __device__ bool group_try_apply(const RoundArgs& a, int32_t j, int q) {
   const int32_t b = a.winner[j], s = a.second[j];
-  const unsigned long long key = signal_key(a.d1[j], j, a.key_mode);
-  // the row bounds of b are read with its lock word: they are used only if j holds b, and
-  // then nobody else edits that row during the round
+  const float dj = a.d1[j];
+  const int32_t m = a.m;
+  const float sx = a.sig[j], sy = a.sig[m + j], sz = a.sig[2 * m + j];
+  // the loads above are issued together before any of them is waited for
+  __builtin_amdgcn_sched_barrier(0);
+  const unsigned long long key = signal_key(dj, j, a.key_mode);
+  // The row bounds of b are read with its lock word, and what the step reads (positions,
+  // error, row bounds of the neighbours) beside the lock words rather than after them:
+  // they are used only if j holds F_j, and then nobody else edits those units or rows
+  // during the round; otherwise they are dropped.
   const int32_t r0 = a.rp[b], l = a.len[b];
-  if (lock_read(&a.lock[b]) != key) return false;
+  const unsigned long long lb = lock_read(&a.lock[b]);
+  unsigned long long ls = 0;
+  int32_t r1b = 0;
+  float bx = 0.0f, by = 0.0f, bz = 0.0f, be = 0.0f, tx = 0.0f, ty = 0.0f, tz = 0.0f;
+  if (q == 0) {
+    ls = lock_read(&a.lock[s]);
+    r1b = a.rp[b + 1];
+    bx = a.x[b]; by = a.y[b]; bz = a.z[b];
+    be = a.err[b];
+    tx = a.x[s]; ty = a.y[s]; tz = a.z[s];
+  }
+  if (lb != key) return false;
   if (l > kGroup) {
     int applied = 0;
     if (q == 0) applied = try_apply(a, j);
     return __shfl(applied, static_cast<int>(threadIdx.x & 63) & ~(kGroup - 1)) != 0;
   }
   const bool has = q < l;
-  int32_t v = -1, a_old = 0;
+  int32_t v = -1, a_old = 0, vr = 0, vl = 0;
+  unsigned long long lv = key;
+  float vx = 0.0f, vy = 0.0f, vz = 0.0f;
   if (has) {
     v = a.col[r0 + q];
     a_old = a.age[r0 + q];
+    lv = lock_read(&a.lock[v]);
+    vx = a.x[v]; vy = a.y[v]; vz = a.z[v];
+    vr = a.rp[v];
+    vl = a.len[v];
   }
-  bool mine = !has || lock_read(&a.lock[v]) == key;
-  if (q == 0) mine = mine && lock_read(&a.lock[s]) == key;
+  bool mine = lv == key;
+  if (q == 0) mine = mine && ls == key;
   if (group_bits(__ballot(!mine)) != 0) return false;
   // j holds F_j: release it, then the step
   if (has) lock_release(&a.lock[v]);
@@ -385,19 +409,24 @@ __device__ bool group_try_apply(const RoundArgs& a, int32_t j, int q) {
     lock_release(&a.lock[b]);
     lock_release(&a.lock[s]);
   }
-  const int32_t m = a.m;
-  const float sx = a.sig[j], sy = a.sig[m + j], sz = a.sig[2 * m + j];
+  // move_unit's expression on positions already loaded
+  auto move = [&](int32_t u, float eps, float px, float py, float pz) {
+    float t;
+    t = sx - px; t = eps * t; a.x[u] = px + t;
+    t = sy - py; t = eps * t; a.y[u] = py + t;
+    t = sz - pz; t = eps * t; a.z[u] = pz + t;
+  };
   const bool is_s = has && v == s;
   const bool new_s = group_bits(__ballot(is_s)) == 0;
   if (q == 0) {
-    move_unit(a.x, a.y, a.z, b, a.eps_b, sx, sy, sz);
-    if (new_s) move_unit(a.x, a.y, a.z, s, a.eps_n, sx, sy, sz);
+    move(b, a.eps_b, bx, by, bz);
+    if (new_s) move(s, a.eps_n, tx, ty, tz);
   }
-  if (has) move_unit(a.x, a.y, a.z, v, a.eps_n, sx, sy, sz);
+  if (has) move(v, a.eps_n, vx, vy, vz);
   const int32_t g = is_s ? 0 : a_old + 1;
   const bool keep = has && g <= a.max_age;
   if (keep) {
-    const int32_t rk = row_find(a.col, a.rp[v], a.len[v], b);
+    const int32_t rk = row_find(a.col, vr, vl, b);
     if (rk >= 0) a.age[rk] = g;
   } else if (has) {
     if (row_remove(a.rp, a.len, a.col, a.age, v, b) == 0 && !a.orphan[v]) {
@@ -409,7 +438,8 @@ __device__ bool group_try_apply(const RoundArgs& a, int32_t j, int q) {
   const uint32_t kept_mask = group_bits(__ballot(keep));
   const uint32_t below_s = group_bits(__ballot(keep && v < s));
   const int32_t kept = __popc(kept_mask);
-  const bool ins = new_s && kept + 1 <= a.rp[b + 1] - r0;
+  const int32_t room = __shfl(r1b, static_cast<int>(threadIdx.x & 63) & ~(kGroup - 1)) - r0;
+  const bool ins = new_s && kept + 1 <= room;
   if (keep) {
     const int32_t pos = __popc(kept_mask & ((1u << q) - 1)) + (ins && s < v ? 1 : 0);
     a.col[r0 + pos] = v;
@@ -424,7 +454,7 @@ __device__ bool group_try_apply(const RoundArgs& a, int32_t j, int q) {
     if (new_s && (!ins || !row_insert(a.rp, a.len, a.col, a.age, s, b, 0)))
       raise_error(a.status, GSN_E_CAPACITY);
     a.len[b] = kept + (ins ? 1 : 0);
-    a.err[b] = a.err[b] + a.d1[j];
+    a.err[b] = be + dj;
   }
   return true;
 }
