@@ -42,16 +42,32 @@ struct GreedyArgs {
   unsigned long long* acc64;
 };
 
+// Rows of up to this many entries (nearly all of them) are read in one batch of loads
+// (indices past the row's end repeat its last entry and are ignored).
+constexpr int kShortRow = 8;
+
 __device__ void g_claim(const GreedyArgs& a, int32_t j) {
   const int32_t b = a.winner[j], s = a.second[j];
   const unsigned long long key = signal_key(a.d1[j], j, a.key_mode);
   atomicMin(&a.lock[b], key);
   atomicMin(&a.lock[s], key);
-  for (int32_t k = a.rp[b]; k < a.rp[b + 1]; ++k) atomicMin(&a.lock[a.col[k]], key);
+  const int32_t r0 = a.rp[b], r1 = a.rp[b + 1], l = r1 - r0;
+  if (l > kShortRow) {
+    for (int32_t k = r0; k < r1; ++k) atomicMin(&a.lock[a.col[k]], key);
+  } else if (l > 0) {
+    int32_t c[kShortRow];
+#pragma unroll
+    for (int k = 0; k < kShortRow; ++k) c[k] = a.col[r0 + min(k, l - 1)];
+#pragma unroll
+    for (int k = 0; k < kShortRow; ++k)
+      if (k < l) atomicMin(&a.lock[c[k]], key);
+  }
 }
-
-// Visits every unit of L_j once (s skipped when it is a neighbour of b), releases the ones
-// j holds, and settles j: 0 rejected, 2 accepted (its units marked taken), 1 pending.
+// Visits b, its neighbours and s (once, when it is no neighbour): a unit taken by an
+// accepted signal blocks j for good; j holds the units whose lock word has its key and
+// releases them.  For a short row the lock and taken words of all of them are read in one
+// round (the units are distinct, another signal only ever clears a word holding its own key,
+// and a taken mark seen a round later only delays the same rejection).
 __device__ uint8_t g_check(const GreedyArgs& a, int32_t j) {
   const int32_t b = a.winner[j], s = a.second[j];
   const unsigned long long key = signal_key(a.d1[j], j, a.key_mode);
@@ -60,19 +76,47 @@ __device__ uint8_t g_check(const GreedyArgs& a, int32_t j) {
     blocked |= a.taken[u] != 0;
     if (lock_read(&a.lock[u]) == key) lock_release(&a.lock[u]); else holds = false;
   };
-  visit(b);
-  bool s_nb = false;
-  for (int32_t k = a.rp[b]; k < a.rp[b + 1]; ++k) {
-    const int32_t v = a.col[k];
-    s_nb |= v == s;
-    visit(v);
+  const int32_t r0 = a.rp[b], r1 = a.rp[b + 1], l = r1 - r0;
+  if (l > kShortRow || l <= 0) {
+    visit(b);
+    bool s_nb = false;
+    for (int32_t k = r0; k < r1; ++k) {
+      const int32_t v = a.col[k];
+      s_nb |= v == s;
+      visit(v);
+    }
+    if (!s_nb) visit(s);
+  } else {
+    int32_t c[kShortRow];
+#pragma unroll
+    for (int k = 0; k < kShortRow; ++k) c[k] = a.col[r0 + min(k, l - 1)];
+    bool s_nb = false;
+#pragma unroll
+    for (int k = 0; k < kShortRow; ++k) s_nb |= k < l && c[k] == s;
+    const bool tb = a.taken[b] != 0, ts = a.taken[s] != 0;
+    const unsigned long long lb = lock_read(&a.lock[b]), ls = lock_read(&a.lock[s]);
+    bool tk[kShortRow];
+    unsigned long long lk[kShortRow];
+#pragma unroll
+    for (int k = 0; k < kShortRow; ++k) {
+      tk[k] = a.taken[c[k]] != 0;
+      lk[k] = lock_read(&a.lock[c[k]]);
+    }
+    auto decide = [&](int32_t u, bool t, unsigned long long w) {
+      blocked |= t;
+      if (w == key) lock_release(&a.lock[u]); else holds = false;
+    };
+    decide(b, tb, lb);
+#pragma unroll
+    for (int k = 0; k < kShortRow; ++k)
+      if (k < l) decide(c[k], tk[k], lk[k]);
+    if (!s_nb) decide(s, ts, ls);
   }
-  if (!s_nb) visit(s);
   if (blocked) return 0;
   if (!holds) return 1;
   a.taken[b] = 1;
   a.taken[s] = 1;
-  for (int32_t k = a.rp[b]; k < a.rp[b + 1]; ++k) a.taken[a.col[k]] = 1;
+  for (int32_t k = r0; k < r1; ++k) a.taken[a.col[k]] = 1;
   return 2;
 }
 
