@@ -120,7 +120,18 @@ __global__ void wl_prepare(int32_t m, int32_t n, const int32_t* __restrict__ win
       const unsigned long long key = signal_key(d1[j], j, key_mode);
       atomicMin(&lock[b], key);
       atomicMin(&lock[s], key);
-      for (int32_t k = rp[b]; k < rp[b + 1]; ++k) atomicMin(&lock[col[k]], key);
+      const int32_t r0 = rp[b], l = rp[b + 1] - r0;
+      if (l > 8) {
+        for (int32_t k = r0; k < r0 + l; ++k) atomicMin(&lock[col[k]], key);
+      } else if (l > 0) {
+        // a short row in one batch of loads (slots past its end repeat the last entry)
+        int32_t c[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) c[k] = col[r0 + min(k, l - 1)];
+#pragma unroll
+        for (int k = 0; k < 8; ++k)
+          if (k < l) atomicMin(&lock[c[k]], key);
+      }
     }
   }
   block_count(ok, &rem[kRmSurvivors], &s_ok);
@@ -254,8 +265,18 @@ __device__ void claim(const RoundArgs& a, int32_t j) {
   const unsigned long long key = signal_key(a.d1[j], j, a.key_mode);
   atomicMin(&a.lock[b], key);
   atomicMin(&a.lock[s], key);
-  const int32_t r0 = a.rp[b], r1 = r0 + a.len[b];
-  for (int32_t k = r0; k < r1; ++k) atomicMin(&a.lock[a.col[k]], key);
+  const int32_t r0 = a.rp[b], l = a.len[b];
+  if (l > 8) {
+    for (int32_t k = r0; k < r0 + l; ++k) atomicMin(&a.lock[a.col[k]], key);
+  } else if (l > 0) {
+    // a short row in one batch of loads (slots past its end repeat the last entry)
+    int32_t c[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) c[k] = a.col[r0 + min(k, l - 1)];
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+      if (k < l) atomicMin(&a.lock[c[k]], key);
+  }
 }
 
 __device__ void apply(const RoundArgs& a, int32_t j);
