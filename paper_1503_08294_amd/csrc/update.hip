@@ -103,7 +103,18 @@ __global__ void rs_claim(int32_t m, int32_t n, const int32_t* __restrict__ winne
   atomicMin(&lock[b], key);
   if (winner_only) return;
   atomicMin(&lock[s], key);
-  for (int32_t k = rp[b]; k < rp[b + 1]; ++k) atomicMin(&lock[col[k]], key);
+  const int32_t r0 = rp[b], l = rp[b + 1] - r0;
+  if (l > kShortRow) {
+    for (int32_t k = r0; k < r0 + l; ++k) atomicMin(&lock[col[k]], key);
+  } else if (l > 0) {
+    // one batch of loads (slots past the row's end repeat its last entry)
+    int32_t c[kShortRow];
+#pragma unroll
+    for (int k = 0; k < kShortRow; ++k) c[k] = col[r0 + min(k, l - 1)];
+#pragma unroll
+    for (int k = 0; k < kShortRow; ++k)
+      if (k < l) atomicMin(&lock[c[k]], key);
+  }
 }
 
 // With the winner alone locked, the survivor also releases its lock (the other claimants
@@ -213,7 +224,7 @@ __device__ __forceinline__ void mark_signal(int32_t b, int32_t s,
       found = true;
     }
     age[k] = a;
-    const int32_t rk = find_in_row(rp, col, v, b);
+    const int32_t rk = find_in_short_span(col, rp[v], rp[v + 1], b);
     if (rk >= 0) age[rk] = a;
   }
   if (!found) {
