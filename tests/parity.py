@@ -1,9 +1,10 @@
 """Helpers that run the HIP path (through the C ABI binding) and the CPU oracle side by
 side on the same seeded inputs and compare them element by element.
 
-Bar: winner, second, acceptance and edge lists bit-exact; d1, d2 bit-exact (same binary32
-expression on both sides); positions within 1e-6 max abs (bit-exact expected: the update
-expressions are the same operations in the same order); errors likewise.
+Bar: winner, second, d1, d2, acceptance, edge lists, positions and errors all bit-exact:
+both sides evaluate the same binary32 expressions in the same order (no contraction), so
+no tolerance is needed.  The looser bar of positions within 1e-6 after a run is implied
+and reported separately by ``max_position_error``.
 """
 from __future__ import annotations
 
@@ -53,8 +54,11 @@ class Pair:
         o = self.orc.find_winners(sig)
         return g, o
 
-    def iterate(self, sig: np.ndarray, it=0, insert_every=0, grow=False):
-        g = [t.cpu().numpy() for t in self.net.iterate(self.to_dev(sig))]
+    def iterate(self, sig: np.ndarray, it=0, insert_every=0, grow=False, calls="fused"):
+        """One iteration on both sides; calls="fused" runs gsn_iterate, calls="steps" the
+        four separate calls (find, resolve, adapt, update_edges)."""
+        run = self.net.iterate if calls == "fused" else self.net.iterate_steps
+        g = [t.cpu().numpy() for t in run(self.to_dev(sig))]
         if grow:
             self.net.grow(it, insert_every)
         o = self.orc.iterate(sig, it, insert_every, grow)
@@ -65,11 +69,15 @@ class Pair:
         os_ = self.orc.export()
         assert self.net.sizes() == tuple(int(v) for v in self.orc.sizes()), where
         np.testing.assert_array_equal(gs["edges"].numpy(), os_["edges"], err_msg=where)
-        np.testing.assert_allclose(gs["xyz"].numpy(), os_["xyz"], rtol=0, atol=POS_TOL,
-                                   err_msg=where)
-        np.testing.assert_allclose(gs["err"].numpy(), os_["err"], rtol=1e-6, atol=1e-12,
-                                   err_msg=where)
+        np.testing.assert_array_equal(gs["xyz"].numpy(), os_["xyz"], err_msg=where)
+        np.testing.assert_array_equal(gs["err"].numpy(), os_["err"], err_msg=where)
         return gs, os_
+
+    def max_position_error(self) -> float:
+        """Largest absolute position difference between the two sides."""
+        gx = self.net.export()["xyz"].numpy().astype(np.float64)
+        ox = self.orc.export()["xyz"].astype(np.float64)
+        return float(np.abs(gx - ox).max()) if gx.size else 0.0
 
 
 def assert_find_equal(g, o, where=""):
@@ -85,7 +93,7 @@ def assert_iter_equal(g, o, where=""):
 
 
 def run_workload(name, iterations=None, compare_every=1, n_points=None, m=None,
-                 n_units=None, **over):
+                 n_units=None, calls="fused", **over):
     from paper_1503_08294_amd.clouds import WORKLOADS, SignalStream
     wl = WORKLOADS[name]
     cloud = wl.make_cloud(n_points)
@@ -102,10 +110,11 @@ def run_workload(name, iterations=None, compare_every=1, n_points=None, m=None,
     rejected = 0
     for t in range(1, its + 1):
         sig = stream.next(m)
-        g, o = pair.iterate(sig, t, wl.insert_every, wl.grow)
+        g, o = pair.iterate(sig, t, wl.insert_every, wl.grow, calls)
         assert_iter_equal(g, o, f"{name} iteration {t}")
         rejected += int(m - o[4].sum())
         if t % compare_every == 0 or t == its:
             pair.compare_state(f"{name} iteration {t}")
     assert pair.net.check() == 0
+    assert pair.max_position_error() <= POS_TOL
     return pair, rejected / (its * m)
