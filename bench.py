@@ -21,15 +21,27 @@ Prints one JSON line:
                    cores' executed rate (32 flops per pair: 32x32x16 products, K = 16) and
                    the algorithmic rate against the fp32 peak; HBM traffic per launch from
                    rocprofv3 counters when a summary for the current kernel source exists
+  late_window      the same step timed over iterations 81-100 of the workload's stated
+                   100-iteration run (a network that has grown its edges), with the edge
+                   counts at both ends of the window
   cpu_baseline     the CPU oracle timed on this host's cores on the first iterations of the
-                   same workload
+                   same workload (its find-winners loop on 16 threads); beside it
+                   ``single_core``: the oracle per phase on one pinned core
+
+--sweep prints one JSON line per (collision rule, m) for the sweep workload (100,000 units
+on the noisy torus, m in {1, 64, 1,024, 16,384, 65,536}, 10 warm-up + 50 timed
+iterations): throughput, conflict rate and, for the winner lock, the birthday estimate of
+the conflict rate that the implicit lock on the winner implies for uniformly hit winners.
 """
 from __future__ import annotations
 
 import argparse
 import hashlib
 import json
+import math
 import os
+import shutil
+import subprocess
 import sys
 import time
 
@@ -68,34 +80,136 @@ def load_traffic(launch_evals: int):
     return t.get("bytes_per_launch")
 
 
-def cpu_baseline(wl, units, cloud, budget_s: float, lock_mode: int = 0, key_mode: int = 0):
+def host_info() -> dict:
+    """CPU model and core counts of this host (the oracle's timing context)."""
+    model = None
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=20).stdout
+        for line in out.splitlines():
+            if line.lower().startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except (OSError, subprocess.SubprocessError):
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        usable = os.cpu_count()
+    return {"cpu_model": model, "logical_cpus": os.cpu_count(), "usable_cpus": usable}
+
+
+def oracle_threads() -> int:
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        usable = os.cpu_count() or 1
+    return max(1, min(16, usable))
+
+
+def oracle_phases_child(args):
+    """Child-process mode (no GPU, no torch): the oracle on ONE core, pinned, timed per
+    phase over the first iterations of a workload, for each m in args.phase_m; prints one
+    JSON object."""
+    import numpy as np
+    import oracle
+    from paper_1503_08294_amd.clouds import WORKLOADS, SignalStream
+    wl = WORKLOADS[args.workload]
+    cloud = wl.make_cloud()
+    units = wl.make_units(cloud)
+    out = {"cpu": sorted(os.sched_getaffinity(0)), "threads": 1, "runs": []}
+    for m in [int(v) for v in args.phase_m.split(",")]:
+        cap = wl.capacity(m)
+        p = oracle.Params(wl.eps_b, wl.eps_n, wl.max_age, wl.err_alpha, wl.err_beta,
+                          cap["n_max"], cap["e_max"], m, lock_mode=args.phase_lock)
+        o = oracle.Oracle(p, units, threads=1)
+        stream = SignalStream(cloud, wl.signal_seed)
+        t = {"find": 0.0, "resolve": 0.0, "adapt": 0.0, "edges": 0.0}
+        done = 0
+        while done < args.phase_iters:
+            sig = stream.next(m)
+            t0 = time.perf_counter()
+            w, sc, d1, _ = o.find_winners(sig)
+            t1 = time.perf_counter()
+            acc = o.resolve_conflicts(w, sc, d1)
+            t2 = time.perf_counter()
+            o.adapt(sig, w, sc, d1, acc)
+            t3 = time.perf_counter()
+            o.update_edges(w, sc, acc)
+            t4 = time.perf_counter()
+            t["find"] += t1 - t0
+            t["resolve"] += t2 - t1
+            t["adapt"] += t3 - t2
+            t["edges"] += t4 - t3
+            done += 1
+            if sum(t.values()) > args.phase_budget:
+                break
+        total = sum(t.values())
+        n = units.shape[1]
+        out["runs"].append({"m": m, "iterations": done,
+                            "phase_ms": {k: 1e3 * v / done for k, v in t.items()},
+                            "fw_evals_per_s": m * n * done / t["find"],
+                            "signals_per_s": m * done / total,
+                            "evals_per_s": m * n * done / total})
+    print(json.dumps(out), flush=True)
+
+
+def single_core_oracle(workload: str, ms, iters: int, budget_s: float, lock_mode: int = 0):
+    """Runs oracle_phases_child in a child process pinned to one core with taskset.  Call
+    it before this process touches the GPU."""
+    try:
+        cpus = sorted(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        cpus = [0]
+    cpu = cpus[-1]
+    cmd = [sys.executable, os.path.abspath(__file__), "--oracle-phases",
+           "--workload", workload, "--phase-m", ",".join(str(v) for v in ms),
+           "--phase-iters", str(iters), "--phase-budget", str(budget_s),
+           "--phase-lock", str(lock_mode)]
+    if shutil.which("taskset"):
+        cmd = ["taskset", "-c", str(cpu)] + cmd
+    env = dict(os.environ, OMP_NUM_THREADS="1")
+    r = subprocess.run(cmd, capture_output=True, text=True, env=env,
+                       timeout=120 + 3 * budget_s * len(ms))
+    if r.returncode != 0:
+        print(r.stderr[-2000:], file=sys.stderr, flush=True)
+        return {"error": f"oracle child exited with {r.returncode}"}
+    res = json.loads(r.stdout.strip().splitlines()[-1])
+    res["pinned_with"] = "taskset -c %d" % cpu if cmd[0] == "taskset" else "sched_setaffinity"
+    return res
+
+
+def cpu_baseline(wl, units, cloud, budget_s: float, lock_mode: int = 0, key_mode: int = 0,
+                 m: int | None = None, max_iters: int = 200):
     """The oracle on the same initial units and the same seeded signal batches as the GPU
     run, whole iterations until about budget_s seconds have passed (at most 200)."""
     import oracle
     from paper_1503_08294_amd.clouds import SignalStream
-    threads = max(1, min(16, os.cpu_count() or 1))
-    cap = wl.capacity()
+    m = m or wl.m
+    threads = oracle_threads()
+    cap = wl.capacity(m)
     p = oracle.Params(wl.eps_b, wl.eps_n, wl.max_age, wl.err_alpha, wl.err_beta,
-                      cap["n_max"], cap["e_max"], cap["m_max"], lock_mode=lock_mode,
+                      cap["n_max"], cap["e_max"], m, lock_mode=lock_mode,
                       key_mode=key_mode)
     o = oracle.Oracle(p, units, threads=threads)
     stream = SignalStream(cloud, wl.signal_seed)
-    batches = [stream.next(wl.m) for _ in range(3)]
     dt = 0.0
     done = 0
-    while done < 200 and dt < budget_s:
-        sig = batches[done] if done < len(batches) else stream.next(wl.m)
+    accepted = 0
+    while done < max_iters and (done == 0 or dt < budget_s):
+        sig = stream.next(m)
         t0 = time.perf_counter()
-        o.iterate(sig)
+        acc = o.iterate(sig)[4]
         if wl.grow:
             o.grow(done + 1, wl.insert_every)
         dt += time.perf_counter() - t0
+        accepted += int(acc.sum())
         done += 1
-    evals = wl.m * units.shape[1] * done
+    evals = m * units.shape[1] * done
     return {"value": evals / dt, "unit": "evals/s", "cores": threads, "kind": "oracle",
-            "signals_per_s": wl.m * done / dt,
+            "signals_per_s": m * done / dt, "accepted_per_s": accepted / dt,
             "sample": f"first {done} whole iterations of {wl.name} (N={units.shape[1]}, "
-                      f"m={wl.m}), oracle find-winners on {threads} threads",
+                      f"m={m}), oracle find-winners loop on {threads} threads, the rest "
+                      "of the iteration sequential",
             "seconds": dt}
 
 
@@ -173,7 +287,7 @@ def run_schedule_bench(args):
         import oracle
         print(f"[bench] cpu baseline (first {SCHEDULE_CPU_SIGNALS} signals)", file=sys.stderr,
               flush=True)
-        threads = max(1, min(16, os.cpu_count() or 1))
+        threads = oracle_threads()
         o = oracle.Oracle(oracle.Params(wl.eps_b, wl.eps_n, wl.max_age, wl.err_alpha,
                                         wl.err_beta, n_max, 4 * n_max + 16,
                                         SCHEDULE["m_cap"], lock_mode=lock_mode,
@@ -204,6 +318,149 @@ def copy_calibration(nbytes: int, reps: int):
     print(json.dumps({"copy_calibration_bytes": nbytes, "reps": reps}), flush=True)
 
 
+
+SCREEN = "f16-split MFMA screen, exact f32 direct-form recheck"
+DTYPE = "f16-split MFMA screen + f32 recheck"
+LATE_WINDOW = (81, 100)      # iterations timed on the grown network (stated run: 100)
+
+
+def lock_modes(gsn, args):
+    lock_mode = {"set": gsn.GSN_LOCK_SET, "winner": gsn.GSN_LOCK_WINNER,
+                 "greedy": gsn.GSN_LOCK_SET_GREEDY}[args.lock]
+    key_mode = gsn.GSN_KEY_INDEX if args.key == "index" else gsn.GSN_KEY_DIST_INDEX
+    return lock_mode, key_mode
+
+
+def timed_steps(torch, gsn, net, step, first, count, scan_only=True):
+    """Runs steps first .. first+count-1 between two synchronizations.  With scan_only the
+    scan's HIP event pair is the only timer inside the window, else every phase timer
+    records.  Returns the elapsed seconds, {timer: (mean ms per launch, launches)}, and
+    the resolved and accepted signal counts."""
+    for w in range(gsn.GSN_T_COUNT):
+        gsn.gsn_timing_read(net.h, w)
+    gsn.gsn_timing_select(net.h, (1 << gsn.GSN_T_FIND_SCAN) if scan_only
+                          else (1 << gsn.GSN_T_COUNT) - 1)
+    torch.cuda.synchronize()
+    net.stat(gsn.GSN_STAT_CLEAR)
+    gsn.gsn_timing_enable(net.h, True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for t in range(first, first + count):
+        step(t)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    gsn.gsn_timing_enable(net.h, False)
+    timers = {}
+    for w in range(gsn.GSN_T_COUNT):
+        ms, launches = gsn.gsn_timing_read(net.h, w)
+        timers[w] = (ms / max(launches, 1), launches)
+    resolved = net.stat(gsn.GSN_STAT_RESOLVED)
+    accepted = net.stat(gsn.GSN_STAT_ACCEPTED)
+    if net.check() != 0:
+        raise SystemExit(f"device status {net.check()} after steps {first}..{first + count}")
+    return elapsed, timers, resolved, accepted
+
+
+def scan_roofline(m, n, scan_ms, launches, traffic):
+    scan_s = max(scan_ms, 1e-9) * 1e-3
+    achieved = FLOPS_PER_EVAL * m * n / scan_s / 1e12
+    return {"bound": "mfma", "kernel": SCAN_KERNEL, "dtype": "f16",
+            "achieved": achieved, "peak": F16_PEAK_TFLOPS, "unit": "TFLOP/s",
+            "frac": achieved / F16_PEAK_TFLOPS, "traffic": traffic,
+            "flops_per_launch": FLOPS_PER_EVAL * m * n,
+            "avg_launch_ms": scan_ms, "launches_timed": launches,
+            "executed_mfma_tflops": EXECUTED_FLOPS_PER_PAIR * m * n / scan_s / 1e12,
+            "executed_mfma_frac": EXECUTED_FLOPS_PER_PAIR * m * n / scan_s / 1e12
+                                  / F16_PEAK_TFLOPS,
+            "algorithmic_rate_vs_fp32_peak": achieved / FP32_PEAK_TFLOPS}
+
+
+def birthday_conflict_rate(n: int, m: int) -> float:
+    """Expected discarded fraction when m signals hit N equally likely winners and one
+    survives per winner: 1 - (N/m)(1 - (1 - 1/N)^m) ~ 1 - (N/m)(1 - e^(-m/N))."""
+    return 1.0 - (n / m) * (1.0 - math.exp(m * math.log1p(-1.0 / n)))
+
+
+def run_sweep(args):
+    """The sweep workload: for each collision rule and each m, a fresh network of 100,000
+    units, 10 warm-up and 50 timed iterations; one JSON line per record."""
+    import numpy as np
+
+    from paper_1503_08294_amd.clouds import WORKLOADS, SignalStream
+
+    wl = WORKLOADS["torus_sweep"]
+    ms = [int(v) for v in args.sweep_m.split(",")] if args.sweep_m else list(wl.sweep_m)
+    locks = args.sweep_locks.split(",")
+    single = None
+    if args.cpu_budget > 0:
+        # before this process touches the GPU: a pinned child process, one core
+        print("[bench] single-core oracle per phase (pinned)", file=sys.stderr, flush=True)
+        single = single_core_oracle(wl.name, ms, 5, min(args.cpu_budget, 6.0))
+
+    import torch
+
+    from paper_1503_08294_amd import gsn
+
+    print(f"[bench] generating {wl.name}: {wl.n_points} cloud points, N={wl.n_units}",
+          file=sys.stderr, flush=True)
+    cloud = wl.make_cloud()
+    units = wl.make_units(cloud)
+    n = units.shape[1]
+    torch.cuda.set_device(0)
+    host = host_info()
+    warm, steps = 10, 50
+    for lock in locks:
+        args.lock = lock
+        lock_mode, key_mode = lock_modes(gsn, args)
+        for m in ms:
+            print(f"[bench] sweep lock={lock} m={m}", file=sys.stderr, flush=True)
+            stream = SignalStream(cloud, wl.signal_seed)
+            dev_sig = torch.from_numpy(np.stack([stream.next(m)
+                                                 for _ in range(warm + steps)])).cuda()
+            cap = wl.capacity(m)
+            params = gsn.make_params(wl.eps_b, wl.eps_n, wl.max_age, wl.err_alpha,
+                                     wl.err_beta, cap["n_max"], cap["e_max"], m, lock_mode,
+                                     key_mode)
+            net = gsn.Network(params, torch.from_numpy(units).cuda())
+
+            def step(t):
+                net.iterate(dev_sig[t])
+
+            for t in range(warm):
+                step(t)
+            el, timers, resolved, accepted = timed_steps(torch, gsn, net, step, warm, steps)
+            scan_ms, launches = timers[gsn.GSN_T_FIND_SCAN]
+            rec = {
+                "metric": "sweep: signals/s and conflict rate vs m at 1 GPU",
+                "value": m * steps / el, "unit": "signals/s", "n_gpus": 1,
+                "steps": steps, "warmup": warm, "ms_per_step": 1e3 * el / steps,
+                "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+                "dtype": DTYPE, "data": "synthetic",
+                "config": {"workload": wl.name, "n_units": n, "m_signals": m,
+                           "cloud_points": wl.n_points, "cloud": "noisy torus",
+                           "collision": {"lock": lock, "key": args.key},
+                           "screen": SCREEN, "parallelism": "single"},
+                "evals_per_s": m * n * steps / el,
+                "accepted_per_s": accepted / el,
+                "conflict_rate": 1.0 - accepted / max(resolved, 1),
+                "roofline": scan_roofline(m, n, scan_ms, launches, None),
+                "state_after": dict(zip(("units", "edges"), net.sizes())),
+            }
+            if lock_mode == gsn.GSN_LOCK_WINNER:
+                rec["birthday_conflict_rate"] = birthday_conflict_rate(n, m)
+            if args.cpu_budget > 0:
+                rec["cpu_baseline"] = cpu_baseline(wl, units, cloud, min(args.cpu_budget, 3.0),
+                                                   lock_mode, key_mode, m=m, max_iters=60)
+                rec["cpu_baseline"]["host"] = host
+                if single and lock == "set":
+                    rec["cpu_baseline"]["single_core"] = dict(
+                        next((r for r in single.get("runs", []) if r["m"] == m), {}),
+                        pinned_with=single.get("pinned_with"))
+            net.close()
+            del net, dev_sig
+            print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -230,7 +487,24 @@ def main():
                     help="instead of fixed-size steps, time one growing-network run "
                          "(gsn_run_schedule) from two units to the quantization-error "
                          "threshold on the genus-3 cloud")
+    ap.add_argument("--sweep", action="store_true",
+                    help="the sweep workload: one JSON line per collision rule and m")
+    ap.add_argument("--sweep-m", default="", help="with --sweep: comma-separated m values")
+    ap.add_argument("--sweep-locks", default="set,winner",
+                    help="with --sweep: comma-separated collision rules")
+    ap.add_argument("--no-late-window", action="store_true",
+                    help="skip the record of iterations 81-100")
+    # child-process mode of the single-core oracle timing (no GPU)
+    ap.add_argument("--oracle-phases", action="store_true", help=argparse.SUPPRESS)
+    ap.add_argument("--phase-m", default="", help=argparse.SUPPRESS)
+    ap.add_argument("--phase-iters", type=int, default=2, help=argparse.SUPPRESS)
+    ap.add_argument("--phase-budget", type=float, default=10.0, help=argparse.SUPPRESS)
+    ap.add_argument("--phase-lock", type=int, default=0, help=argparse.SUPPRESS)
     args = ap.parse_args()
+
+    if args.oracle_phases:
+        oracle_phases_child(args)
+        return
 
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported "
@@ -246,31 +520,48 @@ def main():
         run_schedule_bench(args)
         return
 
-    import numpy as np
-    import torch
+    if args.sweep:
+        run_sweep(args)
+        return
 
-    from paper_1503_08294_amd import gsn
+    import numpy as np
+
     from paper_1503_08294_amd.clouds import WORKLOADS, SignalStream
 
     wl = WORKLOADS[args.workload]
+    single = None
+    if args.cpu_budget > 0:
+        # before this process touches the GPU: a pinned child process, one core
+        print("[bench] single-core oracle per phase (pinned)", file=sys.stderr, flush=True)
+        single = single_core_oracle(wl.name, [wl.m], 3, min(args.cpu_budget, 8.0))
+
+    import torch
+
+    from paper_1503_08294_amd import gsn
+
     print(f"[bench] generating {wl.name}: {wl.n_points} cloud points, N={wl.n_units}, "
           f"m={wl.m}", file=sys.stderr, flush=True)
     cloud = wl.make_cloud()
     units = wl.make_units(cloud)
     stream = SignalStream(cloud, wl.signal_seed)
-    # the timed steps, then a few more with every phase timer on, then one for the
-    # conflict rate
-    phase_steps = min(args.steps, 20)
-    total = args.warmup + args.steps + phase_steps + 1
-    host_sig = np.stack([stream.next(wl.m) for _ in range(total)])      # (T, 3, m)
     n, m = units.shape[1], wl.m
+    # the timed steps, a few more with every phase timer on, one for the conflict rate at
+    # their end, then (untimed) up to the late window of the stated run
+    phase_steps = min(args.steps, 20)
+    t_phase = args.warmup + args.steps
+    t_last = t_phase + phase_steps
+    late = None if args.no_late_window or args.grid_cell > 0 or wl.grow else LATE_WINDOW
+    total = t_last + 1
+    if late and total < late[0] - 1:
+        total = late[1]
+    else:
+        late = None          # the timed steps already reach past the window's start
+    host_sig = np.stack([stream.next(m) for _ in range(total)])      # (T, 3, m)
 
     torch.cuda.set_device(0)
     dev_sig = torch.from_numpy(host_sig).cuda()
     cap = wl.capacity()
-    lock_mode = {"set": gsn.GSN_LOCK_SET, "winner": gsn.GSN_LOCK_WINNER,
-                 "greedy": gsn.GSN_LOCK_SET_GREEDY}[args.lock]
-    key_mode = gsn.GSN_KEY_INDEX if args.key == "index" else gsn.GSN_KEY_DIST_INDEX
+    lock_mode, key_mode = lock_modes(gsn, args)
     params = gsn.make_params(wl.eps_b, wl.eps_n, wl.max_age, wl.err_alpha, wl.err_beta,
                              cap["n_max"], cap["e_max"], cap["m_max"], lock_mode, key_mode)
     net = gsn.Network(params, torch.from_numpy(units).cuda())
@@ -298,52 +589,30 @@ def main():
     for t in range(args.warmup):
         step(t)
     torch.cuda.synchronize()
-    for w in range(gsn.GSN_T_COUNT):
-        gsn.gsn_timing_read(net.h, w)
+    edges_before = net.sizes()[1]
+
     # inside the timed steps only the scan kernel carries an event pair (its average launch
     # duration is the roofline's denominator); each further event pair costs the stream a
     # few microseconds, so the per-phase times come from the steps after them
-    gsn.gsn_timing_select(net.h, 1 << gsn.GSN_T_FIND_SCAN)
-    gsn.gsn_timing_enable(net.h, True)
-
     print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
-    torch.cuda.synchronize()
-    net.stat(gsn.GSN_STAT_CLEAR)
-    t0 = time.perf_counter()
-    for t in range(args.warmup, args.warmup + args.steps):
-        step(t)
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    gsn.gsn_timing_enable(net.h, False)
-    scan_ms_sum, scan_launches = gsn.gsn_timing_read(net.h, gsn.GSN_T_FIND_SCAN)
-    scan_ms = scan_ms_sum / max(scan_launches, 1)
-    resolved = net.stat(gsn.GSN_STAT_RESOLVED)
-    accepted_timed = net.stat(gsn.GSN_STAT_ACCEPTED)
+    elapsed, timers, resolved, accepted_timed = timed_steps(torch, gsn, net, step,
+                                                            args.warmup, args.steps)
+    scan_ms, scan_launches = timers[gsn.GSN_T_FIND_SCAN]
     updates = net.stat(gsn.GSN_STAT_UPDATES)
     rounds = ({"mean": net.stat(gsn.GSN_STAT_ROUNDS) / updates,
                "max": net.stat(gsn.GSN_STAT_ROUNDS_MAX)} if updates else None)
-    if net.check() != 0:
-        raise SystemExit(f"device status {net.check()} after the timed steps")
+    edges_after = net.sizes()[1]
 
     print(f"[bench] phase timers over {phase_steps} more steps", file=sys.stderr, flush=True)
-    gsn.gsn_timing_select(net.h, (1 << gsn.GSN_T_COUNT) - 1)
-    gsn.gsn_timing_enable(net.h, True)
-    t_phase = args.warmup + args.steps
-    for t in range(t_phase, t_phase + phase_steps):
-        step(t)
-    torch.cuda.synchronize()
-    gsn.gsn_timing_enable(net.h, False)
+    _, ptimers, _, _ = timed_steps(torch, gsn, net, step, t_phase, phase_steps,
+                                   scan_only=False)
     phase = {}
     for name, w in (("find_scan", gsn.GSN_T_FIND_SCAN), ("find", gsn.GSN_T_FIND),
                     ("resolve", gsn.GSN_T_RESOLVE), ("adapt", gsn.GSN_T_ADAPT),
                     ("edges", gsn.GSN_T_EDGES), ("update_fused", gsn.GSN_T_UPDATE)):
-        ms, cnt = gsn.gsn_timing_read(net.h, w)
-        phase[name] = ms / max(cnt, 1)
-    if net.check() != 0:
-        raise SystemExit(f"device status {net.check()} after the phase steps")
+        phase[name] = ptimers[w][0] if ptimers[w][1] else 0.0
 
     # one more untimed iteration to report the conflict rate at this state
-    t_last = t_phase + phase_steps
     index_stats = None
     if grid is not None:
         # the index against the exhaustive search on this state and batch
@@ -355,6 +624,7 @@ def main():
                        "second_differs": float((gs_ != es).float().mean().item()),
                        "d1_excess_mean": float((gd1 - ed1).double().mean().item()),
                        "exhaustive_find_ms_same_state": None}
+        gsn.gsn_timing_select(net.h, (1 << gsn.GSN_T_COUNT) - 1)
         gsn.gsn_timing_enable(net.h, True)
         for _ in range(10):
             net.find_winners(dev_sig[t_last])
@@ -369,12 +639,28 @@ def main():
         acc = net.buf.accepted[:m]
     else:
         acc = net.iterate(dev_sig[t_last])[4]
-    conflict_rate = 1.0 - float(acc.sum().item()) / m
+    conflict_at_end = 1.0 - float(acc.sum().item()) / m
     n_units, n_edges = net.sizes()
 
+    late_rec = None
+    if late:
+        # continue the stated run (untimed) to the window, then time it
+        for t in range(t_last + 1, late[0] - 1):
+            step(t)
+        torch.cuda.synchronize()
+        e0 = net.sizes()[1]
+        count = late[1] - late[0] + 1
+        print(f"[bench] late window: iterations {late[0]}-{late[1]}", file=sys.stderr,
+              flush=True)
+        el, lt, res_l, acc_l = timed_steps(torch, gsn, net, step, late[0] - 1, count)
+        late_rec = {"iterations": list(late), "ms_per_step": 1e3 * el / count,
+                    "evals_per_s": m * n * count / el, "signals_per_s": m * count / el,
+                    "accepted_per_s": acc_l / el,
+                    "conflict_rate": 1.0 - acc_l / max(res_l, 1),
+                    "scan_avg_launch_ms": lt[gsn.GSN_T_FIND_SCAN][0],
+                    "edges_at_start": e0, "edges_at_end": net.sizes()[1]}
+
     ms_per_step = 1e3 * elapsed / args.steps
-    scan_s = max(scan_ms, 1e-9) * 1e-3
-    achieved = FLOPS_PER_EVAL * m * n / scan_s / 1e12
     traffic = load_traffic(m * n)
     out = {
         "metric": METRIC,
@@ -387,7 +673,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": DTYPE,
         "data": "synthetic",
         "config": {"workload": wl.name, "n_units": n, "m_signals": m,
                    "cloud_points": wl.n_points, "cloud": "genus-3 tube surface",
@@ -395,29 +681,25 @@ def main():
                    "find": ("exhaustive" if grid is None else
                             f"hash index, cubes of side {args.grid_cell}" +
                             (", certified exact" if args.grid_exact else "")),
+                   "screen": SCREEN if grid is None else None,
+                   "timed_iterations": [args.warmup + 1, args.warmup + args.steps],
                    "collision": {"lock": args.lock, "key": args.key}},
         "signals_per_s": m * args.steps / elapsed,
         "accepted_per_s": accepted_timed / elapsed,
         "accepted_fraction": accepted_timed / max(resolved, 1),
+        "conflict_rate": 1.0 - accepted_timed / max(resolved, 1),
+        "conflict_rate_at_end": conflict_at_end,
+        "edges_timed": [edges_before, edges_after],
         "fw_evals_per_s": m * n / (phase["find"] * 1e-3),
-        "fw_frac_fp32_peak": FLOPS_PER_EVAL * m * n / (phase["find"] * 1e-3) / 1e12
-                             / FP32_PEAK_TFLOPS,
+        "fw_algorithmic_rate_vs_fp32_peak": FLOPS_PER_EVAL * m * n / (phase["find"] * 1e-3)
+                                            / 1e12 / FP32_PEAK_TFLOPS,
         "phase_ms": phase,
         "phase_steps": phase_steps,
-        "conflict_rate": conflict_rate,
         "state_after": {"units": n_units, "edges": n_edges},
+        "late_window": late_rec,
         "update_rounds": rounds,
         "index": index_stats,
-        "roofline": {"bound": "mfma", "kernel": SCAN_KERNEL, "dtype": "f16",
-                     "achieved": achieved, "peak": F16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / F16_PEAK_TFLOPS, "traffic": traffic,
-                     "flops_per_launch": FLOPS_PER_EVAL * m * n,
-                     "avg_launch_ms": scan_ms,
-                     "launches_timed": scan_launches,
-                     "executed_mfma_tflops": EXECUTED_FLOPS_PER_PAIR * m * n / scan_s / 1e12,
-                     "executed_mfma_frac": EXECUTED_FLOPS_PER_PAIR * m * n / scan_s / 1e12
-                                           / F16_PEAK_TFLOPS,
-                     "achieved_vs_fp32_peak": achieved / FP32_PEAK_TFLOPS},
+        "roofline": scan_roofline(m, n, scan_ms, scan_launches, traffic),
         "cpu_baseline": None,
     }
     if grid is not None:
@@ -426,6 +708,11 @@ def main():
         print(f"[bench] cpu baseline (~{args.cpu_budget:.0f} s)", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(wl, units, cloud, args.cpu_budget, lock_mode,
                                            key_mode)
+        out["cpu_baseline"]["host"] = host_info()
+        if single is not None:
+            run = next((r for r in single.get("runs", []) if r["m"] == m), {})
+            out["cpu_baseline"]["single_core"] = dict(run, pinned_with=single.get("pinned_with"),
+                                                      kind="oracle", threads=1)
     print(json.dumps(out), flush=True)
 
 
