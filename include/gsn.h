@@ -150,6 +150,24 @@ int gsn_find_winners_grid(gsn_net* net, const gsn_grid* grid, void* grid_ws,
                           size_t grid_ws_bytes, const float* sig, int32_t m, int32_t* winner,
                           int32_t* second, float* d1, float* d2, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): gsn_find_winners_grid with its grid
+ * workspace taken from a fixed device array inside the library instead of grid_ws.  The
+ * array is GSN_NOALLOC_SCRATCH_BYTES bytes on every GPU the library runs on and is held
+ * from the library's load until the process ends; its device address is looked up once
+ * per GPU (at gsn_create, else at the first call).  This call allocates nothing (no
+ * hipMalloc, no event) and records no timing.  GSN_E_CAPACITY if
+ * gsn_grid_workspace_bytes(grid, n_max, m_max) exceeds GSN_NOALLOC_SCRATCH_BYTES, with
+ * nothing enqueued; GSN_E_HIP if the array's address cannot be found.  Every call on one
+ * GPU, from any handle, uses the same array and leaves its last contents there (each call
+ * clears what it needs on the stream): calls that overlap on one GPU (different streams or
+ * host threads without ordering between them) race and give undefined results.  Arguments,
+ * outputs, order rules and errors otherwise as gsn_find_winners_grid.  Async. */
+#define GSN_NOALLOC_SCRATCH_BYTES (32u << 20)
+int gsn_find_winners_grid_noalloc(gsn_net* net, const gsn_grid* grid, const float* sig,
+                                  int32_t m, int32_t* winner, int32_t* second, float* d1,
+                                  float* d2, void* stream);
+
 /* Collision handling (Sec. 2.2: signals whose updates would move the same unit, change
  * the same neighbourhood or add the same edge collide; an implicit lock lets one of them
  * take effect and discards the others).  With GSN_LOCK_SET (and _GREEDY), signal j locks

@@ -6,10 +6,39 @@
 #include <string.h>
 
 #include <cmath>
+#include <mutex>
 #include <new>
 #include <vector>
 
 #include "gsn_internal.h"
+
+// The grid workspace of gsn_find_winners_grid_noalloc, for callers that cannot allocate:
+// one fixed array per GPU, held from the library's load until the process ends.  In host
+// code the name only stands for the symbol; its device address on each GPU comes from
+// hipGetSymbolAddress (noalloc_scratch below), and only that address is used.
+static __device__ __align__(256) unsigned char scratch[GSN_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices] = {};
+
+// Device address of `scratch` on the current device, looked up once per device with that
+// device current; nullptr if the lookup fails.
+void* noalloc_scratch() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess) return nullptr;
+    g_scratch_dev[dev] = ptr;
+  }
+  return g_scratch_dev[dev];
+}
+
+}  // namespace
 
 namespace gsn {
 
@@ -126,6 +155,7 @@ struct gsn_net {
   int grid_rounds;             // grid-wide rounds of the winner-lock update (0: automatic)
   int32_t* feedback;           // pinned host word: the last update's grid rounds used
   int32_t* feedback_dev;       // its device address, stored by the update's last kernel
+  void* scratch_dev;           // device address of the no-allocation grid workspace
   std::vector<hipEvent_t> pool;
   std::vector<std::pair<hipEvent_t, hipEvent_t>> rec[GSN_T_COUNT];
 };
@@ -312,6 +342,9 @@ int gsn_create(const gsn_params* params, void* workspace, size_t workspace_bytes
   }
   *net->feedback = kDefaultGridRounds - 1;
   net->feedback_dev = nullptr;
+  // set-up of the no-allocation entry point on this device (null if the lookup failed;
+  // that entry point then tries once more and reports GSN_E_HIP)
+  net->scratch_dev = noalloc_scratch();
   if (hipHostGetDevicePointer(reinterpret_cast<void**>(&net->feedback_dev), net->feedback, 0) !=
       hipSuccess) {
     gsn_destroy(net);
@@ -416,9 +449,13 @@ size_t gsn_grid_workspace_bytes(const gsn_grid* grid, int32_t n_max, int32_t m_m
   return gsn::grid_bytes(cells, n_max, m_max);
 }
 
-int gsn_find_winners_grid(gsn_net* net, const gsn_grid* grid, void* grid_ws,
-                          size_t grid_ws_bytes, const float* sig, int32_t m, int32_t* winner,
-                          int32_t* second, float* d1, float* d2, void* stream) {
+}  // extern "C"
+
+namespace {
+
+int find_grid_impl(gsn_net* net, const gsn_grid* grid, void* grid_ws, size_t grid_ws_bytes,
+                   const float* sig, int32_t m, int32_t* winner, int32_t* second, float* d1,
+                   float* d2, void* stream, bool timed) {
   if (!net || m < 0 || m > net->p.m_max) return GSN_E_INVAL;
   if (net->phase != kReady && net->phase != kFound) return GSN_E_STATE;
   int64_t cells = 0;
@@ -439,11 +476,41 @@ int gsn_find_winners_grid(gsn_net* net, const gsn_grid* grid, void* grid_ws,
   spec.cells = cells;
   spec.exact = grid->exact;
   const gsn::GridBufs gb = gsn::carve_grid(grid_ws, cells, net->p.n_max, net->p.m_max);
-  TimedRegion t(net, GSN_T_FIND, st);
-  hipError_t e = gsn::launch_find_grid(net->s, gb, spec, net->n, sig, m, winner, second, d1,
-                                       d2, st);
-  t.end();
+  hipError_t e;
+  if (timed) {
+    TimedRegion t(net, GSN_T_FIND, st);
+    e = gsn::launch_find_grid(net->s, gb, spec, net->n, sig, m, winner, second, d1, d2, st);
+    t.end();
+  } else {
+    e = gsn::launch_find_grid(net->s, gb, spec, net->n, sig, m, winner, second, d1, d2, st);
+  }
   return hip_ok(e);
+}
+
+}  // namespace
+
+extern "C" {
+
+int gsn_find_winners_grid(gsn_net* net, const gsn_grid* grid, void* grid_ws,
+                          size_t grid_ws_bytes, const float* sig, int32_t m, int32_t* winner,
+                          int32_t* second, float* d1, float* d2, void* stream) {
+  return find_grid_impl(net, grid, grid_ws, grid_ws_bytes, sig, m, winner, second, d1, d2,
+                        stream, true);
+}
+
+int gsn_find_winners_grid_noalloc(gsn_net* net, const gsn_grid* grid, const float* sig,
+                                  int32_t m, int32_t* winner, int32_t* second, float* d1,
+                                  float* d2, void* stream) {
+  if (!net) return GSN_E_INVAL;
+  int64_t cells = 0;
+  if (!grid_ok(grid, &cells)) return GSN_E_INVAL;
+  if (gsn::grid_bytes(cells, net->p.n_max, net->p.m_max) > GSN_NOALLOC_SCRATCH_BYTES)
+    return GSN_E_CAPACITY;
+  if (!net->scratch_dev) net->scratch_dev = noalloc_scratch();
+  if (!net->scratch_dev) return GSN_E_HIP;
+  // no event timing here: a first event record would create (allocate) an event
+  return find_grid_impl(net, grid, net->scratch_dev, GSN_NOALLOC_SCRATCH_BYTES, sig, m, winner,
+                        second, d1, d2, stream, false);
 }
 
 int gsn_resolve_conflicts(gsn_net* net, int32_t m, const int32_t* winner,

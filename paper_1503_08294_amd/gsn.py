@@ -44,6 +44,8 @@ GSN_LOCK_SET_GREEDY = 2
 GSN_KEY_DIST_INDEX = 0
 GSN_KEY_INDEX = 1
 
+GSN_NOALLOC_SCRATCH_BYTES = 32 << 20
+
 GSN_STAT_ROUNDS = 0
 GSN_STAT_ROUNDS_MAX = 1
 GSN_STAT_UPDATES = 2
@@ -123,6 +125,8 @@ _sig = {
     "gsn_grid_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(gsn_grid), _I, _I]),
     "gsn_find_winners_grid": (ctypes.c_int, [_P, ctypes.POINTER(gsn_grid), _P, ctypes.c_size_t,
                                              _P, _I, _P, _P, _P, _P, _P]),
+    "gsn_find_winners_grid_noalloc": (ctypes.c_int, [_P, ctypes.POINTER(gsn_grid), _P, _I, _P,
+                                                     _P, _P, _P, _P]),
     "gsn_resolve_conflicts": (ctypes.c_int, [_P, _I, _P, _P, _P, _P, _P]),
     "gsn_adapt": (ctypes.c_int, [_P, _P, _I, _P, _P, _P, _P, _P]),
     "gsn_update_edges": (ctypes.c_int, [_P, _I, _P, _P, _P, _P]),
@@ -314,6 +318,17 @@ def gsn_find_winners_grid(net, grid: gsn_grid, grid_ws: torch.Tensor, sig: torch
            "gsn_find_winners_grid")
 
 
+def gsn_find_winners_grid_noalloc(net, grid: gsn_grid, sig: torch.Tensor, m: int, winner,
+                                  second, d1, d2, stream=None):
+    _check(_lib.gsn_find_winners_grid_noalloc(net, ctypes.byref(grid),
+                                              _dev(sig, torch.float32, 3 * m, "sig"), m,
+                                              _dev(winner, torch.int32, m, "winner"),
+                                              _dev(second, torch.int32, m, "second"),
+                                              _dev(d1, torch.float32, m, "d1"),
+                                              _dev(d2, torch.float32, m, "d2"), _stream(stream)),
+           "gsn_find_winners_grid_noalloc")
+
+
 def gsn_iterate(net, sig: torch.Tensor, m: int, winner, second, d1, d2, accepted,
                 stream=None):
     _check(_lib.gsn_iterate(net, _dev(sig, torch.float32, 3 * m, "sig"), m,
@@ -418,6 +433,13 @@ class Network:
         b = self.buf
         gsn_find_winners_grid(self.h, grid, grid_ws, sig, m, b.winner, b.second, b.d1, b.d2,
                               self.stream)
+        return b.winner[:m], b.second[:m], b.d1[:m], b.d2[:m]
+
+    def find_winners_grid_noalloc(self, sig: torch.Tensor, grid: gsn_grid):
+        m = sig.shape[1]
+        b = self.buf
+        gsn_find_winners_grid_noalloc(self.h, grid, sig, m, b.winner, b.second, b.d1, b.d2,
+                                      self.stream)
         return b.winner[:m], b.second[:m], b.d1[:m], b.d2[:m]
 
     def resolve_conflicts(self, m, winner=None, second=None, d1=None):
