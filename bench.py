@@ -56,6 +56,9 @@ EXECUTED_FLOPS_PER_PAIR = 32  # one 32x32x16 product (32768 flops) per 1,024 pai
 FLOPS_PER_EVAL = 8           # 3 sub + 3 mul + 2 add of one squared distance
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "find_winners_genus3_200k_traffic.json")
 SCAN_KERNEL = "fh_scan"
+SMALL_SCAN_KERNEL = "sm_scan"      # batches of at most SMALL_M signals take the small-batch scan
+SMALL_M = 256
+VALU_PLAIN_PEAK_TFLOPS = 39.32     # 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz (no FMA, no packing)
 SCAN_SOURCES = [os.path.join(ROOT, "paper_1503_08294_amd", "csrc", f)
                 for f in ("find_f16.hip", "gsn_internal.h")]
 
@@ -331,6 +334,16 @@ def lock_modes(gsn, args):
     return lock_mode, key_mode
 
 
+def tune(gsn, net, args):
+    """Launch-configuration knobs from the command line (results never depend on them)."""
+    if args.variant:
+        net.tune(gsn.GSN_TUNE_VARIANT, args.variant)
+    if args.split:
+        net.tune(gsn.GSN_TUNE_SPLIT, args.split)
+    if args.grab:
+        net.tune(gsn.GSN_TUNE_GRAB, args.grab)
+
+
 def timed_steps(torch, gsn, net, step, first, count, scan_only=True):
     """Runs steps first .. first+count-1 between two synchronizations.  With scan_only the
     scan's HIP event pair is the only timer inside the window, else every phase timer
@@ -364,6 +377,16 @@ def timed_steps(torch, gsn, net, step, first, count, scan_only=True):
 def scan_roofline(m, n, scan_ms, launches, traffic):
     scan_s = max(scan_ms, 1e-9) * 1e-3
     achieved = FLOPS_PER_EVAL * m * n / scan_s / 1e12
+    if m <= SMALL_M:
+        # the small-batch scan: direct-form distances on the vector unit, one binary32
+        # operation per lane and cycle (no fused multiply-add in the definition)
+        return {"bound": "alu", "kernel": SMALL_SCAN_KERNEL, "dtype": "f32",
+                "achieved": achieved, "peak": VALU_PLAIN_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": achieved / VALU_PLAIN_PEAK_TFLOPS, "traffic": None,
+                "flops_per_launch": FLOPS_PER_EVAL * m * n, "avg_launch_ms": scan_ms,
+                "launches_timed": launches,
+                "peak_derivation": "256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz, one plain binary32 "
+                                   "operation per lane per cycle"}
     return {"bound": "mfma", "kernel": SCAN_KERNEL, "dtype": "f16",
             "achieved": achieved, "peak": F16_PEAK_TFLOPS, "unit": "TFLOP/s",
             "frac": achieved / F16_PEAK_TFLOPS, "traffic": traffic,
@@ -422,9 +445,11 @@ def run_sweep(args):
                                      wl.err_beta, cap["n_max"], cap["e_max"], m, lock_mode,
                                      key_mode)
             net = gsn.Network(params, torch.from_numpy(units).cuda())
+            tune(gsn, net, args)
+            prep = net.prepare_iterate([dev_sig[t] for t in range(warm + steps)])
 
             def step(t):
-                net.iterate(dev_sig[t])
+                prep(t)
 
             for t in range(warm):
                 step(t)
@@ -457,7 +482,7 @@ def run_sweep(args):
                         next((r for r in single.get("runs", []) if r["m"] == m), {}),
                         pinned_with=single.get("pinned_with"))
             net.close()
-            del net, dev_sig
+            del net, dev_sig, prep
             print(json.dumps(rec), flush=True)
 
 
@@ -492,6 +517,12 @@ def main():
     ap.add_argument("--sweep-m", default="", help="with --sweep: comma-separated m values")
     ap.add_argument("--sweep-locks", default="set,winner",
                     help="with --sweep: comma-separated collision rules")
+    ap.add_argument("--variant", type=int, default=0,
+                    help="find-winners kernel variant (GSN_TUNE_VARIANT; 0 = automatic)")
+    ap.add_argument("--split", type=int, default=0,
+                    help="unit chunks / partial rows of the scan (GSN_TUNE_SPLIT; 0 = automatic)")
+    ap.add_argument("--grab", type=int, default=0,
+                    help="batches per grab of the dynamic scan (GSN_TUNE_GRAB; 0 = default)")
     ap.add_argument("--no-late-window", action="store_true",
                     help="skip the record of iterations 81-100")
     # child-process mode of the single-core oracle timing (no GPU)
@@ -565,6 +596,7 @@ def main():
     params = gsn.make_params(wl.eps_b, wl.eps_n, wl.max_age, wl.err_alpha, wl.err_beta,
                              cap["n_max"], cap["e_max"], cap["m_max"], lock_mode, key_mode)
     net = gsn.Network(params, torch.from_numpy(units).cuda())
+    tune(gsn, net, args)
     grid = grid_ws = None
     if args.grid_cell > 0:
         lo = cloud.min(axis=0) - np.float32(1e-3)
@@ -574,9 +606,12 @@ def main():
                              exact=args.grid_exact)
         grid_ws = net.grid_workspace(grid)
 
+    # the timed loop makes one ctypes call per step: arguments marshalled beforehand
+    prep = net.prepare_iterate([dev_sig[t] for t in range(total)]) if grid is None else None
+
     def step(t):
         if grid is None:
-            net.iterate(dev_sig[t])
+            prep(t)
         else:
             net.find_winners_grid(dev_sig[t], grid, grid_ws)
             net.resolve_conflicts(m)

@@ -301,9 +301,12 @@ void gsn_destroy(gsn_net* net);
  *   GSN_TUNE_VARIANT  find-winners kernel: 0 = automatic (4), 1 = direct scan of every
  *                     distance, 2 = screened scan with the screen on the vector unit,
  *                     3 = screened scan with the screen on the matrix cores in binary32,
- *                     4 = the same screen on the matrix cores in split binary16 (every
- *                     screen carries a rigorous rounding margin; candidates are rechecked
- *                     in the binary32 direct form, so all variants return the same result)
+ *                     4 = the same screen on the matrix cores in split binary16, 5 = variant
+ *                     4 with the unit batches dealt out dynamically (every wave takes
+ *                     GSN_TUNE_GRAB batches at a time with an atomic counter) (every screen
+ *                     carries a rigorous rounding margin; candidates are rechecked in the
+ *                     binary32 direct form, so all variants return the same result)
+ *   GSN_TUNE_GRAB     batches of 64 units per atomic grab of variant 5: 1..1024, 0 = default
  *   GSN_TUNE_GRID_ROUNDS  rounds of the GSN_LOCK_WINNER update and of the
  *                     GSN_LOCK_SET_GREEDY resolve launched over the whole device (each
  *                     skipped once fewer than 128 signals are pending) before the remaining
@@ -311,7 +314,7 @@ void gsn_destroy(gsn_net* net);
  *                     one more than the previous update used, from a pinned host copy of its
  *                     count; greedy resolve: 4)
  * Returns GSN_E_INVAL for an unknown key or value. */
-enum { GSN_TUNE_SPLIT = 1, GSN_TUNE_VARIANT = 2, GSN_TUNE_GRID_ROUNDS = 3 };
+enum { GSN_TUNE_SPLIT = 1, GSN_TUNE_VARIANT = 2, GSN_TUNE_GRID_ROUNDS = 3, GSN_TUNE_GRAB = 4 };
 #define GSN_MAX_SPLIT 64
 int gsn_tune(gsn_net* net, int32_t key, int32_t value);
 

@@ -21,7 +21,7 @@ LIB = os.path.join(HERE, "libgsn.so")
 OBJ_DIR = os.path.join(HERE, "_build")
 SOURCES = ["gsn_host.hip", "find_winners.hip", "staging.hip", "find_screened.hip",
            "find_mfma.hip", "find_f16.hip", "update.hip", "update_winner.hip", "grow.hip",
-           "schedule.hip", "find_grid.hip", "resolve_greedy.hip"]
+           "schedule.hip", "find_grid.hip", "resolve_greedy.hip", "find_small.hip"]
 ARCH = "gfx950"
 
 FLAGS = ["-O3", "-std=c++17", f"--offload-arch={ARCH}", "-fPIC",

@@ -354,7 +354,205 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
   }
 }
 
+// Variant 5: the same scan with dynamic work distribution.  The batches are dealt out as
+// eight lists, list x holding the batches t = x + 8 i (so list x is the eighth of the
+// operand array that the XCD with the same number keeps in its L2); for every wave-level
+// signal block (64 signals) each list has a counter in wctr, zeroed by the staging before
+// the call.  Work-group id = 8 k + x runs on XCD x (work-groups reach the XCDs round-robin)
+// and its four waves take the signal blocks of work-group k mod sblocks; a wave repeatedly
+// takes `grab` consecutive list entries with one atomic addition (the next grab's atomic is
+// issued before the current grab's work), drains its own list first and then the other
+// seven, so all waves of a signal block finish within about one grab of each other, and
+// keeps its top-2 in registers across grabs: it writes one partial row pair, row
+// 8 (k div sblocks) + x, at the end.  Every batch is scanned by exactly one wave of each
+// signal block, so the merged result is the exhaustive one, independent of which wave took
+// which batch.
+__device__ __forceinline__ int32_t take(int32_t* ctr, int32_t grab, int lane) {
+  int32_t v = 0;
+  if (lane == 0) v = atomicAdd(ctr, grab);
+  return __builtin_amdgcn_readfirstlane(v);
+}
+
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void fh_scan_dyn(
+    const float4* __restrict__ pu, const uint4* __restrict__ pmh,
+    const int32_t* __restrict__ pidx, int32_t n, const float* __restrict__ ssig, int32_t m,
+    const float* __restrict__ seed, const int32_t* __restrict__ mag,
+    const float* __restrict__ bb, unsigned long long* __restrict__ part,
+    int32_t* __restrict__ wctr, int32_t sblocks, int32_t grab) {
+  constexpr int NB = kBlocks;
+  __shared__ f4 lds_u[4][64];
+  __shared__ int32_t lds_i[4][64];
+  __shared__ float sdata[4][NB * kSigFields * 64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int j = lane & 31, h = lane >> 5;
+  const int32_t n_batches = (n + 63) >> 6;
+  const int32_t id = static_cast<int32_t>(blockIdx.x);
+  const int32_t xcd = id & 7, k = id >> 3;
+  const int32_t sb = k % sblocks, rep = k / sblocks;
+  const int32_t row = 8 * rep + xcd;
+  int32_t* ctr = wctr + 8 * (4 * sb + wave);
+  const float u = 5.9604644775390625e-8f;
+  const float sgm = bb[6], sig2 = sgm * sgm;
+  const float xm = sgm * __int_as_float(mag[0]), ym = sgm * __int_as_float(mag[1]);
+  const float zm = sgm * __int_as_float(mag[2]), nmx = sig2 * __int_as_float(mag[3]);
+  const bool range_ok = fmaxf(xm, fmaxf(ym, zm)) <= 128.0f;
+
+  // the wave's first grab goes out before the signal set-up
+  int32_t x = xcd;
+  int32_t i0 = take(ctr + x, grab, lane);
+
+  const int32_t base = sb * kSignalsPerWG + wave * 32 * NB;
+  float* sd = sdata[wave];
+  h8 bop[NB];
+  float th[NB];
+  unsigned long long k1[NB], k2[NB];
+  uint32_t open = 0;
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    const int32_t p = base + 32 * b + j;
+    const bool live = p < m;
+    const float sx = live ? ssig[p] : 0.0f;
+    const float sy = live ? ssig[m + p] : 0.0f;
+    const float sz = live ? ssig[2 * m + p] : 0.0f;
+    const float tx = sgm * sx, ty = sgm * sy, tz = sgm * sz;
+    const float ss = norm2(tx, ty, tz);
+    const float B = live ? seed[p] : -__builtin_huge_valf();
+    const float T = 2.0f * (fabsf(tx) * xm + fabsf(ty) * ym + fabsf(tz) * zm) + nmx;
+    const float A = 2.0f * ((fabsf(tx) + fabsf(ty)) + fabsf(tz)) + 400.0f;
+    const float ee = live ? (((46.0f * u * T + 6.0f * u * ss) + 3.0f * u * (B * sig2)) +
+                             u * A) + 7.52316384526264e-37f
+                          : 0.0f;
+    const bool big = !(fmaxf(fabsf(tx), fmaxf(fabsf(ty), fabsf(tz))) <= 16384.0f);
+    if (!range_ok || big || (__float_as_uint(ee) & 0x7fffffffu) > 0x6c800000u) open |= 1u << b;
+    k1[b] = pack(B, kSentinel);
+    k2[b] = k1[b];
+    th[b] = live ? theta_of(k2[b], sig2, ss, ee) : -__builtin_huge_valf();
+    const float bx = -2.0f * tx, by = -2.0f * ty, bz = -2.0f * tz;
+    auto split = [](float v, _Float16& hi, _Float16& lo) {
+      hi = static_cast<_Float16>(v);
+      lo = static_cast<_Float16>(v - static_cast<float>(hi));
+    };
+    _Float16 a1, a2, c1, c2;
+    h8 o;
+    if (h == 0) {
+      split(bx, a1, a2);
+      split(by, c1, c2);
+      o = (h8){a1, a2, a1, a2, c1, c2, c1, c2};
+    } else {
+      split(bz, a1, a2);
+      const _Float16 one = static_cast<_Float16>(1.0f), zero = static_cast<_Float16>(0.0f);
+      o = (h8){a1, a2, a1, a2, one, one, zero, zero};
+    }
+    bop[b] = o;
+    float* f = sd + b * kSigFields * 64 + lane;
+    f[0] = sx;
+    f[64] = sy;
+    f[128] = sz;
+    f[192] = ss;
+    f[256] = ee;
+  }
+  const unsigned long long wave_open = __ballot(open != 0);
+
+  // buffer resources at batch 0: batch t's operands sit 2048 t bytes further (the host
+  // keeps 2048 n_batches below 2^31), its units 1024 t and its indices 256 t
+  const __amdgpu_buffer_rsrc_t rh = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint4*>(pmh), 0, 0x7fffffff, 0x00020000);
+  const __amdgpu_buffer_rsrc_t ru_ = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float4*>(pu), 0, 0x7fffffff, 0x00020000);
+  const __amdgpu_buffer_rsrc_t ri_ = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<int32_t*>(pidx), 0, 0x7fffffff, 0x00020000);
+  const int32_t vh = 32 * lane;
+  const v16f zero16 = {};
+  int32_t tried = 1;   // lists whose counter this wave has read (its own so far)
+  while (true) {
+    // list x holds the batches x, x + 8, ...: len entries
+    int32_t len = x < n_batches ? (n_batches - 1 - x) / 8 + 1 : 0;
+    while (i0 >= len && tried < 8) {
+      x = (x + 1) & 7;
+      ++tried;
+      i0 = take(ctr + x, grab, lane);
+      len = x < n_batches ? (n_batches - 1 - x) / 8 + 1 : 0;
+    }
+    if (i0 >= len) break;
+    const int32_t cnt = min(grab, len - i0);
+    const int32_t last = cnt - 1;
+    const int32_t nxt = take(ctr + x, grab, lane);  // the next grab of the same list
+    // batch of entry e of this grab: t = x + 8 (i0 + e)
+    const int32_t t0 = x + 8 * i0;
+    h8 ra[kDepth][2];
+#pragma unroll
+    for (int q = 0; q < kDepth; ++q) {
+      const int32_t tq = t0 + 8 * min(q, last);
+      ra[q][0] = __builtin_bit_cast(h8, __builtin_amdgcn_raw_buffer_load_b128(rh, vh, 2048 * tq, 0));
+      ra[q][1] = __builtin_bit_cast(h8, __builtin_amdgcn_raw_buffer_load_b128(rh, vh + 16, 2048 * tq, 0));
+      asm volatile("" ::: "memory");
+    }
+    v16f res[NB][2];
+    for (int32_t i = 0; i < cnt; i += kDepth) {
+#pragma unroll
+      for (int q = 0; q < kDepth; ++q) {
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          const h8 a = ra[q][e];
+#pragma unroll
+          for (int b = 0; b < NB; ++b)
+            res[b][e] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, bop[b], zero16, 0, 0, 0);
+        }
+        const int32_t tn = t0 + 8 * min(i + kDepth + q, last);
+        ra[q][0] = __builtin_bit_cast(h8, __builtin_amdgcn_raw_buffer_load_b128(rh, vh, 2048 * tn, 0));
+        ra[q][1] = __builtin_bit_cast(h8, __builtin_amdgcn_raw_buffer_load_b128(rh, vh + 16, 2048 * tn, 0));
+        asm volatile("" ::: "memory");
+        float mn[NB];
+#pragma unroll
+        for (int b = 0; b < NB; ++b) mn[b] = block_min(res[b]);
+        const int32_t tc = t0 + 8 * min(i + q, last);
+        finish_batch(res, mn, true, tc, h, lane, n, ru_, ri_, tc, lds_u[wave], lds_i[wave],
+                     sd, sig2, th, k1, k2, open, wave_open);
+      }
+    }
+    i0 = nxt;
+  }
+
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    const unsigned long long o1 = __shfl_xor(k1[b], 32);
+    const unsigned long long o2 = __shfl_xor(k2[b], 32);
+    insert2(k1[b], k2[b], o1);
+    insert2(k1[b], k2[b], o2);
+  }
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    const int32_t p = base + 32 * b + j;
+    if (h == b && p < m) {
+      part[(2 * row) * static_cast<size_t>(m) + p] = k1[b];
+      part[(2 * row + 1) * static_cast<size_t>(m) + p] = k2[b];
+    }
+  }
+}
+
 }  // namespace
+
+int f16_dyn_split(int32_t m, int cus, int want) {
+  // 8 rep rows per signal (one per XCD list per replica); replicas fill the resident slots
+  // (four work-groups of four waves per CU), at most kMaxSplit / 8
+  if (want > 0) return std::max(1, std::min(want / 8, kMaxSplit / 8)) * 8;
+  const int64_t sblocks = (m + kSignalsPerWG - 1) / kSignalsPerWG;
+  const int64_t slots = 4LL * (cus > 0 ? cus : 256);
+  const int64_t reps = std::max<int64_t>(1, std::min<int64_t>(slots / (8 * sblocks), kMaxSplit / 8));
+  return static_cast<int>(8 * reps);
+}
+
+hipError_t launch_scan_f16_dyn(const DevState& s, const StageBufs& b, int32_t n, int32_t m,
+                               int split, int grab, hipStream_t st) {
+  const int32_t n_batches = (n + 63) / 64;
+  if (static_cast<int64_t>(n_batches) * 2048 >= (1LL << 31)) return hipErrorInvalidValue;
+  if (split < 8 || split % 8 != 0 || split > kMaxSplit || grab < 1) return hipErrorInvalidValue;
+  const int32_t sblocks = (m + kSignalsPerWG - 1) / kSignalsPerWG;
+  fh_scan_dyn<<<8 * sblocks * (split / 8), 256, 0, st>>>(b.pu, b.pmh, b.pidx, n, b.ssig, m,
+                                                         b.seed, b.mag, b.bb, s.part, b.wctr,
+                                                         sblocks, grab);
+  return hipGetLastError();
+}
 
 int f16_split(int32_t n, int32_t m, int cus, int want) {
   if (want > 0) return std::min(want, kMaxSplit);

@@ -126,7 +126,14 @@ int signals_per_lane(int32_t m) { return m >= 8192 ? 4 : (m >= 2048 ? 2 : 1); }
 
 FindConfig find_config(int32_t n, int32_t m, int cus, int want_split, int want_variant) {
   FindConfig c;
-  c.variant = want_variant > 0 ? want_variant : 4;
+  // small batches take the unit-parallel scan (no staging) unless a variant is asked for;
+  // variant 6 is only defined up to kSmallM signals (larger batches take variant 4)
+  c.variant = want_variant > 0 ? want_variant : (m <= kSmallM ? 6 : 4);
+  if (c.variant == 6 && m > kSmallM) c.variant = 4;
+  if (c.variant == 6) {
+    c.split = 0;
+    return c;
+  }
   if (c.variant == 2) {
     c.split = screened_split(n, m, cus, want_split);
     return c;
@@ -137,6 +144,10 @@ FindConfig find_config(int32_t n, int32_t m, int cus, int want_split, int want_v
   }
   if (c.variant == 4) {
     c.split = f16_split(n, m, cus, want_split);
+    return c;
+  }
+  if (c.variant == 5) {
+    c.split = f16_dyn_split(m, cus, want_split);
     return c;
   }
   const int S = signals_per_lane(m);

@@ -88,6 +88,7 @@ Layout layout_for(const gsn_params& p) {
   add(mm);                     // 29 schedule acceptance
   add(8 * kA64Slots);          // 30 64-bit accumulators
   add(4 * (mm / 32 + 2));      // 31 accepted signals per workgroup of the fused check
+  add(8 * small_part_keys(p.m_max));  // 32 partial keys of the small-batch scan
   L.total = (o + 255) & ~static_cast<size_t>(255);
   return L;
 }
@@ -127,6 +128,7 @@ void carve(const gsn_params& p, void* base, DevState* s) {
   s->sacc = reinterpret_cast<uint8_t*>(b + L.off[29]);
   s->acc64 = reinterpret_cast<unsigned long long*>(b + L.off[30]);
   s->apart = reinterpret_cast<int32_t*>(b + L.off[31]);
+  s->spart = reinterpret_cast<unsigned long long*>(b + L.off[32]);
 }
 
 }  // namespace gsn
@@ -135,6 +137,7 @@ using gsn::DevState;
 
 enum Phase { kReady = 0, kFound = 1, kResolved = 2, kAdapted = 3 };
 constexpr int kRebucketEvery = 16;
+constexpr int kDefaultGrab = 4;        // batches per grab of the dynamic scan
 constexpr int kDefaultGridRounds = 6;  // before any update has reported back
 constexpr int kGreedyGridRounds = 4;   // grid-wide rounds of the greedy lock-set resolve
 
@@ -147,6 +150,7 @@ struct gsn_net {
   int cus;          // compute units of the device
   int tune_split;
   int tune_variant;
+  int tune_grab;    // list entries per atomic of the dynamic scan
   int stage_parity;  // which set of signal histogram and cursors the next call uses
   bool timing;
   uint32_t timing_mask;  // timers that record while timing is on (bit GSN_T_*)
@@ -329,6 +333,7 @@ int gsn_create(const gsn_params* params, void* workspace, size_t workspace_bytes
   net->phase = kReady;
   net->tune_split = 0;
   net->tune_variant = 0;
+  net->tune_grab = kDefaultGrab;
   net->stage_parity = 0;
   net->timing = false;
   net->timing_mask = (1u << GSN_T_COUNT) - 1;
@@ -400,7 +405,15 @@ int find_impl(gsn_net* net, const float* sig, int32_t m, int32_t* winner, int32_
       gsn::find_config(net->n, m, net->cus, net->tune_split, net->tune_variant);
   TimedRegion all(net, GSN_T_FIND, st);
   hipError_t e;
-  if (cfg.variant >= 2) {
+  if (cfg.variant == 6) {
+    TimedRegion scan(net, GSN_T_FIND_SCAN, st);
+    e = gsn::launch_find_small_scan(net->s, net->n, sig, m, st);
+    scan.end();
+    if (e == hipSuccess) {
+      e = gsn::launch_find_small_merge(net->s, net->n, m, winner, second, d1, d2, claim, st);
+      if (claimed) *claimed = claim != nullptr;
+    }
+  } else if (cfg.variant >= 2) {
     const gsn::StageBufs sb = gsn::carve_stage(net->s.scr, net->p.n_max, net->p.m_max);
     // the unit order is rebuilt when the network changed and every kRebucketEvery calls
     const bool rebucket = net->bucket_n != net->n || net->finds_since_bucket >= kRebucketEvery;
@@ -414,7 +427,9 @@ int find_impl(gsn_net* net, const float* sig, int32_t m, int32_t* winner, int32_
     ++net->finds_since_bucket;
     if (e == hipSuccess) {
       TimedRegion scan(net, GSN_T_FIND_SCAN, st);
-      e = cfg.variant == 4   ? gsn::launch_scan_f16(net->s, sb, net->n, sig, m, cfg.split, st)
+      e = cfg.variant == 5   ? gsn::launch_scan_f16_dyn(net->s, sb, net->n, m, cfg.split,
+                                                    net->tune_grab, st)
+          : cfg.variant == 4 ? gsn::launch_scan_f16(net->s, sb, net->n, sig, m, cfg.split, st)
           : cfg.variant == 3 ? gsn::launch_scan_mfma(net->s, sb, net->n, sig, m, cfg.split, st)
                              : gsn::launch_scan_screened(net->s, sb, net->n, sig, m, cfg.split,
                                                          st);
@@ -712,28 +727,25 @@ int gsn_export(gsn_net* net, float* xyz, float* err, int32_t* edges, void* strea
   if (!net) return GSN_E_INVAL;
   hipStream_t st = as_stream(stream);
   const size_t n = static_cast<size_t>(net->n);
+  // every copy is ordered on the caller's stream, each group followed by its sync
+  auto copy = [&](void* dst, const void* src, size_t bytes) {
+    return hipMemcpyAsync(dst, src, bytes, hipMemcpyDefault, st) == hipSuccess;
+  };
+  auto sync = [&]() { return hipStreamSynchronize(st) == hipSuccess; };
   try {
-    if (hipStreamSynchronize(st) != hipSuccess) return GSN_E_HIP;
-    if (xyz && n > 0) {
-      if (hipMemcpy(xyz, net->s.x, 4 * n, hipMemcpyDefault) != hipSuccess ||
-          hipMemcpy(xyz + n, net->s.y, 4 * n, hipMemcpyDefault) != hipSuccess ||
-          hipMemcpy(xyz + 2 * n, net->s.z, 4 * n, hipMemcpyDefault) != hipSuccess)
-        return GSN_E_HIP;
-    }
-    if (err && n > 0 && hipMemcpy(err, net->s.err, 4 * n, hipMemcpyDefault) != hipSuccess)
-      return GSN_E_HIP;
+    bool ok = true;
+    if (xyz && n > 0)
+      ok = copy(xyz, net->s.x, 4 * n) && copy(xyz + n, net->s.y, 4 * n) &&
+           copy(xyz + 2 * n, net->s.z, 4 * n);
+    if (ok && err && n > 0) ok = copy(err, net->s.err, 4 * n);
+    if (!ok || !sync()) return GSN_E_HIP;
     if (edges) {
       std::vector<int32_t> rp(n + 1);
-      if (hipMemcpy(rp.data(), net->s.rp[net->cur], 4 * (n + 1), hipMemcpyDeviceToHost) !=
-          hipSuccess)
-        return GSN_E_HIP;
+      if (!copy(rp.data(), net->s.rp[net->cur], 4 * (n + 1)) || !sync()) return GSN_E_HIP;
       const size_t half = static_cast<size_t>(rp[n]);
       std::vector<int32_t> col(half), age(half);
-      if (half > 0 &&
-          (hipMemcpy(col.data(), net->s.col[net->cur], 4 * half, hipMemcpyDeviceToHost) !=
-               hipSuccess ||
-           hipMemcpy(age.data(), net->s.age[net->cur], 4 * half, hipMemcpyDeviceToHost) !=
-               hipSuccess))
+      if (half > 0 && (!copy(col.data(), net->s.col[net->cur], 4 * half) ||
+                       !copy(age.data(), net->s.age[net->cur], 4 * half) || !sync()))
         return GSN_E_HIP;
       const size_t e = half / 2;
       std::vector<int32_t> out(3 * e);
@@ -746,8 +758,7 @@ int gsn_export(gsn_net* net, float* xyz, float* err, int32_t* edges, void* strea
             out[2 * e + t] = age[k];
             ++t;
           }
-      if (e > 0 && hipMemcpy(edges, out.data(), 4 * 3 * e, hipMemcpyDefault) != hipSuccess)
-        return GSN_E_HIP;
+      if (e > 0 && (!copy(edges, out.data(), 4 * 3 * e) || !sync())) return GSN_E_HIP;
     }
   } catch (const std::bad_alloc&) {
     return GSN_E_CAPACITY;
@@ -765,7 +776,9 @@ int gsn_import(gsn_net* net, int32_t n, const float* xyz, const float* err, int3
     if (hipStreamSynchronize(st) != hipSuccess) return GSN_E_HIP;
     const size_t nn = static_cast<size_t>(n), ne = static_cast<size_t>(n_edges);
     std::vector<int32_t> ed(3 * ne);
-    if (ne > 0 && hipMemcpy(ed.data(), edges, 4 * 3 * ne, hipMemcpyDefault) != hipSuccess)
+    if (ne > 0 && (hipMemcpyAsync(ed.data(), edges, 4 * 3 * ne, hipMemcpyDefault, st) !=
+                       hipSuccess ||
+                   hipStreamSynchronize(st) != hipSuccess))
       return GSN_E_HIP;
     std::vector<int32_t> deg(nn + 1, 0);
     for (size_t k = 0; k < ne; ++k) {
@@ -792,34 +805,41 @@ int gsn_import(gsn_net* net, int32_t n, const float* xyz, const float* err, int3
         age[k] = half[k].second;
       }
     }
+    // everything below is ordered on the caller's stream; the host vectors stay alive
+    // until the stream synchronization at the end
     net->cur = 0;
     const DevState& s = net->s;
     bool ok = true;
+    auto copy = [&](void* dst, const void* src, size_t bytes) {
+      ok = ok && hipMemcpyAsync(dst, src, bytes, hipMemcpyDefault, st) == hipSuccess;
+    };
+    auto fill_bytes = [&](void* dst, int value, size_t bytes) {
+      ok = ok && hipMemsetAsync(dst, value, bytes, st) == hipSuccess;
+    };
     if (n > 0) {
-      ok = ok && hipMemcpy(s.x, xyz, 4 * nn, hipMemcpyDefault) == hipSuccess;
-      ok = ok && hipMemcpy(s.y, xyz + nn, 4 * nn, hipMemcpyDefault) == hipSuccess;
-      ok = ok && hipMemcpy(s.z, xyz + 2 * nn, 4 * nn, hipMemcpyDefault) == hipSuccess;
-      if (err) {
-        ok = ok && hipMemcpy(s.err, err, 4 * nn, hipMemcpyDefault) == hipSuccess;
-      } else {
-        ok = ok && hipMemset(s.err, 0, 4 * nn) == hipSuccess;
-      }
+      copy(s.x, xyz, 4 * nn);
+      copy(s.y, xyz + nn, 4 * nn);
+      copy(s.z, xyz + 2 * nn, 4 * nn);
+      if (err)
+        copy(s.err, err, 4 * nn);
+      else
+        fill_bytes(s.err, 0, 4 * nn);
     }
-    ok = ok && hipMemcpy(s.rp[0], rp.data(), 4 * (nn + 1), hipMemcpyHostToDevice) == hipSuccess;
+    copy(s.rp[0], rp.data(), 4 * (nn + 1));
     if (ne > 0) {
-      ok = ok && hipMemcpy(s.col[0], col.data(), 8 * ne, hipMemcpyHostToDevice) == hipSuccess;
-      ok = ok && hipMemcpy(s.age[0], age.data(), 8 * ne, hipMemcpyHostToDevice) == hipSuccess;
+      copy(s.col[0], col.data(), 8 * ne);
+      copy(s.age[0], age.data(), 8 * ne);
     }
     const size_t nm = static_cast<size_t>(net->p.n_max);
-    ok = ok && hipMemset(s.ins, 0xff, 4 * nm) == hipSuccess;
-    ok = ok && hipMemset(s.orphan, 0, 4 * nm) == hipSuccess;
-    ok = ok && hipMemset(s.lock, 0xff, 8 * nm) == hipSuccess;
-    ok = ok && hipMemset(s.extra, 0, 4 * nm) == hipSuccess;
-    ok = ok && hipMemset(s.rem, 0, 4 * gsn::kRmSlots) == hipSuccess;
-    ok = ok && hipMemset(s.status, 0, 4 * gsn::kStSlots) == hipSuccess;
+    fill_bytes(s.ins, 0xff, 4 * nm);
+    fill_bytes(s.orphan, 0, 4 * nm);
+    fill_bytes(s.lock, 0xff, 8 * nm);
+    fill_bytes(s.extra, 0, 4 * nm);
+    fill_bytes(s.rem, 0, 4 * gsn::kRmSlots);
+    fill_bytes(s.status, 0, 4 * gsn::kStSlots);
     ok = ok && gsn::launch_stage_init(gsn::carve_stage(s.scr, net->p.n_max, net->p.m_max),
-                                      nullptr) == hipSuccess;
-    ok = ok && hipDeviceSynchronize() == hipSuccess;
+                                      st) == hipSuccess;
+    ok = hipStreamSynchronize(st) == hipSuccess && ok;
     if (!ok) return GSN_E_HIP;
     net->n = n;
     net->phase = kReady;
@@ -858,8 +878,12 @@ int gsn_tune(gsn_net* net, int32_t key, int32_t value) {
       net->tune_split = value;
       return GSN_OK;
     case GSN_TUNE_VARIANT:
-      if (value < 0 || value > 4) return GSN_E_INVAL;
+      if (value < 0 || value > 6) return GSN_E_INVAL;
       net->tune_variant = value;
+      return GSN_OK;
+    case GSN_TUNE_GRAB:
+      if (value < 0 || value > 1024) return GSN_E_INVAL;
+      net->tune_grab = value ? value : kDefaultGrab;
       return GSN_OK;
     case GSN_TUNE_GRID_ROUNDS:
       if (value < 0 || value > gsn::kMaxGridRounds) return GSN_E_INVAL;  // 0: automatic

@@ -12,6 +12,8 @@ namespace gsn {
 
 constexpr int kBlock = 256;            // threads per workgroup of the per-unit kernels
 constexpr int kMaxSplit = GSN_MAX_SPLIT;
+constexpr int kSmallM = 256;           // batches up to this size may take the small-batch scan
+constexpr int kSmallRows = 1024;       // its partial rows (workgroups) at most
 constexpr int32_t kDead = -1;          // age marking a half-edge removed this iteration
 
 // Sticky status word layout (int32 slots in the status area).
@@ -169,6 +171,8 @@ struct DevState {
   float* tmp;                      // [4 n_max]     compaction staging
   int32_t* status;                 // [kStSlots]
   unsigned long long* part;        // [kMaxSplit][2][m_max] per-chunk top-2 keys
+  unsigned long long* spart;       // [small_part_keys(m_max)] partial keys of the small-batch
+                                   // scan: [2 kSmallRows][slots]
   void* scr;                       // staging area of the screened scans (staging.hip)
   // sequential-survivor update (winner lock)
   uint8_t* pend;                   // [m_max]       1 pending survivor, 0 otherwise
@@ -187,7 +191,7 @@ struct DevState {
 };
 
 struct Layout {
-  size_t off[32];
+  size_t off[40];
   size_t total;
 };
 
@@ -198,8 +202,10 @@ void carve(const gsn_params& p, void* base, DevState* s);
 // Every launcher enqueues on `stream` and returns the hipGetLastError() of its launches.
 
 struct FindConfig {
-  int variant;   // 1 = direct scan, 2 = screened scan (VALU), 3 = screened scan (MFMA)
-  int split;     // unit chunks
+  int variant;   // 1 = direct scan, 2 = screened scan (VALU), 3 = screened scan (MFMA),
+                 // 4 = screened scan (split binary16 MFMA), 5 = variant 4 with dynamic grabs,
+                 // 6 = small-batch unit-parallel scan
+  int split;     // unit chunks (variant 5: partial rows, 8 per replica)
 };
 FindConfig find_config(int32_t n, int32_t m, int cus, int want_split, int want_variant);
 
@@ -209,6 +215,18 @@ hipError_t launch_find_scan(const DevState& s, int32_t n, const float* sig, int3
 hipError_t launch_find_merge(const DevState& s, int32_t m, const FindConfig& cfg,
                              int32_t* winner, int32_t* second, float* d1, float* d2,
                              hipStream_t st);
+
+// Small-batch find winners (find_small.hip): unit-parallel, no staging, for
+// 1 <= m <= kSmallM (variant 6).  slots = the smallest power of two >= m.
+int32_t small_slots(int32_t m);
+int32_t small_rows(int32_t n, int32_t m);
+size_t small_part_keys(int32_t m_max);
+hipError_t launch_find_small_scan(const DevState& s, int32_t n, const float* sig, int32_t m,
+                                  hipStream_t st);
+struct ClaimArgs;
+hipError_t launch_find_small_merge(const DevState& s, int32_t n, int32_t m, int32_t* winner,
+                                   int32_t* second, float* d1, float* d2,
+                                   const ClaimArgs* claim, hipStream_t st);
 
 // Spatial staging of the screened scans (staging.hip).
 constexpr int kBuckets = 32 * 32 * 32;
@@ -231,7 +249,11 @@ struct StageBufs {
   float* pm;        // [ceil(n_max / 64) * 256] units in matrix-core operand order
   uint4* pmh;       // [ceil(n_max / 64)][64 lanes][2 groups] scaled units split into binary16
                     // pairs, in the operand order of the 32x32x16 f16 product (16 B each)
+  int32_t* wctr;    // [wctr_count(m_max)] grab counters of the dynamic scan, zeroed by the
+                    // seed kernel of every call: 8 lists per 64-signal block
 };
+// 8 counters per 64-signal block, for whole blocks of 256 signals
+inline int32_t wctr_count(int32_t m) { return 32 * ((m + 255) / 256); }
 size_t stage_bytes(int32_t n_max, int32_t m_max);
 StageBufs carve_stage(void* base, int32_t n_max, int32_t m_max);
 hipError_t launch_stage_init(const StageBufs& b, hipStream_t st);
@@ -260,6 +282,10 @@ int mfma_split(int32_t n, int32_t m, int cus, int want);
 int f16_split(int32_t n, int32_t m, int cus, int want);
 hipError_t launch_scan_f16(const DevState& s, const StageBufs& b, int32_t n, const float* sig,
                            int32_t m, int split, hipStream_t st);
+// variant 5: split = 8 x replicas (a multiple of 8), grab = list entries per atomic
+int f16_dyn_split(int32_t m, int cus, int want);
+hipError_t launch_scan_f16_dyn(const DevState& s, const StageBufs& b, int32_t n, int32_t m,
+                               int split, int grab, hipStream_t st);
 hipError_t launch_scan_mfma(const DevState& s, const StageBufs& b, int32_t n, const float* sig,
                             int32_t m, int split, hipStream_t st);
 

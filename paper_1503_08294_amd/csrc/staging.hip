@@ -403,7 +403,7 @@ __global__ __launch_bounds__(kBlock) void st_place_seed(
     const float4* __restrict__ pu, const int32_t* __restrict__ pidx, int32_t n,
     const int32_t* __restrict__ off_u, int32_t* __restrict__ sperm, float* __restrict__ seed,
     float* __restrict__ ssig, const float* __restrict__ bmag,
-    int32_t nmag, int32_t* __restrict__ mag) {
+    int32_t nmag, int32_t* __restrict__ mag, int32_t* __restrict__ wctr, int32_t nctr) {
   static_assert(kBlock == 256 && kSignalBuckets % kBlock == 0, "four waves, whole bins");
   constexpr int per = kSignalBuckets / kBlock;
   __shared__ int32_t soff[kSignalBuckets];
@@ -455,6 +455,7 @@ __global__ __launch_bounds__(kBlock) void st_place_seed(
   __syncthreads();
 
   const int32_t t = blockIdx.x * kBlock + tid;
+  if (t < nctr) wctr[t] = 0;  // grab counters of the dynamic scan (variant 5)
   const int32_t j = t / kSeedLanes;
   const int q = t % kSeedLanes;
   int32_t pos = -1;
@@ -611,6 +612,7 @@ size_t stage_bytes(int32_t n_max, int32_t m_max) {
   add(16 * (nm / kBlock + 2));  // bmag
   add(16 * ((nm + 63) / 64 * 64));  // pm
   add(32 * ((nm + 63) / 64 * 64));  // pmh
+  add(4 * wctr_count(m_max));        // wctr
   return b;
 }
 
@@ -645,6 +647,7 @@ StageBufs carve_stage(void* base, int32_t n_max, int32_t m_max) {
   s.bmag = reinterpret_cast<float*>(take(16 * (nm / kBlock + 2)));
   s.pm = reinterpret_cast<float*>(take(16 * ((nm + 63) / 64 * 64)));
   s.pmh = reinterpret_cast<uint4*>(take(32 * ((nm + 63) / 64 * 64)));
+  s.wctr = reinterpret_cast<int32_t*>(take(4 * wctr_count(m_max)));
   return s;
 }
 
@@ -661,7 +664,7 @@ hipError_t launch_stage_init(const StageBufs& b, hipStream_t st) {
 
 hipError_t launch_stage(const DevState& s, const StageBufs& b, int32_t n, const float* sig,
                         int32_t m, bool rebucket, int parity, int variant, hipStream_t st) {
-  const int layouts = variant == 3 ? kLayoutF32 : variant == 4 ? kLayoutF16 : 0;
+  const int layouts = variant == 3 ? kLayoutF32 : variant >= 4 ? kLayoutF16 : 0;
   const int nb_u = blocks(n);
   if (rebucket) {
     st_bbox<<<std::min(nb_u, 64), kBlock, 0, st>>>(s.x, s.y, s.z, n, b.acc);
@@ -682,7 +685,7 @@ hipError_t launch_stage(const DevState& s, const StageBufs& b, int32_t n, const 
                                                  cur_next, b.bmag, layouts);
   st_place_seed<<<blocks(static_cast<int64_t>(m) * kSeedLanes), kBlock, 0, st>>>(
       hist, cur, b.skey, sig, m, b.pu, b.pidx, n, b.off_u, b.sperm, b.seed, b.ssig,
-      b.bmag, nb_g, b.mag);
+      b.bmag, nb_g, b.mag, b.wctr, wctr_count(m));
   return hipGetLastError();
 }
 

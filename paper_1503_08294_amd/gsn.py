@@ -28,6 +28,7 @@ GSN_E_STATE = -4
 GSN_TUNE_SPLIT = 1
 GSN_TUNE_VARIANT = 2
 GSN_TUNE_GRID_ROUNDS = 3
+GSN_TUNE_GRAB = 4
 GSN_MAX_SPLIT = 64
 
 GSN_T_FIND_SCAN = 0
@@ -364,6 +365,35 @@ def gsn_stat(net, key: int, stream=None) -> int:
 
 # ------------------------------------------------------------------ convenience ----
 
+class PreparedIterate:
+    """Pre-marshalled gsn_iterate calls over a fixed list of signal batches (see
+    Network.prepare_iterate).  The tensors must stay alive and unchanged in shape."""
+
+    def __init__(self, net, sigs):
+        b = net.buf
+        self._net = net
+        self._keep = list(sigs)
+        m = self._keep[0].shape[1]
+        outs = [_dev(b.winner, torch.int32, m, "winner"), _dev(b.second, torch.int32, m, "second"),
+                _dev(b.d1, torch.float32, m, "d1"), _dev(b.d2, torch.float32, m, "d2"),
+                _dev(b.accepted, torch.uint8, m, "accepted")]
+        st = _stream(net.stream)
+        self._args = []
+        for sig in self._keep:
+            if sig.shape[1] != m:
+                raise ValueError("every batch must hold the same number of signals")
+            self._args.append((net.h, _dev(sig, torch.float32, 3 * m, "sig"), m, *outs, st))
+        self.m = m
+
+    def __len__(self):
+        return len(self._args)
+
+    def __call__(self, t: int):
+        rc = _lib.gsn_iterate(*self._args[t])
+        if rc != GSN_OK:
+            raise GsnError(rc, "gsn_iterate")
+
+
 @dataclass
 class Buffers:
     """Per-iteration device buffers for up to m_max signals."""
@@ -469,6 +499,13 @@ class Network:
         b = self.buf
         gsn_iterate(self.h, sig, m, b.winner, b.second, b.d1, b.d2, b.accepted, self.stream)
         return b.winner[:m], b.second[:m], b.d1[:m], b.d2[:m], b.accepted[:m]
+
+    def prepare_iterate(self, sigs):
+        """gsn_iterate arguments for each batch of ``sigs`` (device SoA (3, m) tensors, or a
+        (T, 3, m) tensor), validated and marshalled once; calling the result with t makes
+        the one gsn_iterate call of batch t.  For timed loops where the per-call argument
+        checks would cost more host time than the call itself."""
+        return PreparedIterate(self, sigs)
 
     def iterate_steps(self, sig: torch.Tensor):
         """The same iteration through the four separate calls."""

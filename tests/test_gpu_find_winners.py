@@ -92,7 +92,7 @@ def test_genus3_full_size():
     assert_find_equal(g, o, "genus3_200k")
 
 
-@pytest.mark.parametrize("variant", [1, 2, 3, 4])
+@pytest.mark.parametrize("variant", [1, 2, 3, 4, 5, 6])
 @pytest.mark.parametrize("n,m,seed", [(2, 3, 0), (3, 1, 1), (257, 999, 2), (4000, 16_384, 3),
                                       (30_000, 5_000, 4)])
 def test_both_kernel_variants(variant, n, m, seed):
@@ -106,7 +106,7 @@ def test_both_kernel_variants(variant, n, m, seed):
     assert_find_equal(g, o, f"variant={variant} n={n} m={m}")
 
 
-@pytest.mark.parametrize("variant", [1, 2, 3, 4])
+@pytest.mark.parametrize("variant", [1, 2, 3, 4, 5, 6])
 def test_cancellation_and_near_ties_far_from_the_origin(variant):
     """Units and signals around (1000, -1000, 1000) separated by ~1e-3: the expanded form
     loses about 12 bits to cancellation here, and many distances differ by a few ulps, so a
@@ -130,7 +130,7 @@ def test_cancellation_and_near_ties_far_from_the_origin(variant):
     assert_find_equal(g, o, f"variant={variant}")
 
 
-@pytest.mark.parametrize("variant", [2, 3, 4])
+@pytest.mark.parametrize("variant", [2, 3, 4, 5])
 def test_screened_variants_ties_on_a_grid(variant):
     from paper_1503_08294_amd import gsn
     rng = np.random.default_rng(5)
@@ -144,7 +144,7 @@ def test_screened_variants_ties_on_a_grid(variant):
         assert_find_equal(g, o, f"split={split}")
 
 
-@pytest.mark.parametrize("variant", [1, 2, 3, 4])
+@pytest.mark.parametrize("variant", [1, 2, 3, 4, 5, 6])
 @pytest.mark.parametrize("scale", [1e17, 1e20])
 def test_huge_signal_coordinates_are_scanned_exactly(variant, scale):
     """Signals far outside the screen's range (margin above 2^90, distances near or past
@@ -162,7 +162,7 @@ def test_huge_signal_coordinates_are_scanned_exactly(variant, scale):
     assert_find_equal(g, o, f"variant={variant} scale={scale:g}")
 
 
-@pytest.mark.parametrize("variant", [2, 3, 4])
+@pytest.mark.parametrize("variant", [2, 3, 4, 5])
 def test_one_huge_unit_opens_every_signal(variant):
     """A single unit at 1e19 makes the magnitude bounds overflow, so every signal is open
     (scanned exactly); results still match the oracle."""
@@ -177,7 +177,7 @@ def test_one_huge_unit_opens_every_signal(variant):
     assert_find_equal(g, o, f"variant={variant}")
 
 
-@pytest.mark.parametrize("variant", [2, 3, 4])
+@pytest.mark.parametrize("variant", [2, 3, 4, 5])
 def test_everything_at_1e17_is_scanned_exactly(variant):
     """Units and signals spread at the 1e17 scale: distances are finite and distinct but the
     screen's margin exceeds its range for every signal, so all are scanned exactly."""
@@ -190,3 +190,65 @@ def test_everything_at_1e17_is_scanned_exactly(variant):
     g, o = pair.find(sig)
     assert len(np.unique(o[0])) > 100, "the case must not collapse into ties"
     assert_find_equal(g, o, f"variant={variant}")
+
+
+@pytest.mark.parametrize("n,m,seed", [(2, 5, 0), (130, 700, 1), (511, 64, 2), (40_037, 2_999, 3),
+                                      (200_003, 1_300, 4)])
+def test_dynamic_scan_any_grab_and_replica_count(n, m, seed):
+    """Variant 5 deals the unit batches out with atomic counters; the answer cannot depend
+    on the grab size, the number of replicas (rows of partial keys), or on which wave took
+    which batch.  Sizes with fewer batches than lists (2, 130, 511 units), ragged batches
+    and signal blocks, duplicates across lists and signals on units."""
+    from paper_1503_08294_amd import gsn
+    rng = np.random.default_rng(300 + seed)
+    units = rng.standard_normal((3, n)).astype(np.float32)
+    if n >= 2_000:
+        units[:, n - 1_000:] = units[:, :1_000]
+    sig = rng.standard_normal((3, m)).astype(np.float32)
+    k = min(m, n) // 2
+    sig[:, :k] = units[:, n - k:]
+    pair = Pair(units, m_max=m)
+    o = pair.orc.find_winners(sig)
+    pair.net.tune(gsn.GSN_TUNE_VARIANT, 5)
+    for split, grab in ((0, 0), (8, 1), (16, 3), (64, 2), (24, 1024), (0, 7)):
+        pair.net.tune(gsn.GSN_TUNE_SPLIT, split)
+        pair.net.tune(gsn.GSN_TUNE_GRAB, grab)
+        g = [t.cpu().numpy() for t in pair.net.find_winners(pair.to_dev(sig))]
+        assert_find_equal(g, o, f"n={n} m={m} split={split} grab={grab}")
+
+
+def test_dynamic_scan_genus3_full_size():
+    """Variant 5 on the full 200,000 x 16,384 genus-3 launch, every output compared."""
+    from paper_1503_08294_amd import gsn
+    from paper_1503_08294_amd.clouds import WORKLOADS, SignalStream
+    wl = WORKLOADS["genus3_200k"]
+    cloud = wl.make_cloud()
+    units = wl.make_units(cloud)
+    sig = SignalStream(cloud, wl.signal_seed).next(wl.m)
+    pair = Pair(units, m_max=wl.m)
+    pair.net.tune(gsn.GSN_TUNE_VARIANT, 5)
+    g, o = pair.find(sig)
+    assert_find_equal(g, o, "genus3_200k variant 5")
+
+
+@pytest.mark.parametrize("m", [1, 2, 3, 63, 64, 65, 200, 256, 257, 1024])
+@pytest.mark.parametrize("n,kind", [(2, "random"), (3, "grid"), (1_000, "grid"),
+                                    (100_000, "random"), (200_003, "random")])
+def test_small_batches(m, n, kind):
+    """Batches of at most 256 signals take the unit-parallel scan by default (larger ones the
+    staged scan): every slot count from 1 to 256, ragged slot groups (3, 63, 65, 200),
+    integer grids with many exact ties and duplicated units, signals on top of units."""
+    rng = np.random.default_rng(1000 * m + n)
+    if kind == "grid":
+        units = rng.integers(-3, 4, (3, n)).astype(np.float32)
+        sig = rng.integers(-3, 4, (3, m)).astype(np.float32)
+    else:
+        units = rng.standard_normal((3, n)).astype(np.float32)
+        sig = rng.standard_normal((3, m)).astype(np.float32)
+        if n >= 4:
+            units[:, n // 2:n // 2 + n // 4] = units[:, :n // 4]      # exact duplicates
+    k = min(m, n) // 2
+    sig[:, :k] = units[:, n - k:]
+    pair = Pair(units, m_max=max(m, 256))
+    g, o = pair.find(sig)
+    assert_find_equal(g, o, f"n={n} m={m} {kind}")
