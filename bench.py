@@ -342,6 +342,8 @@ def tune(gsn, net, args):
         net.tune(gsn.GSN_TUNE_SPLIT, args.split)
     if args.grab:
         net.tune(gsn.GSN_TUNE_GRAB, args.grab)
+    if args.rebucket:
+        net.tune(gsn.GSN_TUNE_REBUCKET, args.rebucket)
 
 
 def timed_steps(torch, gsn, net, step, first, count, scan_only=True):
@@ -473,6 +475,10 @@ def run_sweep(args):
             }
             if lock_mode == gsn.GSN_LOCK_WINNER:
                 rec["birthday_conflict_rate"] = birthday_conflict_rate(n, m)
+                updates = net.stat(gsn.GSN_STAT_UPDATES)
+                rec["update_rounds"] = ({"mean": net.stat(gsn.GSN_STAT_ROUNDS) / updates,
+                                         "max": net.stat(gsn.GSN_STAT_ROUNDS_MAX)}
+                                        if updates else None)
             if args.cpu_budget > 0:
                 rec["cpu_baseline"] = cpu_baseline(wl, units, cloud, min(args.cpu_budget, 3.0),
                                                    lock_mode, key_mode, m=m, max_iters=60)
@@ -523,6 +529,8 @@ def main():
                     help="unit chunks / partial rows of the scan (GSN_TUNE_SPLIT; 0 = automatic)")
     ap.add_argument("--grab", type=int, default=0,
                     help="batches per grab of the dynamic scan (GSN_TUNE_GRAB; 0 = default)")
+    ap.add_argument("--rebucket", type=int, default=0,
+                    help="find calls between rebuilds of the unit order (GSN_TUNE_REBUCKET)")
     ap.add_argument("--no-late-window", action="store_true",
                     help="skip the record of iterations 81-100")
     # child-process mode of the single-core oracle timing (no GPU)

@@ -307,6 +307,9 @@ void gsn_destroy(gsn_net* net);
  *                     carries a rigorous rounding margin; candidates are rechecked in the
  *                     binary32 direct form, so all variants return the same result)
  *   GSN_TUNE_GRAB     batches of 64 units per atomic grab of variant 5: 1..1024, 0 = default
+ *   GSN_TUNE_REBUCKET staged find calls (variants 2-5) between rebuilds of the spatial order
+ *                     of the units (it is also rebuilt whenever N or the indices change):
+ *                     1..4096, 0 = default (64)
  *   GSN_TUNE_GRID_ROUNDS  rounds of the GSN_LOCK_WINNER update and of the
  *                     GSN_LOCK_SET_GREEDY resolve launched over the whole device (each
  *                     skipped once fewer than 128 signals are pending) before the remaining
@@ -314,7 +317,8 @@ void gsn_destroy(gsn_net* net);
  *                     one more than the previous update used, from a pinned host copy of its
  *                     count; greedy resolve: 4)
  * Returns GSN_E_INVAL for an unknown key or value. */
-enum { GSN_TUNE_SPLIT = 1, GSN_TUNE_VARIANT = 2, GSN_TUNE_GRID_ROUNDS = 3, GSN_TUNE_GRAB = 4 };
+enum { GSN_TUNE_SPLIT = 1, GSN_TUNE_VARIANT = 2, GSN_TUNE_GRID_ROUNDS = 3, GSN_TUNE_GRAB = 4,
+       GSN_TUNE_REBUCKET = 5 };
 #define GSN_MAX_SPLIT 64
 int gsn_tune(gsn_net* net, int32_t key, int32_t value);
 

@@ -89,6 +89,8 @@ Layout layout_for(const gsn_params& p) {
   add(8 * kA64Slots);          // 30 64-bit accumulators
   add(4 * (mm / 32 + 2));      // 31 accepted signals per workgroup of the fused check
   add(8 * small_part_keys(p.m_max));  // 32 partial keys of the small-batch scan
+  add(4 * (nm / kBlock + 2));  // 33 per-block half-edge changes, set 0
+  add(4 * (nm / kBlock + 2));  // 34 per-block half-edge changes, set 1
   L.total = (o + 255) & ~static_cast<size_t>(255);
   return L;
 }
@@ -129,6 +131,8 @@ void carve(const gsn_params& p, void* base, DevState* s) {
   s->acc64 = reinterpret_cast<unsigned long long*>(b + L.off[30]);
   s->apart = reinterpret_cast<int32_t*>(b + L.off[31]);
   s->spart = reinterpret_cast<unsigned long long*>(b + L.off[32]);
+  s->bdelta[0] = reinterpret_cast<int32_t*>(b + L.off[33]);
+  s->bdelta[1] = reinterpret_cast<int32_t*>(b + L.off[34]);
 }
 
 }  // namespace gsn
@@ -136,7 +140,7 @@ void carve(const gsn_params& p, void* base, DevState* s) {
 using gsn::DevState;
 
 enum Phase { kReady = 0, kFound = 1, kResolved = 2, kAdapted = 3 };
-constexpr int kRebucketEvery = 16;
+constexpr int kRebucketEvery = 64;     // default calls between rebuilds of the unit order
 constexpr int kDefaultGrab = 4;        // batches per grab of the dynamic scan
 constexpr int kDefaultGridRounds = 6;  // before any update has reported back
 constexpr int kGreedyGridRounds = 4;   // grid-wide rounds of the greedy lock-set resolve
@@ -146,11 +150,13 @@ struct gsn_net {
   DevState s;
   int32_t n;        // live units (host copy, changed only by grow/import)
   int cur;          // current CSR buffer
+  int dpar;         // which per-block delta array the next lock-set edge update uses
   int phase;
   int cus;          // compute units of the device
   int tune_split;
   int tune_variant;
   int tune_grab;    // list entries per atomic of the dynamic scan
+  int tune_rebucket;  // staged find calls between rebuilds of the spatial unit order
   int stage_parity;  // which set of signal histogram and cursors the next call uses
   bool timing;
   uint32_t timing_mask;  // timers that record while timing is on (bit GSN_T_*)
@@ -330,10 +336,12 @@ int gsn_create(const gsn_params* params, void* workspace, size_t workspace_bytes
   gsn::carve(*params, workspace, &net->s);
   net->n = n0;
   net->cur = 0;
+  net->dpar = 0;
   net->phase = kReady;
   net->tune_split = 0;
   net->tune_variant = 0;
   net->tune_grab = kDefaultGrab;
+  net->tune_rebucket = kRebucketEvery;
   net->stage_parity = 0;
   net->timing = false;
   net->timing_mask = (1u << GSN_T_COUNT) - 1;
@@ -416,7 +424,7 @@ int find_impl(gsn_net* net, const float* sig, int32_t m, int32_t* winner, int32_
   } else if (cfg.variant >= 2) {
     const gsn::StageBufs sb = gsn::carve_stage(net->s.scr, net->p.n_max, net->p.m_max);
     // the unit order is rebuilt when the network changed and every kRebucketEvery calls
-    const bool rebucket = net->bucket_n != net->n || net->finds_since_bucket >= kRebucketEvery;
+    const bool rebucket = net->bucket_n != net->n || net->finds_since_bucket >= net->tune_rebucket;
     e = gsn::launch_stage(net->s, sb, net->n, sig, m, rebucket, net->stage_parity,
                           cfg.variant, st);
     net->stage_parity ^= 1;
@@ -589,11 +597,13 @@ int gsn_update_edges(gsn_net* net, int32_t m, const int32_t* winner, const int32
     return GSN_OK;
   }
   TimedRegion t(net, GSN_T_EDGES, st);
-  hipError_t e = gsn::launch_edges(net->s, net->cur, net->n, m, winner, second, accepted,
+  hipError_t e = gsn::launch_edges(net->s, net->cur, net->dpar, net->n, m, winner, second,
+                                   accepted,
                                    net->p.max_age, 2 * static_cast<int64_t>(net->p.e_max), st);
   t.end();
   if (e != hipSuccess) return GSN_E_HIP;
   net->cur ^= 1;
+  net->dpar ^= 1;
   net->phase = kReady;
   return GSN_OK;
 }
@@ -619,12 +629,14 @@ int gsn_iterate(gsn_net* net, const float* sig, int32_t m, int32_t* winner, int3
   hipStream_t st = as_stream(stream);
   TimedRegion t(net, GSN_T_UPDATE, st);
   const hipError_t e = gsn::launch_iterate_set(
-      net->s, net->cur, net->n, sig, m, winner, second, d1, accepted, net->p.key_mode,
+      net->s, net->cur, net->dpar, net->n, sig, m, winner, second, d1, accepted,
+      net->p.key_mode,
       net->p.eps_b, net->p.eps_n, net->p.err_beta, net->p.max_age,
       2 * static_cast<int64_t>(net->p.e_max), claimed, st);
   t.end();
   if (e != hipSuccess) return GSN_E_HIP;
   net->cur ^= 1;
+  net->dpar ^= 1;
   net->phase = kReady;
   return GSN_OK;
 }
@@ -837,11 +849,14 @@ int gsn_import(gsn_net* net, int32_t n, const float* xyz, const float* err, int3
     fill_bytes(s.extra, 0, 4 * nm);
     fill_bytes(s.rem, 0, 4 * gsn::kRmSlots);
     fill_bytes(s.status, 0, 4 * gsn::kStSlots);
+    fill_bytes(s.bdelta[0], 0, 4 * (nm / gsn::kBlock + 2));
+    fill_bytes(s.bdelta[1], 0, 4 * (nm / gsn::kBlock + 2));
     ok = ok && gsn::launch_stage_init(gsn::carve_stage(s.scr, net->p.n_max, net->p.m_max),
                                       st) == hipSuccess;
     ok = hipStreamSynchronize(st) == hipSuccess && ok;
     if (!ok) return GSN_E_HIP;
     net->n = n;
+    net->dpar = 0;
     net->phase = kReady;
     net->bucket_n = -1;
   } catch (const std::bad_alloc&) {
@@ -884,6 +899,10 @@ int gsn_tune(gsn_net* net, int32_t key, int32_t value) {
     case GSN_TUNE_GRAB:
       if (value < 0 || value > 1024) return GSN_E_INVAL;
       net->tune_grab = value ? value : kDefaultGrab;
+      return GSN_OK;
+    case GSN_TUNE_REBUCKET:
+      if (value < 0 || value > 4096) return GSN_E_INVAL;
+      net->tune_rebucket = value ? value : kRebucketEvery;
       return GSN_OK;
     case GSN_TUNE_GRID_ROUNDS:
       if (value < 0 || value > gsn::kMaxGridRounds) return GSN_E_INVAL;  // 0: automatic

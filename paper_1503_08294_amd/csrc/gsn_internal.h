@@ -168,6 +168,10 @@ struct DevState {
   int32_t* orphan;                 // [n_max]       1 = last edge removed by aging
   int32_t* cnt;                    // [n_max]       per-unit scratch counts / new ids
   int32_t* bsum;                   // [n_max / kBlock + 2] per-block sums / offsets
+  int32_t* bdelta[2];              // [n_max / kBlock + 2] each: change of the half-edge count
+                                   // of every block of kBlock units in this update (+1 per
+                                   // requested edge, -1 per half-edge marked dead); the
+                                   // update uses one and zeroes the other for the next
   float* tmp;                      // [4 n_max]     compaction staging
   int32_t* status;                 // [kStSlots]
   unsigned long long* part;        // [kMaxSplit][2][m_max] per-chunk top-2 keys
@@ -298,7 +302,7 @@ hipError_t launch_adapt(const DevState& s, int cur, int32_t n, const float* sig,
                         const int32_t* winner, const int32_t* second, const float* d1,
                         const uint8_t* accepted, float eps_b, float eps_n, float beta,
                         hipStream_t st);
-hipError_t launch_edges(const DevState& s, int cur, int32_t n, int32_t m,
+hipError_t launch_edges(const DevState& s, int cur, int dpar, int32_t n, int32_t m,
                         const int32_t* winner, const int32_t* second,
                         const uint8_t* accepted, int32_t max_age, int64_t half_cap,
                         hipStream_t st);
@@ -333,7 +337,7 @@ hipError_t launch_winner_update(const DevState& s, int cur, int32_t n, const Win
 // The lock-set resolve, adaptation and edge update of one iteration in five launches (claim;
 // check fused with the accepted signals' updates; degree count fused with the error
 // decay; scan; rewrite into buffer cur ^ 1).
-hipError_t launch_iterate_set(const DevState& s, int cur, int32_t n, const float* sig,
+hipError_t launch_iterate_set(const DevState& s, int cur, int dpar, int32_t n, const float* sig,
                               int32_t m, const int32_t* winner, const int32_t* second,
                               const float* d1, uint8_t* accepted, int key_mode, float eps_b,
                               float eps_n, float beta, int32_t max_age, int64_t half_cap,

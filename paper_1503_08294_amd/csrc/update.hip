@@ -213,7 +213,8 @@ __device__ __forceinline__ void mark_signal(int32_t b, int32_t s,
                                             const int32_t* __restrict__ col,
                                             int32_t* __restrict__ age, int32_t* __restrict__ ins,
                                             int32_t* __restrict__ orphan,
-                                            int32_t* __restrict__ status, int32_t max_age) {
+                                            int32_t* __restrict__ status, int32_t max_age,
+                                            int32_t* __restrict__ bdelta) {
   const int32_t r0 = rp[b], r1 = rp[b + 1];
   bool found = false;
   for (int32_t k = r0; k < r1; ++k) {
@@ -230,13 +231,19 @@ __device__ __forceinline__ void mark_signal(int32_t b, int32_t s,
   if (!found) {
     ins[b] = s;
     ins[s] = b;
+    atomicAdd(&bdelta[b / kBlock], 1);
+    atomicAdd(&bdelta[s / kBlock], 1);
   }
   for (int32_t k = r0; k < r1; ++k) {
     if (age[k] <= max_age) continue;
     const int32_t v = col[k];
     age[k] = kDead;
+    atomicAdd(&bdelta[b / kBlock], -1);
     const int32_t rk = find_in_row(rp, col, v, b);
-    if (rk >= 0) age[rk] = kDead;
+    if (rk >= 0) {
+      age[rk] = kDead;
+      atomicAdd(&bdelta[v / kBlock], -1);
+    }
     bool live = ins[v] >= 0;
     for (int32_t kk = rp[v]; !live && kk < rp[v + 1]; ++kk) live = age[kk] != kDead;
     if (!live && !orphan[v]) {
@@ -252,12 +259,13 @@ __global__ void ed_mark(int32_t m, int32_t n, const int32_t* __restrict__ winner
                         const uint8_t* __restrict__ accepted, const int32_t* __restrict__ rp,
                         const int32_t* __restrict__ col, int32_t* __restrict__ age,
                         int32_t* __restrict__ ins, int32_t* __restrict__ orphan,
-                        int32_t* __restrict__ status, int32_t max_age) {
+                        int32_t* __restrict__ status, int32_t max_age,
+                        int32_t* __restrict__ bdelta) {
   const int32_t j = blockIdx.x * kBlock + threadIdx.x;
   if (j >= m || !accepted[j]) return;
   const int32_t b = winner[j], s = second[j];
   if (!pair_ok(b, s, n)) return;
-  mark_signal(b, s, rp, col, age, ins, orphan, status, max_age);
+  mark_signal(b, s, rp, col, age, ins, orphan, status, max_age, bdelta);
 }
 
 // The lock-set resolve of rs_check fused with the update of the accepted signals (the
@@ -284,6 +292,7 @@ struct FusedArgs {
   int32_t* status;
   int32_t max_age;
   int32_t* apart;  // accepted signals of each workgroup (plain stores)
+  int32_t* bdelta;  // change of the half-edge count of every block of kBlock units
 };
 
 // The fused kernels give each signal a group of kGroup lanes of one wave: lane q takes the
@@ -408,6 +417,8 @@ __global__ void fu_check_apply(FusedArgs a) {
             move(s, a.eps_n, tx, ty, tz);
             a.ins[b] = s;
             a.ins[s] = b;
+            atomicAdd(&a.bdelta[b / kBlock], 1);
+            atomicAdd(&a.bdelta[s / kBlock], 1);
           }
           a.err[b] = be + dj;
         }
@@ -424,7 +435,11 @@ __global__ void fu_check_apply(FusedArgs a) {
             continue;
           }
           a.age[k] = kDead;
-          if (rk >= 0) a.age[rk] = kDead;
+          atomicAdd(&a.bdelta[b / kBlock], -1);
+          if (rk >= 0) {
+            a.age[rk] = kDead;
+            atomicAdd(&a.bdelta[v / kBlock], -1);
+          }
           bool live = a.ins[v] >= 0;
           for (int32_t kk = a.rp[v]; !live && kk < a.rp[v + 1]; ++kk) live = a.age[kk] != kDead;
           if (!live && !a.orphan[v]) {
@@ -456,8 +471,10 @@ __global__ void ed_count(int32_t n, const int32_t* __restrict__ rp,
                          int32_t* __restrict__ cnt, int32_t* __restrict__ bsum,
                          float* __restrict__ err, float beta,
                          const int32_t* __restrict__ apart, int32_t napart,
-                         unsigned long long* __restrict__ acc) {
+                         unsigned long long* __restrict__ acc,
+                         int32_t* __restrict__ bdelta_next) {
   __shared__ int32_t wt[2][kBlock / 64];
+  if (threadIdx.x == 0) bdelta_next[blockIdx.x] = 0;
   if (apart != nullptr && blockIdx.x == 0) {
     int32_t v = 0;
     for (int32_t i = threadIdx.x; i < napart; i += kBlock) v += apart[i];
@@ -601,12 +618,110 @@ __global__ void ed_write(int32_t n, const int32_t* __restrict__ rp,
   }
 }
 
+// The rewrite without a separate count (up to kFoldBlocks workgroups): the marking kernels
+// added, for every block of kBlock units, the change of its half-edge count (+1 for each
+// requested edge, -1 for each half-edge marked dead) to bdelta, so the new start of block
+// b is the old start rp[kBlock b] plus the changes of the blocks before it (every workgroup
+// sums them itself), and the new total is rp[n] plus all changes.  Each thread counts its
+// own row's live entries and request, a block scan places the rows, and the row is written
+// as in ed_write.  Also the error decay (err not null), the per-workgroup accepted counts of
+// the fused check (apart not null, workgroup 0), and zeroing of the other delta array for
+// the next update (every workgroup its own entry).
+__global__ void ed_rewrite(int32_t n, const int32_t* __restrict__ rp,
+                           const int32_t* __restrict__ col, const int32_t* __restrict__ age,
+                           int32_t* __restrict__ ins, const int32_t* __restrict__ bdelta,
+                           int32_t* __restrict__ bdelta_next, int32_t* __restrict__ rp_new,
+                           int32_t* __restrict__ col_new, int32_t* __restrict__ age_new,
+                           int32_t* __restrict__ status, int32_t nb, int64_t cap,
+                           float* __restrict__ err, float beta,
+                           const int32_t* __restrict__ apart, int32_t napart,
+                           unsigned long long* __restrict__ acc) {
+  __shared__ int32_t wt[kBlock / 64];
+  __shared__ int32_t wa[kBlock / 64];
+  __shared__ int32_t red[2 * kBlock / 64];
+  const int32_t u = blockIdx.x * kBlock + threadIdx.x;
+  const bool in = u < n;
+  // the row (slots past its end repeat the last entry), the request, the error and the old
+  // start of the block, all loaded before any is waited for
+  const int32_t r0 = in ? rp[u] : 0, r1 = in ? rp[u + 1] : 0, l = r1 - r0;
+  const int32_t extra = in ? ins[u] : -1;
+  const float e = in && err ? err[u] : 0.0f;
+  const int32_t base = rp[blockIdx.x * kBlock];
+  int32_t cv[kShortRow], gv[kShortRow];
+  const bool short_row = l > 0 && l <= kShortRow;
+  if (short_row) {
+#pragma unroll
+    for (int k = 0; k < kShortRow; ++k) {
+      cv[k] = col[r0 + min(k, l - 1)];
+      gv[k] = age[r0 + min(k, l - 1)];
+    }
+  }
+  int32_t c = extra >= 0 ? 1 : 0;
+  if (short_row) {
+#pragma unroll
+    for (int k = 0; k < kShortRow; ++k) c += k < l && gv[k] != kDead;
+  } else {
+    for (int32_t k = r0; k < r1; ++k) c += age[k] != kDead;
+  }
+  if (apart != nullptr && blockIdx.x == 0) {
+    int32_t v = 0;
+    for (int32_t i = threadIdx.x; i < napart; i += kBlock) v += apart[i];
+    v = block_sum(v, wa);
+    if (threadIdx.x == 0 && v != 0) atomicAdd(acc, static_cast<unsigned long long>(v));
+  }
+  int32_t before, dtotal;
+  fold_offsets(bdelta, nb, red, &before, &dtotal);
+  const int32_t abort = fold_abort(rp[n] + dtotal, cap, status, rp_new + n);
+  const int32_t inc = block_inclusive_scan(c, wt);
+  if (threadIdx.x == 0) bdelta_next[blockIdx.x] = 0;
+  if (!in) return;
+  if (err) err[u] = e * beta;
+  ins[u] = -1;
+  if (abort) {
+    // the rewrite did not fit: leave a valid, empty adjacency (state is flagged invalid)
+    rp_new[u] = 0;
+    return;
+  }
+  const int32_t start = base + before + inc - c;
+  rp_new[u] = start;
+  int32_t o = start;
+  bool pending = extra >= 0;
+  auto put = [&](int32_t v, int32_t g) {
+    if (g == kDead) return;
+    if (pending && extra < v) {
+      col_new[o] = extra;
+      age_new[o] = 0;
+      ++o;
+      pending = false;
+    }
+    col_new[o] = v;
+    age_new[o] = g;
+    ++o;
+  };
+  if (short_row) {
+#pragma unroll
+    for (int k = 0; k < kShortRow; ++k)
+      if (k < l) put(cv[k], gv[k]);
+  } else {
+    for (int32_t k = r0; k < r1; ++k) put(col[k], age[k]);
+  }
+  if (pending) {
+    col_new[o] = extra;
+    age_new[o] = 0;
+  }
+}
+
 __global__ void init_state(float* __restrict__ err, int32_t* __restrict__ ins,
                            int32_t* __restrict__ orphan, int32_t* __restrict__ rp,
                            unsigned long long* __restrict__ lock, int32_t* __restrict__ extra,
                            int32_t* __restrict__ rem, unsigned long long* __restrict__ acc64,
-                           int32_t n_max, int32_t* __restrict__ status) {
+                           int32_t n_max, int32_t* __restrict__ status,
+                           int32_t* __restrict__ bd0, int32_t* __restrict__ bd1) {
   const int32_t i = blockIdx.x * kBlock + threadIdx.x;
+  if (i < n_max / kBlock + 2) {
+    bd0[i] = 0;
+    bd1[i] = 0;
+  }
   if (i < n_max) {
     err[i] = 0.0f;
     ins[i] = -1;
@@ -628,7 +743,8 @@ hipError_t launch_init(const DevState& s, int cur, int32_t, int32_t n_max, hipSt
   const int64_t cover =
       std::max<int64_t>(static_cast<int64_t>(n_max) + 1, std::max<int>(kStSlots, kRmSlots));
   init_state<<<blocks(cover), kBlock, 0, st>>>(s.err, s.ins, s.orphan, s.rp[cur], s.lock,
-                                               s.extra, s.rem, s.acc64, n_max, s.status);
+                                               s.extra, s.rem, s.acc64, n_max, s.status,
+                                               s.bdelta[0], s.bdelta[1]);
   return hipGetLastError();
 }
 
@@ -656,58 +772,70 @@ hipError_t launch_adapt(const DevState& s, int cur, int32_t n, const float* sig,
   return hipGetLastError();
 }
 
-hipError_t launch_edges(const DevState& s, int cur, int32_t n, int32_t m,
+hipError_t launch_edges(const DevState& s, int cur, int dpar, int32_t n, int32_t m,
                         const int32_t* winner, const int32_t* second,
                         const uint8_t* accepted, int32_t max_age, int64_t half_cap,
                         hipStream_t st) {
   const int nxt = cur ^ 1;
+  int32_t* bd = s.bdelta[dpar];
+  int32_t* bd_next = s.bdelta[dpar ^ 1];
   if (m > 0)
     ed_mark<<<blocks(m), kBlock, 0, st>>>(m, n, winner, second, accepted, s.rp[cur],
                                           s.col[cur], s.age[cur], s.ins, s.orphan, s.status,
-                                          max_age);
+                                          max_age, bd);
   const int nb = blocks(n);
-  const int fold = nb > 0 && nb <= kFoldBlocks;
-  if (n > 0)
-    ed_count<<<nb, kBlock, 0, st>>>(n, s.rp[cur], s.age[cur], s.ins, s.cnt, s.bsum, nullptr,
-                                    1.0f, nullptr, 0, nullptr);
-  if (!fold) scan_blocks<<<1, 1024, 0, st>>>(s.bsum, nb, half_cap, s.rp[nxt] + n, s.status, -1);
-  if (n > 0)
-    ed_write<<<nb, kBlock, 0, st>>>(n, s.rp[cur], s.col[cur], s.age[cur], s.ins, s.cnt,
-                                    s.bsum, s.rp[nxt], s.col[nxt], s.age[nxt], s.status, fold,
-                                    nb, half_cap, s.rp[nxt] + n);
+  if (n == 0) return hipGetLastError();
+  if (nb <= kFoldBlocks) {
+    ed_rewrite<<<nb, kBlock, 0, st>>>(n, s.rp[cur], s.col[cur], s.age[cur], s.ins, bd, bd_next,
+                                      s.rp[nxt], s.col[nxt], s.age[nxt], s.status, nb, half_cap,
+                                      nullptr, 1.0f, nullptr, 0, nullptr);
+    return hipGetLastError();
+  }
+  ed_count<<<nb, kBlock, 0, st>>>(n, s.rp[cur], s.age[cur], s.ins, s.cnt, s.bsum, nullptr,
+                                  1.0f, nullptr, 0, nullptr, bd_next);
+  scan_blocks<<<1, 1024, 0, st>>>(s.bsum, nb, half_cap, s.rp[nxt] + n, s.status, -1);
+  ed_write<<<nb, kBlock, 0, st>>>(n, s.rp[cur], s.col[cur], s.age[cur], s.ins, s.cnt, s.bsum,
+                                  s.rp[nxt], s.col[nxt], s.age[nxt], s.status, 0, nb, half_cap,
+                                  s.rp[nxt] + n);
   return hipGetLastError();
 }
 
-hipError_t launch_iterate_set(const DevState& s, int cur, int32_t n, const float* sig,
+hipError_t launch_iterate_set(const DevState& s, int cur, int dpar, int32_t n, const float* sig,
                               int32_t m, const int32_t* winner, const int32_t* second,
                               const float* d1, uint8_t* accepted, int key_mode, float eps_b,
                               float eps_n, float beta, int32_t max_age, int64_t half_cap,
                               bool claimed, hipStream_t st) {
   const int nxt = cur ^ 1;
+  int32_t* bd = s.bdelta[dpar];
+  int32_t* bd_next = s.bdelta[dpar ^ 1];
+  const int gb = blocks(static_cast<int64_t>(m) * kGroup);
   if (m > 0) {
-    const int gb = blocks(static_cast<int64_t>(m) * kGroup);
     if (!claimed)
       fu_claim<<<gb, kBlock, 0, st>>>(m, n, winner, second, d1, s.rp[cur], s.col[cur], s.lock,
                                       s.status, key_mode);
     FusedArgs a{sig,      m,          n,          winner,  second,   d1,     key_mode,
                 s.rp[cur], s.col[cur], s.lock,     accepted, s.acc64, s.x,    s.y,
                 s.z,      s.err,      eps_b,      eps_n,   s.age[cur], s.ins, s.orphan,
-                s.status, max_age, s.apart};
+                s.status, max_age, s.apart, bd};
     fu_check_apply<<<gb, kBlock, 0, st>>>(a);
   }
+  // (with no units no signal is accepted, so skipping the rewrite loses nothing)
+  if (n == 0) return hipGetLastError();
   const int nb = blocks(n);
-  const int fold = nb > 0 && nb <= kFoldBlocks;
-  // (with no units no signal is accepted, so skipping the count loses nothing)
-  if (n > 0)
-    ed_count<<<nb, kBlock, 0, st>>>(n, s.rp[cur], s.age[cur], s.ins, s.cnt, s.bsum, s.err,
-                                    beta, m > 0 ? s.apart : nullptr,
-                                    blocks(static_cast<int64_t>(m) * kGroup),
-                                    s.acc64 + kA64Accepted);
-  if (!fold) scan_blocks<<<1, 1024, 0, st>>>(s.bsum, nb, half_cap, s.rp[nxt] + n, s.status, -1);
-  if (n > 0)
-    ed_write<<<nb, kBlock, 0, st>>>(n, s.rp[cur], s.col[cur], s.age[cur], s.ins, s.cnt,
-                                    s.bsum, s.rp[nxt], s.col[nxt], s.age[nxt], s.status, fold,
-                                    nb, half_cap, s.rp[nxt] + n);
+  if (nb <= kFoldBlocks) {
+    ed_rewrite<<<nb, kBlock, 0, st>>>(n, s.rp[cur], s.col[cur], s.age[cur], s.ins, bd, bd_next,
+                                      s.rp[nxt], s.col[nxt], s.age[nxt], s.status, nb, half_cap,
+                                      s.err, beta, m > 0 ? s.apart : nullptr, gb,
+                                      s.acc64 + kA64Accepted);
+    return hipGetLastError();
+  }
+  ed_count<<<nb, kBlock, 0, st>>>(n, s.rp[cur], s.age[cur], s.ins, s.cnt, s.bsum, s.err, beta,
+                                  m > 0 ? s.apart : nullptr, gb, s.acc64 + kA64Accepted,
+                                  bd_next);
+  scan_blocks<<<1, 1024, 0, st>>>(s.bsum, nb, half_cap, s.rp[nxt] + n, s.status, -1);
+  ed_write<<<nb, kBlock, 0, st>>>(n, s.rp[cur], s.col[cur], s.age[cur], s.ins, s.cnt, s.bsum,
+                                  s.rp[nxt], s.col[nxt], s.age[nxt], s.status, 0, nb, half_cap,
+                                  s.rp[nxt] + n);
   return hipGetLastError();
 }
 

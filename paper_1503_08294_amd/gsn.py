@@ -29,6 +29,7 @@ GSN_TUNE_SPLIT = 1
 GSN_TUNE_VARIANT = 2
 GSN_TUNE_GRID_ROUNDS = 3
 GSN_TUNE_GRAB = 4
+GSN_TUNE_REBUCKET = 5
 GSN_MAX_SPLIT = 64
 
 GSN_T_FIND_SCAN = 0
