@@ -29,7 +29,7 @@ enum StatusSlot {
 // Counters of the sequential-survivor update (int32 slots of DevState::rem): the signals
 // still pending after each grid-wide round, the survivors of the current call, and round
 // statistics accumulated until the host clears them.
-constexpr int kMaxGridRounds = 16;
+constexpr int kMaxGridRounds = 32;
 enum RoundSlot {
   kRmSurvivors = kMaxGridRounds,
   kRmRounds,       // rounds summed over the updates since the last clear

@@ -506,7 +506,7 @@ __global__ __launch_bounds__(kStepBlock) void wl_step(RoundArgs a, int32_t t) {
 // without progress ends it with an error.  Also adds this update's round count to the
 // statistics and clears the survivor count.
 __global__ __launch_bounds__(kTailBlock) void wl_tail(RoundArgs a, int32_t grid_rounds) {
-  __shared__ int32_t s_n, s_next, s_rounds;
+  __shared__ int32_t s_n, s_next, s_rounds, s_ran, s_big;
   const int tid = threadIdx.x;
   if (tid == 0) {
     // grid rounds that ran: the first, then each one after a round that left kTailMin or
@@ -515,9 +515,8 @@ __global__ __launch_bounds__(kTailBlock) void wl_tail(RoundArgs a, int32_t grid_
     while (ran < grid_rounds && a.rem[ran - 1] >= kTailMin) ++ran;
     s_rounds = ran > 0 && a.rem[kRmSurvivors] > 0 ? ran : 0;
     a.rem[kRmGridUsed] = ran;
-    // the host reads it when it enqueues a later update (a stale value only changes how
-    // the rounds are split); a store straight to its pinned word spares the stream a copy
-    if (a.feedback) __hip_atomic_store(a.feedback, ran, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    s_ran = ran;
+    s_big = 0;
     s_n = 0;
     s_next = 0;
   }
@@ -530,6 +529,8 @@ __global__ __launch_bounds__(kTailBlock) void wl_tail(RoundArgs a, int32_t grid_
   for (;;) {
     const int32_t n = s_n;
     if (n == 0) break;
+    // a round that starts with kTailMin or more pending would have run grid-wide
+    if (tid == 0 && n >= kTailMin) ++s_big;
     for (int32_t i = tid; i < n; i += kTailBlock) claim(a, cur[i]);
     __syncthreads();
     for (int32_t i = tid / kGroup; i < n; i += kTailBlock / kGroup) {
@@ -559,6 +560,12 @@ __global__ __launch_bounds__(kTailBlock) void wl_tail(RoundArgs a, int32_t grid_
     nxt = t;
   }
   if (tid == 0) {
+    // the grid-wide rounds this update could have used: those that ran, plus the rounds of
+    // this workgroup that started with kTailMin or more pending.  The host reads the count
+    // when it enqueues a later update (a stale value only changes how the rounds are split,
+    // never a result); a store straight to its pinned word spares the stream a copy.
+    if (a.feedback)
+      __hip_atomic_store(a.feedback, s_ran + s_big, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
     a.rem[kRmSurvivors] = 0;
     a.rem[kRmRounds] += s_rounds;
     a.rem[kRmRoundsMax] = max(a.rem[kRmRoundsMax], s_rounds);

@@ -45,7 +45,7 @@ def dense_pair(seed, n, e, m, key_mode, max_age=3, e_max=None, grid_rounds=None)
     return pair, rng
 
 
-@pytest.mark.parametrize("grid_rounds", [None, 0, 1, 16])
+@pytest.mark.parametrize("grid_rounds", [None, 0, 1, 16, 32])
 @pytest.mark.parametrize("key_mode", [0, 1])
 @pytest.mark.parametrize("seed,n,e,m", [(0, 30, 40, 200), (1, 200, 500, 1_000),
                                         (2, 1_000, 2_500, 4_096), (3, 12, 0, 64)])
