@@ -126,7 +126,7 @@ def oracle_phases_child(args):
                           cap["n_max"], cap["e_max"], m, lock_mode=args.phase_lock)
         o = oracle.Oracle(p, units, threads=1)
         stream = SignalStream(cloud, wl.signal_seed)
-        t = {"find": 0.0, "resolve": 0.0, "adapt": 0.0, "edges": 0.0}
+        t = {"find": 0.0, "resolve": 0.0, "adapt": 0.0, "edges": 0.0, "grow": 0.0}
         done = 0
         while done < args.phase_iters:
             sig = stream.next(m)
@@ -139,10 +139,14 @@ def oracle_phases_child(args):
             t3 = time.perf_counter()
             o.update_edges(w, sc, acc)
             t4 = time.perf_counter()
+            if wl.grow:
+                o.grow(done + 1, wl.insert_every)
+            t5 = time.perf_counter()
             t["find"] += t1 - t0
             t["resolve"] += t2 - t1
             t["adapt"] += t3 - t2
             t["edges"] += t4 - t3
+            t["grow"] += t5 - t4
             done += 1
             if sum(t.values()) > args.phase_budget:
                 break
@@ -172,7 +176,7 @@ def single_core_oracle(workload: str, ms, iters: int, budget_s: float, lock_mode
         cmd = ["taskset", "-c", str(cpu)] + cmd
     env = dict(os.environ, OMP_NUM_THREADS="1")
     r = subprocess.run(cmd, capture_output=True, text=True, env=env,
-                       timeout=120 + 3 * budget_s * len(ms))
+                       timeout=300 + 3 * budget_s * len(ms))
     if r.returncode != 0:
         print(r.stderr[-2000:], file=sys.stderr, flush=True)
         return {"error": f"oracle child exited with {r.returncode}"}
@@ -533,6 +537,10 @@ def main():
                     help="find calls between rebuilds of the unit order (GSN_TUNE_REBUCKET)")
     ap.add_argument("--no-late-window", action="store_true",
                     help="skip the record of iterations 81-100")
+    ap.add_argument("--oracle-iters", type=int, default=3,
+                    help="iterations of the single-core oracle timing (bounded by its budget)")
+    ap.add_argument("--oracle-budget", type=float, default=0.0,
+                    help="seconds of single-core oracle work (0 = min(cpu-budget, 8))")
     # child-process mode of the single-core oracle timing (no GPU)
     ap.add_argument("--oracle-phases", action="store_true", help=argparse.SUPPRESS)
     ap.add_argument("--phase-m", default="", help=argparse.SUPPRESS)
@@ -572,7 +580,8 @@ def main():
     if args.cpu_budget > 0:
         # before this process touches the GPU: a pinned child process, one core
         print("[bench] single-core oracle per phase (pinned)", file=sys.stderr, flush=True)
-        single = single_core_oracle(wl.name, [wl.m], 3, min(args.cpu_budget, 8.0))
+        single = single_core_oracle(wl.name, [wl.m], args.oracle_iters,
+                                    args.oracle_budget or min(args.cpu_budget, 8.0))
 
     import torch
 

@@ -215,10 +215,11 @@ int gsn_update_edges(gsn_net* net, int32_t m, const int32_t* winner, const int32
 /* One whole iteration (Sec. 2.2: find winners, resolve, adapt, update edges) in one call:
  * the outputs and the state afterwards are those of the four calls above in order (same
  * order rules: it starts like gsn_find_winners and leaves the handle ready for gsn_grow).
- * With GSN_LOCK_SET the update runs fused: resolve's check applies each accepted signal's
- * adaptation and edge marks at once (accepted lock sets are disjoint) and the error decay
- * rides on the degree count, five launches instead of eight.  The other rules run the
- * four steps.  Outputs: device arrays of length m.  Async. */
+ * With GSN_LOCK_SET the update runs fused: the find's merge makes the claims, resolve's
+ * check applies each accepted signal's adaptation and edge marks at once (accepted lock
+ * sets are disjoint), and one rewrite of the adjacency applies the error decay: two update
+ * launches after the find instead of six.  The other rules run the four steps.  Outputs:
+ * device arrays of length m.  Async. */
 int gsn_iterate(gsn_net* net, const float* sig, int32_t m, int32_t* winner, int32_t* second,
                 float* d1, float* d2, uint8_t* accepted, void* stream);
 
