@@ -350,21 +350,29 @@ def tune(gsn, net, args):
         net.tune(gsn.GSN_TUNE_REBUCKET, args.rebucket)
 
 
+SCAN_TIMER_EVERY = 4   # inside the timed steps the scan carries an event pair every 4th step
+
+
 def timed_steps(torch, gsn, net, step, first, count, scan_only=True):
     """Runs steps first .. first+count-1 between two synchronizations.  With scan_only the
-    scan's HIP event pair is the only timer inside the window, else every phase timer
-    records.  Returns the elapsed seconds, {timer: (mean ms per launch, launches)}, and
-    the resolved and accepted signal counts."""
+    scan's HIP event pair is the only timer inside the window, recorded on every
+    SCAN_TIMER_EVERY-th step (each pair of markers idles the stream a few microseconds), else
+    every phase timer records on every step.  Returns the elapsed seconds, {timer: (mean ms
+    per launch, launches)}, and the resolved and accepted signal counts."""
     for w in range(gsn.GSN_T_COUNT):
         gsn.gsn_timing_read(net.h, w)
     gsn.gsn_timing_select(net.h, (1 << gsn.GSN_T_FIND_SCAN) if scan_only
                           else (1 << gsn.GSN_T_COUNT) - 1)
     torch.cuda.synchronize()
     net.stat(gsn.GSN_STAT_CLEAR)
-    gsn.gsn_timing_enable(net.h, True)
+    every = SCAN_TIMER_EVERY if scan_only else 1
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for t in range(first, first + count):
+        if every > 1:
+            gsn.gsn_timing_enable(net.h, (t - first) % every == 0)
+        else:
+            gsn.gsn_timing_enable(net.h, True)
         step(t)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
