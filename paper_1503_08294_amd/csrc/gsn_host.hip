@@ -400,8 +400,9 @@ namespace {
 // merge does not).
 int find_impl(gsn_net* net, const float* sig, int32_t m, int32_t* winner, int32_t* second,
               float* d1, float* d2, void* stream, const gsn::ClaimArgs* claim,
-              bool* claimed) {
+              bool* claimed, const int32_t** order = nullptr) {
   if (claimed) *claimed = false;
+  if (order) *order = nullptr;
   if (!net || m < 0 || m > net->p.m_max) return GSN_E_INVAL;
   if (net->phase != kReady && net->phase != kFound) return GSN_E_STATE;
   if (net->n < 2) return GSN_E_INVAL;
@@ -446,6 +447,7 @@ int find_impl(gsn_net* net, const float* sig, int32_t m, int32_t* winner, int32_
     if (e == hipSuccess) {
       e = gsn::launch_stage_merge(net->s, sb, m, cfg.split, winner, second, d1, d2, claim, st);
       if (claimed) *claimed = claim != nullptr;
+      if (order) *order = sb.sperm;  // the signals' spatial order of this call
     }
   } else {
     TimedRegion scan(net, GSN_T_FIND_SCAN, st);
@@ -624,7 +626,8 @@ int gsn_iterate(gsn_net* net, const float* sig, int32_t m, int32_t* winner, int3
   const gsn::ClaimArgs claim{net->n, net->s.rp[net->cur], net->s.col[net->cur], net->s.lock,
                              net->s.status, net->p.key_mode};
   bool claimed = false;
-  int rc = find_impl(net, sig, m, winner, second, d1, d2, stream, &claim, &claimed);
+  const int32_t* order = nullptr;
+  int rc = find_impl(net, sig, m, winner, second, d1, d2, stream, &claim, &claimed, &order);
   if (rc) return rc;
   hipStream_t st = as_stream(stream);
   TimedRegion t(net, GSN_T_UPDATE, st);
@@ -632,7 +635,7 @@ int gsn_iterate(gsn_net* net, const float* sig, int32_t m, int32_t* winner, int3
       net->s, net->cur, net->dpar, net->n, sig, m, winner, second, d1, accepted,
       net->p.key_mode,
       net->p.eps_b, net->p.eps_n, net->p.err_beta, net->p.max_age,
-      2 * static_cast<int64_t>(net->p.e_max), claimed, st);
+      2 * static_cast<int64_t>(net->p.e_max), claimed, order, st);
   t.end();
   if (e != hipSuccess) return GSN_E_HIP;
   net->cur ^= 1;

@@ -293,6 +293,7 @@ struct FusedArgs {
   int32_t max_age;
   int32_t* apart;  // accepted signals of each workgroup (plain stores)
   int32_t* bdelta;  // change of the half-edge count of every block of kBlock units
+  const int32_t* order;  // optional: the signals in a spatial order (a permutation of 0..m-1)
 };
 
 // The fused kernels give each signal a group of kGroup lanes of one wave: lane q takes the
@@ -347,10 +348,15 @@ __global__ void fu_check_apply(FusedArgs a) {
   if (threadIdx.x == 0) s_acc = 0;
   __syncthreads();
   const int32_t gt = blockIdx.x * kBlock + threadIdx.x;
-  const int32_t j = gt / kGroup;
+  // Signal j of the group.  The outcome of every signal does not depend on which group takes
+  // it (the claims are all made before this launch and accepted lock sets are disjoint), so
+  // with a spatial order the groups of a workgroup take nearby signals, whose lock words,
+  // positions and rows share cache lines.
+  const int32_t p = gt / kGroup;
   const int q = gt % kGroup;
+  const int32_t j = p < a.m && a.order ? a.order[p] : p;
   bool ok = false;
-  if (j < a.m) {
+  if (p < a.m && j >= 0 && j < a.m) {
     const int32_t b = a.winner[j], s = a.second[j];
     const float dj = a.d1[j];
     const float sx = a.sig[j], sy = a.sig[a.m + j], sz = a.sig[2 * a.m + j];
@@ -804,7 +810,7 @@ hipError_t launch_iterate_set(const DevState& s, int cur, int dpar, int32_t n, c
                               int32_t m, const int32_t* winner, const int32_t* second,
                               const float* d1, uint8_t* accepted, int key_mode, float eps_b,
                               float eps_n, float beta, int32_t max_age, int64_t half_cap,
-                              bool claimed, hipStream_t st) {
+                              bool claimed, const int32_t* order, hipStream_t st) {
   const int nxt = cur ^ 1;
   int32_t* bd = s.bdelta[dpar];
   int32_t* bd_next = s.bdelta[dpar ^ 1];
@@ -816,7 +822,7 @@ hipError_t launch_iterate_set(const DevState& s, int cur, int dpar, int32_t n, c
     FusedArgs a{sig,      m,          n,          winner,  second,   d1,     key_mode,
                 s.rp[cur], s.col[cur], s.lock,     accepted, s.acc64, s.x,    s.y,
                 s.z,      s.err,      eps_b,      eps_n,   s.age[cur], s.ins, s.orphan,
-                s.status, max_age, s.apart, bd};
+                s.status, max_age, s.apart, bd, order};
     fu_check_apply<<<gb, kBlock, 0, st>>>(a);
   }
   // (with no units no signal is accepted, so skipping the rewrite loses nothing)
