@@ -223,6 +223,26 @@ int gsn_update_edges(gsn_net* net, int32_t m, const int32_t* winner, const int32
 int gsn_iterate(gsn_net* net, const float* sig, int32_t m, int32_t* winner, int32_t* second,
                 float* d1, float* d2, uint8_t* accepted, void* stream);
 
+/* count whole iterations (Sec. 2.2, the multi-signal loop) in one call: the result, the
+ * state afterwards and the outputs (those of the last iteration) are exactly those of count
+ * gsn_iterate calls in order over the batches sigs + 3 m k, k = 0 .. count - 1 (each batch
+ * laid out as gsn_iterate's sig; device memory, count x 3 x m floats, read by the device
+ * when the iterations run).  The launches of the whole loop are recorded once into a HIP
+ * graph and replayed: a later call with the same arguments and network state (unit count,
+ * tuning, which internal buffer set is current) replays the recorded graph without any
+ * per-launch host work, on the caller's stream.  Up to GSN_GRAPH_CACHE graphs are kept per
+ * handle (least recently used one replaced); they hold no memory of their own.  The only
+ * difference from the separate calls: the spatial unit order of the staged find is rebuilt
+ * at the first iteration when the rebuild would fall inside the loop, never later in it
+ * (the order affects speed only).  The event timers (gsn_timing_enable) do not record
+ * inside the loop.  count is 1 .. GSN_MAX_LOOP.  Errors as gsn_iterate (checked on the
+ * host before anything is recorded).  Async. */
+#define GSN_MAX_LOOP 4096
+#define GSN_GRAPH_CACHE 4
+int gsn_iterate_loop(gsn_net* net, const float* sigs, int32_t m, int32_t count,
+                     int32_t* winner, int32_t* second, float* d1, float* d2,
+                     uint8_t* accepted, void* stream);
+
 /* Growth (Sec. 2.1: units may be added and removed during the update; GNG inserts next
  * to the unit of largest accumulated error).  First removes, by stable
  * compaction (indices shift down, edges are renumbered), every unit marked by

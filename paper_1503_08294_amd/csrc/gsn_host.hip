@@ -6,6 +6,7 @@
 #include <string.h>
 
 #include <cmath>
+#include <cstddef>
 #include <mutex>
 #include <new>
 #include <vector>
@@ -168,6 +169,31 @@ struct gsn_net {
   void* scratch_dev;           // device address of the no-allocation grid workspace
   std::vector<hipEvent_t> pool;
   std::vector<std::pair<hipEvent_t, hipEvent_t>> rec[GSN_T_COUNT];
+  // gsn_iterate_loop: recorded loops, the stream they are recorded on, and the recording
+  // state (event timers off; the unit-order rule of the first staged find overridden)
+  struct LoopGraph {
+    // what the recorded launches depend on
+    const float* sigs;
+    int32_t m, count;
+    int32_t *winner, *second;
+    float *d1, *d2;
+    uint8_t* accepted;
+    int32_t n;
+    int cur, dpar, stage_parity;
+    bool rebuild_first;
+    int tune_split, tune_variant, tune_grab, tune_rebucket, grid_rounds;
+    // the host state the loop leaves
+    bool rebuilt;   // the first find rebuilt the unit order (else finds_delta counts finds)
+    int cur_after, dpar_after, stage_parity_after;
+    int32_t finds_after, finds_delta, bucket_n_after;
+    hipGraphExec_t exec;
+    uint64_t used;
+  };
+  std::vector<LoopGraph> graphs;
+  uint64_t graph_clock;
+  hipStream_t cap_stream;
+  bool capturing;
+  int loop_rebuild;   // -1, or the unit-order decision (0/1) of the next staged find
 };
 
 namespace {
@@ -229,7 +255,7 @@ struct TimedRegion {
   hipStream_t st;
   hipEvent_t a = nullptr;
   TimedRegion(gsn_net* n, int w, hipStream_t s) : net(n), which(w), st(s) {
-    if (net->timing && ((net->timing_mask >> w) & 1u)) {
+    if (net->timing && !net->capturing && ((net->timing_mask >> w) & 1u)) {
       a = take_event(net);
       if (a && hipEventRecord(a, st) != hipSuccess) {
         net->pool.push_back(a);
@@ -348,6 +374,10 @@ int gsn_create(const gsn_params* params, void* workspace, size_t workspace_bytes
   net->bucket_n = -1;
   net->finds_since_bucket = 0;
   net->grid_rounds = 0;
+  net->graph_clock = 0;
+  net->cap_stream = nullptr;
+  net->capturing = false;
+  net->loop_rebuild = -1;
   net->feedback = nullptr;
   if (hipHostMalloc(reinterpret_cast<void**>(&net->feedback), sizeof(int32_t)) != hipSuccess) {
     delete net;
@@ -425,7 +455,11 @@ int find_impl(gsn_net* net, const float* sig, int32_t m, int32_t* winner, int32_
   } else if (cfg.variant >= 2) {
     const gsn::StageBufs sb = gsn::carve_stage(net->s.scr, net->p.n_max, net->p.m_max);
     // the unit order is rebuilt when the network changed and every kRebucketEvery calls
-    const bool rebucket = net->bucket_n != net->n || net->finds_since_bucket >= net->tune_rebucket;
+    bool rebucket = net->bucket_n != net->n || net->finds_since_bucket >= net->tune_rebucket;
+    if (net->loop_rebuild >= 0) {  // the first staged find of a recorded loop
+      rebucket = net->loop_rebuild == 1;
+      net->loop_rebuild = -1;
+    }
     e = gsn::launch_stage(net->s, sb, net->n, sig, m, rebucket, net->stage_parity,
                           cfg.variant, st);
     net->stage_parity ^= 1;
@@ -640,6 +674,113 @@ int gsn_iterate(gsn_net* net, const float* sig, int32_t m, int32_t* winner, int3
   if (e != hipSuccess) return GSN_E_HIP;
   net->cur ^= 1;
   net->dpar ^= 1;
+  net->phase = kReady;
+  return GSN_OK;
+}
+
+int gsn_iterate_loop(gsn_net* net, const float* sigs, int32_t m, int32_t count,
+                     int32_t* winner, int32_t* second, float* d1, float* d2,
+                     uint8_t* accepted, void* stream) {
+  if (!net || count < 1 || count > GSN_MAX_LOOP || m < 0 || m > net->p.m_max)
+    return GSN_E_INVAL;
+  if (net->phase != kReady && net->phase != kFound) return GSN_E_STATE;
+  if (net->n < 2) return GSN_E_INVAL;
+  if (m > 0 && (!sigs || !winner || !second || !d1 || !d2 || !accepted)) return GSN_E_INVAL;
+  hipStream_t st = as_stream(stream);
+  // the unit order is rebuilt at the first iteration if the usual rule would rebuild it
+  // anywhere inside the loop (after that the usual rule applies, from a fresh count)
+  const bool rebuild_first =
+      net->bucket_n != net->n || net->finds_since_bucket + count > net->tune_rebucket;
+  using LoopGraph = gsn_net::LoopGraph;
+  auto same = [&](const LoopGraph& g) {
+    return g.sigs == sigs && g.m == m && g.count == count && g.winner == winner &&
+           g.second == second && g.d1 == d1 && g.d2 == d2 && g.accepted == accepted &&
+           g.n == net->n && g.cur == net->cur && g.dpar == net->dpar &&
+           g.stage_parity == net->stage_parity && g.rebuild_first == rebuild_first &&
+           g.tune_split == net->tune_split && g.tune_variant == net->tune_variant &&
+           g.tune_grab == net->tune_grab && g.tune_rebucket == net->tune_rebucket &&
+           g.grid_rounds == net->grid_rounds;
+  };
+  LoopGraph* hit = nullptr;
+  for (auto& g : net->graphs)
+    if (same(g)) hit = &g;
+  if (!hit) {
+    if (!net->cap_stream &&
+        hipStreamCreateWithFlags(&net->cap_stream, hipStreamNonBlocking) != hipSuccess) {
+      net->cap_stream = nullptr;
+      return GSN_E_HIP;
+    }
+    LoopGraph g{};
+    g.sigs = sigs; g.m = m; g.count = count;
+    g.winner = winner; g.second = second; g.d1 = d1; g.d2 = d2; g.accepted = accepted;
+    g.n = net->n; g.cur = net->cur; g.dpar = net->dpar; g.stage_parity = net->stage_parity;
+    g.rebuild_first = rebuild_first;
+    g.tune_split = net->tune_split; g.tune_variant = net->tune_variant;
+    g.tune_grab = net->tune_grab; g.tune_rebucket = net->tune_rebucket;
+    g.grid_rounds = net->grid_rounds;
+    // record the loop: the calls run on the host as usual (argument checks, state), their
+    // launches go into the graph
+    const int cur0 = net->cur, dpar0 = net->dpar, sp0 = net->stage_parity, phase0 = net->phase;
+    const int32_t bn0 = net->bucket_n, f0 = net->finds_since_bucket;
+    (void)hipGetLastError();
+    if (hipStreamBeginCapture(net->cap_stream, hipStreamCaptureModeThreadLocal) != hipSuccess)
+      return GSN_E_HIP;
+    net->capturing = true;
+    net->loop_rebuild = rebuild_first ? 1 : 0;
+    int rc = GSN_OK;
+    for (int32_t k = 0; k < count && rc == GSN_OK; ++k)
+      rc = gsn_iterate(net, sigs ? sigs + 3 * static_cast<size_t>(m) * k : nullptr, m, winner,
+                       second, d1, d2, accepted, net->cap_stream);
+    net->capturing = false;
+    // a staged find consumed the unit-order decision; other finds leave the order alone
+    const bool rebuilt = rebuild_first && net->loop_rebuild == -1;
+    net->loop_rebuild = -1;
+    hipGraph_t graph = nullptr;
+    const hipError_t ec = hipStreamEndCapture(net->cap_stream, &graph);
+    hipGraphExec_t exec = nullptr;
+    if (rc == GSN_OK && ec == hipSuccess && graph &&
+        hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0) != hipSuccess) {
+      exec = nullptr;
+    }
+    if (graph) (void)hipGraphDestroy(graph);
+    if (rc != GSN_OK || !exec) {
+      // nothing ran: the handle is as before the call
+      net->cur = cur0; net->dpar = dpar0; net->stage_parity = sp0; net->phase = phase0;
+      net->bucket_n = bn0; net->finds_since_bucket = f0;
+      (void)hipGetLastError();
+      return rc != GSN_OK ? rc : GSN_E_HIP;
+    }
+    g.exec = exec;
+    g.rebuilt = rebuilt;
+    g.cur_after = net->cur; g.dpar_after = net->dpar;
+    g.stage_parity_after = net->stage_parity;
+    g.finds_after = net->finds_since_bucket;
+    g.finds_delta = net->finds_since_bucket - f0;
+    g.bucket_n_after = net->bucket_n;
+    // the host state is back at the start until the graph is launched below
+    net->cur = cur0; net->dpar = dpar0; net->stage_parity = sp0;
+    net->bucket_n = bn0; net->finds_since_bucket = f0;
+    if (net->graphs.size() >= GSN_GRAPH_CACHE) {
+      size_t old = 0;
+      for (size_t i = 1; i < net->graphs.size(); ++i)
+        if (net->graphs[i].used < net->graphs[old].used) old = i;
+      (void)hipGraphExecDestroy(net->graphs[old].exec);
+      net->graphs.erase(net->graphs.begin() + static_cast<std::ptrdiff_t>(old));
+    }
+    net->graphs.push_back(g);
+    hit = &net->graphs.back();
+  }
+  hit->used = ++net->graph_clock;
+  if (hipGraphLaunch(hit->exec, st) != hipSuccess) return GSN_E_HIP;
+  net->cur = hit->cur_after;
+  net->dpar = hit->dpar_after;
+  net->stage_parity = hit->stage_parity_after;
+  if (hit->rebuilt) {
+    net->finds_since_bucket = hit->finds_after;
+    net->bucket_n = hit->bucket_n_after;
+  } else {
+    net->finds_since_bucket += hit->finds_delta;
+  }
   net->phase = kReady;
   return GSN_OK;
 }
@@ -878,6 +1019,8 @@ int gsn_check(gsn_net* net, void* stream) {
 
 void gsn_destroy(gsn_net* net) {
   if (!net) return;
+  for (auto& g : net->graphs) (void)hipGraphExecDestroy(g.exec);
+  if (net->cap_stream) (void)hipStreamDestroy(net->cap_stream);
   for (auto& v : net->rec)
     for (auto& pr : v) {
       (void)hipEventDestroy(pr.first);

@@ -47,6 +47,8 @@ GSN_KEY_DIST_INDEX = 0
 GSN_KEY_INDEX = 1
 
 GSN_NOALLOC_SCRATCH_BYTES = 32 << 20
+GSN_MAX_LOOP = 4096
+GSN_GRAPH_CACHE = 4
 
 GSN_STAT_ROUNDS = 0
 GSN_STAT_ROUNDS_MAX = 1
@@ -133,6 +135,7 @@ _sig = {
     "gsn_adapt": (ctypes.c_int, [_P, _P, _I, _P, _P, _P, _P, _P]),
     "gsn_update_edges": (ctypes.c_int, [_P, _I, _P, _P, _P, _P]),
     "gsn_iterate": (ctypes.c_int, [_P, _P, _I, _P, _P, _P, _P, _P, _P]),
+    "gsn_iterate_loop": (ctypes.c_int, [_P, _P, _I, _I, _P, _P, _P, _P, _P, _P]),
     "gsn_grow": (ctypes.c_int, [_P, _I, _I, _P]),
     "gsn_run_schedule": (ctypes.c_int, [_P, _P, ctypes.c_int64, ctypes.POINTER(gsn_schedule),
                                         ctypes.POINTER(gsn_schedule_result), _P]),
@@ -341,6 +344,17 @@ def gsn_iterate(net, sig: torch.Tensor, m: int, winner, second, d1, d2, accepted
            "gsn_iterate")
 
 
+def gsn_iterate_loop(net, sigs: torch.Tensor, m: int, count: int, winner, second, d1, d2,
+                     accepted, stream=None):
+    _check(_lib.gsn_iterate_loop(net, _dev(sigs, torch.float32, 3 * m * count, "sigs"), m,
+                                 count, _dev(winner, torch.int32, m, "winner"),
+                                 _dev(second, torch.int32, m, "second"),
+                                 _dev(d1, torch.float32, m, "d1"),
+                                 _dev(d2, torch.float32, m, "d2"),
+                                 _dev(accepted, torch.uint8, m, "accepted"), _stream(stream)),
+           "gsn_iterate_loop")
+
+
 def make_schedule(m_cap=8192, fixed_m=0, insert_every=100, qe_window=8192,
                   max_signals=1 << 20, qe_threshold=0.0, seed=0) -> gsn_schedule:
     return gsn_schedule(m_cap, fixed_m, insert_every, qe_window, max_signals, qe_threshold,
@@ -499,6 +513,16 @@ class Network:
         m = sig.shape[1]
         b = self.buf
         gsn_iterate(self.h, sig, m, b.winner, b.second, b.d1, b.d2, b.accepted, self.stream)
+        return b.winner[:m], b.second[:m], b.d1[:m], b.d2[:m], b.accepted[:m]
+
+    def iterate_loop(self, sigs: torch.Tensor):
+        """One iteration per batch of ``sigs`` (a contiguous device (T, 3, m) tensor) in one
+        gsn_iterate_loop call (recorded into a HIP graph once, replayed afterwards); returns
+        the last iteration's outputs."""
+        count, _, m = sigs.shape
+        b = self.buf
+        gsn_iterate_loop(self.h, sigs, m, count, b.winner, b.second, b.d1, b.d2, b.accepted,
+                         self.stream)
         return b.winner[:m], b.second[:m], b.d1[:m], b.d2[:m], b.accepted[:m]
 
     def prepare_iterate(self, sigs):

@@ -77,6 +77,7 @@ def test_host_side_validation(lib):
                           ctypes.byref(h)) == -1                      # no positions
     for name, nargs in (("gsn_find_winners", 8), ("gsn_resolve_conflicts", 7),
                         ("gsn_adapt", 8), ("gsn_update_edges", 6), ("gsn_grow", 4),
+                        ("gsn_iterate", 9), ("gsn_iterate_loop", 10),
                         ("gsn_check", 2), ("gsn_tune", 3), ("gsn_timing_enable", 2),
                         ("gsn_timing_select", 2)):
         f = getattr(lib, name)

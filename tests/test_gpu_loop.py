@@ -1,0 +1,77 @@
+"""gsn_iterate_loop: count iterations recorded into a HIP graph once and replayed.  Every
+call leaves the state of count gsn_iterate calls (bit-exact against the oracle stepping
+the same batches) and the outputs of the last one, whether the call records a new graph or
+replays a cached one; eager calls between the loop calls change the handle's internal
+buffer parities, so later calls need other graphs; batch contents change between replays
+(the graph reads them when it runs)."""
+import numpy as np
+import pytest
+
+from parity import Pair, assert_iter_equal
+
+pytestmark = pytest.mark.gpu
+
+
+def run_loop_case(m, lock, counts, rebucket, seed, n=6_000):
+    import torch
+    from paper_1503_08294_amd import gsn
+    rng = np.random.default_rng(seed)
+    units = rng.standard_normal((3, n)).astype(np.float32)
+    pair = Pair(units, m_max=m, lock_mode=lock)
+    net = pair.net
+    if rebucket:
+        net.tune(gsn.GSN_TUNE_REBUCKET, rebucket)
+    bufs = {}
+    for call, count in enumerate(counts):
+        sigs = rng.standard_normal((count, 3, m)).astype(np.float32)
+        if count not in bufs:
+            bufs[count] = torch.empty((count, 3, m), dtype=torch.float32, device="cuda")
+        dev = bufs[count]
+        dev.copy_(pair.to_dev(sigs))          # same address, new contents
+        g = [t.cpu().numpy() for t in net.iterate_loop(dev)]
+        for k in range(count):
+            o = pair.orc.iterate(sigs[k], 0, 0, False)
+        where = f"m={m} lock={lock} call {call} count {count}"
+        assert_iter_equal(g, o, where + " (last iteration)")
+        pair.compare_state(where)
+        if call % 2 == 1:
+            # an eager iteration in between: the buffer parities change
+            extra = rng.standard_normal((3, m)).astype(np.float32)
+            g, o = pair.iterate(extra)
+            assert_iter_equal(g, o, where + " eager")
+    assert net.check() == 0
+    torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("m,lock,counts,rebucket", [
+    (2_000, 0, [4, 4, 4, 4, 3, 3, 3], 0),       # staged find, lock set; replays, odd counts
+    (2_000, 0, [4, 4, 4, 4], 3),                # the unit order rebuilt at every call's start
+    (2_000, 0, [1, 2, 3, 4, 5, 1, 2], 0),       # more graphs than the cache holds
+    (100, 0, [5, 5, 5, 2], 0),                  # unit-parallel small-batch find
+    (2_000, 1, [4, 4, 3, 3], 0),                # winner lock (the paper's rule)
+    (2_000, 2, [2, 2, 2], 0),                   # greedy re-admission
+])
+def test_loop_matches_the_oracle(m, lock, counts, rebucket):
+    run_loop_case(m, lock, counts, rebucket, seed=2000 + m + 10 * lock + rebucket)
+
+
+def test_loop_argument_errors():
+    from paper_1503_08294_amd import gsn
+    import torch
+    rng = np.random.default_rng(7)
+    pair = Pair(rng.standard_normal((3, 500)).astype(np.float32), m_max=64)
+    b = pair.net.buf
+    sigs = torch.zeros((2, 3, 64), dtype=torch.float32, device="cuda")
+    import ctypes
+    ptrs = [ctypes.c_void_p(t.data_ptr()) for t in (sigs, b.winner, b.second, b.d1, b.d2,
+                                                      b.accepted)]
+    for count in (0, -1, gsn.GSN_MAX_LOOP + 1):
+        # the C call itself (the binding would refuse the tensor size first)
+        rc = gsn._lib.gsn_iterate_loop(pair.net.h, ptrs[0], 64, count, *ptrs[1:],
+                                       ctypes.c_void_p(0))
+        assert rc == gsn.GSN_E_INVAL, count
+    # more signals than m_max
+    assert gsn._lib.gsn_iterate_loop(pair.net.h, ptrs[0], 65, 1, *ptrs[1:],
+                                     ctypes.c_void_p(0)) == gsn.GSN_E_INVAL
+    # nothing ran: the state is still the initial one
+    pair.compare_state("after rejected loop calls")
