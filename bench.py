@@ -353,6 +353,53 @@ def tune(gsn, net, args):
 SCAN_TIMER_EVERY = 4   # inside the timed steps the scan carries an event pair every 4th step
 
 
+def time_loop(torch, gsn, units, params, args, warm_batches, batches):
+    """The same iterations through gsn_iterate_loop on a second network from the same start:
+    the warm-up batches one gsn_iterate call each, a snapshot (gsn_export) imported back at
+    once (so that both loop calls below start from the host state an import leaves), one
+    loop call over ``batches`` (it records the loop's HIP graph and runs it: timed as the
+    first call), the snapshot imported again, and the same loop call again: a replay of the
+    recorded graph over the same iterations from the same state (the loop's rate; its end
+    state must equal the first call's bit for bit).  No event timers (they do not record
+    inside a loop)."""
+    import numpy as np
+    count, _, m = batches.shape
+    net = gsn.Network(params, torch.from_numpy(units).cuda())
+    tune(gsn, net, args)
+    for sig in warm_batches:
+        net.iterate(torch.from_numpy(np.ascontiguousarray(sig)).cuda())
+    snap = net.export()
+    net.import_state(snap["xyz"], snap["err"], snap["edges"])
+    buf = torch.from_numpy(np.ascontiguousarray(batches)).cuda()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    net.iterate_loop(buf)
+    torch.cuda.synchronize()
+    first_s = time.perf_counter() - t0
+    end1 = net.export()
+    records = net.stat(gsn.GSN_STAT_LOOP_RECORDS)
+    net.import_state(snap["xyz"], snap["err"], snap["edges"])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    net.iterate_loop(buf)
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
+    if net.check() != 0:
+        raise SystemExit(f"device status {net.check()} after the loop")
+    end2 = net.export()
+    same = all(torch.equal(end1[k], end2[k]) for k in ("xyz", "err", "edges"))
+    w = len(warm_batches)
+    rec = {"iterations": [w + 1, w + count],
+           "first_call_ms_per_step": 1e3 * first_s / count,
+           "replayed": net.stat(gsn.GSN_STAT_LOOP_RECORDS) == records,
+           "replay_equals_first_call": same,
+           "ms_per_step": 1e3 * el / count, "evals_per_s": m * units.shape[1] * count / el,
+           "signals_per_s": m * count / el, "edges_at_start": int(snap["edges"].shape[1]),
+           "edges_at_end": int(end2["edges"].shape[1])}
+    del net, buf
+    return rec
+
+
 def timed_steps(torch, gsn, net, step, first, count, scan_only=True):
     """Runs steps first .. first+count-1 between two synchronizations.  With scan_only the
     scan's HIP event pair is the only timer inside the window, recorded on every
@@ -469,6 +516,11 @@ def run_sweep(args):
                 step(t)
             el, timers, resolved, accepted = timed_steps(torch, gsn, net, step, warm, steps)
             scan_ms, launches = timers[gsn.GSN_T_FIND_SCAN]
+            loop_rec = None
+            if not args.no_loop:
+                host = dev_sig.cpu().numpy()
+                loop_rec = time_loop(torch, gsn, units, params, args, host[:warm],
+                                     host[warm:warm + steps])
             rec = {
                 "metric": "sweep: signals/s and conflict rate vs m at 1 GPU",
                 "value": m * steps / el, "unit": "signals/s", "n_gpus": 1,
@@ -484,6 +536,7 @@ def run_sweep(args):
                 "conflict_rate": 1.0 - accepted / max(resolved, 1),
                 "roofline": scan_roofline(m, n, scan_ms, launches, None),
                 "state_after": dict(zip(("units", "edges"), net.sizes())),
+                "loop": loop_rec,
             }
             if lock_mode == gsn.GSN_LOCK_WINNER:
                 rec["birthday_conflict_rate"] = birthday_conflict_rate(n, m)
@@ -543,6 +596,8 @@ def main():
                     help="batches per grab of the dynamic scan (GSN_TUNE_GRAB; 0 = default)")
     ap.add_argument("--rebucket", type=int, default=0,
                     help="find calls between rebuilds of the unit order (GSN_TUNE_REBUCKET)")
+    ap.add_argument("--no-loop", action="store_true",
+                    help="skip the record of the same iterations run through gsn_iterate_loop")
     ap.add_argument("--no-late-window", action="store_true",
                     help="skip the record of iterations 81-100")
     ap.add_argument("--oracle-iters", type=int, default=3,
@@ -720,6 +775,12 @@ def main():
                     "scan_avg_launch_ms": lt[gsn.GSN_T_FIND_SCAN][0],
                     "edges_at_start": e0, "edges_at_end": net.sizes()[1]}
 
+    loop_rec = None
+    if grid is None and not wl.grow and not args.no_loop:
+        count = min(args.steps, gsn.GSN_MAX_LOOP)
+        loop_rec = time_loop(torch, gsn, units, params, args, host_sig[:args.warmup],
+                             host_sig[args.warmup:args.warmup + count])
+
     ms_per_step = 1e3 * elapsed / args.steps
     traffic = load_traffic(m * n)
     out = {
@@ -757,6 +818,7 @@ def main():
         "phase_steps": phase_steps,
         "state_after": {"units": n_units, "edges": n_edges},
         "late_window": late_rec,
+        "loop": loop_rec,
         "update_rounds": rounds,
         "index": index_stats,
         "roofline": scan_roofline(m, n, scan_ms, scan_launches, traffic),

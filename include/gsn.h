@@ -15,7 +15,9 @@
  *           torch tensor) and must outlive the handle.  The network state lives in one
  *           caller-provided device workspace of gsn_workspace_bytes() bytes, aligned to
  *           256 bytes.  The library allocates only the host-side handle (with a few bytes
- *           of pinned host memory in it).
+ *           of pinned host memory in it) and, once gsn_iterate_loop is called, the HIP
+ *           runtime objects that call keeps (a stream and its recorded graphs), released by
+ *           gsn_destroy.
  * Layout.   Points are structure-of-arrays binary32: a buffer "SoA [3][k]" holds all k x
  *           coordinates, then all y, then all z.  Unit indices are int32 in [0, N).
  * Streams.  `stream` is a hipStream_t passed as void* (NULL = the default stream).  Calls
@@ -231,7 +233,9 @@ int gsn_iterate(gsn_net* net, const float* sig, int32_t m, int32_t* winner, int3
  * graph and replayed: a later call with the same arguments and network state (unit count,
  * tuning, which internal buffer set is current) replays the recorded graph without any
  * per-launch host work, on the caller's stream.  Up to GSN_GRAPH_CACHE graphs are kept per
- * handle (least recently used one replaced); they hold no memory of their own.  The only
+ * handle (the least recently used one is replaced); GSN_STAT_LOOP_RECORDS counts the calls
+ * that recorded one.  A graph reads the batches and writes the outputs at the addresses
+ * given, when it runs; it uses no buffer beyond the handle's workspace.  The only
  * difference from the separate calls: the spatial unit order of the staged find is rebuilt
  * at the first iteration when the rebuild would fall inside the loop, never later in it
  * (the order affects speed only).  The event timers (gsn_timing_enable) do not record
@@ -372,9 +376,12 @@ int gsn_timing_select(gsn_net* net, uint32_t mask);
  *   GSN_STAT_UPDATES     gsn_adapt calls that applied the winner-lock update
  *   GSN_STAT_CLEAR       sets every statistic to zero (value may be NULL)
  *   GSN_STAT_RESOLVED    signals that went through gsn_resolve_conflicts
- *   GSN_STAT_ACCEPTED    of those, the accepted ones */
+ *   GSN_STAT_ACCEPTED    of those, the accepted ones
+ *   GSN_STAT_LOOP_RECORDS  gsn_iterate_loop calls that recorded a graph (the others
+ *                        replayed one); a host count, the stream is not used */
 enum { GSN_STAT_ROUNDS = 0, GSN_STAT_ROUNDS_MAX = 1, GSN_STAT_UPDATES = 2,
-       GSN_STAT_CLEAR = 3, GSN_STAT_RESOLVED = 4, GSN_STAT_ACCEPTED = 5 };
+       GSN_STAT_CLEAR = 3, GSN_STAT_RESOLVED = 4, GSN_STAT_ACCEPTED = 5,
+       GSN_STAT_LOOP_RECORDS = 6 };
 int gsn_stat(gsn_net* net, int32_t key, int64_t* value, void* stream);
 
 #ifdef __cplusplus

@@ -191,6 +191,7 @@ struct gsn_net {
   };
   std::vector<LoopGraph> graphs;
   uint64_t graph_clock;
+  int64_t loop_records;   // loop calls that recorded a graph
   hipStream_t cap_stream;
   bool capturing;
   int loop_rebuild;   // -1, or the unit-order decision (0/1) of the next staged find
@@ -375,6 +376,7 @@ int gsn_create(const gsn_params* params, void* workspace, size_t workspace_bytes
   net->finds_since_bucket = 0;
   net->grid_rounds = 0;
   net->graph_clock = 0;
+  net->loop_records = 0;
   net->cap_stream = nullptr;
   net->capturing = false;
   net->loop_rebuild = -1;
@@ -769,6 +771,7 @@ int gsn_iterate_loop(gsn_net* net, const float* sigs, int32_t m, int32_t count,
     }
     net->graphs.push_back(g);
     hit = &net->graphs.back();
+    ++net->loop_records;
   }
   hit->used = ++net->graph_clock;
   if (hipGraphLaunch(hit->exec, st) != hipSuccess) return GSN_E_HIP;
@@ -1001,6 +1004,7 @@ int gsn_import(gsn_net* net, int32_t n, const float* xyz, const float* err, int3
     if (!ok) return GSN_E_HIP;
     net->n = n;
     net->dpar = 0;
+    net->stage_parity = 0;   // both histogram sets were cleared above
     net->phase = kReady;
     net->bucket_n = -1;
   } catch (const std::bad_alloc&) {
@@ -1060,11 +1064,16 @@ int gsn_tune(gsn_net* net, int32_t key, int32_t value) {
 }
 
 int gsn_stat(gsn_net* net, int32_t key, int64_t* value, void* stream) {
-  if (!net || key < 0 || key > GSN_STAT_ACCEPTED) return GSN_E_INVAL;
+  if (!net || key < 0 || key > GSN_STAT_LOOP_RECORDS) return GSN_E_INVAL;
   if (key != GSN_STAT_CLEAR && !value) return GSN_E_INVAL;
+  if (key == GSN_STAT_LOOP_RECORDS) {
+    *value = net->loop_records;
+    return GSN_OK;
+  }
   hipStream_t st = as_stream(stream);
   int32_t* slots = net->s.rem + gsn::kRmRounds;
   if (key == GSN_STAT_CLEAR) {
+    net->loop_records = 0;
     const int32_t zero[3] = {0, 0, 0};
     const unsigned long long zero64[2] = {0, 0};
     if (hipMemcpyAsync(slots, zero, sizeof(zero), hipMemcpyHostToDevice, st) != hipSuccess ||

@@ -56,6 +56,7 @@ GSN_STAT_UPDATES = 2
 GSN_STAT_CLEAR = 3
 GSN_STAT_RESOLVED = 4
 GSN_STAT_ACCEPTED = 5
+GSN_STAT_LOOP_RECORDS = 6
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "

@@ -41,18 +41,22 @@ def run_loop_case(m, lock, counts, rebucket, seed, n=6_000):
             assert_iter_equal(g, o, where + " eager")
     assert net.check() == 0
     torch.cuda.synchronize()
+    return net.stat(gsn.GSN_STAT_LOOP_RECORDS)
 
 
-@pytest.mark.parametrize("m,lock,counts,rebucket", [
-    (2_000, 0, [4, 4, 4, 4, 3, 3, 3], 0),       # staged find, lock set; replays, odd counts
-    (2_000, 0, [4, 4, 4, 4], 3),                # the unit order rebuilt at every call's start
-    (2_000, 0, [1, 2, 3, 4, 5, 1, 2], 0),       # more graphs than the cache holds
-    (100, 0, [5, 5, 5, 2], 0),                  # unit-parallel small-batch find
-    (2_000, 1, [4, 4, 3, 3], 0),                # winner lock (the paper's rule)
-    (2_000, 2, [2, 2, 2], 0),                   # greedy re-admission
+@pytest.mark.parametrize("m,lock,counts,rebucket,replays", [
+    (2_000, 0, [4, 4, 4, 4, 3, 3, 3], 0, True),   # staged find, lock set; odd counts
+    (2_000, 0, [4, 4, 4, 4], 3, True),            # unit order rebuilt at every call's start
+    (2_000, 0, [1, 2, 3, 4, 5, 1, 2], 0, False),  # more graphs than the cache holds
+    (100, 0, [5, 5, 5, 2], 0, True),              # unit-parallel small-batch find
+    (2_000, 1, [4, 4, 3, 3], 0, False),           # winner lock (the paper's rule)
+    (2_000, 2, [2, 2, 2], 0, False),              # greedy re-admission
 ])
-def test_loop_matches_the_oracle(m, lock, counts, rebucket):
-    run_loop_case(m, lock, counts, rebucket, seed=2000 + m + 10 * lock + rebucket)
+def test_loop_matches_the_oracle(m, lock, counts, rebucket, replays):
+    records = run_loop_case(m, lock, counts, rebucket, seed=2000 + m + 10 * lock + rebucket)
+    assert 1 <= records <= len(counts)
+    if replays:
+        assert records < len(counts)       # some calls replayed a recorded graph
 
 
 def test_loop_argument_errors():
