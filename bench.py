@@ -518,9 +518,9 @@ def run_sweep(args):
             scan_ms, launches = timers[gsn.GSN_T_FIND_SCAN]
             loop_rec = None
             if not args.no_loop:
-                host = dev_sig.cpu().numpy()
-                loop_rec = time_loop(torch, gsn, units, params, args, host[:warm],
-                                     host[warm:warm + steps])
+                batches = dev_sig.cpu().numpy()
+                loop_rec = time_loop(torch, gsn, units, params, args, batches[:warm],
+                                     batches[warm:warm + steps])
             rec = {
                 "metric": "sweep: signals/s and conflict rate vs m at 1 GPU",
                 "value": m * steps / el, "unit": "signals/s", "n_gpus": 1,
