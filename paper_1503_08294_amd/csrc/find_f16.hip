@@ -312,7 +312,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
   }
   v16f res[NB][2];
   const v16f zero16 = {};
+  // Issue priority by progress: a wave starts at the highest priority and steps down at a
+  // quarter, a half and three quarters of its chunk, so that the SIMD favours the waves that
+  // are furthest behind (the hardware otherwise favours the oldest wave, and the youngest
+  // waves of a SIMD finish last); priority only orders the issue of ready waves.
+  __builtin_amdgcn_s_setprio(3);
+  const int32_t p1 = cnt / 4, p2 = cnt / 2, p3 = (3 * cnt) / 4;
   for (int32_t i = 0; i < cnt; i += kDepth) {
+    if (i >= p1 && i < p1 + kDepth) __builtin_amdgcn_s_setprio(2);
+    if (i >= p2 && i < p2 + kDepth) __builtin_amdgcn_s_setprio(1);
+    if (i >= p3 && i < p3 + kDepth) __builtin_amdgcn_s_setprio(0);
 #pragma unroll
     for (int q = 0; q < kDepth; ++q) {
 #pragma unroll
