@@ -609,8 +609,13 @@ int gsn_adapt(gsn_net* net, const float* sig, int32_t m, const int32_t* winner,
     // automatic: one grid round more than the last update used (read from the pinned copy
     // of its count; a stale value only changes the split, never the result)
     int g = net->grid_rounds;
-    if (g == 0) g = std::clamp(*static_cast<volatile int32_t*>(net->feedback) + 1, 1,
-                               gsn::kMaxGridRounds);
+    if (g == 0) {
+      // a quarter more than the last update could use grid-wide: the single-workgroup tail
+      // is the slow part, and a recorded loop keeps this count for all its iterations while
+      // the network (and the rounds its updates need) grows
+      const int used = *static_cast<volatile int32_t*>(net->feedback) + 1;
+      g = std::clamp(used + used / 4, 1, gsn::kMaxGridRounds);
+    }
     gsn::WinnerStep w{sig, m, winner, second, d1, accepted, net->p.key_mode, net->p.eps_b,
                       net->p.eps_n, net->p.err_beta, net->p.max_age, g,
                       2 * (static_cast<int64_t>(net->p.e_max) + net->p.m_max),
