@@ -110,3 +110,21 @@ def test_loop_genus3_against_the_oracle():
         pair.compare_state(f"genus3 after loop call {call}")
     assert pair.net.check() == 0
     assert pair.net.stat(gsn.GSN_STAT_LOOP_RECORDS) < 4
+
+
+def test_loop_of_empty_batches_decays_the_errors():
+    """Iterations without signals still apply the error decay (and age nothing): a loop of
+    empty batches, recorded and replayed, against the oracle."""
+    import torch
+    rng = np.random.default_rng(11)
+    pair = Pair(rng.standard_normal((3, 3_000)).astype(np.float32), m_max=500)
+    for _ in range(3):
+        g, o = pair.iterate(rng.standard_normal((3, 500)).astype(np.float32))
+        assert_iter_equal(g, o, "warm-up")
+    empty = torch.zeros((4, 3, 0), dtype=torch.float32, device="cuda")
+    for call in range(3):
+        pair.net.iterate_loop(empty)
+        for _ in range(4):
+            pair.orc.iterate(np.zeros((3, 0), np.float32), 0, 0, False)
+        pair.compare_state(f"empty loop call {call}")
+    assert pair.net.check() == 0
