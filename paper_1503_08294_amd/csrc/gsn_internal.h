@@ -244,8 +244,10 @@ struct StageBufs {
   int32_t* sperm;   // [m_max] original index of the signal at every sorted position
   float* seed;      // [m_max] seed bound B at every sorted position
   float* ssig;      // [3][m] the signals in sorted order (x, y, z rows of stride m)
-  int32_t *hist_u, *off_u, *cur_u, *hist_s, *off_s, *cur_s;  // [kBuckets + 1] each; the
-                    // signal histogram and cursors use two sets of kBuckets / 8 in hist_s, cur_s
+  int32_t* stk;     // [m_max] rank of every signal inside its histogram bin (the ticket its
+                    // count increment returned)
+  int32_t *hist_u, *off_u, *cur_u, *hist_s;  // [kBuckets + 1] each; the signal histogram
+                    // uses two sets of kBuckets / 8 in hist_s
   int32_t* acc;     // [16] bounding-box accumulators
   float* bb;        // [8] grid of the last unit bucketing: lo.xyz, cells per length.xyz
   int32_t* mag;     // [4] max |x|, |y|, |z|, |w|^2 of this call (float bits)

@@ -117,9 +117,7 @@ __global__ __launch_bounds__(kBlock) void st_init(StageBufs b) {
     b.hist_u[i] = 0;
     b.hist_s[i] = 0;
     b.off_u[i] = 0;
-    b.off_s[i] = 0;
     b.cur_u[i] = 0;
-    b.cur_s[i] = 0;
   }
   if (i < 16) b.acc[i] = i < 6 ? acc_identity(i) : 0;
   if (i < 8) b.bb[i] = 0.0f;
@@ -295,9 +293,9 @@ __global__ __launch_bounds__(kBlock) void st_gather(const float* __restrict__ x,
                                                     const float* __restrict__ sig, int32_t m,
                                                     int32_t ub, const float* __restrict__ bb,
                                                     int32_t* __restrict__ skey,
+                                                    int32_t* __restrict__ stk,
                                                     int32_t* __restrict__ hist_s,
-                                                    int32_t* __restrict__ clear_a,
-                                                    int32_t* __restrict__ clear_b,
+                                                    int32_t* __restrict__ clear,
                                                     float* __restrict__ bmag, int layouts) {
   if (static_cast<int32_t>(blockIdx.x) < ub) {
     const int32_t pos = blockIdx.x * kBlock + threadIdx.x;
@@ -361,15 +359,14 @@ __global__ __launch_bounds__(kBlock) void st_gather(const float* __restrict__ x,
     if (j < m) {
       const int32_t k = bucket_of(sig[j], sig[m + j], sig[2 * m + j], bb);
       skey[j] = k;
-      atomicAdd(&hist_s[k >> kSignalShift], 1);
+      // the count's old value is the signal's rank inside its bin (the order inside a bin
+      // is immaterial)
+      stk[j] = atomicAdd(&hist_s[k >> kSignalShift], 1);
     }
-    // the first signal workgroup zeroes the other parity's histogram and cursors, which
-    // the next call uses
+    // the first signal workgroup zeroes the other parity's histogram, which the next call
+    // uses
     if (static_cast<int32_t>(blockIdx.x) == ub)
-      for (int32_t i = threadIdx.x; i < kSignalBuckets; i += kBlock) {
-        clear_a[i] = 0;
-        clear_b[i] = 0;
-      }
+      for (int32_t i = threadIdx.x; i < kSignalBuckets; i += kBlock) clear[i] = 0;
   }
 }
 
@@ -390,18 +387,18 @@ __device__ __forceinline__ void merge2(unsigned long long& a1, unsigned long lon
 // Places the signals in bucket order and computes their seed bounds, in one launch.  Every
 // workgroup scans the signal histogram (kSignalBuckets bins, zeroed by the previous call) in
 // LDS itself, so the bins' offsets need no launch of their own; a signal's sorted position is
-// its bin's offset plus a ticket from the bin's cursor (atomics; the order inside a bin is
-// immaterial).  The signal's index and coordinates are written at that position (sperm,
+// its bin's offset plus its rank inside the bin (stk, from the gather's count).  The signal's index and coordinates are written at that position (sperm,
 // ssig), so the scan's prologue reads its signals directly.
 // Workgroup 0 also reduces the per-block unit magnitudes of this call.
-// kSeedLanes lanes per signal then scan a strided part of the kSeedWindow units around the
+// kSeedLanes lanes per signal scan a strided part of the kSeedWindow units around the
 // signal's unit bucket in the sorted order; the second smallest direct-form distance over
-// these distinct units is the seed bound B >= the signal's true second-best distance.
+// these distinct units is the seed bound B >= the signal's true second-best distance.  Only
+// the distance is kept, so the window slot (distinct per unit) stands in for the unit's
+// index in the keys and the indices are not read.
 __global__ __launch_bounds__(kBlock) void st_place_seed(
-    const int32_t* __restrict__ hist_s, int32_t* __restrict__ cur_s,
+    const int32_t* __restrict__ hist_s, const int32_t* __restrict__ stk,
     const int32_t* __restrict__ skey, const float* __restrict__ sig, int32_t m,
-    const float4* __restrict__ pu, const int32_t* __restrict__ pidx, int32_t n,
-    const int32_t* __restrict__ off_u, int32_t* __restrict__ sperm, float* __restrict__ seed,
+    const float4* __restrict__ pu, int32_t n, const int32_t* __restrict__ off_u, int32_t* __restrict__ sperm, float* __restrict__ seed,
     float* __restrict__ ssig, const float* __restrict__ bmag,
     int32_t nmag, int32_t* __restrict__ mag, int32_t* __restrict__ wctr, int32_t nctr) {
   static_assert(kBlock == 256 && kSignalBuckets % kBlock == 0, "four waves, whole bins");
@@ -409,6 +406,49 @@ __global__ __launch_bounds__(kBlock) void st_place_seed(
   __shared__ int32_t soff[kSignalBuckets];
   __shared__ int32_t wsum[kBlock / 64];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int32_t t = blockIdx.x * kBlock + tid;
+  const int32_t j = t / kSeedLanes;
+  const int q = t % kSeedLanes;
+
+  // The seed first: its chain of loads (key, bucket bounds, window units) does not depend on
+  // the placement, so it runs beside the histogram scan below instead of after it.
+  unsigned long long k1 = ~0ull, k2 = ~0ull;
+  float sx = 0.0f, sy = 0.0f, sz = 0.0f;
+  int32_t key = 0, rank = 0;
+  if (j < m) {
+    if (q == 0) rank = stk[j];
+    sx = sig[j];
+    sy = sig[m + j];
+    sz = sig[2 * m + j];
+    key = skey[j];
+    const int32_t b0 = off_u[key], b1 = off_u[key + 1];
+    int32_t lo = (b0 + b1) / 2 - kSeedWindow / 2;
+    lo = max(0, min(lo, n - kSeedWindow));
+    const int32_t hi = min(n, lo + kSeedWindow);
+    // the lane's kSeedWindow / kSeedLanes units in one batch of loads (indices past hi
+    // repeat the last unit and enter as the all-ones key, which changes nothing)
+    constexpr int kPer = kSeedWindow / kSeedLanes;
+    if (hi > lo) {
+      float4 wu[kPer];
+#pragma unroll
+      for (int i = 0; i < kPer; ++i) wu[i] = pu[min(lo + q + i * kSeedLanes, hi - 1)];
+#pragma unroll
+      for (int i = 0; i < kPer; ++i) {
+        const int32_t r = lo + q + i * kSeedLanes;
+        const float dx = sx - wu[i].x, dy = sy - wu[i].y, dz = sz - wu[i].z;
+        const unsigned long long kk =
+            r < hi ? pack((dx * dx + dy * dy) + dz * dz, r) : ~0ull;
+        merge2(k1, k2, kk, ~0ull);
+      }
+    }
+  }
+#pragma unroll
+  for (int off = 1; off < kSeedLanes; off <<= 1) {
+    const unsigned long long o1 = __shfl_xor(k1, off);
+    const unsigned long long o2 = __shfl_xor(k2, off);
+    merge2(k1, k2, o1, o2);
+  }
+
   {
     int32_t v[per], sum = 0;
 #pragma unroll
@@ -454,61 +494,19 @@ __global__ __launch_bounds__(kBlock) void st_place_seed(
   }
   __syncthreads();
 
-  const int32_t t = blockIdx.x * kBlock + tid;
   if (t < nctr) wctr[t] = 0;  // grab counters of the dynamic scan (variant 5)
-  const int32_t j = t / kSeedLanes;
-  const int q = t % kSeedLanes;
-  int32_t pos = -1;
   if (j < m && q == 0) {
-    const int32_t bin = skey[j] >> kSignalShift;
-    pos = soff[bin] + atomicAdd(&cur_s[bin], 1);
-    if (pos >= 0 && pos < m) sperm[pos] = j;  // always true when counts match keys
-  }
-  pos = __shfl(pos, lane & ~(kSeedLanes - 1));  // the signal's lanes are consecutive
-  unsigned long long k1 = ~0ull, k2 = ~0ull;
-  if (j < m) {
-    const float sx = sig[j], sy = sig[m + j], sz = sig[2 * m + j];
-    if (q == 0 && pos >= 0 && pos < m) {
+    const int32_t bin = key >> kSignalShift;
+    const int32_t pos = soff[bin] + rank;
+    if (pos >= 0 && pos < m) {  // always true when counts match keys
+      sperm[pos] = j;
       ssig[pos] = sx;
       ssig[m + pos] = sy;
       ssig[2 * m + pos] = sz;
-    }
-    const int32_t k = skey[j];
-    const int32_t b0 = off_u[k], b1 = off_u[k + 1];
-    int32_t lo = (b0 + b1) / 2 - kSeedWindow / 2;
-    lo = max(0, min(lo, n - kSeedWindow));
-    const int32_t hi = min(n, lo + kSeedWindow);
-    // the lane's kSeedWindow / kSeedLanes units in one batch of loads (indices past hi
-    // repeat the last unit and enter as the all-ones key, which changes nothing)
-    constexpr int kPer = kSeedWindow / kSeedLanes;
-    if (hi > lo) {
-      float4 wu[kPer];
-      int32_t wi[kPer];
-#pragma unroll
-      for (int i = 0; i < kPer; ++i) {
-        const int32_t r = min(lo + q + i * kSeedLanes, hi - 1);
-        wu[i] = pu[r];
-        wi[i] = pidx[r];
-      }
-#pragma unroll
-      for (int i = 0; i < kPer; ++i) {
-        const float dx = sx - wu[i].x, dy = sy - wu[i].y, dz = sz - wu[i].z;
-        const unsigned long long key = lo + q + i * kSeedLanes < hi
-                                           ? pack((dx * dx + dy * dy) + dz * dz, wi[i])
-                                           : ~0ull;
-        merge2(k1, k2, key, ~0ull);
-      }
+      seed[pos] = k2 != ~0ull ? __uint_as_float(static_cast<uint32_t>(k2 >> 32))
+                              : __builtin_huge_valf();
     }
   }
-#pragma unroll
-  for (int off = 1; off < kSeedLanes; off <<= 1) {
-    const unsigned long long o1 = __shfl_xor(k1, off);
-    const unsigned long long o2 = __shfl_xor(k2, off);
-    merge2(k1, k2, o1, o2);
-  }
-  if (j < m && q == 0 && pos >= 0 && pos < m)
-    seed[pos] = k2 != ~0ull ? __uint_as_float(static_cast<uint32_t>(k2 >> 32))
-                            : __builtin_huge_valf();
 }
 
 // 32 signals per workgroup, 8 groups of lanes split the partial rows, merged in LDS.
@@ -602,10 +600,11 @@ size_t stage_bytes(int32_t n_max, int32_t m_max) {
   add(4 * nb64);   // pidx
   add(4 * nm);   // ukey
   add(4 * mm);   // skey
+  add(4 * mm);   // stk
   add(4 * mm);   // sperm
   add(4 * mm);   // seed
   add(12 * mm);  // ssig
-  for (int i = 0; i < 6; ++i) add(hb);  // hist/off/cur for units and signals
+  for (int i = 0; i < 4; ++i) add(hb);  // hist/off/cur for units, hist for signals
   add(4 * 16);   // acc
   add(4 * 8);    // bb
   add(4 * 4);    // mag
@@ -632,6 +631,7 @@ StageBufs carve_stage(void* base, int32_t n_max, int32_t m_max) {
   s.pidx = reinterpret_cast<int32_t*>(take(4 * nb64));
   s.ukey = reinterpret_cast<int32_t*>(take(4 * nm));
   s.skey = reinterpret_cast<int32_t*>(take(4 * mm));
+  s.stk = reinterpret_cast<int32_t*>(take(4 * mm));
   s.sperm = reinterpret_cast<int32_t*>(take(4 * mm));
   s.seed = reinterpret_cast<float*>(take(4 * mm));
   s.ssig = reinterpret_cast<float*>(take(12 * mm));
@@ -639,8 +639,6 @@ StageBufs carve_stage(void* base, int32_t n_max, int32_t m_max) {
   s.off_u = reinterpret_cast<int32_t*>(take(hb));
   s.cur_u = reinterpret_cast<int32_t*>(take(hb));
   s.hist_s = reinterpret_cast<int32_t*>(take(hb));
-  s.off_s = reinterpret_cast<int32_t*>(take(hb));
-  s.cur_s = reinterpret_cast<int32_t*>(take(hb));
   s.acc = reinterpret_cast<int32_t*>(take(4 * 16));
   s.bb = reinterpret_cast<float*>(take(4 * 8));
   s.mag = reinterpret_cast<int32_t*>(take(4 * 4));
@@ -674,17 +672,15 @@ hipError_t launch_stage(const DevState& s, const StageBufs& b, int32_t n, const 
     st_scatter_units<<<nb_u, kBlock, 0, st>>>(n, b.ukey, b.cur_u, b.pidx);
   }
   const int nb_g = blocks((static_cast<int64_t>(n) + 63) & ~static_cast<int64_t>(63));
-  // signal histogram and cursors alternate between two sets by call parity; each call's
-  // gather zeroes the other set for the next call
+  // the signal histogram alternates between two sets by call parity; each call's gather
+  // zeroes the other set for the next call
   int32_t* hist = b.hist_s + parity * kSignalBuckets;
-  int32_t* cur = b.cur_s + parity * kSignalBuckets;
   int32_t* hist_next = b.hist_s + (parity ^ 1) * kSignalBuckets;
-  int32_t* cur_next = b.cur_s + (parity ^ 1) * kSignalBuckets;
   st_gather<<<nb_g + blocks(m), kBlock, 0, st>>>(s.x, s.y, s.z, n, b.pidx, b.pu, b.pm, b.pmh, sig,
-                                                 m, nb_g, b.bb, b.skey, hist, hist_next,
-                                                 cur_next, b.bmag, layouts);
+                                                 m, nb_g, b.bb, b.skey, b.stk, hist, hist_next,
+                                                 b.bmag, layouts);
   st_place_seed<<<blocks(static_cast<int64_t>(m) * kSeedLanes), kBlock, 0, st>>>(
-      hist, cur, b.skey, sig, m, b.pu, b.pidx, n, b.off_u, b.sperm, b.seed, b.ssig,
+      hist, b.stk, b.skey, sig, m, b.pu, n, b.off_u, b.sperm, b.seed, b.ssig,
       b.bmag, nb_g, b.mag, b.wctr, wctr_count(m));
   return hipGetLastError();
 }
