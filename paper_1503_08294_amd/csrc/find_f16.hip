@@ -552,14 +552,13 @@ int f16_dyn_split(int32_t m, int cus, int want) {
 }
 
 hipError_t launch_scan_f16_dyn(const DevState& s, const StageBufs& b, int32_t n, int32_t m,
-                               int split, int grab, hipStream_t st) {
+                               int split, int grab, hipStream_t st, LaunchEvents ev) {
   const int32_t n_batches = (n + 63) / 64;
   if (static_cast<int64_t>(n_batches) * 2048 >= (1LL << 31)) return hipErrorInvalidValue;
   if (split < 8 || split % 8 != 0 || split > kMaxSplit || grab < 1) return hipErrorInvalidValue;
   const int32_t sblocks = (m + kSignalsPerWG - 1) / kSignalsPerWG;
-  fh_scan_dyn<<<8 * sblocks * (split / 8), 256, 0, st>>>(b.pu, b.pmh, b.pidx, n, b.ssig, m,
-                                                         b.seed, b.mag, b.bb, s.part, b.wctr,
-                                                         sblocks, grab);
+  launch_with(fh_scan_dyn, dim3(8 * sblocks * (split / 8)), dim3(256), st, ev, b.pu, b.pmh,
+              b.pidx, n, b.ssig, m, b.seed, b.mag, b.bb, s.part, b.wctr, sblocks, grab);
   return hipGetLastError();
 }
 
@@ -576,13 +575,13 @@ int f16_split(int32_t n, int32_t m, int cus, int want) {
 }
 
 hipError_t launch_scan_f16(const DevState& s, const StageBufs& b, int32_t n, const float* sig,
-                           int32_t m, int split, hipStream_t st) {
+                           int32_t m, int split, hipStream_t st, LaunchEvents ev) {
   const int32_t n_batches = (n + 63) / 64;
   // buffer offsets from a chunk's first batch are 32-bit: 2 KB per batch
   if (static_cast<int64_t>(n_batches) * 2048 >= (1LL << 31)) return hipErrorInvalidValue;
   dim3 grid((m + kSignalsPerWG - 1) / kSignalsPerWG, split);
-  fh_scan<<<grid, 256, 0, st>>>(b.pu, b.pmh, b.pidx, n, b.ssig, m,
-                                b.seed, b.mag, b.bb, s.part);
+  launch_with(fh_scan, grid, dim3(256), st, ev, b.pu, b.pmh, b.pidx, n, b.ssig, m, b.seed, b.mag,
+              b.bb, s.part);
   return hipGetLastError();
 }
 

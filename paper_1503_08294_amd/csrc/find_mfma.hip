@@ -380,12 +380,12 @@ int mfma_split(int32_t n, int32_t m, int cus, int want) {
 }
 
 hipError_t launch_scan_mfma(const DevState& s, const StageBufs& b, int32_t n, const float* sig,
-                            int32_t m, int split, hipStream_t st) {
+                            int32_t m, int split, hipStream_t st, LaunchEvents ev) {
   const int32_t n_batches = (n + 63) / 64;
   const int32_t chunk_batches = (n_batches + split - 1) / split;
   dim3 grid((m + kSignalsPerWG - 1) / kSignalsPerWG, split);
-  fm_scan<<<grid, 256, 0, st>>>(b.pu, b.pm, b.pidx, n, chunk_batches, sig, m, b.sperm, b.skey,
-                                b.off_u, b.seed, b.mag, s.part);
+  launch_with(fm_scan, grid, dim3(256), st, ev, b.pu, b.pm, b.pidx, n, chunk_batches, sig, m,
+              b.sperm, b.skey, b.off_u, b.seed, b.mag, s.part);
   return hipGetLastError();
 }
 

@@ -195,22 +195,23 @@ int screened_split(int32_t n, int32_t m, int cus, int want) {
 }
 
 hipError_t launch_scan_screened(const DevState& s, const StageBufs& b, int32_t n,
-                                const float* sig, int32_t m, int split, hipStream_t st) {
+                                const float* sig, int32_t m, int split, hipStream_t st,
+                                LaunchEvents ev) {
   const int S = screened_signals_per_lane(m);
   const int32_t chunk = (n + split - 1) / split;
   dim3 grid((m + kBlock * S - 1) / (kBlock * S), split);
   switch (S) {
     case 8:
-      fs_scan<8><<<grid, kBlock, 0, st>>>(b.pu, b.pidx, n, chunk, sig, m, b.sperm, b.seed,
-                                          b.mag, s.part);
+      launch_with(fs_scan<8>, grid, kBlock, st, ev, b.pu, b.pidx, n, chunk, sig, m, b.sperm,
+                  b.seed, b.mag, s.part);
       break;
     case 4:
-      fs_scan<4><<<grid, kBlock, 0, st>>>(b.pu, b.pidx, n, chunk, sig, m, b.sperm, b.seed,
-                                          b.mag, s.part);
+      launch_with(fs_scan<4>, grid, kBlock, st, ev, b.pu, b.pidx, n, chunk, sig, m, b.sperm,
+                  b.seed, b.mag, s.part);
       break;
     default:
-      fs_scan<1><<<grid, kBlock, 0, st>>>(b.pu, b.pidx, n, chunk, sig, m, b.sperm, b.seed,
-                                          b.mag, s.part);
+      launch_with(fs_scan<1>, grid, kBlock, st, ev, b.pu, b.pidx, n, chunk, sig, m, b.sperm,
+                  b.seed, b.mag, s.part);
       break;
   }
   return hipGetLastError();

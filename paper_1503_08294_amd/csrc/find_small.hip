@@ -211,12 +211,13 @@ int32_t small_rows(int32_t n, int32_t m) {
 }
 
 hipError_t launch_find_small_scan(const DevState& s, int32_t n, const float* sig, int32_t m,
-                                  hipStream_t st) {
+                                  hipStream_t st, LaunchEvents ev) {
   if (m < 1 || m > kSmallM || n < 2) return hipErrorInvalidValue;
   const int32_t T = small_slots(m);
   const int32_t chunk = small_chunk(n, m);
   const int32_t rows = (n + chunk - 1) / chunk;
-  sm_scan<<<rows, kBlock, 0, st>>>(s.x, s.y, s.z, n, chunk, sig, m, T, s.spart);
+  launch_with(sm_scan, dim3(rows), dim3(kBlock), st, ev, s.x, s.y, s.z, n, chunk, sig, m, T,
+              s.spart);
   return hipGetLastError();
 }
 

@@ -167,19 +167,22 @@ FindConfig find_config(int32_t n, int32_t m, int cus, int want_split, int want_v
 
 hipError_t launch_find_scan(const DevState& s, int32_t n, const float* sig, int32_t m,
                             const FindConfig& cfg, int32_t*, int32_t*, float*, float*,
-                            hipStream_t st) {
+                            hipStream_t st, LaunchEvents ev) {
   const int S = signals_per_lane(m);
   const int32_t chunk = (n + cfg.split - 1) / cfg.split;
   dim3 grid((m + kBlock * S - 1) / (kBlock * S), cfg.split);
   switch (S) {
     case 4:
-      fw_scan_direct<4><<<grid, kBlock, 0, st>>>(s.x, s.y, s.z, n, chunk, sig, m, s.part);
+      launch_with(fw_scan_direct<4>, grid, kBlock, st, ev, s.x, s.y, s.z, n, chunk, sig, m,
+                  s.part);
       break;
     case 2:
-      fw_scan_direct<2><<<grid, kBlock, 0, st>>>(s.x, s.y, s.z, n, chunk, sig, m, s.part);
+      launch_with(fw_scan_direct<2>, grid, kBlock, st, ev, s.x, s.y, s.z, n, chunk, sig, m,
+                  s.part);
       break;
     default:
-      fw_scan_direct<1><<<grid, kBlock, 0, st>>>(s.x, s.y, s.z, n, chunk, sig, m, s.part);
+      launch_with(fw_scan_direct<1>, grid, kBlock, st, ev, s.x, s.y, s.z, n, chunk, sig, m,
+                  s.part);
       break;
   }
   return hipGetLastError();

@@ -282,6 +282,34 @@ struct TimedRegion {
   }
 };
 
+// A timer whose event pair is bound to one kernel launch (gsn::LaunchEvents): the pair is
+// taken from the pool when the timer records, and end() keeps it only if the launch was made.
+struct LaunchTimer {
+  gsn_net* net;
+  int which;
+  gsn::LaunchEvents ev;
+  LaunchTimer(gsn_net* n, int w) : net(n), which(w) {
+    if (net->timing && !net->capturing && ((net->timing_mask >> w) & 1u)) {
+      ev.start = take_event(net);
+      ev.stop = ev.start ? take_event(net) : nullptr;
+      if (ev.start && !ev.stop) {
+        net->pool.push_back(ev.start);
+        ev.start = nullptr;
+      }
+    }
+  }
+  void end(bool launched) {
+    if (!ev.start) return;
+    if (launched) {
+      net->rec[which].emplace_back(ev.start, ev.stop);
+    } else {
+      net->pool.push_back(ev.start);
+      net->pool.push_back(ev.stop);
+    }
+    ev = {};
+  }
+};
+
 int read_status_slot(gsn_net* net, int slot, int32_t* out, hipStream_t st) {
   if (hipMemcpyAsync(out, net->s.status + slot, sizeof(int32_t), hipMemcpyDeviceToHost, st) !=
       hipSuccess)
@@ -447,9 +475,9 @@ int find_impl(gsn_net* net, const float* sig, int32_t m, int32_t* winner, int32_
   TimedRegion all(net, GSN_T_FIND, st);
   hipError_t e;
   if (cfg.variant == 6) {
-    TimedRegion scan(net, GSN_T_FIND_SCAN, st);
-    e = gsn::launch_find_small_scan(net->s, net->n, sig, m, st);
-    scan.end();
+    LaunchTimer scan(net, GSN_T_FIND_SCAN);
+    e = gsn::launch_find_small_scan(net->s, net->n, sig, m, st, scan.ev);
+    scan.end(e == hipSuccess);
     if (e == hipSuccess) {
       e = gsn::launch_find_small_merge(net->s, net->n, m, winner, second, d1, d2, claim, st);
       if (claimed) *claimed = claim != nullptr;
@@ -471,14 +499,16 @@ int find_impl(gsn_net* net, const float* sig, int32_t m, int32_t* winner, int32_
     }
     ++net->finds_since_bucket;
     if (e == hipSuccess) {
-      TimedRegion scan(net, GSN_T_FIND_SCAN, st);
+      LaunchTimer scan(net, GSN_T_FIND_SCAN);
       e = cfg.variant == 5   ? gsn::launch_scan_f16_dyn(net->s, sb, net->n, m, cfg.split,
-                                                    net->tune_grab, st)
-          : cfg.variant == 4 ? gsn::launch_scan_f16(net->s, sb, net->n, sig, m, cfg.split, st)
-          : cfg.variant == 3 ? gsn::launch_scan_mfma(net->s, sb, net->n, sig, m, cfg.split, st)
+                                                    net->tune_grab, st, scan.ev)
+          : cfg.variant == 4 ? gsn::launch_scan_f16(net->s, sb, net->n, sig, m, cfg.split, st,
+                                                    scan.ev)
+          : cfg.variant == 3 ? gsn::launch_scan_mfma(net->s, sb, net->n, sig, m, cfg.split, st,
+                                                     scan.ev)
                              : gsn::launch_scan_screened(net->s, sb, net->n, sig, m, cfg.split,
-                                                         st);
-      scan.end();
+                                                         st, scan.ev);
+      scan.end(e == hipSuccess);
     }
     if (e == hipSuccess) {
       e = gsn::launch_stage_merge(net->s, sb, m, cfg.split, winner, second, d1, d2, claim, st);
@@ -486,9 +516,9 @@ int find_impl(gsn_net* net, const float* sig, int32_t m, int32_t* winner, int32_
       if (order) *order = sb.sperm;  // the signals' spatial order of this call
     }
   } else {
-    TimedRegion scan(net, GSN_T_FIND_SCAN, st);
-    e = gsn::launch_find_scan(net->s, net->n, sig, m, cfg, winner, second, d1, d2, st);
-    scan.end();
+    LaunchTimer scan(net, GSN_T_FIND_SCAN);
+    e = gsn::launch_find_scan(net->s, net->n, sig, m, cfg, winner, second, d1, d2, st, scan.ev);
+    scan.end(e == hipSuccess);
     if (e == hipSuccess) e = gsn::launch_find_merge(net->s, m, cfg, winner, second, d1, d2, st);
   }
   all.end();

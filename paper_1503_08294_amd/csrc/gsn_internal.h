@@ -1,6 +1,7 @@
 // Internal declarations shared by the HIP translation units of libgsn.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -15,6 +16,23 @@ constexpr int kMaxSplit = GSN_MAX_SPLIT;
 constexpr int kSmallM = 256;           // batches up to this size may take the small-batch scan
 constexpr int kSmallRows = 1024;       // its partial rows (workgroups) at most
 constexpr int32_t kDead = -1;          // age marking a half-edge removed this iteration
+
+// An event pair bound to one kernel launch: the runtime sets start and stop from the
+// kernel's own start and end (hipExtLaunchKernel), which excludes the end-of-kernel cache
+// flush and adds no marker to the stream.  Both null: a plain launch.
+struct LaunchEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+
+template <typename... KArgs, typename... Args>
+inline void launch_with(void (*k)(KArgs...), dim3 grid, dim3 block, hipStream_t st,
+                        LaunchEvents ev, Args... args) {
+  if (ev.start != nullptr && ev.stop != nullptr)
+    hipExtLaunchKernelGGL(k, grid, block, 0, st, ev.start, ev.stop, 0,
+                          static_cast<KArgs>(args)...);
+  else
+    k<<<grid, block, 0, st>>>(static_cast<KArgs>(args)...);
+}
 
 // Sticky status word layout (int32 slots in the status area).
 enum StatusSlot {
@@ -215,7 +233,7 @@ FindConfig find_config(int32_t n, int32_t m, int cus, int want_split, int want_v
 
 hipError_t launch_find_scan(const DevState& s, int32_t n, const float* sig, int32_t m,
                             const FindConfig& cfg, int32_t* winner, int32_t* second,
-                            float* d1, float* d2, hipStream_t st);
+                            float* d1, float* d2, hipStream_t st, LaunchEvents ev = {});
 hipError_t launch_find_merge(const DevState& s, int32_t m, const FindConfig& cfg,
                              int32_t* winner, int32_t* second, float* d1, float* d2,
                              hipStream_t st);
@@ -226,7 +244,7 @@ int32_t small_slots(int32_t m);
 int32_t small_rows(int32_t n, int32_t m);
 size_t small_part_keys(int32_t m_max);
 hipError_t launch_find_small_scan(const DevState& s, int32_t n, const float* sig, int32_t m,
-                                  hipStream_t st);
+                                  hipStream_t st, LaunchEvents ev = {});
 struct ClaimArgs;
 hipError_t launch_find_small_merge(const DevState& s, int32_t n, int32_t m, int32_t* winner,
                                    int32_t* second, float* d1, float* d2,
@@ -283,17 +301,18 @@ hipError_t launch_stage_merge(const DevState& s, const StageBufs& b, int32_t m, 
                               const ClaimArgs* claim, hipStream_t st);
 int screened_split(int32_t n, int32_t m, int cus, int want);
 hipError_t launch_scan_screened(const DevState& s, const StageBufs& b, int32_t n,
-                                const float* sig, int32_t m, int split, hipStream_t st);
+                                const float* sig, int32_t m, int split, hipStream_t st,
+                                LaunchEvents ev = {});
 int mfma_split(int32_t n, int32_t m, int cus, int want);
 int f16_split(int32_t n, int32_t m, int cus, int want);
 hipError_t launch_scan_f16(const DevState& s, const StageBufs& b, int32_t n, const float* sig,
-                           int32_t m, int split, hipStream_t st);
+                           int32_t m, int split, hipStream_t st, LaunchEvents ev = {});
 // variant 5: split = 8 x replicas (a multiple of 8), grab = list entries per atomic
 int f16_dyn_split(int32_t m, int cus, int want);
 hipError_t launch_scan_f16_dyn(const DevState& s, const StageBufs& b, int32_t n, int32_t m,
-                               int split, int grab, hipStream_t st);
+                               int split, int grab, hipStream_t st, LaunchEvents ev = {});
 hipError_t launch_scan_mfma(const DevState& s, const StageBufs& b, int32_t n, const float* sig,
-                            int32_t m, int split, hipStream_t st);
+                            int32_t m, int split, hipStream_t st, LaunchEvents ev = {});
 
 // lock_mode: 0 = lock set {b, s} + N(b), 1 = the winner alone; key_mode: 0 = (d1 bits,
 // index), 1 = index

@@ -8,7 +8,8 @@ from parity import Pair, assert_find_equal
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("variant,m", [(4, 1_500), (5, 1_500), (6, 100), (3, 1_500), (1, 300)])
+@pytest.mark.parametrize("variant,m", [(4, 1_500), (5, 1_500), (6, 100), (3, 1_500), (2, 1_500),
+                                       (1, 300)])
 def test_scan_timer_counts_launches_and_changes_nothing(variant, m):
     from paper_1503_08294_amd import gsn
     rng = np.random.default_rng(variant)
