@@ -354,9 +354,12 @@ int gsn_tune(gsn_net* net, int32_t key, int32_t value);
  * the last read, and clears them (syncs).  The events are made without the system-scope
  * memory fence (hipEventDisableSystemFence): they time the work, they publish nothing to
  * the host, and recording them does not stall the stream.
- *   GSN_T_FIND_SCAN   the find-winners scan kernel alone; its pair is bound to the kernel's
- *                     launch (hipExtLaunchKernel), so it spans the kernel's own start to end
- *                     (not the end-of-kernel cache flush) and puts no marker on the stream
+ *   GSN_T_FIND_SCAN   the find-winners scan kernel alone.  For the staged scans (variants
+ *                     2-5) the pair is bound to the kernel's launch (hipExtLaunchKernel): it
+ *                     spans the kernel's own start to end (not the end-of-kernel cache
+ *                     flush) and puts no marker on the stream, but costs the host tens of
+ *                     microseconds per launch; the unstaged scans (variants 1 and 6, small
+ *                     batches, whose steps are bound by launches) take a marker pair
  *   GSN_T_FIND        all of gsn_find_winners
  *   GSN_T_RESOLVE, GSN_T_ADAPT, GSN_T_EDGES   all of the corresponding call
  *   GSN_T_UPDATE      the fused update of gsn_iterate (resolve, adapt and edges) */

@@ -475,9 +475,11 @@ int find_impl(gsn_net* net, const float* sig, int32_t m, int32_t* winner, int32_
   TimedRegion all(net, GSN_T_FIND, st);
   hipError_t e;
   if (cfg.variant == 6) {
-    LaunchTimer scan(net, GSN_T_FIND_SCAN);
-    e = gsn::launch_find_small_scan(net->s, net->n, sig, m, st, scan.ev);
-    scan.end(e == hipSuccess);
+    // a marker pair here: binding a pair to a launch costs the host tens of microseconds,
+    // which a launch-bound small batch would show in its step time
+    TimedRegion scan(net, GSN_T_FIND_SCAN, st);
+    e = gsn::launch_find_small_scan(net->s, net->n, sig, m, st);
+    scan.end();
     if (e == hipSuccess) {
       e = gsn::launch_find_small_merge(net->s, net->n, m, winner, second, d1, d2, claim, st);
       if (claimed) *claimed = claim != nullptr;
@@ -516,9 +518,9 @@ int find_impl(gsn_net* net, const float* sig, int32_t m, int32_t* winner, int32_
       if (order) *order = sb.sperm;  // the signals' spatial order of this call
     }
   } else {
-    LaunchTimer scan(net, GSN_T_FIND_SCAN);
-    e = gsn::launch_find_scan(net->s, net->n, sig, m, cfg, winner, second, d1, d2, st, scan.ev);
-    scan.end(e == hipSuccess);
+    TimedRegion scan(net, GSN_T_FIND_SCAN, st);
+    e = gsn::launch_find_scan(net->s, net->n, sig, m, cfg, winner, second, d1, d2, st);
+    scan.end();
     if (e == hipSuccess) e = gsn::launch_find_merge(net->s, m, cfg, winner, second, d1, d2, st);
   }
   all.end();
