@@ -22,7 +22,7 @@ namespace gsn {
 namespace {
 
 constexpr int kSmallTile = 1024;         // units per LDS tile
-constexpr int kSmallPerThread = 64;      // units per thread the chunking aims at (one tile
+constexpr int kSmallPerThread = 16;      // units per thread the chunking aims at (one tile
                                          // per workgroup, so one round of global loads)
 constexpr unsigned long long kNone = ~0ull;
 
