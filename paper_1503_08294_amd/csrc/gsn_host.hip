@@ -79,7 +79,7 @@ Layout layout_for(const gsn_params& p) {
   add(mm);                     // 19 pend
   add(4 * nm);                 // 20 len
   add(4 * nm);                 // 21 extra
-  add(4 * kRmSlots);           // 22 rem
+  add(4 * kRmWords);           // 22 rem
   add(8 * mm);                 // 23 list
   add(12 * mm);                // 24 schedule signals
   add(4 * mm);                 // 25 schedule winners
@@ -1031,7 +1031,7 @@ int gsn_import(gsn_net* net, int32_t n, const float* xyz, const float* err, int3
     fill_bytes(s.orphan, 0, 4 * nm);
     fill_bytes(s.lock, 0xff, 8 * nm);
     fill_bytes(s.extra, 0, 4 * nm);
-    fill_bytes(s.rem, 0, 4 * gsn::kRmSlots);
+    fill_bytes(s.rem, 0, 4 * gsn::kRmWords);
     fill_bytes(s.status, 0, 4 * gsn::kStSlots);
     fill_bytes(s.bdelta[0], 0, 4 * (nm / gsn::kBlock + 2));
     fill_bytes(s.bdelta[1], 0, 4 * (nm / gsn::kBlock + 2));

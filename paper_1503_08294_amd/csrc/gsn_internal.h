@@ -44,18 +44,31 @@ enum StatusSlot {
   kStSlots = 16
 };
 
-// Counters of the sequential-survivor update (int32 slots of DevState::rem): the signals
-// still pending after each grid-wide round, the survivors of the current call, and round
-// statistics accumulated until the host clears them.
+// Counters of the sequential-survivor update and the greedy resolve (int32 words of
+// DevState::rem): round statistics accumulated until the host clears them, then spread
+// counters (below) for the signals still pending after each grid-wide round and for the
+// survivors of the current call.
 constexpr int kMaxGridRounds = 32;
 enum RoundSlot {
-  kRmSurvivors = kMaxGridRounds,
   kRmRounds,       // rounds summed over the updates since the last clear
   kRmRoundsMax,    // the most rounds one update took
   kRmUpdates,      // updates since the last clear
   kRmGridUsed,     // grid-wide rounds that did work in the last update
   kRmSlots
 };
+// A spread counter: kSpreadParts words, one per 128-byte line, so that the workgroups of a
+// grid-wide launch add to it without queueing at one address (device-scope atomics on one
+// word are serialized: ~2,000 workgroups adding to one word cost a round tens of
+// microseconds); its value is the sum of the parts.
+constexpr int kSpreadParts = 64;
+constexpr int kSpreadStride = 32;  // int32 words from one part to the next
+constexpr int kSpreadWords = kSpreadParts * kSpreadStride;
+constexpr int kRmSpread = 32;      // first word of the spread counters (past the slots)
+static_assert(kRmSlots <= kRmSpread, "round slots overlap the spread counters");
+// round t's pending count, and the survivors of the current update
+__host__ __device__ constexpr int rm_round(int t) { return kRmSpread + t * kSpreadWords; }
+constexpr int kRmSurvivors = rm_round(kMaxGridRounds);
+constexpr int kRmWords = kRmSurvivors + kSpreadWords;
 // A grid-wide round is skipped, and its signals left to the single-workgroup rounds, once
 // fewer than this many survivors are pending.
 constexpr int kTailMin = 128;
@@ -95,6 +108,26 @@ __device__ __forceinline__ void block_count(bool pred, T* ctr, int32_t* acc) {
     atomicAdd(acc, static_cast<int32_t>(__popcll(mask)));
   __syncthreads();
   if (threadIdx.x == 0 && *acc != 0) atomicAdd(ctr, static_cast<T>(*acc));
+}
+
+// The same into the part blockIdx.x mod kSpreadParts of the spread counter at ctr.
+__device__ __forceinline__ void block_count_spread(bool pred, int32_t* ctr, int32_t* acc) {
+  block_count(pred, ctr + static_cast<int>(blockIdx.x % kSpreadParts) * kSpreadStride, acc);
+}
+
+// The value of the spread counter at ctr, in every lane of the calling wave (lane l reads
+// part l).  For a counter written by earlier launches.
+__device__ __forceinline__ int32_t spread_value(const int32_t* ctr) {
+  static_assert(kSpreadParts == 64, "one part per lane");
+  int32_t v = ctr[static_cast<int>(threadIdx.x & 63) * kSpreadStride];
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+// Zeroes the spread counter at ctr: thread tid < kSpreadParts clears part tid.
+__device__ __forceinline__ void spread_clear(int32_t* ctr, int tid) {
+  if (tid < kSpreadParts) ctr[tid * kSpreadStride] = 0;
 }
 
 // A rewrite of per-row counts into offsets (count -> scan of the per-workgroup sums ->
@@ -200,7 +233,7 @@ struct DevState {
   uint8_t* pend;                   // [m_max]       1 pending survivor, 0 otherwise
   int32_t* len;                    // [n_max]       live length of every row of the slack CSR
   int32_t* extra;                  // [n_max]       insertions a row may receive (kept zero)
-  int32_t* rem;                    // [kRmSlots]    round counters (RoundSlot)
+  int32_t* rem;                    // [kRmWords]    round counters (RoundSlot, rm_round)
   int32_t* list;                   // [2 m_max]     pending signals of the last rounds
   // growing-network schedule
   float* ssig;                     // [3 m_max]     signals of the iteration, SoA

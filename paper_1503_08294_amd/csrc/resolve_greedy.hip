@@ -18,11 +18,21 @@ constexpr int kTailBlock = 1024;
 
 inline int blocks(int64_t n) { return static_cast<int>((n + kBlock - 1) / kBlock); }
 
+// Lock words in the checks.  The single-workgroup rounds claim and check in one launch, so
+// their checks read atomically (the claims' minima are made at device scope); a grid-wide
+// check reads words the claims of an earlier launch left (kernel boundaries make them
+// visible to plain loads) while the only writes are releases by the holders, so plain
+// loads and stores serve there: a stale word reads as its claimed key or as all ones, and
+// only the signal that held it at the end of the claims sees its own key.
+template <bool kGrid>
 __device__ __forceinline__ unsigned long long lock_read(unsigned long long* p) {
+  if constexpr (kGrid) return *p;
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+template <bool kGrid>
 __device__ __forceinline__ void lock_release(unsigned long long* p) {
-  __hip_atomic_store(p, ~0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if constexpr (kGrid) *p = ~0ull;
+  else __hip_atomic_store(p, ~0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 struct GreedyArgs {
@@ -68,13 +78,14 @@ __device__ void g_claim(const GreedyArgs& a, int32_t j) {
 // releases them.  For a short row the lock and taken words of all of them are read in one
 // round (the units are distinct, another signal only ever clears a word holding its own key,
 // and a taken mark seen a round later only delays the same rejection).
+template <bool kGrid>
 __device__ uint8_t g_check(const GreedyArgs& a, int32_t j) {
   const int32_t b = a.winner[j], s = a.second[j];
   const unsigned long long key = signal_key(a.d1[j], j, a.key_mode);
   bool blocked = false, holds = true;
   auto visit = [&](int32_t u) {
     blocked |= a.taken[u] != 0;
-    if (lock_read(&a.lock[u]) == key) lock_release(&a.lock[u]); else holds = false;
+    if (lock_read<kGrid>(&a.lock[u]) == key) lock_release<kGrid>(&a.lock[u]); else holds = false;
   };
   const int32_t r0 = a.rp[b], r1 = a.rp[b + 1], l = r1 - r0;
   if (l > kShortRow || l <= 0) {
@@ -94,17 +105,17 @@ __device__ uint8_t g_check(const GreedyArgs& a, int32_t j) {
 #pragma unroll
     for (int k = 0; k < kShortRow; ++k) s_nb |= k < l && c[k] == s;
     const bool tb = a.taken[b] != 0, ts = a.taken[s] != 0;
-    const unsigned long long lb = lock_read(&a.lock[b]), ls = lock_read(&a.lock[s]);
+    const unsigned long long lb = lock_read<kGrid>(&a.lock[b]), ls = lock_read<kGrid>(&a.lock[s]);
     bool tk[kShortRow];
     unsigned long long lk[kShortRow];
 #pragma unroll
     for (int k = 0; k < kShortRow; ++k) {
       tk[k] = a.taken[c[k]] != 0;
-      lk[k] = lock_read(&a.lock[c[k]]);
+      lk[k] = lock_read<kGrid>(&a.lock[c[k]]);
     }
     auto decide = [&](int32_t u, bool t, unsigned long long w) {
       blocked |= t;
-      if (w == key) lock_release(&a.lock[u]); else holds = false;
+      if (w == key) lock_release<kGrid>(&a.lock[u]); else holds = false;
     };
     decide(b, tb, lb);
 #pragma unroll
@@ -133,29 +144,29 @@ __global__ void rg_init(GreedyArgs a) {
   }
 }
 
-// Grid-wide round t; rem[t] counts the signals left pending; rounds after one that left
-// fewer than kTailMin return at once.
+// Grid-wide round t; the spread counter rm_round(t) counts the signals left pending; rounds
+// after one that left fewer than kTailMin return at once.
 __global__ void rg_claim(GreedyArgs a, int32_t t) {
-  if (blockIdx.x == 0 && threadIdx.x == 0) a.rem[t] = 0;
-  if (t > 0 && a.rem[t - 1] < kTailMin) return;
+  if (blockIdx.x == 0) spread_clear(a.rem + rm_round(t), threadIdx.x);
+  if (t > 0 && spread_value(a.rem + rm_round(t - 1)) < kTailMin) return;
   const int32_t j = blockIdx.x * kRoundBlock + threadIdx.x;
   if (j < a.m && a.state[j] == 1) g_claim(a, j);
 }
 
 __global__ void rg_check(GreedyArgs a, int32_t t) {
-  // (the same for every thread: the word was written by an earlier launch)
-  if (t > 0 && a.rem[t - 1] < kTailMin) return;
+  // (the same for every wave: the counter was written by earlier launches)
+  if (t > 0 && spread_value(a.rem + rm_round(t - 1)) < kTailMin) return;
   __shared__ int32_t s_left;
   if (threadIdx.x == 0) s_left = 0;
   __syncthreads();
   const int32_t j = blockIdx.x * kRoundBlock + threadIdx.x;
   bool left = false;
   if (j < a.m && a.state[j] == 1) {
-    const uint8_t st = g_check(a, j);
+    const uint8_t st = g_check<true>(a, j);
     a.state[j] = st;
     left = st == 1;
   }
-  block_count(left, &a.rem[t], &s_left);
+  block_count_spread(left, a.rem + rm_round(t), &s_left);
 }
 
 // The remaining rounds in one workgroup, then the acceptance flags of all signals (and
@@ -178,7 +189,7 @@ __global__ __launch_bounds__(kTailBlock) void rg_tail(GreedyArgs a, uint8_t* acc
     if (n == 0) break;
     for (int32_t i = tid; i < n; i += kTailBlock) g_claim(a, cur[i]);
     __syncthreads();
-    for (int32_t i = tid; i < n; i += kTailBlock) a.state[cur[i]] = g_check(a, cur[i]);
+    for (int32_t i = tid; i < n; i += kTailBlock) a.state[cur[i]] = g_check<false>(a, cur[i]);
     __syncthreads();
     for (int32_t i = tid; i < n; i += kTailBlock)
       if (a.state[cur[i]] == 1) nxt[atomicAdd(&s_next, 1)] = cur[i];

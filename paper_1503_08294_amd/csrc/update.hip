@@ -737,7 +737,7 @@ __global__ void init_state(float* __restrict__ err, int32_t* __restrict__ ins,
   }
   if (i <= n_max) rp[i] = 0;
   if (i < kStSlots) status[i] = 0;
-  if (i < kRmSlots) rem[i] = 0;
+  if (i < kRmWords) rem[i] = 0;
   if (i < kA64Slots) acc64[i] = 0;
 }
 
@@ -747,7 +747,7 @@ inline int blocks(int64_t n) { return static_cast<int>((n + kBlock - 1) / kBlock
 
 hipError_t launch_init(const DevState& s, int cur, int32_t, int32_t n_max, hipStream_t st) {
   const int64_t cover =
-      std::max<int64_t>(static_cast<int64_t>(n_max) + 1, std::max<int>(kStSlots, kRmSlots));
+      std::max<int64_t>(static_cast<int64_t>(n_max) + 1, std::max<int>(kStSlots, kRmWords));
   init_state<<<blocks(cover), kBlock, 0, st>>>(s.err, s.ins, s.orphan, s.rp[cur], s.lock,
                                                s.extra, s.rem, s.acc64, n_max, s.status,
                                                s.bdelta[0], s.bdelta[1]);

@@ -106,7 +106,7 @@ __global__ void wl_prepare(int32_t m, int32_t n, const int32_t* __restrict__ win
   if (threadIdx.x == 0) s_ok = 0;
   __syncthreads();
   const int32_t j = blockIdx.x * kBlock + threadIdx.x;
-  if (j == 0) rem[0] = 0;
+  if (blockIdx.x == 0) spread_clear(rem + rm_round(0), threadIdx.x);
   bool ok = false;
   if (j < m) {
     const bool a = accepted[j] != 0;
@@ -134,7 +134,7 @@ __global__ void wl_prepare(int32_t m, int32_t n, const int32_t* __restrict__ win
       }
     }
   }
-  block_count(ok, &rem[kRmSurvivors], &s_ok);
+  block_count_spread(ok, rem + kRmSurvivors, &s_ok);
 }
 
 // Row sizes for a rewrite: the live length (len, or the CSR row length when len is null)
@@ -229,11 +229,22 @@ constexpr int kTailBlock = 1024;   // threads of the single workgroup of the las
 // rounds of several workgroups and the claims (atomic minima) meet there.  The last rounds
 // run in one workgroup whose phases are separated by barriers, not by kernel ends; the
 // barrier's workgroup-scope ordering covers the rows and flags its waves share.
+// Lock words during the rounds.  In the single-workgroup rounds, claims and checks share one
+// launch, so the checks read the words atomically (the claims' minima are made at device
+// scope).  A grid-wide step reads words that the claims of an earlier launch left (kernel
+// boundaries make those visible to plain loads) and writes only releases (all ones), so
+// plain loads and stores serve there: a stale or released word reads as some other key or
+// all ones, never as the reader's own key unless it held the unit at the end of the
+// claims, so a stale read can only make a survivor wait a round.
+template <bool kGrid>
 __device__ __forceinline__ unsigned long long lock_read(unsigned long long* p) {
+  if constexpr (kGrid) return *p;
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+template <bool kGrid>
 __device__ __forceinline__ void lock_release(unsigned long long* p) {
-  __hip_atomic_store(p, ~0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if constexpr (kGrid) *p = ~0ull;
+  else __hip_atomic_store(p, ~0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 struct RoundArgs {
@@ -289,17 +300,18 @@ __device__ void apply(const RoundArgs& a, int32_t j);
 // A signal that does not go keeps what it holds: those units stay in its F, because F_j
 // loses only winners of survivors that go, which j does not hold, so it claims them again
 // with the same key in the next round, and releases them when it goes.
+template <bool kGrid>
 __device__ bool try_apply(const RoundArgs& a, int32_t j) {
   const int32_t b = a.winner[j], s = a.second[j];
   const unsigned long long key = signal_key(a.d1[j], j, a.key_mode);
-  if (lock_read(&a.lock[b]) != key) return false;
-  bool ok = lock_read(&a.lock[s]) == key;
+  if (lock_read<kGrid>(&a.lock[b]) != key) return false;
+  bool ok = lock_read<kGrid>(&a.lock[s]) == key;
   const int32_t r0 = a.rp[b], r1 = r0 + a.len[b];
-  for (int32_t k = r0; ok && k < r1; ++k) ok = lock_read(&a.lock[a.col[k]]) == key;
+  for (int32_t k = r0; ok && k < r1; ++k) ok = lock_read<kGrid>(&a.lock[a.col[k]]) == key;
   if (!ok) return false;
-  lock_release(&a.lock[b]);
-  lock_release(&a.lock[s]);
-  for (int32_t k = r0; k < r1; ++k) lock_release(&a.lock[a.col[k]]);
+  lock_release<kGrid>(&a.lock[b]);
+  lock_release<kGrid>(&a.lock[s]);
+  for (int32_t k = r0; k < r1; ++k) lock_release<kGrid>(&a.lock[a.col[k]]);
   apply(a, j);
   return true;
 }
@@ -361,8 +373,8 @@ __device__ void apply(const RoundArgs& a, int32_t j) {
 // fewer than kTailMin returns at once (the single-workgroup rounds take them), and so do
 // the later ones (their counts stay zero).
 __global__ void wl_claim(RoundArgs a, int32_t t) {
-  if (blockIdx.x == 0 && threadIdx.x == 0) a.rem[t] = 0;
-  if (t > 0 && a.rem[t - 1] < kTailMin) return;
+  if (blockIdx.x == 0) spread_clear(a.rem + rm_round(t), threadIdx.x);
+  if (t > 0 && spread_value(a.rem + rm_round(t - 1)) < kTailMin) return;
   const int32_t j = blockIdx.x * kRoundBlock + threadIdx.x;
   if (j < a.m && a.pend[j] == 1) claim(a, j);
 }
@@ -379,6 +391,7 @@ __device__ __forceinline__ uint32_t group_bits(unsigned long long wave_mask) {
   return static_cast<uint32_t>(wave_mask >> base) & ((1u << kGroup) - 1);
 }
 
+template <bool kGrid>
 __device__ bool group_try_apply(const RoundArgs& a, int32_t j, int q) {
   const int32_t b = a.winner[j], s = a.second[j];
   const float dj = a.d1[j];
@@ -392,12 +405,12 @@ __device__ bool group_try_apply(const RoundArgs& a, int32_t j, int q) {
   // they are used only if j holds F_j, and then nobody else edits those units or rows
   // during the round; otherwise they are dropped.
   const int32_t r0 = a.rp[b], l = a.len[b];
-  const unsigned long long lb = lock_read(&a.lock[b]);
+  const unsigned long long lb = lock_read<kGrid>(&a.lock[b]);
   unsigned long long ls = 0;
   int32_t r1b = 0;
   float bx = 0.0f, by = 0.0f, bz = 0.0f, be = 0.0f, tx = 0.0f, ty = 0.0f, tz = 0.0f;
   if (q == 0) {
-    ls = lock_read(&a.lock[s]);
+    ls = lock_read<kGrid>(&a.lock[s]);
     r1b = a.rp[b + 1];
     bx = a.x[b]; by = a.y[b]; bz = a.z[b];
     be = a.err[b];
@@ -406,7 +419,7 @@ __device__ bool group_try_apply(const RoundArgs& a, int32_t j, int q) {
   if (lb != key) return false;
   if (l > kGroup) {
     int applied = 0;
-    if (q == 0) applied = try_apply(a, j);
+    if (q == 0) applied = try_apply<kGrid>(a, j);
     return __shfl(applied, static_cast<int>(threadIdx.x & 63) & ~(kGroup - 1)) != 0;
   }
   const bool has = q < l;
@@ -416,7 +429,7 @@ __device__ bool group_try_apply(const RoundArgs& a, int32_t j, int q) {
   if (has) {
     v = a.col[r0 + q];
     a_old = a.age[r0 + q];
-    lv = lock_read(&a.lock[v]);
+    lv = lock_read<kGrid>(&a.lock[v]);
     vx = a.x[v]; vy = a.y[v]; vz = a.z[v];
     vr = a.rp[v];
     vl = a.len[v];
@@ -425,10 +438,10 @@ __device__ bool group_try_apply(const RoundArgs& a, int32_t j, int q) {
   if (q == 0) mine = mine && ls == key;
   if (group_bits(__ballot(!mine)) != 0) return false;
   // j holds F_j: release it, then the step
-  if (has) lock_release(&a.lock[v]);
+  if (has) lock_release<kGrid>(&a.lock[v]);
   if (q == 0) {
-    lock_release(&a.lock[b]);
-    lock_release(&a.lock[s]);
+    lock_release<kGrid>(&a.lock[b]);
+    lock_release<kGrid>(&a.lock[s]);
   }
   // move_unit's expression on positions already loaded
   auto move = [&](int32_t u, float eps, float px, float py, float pz) {
@@ -482,7 +495,8 @@ __device__ bool group_try_apply(const RoundArgs& a, int32_t j, int q) {
 
 __global__ __launch_bounds__(kStepBlock) void wl_step(RoundArgs a, int32_t t) {
   __shared__ int32_t s_left;
-  if (t > 0 && a.rem[t - 1] < kTailMin) return;
+  // (the same for every wave: the counter was written by earlier launches)
+  if (t > 0 && spread_value(a.rem + rm_round(t - 1)) < kTailMin) return;
   if (threadIdx.x == 0) s_left = 0;
   __syncthreads();
   const int32_t gt = blockIdx.x * kStepBlock + threadIdx.x;
@@ -490,13 +504,13 @@ __global__ __launch_bounds__(kStepBlock) void wl_step(RoundArgs a, int32_t t) {
   const int q = gt % kGroup;
   bool left = false;
   if (j < a.m && a.pend[j] == 1) {
-    if (group_try_apply(a, j, q)) {
+    if (group_try_apply<true>(a, j, q)) {
       if (q == 0) a.pend[j] = 0;
     } else {
       left = q == 0;
     }
   }
-  block_count(left, &a.rem[t], &s_left);
+  block_count_spread(left, a.rem + rm_round(t), &s_left);
 }
 
 // The remaining rounds in one workgroup: the pending signals are gathered into a list, and
@@ -507,13 +521,19 @@ __global__ __launch_bounds__(kStepBlock) void wl_step(RoundArgs a, int32_t t) {
 // statistics and clears the survivor count.
 __global__ __launch_bounds__(kTailBlock) void wl_tail(RoundArgs a, int32_t grid_rounds) {
   __shared__ int32_t s_n, s_next, s_rounds, s_ran, s_big;
+  __shared__ int32_t s_pend[kMaxGridRounds + 1];  // the counters' values, survivors last
   const int tid = threadIdx.x;
+  for (int r = tid >> 6; r <= kMaxGridRounds; r += kTailBlock / 64) {
+    const int32_t v = spread_value(a.rem + (r < kMaxGridRounds ? rm_round(r) : kRmSurvivors));
+    if ((tid & 63) == 0) s_pend[r] = v;
+  }
+  __syncthreads();
   if (tid == 0) {
     // grid rounds that ran: the first, then each one after a round that left kTailMin or
     // more; those that applied something: the ones that found survivors pending
     int32_t ran = grid_rounds > 0 ? 1 : 0;
-    while (ran < grid_rounds && a.rem[ran - 1] >= kTailMin) ++ran;
-    s_rounds = ran > 0 && a.rem[kRmSurvivors] > 0 ? ran : 0;
+    while (ran < grid_rounds && s_pend[ran - 1] >= kTailMin) ++ran;
+    s_rounds = ran > 0 && s_pend[kMaxGridRounds] > 0 ? ran : 0;
     a.rem[kRmGridUsed] = ran;
     s_ran = ran;
     s_big = 0;
@@ -535,7 +555,7 @@ __global__ __launch_bounds__(kTailBlock) void wl_tail(RoundArgs a, int32_t grid_
     __syncthreads();
     for (int32_t i = tid / kGroup; i < n; i += kTailBlock / kGroup) {
       const int32_t j = cur[i];
-      if (group_try_apply(a, j, tid % kGroup) && tid % kGroup == 0) a.pend[j] = 0;
+      if (group_try_apply<false>(a, j, tid % kGroup) && tid % kGroup == 0) a.pend[j] = 0;
     }
     __syncthreads();
     for (int32_t i = tid; i < n; i += kTailBlock) {
@@ -559,6 +579,7 @@ __global__ __launch_bounds__(kTailBlock) void wl_tail(RoundArgs a, int32_t grid_
     cur = nxt;
     nxt = t;
   }
+  spread_clear(a.rem + kRmSurvivors, tid);
   if (tid == 0) {
     // the grid-wide rounds this update could have used: those that ran, plus the rounds of
     // this workgroup that started with kTailMin or more pending.  The host reads the count
@@ -566,7 +587,6 @@ __global__ __launch_bounds__(kTailBlock) void wl_tail(RoundArgs a, int32_t grid_
     // never a result); a store straight to its pinned word spares the stream a copy.
     if (a.feedback)
       __hip_atomic_store(a.feedback, s_ran + s_big, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-    a.rem[kRmSurvivors] = 0;
     a.rem[kRmRounds] += s_rounds;
     a.rem[kRmRoundsMax] = max(a.rem[kRmRoundsMax], s_rounds);
     a.rem[kRmUpdates] += 1;
