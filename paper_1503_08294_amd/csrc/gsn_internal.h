@@ -110,6 +110,22 @@ __device__ __forceinline__ void block_count(bool pred, T* ctr, int32_t* acc) {
   if (threadIdx.x == 0 && *acc != 0) atomicAdd(ctr, static_cast<T>(*acc));
 }
 
+// Claims the units col[r0, r0 + l) with an atomic minimum of key, eight entries per batch of
+// loads (slots past the row's end repeat its last entry): the claims of a row wait for one
+// round of loads per eight entries rather than one per entry.
+__device__ __forceinline__ void claim_row(unsigned long long* lock, const int32_t* col,
+                                          int32_t r0, int32_t l, unsigned long long key) {
+  for (int32_t k0 = 0; k0 < l; k0 += 8) {
+    const int32_t n = min(8, l - k0);
+    int32_t c[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) c[k] = col[r0 + k0 + min(k, n - 1)];
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+      if (k < n) atomicMin(&lock[c[k]], key);
+  }
+}
+
 // The same into the part blockIdx.x mod kSpreadParts of the spread counter at ctr.
 __device__ __forceinline__ void block_count_spread(bool pred, int32_t* ctr, int32_t* acc) {
   block_count(pred, ctr + static_cast<int>(blockIdx.x % kSpreadParts) * kSpreadStride, acc);

@@ -61,17 +61,8 @@ __device__ void g_claim(const GreedyArgs& a, int32_t j) {
   const unsigned long long key = signal_key(a.d1[j], j, a.key_mode);
   atomicMin(&a.lock[b], key);
   atomicMin(&a.lock[s], key);
-  const int32_t r0 = a.rp[b], r1 = a.rp[b + 1], l = r1 - r0;
-  if (l > kShortRow) {
-    for (int32_t k = r0; k < r1; ++k) atomicMin(&a.lock[a.col[k]], key);
-  } else if (l > 0) {
-    int32_t c[kShortRow];
-#pragma unroll
-    for (int k = 0; k < kShortRow; ++k) c[k] = a.col[r0 + min(k, l - 1)];
-#pragma unroll
-    for (int k = 0; k < kShortRow; ++k)
-      if (k < l) atomicMin(&a.lock[c[k]], key);
-  }
+  const int32_t r0 = a.rp[b];
+  claim_row(a.lock, a.col, r0, a.rp[b + 1] - r0, key);
 }
 // Visits b, its neighbours and s (once, when it is no neighbour): a unit taken by an
 // accepted signal blocks j for good; j holds the units whose lock word has its key and

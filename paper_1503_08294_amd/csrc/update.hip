@@ -103,18 +103,8 @@ __global__ void rs_claim(int32_t m, int32_t n, const int32_t* __restrict__ winne
   atomicMin(&lock[b], key);
   if (winner_only) return;
   atomicMin(&lock[s], key);
-  const int32_t r0 = rp[b], l = rp[b + 1] - r0;
-  if (l > kShortRow) {
-    for (int32_t k = r0; k < r0 + l; ++k) atomicMin(&lock[col[k]], key);
-  } else if (l > 0) {
-    // one batch of loads (slots past the row's end repeat its last entry)
-    int32_t c[kShortRow];
-#pragma unroll
-    for (int k = 0; k < kShortRow; ++k) c[k] = col[r0 + min(k, l - 1)];
-#pragma unroll
-    for (int k = 0; k < kShortRow; ++k)
-      if (k < l) atomicMin(&lock[c[k]], key);
-  }
+  const int32_t r0 = rp[b];
+  claim_row(lock, col, r0, rp[b + 1] - r0, key);
 }
 
 // With the winner alone locked, the survivor also releases its lock (the other claimants

@@ -120,18 +120,8 @@ __global__ void wl_prepare(int32_t m, int32_t n, const int32_t* __restrict__ win
       const unsigned long long key = signal_key(d1[j], j, key_mode);
       atomicMin(&lock[b], key);
       atomicMin(&lock[s], key);
-      const int32_t r0 = rp[b], l = rp[b + 1] - r0;
-      if (l > 8) {
-        for (int32_t k = r0; k < r0 + l; ++k) atomicMin(&lock[col[k]], key);
-      } else if (l > 0) {
-        // a short row in one batch of loads (slots past its end repeat the last entry)
-        int32_t c[8];
-#pragma unroll
-        for (int k = 0; k < 8; ++k) c[k] = col[r0 + min(k, l - 1)];
-#pragma unroll
-        for (int k = 0; k < 8; ++k)
-          if (k < l) atomicMin(&lock[c[k]], key);
-      }
+      const int32_t r0 = rp[b];
+      claim_row(lock, col, r0, rp[b + 1] - r0, key);
     }
   }
   block_count_spread(ok, rem + kRmSurvivors, &s_ok);
@@ -276,18 +266,7 @@ __device__ void claim(const RoundArgs& a, int32_t j) {
   const unsigned long long key = signal_key(a.d1[j], j, a.key_mode);
   atomicMin(&a.lock[b], key);
   atomicMin(&a.lock[s], key);
-  const int32_t r0 = a.rp[b], l = a.len[b];
-  if (l > 8) {
-    for (int32_t k = r0; k < r0 + l; ++k) atomicMin(&a.lock[a.col[k]], key);
-  } else if (l > 0) {
-    // a short row in one batch of loads (slots past its end repeat the last entry)
-    int32_t c[8];
-#pragma unroll
-    for (int k = 0; k < 8; ++k) c[k] = a.col[r0 + min(k, l - 1)];
-#pragma unroll
-    for (int k = 0; k < 8; ++k)
-      if (k < l) atomicMin(&a.lock[c[k]], key);
-  }
+  claim_row(a.lock, a.col, a.rp[b], a.len[b], key);
 }
 
 __device__ void apply(const RoundArgs& a, int32_t j);
