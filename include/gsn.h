@@ -337,11 +337,11 @@ void gsn_destroy(gsn_net* net);
  *                     1..4096, 0 = default (64)
  *   GSN_TUNE_GRID_ROUNDS  rounds of the GSN_LOCK_WINNER update and of the
  *                     GSN_LOCK_SET_GREEDY resolve launched over the whole device (each
- *                     skipped once fewer than 128 signals are pending) before the remaining
+ *                     skipped once fewer than 32 signals are pending) before the remaining
  *                     ones run in a single workgroup: 1..32, or 0 = automatic (winner lock:
- *                     one more than the rounds the previous update could have used
- *                     grid-wide, i.e. the rounds that started with 128 or more pending, from
- *                     a pinned host copy of that count; greedy resolve: 4)
+ *                     u + u / 4 with u one more than the rounds the previous update could
+ *                     have used grid-wide, i.e. the rounds that started with 32 or more
+ *                     pending, from a pinned host copy of that count; greedy resolve: 4)
  * Returns GSN_E_INVAL for an unknown key or value. */
 enum { GSN_TUNE_SPLIT = 1, GSN_TUNE_VARIANT = 2, GSN_TUNE_GRID_ROUNDS = 3, GSN_TUNE_GRAB = 4,
        GSN_TUNE_REBUCKET = 5 };

@@ -638,7 +638,7 @@ int gsn_adapt(gsn_net* net, const float* sig, int32_t m, const int32_t* winner,
   TimedRegion t(net, GSN_T_ADAPT, st);
   hipError_t e;
   if (net->p.lock_mode == 1 && m > 0 && net->n > 0) {
-    // automatic: one grid round more than the last update used (read from the pinned copy
+    // automatic: from the grid rounds the last update could use (read from the pinned copy
     // of its count; a stale value only changes the split, never the result)
     int g = net->grid_rounds;
     if (g == 0) {

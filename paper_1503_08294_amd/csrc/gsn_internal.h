@@ -70,8 +70,10 @@ __host__ __device__ constexpr int rm_round(int t) { return kRmSpread + t * kSpre
 constexpr int kRmSurvivors = rm_round(kMaxGridRounds);
 constexpr int kRmWords = kRmSurvivors + kSpreadWords;
 // A grid-wide round is skipped, and its signals left to the single-workgroup rounds, once
-// fewer than this many survivors are pending.
-constexpr int kTailMin = 128;
+// fewer than this many survivors are pending (a round of the single workgroup, whose claims
+// and checks share a launch and so use device-scope atomics, costs about as much as a
+// grid-wide round with a few dozen survivors).
+constexpr int kTailMin = 32;
 
 // 64-bit accumulators (DevState::acc64).
 enum Acc64Slot {
