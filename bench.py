@@ -279,11 +279,13 @@ def run_schedule_bench(args):
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": DTYPE,
         "data": "synthetic",
         "config": {"workload": "genus3_schedule", "cloud_points": wl.n_points,
                    "initial_units": 2, "n_max": n_max, **SCHEDULE,
                    "collision": {"lock": args.lock, "key": args.key},
+                   "screen": SCREEN + " above 256 signals per iteration; binary32 direct "
+                             "form at and below",
                    "parallelism": "single"},
         "seconds": el,
         "result": r,
