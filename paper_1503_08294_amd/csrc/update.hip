@@ -657,7 +657,16 @@ __global__ void ed_rewrite(int32_t n, const int32_t* __restrict__ rp,
 #pragma unroll
     for (int k = 0; k < kShortRow; ++k) c += k < l && gv[k] != kDead;
   } else {
-    for (int32_t k = r0; k < r1; ++k) c += age[k] != kDead;
+    // a long row: kShortRow ages per batch of loads (a load per entry, each waited for
+    // before the next, would hold up the whole workgroup)
+    for (int32_t k0 = r0; k0 < r1; k0 += kShortRow) {
+      const int32_t nk = min(kShortRow, r1 - k0);
+      int32_t g[kShortRow];
+#pragma unroll
+      for (int k = 0; k < kShortRow; ++k) g[k] = age[k0 + min(k, nk - 1)];
+#pragma unroll
+      for (int k = 0; k < kShortRow; ++k) c += k < nk && g[k] != kDead;
+    }
   }
   if (apart != nullptr && blockIdx.x == 0) {
     int32_t v = 0;
@@ -699,7 +708,18 @@ __global__ void ed_rewrite(int32_t n, const int32_t* __restrict__ rp,
     for (int k = 0; k < kShortRow; ++k)
       if (k < l) put(cv[k], gv[k]);
   } else {
-    for (int32_t k = r0; k < r1; ++k) put(col[k], age[k]);
+    for (int32_t k0 = r0; k0 < r1; k0 += kShortRow) {
+      const int32_t nk = min(kShortRow, r1 - k0);
+      int32_t cc[kShortRow], g[kShortRow];
+#pragma unroll
+      for (int k = 0; k < kShortRow; ++k) {
+        cc[k] = col[k0 + min(k, nk - 1)];
+        g[k] = age[k0 + min(k, nk - 1)];
+      }
+#pragma unroll
+      for (int k = 0; k < kShortRow; ++k)
+        if (k < nk) put(cc[k], g[k]);
+    }
   }
   if (pending) {
     col_new[o] = extra;
