@@ -154,109 +154,12 @@ __global__ void rs_check(int32_t m, int32_t n, const int32_t* __restrict__ winne
 
 // -------------------------------------------------------------------- adapt ----
 
-// The adaptation of one accepted signal j (winner b, second s).
-__device__ __forceinline__ void adapt_signal(const float* __restrict__ sig, int32_t m,
-                                             int32_t j, int32_t b, int32_t s, float d1j,
-                                             const int32_t* __restrict__ rp,
-                                             const int32_t* __restrict__ col,
-                                             float* __restrict__ x, float* __restrict__ y,
-                                             float* __restrict__ z, float* __restrict__ err,
-                                             float eps_b, float eps_n) {
-  const float sx = sig[j], sy = sig[m + j], sz = sig[2 * m + j];
-  move_unit(x, y, z, b, eps_b, sx, sy, sz);
-  bool s_is_nb = false;
-  for (int32_t k = rp[b]; k < rp[b + 1]; ++k) {
-    const int32_t v = col[k];
-    s_is_nb |= v == s;
-    move_unit(x, y, z, v, eps_n, sx, sy, sz);
-  }
-  if (!s_is_nb) move_unit(x, y, z, s, eps_n, sx, sy, sz);
-  err[b] = err[b] + d1j;
-}
-
-__global__ void ad_move(const float* __restrict__ sig, int32_t m, int32_t n,
-                        const int32_t* __restrict__ winner, const int32_t* __restrict__ second,
-                        const float* __restrict__ d1, const uint8_t* __restrict__ accepted,
-                        const int32_t* __restrict__ rp, const int32_t* __restrict__ col,
-                        float* __restrict__ x, float* __restrict__ y, float* __restrict__ z,
-                        float* __restrict__ err, float eps_b, float eps_n) {
-  const int32_t j = blockIdx.x * kBlock + threadIdx.x;
-  if (j >= m || !accepted[j]) return;
-  const int32_t b = winner[j], s = second[j];
-  if (!pair_ok(b, s, n)) return;
-  adapt_signal(sig, m, j, b, s, d1[j], rp, col, x, y, z, err, eps_b, eps_n);
-}
-
 __global__ void ad_decay(float* __restrict__ err, int32_t n, float beta) {
   const int32_t i = blockIdx.x * kBlock + threadIdx.x;
   if (i < n) err[i] = err[i] * beta;
 }
 
 // -------------------------------------------------------------------- edges ----
-
-// Per accepted signal: age the edges at b (both half-edges), reset or request the edge
-// {b, s}, then mark the edges at b older than max_age as dead and flag neighbours left
-// without a live edge.  Rows touched belong to L_j only, so threads never share a row.
-// The connection update of one accepted signal (winner b, second s) on its own rows.
-__device__ __forceinline__ void mark_signal(int32_t b, int32_t s,
-                                            const int32_t* __restrict__ rp,
-                                            const int32_t* __restrict__ col,
-                                            int32_t* __restrict__ age, int32_t* __restrict__ ins,
-                                            int32_t* __restrict__ orphan,
-                                            int32_t* __restrict__ status, int32_t max_age,
-                                            int32_t* __restrict__ bdelta) {
-  const int32_t r0 = rp[b], r1 = rp[b + 1];
-  bool found = false;
-  for (int32_t k = r0; k < r1; ++k) {
-    const int32_t v = col[k];
-    int32_t a = age[k] + 1;
-    if (v == s) {
-      a = 0;
-      found = true;
-    }
-    age[k] = a;
-    const int32_t rk = find_in_short_span(col, rp[v], rp[v + 1], b);
-    if (rk >= 0) age[rk] = a;
-  }
-  if (!found) {
-    ins[b] = s;
-    ins[s] = b;
-    atomicAdd(&bdelta[b / kBlock], 1);
-    atomicAdd(&bdelta[s / kBlock], 1);
-  }
-  for (int32_t k = r0; k < r1; ++k) {
-    if (age[k] <= max_age) continue;
-    const int32_t v = col[k];
-    age[k] = kDead;
-    atomicAdd(&bdelta[b / kBlock], -1);
-    const int32_t rk = find_in_row(rp, col, v, b);
-    if (rk >= 0) {
-      age[rk] = kDead;
-      atomicAdd(&bdelta[v / kBlock], -1);
-    }
-    bool live = ins[v] >= 0;
-    for (int32_t kk = rp[v]; !live && kk < rp[v + 1]; ++kk) live = age[kk] != kDead;
-    if (!live && !orphan[v]) {
-      orphan[v] = 1;
-      atomicAdd(&status[kStOrphans], 1);
-    }
-  }
-}
-
-
-__global__ void ed_mark(int32_t m, int32_t n, const int32_t* __restrict__ winner,
-                        const int32_t* __restrict__ second,
-                        const uint8_t* __restrict__ accepted, const int32_t* __restrict__ rp,
-                        const int32_t* __restrict__ col, int32_t* __restrict__ age,
-                        int32_t* __restrict__ ins, int32_t* __restrict__ orphan,
-                        int32_t* __restrict__ status, int32_t max_age,
-                        int32_t* __restrict__ bdelta) {
-  const int32_t j = blockIdx.x * kBlock + threadIdx.x;
-  if (j >= m || !accepted[j]) return;
-  const int32_t b = winner[j], s = second[j];
-  if (!pair_ok(b, s, n)) return;
-  mark_signal(b, s, rp, col, age, ins, orphan, status, max_age, bdelta);
-}
 
 // The lock-set resolve of rs_check fused with the update of the accepted signals (the
 // adaptation of ad_move and the marks of ed_mark): an accepted lock set is held by its
@@ -298,6 +201,108 @@ __device__ __forceinline__ uint32_t group_bits(unsigned long long wave_mask) {
   return static_cast<uint32_t>(wave_mask >> base) & ((1u << kGroup) - 1);
 }
 
+// The separate adaptation (gsn_adapt) of the accepted signals (Eq. (adaptation)): the winner
+// b moves eps_b of the way to the signal, its neighbours and the second (once, when it is no
+// neighbour) eps_n, by move_unit, and d1 is added to b's error.  A group of kGroup lanes per
+// signal: lane q moves the neighbours k = q, q + kGroup, ... of b, lane 0 the winner and the
+// second (whether s is a neighbour comes from a ballot over the group).  Accepted lock sets
+// are disjoint, so every unit moves once: the result is that of the signals applied one
+// after another.
+__global__ void ad_move(const float* __restrict__ sig, int32_t m, int32_t n,
+                        const int32_t* __restrict__ winner, const int32_t* __restrict__ second,
+                        const float* __restrict__ d1, const uint8_t* __restrict__ accepted,
+                        const int32_t* __restrict__ rp, const int32_t* __restrict__ col,
+                        float* __restrict__ x, float* __restrict__ y, float* __restrict__ z,
+                        float* __restrict__ err, float eps_b, float eps_n) {
+  const int64_t gt = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  const int32_t j = static_cast<int32_t>(gt / kGroup);
+  const int q = static_cast<int>(gt % kGroup);
+  int32_t b = 0, s = 0;
+  const bool act = j < m && accepted[j] && pair_ok(b = winner[j], s = second[j], n);
+  float sx = 0.0f, sy = 0.0f, sz = 0.0f;
+  bool is_s = false;
+  if (act) {
+    sx = sig[j];
+    sy = sig[m + j];
+    sz = sig[2 * m + j];
+    for (int32_t k = rp[b] + q; k < rp[b + 1]; k += kGroup) {
+      const int32_t v = col[k];
+      is_s |= v == s;
+      move_unit(x, y, z, v, eps_n, sx, sy, sz);
+    }
+  }
+  const bool s_nb = group_bits(__ballot(is_s)) != 0;
+  if (act && q == 0) {
+    move_unit(x, y, z, b, eps_b, sx, sy, sz);
+    if (!s_nb) move_unit(x, y, z, s, eps_n, sx, sy, sz);
+    err[b] = err[b] + d1[j];
+  }
+}
+
+// The separate connection update (gsn_update_edges) of the accepted signals: every edge at b
+// is aged by one on both half-edges, the edge {b, s} reset to age 0 (or requested when it is
+// missing), the edges at b older than max_age marked dead on both half-edges, and a
+// neighbour left without a live or requested edge flagged for removal.  A group of kGroup
+// lanes per signal: lane q takes the neighbours k = q, q + kGroup, ... of b (ages, then
+// removals), lane 0 the request.  The rows touched belong to L_j only, and the lane of
+// neighbour v alone writes the row of v, so the result is that of the signals applied one
+// after another.
+__global__ void ed_mark(int32_t m, int32_t n, const int32_t* __restrict__ winner,
+                        const int32_t* __restrict__ second,
+                        const uint8_t* __restrict__ accepted, const int32_t* __restrict__ rp,
+                        const int32_t* __restrict__ col, int32_t* __restrict__ age,
+                        int32_t* __restrict__ ins, int32_t* __restrict__ orphan,
+                        int32_t* __restrict__ status, int32_t max_age,
+                        int32_t* __restrict__ bdelta) {
+  const int64_t gt = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  const int32_t j = static_cast<int32_t>(gt / kGroup);
+  const int q = static_cast<int>(gt % kGroup);
+  int32_t b = 0, s = 0;
+  const bool act = j < m && accepted[j] && pair_ok(b = winner[j], s = second[j], n);
+  int32_t r0 = 0, r1 = 0;
+  bool found = false;
+  if (act) {
+    r0 = rp[b];
+    r1 = rp[b + 1];
+    for (int32_t k = r0 + q; k < r1; k += kGroup) {
+      const int32_t v = col[k];
+      int32_t a = age[k] + 1;
+      if (v == s) {
+        a = 0;
+        found = true;
+      }
+      age[k] = a;
+      const int32_t rk = find_in_short_span(col, rp[v], rp[v + 1], b);
+      if (rk >= 0) age[rk] = a;
+    }
+  }
+  const bool s_nb = group_bits(__ballot(found)) != 0;
+  if (act && q == 0 && !s_nb) {
+    ins[b] = s;
+    ins[s] = b;
+    atomicAdd(&bdelta[b / kBlock], 1);
+    atomicAdd(&bdelta[s / kBlock], 1);
+  }
+  if (!act) return;
+  for (int32_t k = r0 + q; k < r1; k += kGroup) {
+    if (age[k] <= max_age) continue;
+    const int32_t v = col[k];
+    age[k] = kDead;
+    atomicAdd(&bdelta[b / kBlock], -1);
+    const int32_t rk = find_in_row(rp, col, v, b);
+    if (rk >= 0) {
+      age[rk] = kDead;
+      atomicAdd(&bdelta[v / kBlock], -1);
+    }
+    bool live = ins[v] >= 0;
+    for (int32_t kk = rp[v]; !live && kk < rp[v + 1]; ++kk) live = age[kk] != kDead;
+    if (!live && !orphan[v]) {
+      orphan[v] = 1;
+      atomicAdd(&status[kStOrphans], 1);
+    }
+  }
+}
+
 // Claims of the lock sets L_j = {b, s} + N(b), as rs_claim.
 __global__ void fu_claim(int32_t m, int32_t n, const int32_t* __restrict__ winner,
                          const int32_t* __restrict__ second, const float* __restrict__ d1,
@@ -321,8 +326,8 @@ __global__ void fu_claim(int32_t m, int32_t n, const int32_t* __restrict__ winne
   for (int32_t k = rp[b] + q; k < rp[b + 1]; k += kGroup) atomicMin(&lock[col[k]], key);
 }
 
-// The check of rs_check and, for an accepted signal, the adaptation of adapt_signal and
-// the marks of mark_signal, with the same result: each unit of L_j is moved once with the
+// The check of rs_check and, for an accepted signal, the adaptation of ad_move and the marks
+// of ed_mark, with the same result: each unit of L_j is moved once with the
 // same expression, every edge at b is aged (or reset, for {b, s}) and, if older than
 // max_age, marked dead on both half-edges, and a neighbour left without a live edge or a
 // requested one is flagged.  The lane of neighbour v alone writes the row of v, so its
@@ -782,8 +787,9 @@ hipError_t launch_adapt(const DevState& s, int cur, int32_t n, const float* sig,
                         const uint8_t* accepted, float eps_b, float eps_n, float beta,
                         hipStream_t st) {
   if (m > 0)
-    ad_move<<<blocks(m), kBlock, 0, st>>>(sig, m, n, winner, second, d1, accepted, s.rp[cur],
-                                          s.col[cur], s.x, s.y, s.z, s.err, eps_b, eps_n);
+    ad_move<<<blocks(static_cast<int64_t>(m) * kGroup), kBlock, 0, st>>>(
+        sig, m, n, winner, second, d1, accepted, s.rp[cur], s.col[cur], s.x, s.y, s.z, s.err,
+        eps_b, eps_n);
   if (n > 0) ad_decay<<<blocks(n), kBlock, 0, st>>>(s.err, n, beta);
   return hipGetLastError();
 }
@@ -796,9 +802,9 @@ hipError_t launch_edges(const DevState& s, int cur, int dpar, int32_t n, int32_t
   int32_t* bd = s.bdelta[dpar];
   int32_t* bd_next = s.bdelta[dpar ^ 1];
   if (m > 0)
-    ed_mark<<<blocks(m), kBlock, 0, st>>>(m, n, winner, second, accepted, s.rp[cur],
-                                          s.col[cur], s.age[cur], s.ins, s.orphan, s.status,
-                                          max_age, bd);
+    ed_mark<<<blocks(static_cast<int64_t>(m) * kGroup), kBlock, 0, st>>>(
+        m, n, winner, second, accepted, s.rp[cur], s.col[cur], s.age[cur], s.ins, s.orphan,
+        s.status, max_age, bd);
   const int nb = blocks(n);
   if (n == 0) return hipGetLastError();
   if (nb <= kFoldBlocks) {
