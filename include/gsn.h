@@ -220,8 +220,12 @@ int gsn_update_edges(gsn_net* net, int32_t m, const int32_t* winner, const int32
  * With GSN_LOCK_SET the update runs fused: the find's merge makes the claims, resolve's
  * check applies each accepted signal's adaptation and edge marks at once (accepted lock
  * sets are disjoint), and one rewrite of the adjacency applies the error decay: two update
- * launches after the find instead of six.  The other rules run the four steps.  Outputs:
- * device arrays of length m.  Async. */
+ * launches after the find instead of six.  With GSN_LOCK_WINNER the resolve leaves at most
+ * one survivor per winner unit, so each edge changes only in the steps of its two ends'
+ * survivors: the update of gsn_adapt is computed per unit in one pass instead of rounds
+ * (its moves applied in key order, its edges after the two steps that can change each,
+ * its removal mark), in three launches after the resolve, with the same result.
+ * GSN_LOCK_SET_GREEDY runs the four steps.  Outputs: device arrays of length m.  Async. */
 int gsn_iterate(gsn_net* net, const float* sig, int32_t m, int32_t* winner, int32_t* second,
                 float* d1, float* d2, uint8_t* accepted, void* stream);
 
@@ -335,7 +339,7 @@ void gsn_destroy(gsn_net* net);
  *   GSN_TUNE_REBUCKET staged find calls (variants 2-5) between rebuilds of the spatial order
  *                     of the units (it is also rebuilt whenever N or the indices change):
  *                     1..4096, 0 = default (64)
- *   GSN_TUNE_GRID_ROUNDS  rounds of the GSN_LOCK_WINNER update and of the
+ *   GSN_TUNE_GRID_ROUNDS  rounds of the GSN_LOCK_WINNER update of gsn_adapt and of the
  *                     GSN_LOCK_SET_GREEDY resolve launched over the whole device (each
  *                     skipped once fewer than 32 signals are pending) before the remaining
  *                     ones run in a single workgroup: 1..32, or 0 = automatic (winner lock:
@@ -362,7 +366,9 @@ int gsn_tune(gsn_net* net, int32_t key, int32_t value);
  *                     batches, whose steps are bound by launches) take a marker pair
  *   GSN_T_FIND        all of gsn_find_winners
  *   GSN_T_RESOLVE, GSN_T_ADAPT, GSN_T_EDGES   all of the corresponding call
- *   GSN_T_UPDATE      the fused update of gsn_iterate (resolve, adapt and edges) */
+ *   GSN_T_UPDATE      the fused update of gsn_iterate (with GSN_LOCK_SET resolve, adapt
+ *                     and edges; with GSN_LOCK_WINNER adapt and edges, the resolve being
+ *                     timed as GSN_T_RESOLVE) */
 enum { GSN_T_FIND_SCAN = 0, GSN_T_FIND = 1, GSN_T_RESOLVE = 2, GSN_T_ADAPT = 3,
        GSN_T_EDGES = 4, GSN_T_UPDATE = 5, GSN_T_COUNT = 6 };
 int gsn_timing_enable(gsn_net* net, int32_t enable);
@@ -378,7 +384,8 @@ int gsn_timing_select(gsn_net* net, uint32_t mask);
  *                        every pending survivor whose units no pending survivor of smaller
  *                        key touches)
  *   GSN_STAT_ROUNDS_MAX  the most rounds one such update took
- *   GSN_STAT_UPDATES     gsn_adapt calls that applied the winner-lock update
+ *   GSN_STAT_UPDATES     gsn_adapt calls that applied the winner-lock update in rounds
+ *                        (gsn_iterate takes it in one pass and counts no rounds)
  *   GSN_STAT_CLEAR       sets every statistic to zero (value may be NULL)
  *   GSN_STAT_RESOLVED    signals that went through gsn_resolve_conflicts
  *   GSN_STAT_ACCEPTED    of those, the accepted ones

@@ -92,6 +92,12 @@ Layout layout_for(const gsn_params& p) {
   add(8 * small_part_keys(p.m_max));  // 32 partial keys of the small-batch scan
   add(4 * (nm / kBlock + 2));  // 33 per-block half-edge changes, set 0
   add(4 * (nm / kBlock + 2));  // 34 per-block half-edge changes, set 1
+  const bool wl = p.lock_mode == 1;
+  add(wl ? 16 * nm : 0);       // 35 survivor keys, two parities
+  add(wl ? 8 * nm : 0);        // 36 survivor seconds, two parities
+  add(wl ? 8 * nm : 0);        // 37 heads of the second lists, two parities
+  add(wl ? 4 * mm : 0);        // 38 links of the second lists
+  add(wl ? 8 : 0);             // 39 table bounds
   L.total = (o + 255) & ~static_cast<size_t>(255);
   return L;
 }
@@ -134,6 +140,12 @@ void carve(const gsn_params& p, void* base, DevState* s) {
   s->spart = reinterpret_cast<unsigned long long*>(b + L.off[32]);
   s->bdelta[0] = reinterpret_cast<int32_t*>(b + L.off[33]);
   s->bdelta[1] = reinterpret_cast<int32_t*>(b + L.off[34]);
+  const bool wl = p.lock_mode == 1;
+  s->wkey = wl ? reinterpret_cast<unsigned long long*>(b + L.off[35]) : nullptr;
+  s->wsec = wl ? reinterpret_cast<int32_t*>(b + L.off[36]) : nullptr;
+  s->rhead = wl ? reinterpret_cast<int32_t*>(b + L.off[37]) : nullptr;
+  s->rnext = wl ? reinterpret_cast<int32_t*>(b + L.off[38]) : nullptr;
+  s->whi = wl ? reinterpret_cast<int32_t*>(b + L.off[39]) : nullptr;
 }
 
 }  // namespace gsn
@@ -152,6 +164,7 @@ struct gsn_net {
   int32_t n;        // live units (host copy, changed only by grow/import)
   int cur;          // current CSR buffer
   int dpar;         // which per-block delta array the next lock-set edge update uses
+  int wpar;         // which survivor tables the next one-pass winner-lock update uses
   int phase;
   int cus;          // compute units of the device
   int tune_split;
@@ -179,12 +192,12 @@ struct gsn_net {
     float *d1, *d2;
     uint8_t* accepted;
     int32_t n;
-    int cur, dpar, stage_parity;
+    int cur, dpar, wpar, stage_parity;
     bool rebuild_first;
     int tune_split, tune_variant, tune_grab, tune_rebucket, grid_rounds;
     // the host state the loop leaves
     bool rebuilt;   // the first find rebuilt the unit order (else finds_delta counts finds)
-    int cur_after, dpar_after, stage_parity_after;
+    int cur_after, dpar_after, wpar_after, stage_parity_after;
     int32_t finds_after, finds_delta, bucket_n_after;
     hipGraphExec_t exec;
     uint64_t used;
@@ -392,6 +405,7 @@ int gsn_create(const gsn_params* params, void* workspace, size_t workspace_bytes
   net->n = n0;
   net->cur = 0;
   net->dpar = 0;
+  net->wpar = 0;
   net->phase = kReady;
   net->tune_split = 0;
   net->tune_variant = 0;
@@ -692,6 +706,21 @@ int gsn_iterate(gsn_net* net, const float* sig, int32_t m, int32_t* winner, int3
     int rc = gsn_find_winners(net, sig, m, winner, second, d1, d2, stream);
     if (rc) return rc;
     if ((rc = gsn_resolve_conflicts(net, m, winner, second, d1, accepted, stream))) return rc;
+    if (net->p.lock_mode == 1 && m > 0) {
+      // the resolve leaves one survivor per winner: the update in one pass, no rounds
+      hipStream_t st = as_stream(stream);
+      TimedRegion t(net, GSN_T_UPDATE, st);
+      gsn::WinnerStep w{sig, m, winner, second, d1, accepted, net->p.key_mode, net->p.eps_b,
+                        net->p.eps_n, net->p.err_beta, net->p.max_age, 0, 0,
+                        2 * static_cast<int64_t>(net->p.e_max), nullptr, net->p.n_max};
+      const hipError_t e = gsn::launch_winner_local(net->s, net->cur, net->wpar, net->n, w, st);
+      t.end();
+      if (e != hipSuccess) return GSN_E_HIP;
+      net->cur ^= 1;
+      net->wpar ^= 1;
+      net->phase = kReady;
+      return GSN_OK;
+    }
     if ((rc = gsn_adapt(net, sig, m, winner, second, d1, accepted, stream))) return rc;
     return gsn_update_edges(net, m, winner, second, accepted, stream);
   }
@@ -734,7 +763,7 @@ int gsn_iterate_loop(gsn_net* net, const float* sigs, int32_t m, int32_t count,
   auto same = [&](const LoopGraph& g) {
     return g.sigs == sigs && g.m == m && g.count == count && g.winner == winner &&
            g.second == second && g.d1 == d1 && g.d2 == d2 && g.accepted == accepted &&
-           g.n == net->n && g.cur == net->cur && g.dpar == net->dpar &&
+           g.n == net->n && g.cur == net->cur && g.dpar == net->dpar && g.wpar == net->wpar &&
            g.stage_parity == net->stage_parity && g.rebuild_first == rebuild_first &&
            g.tune_split == net->tune_split && g.tune_variant == net->tune_variant &&
            g.tune_grab == net->tune_grab && g.tune_rebucket == net->tune_rebucket &&
@@ -752,14 +781,16 @@ int gsn_iterate_loop(gsn_net* net, const float* sigs, int32_t m, int32_t count,
     LoopGraph g{};
     g.sigs = sigs; g.m = m; g.count = count;
     g.winner = winner; g.second = second; g.d1 = d1; g.d2 = d2; g.accepted = accepted;
-    g.n = net->n; g.cur = net->cur; g.dpar = net->dpar; g.stage_parity = net->stage_parity;
+    g.n = net->n; g.cur = net->cur; g.dpar = net->dpar; g.wpar = net->wpar;
+    g.stage_parity = net->stage_parity;
     g.rebuild_first = rebuild_first;
     g.tune_split = net->tune_split; g.tune_variant = net->tune_variant;
     g.tune_grab = net->tune_grab; g.tune_rebucket = net->tune_rebucket;
     g.grid_rounds = net->grid_rounds;
     // record the loop: the calls run on the host as usual (argument checks, state), their
     // launches go into the graph
-    const int cur0 = net->cur, dpar0 = net->dpar, sp0 = net->stage_parity, phase0 = net->phase;
+    const int cur0 = net->cur, dpar0 = net->dpar, wpar0 = net->wpar, sp0 = net->stage_parity;
+    const int phase0 = net->phase;
     const int32_t bn0 = net->bucket_n, f0 = net->finds_since_bucket;
     (void)hipGetLastError();
     if (hipStreamBeginCapture(net->cap_stream, hipStreamCaptureModeThreadLocal) != hipSuccess)
@@ -784,20 +815,21 @@ int gsn_iterate_loop(gsn_net* net, const float* sigs, int32_t m, int32_t count,
     if (graph) (void)hipGraphDestroy(graph);
     if (rc != GSN_OK || !exec) {
       // nothing ran: the handle is as before the call
-      net->cur = cur0; net->dpar = dpar0; net->stage_parity = sp0; net->phase = phase0;
+      net->cur = cur0; net->dpar = dpar0; net->wpar = wpar0; net->stage_parity = sp0;
+      net->phase = phase0;
       net->bucket_n = bn0; net->finds_since_bucket = f0;
       (void)hipGetLastError();
       return rc != GSN_OK ? rc : GSN_E_HIP;
     }
     g.exec = exec;
     g.rebuilt = rebuilt;
-    g.cur_after = net->cur; g.dpar_after = net->dpar;
+    g.cur_after = net->cur; g.dpar_after = net->dpar; g.wpar_after = net->wpar;
     g.stage_parity_after = net->stage_parity;
     g.finds_after = net->finds_since_bucket;
     g.finds_delta = net->finds_since_bucket - f0;
     g.bucket_n_after = net->bucket_n;
     // the host state is back at the start until the graph is launched below
-    net->cur = cur0; net->dpar = dpar0; net->stage_parity = sp0;
+    net->cur = cur0; net->dpar = dpar0; net->wpar = wpar0; net->stage_parity = sp0;
     net->bucket_n = bn0; net->finds_since_bucket = f0;
     if (net->graphs.size() >= GSN_GRAPH_CACHE) {
       size_t old = 0;
@@ -814,6 +846,7 @@ int gsn_iterate_loop(gsn_net* net, const float* sigs, int32_t m, int32_t count,
   if (hipGraphLaunch(hit->exec, st) != hipSuccess) return GSN_E_HIP;
   net->cur = hit->cur_after;
   net->dpar = hit->dpar_after;
+  net->wpar = hit->wpar_after;
   net->stage_parity = hit->stage_parity_after;
   if (hit->rebuilt) {
     net->finds_since_bucket = hit->finds_after;
@@ -1035,12 +1068,18 @@ int gsn_import(gsn_net* net, int32_t n, const float* xyz, const float* err, int3
     fill_bytes(s.status, 0, 4 * gsn::kStSlots);
     fill_bytes(s.bdelta[0], 0, 4 * (nm / gsn::kBlock + 2));
     fill_bytes(s.bdelta[1], 0, 4 * (nm / gsn::kBlock + 2));
+    if (s.wkey) {
+      fill_bytes(s.wkey, 0xff, 16 * nm);
+      fill_bytes(s.rhead, 0xff, 8 * nm);
+      fill_bytes(s.whi, 0, 8);
+    }
     ok = ok && gsn::launch_stage_init(gsn::carve_stage(s.scr, net->p.n_max, net->p.m_max),
                                       st) == hipSuccess;
     ok = hipStreamSynchronize(st) == hipSuccess && ok;
     if (!ok) return GSN_E_HIP;
     net->n = n;
     net->dpar = 0;
+    net->wpar = 0;
     net->stage_parity = 0;   // both histogram sets were cleared above
     net->phase = kReady;
     net->bucket_n = -1;

@@ -253,6 +253,15 @@ struct DevState {
   int32_t* extra;                  // [n_max]       insertions a row may receive (kept zero)
   int32_t* rem;                    // [kRmWords]    round counters (RoundSlot, rm_round)
   int32_t* list;                   // [2 m_max]     pending signals of the last rounds
+  // one-pass update of the winner-lock survivors (winner lock only; null otherwise): two
+  // parities of survivor tables, parity q at offset q n_max, taken by successive updates in
+  // turn
+  unsigned long long* wkey;        // [2 n_max]     key of the survivor a unit is winner of,
+                                   //               all ones for none
+  int32_t* wsec;                   // [2 n_max]     that survivor's second
+  int32_t* rhead;                  // [2 n_max]     a survivor whose second is the unit, -1 none
+  int32_t* rnext;                  // [m_max]       the next survivor with the same second
+  int32_t* whi;                    // [2]           tables of parity q hold entries below whi[q]
   // growing-network schedule
   float* ssig;                     // [3 m_max]     signals of the iteration, SoA
   int32_t *swin, *ssec;            // [m_max]
@@ -403,9 +412,16 @@ struct WinnerStep {
   int grid_rounds;   // 0..kMaxGridRounds
   int64_t slack_cap, half_cap;
   int32_t* feedback; // pinned host word (device address) that receives the grid rounds used
+  int32_t n_max;     // (the one-pass update: the stride of the table parities)
 };
 hipError_t launch_winner_update(const DevState& s, int cur, int32_t n, const WinnerStep& w,
                                 hipStream_t st);
+// The same update in three launches, for survivors with pairwise distinct winners (those of
+// the winner-lock resolve): survivor tables, the moves with the new degrees, and the rows,
+// written into buffer cur ^ 1 with the error decay (grid_rounds and feedback are not used).
+// par selects the survivor tables; consecutive calls must alternate it.
+hipError_t launch_winner_local(const DevState& s, int cur, int par, int32_t n,
+                               const WinnerStep& w, hipStream_t st);
 // The lock-set resolve, adaptation and edge update of one iteration: the claims (unless the
 // find's merge made them, claimed = true); the check fused with the accepted signals'
 // updates, taking the signals in the given order when order is not null (a permutation of

@@ -737,8 +737,17 @@ __global__ void init_state(float* __restrict__ err, int32_t* __restrict__ ins,
                            unsigned long long* __restrict__ lock, int32_t* __restrict__ extra,
                            int32_t* __restrict__ rem, unsigned long long* __restrict__ acc64,
                            int32_t n_max, int32_t* __restrict__ status,
-                           int32_t* __restrict__ bd0, int32_t* __restrict__ bd1) {
+                           int32_t* __restrict__ bd0, int32_t* __restrict__ bd1,
+                           unsigned long long* __restrict__ wkey, int32_t* __restrict__ rhead,
+                           int32_t* __restrict__ whi) {
   const int32_t i = blockIdx.x * kBlock + threadIdx.x;
+  if (wkey && i < n_max) {
+    wkey[i] = ~0ull;
+    wkey[n_max + i] = ~0ull;
+    rhead[i] = -1;
+    rhead[n_max + i] = -1;
+  }
+  if (whi && i < 2) whi[i] = 0;
   if (i < n_max / kBlock + 2) {
     bd0[i] = 0;
     bd1[i] = 0;
@@ -765,7 +774,8 @@ hipError_t launch_init(const DevState& s, int cur, int32_t, int32_t n_max, hipSt
       std::max<int64_t>(static_cast<int64_t>(n_max) + 1, std::max<int>(kStSlots, kRmWords));
   init_state<<<blocks(cover), kBlock, 0, st>>>(s.err, s.ins, s.orphan, s.rp[cur], s.lock,
                                                s.extra, s.rem, s.acc64, n_max, s.status,
-                                               s.bdelta[0], s.bdelta[1]);
+                                               s.bdelta[0], s.bdelta[1], s.wkey, s.rhead,
+                                               s.whi);
   return hipGetLastError();
 }
 

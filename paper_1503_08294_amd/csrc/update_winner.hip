@@ -575,6 +575,314 @@ __global__ __launch_bounds__(kTailBlock) void wl_tail(RoundArgs a, int32_t grid_
   }
 }
 
+// ---------------------------------------------------------- one-pass update ----
+//
+// The same update when no two survivors share a winner, as after the winner-lock resolve.
+// Then a unit u is the winner of at most one step E_u (key k_u, second t_u), and the edge
+// {u, v} changes only in E_u and E_v: a step ages it by one, or sets it to age 0 (creating
+// it) when the step's second is the other end, and then removes it if it is older than
+// max_age.  The state of every edge before or after any step therefore follows from its
+// state before the update and those two steps alone, and so does all that the sequential
+// update does to a unit x:
+//   * x moves in E_x (eps_b) and, once with eps_n, in every E_b (b != x) whose second is x
+//     or that finds {b, x} alive, which means alive after E_x when k_x < k_b; a move reads
+//     and writes the moved unit only, so the moves of x applied to it in ascending key
+//     order give its position after the sequential update;
+//   * its row afterwards holds its edges alive after the steps of both ends, with their
+//     ages;
+//   * it is marked for removal when some E_v removes {v, x} and no edge of x is alive right
+//     after E_v;
+//   * its error grows by d1 in E_x.
+// The steps that can involve x are those of x, of its neighbours before the update, of the
+// survivors whose second is x (a list per unit, rhead / rnext), and that of the second of
+// E_x.  One thread per unit finds them: three launches and no rounds.  The tables have two
+// parities so that the update can clear the other parity while it reads its own: an update
+// with parity q finds tables q clean, fills them below n (whi[q] = n), and clears tables
+// q ^ 1 below whi[q ^ 1], which the previous update filled.
+
+struct LocalArgs {
+  const float* sig;
+  int32_t m, n;
+  const int32_t* winner;
+  const int32_t* second;
+  const float* d1;
+  const uint8_t* accepted;
+  int key_mode;
+  unsigned long long* wkey;  // tables of this update's parity
+  int32_t* wsec;
+  int32_t* rhead;
+  int32_t* rnext;
+  unsigned long long* wkey_o;  // tables of the other parity (cleared by wu_write)
+  int32_t* rhead_o;
+  int32_t* whi;
+  int par;
+  const int32_t* rp;  // adjacency before the update
+  const int32_t* col;
+  const int32_t* age;
+  int32_t* rp2;  // adjacency after it
+  int32_t* col2;
+  int32_t* age2;
+  float *x, *y, *z, *err;
+  int32_t* orphan;
+  int32_t* status;
+  int32_t* cnt;
+  int32_t* bsum;
+  float eps_b, eps_n, beta;
+  int32_t max_age;
+  int64_t cap;
+  int32_t nb;
+  int fold;
+};
+
+// Survivor tables: the key and second of the step each winner takes, and the list of the
+// survivors by second.  Requires pairwise distinct winners among the accepted signals.
+__global__ void wu_tables(LocalArgs a) {
+  const int32_t j = blockIdx.x * kBlock + threadIdx.x;
+  if (j == 0) a.whi[a.par] = a.n;
+  if (j >= a.m || !a.accepted[j]) return;
+  const int32_t b = a.winner[j], s = a.second[j];
+  if (!pair_ok(b, s, a.n)) {
+    raise_error(a.status, GSN_E_INVAL);
+    return;
+  }
+  a.wkey[b] = signal_key(a.d1[j], j, a.key_mode);
+  a.wsec[b] = s;
+  a.rnext[j] = atomicExch(&a.rhead[s], j);
+}
+
+struct Surv {
+  unsigned long long key;  // all ones: the unit takes no step as a winner
+  int32_t sec;             // the step's second (meaningful only with a key)
+};
+
+__device__ __forceinline__ Surv surv_of(const LocalArgs& a, int32_t u) {
+  return Surv{a.wkey[u], a.wsec[u]};
+}
+
+__device__ __forceinline__ bool has_step(const Surv& s) { return s.key != ~0ull; }
+
+// One step on an edge, taken by one of its ends: age 0 (the edge created if absent) when
+// the step's second is the other end, else one year older if alive, then removed if older
+// than max_age.  Returns whether this step removed it.
+__device__ __forceinline__ bool edge_event(bool& alive, int32_t& ag, bool to_other,
+                                           int32_t max_age) {
+  if (to_other) {
+    alive = true;
+    ag = 0;
+    return false;
+  }
+  if (!alive) return false;
+  ag += 1;
+  if (ag > max_age) {
+    alive = false;
+    return true;
+  }
+  return false;
+}
+
+struct EdgeState {
+  bool alive;
+  int32_t age;
+  bool removed_by_w;  // the step of w removed it
+};
+
+// The edge {x, w} after those steps of x and w whose keys are below limit, from its state
+// before the update (alive0, age0).
+__device__ __forceinline__ EdgeState edge_state(bool alive0, int32_t age0, int32_t x,
+                                                const Surv& sx, int32_t w, const Surv& sw,
+                                                int32_t max_age, unsigned long long limit) {
+  bool alive = alive0;
+  int32_t ag = alive0 ? age0 : 0;
+  bool rw = false;
+  const bool ex = sx.key < limit, ew = sw.key < limit;
+  if (ex && ew && sw.key < sx.key) {
+    rw = edge_event(alive, ag, sw.sec == x, max_age);
+    edge_event(alive, ag, sx.sec == w, max_age);
+  } else {
+    if (ex) edge_event(alive, ag, sx.sec == w, max_age);
+    if (ew) rw = edge_event(alive, ag, sw.sec == x, max_age);
+  }
+  return EdgeState{alive, ag, rw};
+}
+
+// f(w, alive0, age0, sw) for every unit w that can share an edge with x in this update, each
+// once: the neighbours before it (in ascending order), then the winners of the survivors
+// whose second is x, then the second of the step of x.
+template <typename F>
+__device__ __forceinline__ void for_each_incident(const LocalArgs& a, int32_t x, const Surv& sx,
+                                                  F&& f) {
+  const int32_t r0 = a.rp[x], l = a.rp[x + 1] - r0;
+  for (int32_t k = 0; k < l; ++k) {
+    const int32_t w = a.col[r0 + k];
+    f(w, true, a.age[r0 + k], surv_of(a, w));
+  }
+  // (a list holds distinct signals of this update, so it ends within m links; the bounds
+  // only keep a corrupted table from reading out of range)
+  int32_t steps = 0;
+  for (int32_t j = a.rhead[x]; j >= 0 && j < a.m && steps < a.m; j = a.rnext[j], ++steps) {
+    const int32_t b = a.winner[j];
+    if (b >= 0 && b < a.n && row_find(a.col, r0, l, b) < 0) f(b, false, 0, surv_of(a, b));
+  }
+  if (has_step(sx) && sx.sec >= 0 && sx.sec < a.n) {
+    const int32_t t = sx.sec;
+    const Surv st = surv_of(a, t);
+    // (a second whose own step has x as its second is in the list above)
+    if (row_find(a.col, r0, l, t) < 0 && !(has_step(st) && st.sec == x)) f(t, false, 0, st);
+  }
+}
+
+constexpr int kMoves = 8;  // moves of a unit gathered per pass
+
+// keys ascending (all ones = empty): keeps the kMoves smallest of keys and k
+__device__ __forceinline__ void keep_smallest(unsigned long long (&keys)[kMoves],
+                                              unsigned long long k) {
+#pragma unroll
+  for (int i = 0; i < kMoves; ++i) {
+    const bool lt = keys[i] < k;
+    const unsigned long long lo = lt ? keys[i] : k;
+    k = lt ? k : keys[i];
+    keys[i] = lo;
+  }
+}
+
+// Per unit: its moves in key order, its mark, its error (with the decay), and the length of
+// its row after the update (cnt, and per-workgroup sums in bsum).
+__global__ __launch_bounds__(kBlock) void wu_apply(LocalArgs a) {
+  __shared__ int32_t red[kBlock / 64];
+  const int32_t x = blockIdx.x * kBlock + threadIdx.x;
+  int32_t c = 0;
+  if (x < a.n) {
+    const Surv sx = surv_of(a, x);
+    float px = a.x[x], py = a.y[x], pz = a.z[x];
+    bool moved = false;
+    unsigned long long lo = 0;  // keys below lo were applied in earlier passes
+    for (;;) {
+      unsigned long long keys[kMoves];
+#pragma unroll
+      for (int i = 0; i < kMoves; ++i) keys[i] = ~0ull;
+      int32_t found = 0;
+      auto offer = [&](unsigned long long k) {
+        if (k < lo) return;
+        ++found;
+        keep_smallest(keys, k);
+      };
+      if (has_step(sx)) offer(sx.key);
+      for_each_incident(a, x, sx,
+                        [&](int32_t w, bool alive0, int32_t age0, const Surv& sw) {
+                          if (!has_step(sw)) return;
+                          if (sw.sec == x ||
+                              edge_state(alive0, age0, x, sx, w, sw, a.max_age, sw.key).alive)
+                            offer(sw.key);
+                        });
+#pragma unroll
+      for (int i = 0; i < kMoves; ++i) {
+        if (keys[i] == ~0ull) continue;
+        const int32_t j = static_cast<int32_t>(static_cast<uint32_t>(keys[i]));
+        const float eps = keys[i] == sx.key ? a.eps_b : a.eps_n;
+        float t;
+        t = a.sig[j] - px; t = eps * t; px = px + t;
+        t = a.sig[a.m + j] - py; t = eps * t; py = py + t;
+        t = a.sig[2 * a.m + j] - pz; t = eps * t; pz = pz + t;
+        moved = true;
+      }
+      if (found <= kMoves) break;
+      lo = keys[kMoves - 1] + 1;
+    }
+    if (moved) {
+      a.x[x] = px;
+      a.y[x] = py;
+      a.z[x] = pz;
+    }
+    // the row afterwards, and whether some step removed an edge of x and left it none
+    bool lone = false;
+    for_each_incident(a, x, sx, [&](int32_t w, bool alive0, int32_t age0, const Surv& sw) {
+      const EdgeState e = edge_state(alive0, age0, x, sx, w, sw, a.max_age, ~0ull);
+      c += e.alive ? 1 : 0;
+      if (e.removed_by_w && !lone) {
+        int32_t d = 0;
+        for_each_incident(a, x, sx, [&](int32_t v, bool al0, int32_t ag0, const Surv& sv) {
+          if (v != w && edge_state(al0, ag0, x, sx, v, sv, a.max_age, sw.key).alive) ++d;
+        });
+        lone = d == 0;
+      }
+    });
+    if (lone && !a.orphan[x]) {
+      a.orphan[x] = 1;
+      atomicAdd(&a.status[kStOrphans], 1);
+    }
+    float ev = a.err[x];
+    if (has_step(sx)) ev = ev + a.d1[static_cast<uint32_t>(sx.key)];
+    a.err[x] = ev * a.beta;
+    a.cnt[x] = c;
+  }
+  int32_t v = c;
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int32_t t = 0;
+    for (int k = 0; k < kBlock / 64; ++k) t += red[k];
+    a.bsum[blockIdx.x] = t;
+  }
+}
+
+// Per unit: its row after the update at the offset of the scanned lengths, ascending (the
+// neighbours before the update keep their order, each new edge is put in its place); and
+// the other parity's tables cleared.  out_total receives the number of half-edges.
+__global__ __launch_bounds__(kBlock) void wu_write(LocalArgs a, int32_t* out_total) {
+  __shared__ int32_t sc[kBlock];
+  __shared__ int32_t red[2 * kBlock / 64];
+  const int32_t x = blockIdx.x * kBlock + threadIdx.x;
+  const int32_t c = x < a.n ? a.cnt[x] : 0;
+  int32_t boff;
+  bool abort;
+  if (a.fold) {
+    int32_t total;
+    fold_offsets(a.bsum, a.nb, red, &boff, &total);
+    abort = fold_abort(total, a.cap, a.status, out_total);
+  } else {
+    boff = a.bsum[blockIdx.x];
+    abort = a.status[kStAbort] != 0;
+  }
+  sc[threadIdx.x] = c;
+  __syncthreads();
+  for (int off = 1; off < kBlock; off <<= 1) {
+    const int32_t v = threadIdx.x >= off ? sc[threadIdx.x - off] : 0;
+    __syncthreads();
+    sc[threadIdx.x] += v;
+    __syncthreads();
+  }
+  const int32_t hi_o = a.whi[a.par ^ 1];
+  const int32_t stride = static_cast<int32_t>(gridDim.x) * kBlock;
+  for (int32_t u = x; u < hi_o; u += stride) {
+    a.wkey_o[u] = ~0ull;
+    a.rhead_o[u] = -1;
+  }
+  if (x >= a.n) return;
+  if (abort) {
+    // the rewrite did not fit: a valid, empty adjacency (the state is flagged invalid)
+    a.rp2[x] = 0;
+    return;
+  }
+  const int32_t start = boff + sc[threadIdx.x] - c;
+  a.rp2[x] = start;
+  const Surv sx = surv_of(a, x);
+  int32_t e = start;
+  for_each_incident(a, x, sx, [&](int32_t w, bool alive0, int32_t age0, const Surv& sw) {
+    const EdgeState st = edge_state(alive0, age0, x, sx, w, sw, a.max_age, ~0ull);
+    if (!st.alive) return;
+    int32_t k = e;
+    if (!alive0)
+      for (; k > start && a.col2[k - 1] > w; --k) {
+        a.col2[k] = a.col2[k - 1];
+        a.age2[k] = a.age2[k - 1];
+      }
+    a.col2[k] = w;
+    a.age2[k] = st.age;
+    ++e;
+  });
+}
+
 }  // namespace
 
 hipError_t launch_winner_update(const DevState& s, int cur, int32_t n, const WinnerStep& w,
@@ -619,6 +927,34 @@ hipError_t launch_winner_update(const DevState& s, int cur, int32_t n, const Win
   wl_write<<<nb, kBlock, 0, st>>>(n, s.rp[nxt], s.len, s.col[nxt], s.age[nxt], s.cnt, s.bsum,
                                   s.rp[cur], s.col[cur], s.age[cur], nullptr, s.err, w.beta,
                                   s.status, fold, nb, w.half_cap, s.rp[cur] + n);
+  return hipGetLastError();
+}
+
+}  // namespace gsn
+
+namespace gsn {
+
+hipError_t launch_winner_local(const DevState& s, int cur, int par, int32_t n,
+                               const WinnerStep& w, hipStream_t st) {
+  const int nxt = cur ^ 1;
+  const int po = par ^ 1;
+  const size_t nm = static_cast<size_t>(w.n_max);
+  const int nb = blocks(n);
+  const int fold = nb <= kFoldBlocks;
+  LocalArgs a{w.sig, w.m, n, w.winner, w.second, w.d1, w.accepted, w.key_mode,
+              s.wkey + par * nm, s.wsec + par * nm, s.rhead + par * nm, s.rnext,
+              s.wkey + po * nm, s.rhead + po * nm, s.whi, par,
+              s.rp[cur], s.col[cur], s.age[cur], s.rp[nxt], s.col[nxt], s.age[nxt],
+              s.x, s.y, s.z, s.err, s.orphan, s.status, s.cnt, s.bsum,
+              w.eps_b, w.eps_n, w.beta, w.max_age, w.half_cap, nb, fold};
+  if (w.m > 0) wu_tables<<<blocks(w.m), kBlock, 0, st>>>(a);
+  wu_apply<<<nb, kBlock, 0, st>>>(a);
+  if (!fold) {
+    const hipError_t e = launch_scan_blocks(s.bsum, nb, w.half_cap, s.rp[nxt] + n, s.status,
+                                            -1, st);
+    if (e != hipSuccess) return e;
+  }
+  wu_write<<<nb, kBlock, 0, st>>>(a, s.rp[nxt] + n);
   return hipGetLastError();
 }
 
