@@ -256,9 +256,9 @@ struct DevState {
   // one-pass update of the winner-lock survivors (winner lock only; null otherwise): two
   // parities of survivor tables, parity q at offset q n_max, taken by successive updates in
   // turn
-  unsigned long long* wkey;        // [2 n_max]     key of the survivor a unit is winner of,
-                                   //               all ones for none
-  int32_t* wsec;                   // [2 n_max]     that survivor's second
+  unsigned long long* wkey;        // [2 n_max][2]  per unit: the key of the survivor it is the
+                                   //               winner of (all ones for none), and that
+                                   //               survivor's second (one 16-byte record)
   int32_t* rhead;                  // [2 n_max]     a survivor whose second is the unit, -1 none
   int32_t* rnext;                  // [m_max]       the next survivor with the same second
   int32_t* whi;                    // [2]           tables of parity q hold entries below whi[q]

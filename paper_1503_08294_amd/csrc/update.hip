@@ -742,8 +742,8 @@ __global__ void init_state(float* __restrict__ err, int32_t* __restrict__ ins,
                            int32_t* __restrict__ whi) {
   const int32_t i = blockIdx.x * kBlock + threadIdx.x;
   if (wkey && i < n_max) {
-    wkey[i] = ~0ull;
-    wkey[n_max + i] = ~0ull;
+    wkey[2 * i] = ~0ull;
+    wkey[2 * (n_max + i)] = ~0ull;
     rhead[i] = -1;
     rhead[n_max + i] = -1;
   }

@@ -608,8 +608,7 @@ struct LocalArgs {
   const float* d1;
   const uint8_t* accepted;
   int key_mode;
-  unsigned long long* wkey;  // tables of this update's parity
-  int32_t* wsec;
+  unsigned long long* wkey;  // tables of this update's parity (records of key and second)
   int32_t* rhead;
   int32_t* rnext;
   unsigned long long* wkey_o;  // tables of the other parity (cleared by wu_write)
@@ -645,8 +644,8 @@ __global__ void wu_tables(LocalArgs a) {
     raise_error(a.status, GSN_E_INVAL);
     return;
   }
-  a.wkey[b] = signal_key(a.d1[j], j, a.key_mode);
-  a.wsec[b] = s;
+  reinterpret_cast<ulonglong2*>(a.wkey)[b] =
+      make_ulonglong2(signal_key(a.d1[j], j, a.key_mode), static_cast<uint32_t>(s));
   a.rnext[j] = atomicExch(&a.rhead[s], j);
 }
 
@@ -656,7 +655,8 @@ struct Surv {
 };
 
 __device__ __forceinline__ Surv surv_of(const LocalArgs& a, int32_t u) {
-  return Surv{a.wkey[u], a.wsec[u]};
+  const ulonglong2 r = reinterpret_cast<const ulonglong2*>(a.wkey)[u];
+  return Surv{r.x, static_cast<int32_t>(static_cast<uint32_t>(r.y))};
 }
 
 __device__ __forceinline__ bool has_step(const Surv& s) { return s.key != ~0ull; }
@@ -712,9 +712,25 @@ template <typename F>
 __device__ __forceinline__ void for_each_incident(const LocalArgs& a, int32_t x, const Surv& sx,
                                                   F&& f) {
   const int32_t r0 = a.rp[x], l = a.rp[x + 1] - r0;
-  for (int32_t k = 0; k < l; ++k) {
-    const int32_t w = a.col[r0 + k];
-    f(w, true, a.age[r0 + k], surv_of(a, w));
+  // the row in batches of eight entries, each batch's entries and then their survivor
+  // records loaded together
+  for (int32_t k0 = 0; k0 < l; k0 += 8) {
+    int32_t w[8], g[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      w[i] = 0;
+      g[i] = 0;
+      if (k0 + i < l) {
+        w[i] = a.col[r0 + k0 + i];
+        g[i] = a.age[r0 + k0 + i];
+      }
+    }
+    Surv sw[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) sw[i] = k0 + i < l ? surv_of(a, w[i]) : Surv{~0ull, -1};
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      if (k0 + i < l) f(w[i], true, g[i], sw[i]);
   }
   // (a list holds distinct signals of this update, so it ends within m links; the bounds
   // only keep a corrupted table from reading out of range)
@@ -755,25 +771,23 @@ __global__ __launch_bounds__(kBlock) void wu_apply(LocalArgs a) {
     const Surv sx = surv_of(a, x);
     float px = a.x[x], py = a.y[x], pz = a.z[x];
     bool moved = false;
+    // one pass over the incident edges: the row length afterwards, whether a step of the
+    // other end removed one of them, and the moves (up to kMoves of them; more take further
+    // passes over the keys above those applied)
+    unsigned long long keys[kMoves];
     unsigned long long lo = 0;  // keys below lo were applied in earlier passes
-    for (;;) {
-      unsigned long long keys[kMoves];
-#pragma unroll
-      for (int i = 0; i < kMoves; ++i) keys[i] = ~0ull;
-      int32_t found = 0;
-      auto offer = [&](unsigned long long k) {
-        if (k < lo) return;
-        ++found;
-        keep_smallest(keys, k);
-      };
-      if (has_step(sx)) offer(sx.key);
-      for_each_incident(a, x, sx,
-                        [&](int32_t w, bool alive0, int32_t age0, const Surv& sw) {
-                          if (!has_step(sw)) return;
-                          if (sw.sec == x ||
-                              edge_state(alive0, age0, x, sx, w, sw, a.max_age, sw.key).alive)
-                            offer(sw.key);
-                        });
+    int32_t found = 0;
+    auto offer = [&](unsigned long long k) {
+      if (k < lo) return;
+      ++found;
+      keep_smallest(keys, k);
+    };
+    auto mover = [&](int32_t w, bool alive0, int32_t age0, const Surv& sw) {
+      if (has_step(sw) &&
+          (sw.sec == x || edge_state(alive0, age0, x, sx, w, sw, a.max_age, sw.key).alive))
+        offer(sw.key);
+    };
+    auto apply_moves = [&]() {
 #pragma unroll
       for (int i = 0; i < kMoves; ++i) {
         if (keys[i] == ~0ull) continue;
@@ -785,30 +799,48 @@ __global__ __launch_bounds__(kBlock) void wu_apply(LocalArgs a) {
         t = a.sig[2 * a.m + j] - pz; t = eps * t; pz = pz + t;
         moved = true;
       }
-      if (found <= kMoves) break;
+    };
+#pragma unroll
+    for (int i = 0; i < kMoves; ++i) keys[i] = ~0ull;
+    if (has_step(sx)) offer(sx.key);
+    bool removal = false;
+    for_each_incident(a, x, sx, [&](int32_t w, bool alive0, int32_t age0, const Surv& sw) {
+      const EdgeState e = edge_state(alive0, age0, x, sx, w, sw, a.max_age, ~0ull);
+      c += e.alive ? 1 : 0;
+      removal |= e.removed_by_w;
+      mover(w, alive0, age0, sw);
+    });
+    apply_moves();
+    while (found > kMoves) {
       lo = keys[kMoves - 1] + 1;
+      found = 0;
+#pragma unroll
+      for (int i = 0; i < kMoves; ++i) keys[i] = ~0ull;
+      if (has_step(sx)) offer(sx.key);
+      for_each_incident(a, x, sx, mover);
+      apply_moves();
     }
     if (moved) {
       a.x[x] = px;
       a.y[x] = py;
       a.z[x] = pz;
     }
-    // the row afterwards, and whether some step removed an edge of x and left it none
-    bool lone = false;
-    for_each_incident(a, x, sx, [&](int32_t w, bool alive0, int32_t age0, const Surv& sw) {
-      const EdgeState e = edge_state(alive0, age0, x, sx, w, sw, a.max_age, ~0ull);
-      c += e.alive ? 1 : 0;
-      if (e.removed_by_w && !lone) {
+    // removal mark: some step of the other end removed an edge of x and left it none
+    if (removal) {
+      bool lone = false;
+      for_each_incident(a, x, sx, [&](int32_t w, bool alive0, int32_t age0, const Surv& sw) {
+        if (lone || !edge_state(alive0, age0, x, sx, w, sw, a.max_age, ~0ull).removed_by_w)
+          return;
         int32_t d = 0;
         for_each_incident(a, x, sx, [&](int32_t v, bool al0, int32_t ag0, const Surv& sv) {
           if (v != w && edge_state(al0, ag0, x, sx, v, sv, a.max_age, sw.key).alive) ++d;
         });
         lone = d == 0;
+      });
+      if (lone && !a.orphan[x]) {
+        a.orphan[x] = 1;
+        atomicAdd(&a.status[kStOrphans], 1);
       }
-    });
-    if (lone && !a.orphan[x]) {
-      a.orphan[x] = 1;
-      atomicAdd(&a.status[kStOrphans], 1);
     }
     float ev = a.err[x];
     if (has_step(sx)) ev = ev + a.d1[static_cast<uint32_t>(sx.key)];
@@ -855,7 +887,7 @@ __global__ __launch_bounds__(kBlock) void wu_write(LocalArgs a, int32_t* out_tot
   const int32_t hi_o = a.whi[a.par ^ 1];
   const int32_t stride = static_cast<int32_t>(gridDim.x) * kBlock;
   for (int32_t u = x; u < hi_o; u += stride) {
-    a.wkey_o[u] = ~0ull;
+    a.wkey_o[2 * u] = ~0ull;
     a.rhead_o[u] = -1;
   }
   if (x >= a.n) return;
@@ -942,8 +974,8 @@ hipError_t launch_winner_local(const DevState& s, int cur, int par, int32_t n,
   const int nb = blocks(n);
   const int fold = nb <= kFoldBlocks;
   LocalArgs a{w.sig, w.m, n, w.winner, w.second, w.d1, w.accepted, w.key_mode,
-              s.wkey + par * nm, s.wsec + par * nm, s.rhead + par * nm, s.rnext,
-              s.wkey + po * nm, s.rhead + po * nm, s.whi, par,
+              s.wkey + 2 * par * nm, s.rhead + par * nm, s.rnext,
+              s.wkey + 2 * po * nm, s.rhead + po * nm, s.whi, par,
               s.rp[cur], s.col[cur], s.age[cur], s.rp[nxt], s.col[nxt], s.age[nxt],
               s.x, s.y, s.z, s.err, s.orphan, s.status, s.cnt, s.bsum,
               w.eps_b, w.eps_n, w.beta, w.max_age, w.half_cap, nb, fold};
