@@ -94,7 +94,7 @@ Layout layout_for(const gsn_params& p) {
   add(4 * (nm / kBlock + 2));  // 34 per-block half-edge changes, set 1
   const bool wl = p.lock_mode == 1;
   add(wl ? 32 * nm : 0);       // 35 survivor records (key, second), two parities
-  add(0);                      // 36 (unused)
+  add(wl ? 2 * nm : 0);        // 36 survivor flags, two parities
   add(wl ? 8 * nm : 0);        // 37 heads of the second lists, two parities
   add(wl ? 4 * mm : 0);        // 38 links of the second lists
   add(wl ? 8 : 0);             // 39 table bounds
@@ -142,6 +142,7 @@ void carve(const gsn_params& p, void* base, DevState* s) {
   s->bdelta[1] = reinterpret_cast<int32_t*>(b + L.off[34]);
   const bool wl = p.lock_mode == 1;
   s->wkey = wl ? reinterpret_cast<unsigned long long*>(b + L.off[35]) : nullptr;
+  s->wflag = wl ? reinterpret_cast<uint8_t*>(b + L.off[36]) : nullptr;
   s->rhead = wl ? reinterpret_cast<int32_t*>(b + L.off[37]) : nullptr;
   s->rnext = wl ? reinterpret_cast<int32_t*>(b + L.off[38]) : nullptr;
   s->whi = wl ? reinterpret_cast<int32_t*>(b + L.off[39]) : nullptr;
@@ -1069,6 +1070,7 @@ int gsn_import(gsn_net* net, int32_t n, const float* xyz, const float* err, int3
     fill_bytes(s.bdelta[1], 0, 4 * (nm / gsn::kBlock + 2));
     if (s.wkey) {
       fill_bytes(s.wkey, 0xff, 32 * nm);
+      fill_bytes(s.wflag, 0, 2 * nm);
       fill_bytes(s.rhead, 0xff, 8 * nm);
       fill_bytes(s.whi, 0, 8);
     }

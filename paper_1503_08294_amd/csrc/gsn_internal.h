@@ -259,6 +259,9 @@ struct DevState {
   unsigned long long* wkey;        // [2 n_max][2]  per unit: the key of the survivor it is the
                                    //               winner of (all ones for none), and that
                                    //               survivor's second (one 16-byte record)
+  uint8_t* wflag;                  // [2 n_max]     1 iff the unit has a survivor record: read
+                                   //               first, so that the records of the many
+                                   //               units without one are not fetched
   int32_t* rhead;                  // [2 n_max]     a survivor whose second is the unit, -1 none
   int32_t* rnext;                  // [m_max]       the next survivor with the same second
   int32_t* whi;                    // [2]           tables of parity q hold entries below whi[q]

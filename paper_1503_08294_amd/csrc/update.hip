@@ -738,12 +738,14 @@ __global__ void init_state(float* __restrict__ err, int32_t* __restrict__ ins,
                            int32_t* __restrict__ rem, unsigned long long* __restrict__ acc64,
                            int32_t n_max, int32_t* __restrict__ status,
                            int32_t* __restrict__ bd0, int32_t* __restrict__ bd1,
-                           unsigned long long* __restrict__ wkey, int32_t* __restrict__ rhead,
-                           int32_t* __restrict__ whi) {
+                           unsigned long long* __restrict__ wkey, uint8_t* __restrict__ wflag,
+                           int32_t* __restrict__ rhead, int32_t* __restrict__ whi) {
   const int32_t i = blockIdx.x * kBlock + threadIdx.x;
   if (wkey && i < n_max) {
     wkey[2 * i] = ~0ull;
     wkey[2 * (n_max + i)] = ~0ull;
+    wflag[i] = 0;
+    wflag[n_max + i] = 0;
     rhead[i] = -1;
     rhead[n_max + i] = -1;
   }
@@ -774,7 +776,8 @@ hipError_t launch_init(const DevState& s, int cur, int32_t, int32_t n_max, hipSt
       std::max<int64_t>(static_cast<int64_t>(n_max) + 1, std::max<int>(kStSlots, kRmWords));
   init_state<<<blocks(cover), kBlock, 0, st>>>(s.err, s.ins, s.orphan, s.rp[cur], s.lock,
                                                s.extra, s.rem, s.acc64, n_max, s.status,
-                                               s.bdelta[0], s.bdelta[1], s.wkey, s.rhead,
+                                               s.bdelta[0], s.bdelta[1], s.wkey, s.wflag,
+                                               s.rhead,
                                                s.whi);
   return hipGetLastError();
 }

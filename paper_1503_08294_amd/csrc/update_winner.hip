@@ -609,9 +609,11 @@ struct LocalArgs {
   const uint8_t* accepted;
   int key_mode;
   unsigned long long* wkey;  // tables of this update's parity (records of key and second)
+  uint8_t* wflag;            // 1 iff the unit has a record
   int32_t* rhead;
   int32_t* rnext;
   unsigned long long* wkey_o;  // tables of the other parity (cleared by wu_write)
+  uint8_t* wflag_o;
   int32_t* rhead_o;
   int32_t* whi;
   int par;
@@ -646,6 +648,7 @@ __global__ void wu_tables(LocalArgs a) {
   }
   reinterpret_cast<ulonglong2*>(a.wkey)[b] =
       make_ulonglong2(signal_key(a.d1[j], j, a.key_mode), static_cast<uint32_t>(s));
+  a.wflag[b] = 1;
   a.rnext[j] = atomicExch(&a.rhead[s], j);
 }
 
@@ -657,6 +660,11 @@ struct Surv {
 __device__ __forceinline__ Surv surv_of(const LocalArgs& a, int32_t u) {
   const ulonglong2 r = reinterpret_cast<const ulonglong2*>(a.wkey)[u];
   return Surv{r.x, static_cast<int32_t>(static_cast<uint32_t>(r.y))};
+}
+
+// The same, reading the unit's flag first and its record only if it has one.
+__device__ __forceinline__ Surv surv_flagged(const LocalArgs& a, int32_t u) {
+  return a.wflag[u] ? surv_of(a, u) : Surv{~0ull, -1};
 }
 
 __device__ __forceinline__ bool has_step(const Surv& s) { return s.key != ~0ull; }
@@ -725,9 +733,12 @@ __device__ __forceinline__ void for_each_incident(const LocalArgs& a, int32_t x,
         g[i] = a.age[r0 + k0 + i];
       }
     }
+    bool fl[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) fl[i] = k0 + i < l && a.wflag[w[i]] != 0;
     Surv sw[8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) sw[i] = k0 + i < l ? surv_of(a, w[i]) : Surv{~0ull, -1};
+    for (int i = 0; i < 8; ++i) sw[i] = fl[i] ? surv_of(a, w[i]) : Surv{~0ull, -1};
 #pragma unroll
     for (int i = 0; i < 8; ++i)
       if (k0 + i < l) f(w[i], true, g[i], sw[i]);
@@ -741,7 +752,7 @@ __device__ __forceinline__ void for_each_incident(const LocalArgs& a, int32_t x,
   }
   if (has_step(sx) && sx.sec >= 0 && sx.sec < a.n) {
     const int32_t t = sx.sec;
-    const Surv st = surv_of(a, t);
+    const Surv st = surv_flagged(a, t);
     // (a second whose own step has x as its second is in the list above)
     if (row_find(a.col, r0, l, t) < 0 && !(has_step(st) && st.sec == x)) f(t, false, 0, st);
   }
@@ -768,7 +779,7 @@ __global__ __launch_bounds__(kBlock) void wu_apply(LocalArgs a) {
   const int32_t x = blockIdx.x * kBlock + threadIdx.x;
   int32_t c = 0;
   if (x < a.n) {
-    const Surv sx = surv_of(a, x);
+    const Surv sx = surv_flagged(a, x);
     float px = a.x[x], py = a.y[x], pz = a.z[x];
     bool moved = false;
     // one pass over the incident edges: the row length afterwards, whether a step of the
@@ -888,6 +899,7 @@ __global__ __launch_bounds__(kBlock) void wu_write(LocalArgs a, int32_t* out_tot
   const int32_t stride = static_cast<int32_t>(gridDim.x) * kBlock;
   for (int32_t u = x; u < hi_o; u += stride) {
     a.wkey_o[2 * u] = ~0ull;
+    a.wflag_o[u] = 0;
     a.rhead_o[u] = -1;
   }
   if (x >= a.n) return;
@@ -898,7 +910,7 @@ __global__ __launch_bounds__(kBlock) void wu_write(LocalArgs a, int32_t* out_tot
   }
   const int32_t start = boff + sc[threadIdx.x] - c;
   a.rp2[x] = start;
-  const Surv sx = surv_of(a, x);
+  const Surv sx = surv_flagged(a, x);
   int32_t e = start;
   for_each_incident(a, x, sx, [&](int32_t w, bool alive0, int32_t age0, const Surv& sw) {
     const EdgeState st = edge_state(alive0, age0, x, sx, w, sw, a.max_age, ~0ull);
@@ -974,8 +986,8 @@ hipError_t launch_winner_local(const DevState& s, int cur, int par, int32_t n,
   const int nb = blocks(n);
   const int fold = nb <= kFoldBlocks;
   LocalArgs a{w.sig, w.m, n, w.winner, w.second, w.d1, w.accepted, w.key_mode,
-              s.wkey + 2 * par * nm, s.rhead + par * nm, s.rnext,
-              s.wkey + 2 * po * nm, s.rhead + po * nm, s.whi, par,
+              s.wkey + 2 * par * nm, s.wflag + par * nm, s.rhead + par * nm, s.rnext,
+              s.wkey + 2 * po * nm, s.wflag + po * nm, s.rhead + po * nm, s.whi, par,
               s.rp[cur], s.col[cur], s.age[cur], s.rp[nxt], s.col[nxt], s.age[nxt],
               s.x, s.y, s.z, s.err, s.orphan, s.status, s.cnt, s.bsum,
               w.eps_b, w.eps_n, w.beta, w.max_age, w.half_cap, nb, fold};
