@@ -705,15 +705,24 @@ int gsn_iterate(gsn_net* net, const float* sig, int32_t m, int32_t* winner, int3
   if (net->p.lock_mode != 0) {
     int rc = gsn_find_winners(net, sig, m, winner, second, d1, d2, stream);
     if (rc) return rc;
-    if ((rc = gsn_resolve_conflicts(net, m, winner, second, d1, accepted, stream))) return rc;
     if (net->p.lock_mode == 1 && m > 0) {
-      // the resolve leaves one survivor per winner: the update in one pass, no rounds
+      // the resolve leaves one survivor per winner: the update in one pass, no rounds (the
+      // resolve's check fills the survivor tables)
       hipStream_t st = as_stream(stream);
+      const gsn::WinnerTables tab = gsn::winner_tables(net->s, net->wpar, net->p.n_max);
+      {
+        TimedRegion tr(net, GSN_T_RESOLVE, st);
+        const hipError_t e = gsn::launch_resolve(net->s, net->cur, net->n, m, winner, second,
+                                                 d1, accepted, 1, net->p.key_mode, st, &tab);
+        tr.end();
+        if (e != hipSuccess) return GSN_E_HIP;
+      }
       TimedRegion t(net, GSN_T_UPDATE, st);
       gsn::WinnerStep w{sig, m, winner, second, d1, accepted, net->p.key_mode, net->p.eps_b,
                         net->p.eps_n, net->p.err_beta, net->p.max_age, 0, 0,
                         2 * static_cast<int64_t>(net->p.e_max), nullptr, net->p.n_max};
-      const hipError_t e = gsn::launch_winner_local(net->s, net->cur, net->wpar, net->n, w, st);
+      const hipError_t e =
+          gsn::launch_winner_local(net->s, net->cur, net->wpar, net->n, w, st, true);
       t.end();
       if (e != hipSuccess) return GSN_E_HIP;
       net->cur ^= 1;
@@ -721,6 +730,7 @@ int gsn_iterate(gsn_net* net, const float* sig, int32_t m, int32_t* winner, int3
       net->phase = kReady;
       return GSN_OK;
     }
+    if ((rc = gsn_resolve_conflicts(net, m, winner, second, d1, accepted, stream))) return rc;
     if ((rc = gsn_adapt(net, sig, m, winner, second, d1, accepted, stream))) return rc;
     return gsn_update_edges(net, m, winner, second, accepted, stream);
   }

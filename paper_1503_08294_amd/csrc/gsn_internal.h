@@ -377,11 +377,24 @@ hipError_t launch_scan_f16_dyn(const DevState& s, const StageBufs& b, int32_t n,
 hipError_t launch_scan_mfma(const DevState& s, const StageBufs& b, int32_t n, const float* sig,
                             int32_t m, int split, hipStream_t st, LaunchEvents ev = {});
 
+// The survivor tables of the one-pass winner-lock update (launch_winner_local) of parity par.
+struct WinnerTables {
+  unsigned long long* wkey;
+  uint8_t* wflag;
+  int32_t* rhead;
+  int32_t* rnext;
+  int32_t* whi;
+  int par;
+};
+WinnerTables winner_tables(const DevState& s, int par, int32_t n_max);
+
 // lock_mode: 0 = lock set {b, s} + N(b), 1 = the winner alone; key_mode: 0 = (d1 bits,
-// index), 1 = index
+// index), 1 = index.  With tables (winner alone only) the check also fills the survivor
+// tables of the one-pass update, which then skips that launch.
 hipError_t launch_resolve(const DevState& s, int cur, int32_t n, int32_t m,
                           const int32_t* winner, const int32_t* second, const float* d1,
-                          uint8_t* accepted, int lock_mode, int key_mode, hipStream_t st);
+                          uint8_t* accepted, int lock_mode, int key_mode, hipStream_t st,
+                          const WinnerTables* tables = nullptr);
 hipError_t launch_adapt(const DevState& s, int cur, int32_t n, const float* sig, int32_t m,
                         const int32_t* winner, const int32_t* second, const float* d1,
                         const uint8_t* accepted, float eps_b, float eps_n, float beta,
@@ -424,7 +437,7 @@ hipError_t launch_winner_update(const DevState& s, int cur, int32_t n, const Win
 // written into buffer cur ^ 1 with the error decay (grid_rounds and feedback are not used).
 // par selects the survivor tables; consecutive calls must alternate it.
 hipError_t launch_winner_local(const DevState& s, int cur, int par, int32_t n,
-                               const WinnerStep& w, hipStream_t st);
+                               const WinnerStep& w, hipStream_t st, bool tables_made = false);
 // The lock-set resolve, adaptation and edge update of one iteration: the claims (unless the
 // find's merge made them, claimed = true); the check fused with the accepted signals'
 // updates, taking the signals in the given order when order is not null (a permutation of

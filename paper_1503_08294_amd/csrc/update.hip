@@ -120,11 +120,12 @@ __global__ void rs_check(int32_t m, int32_t n, const int32_t* __restrict__ winne
                          const int32_t* __restrict__ rp, const int32_t* __restrict__ col,
                          unsigned long long* __restrict__ lock,
                          uint8_t* __restrict__ accepted, int winner_only, int key_mode,
-                         unsigned long long* __restrict__ acc64) {
+                         unsigned long long* __restrict__ acc64, WinnerTables tab) {
   __shared__ int32_t s_acc;
   if (threadIdx.x == 0) s_acc = 0;
   __syncthreads();
   const int32_t j = blockIdx.x * kBlock + threadIdx.x;
+  if (tab.wkey && j == 0) tab.whi[tab.par] = n;
   bool ok = false;
   if (j < m) {
     const int32_t b = winner[j], s = second[j];
@@ -143,6 +144,13 @@ __global__ void rs_check(int32_t m, int32_t n, const int32_t* __restrict__ winne
           visit(v);
         }
         if (!s_nb) visit(s);
+      }
+      if (ok && tab.wkey) {
+        // the survivor tables of the one-pass update (one survivor per winner here)
+        reinterpret_cast<ulonglong2*>(tab.wkey)[b] =
+            make_ulonglong2(key, static_cast<uint32_t>(s));
+        tab.wflag[b] = 1;
+        tab.rnext[j] = atomicExch(&tab.rhead[s], j);
       }
     }
     accepted[j] = ok ? 1 : 0;
@@ -784,14 +792,16 @@ hipError_t launch_init(const DevState& s, int cur, int32_t, int32_t n_max, hipSt
 
 hipError_t launch_resolve(const DevState& s, int cur, int32_t n, int32_t m,
                           const int32_t* winner, const int32_t* second, const float* d1,
-                          uint8_t* accepted, int lock_mode, int key_mode, hipStream_t st) {
+                          uint8_t* accepted, int lock_mode, int key_mode, hipStream_t st,
+                          const WinnerTables* tables) {
   const int wo = lock_mode == 1;
+  const WinnerTables tab = tables && wo ? *tables : WinnerTables{};
   // the lock words are all ones between calls (set at creation and import, released by
   // their holders in every check)
   rs_claim<<<blocks(m), kBlock, 0, st>>>(m, n, winner, second, d1, s.rp[cur], s.col[cur],
                                          s.lock, s.status, wo, key_mode);
   rs_check<<<blocks(m), kBlock, 0, st>>>(m, n, winner, second, d1, s.rp[cur], s.col[cur],
-                                         s.lock, accepted, wo, key_mode, s.acc64);
+                                         s.lock, accepted, wo, key_mode, s.acc64, tab);
   return hipGetLastError();
 }
 

@@ -978,8 +978,14 @@ hipError_t launch_winner_update(const DevState& s, int cur, int32_t n, const Win
 
 namespace gsn {
 
+WinnerTables winner_tables(const DevState& s, int par, int32_t n_max) {
+  const size_t nm = static_cast<size_t>(n_max);
+  return WinnerTables{s.wkey + 2 * par * nm, s.wflag + par * nm, s.rhead + par * nm, s.rnext,
+                      s.whi, par};
+}
+
 hipError_t launch_winner_local(const DevState& s, int cur, int par, int32_t n,
-                               const WinnerStep& w, hipStream_t st) {
+                               const WinnerStep& w, hipStream_t st, bool tables_made) {
   const int nxt = cur ^ 1;
   const int po = par ^ 1;
   const size_t nm = static_cast<size_t>(w.n_max);
@@ -991,7 +997,7 @@ hipError_t launch_winner_local(const DevState& s, int cur, int par, int32_t n,
               s.rp[cur], s.col[cur], s.age[cur], s.rp[nxt], s.col[nxt], s.age[nxt],
               s.x, s.y, s.z, s.err, s.orphan, s.status, s.cnt, s.bsum,
               w.eps_b, w.eps_n, w.beta, w.max_age, w.half_cap, nb, fold};
-  if (w.m > 0) wu_tables<<<blocks(w.m), kBlock, 0, st>>>(a);
+  if (w.m > 0 && !tables_made) wu_tables<<<blocks(w.m), kBlock, 0, st>>>(a);
   wu_apply<<<nb, kBlock, 0, st>>>(a);
   if (!fold) {
     const hipError_t e = launch_scan_blocks(s.bsum, nb, w.half_cap, s.rp[nxt] + n, s.status,
