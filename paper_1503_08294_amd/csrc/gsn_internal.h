@@ -148,6 +148,34 @@ __device__ __forceinline__ void spread_clear(int32_t* ctr, int tid) {
   if (tid < kSpreadParts) ctr[tid * kSpreadStride] = 0;
 }
 
+// Sum of v over a kBlock workgroup, valid in every thread: wave shuffles, then the wave
+// totals through LDS (wt holds kBlock / 64 words; one barrier before it may be reused).
+__device__ __forceinline__ int32_t block_sum(int32_t v, int32_t* wt) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  if ((threadIdx.x & 63) == 0) wt[threadIdx.x >> 6] = v;
+  __syncthreads();
+  int32_t t = 0;
+#pragma unroll
+  for (int w = 0; w < kBlock / 64; ++w) t += wt[w];
+  return t;
+}
+
+// Inclusive prefix sum of v over a kBlock workgroup in thread order: a shuffle scan per
+// wave, then the totals of the earlier waves through LDS (one barrier).
+__device__ __forceinline__ int32_t block_inclusive_scan(int32_t v, int32_t* wt) {
+  const int lane = static_cast<int>(threadIdx.x & 63), w = static_cast<int>(threadIdx.x >> 6);
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int32_t x = __shfl_up(v, o);
+    if (lane >= o) v += x;
+  }
+  if (lane == 63) wt[w] = v;
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < kBlock / 64; ++k) v += k < w ? wt[k] : 0;
+  return v;
+}
+
 // A rewrite of per-row counts into offsets (count -> scan of the per-workgroup sums ->
 // write) can skip the single-workgroup scan when it has at most kFoldBlocks workgroups:
 // each writing workgroup sums the block sums before its own and all of them itself.

@@ -6,8 +6,7 @@
 // + N(b_j) with a 64-bit atomic minimum of its key, and survives iff it holds every unit
 // of L_j.  Surviving lock sets are pairwise disjoint, which makes the adaptation and the
 // edge update write-disjoint: no atomics on positions, errors or rows, and the result
-// equals any sequential order (one thread per signal in the separate calls, a group of
-// eight lanes per signal in the fused iteration).  The adjacency is a symmetric CSR (row_ptr, col, age per half-edge),
+// equals any sequential order (a group of eight lanes per signal).  The adjacency is a symmetric CSR (row_ptr, col, age per half-edge),
 // rows ascending by neighbour; the edge update modifies ages in place, then rewrites a
 // compacted CSR into the other buffer (count -> scan -> scatter).
 #include "gsn_internal.h"
@@ -17,34 +16,6 @@ namespace {
 
 // Rows of up to this many entries (nearly all of them) are read in one batch of loads.
 constexpr int kShortRow = 8;
-
-// Sum of v over a kBlock workgroup, valid in every thread: wave shuffles, then the wave
-// totals through LDS (wt holds kBlock / 64 words; one barrier before it may be reused).
-__device__ __forceinline__ int32_t block_sum(int32_t v, int32_t* wt) {
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  if ((threadIdx.x & 63) == 0) wt[threadIdx.x >> 6] = v;
-  __syncthreads();
-  int32_t t = 0;
-#pragma unroll
-  for (int w = 0; w < kBlock / 64; ++w) t += wt[w];
-  return t;
-}
-
-// Inclusive prefix sum of v over a kBlock workgroup in thread order: a shuffle scan per
-// wave, then the totals of the earlier waves through LDS (one barrier).
-__device__ __forceinline__ int32_t block_inclusive_scan(int32_t v, int32_t* wt) {
-  const int lane = static_cast<int>(threadIdx.x & 63), w = static_cast<int>(threadIdx.x >> 6);
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int32_t x = __shfl_up(v, o);
-    if (lane >= o) v += x;
-  }
-  if (lane == 63) wt[w] = v;
-  __syncthreads();
-#pragma unroll
-  for (int k = 0; k < kBlock / 64; ++k) v += k < w ? wt[k] : 0;
-  return v;
-}
 
 // Position of neighbour v in the ascending row col[lo, hi), or -1.
 __device__ __forceinline__ int32_t find_in_span(const int32_t* __restrict__ col, int32_t lo,

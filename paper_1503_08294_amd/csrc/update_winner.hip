@@ -858,22 +858,15 @@ __global__ __launch_bounds__(kBlock) void wu_apply(LocalArgs a) {
     a.err[x] = ev * a.beta;
     a.cnt[x] = c;
   }
-  int32_t v = c;
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    int32_t t = 0;
-    for (int k = 0; k < kBlock / 64; ++k) t += red[k];
-    a.bsum[blockIdx.x] = t;
-  }
+  const int32_t t = block_sum(c, red);
+  if (threadIdx.x == 0) a.bsum[blockIdx.x] = t;
 }
 
 // Per unit: its row after the update at the offset of the scanned lengths, ascending (the
 // neighbours before the update keep their order, each new edge is put in its place); and
 // the other parity's tables cleared.  out_total receives the number of half-edges.
 __global__ __launch_bounds__(kBlock) void wu_write(LocalArgs a, int32_t* out_total) {
-  __shared__ int32_t sc[kBlock];
+  __shared__ int32_t wt[kBlock / 64];
   __shared__ int32_t red[2 * kBlock / 64];
   const int32_t x = blockIdx.x * kBlock + threadIdx.x;
   const int32_t c = x < a.n ? a.cnt[x] : 0;
@@ -887,14 +880,7 @@ __global__ __launch_bounds__(kBlock) void wu_write(LocalArgs a, int32_t* out_tot
     boff = a.bsum[blockIdx.x];
     abort = a.status[kStAbort] != 0;
   }
-  sc[threadIdx.x] = c;
-  __syncthreads();
-  for (int off = 1; off < kBlock; off <<= 1) {
-    const int32_t v = threadIdx.x >= off ? sc[threadIdx.x - off] : 0;
-    __syncthreads();
-    sc[threadIdx.x] += v;
-    __syncthreads();
-  }
+  const int32_t inc = block_inclusive_scan(c, wt);
   const int32_t hi_o = a.whi[a.par ^ 1];
   const int32_t stride = static_cast<int32_t>(gridDim.x) * kBlock;
   for (int32_t u = x; u < hi_o; u += stride) {
@@ -908,7 +894,7 @@ __global__ __launch_bounds__(kBlock) void wu_write(LocalArgs a, int32_t* out_tot
     a.rp2[x] = 0;
     return;
   }
-  const int32_t start = boff + sc[threadIdx.x] - c;
+  const int32_t start = boff + inc - c;
   a.rp2[x] = start;
   const Surv sx = surv_flagged(a, x);
   int32_t e = start;
