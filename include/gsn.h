@@ -224,7 +224,7 @@ int gsn_update_edges(gsn_net* net, int32_t m, const int32_t* winner, const int32
  * one survivor per winner unit, so each edge changes only in the steps of its two ends'
  * survivors: the update of gsn_adapt is computed per unit in one pass instead of rounds
  * (its moves applied in key order, its edges after the two steps that can change each,
- * its removal mark), in three launches after the resolve, with the same result.
+ * its removal mark), in two launches after the resolve, with the same result.
  * GSN_LOCK_SET_GREEDY runs the four steps.  Outputs: device arrays of length m.  Async. */
 int gsn_iterate(gsn_net* net, const float* sig, int32_t m, int32_t* winner, int32_t* second,
                 float* d1, float* d2, uint8_t* accepted, void* stream);

@@ -721,8 +721,7 @@ int gsn_iterate(gsn_net* net, const float* sig, int32_t m, int32_t* winner, int3
       gsn::WinnerStep w{sig, m, winner, second, d1, accepted, net->p.key_mode, net->p.eps_b,
                         net->p.eps_n, net->p.err_beta, net->p.max_age, 0, 0,
                         2 * static_cast<int64_t>(net->p.e_max), nullptr, net->p.n_max};
-      const hipError_t e =
-          gsn::launch_winner_local(net->s, net->cur, net->wpar, net->n, w, st, true);
+      const hipError_t e = gsn::launch_winner_local(net->s, net->cur, net->wpar, net->n, w, st);
       t.end();
       if (e != hipSuccess) return GSN_E_HIP;
       net->cur ^= 1;

@@ -460,12 +460,13 @@ struct WinnerStep {
 };
 hipError_t launch_winner_update(const DevState& s, int cur, int32_t n, const WinnerStep& w,
                                 hipStream_t st);
-// The same update in three launches, for survivors with pairwise distinct winners (those of
-// the winner-lock resolve): survivor tables, the moves with the new degrees, and the rows,
-// written into buffer cur ^ 1 with the error decay (grid_rounds and feedback are not used).
-// par selects the survivor tables; consecutive calls must alternate it.
+// The same update in two launches after the winner-lock resolve, whose check (launch_resolve
+// with the tables of parity par) leaves one survivor per winner and fills the survivor
+// tables: the moves with the new degrees, and the rows, written into buffer cur ^ 1 with the
+// error decay (grid_rounds and feedback are not used).  Consecutive calls must alternate
+// par.
 hipError_t launch_winner_local(const DevState& s, int cur, int par, int32_t n,
-                               const WinnerStep& w, hipStream_t st, bool tables_made = false);
+                               const WinnerStep& w, hipStream_t st);
 // The lock-set resolve, adaptation and edge update of one iteration: the claims (unless the
 // find's merge made them, claimed = true); the check fused with the accepted signals'
 // updates, taking the signals in the given order when order is not null (a permutation of

@@ -595,7 +595,9 @@ __global__ __launch_bounds__(kTailBlock) void wl_tail(RoundArgs a, int32_t grid_
 //   * its error grows by d1 in E_x.
 // The steps that can involve x are those of x, of its neighbours before the update, of the
 // survivors whose second is x (a list per unit, rhead / rnext), and that of the second of
-// E_x.  One thread per unit finds them: three launches and no rounds.  The tables have two
+// E_x.  The resolve's check fills the tables (the key and second of each winner's
+// survivor, and the list of the survivors by second); then one thread per unit finds the
+// steps: two launches and no rounds.  The tables have two
 // parities so that the update can clear the other parity while it reads its own: an update
 // with parity q finds tables q clean, fills them below n (whi[q] = n), and clears tables
 // q ^ 1 below whi[q ^ 1], which the previous update filled.
@@ -604,10 +606,7 @@ struct LocalArgs {
   const float* sig;
   int32_t m, n;
   const int32_t* winner;
-  const int32_t* second;
   const float* d1;
-  const uint8_t* accepted;
-  int key_mode;
   unsigned long long* wkey;  // tables of this update's parity (records of key and second)
   uint8_t* wflag;            // 1 iff the unit has a record
   int32_t* rhead;
@@ -634,23 +633,6 @@ struct LocalArgs {
   int32_t nb;
   int fold;
 };
-
-// Survivor tables: the key and second of the step each winner takes, and the list of the
-// survivors by second.  Requires pairwise distinct winners among the accepted signals.
-__global__ void wu_tables(LocalArgs a) {
-  const int32_t j = blockIdx.x * kBlock + threadIdx.x;
-  if (j == 0) a.whi[a.par] = a.n;
-  if (j >= a.m || !a.accepted[j]) return;
-  const int32_t b = a.winner[j], s = a.second[j];
-  if (!pair_ok(b, s, a.n)) {
-    raise_error(a.status, GSN_E_INVAL);
-    return;
-  }
-  reinterpret_cast<ulonglong2*>(a.wkey)[b] =
-      make_ulonglong2(signal_key(a.d1[j], j, a.key_mode), static_cast<uint32_t>(s));
-  a.wflag[b] = 1;
-  a.rnext[j] = atomicExch(&a.rhead[s], j);
-}
 
 struct Surv {
   unsigned long long key;  // all ones: the unit takes no step as a winner
@@ -971,19 +953,18 @@ WinnerTables winner_tables(const DevState& s, int par, int32_t n_max) {
 }
 
 hipError_t launch_winner_local(const DevState& s, int cur, int par, int32_t n,
-                               const WinnerStep& w, hipStream_t st, bool tables_made) {
+                               const WinnerStep& w, hipStream_t st) {
   const int nxt = cur ^ 1;
   const int po = par ^ 1;
   const size_t nm = static_cast<size_t>(w.n_max);
   const int nb = blocks(n);
   const int fold = nb <= kFoldBlocks;
-  LocalArgs a{w.sig, w.m, n, w.winner, w.second, w.d1, w.accepted, w.key_mode,
+  LocalArgs a{w.sig, w.m, n, w.winner, w.d1,
               s.wkey + 2 * par * nm, s.wflag + par * nm, s.rhead + par * nm, s.rnext,
               s.wkey + 2 * po * nm, s.wflag + po * nm, s.rhead + po * nm, s.whi, par,
               s.rp[cur], s.col[cur], s.age[cur], s.rp[nxt], s.col[nxt], s.age[nxt],
               s.x, s.y, s.z, s.err, s.orphan, s.status, s.cnt, s.bsum,
               w.eps_b, w.eps_n, w.beta, w.max_age, w.half_cap, nb, fold};
-  if (w.m > 0 && !tables_made) wu_tables<<<blocks(w.m), kBlock, 0, st>>>(a);
   wu_apply<<<nb, kBlock, 0, st>>>(a);
   if (!fold) {
     const hipError_t e = launch_scan_blocks(s.bsum, nb, w.half_cap, s.rp[nxt] + n, s.status,
