@@ -225,7 +225,9 @@ int gsn_update_edges(gsn_net* net, int32_t m, const int32_t* winner, const int32
  * survivors: the update of gsn_adapt is computed per unit in one pass instead of rounds
  * (its moves applied in key order, its edges after the two steps that can change each,
  * its removal mark), in two launches after the resolve, with the same result.
- * GSN_LOCK_SET_GREEDY runs the four steps.  Outputs: device arrays of length m.  Async. */
+ * With GSN_LOCK_SET_GREEDY the resolve runs its rounds and the fused update of GSN_LOCK_SET
+ * applies the accepted signals (disjoint lock sets) without claims or check.  Outputs:
+ * device arrays of length m.  Async. */
 int gsn_iterate(gsn_net* net, const float* sig, int32_t m, int32_t* winner, int32_t* second,
                 float* d1, float* d2, uint8_t* accepted, void* stream);
 

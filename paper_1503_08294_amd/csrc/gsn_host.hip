@@ -702,6 +702,26 @@ int gsn_iterate(gsn_net* net, const float* sig, int32_t m, int32_t* winner, int3
   if (!net || m < 0 || m > net->p.m_max) return GSN_E_INVAL;
   if (net->phase != kReady && net->phase != kFound) return GSN_E_STATE;
   if (m > 0 && !accepted) return GSN_E_INVAL;
+  if (net->p.lock_mode == 2) {
+    // greedy: the rounds of the resolve decide, then the lock-set rule's fused update applies
+    // the accepted signals (their lock sets are disjoint) in the staging's spatial order
+    const int32_t* order = nullptr;
+    int rc = find_impl(net, sig, m, winner, second, d1, d2, stream, nullptr, nullptr, &order);
+    if (rc) return rc;
+    if ((rc = gsn_resolve_conflicts(net, m, winner, second, d1, accepted, stream))) return rc;
+    hipStream_t st = as_stream(stream);
+    TimedRegion t(net, GSN_T_UPDATE, st);
+    const hipError_t e = gsn::launch_iterate_set(
+        net->s, net->cur, net->dpar, net->n, sig, m, winner, second, d1, accepted,
+        net->p.key_mode, net->p.eps_b, net->p.eps_n, net->p.err_beta, net->p.max_age,
+        2 * static_cast<int64_t>(net->p.e_max), true, order, st, accepted);
+    t.end();
+    if (e != hipSuccess) return GSN_E_HIP;
+    net->cur ^= 1;
+    net->dpar ^= 1;
+    net->phase = kReady;
+    return GSN_OK;
+  }
   if (net->p.lock_mode != 0) {
     int rc = gsn_find_winners(net, sig, m, winner, second, d1, d2, stream);
     if (rc) return rc;

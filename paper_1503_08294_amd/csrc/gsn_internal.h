@@ -472,11 +472,14 @@ hipError_t launch_winner_local(const DevState& s, int cur, int par, int32_t n,
 // updates, taking the signals in the given order when order is not null (a permutation of
 // 0..m-1, e.g. the staging's spatial order); the rewrite into buffer cur ^ 1 with the error
 // decay (one launch up to kFoldBlocks blocks of units, else degree count, scan and write).
+// With given (the acceptance of the greedy resolve, whose accepted lock sets are disjoint
+// as well) there are no claims and no check: the accepted signals are applied.
 hipError_t launch_iterate_set(const DevState& s, int cur, int dpar, int32_t n, const float* sig,
                               int32_t m, const int32_t* winner, const int32_t* second,
                               const float* d1, uint8_t* accepted, int key_mode, float eps_b,
                               float eps_n, float beta, int32_t max_age, int64_t half_cap,
-                              bool claimed, const int32_t* order, hipStream_t st);
+                              bool claimed, const int32_t* order, hipStream_t st,
+                              const uint8_t* given = nullptr);
 hipError_t launch_scan_blocks(int32_t* bsum, int32_t nb, int64_t cap, int32_t* out_total,
                               int32_t* status, int32_t slot, hipStream_t st);
 hipError_t launch_init(const DevState& s, int cur, int32_t n0, int32_t n_max,

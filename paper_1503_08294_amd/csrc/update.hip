@@ -166,6 +166,9 @@ struct FusedArgs {
   int32_t* apart;  // accepted signals of each workgroup (plain stores)
   int32_t* bdelta;  // change of the half-edge count of every block of kBlock units
   const int32_t* order;  // optional: the signals in a spatial order (a permutation of 0..m-1)
+  const uint8_t* given;  // optional: the acceptance decided already (the greedy resolve, whose
+                         // accepted lock sets are disjoint too): no lock word is read or
+                         // written and no statistic counted
 };
 
 // The fused kernels give each signal a group of kGroup lanes of one wave: lane q takes the
@@ -330,7 +333,8 @@ __global__ void fu_check_apply(FusedArgs a) {
   const int q = gt % kGroup;
   const int32_t j = p < a.m && a.order ? a.order[p] : p;
   bool ok = false;
-  if (p < a.m && j >= 0 && j < a.m) {
+  // (with the acceptance given, a rejected signal's group has nothing to load or do)
+  if (p < a.m && j >= 0 && j < a.m && (a.given == nullptr || a.given[j] != 0)) {
     const int32_t b = a.winner[j], s = a.second[j];
     const float dj = a.d1[j];
     const float sx = a.sig[j], sy = a.sig[a.m + j], sz = a.sig[2 * a.m + j];
@@ -339,12 +343,15 @@ __global__ void fu_check_apply(FusedArgs a) {
     if (pair_ok(b, s, a.n)) {
       const unsigned long long key = signal_key(dj, j, a.key_mode);
       const int32_t r0 = a.rp[b], r1 = a.rp[b + 1];
+      const bool gv = a.given != nullptr;
       // lane 0: the lock words, positions and error of b and s
       unsigned long long lb = 0, ls = 0;
       float bx = 0.0f, by = 0.0f, bz = 0.0f, be = 0.0f, tx = 0.0f, ty = 0.0f, tz = 0.0f;
       if (q == 0) {
-        lb = a.lock[b];
-        ls = a.lock[s];
+        if (!gv) {
+          lb = a.lock[b];
+          ls = a.lock[s];
+        }
         bx = a.x[b]; by = a.y[b]; bz = a.z[b];
         be = a.err[b];
         tx = a.x[s]; ty = a.y[s]; tz = a.z[s];
@@ -358,7 +365,7 @@ __global__ void fu_check_apply(FusedArgs a) {
       if (has0) {
         v0 = a.col[k0];
         g0 = a.age[k0];
-        l0 = a.lock[v0];
+        if (!gv) l0 = a.lock[v0];
         vx = a.x[v0]; vy = a.y[v0]; vz = a.z[v0];
         w0 = a.rp[v0];
         w1 = a.rp[v0 + 1];
@@ -366,6 +373,7 @@ __global__ void fu_check_apply(FusedArgs a) {
       const int32_t rk0 = has0 ? find_in_short_span(a.col, w0, w1, b) : -1;
       bool mine = true, is_s = false;
       auto visit = [&](int32_t u, unsigned long long word) {
+        if (gv) return;
         if (word == key) a.lock[u] = ~0ull; else mine = false;
       };
       if (has0) {
@@ -375,14 +383,14 @@ __global__ void fu_check_apply(FusedArgs a) {
       for (int32_t k = k0 + kGroup; k < r1; k += kGroup) {
         const int32_t v = a.col[k];
         is_s |= v == s;
-        visit(v, a.lock[v]);
+        if (!gv) visit(v, a.lock[v]);
       }
       const bool s_nb = group_bits(__ballot(is_s)) != 0;
       if (q == 0) {
         visit(b, lb);
         if (!s_nb) visit(s, ls);
       }
-      ok = group_bits(__ballot(!mine)) == 0;
+      ok = gv ? a.given[j] != 0 : group_bits(__ballot(!mine)) == 0;
       if (ok) {
         // move_unit's expression on positions already loaded
         auto move = [&](int32_t u, float eps, float px, float py, float pz) {
@@ -431,7 +439,7 @@ __global__ void fu_check_apply(FusedArgs a) {
     }
     if (q == 0) a.accepted[j] = ok ? 1 : 0;
   }
-  if (blockIdx.x == 0 && threadIdx.x == 0)
+  if (blockIdx.x == 0 && threadIdx.x == 0 && a.given == nullptr)
     atomicAdd(&a.acc64[kA64Resolved], static_cast<unsigned long long>(a.m));
   // the workgroup's accepted count goes to its own word; the degree count that follows
   // adds them with one atomic (hundreds of same-address atomics at the end of this launch
@@ -820,19 +828,22 @@ hipError_t launch_iterate_set(const DevState& s, int cur, int dpar, int32_t n, c
                               int32_t m, const int32_t* winner, const int32_t* second,
                               const float* d1, uint8_t* accepted, int key_mode, float eps_b,
                               float eps_n, float beta, int32_t max_age, int64_t half_cap,
-                              bool claimed, const int32_t* order, hipStream_t st) {
+                              bool claimed, const int32_t* order, hipStream_t st,
+                              const uint8_t* given) {
   const int nxt = cur ^ 1;
   int32_t* bd = s.bdelta[dpar];
   int32_t* bd_next = s.bdelta[dpar ^ 1];
   const int gb = blocks(static_cast<int64_t>(m) * kGroup);
+  // the accepted counts go to the statistics unless the resolve that decided them counted
+  const int32_t* apart = m > 0 && !given ? s.apart : nullptr;
   if (m > 0) {
-    if (!claimed)
+    if (!claimed && !given)
       fu_claim<<<gb, kBlock, 0, st>>>(m, n, winner, second, d1, s.rp[cur], s.col[cur], s.lock,
                                       s.status, key_mode);
     FusedArgs a{sig,      m,          n,          winner,  second,   d1,     key_mode,
                 s.rp[cur], s.col[cur], s.lock,     accepted, s.acc64, s.x,    s.y,
                 s.z,      s.err,      eps_b,      eps_n,   s.age[cur], s.ins, s.orphan,
-                s.status, max_age, s.apart, bd, order};
+                s.status, max_age, s.apart, bd, order, given};
     fu_check_apply<<<gb, kBlock, 0, st>>>(a);
   }
   // (with no units no signal is accepted, so skipping the rewrite loses nothing)
@@ -841,13 +852,11 @@ hipError_t launch_iterate_set(const DevState& s, int cur, int dpar, int32_t n, c
   if (nb <= kFoldBlocks) {
     ed_rewrite<<<nb, kBlock, 0, st>>>(n, s.rp[cur], s.col[cur], s.age[cur], s.ins, bd, bd_next,
                                       s.rp[nxt], s.col[nxt], s.age[nxt], s.status, nb, half_cap,
-                                      s.err, beta, m > 0 ? s.apart : nullptr, gb,
-                                      s.acc64 + kA64Accepted);
+                                      s.err, beta, apart, gb, s.acc64 + kA64Accepted);
     return hipGetLastError();
   }
   ed_count<<<nb, kBlock, 0, st>>>(n, s.rp[cur], s.age[cur], s.ins, s.cnt, s.bsum, s.err, beta,
-                                  m > 0 ? s.apart : nullptr, gb, s.acc64 + kA64Accepted,
-                                  bd_next);
+                                  apart, gb, s.acc64 + kA64Accepted, bd_next);
   scan_blocks<<<1, 1024, 0, st>>>(s.bsum, nb, half_cap, s.rp[nxt] + n, s.status, -1);
   ed_write<<<nb, kBlock, 0, st>>>(n, s.rp[cur], s.col[cur], s.age[cur], s.ins, s.cnt, s.bsum,
                                   s.rp[nxt], s.col[nxt], s.age[nxt], s.status, 0, nb, half_cap,
