@@ -369,7 +369,7 @@ int gsn_tune(gsn_net* net, int32_t key, int32_t value);
  *   GSN_T_FIND        all of gsn_find_winners
  *   GSN_T_RESOLVE, GSN_T_ADAPT, GSN_T_EDGES   all of the corresponding call
  *   GSN_T_UPDATE      the fused update of gsn_iterate (with GSN_LOCK_SET resolve, adapt
- *                     and edges; with GSN_LOCK_WINNER adapt and edges, the resolve being
+ *                     and edges; with the other rules adapt and edges, the resolve being
  *                     timed as GSN_T_RESOLVE) */
 enum { GSN_T_FIND_SCAN = 0, GSN_T_FIND = 1, GSN_T_RESOLVE = 2, GSN_T_ADAPT = 3,
        GSN_T_EDGES = 4, GSN_T_UPDATE = 5, GSN_T_COUNT = 6 };
