@@ -696,9 +696,7 @@ def main():
             prep(t)
         else:
             net.find_winners_grid(dev_sig[t], grid, grid_ws)
-            net.resolve_conflicts(m)
-            net.adapt(dev_sig[t])
-            net.update_edges(m)
+            net.update(dev_sig[t])
         if wl.grow:
             net.grow(t + 1, wl.insert_every)
 

@@ -231,6 +231,15 @@ int gsn_update_edges(gsn_net* net, int32_t m, const int32_t* winner, const int32
 int gsn_iterate(gsn_net* net, const float* sig, int32_t m, int32_t* winner, int32_t* second,
                 float* d1, float* d2, uint8_t* accepted, void* stream);
 
+/* The update of gsn_iterate (resolve, adapt and edges, fused as there) after any find: its
+ * outputs and the state afterwards are those of gsn_resolve_conflicts, gsn_adapt and
+ * gsn_update_edges called in order on the same arguments, so it serves the hash index
+ * (gsn_find_winners_grid) as well as the exhaustive search.  Call it after a find
+ * (GSN_E_STATE otherwise); it leaves the handle ready for gsn_grow.  Inputs as for
+ * gsn_adapt; output accepted (device uint8[m]).  Async. */
+int gsn_update(gsn_net* net, const float* sig, int32_t m, const int32_t* winner,
+               const int32_t* second, const float* d1, uint8_t* accepted, void* stream);
+
 /* count whole iterations (Sec. 2.2, the multi-signal loop) in one call: the result, the
  * state afterwards and the outputs (those of the last iteration) are exactly those of count
  * gsn_iterate calls in order over the batches sigs + 3 m k, k = 0 .. count - 1 (each batch

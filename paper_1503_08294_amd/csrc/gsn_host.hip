@@ -541,6 +541,63 @@ int find_impl(gsn_net* net, const float* sig, int32_t m, int32_t* winner, int32_
   return hip_ok(e);
 }
 
+// Resolve, adapt and edges after a find, fused where the rule allows (the outputs and state
+// of gsn_resolve_conflicts, gsn_adapt and gsn_update_edges in order).  claimed: the find's
+// merge made the lock-set claims; order: the signals in the staging's spatial order, or null.
+int update_impl(gsn_net* net, const float* sig, int32_t m, const int32_t* winner,
+                const int32_t* second, const float* d1, uint8_t* accepted, void* stream,
+                bool claimed, const int32_t* order) {
+  hipStream_t st = as_stream(stream);
+  const int64_t half_cap = 2 * static_cast<int64_t>(net->p.e_max);
+  if (net->p.lock_mode == 1) {
+    if (m == 0) {
+      int rc = gsn_resolve_conflicts(net, m, winner, second, d1, accepted, stream);
+      if (!rc) rc = gsn_adapt(net, sig, m, winner, second, d1, accepted, stream);
+      if (!rc) rc = gsn_update_edges(net, m, winner, second, accepted, stream);
+      return rc;
+    }
+    // the resolve leaves one survivor per winner: the update in one pass, no rounds (the
+    // resolve's check fills the survivor tables)
+    const gsn::WinnerTables tab = gsn::winner_tables(net->s, net->wpar, net->p.n_max);
+    {
+      TimedRegion tr(net, GSN_T_RESOLVE, st);
+      const hipError_t e = gsn::launch_resolve(net->s, net->cur, net->n, m, winner, second, d1,
+                                               accepted, 1, net->p.key_mode, st, &tab);
+      tr.end();
+      if (e != hipSuccess) return GSN_E_HIP;
+    }
+    TimedRegion t(net, GSN_T_UPDATE, st);
+    const gsn::WinnerStep w{sig, m, winner, second, d1, accepted, net->p.key_mode,
+                            net->p.eps_b, net->p.eps_n, net->p.err_beta, net->p.max_age, 0, 0,
+                            half_cap, nullptr, net->p.n_max};
+    const hipError_t e = gsn::launch_winner_local(net->s, net->cur, net->wpar, net->n, w, st);
+    t.end();
+    if (e != hipSuccess) return GSN_E_HIP;
+    net->cur ^= 1;
+    net->wpar ^= 1;
+    net->phase = kReady;
+    return GSN_OK;
+  }
+  // the lock sets: the fused check and update; greedy: the resolve's rounds decide, and the
+  // same update applies the accepted signals (disjoint lock sets) without claims or check
+  const bool greedy = net->p.lock_mode == 2;
+  if (greedy) {
+    const int rc = gsn_resolve_conflicts(net, m, winner, second, d1, accepted, stream);
+    if (rc) return rc;
+  }
+  TimedRegion t(net, GSN_T_UPDATE, st);
+  const hipError_t e = gsn::launch_iterate_set(
+      net->s, net->cur, net->dpar, net->n, sig, m, winner, second, d1, accepted,
+      net->p.key_mode, net->p.eps_b, net->p.eps_n, net->p.err_beta, net->p.max_age, half_cap,
+      greedy || claimed, order, st, greedy ? accepted : nullptr);
+  t.end();
+  if (e != hipSuccess) return GSN_E_HIP;
+  net->cur ^= 1;
+  net->dpar ^= 1;
+  net->phase = kReady;
+  return GSN_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -702,77 +759,23 @@ int gsn_iterate(gsn_net* net, const float* sig, int32_t m, int32_t* winner, int3
   if (!net || m < 0 || m > net->p.m_max) return GSN_E_INVAL;
   if (net->phase != kReady && net->phase != kFound) return GSN_E_STATE;
   if (m > 0 && !accepted) return GSN_E_INVAL;
-  if (net->p.lock_mode == 2) {
-    // greedy: the rounds of the resolve decide, then the lock-set rule's fused update applies
-    // the accepted signals (their lock sets are disjoint) in the staging's spatial order
-    const int32_t* order = nullptr;
-    int rc = find_impl(net, sig, m, winner, second, d1, d2, stream, nullptr, nullptr, &order);
-    if (rc) return rc;
-    if ((rc = gsn_resolve_conflicts(net, m, winner, second, d1, accepted, stream))) return rc;
-    hipStream_t st = as_stream(stream);
-    TimedRegion t(net, GSN_T_UPDATE, st);
-    const hipError_t e = gsn::launch_iterate_set(
-        net->s, net->cur, net->dpar, net->n, sig, m, winner, second, d1, accepted,
-        net->p.key_mode, net->p.eps_b, net->p.eps_n, net->p.err_beta, net->p.max_age,
-        2 * static_cast<int64_t>(net->p.e_max), true, order, st, accepted);
-    t.end();
-    if (e != hipSuccess) return GSN_E_HIP;
-    net->cur ^= 1;
-    net->dpar ^= 1;
-    net->phase = kReady;
-    return GSN_OK;
-  }
-  if (net->p.lock_mode != 0) {
-    int rc = gsn_find_winners(net, sig, m, winner, second, d1, d2, stream);
-    if (rc) return rc;
-    if (net->p.lock_mode == 1 && m > 0) {
-      // the resolve leaves one survivor per winner: the update in one pass, no rounds (the
-      // resolve's check fills the survivor tables)
-      hipStream_t st = as_stream(stream);
-      const gsn::WinnerTables tab = gsn::winner_tables(net->s, net->wpar, net->p.n_max);
-      {
-        TimedRegion tr(net, GSN_T_RESOLVE, st);
-        const hipError_t e = gsn::launch_resolve(net->s, net->cur, net->n, m, winner, second,
-                                                 d1, accepted, 1, net->p.key_mode, st, &tab);
-        tr.end();
-        if (e != hipSuccess) return GSN_E_HIP;
-      }
-      TimedRegion t(net, GSN_T_UPDATE, st);
-      gsn::WinnerStep w{sig, m, winner, second, d1, accepted, net->p.key_mode, net->p.eps_b,
-                        net->p.eps_n, net->p.err_beta, net->p.max_age, 0, 0,
-                        2 * static_cast<int64_t>(net->p.e_max), nullptr, net->p.n_max};
-      const hipError_t e = gsn::launch_winner_local(net->s, net->cur, net->wpar, net->n, w, st);
-      t.end();
-      if (e != hipSuccess) return GSN_E_HIP;
-      net->cur ^= 1;
-      net->wpar ^= 1;
-      net->phase = kReady;
-      return GSN_OK;
-    }
-    if ((rc = gsn_resolve_conflicts(net, m, winner, second, d1, accepted, stream))) return rc;
-    if ((rc = gsn_adapt(net, sig, m, winner, second, d1, accepted, stream))) return rc;
-    return gsn_update_edges(net, m, winner, second, accepted, stream);
-  }
-  // the lock-set rule: the merge makes the claims where it can, then the fused update
+  // with the lock-set rule the merge of a staged find makes the claims where it can
   const gsn::ClaimArgs claim{net->n, net->s.rp[net->cur], net->s.col[net->cur], net->s.lock,
                              net->s.status, net->p.key_mode};
   bool claimed = false;
   const int32_t* order = nullptr;
-  int rc = find_impl(net, sig, m, winner, second, d1, d2, stream, &claim, &claimed, &order);
+  const int rc = find_impl(net, sig, m, winner, second, d1, d2, stream,
+                           net->p.lock_mode == 0 ? &claim : nullptr, &claimed, &order);
   if (rc) return rc;
-  hipStream_t st = as_stream(stream);
-  TimedRegion t(net, GSN_T_UPDATE, st);
-  const hipError_t e = gsn::launch_iterate_set(
-      net->s, net->cur, net->dpar, net->n, sig, m, winner, second, d1, accepted,
-      net->p.key_mode,
-      net->p.eps_b, net->p.eps_n, net->p.err_beta, net->p.max_age,
-      2 * static_cast<int64_t>(net->p.e_max), claimed, order, st);
-  t.end();
-  if (e != hipSuccess) return GSN_E_HIP;
-  net->cur ^= 1;
-  net->dpar ^= 1;
-  net->phase = kReady;
-  return GSN_OK;
+  return update_impl(net, sig, m, winner, second, d1, accepted, stream, claimed, order);
+}
+
+int gsn_update(gsn_net* net, const float* sig, int32_t m, const int32_t* winner,
+               const int32_t* second, const float* d1, uint8_t* accepted, void* stream) {
+  if (!net || m < 0 || m > net->p.m_max) return GSN_E_INVAL;
+  if (net->phase != kFound && net->phase != kResolved) return GSN_E_STATE;
+  if (m > 0 && (!sig || !winner || !second || !d1 || !accepted)) return GSN_E_INVAL;
+  return update_impl(net, sig, m, winner, second, d1, accepted, stream, false, nullptr);
 }
 
 int gsn_iterate_loop(gsn_net* net, const float* sigs, int32_t m, int32_t count,

@@ -136,6 +136,7 @@ _sig = {
     "gsn_adapt": (ctypes.c_int, [_P, _P, _I, _P, _P, _P, _P, _P]),
     "gsn_update_edges": (ctypes.c_int, [_P, _I, _P, _P, _P, _P]),
     "gsn_iterate": (ctypes.c_int, [_P, _P, _I, _P, _P, _P, _P, _P, _P]),
+    "gsn_update": (ctypes.c_int, [_P, _P, _I, _P, _P, _P, _P, _P]),
     "gsn_iterate_loop": (ctypes.c_int, [_P, _P, _I, _I, _P, _P, _P, _P, _P, _P]),
     "gsn_grow": (ctypes.c_int, [_P, _I, _I, _P]),
     "gsn_run_schedule": (ctypes.c_int, [_P, _P, ctypes.c_int64, ctypes.POINTER(gsn_schedule),
@@ -345,6 +346,15 @@ def gsn_iterate(net, sig: torch.Tensor, m: int, winner, second, d1, d2, accepted
            "gsn_iterate")
 
 
+def gsn_update(net, sig: torch.Tensor, m: int, winner, second, d1, accepted, stream=None):
+    _check(_lib.gsn_update(net, _dev(sig, torch.float32, 3 * m, "sig"), m,
+                           _dev(winner, torch.int32, m, "winner"),
+                           _dev(second, torch.int32, m, "second"),
+                           _dev(d1, torch.float32, m, "d1"),
+                           _dev(accepted, torch.uint8, m, "accepted"), _stream(stream)),
+           "gsn_update")
+
+
 def gsn_iterate_loop(net, sigs: torch.Tensor, m: int, count: int, winner, second, d1, d2,
                      accepted, stream=None):
     _check(_lib.gsn_iterate_loop(net, _dev(sigs, torch.float32, 3 * m * count, "sigs"), m,
@@ -515,6 +525,16 @@ class Network:
         b = self.buf
         gsn_iterate(self.h, sig, m, b.winner, b.second, b.d1, b.d2, b.accepted, self.stream)
         return b.winner[:m], b.second[:m], b.d1[:m], b.d2[:m], b.accepted[:m]
+
+    def update(self, sig: torch.Tensor, winner=None, second=None, d1=None):
+        """resolve -> adapt -> update_edges after a find, fused as in gsn_iterate (one
+        gsn_update call); returns the acceptance."""
+        m = sig.shape[1]
+        b = self.buf
+        gsn_update(self.h, sig, m, b.winner if winner is None else winner,
+                   b.second if second is None else second, b.d1 if d1 is None else d1,
+                   b.accepted, self.stream)
+        return b.accepted[:m]
 
     def iterate_loop(self, sigs: torch.Tensor):
         """One iteration per batch of ``sigs`` (a contiguous device (T, 3, m) tensor) in one

@@ -117,6 +117,45 @@ def test_iterations_with_the_index_match_the_oracle():
         np.testing.assert_array_equal(gs[f].numpy(), os_[f], err_msg=f)
 
 
+@pytest.mark.parametrize("lock_mode", [0, 1, 2])
+def test_fused_update_after_the_index_matches_the_oracle(lock_mode):
+    """find (indexed) -> gsn_update (resolve, adapt and edges fused as in gsn_iterate) in
+    each collision rule, with pruning (max_age 2), against the oracle's four steps."""
+    import torch
+    import oracle
+    from paper_1503_08294_amd import gsn
+    from paper_1503_08294_amd.clouds import WORKLOADS, SignalStream
+    wl = WORKLOADS["torus_grow"]
+    cloud = wl.make_cloud(50_000)
+    units = wl.make_units(cloud, 2_000)
+    kw = dict(n_max=2_100, e_max=8_400, m_max=1024, max_age=2, lock_mode=lock_mode)
+    g = gsn.Network(gsn.make_params(**kw), torch.from_numpy(np.ascontiguousarray(units)).cuda())
+    o = oracle.Oracle(oracle.Params(**kw), units, threads=oracle_threads())
+    stream = SignalStream(cloud, wl.signal_seed)
+    lo, h = (-1.4, -1.4, -0.4), 0.05
+    dims = (56, 56, 16)
+    grid = gsn.make_grid(lo, h, dims)
+    ws = g.grid_workspace(grid)
+    with pytest.raises(gsn.GsnError) as e:          # an update needs a find first
+        g.update(torch.zeros((3, 8), dtype=torch.float32, device="cuda"))
+    assert e.value.code == gsn.GSN_E_STATE
+    for t in range(10):
+        sig = stream.next(1024)
+        dsig = torch.from_numpy(sig).cuda()
+        g.find_winners_grid(dsig, grid, ws)
+        got = g.update(dsig).cpu().numpy()
+        w, s, d1, d2, _ = o.find_winners_grid(sig, lo, h, dims)
+        acc = o.resolve_conflicts(w, s, d1)
+        o.adapt(sig, w, s, d1, acc)
+        o.update_edges(w, s, acc)
+        np.testing.assert_array_equal(g.buf.winner[:1024].cpu().numpy(), w, err_msg=f"{t}")
+        np.testing.assert_array_equal(got, acc, err_msg=f"iteration {t}")
+        gs, os_ = g.export(), o.export()
+        for f in ("xyz", "err", "edges"):
+            np.testing.assert_array_equal(gs[f].numpy(), os_[f], err_msg=f"{t} {f}")
+    assert g.check() == 0
+
+
 def test_grid_arguments_are_checked():
     import torch
     from paper_1503_08294_amd import gsn
