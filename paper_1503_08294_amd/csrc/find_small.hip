@@ -179,8 +179,9 @@ __global__ __launch_bounds__(kBlock) void sm_merge(const unsigned long long* __r
       signal_key(__uint_as_float(static_cast<uint32_t>(ka >> 32)), j, claim.key_mode);
   if (tid == 0) {
     atomicMin(&claim.lock[bw], key);
-    atomicMin(&claim.lock[sw], key);
+    if (!claim.winner_only) atomicMin(&claim.lock[sw], key);
   }
+  if (claim.winner_only) return;
   for (int32_t k = claim.rp[bw] + tid; k < claim.rp[bw + 1]; k += kBlock)
     atomicMin(&claim.lock[claim.col[k]], key);
 }

@@ -562,7 +562,8 @@ int update_impl(gsn_net* net, const float* sig, int32_t m, const int32_t* winner
     {
       TimedRegion tr(net, GSN_T_RESOLVE, st);
       const hipError_t e = gsn::launch_resolve(net->s, net->cur, net->n, m, winner, second, d1,
-                                               accepted, 1, net->p.key_mode, st, &tab);
+                                               accepted, 1, net->p.key_mode, st, &tab,
+                                               claimed);
       tr.end();
       if (e != hipSuccess) return GSN_E_HIP;
     }
@@ -759,13 +760,13 @@ int gsn_iterate(gsn_net* net, const float* sig, int32_t m, int32_t* winner, int3
   if (!net || m < 0 || m > net->p.m_max) return GSN_E_INVAL;
   if (net->phase != kReady && net->phase != kFound) return GSN_E_STATE;
   if (m > 0 && !accepted) return GSN_E_INVAL;
-  // with the lock-set rule the merge of a staged find makes the claims where it can
+  // with the lock-set and winner-lock rules the find's merge makes the claims where it can
   const gsn::ClaimArgs claim{net->n, net->s.rp[net->cur], net->s.col[net->cur], net->s.lock,
-                             net->s.status, net->p.key_mode};
+                             net->s.status, net->p.key_mode, net->p.lock_mode == 1 ? 1 : 0};
   bool claimed = false;
   const int32_t* order = nullptr;
   const int rc = find_impl(net, sig, m, winner, second, d1, d2, stream,
-                           net->p.lock_mode == 0 ? &claim : nullptr, &claimed, &order);
+                           net->p.lock_mode != 2 ? &claim : nullptr, &claimed, &order);
   if (rc) return rc;
   return update_impl(net, sig, m, winner, second, d1, accepted, stream, claimed, order);
 }

@@ -386,6 +386,7 @@ struct ClaimArgs {
   unsigned long long* lock;
   int32_t* status;
   int key_mode;
+  int winner_only;  // the winner-lock rule's claim: the winner alone
 };
 hipError_t launch_stage_merge(const DevState& s, const StageBufs& b, int32_t m, int split,
                               int32_t* winner, int32_t* second, float* d1, float* d2,
@@ -419,10 +420,11 @@ WinnerTables winner_tables(const DevState& s, int par, int32_t n_max);
 // lock_mode: 0 = lock set {b, s} + N(b), 1 = the winner alone; key_mode: 0 = (d1 bits,
 // index), 1 = index.  With tables (winner alone only) the check also fills the survivor
 // tables of the one-pass update, which then skips that launch.
+// claimed: the find's merge made the claims already.
 hipError_t launch_resolve(const DevState& s, int cur, int32_t n, int32_t m,
                           const int32_t* winner, const int32_t* second, const float* d1,
                           uint8_t* accepted, int lock_mode, int key_mode, hipStream_t st,
-                          const WinnerTables* tables = nullptr);
+                          const WinnerTables* tables = nullptr, bool claimed = false);
 hipError_t launch_adapt(const DevState& s, int cur, int32_t n, const float* sig, int32_t m,
                         const int32_t* winner, const int32_t* second, const float* d1,
                         const uint8_t* accepted, float eps_b, float eps_n, float beta,

@@ -510,9 +510,10 @@ __global__ __launch_bounds__(kBlock) void st_place_seed(
 }
 
 // 32 signals per workgroup, 8 groups of lanes split the partial rows, merged in LDS.
-// With claim set (the fused lock-set iteration), the merge then makes the claims of each
-// signal's lock set {b, s} + N(b): its eight threads (one per group) take the neighbours
-// k = g, g + 8, ... of b's row, the first also b and s, each an atomic minimum of the key.
+// With claim set (the fused iteration), the merge then makes the claims of each signal's
+// lock set {b, s} + N(b): its eight threads (one per group) take the neighbours k = g,
+// g + 8, ... of b's row, the first also b and s, each an atomic minimum of the key (with
+// winner_only, the winner-lock rule's claim of b alone).
 __global__ __launch_bounds__(kBlock) void st_merge(const unsigned long long* __restrict__ part,
                                                    int32_t rows, int32_t m,
                                                    const int32_t* __restrict__ sperm,
@@ -580,8 +581,9 @@ __global__ __launch_bounds__(kBlock) void st_merge(const unsigned long long* __r
       signal_key(__uint_as_float(static_cast<uint32_t>(ka >> 32)), sj[c], claim.key_mode);
   if (g == 0) {
     atomicMin(&claim.lock[bw], key);
-    atomicMin(&claim.lock[sw], key);
+    if (!claim.winner_only) atomicMin(&claim.lock[sw], key);
   }
+  if (claim.winner_only) return;
   for (int32_t k = claim.rp[bw] + g; k < claim.rp[bw + 1]; k += 8)
     atomicMin(&claim.lock[claim.col[k]], key);
 }

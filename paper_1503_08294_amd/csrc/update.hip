@@ -772,13 +772,14 @@ hipError_t launch_init(const DevState& s, int cur, int32_t, int32_t n_max, hipSt
 hipError_t launch_resolve(const DevState& s, int cur, int32_t n, int32_t m,
                           const int32_t* winner, const int32_t* second, const float* d1,
                           uint8_t* accepted, int lock_mode, int key_mode, hipStream_t st,
-                          const WinnerTables* tables) {
+                          const WinnerTables* tables, bool claimed) {
   const int wo = lock_mode == 1;
   const WinnerTables tab = tables && wo ? *tables : WinnerTables{};
   // the lock words are all ones between calls (set at creation and import, released by
   // their holders in every check)
-  rs_claim<<<blocks(m), kBlock, 0, st>>>(m, n, winner, second, d1, s.rp[cur], s.col[cur],
-                                         s.lock, s.status, wo, key_mode);
+  if (!claimed)
+    rs_claim<<<blocks(m), kBlock, 0, st>>>(m, n, winner, second, d1, s.rp[cur], s.col[cur],
+                                           s.lock, s.status, wo, key_mode);
   rs_check<<<blocks(m), kBlock, 0, st>>>(m, n, winner, second, d1, s.rp[cur], s.col[cur],
                                          s.lock, accepted, wo, key_mode, s.acc64, tab);
   return hipGetLastError();
