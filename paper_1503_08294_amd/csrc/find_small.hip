@@ -171,7 +171,9 @@ __global__ __launch_bounds__(kBlock) void sm_merge(const unsigned long long* __r
   const unsigned long long ka = s1[0];
   const int32_t bw = static_cast<int32_t>(static_cast<uint32_t>(ka));
   const int32_t sw = static_cast<int32_t>(static_cast<uint32_t>(s2[0]));
-  if (!pair_ok(bw, sw, claim.n)) {
+  const bool ok = pair_ok(bw, sw, claim.n);
+  if (claim.pend && tid == 0) claim.pend[j] = ok ? 1 : 0;
+  if (!ok) {
     if (tid == 0) raise_error(claim.status, GSN_E_INVAL);
     return;
   }

@@ -582,9 +582,14 @@ int update_impl(gsn_net* net, const float* sig, int32_t m, const int32_t* winner
   // the lock sets: the fused check and update; greedy: the resolve's rounds decide, and the
   // same update applies the accepted signals (disjoint lock sets) without claims or check
   const bool greedy = net->p.lock_mode == 2;
-  if (greedy) {
-    const int rc = gsn_resolve_conflicts(net, m, winner, second, d1, accepted, stream);
-    if (rc) return rc;
+  if (greedy && m > 0) {
+    // (with claimed the find's merge made the first round's claims and the signal states)
+    TimedRegion tr(net, GSN_T_RESOLVE, st);
+    const hipError_t e = gsn::launch_resolve_greedy(
+        net->s, net->cur, net->n, m, winner, second, d1, accepted, net->p.key_mode,
+        net->grid_rounds ? net->grid_rounds : kGreedyGridRounds, st, claimed);
+    tr.end();
+    if (e != hipSuccess) return GSN_E_HIP;
   }
   TimedRegion t(net, GSN_T_UPDATE, st);
   const hipError_t e = gsn::launch_iterate_set(
@@ -746,7 +751,8 @@ int gsn_update_edges(gsn_net* net, int32_t m, const int32_t* winner, const int32
   TimedRegion t(net, GSN_T_EDGES, st);
   hipError_t e = gsn::launch_edges(net->s, net->cur, net->dpar, net->n, m, winner, second,
                                    accepted,
-                                   net->p.max_age, 2 * static_cast<int64_t>(net->p.e_max), st);
+                                   net->p.max_age, 2 * static_cast<int64_t>(net->p.e_max), st,
+                                   net->p.lock_mode == 2 ? net->s.extra : nullptr);
   t.end();
   if (e != hipSuccess) return GSN_E_HIP;
   net->cur ^= 1;
@@ -762,11 +768,12 @@ int gsn_iterate(gsn_net* net, const float* sig, int32_t m, int32_t* winner, int3
   if (m > 0 && !accepted) return GSN_E_INVAL;
   // with the lock-set and winner-lock rules the find's merge makes the claims where it can
   const gsn::ClaimArgs claim{net->n, net->s.rp[net->cur], net->s.col[net->cur], net->s.lock,
-                             net->s.status, net->p.key_mode, net->p.lock_mode == 1 ? 1 : 0};
+                             net->s.status, net->p.key_mode, net->p.lock_mode == 1 ? 1 : 0,
+                             net->p.lock_mode == 2 ? net->s.pend : nullptr};
   bool claimed = false;
   const int32_t* order = nullptr;
-  const int rc = find_impl(net, sig, m, winner, second, d1, d2, stream,
-                           net->p.lock_mode != 2 ? &claim : nullptr, &claimed, &order);
+  const int rc = find_impl(net, sig, m, winner, second, d1, d2, stream, &claim, &claimed,
+                           &order);
   if (rc) return rc;
   return update_impl(net, sig, m, winner, second, d1, accepted, stream, claimed, order);
 }

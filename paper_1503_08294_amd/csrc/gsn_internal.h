@@ -387,6 +387,8 @@ struct ClaimArgs {
   int32_t* status;
   int key_mode;
   int winner_only;  // the winner-lock rule's claim: the winner alone
+  uint8_t* pend;    // greedy rule (round 0 of its resolve): each signal's state, 1 pending,
+                    // 0 for an invalid pair (null otherwise)
 };
 hipError_t launch_stage_merge(const DevState& s, const StageBufs& b, int32_t m, int split,
                               int32_t* winner, int32_t* second, float* d1, float* d2,
@@ -429,17 +431,21 @@ hipError_t launch_adapt(const DevState& s, int cur, int32_t n, const float* sig,
                         const int32_t* winner, const int32_t* second, const float* d1,
                         const uint8_t* accepted, float eps_b, float eps_n, float beta,
                         hipStream_t st);
+// taken (greedy rule): the resolve's taken marks, cleared by the rewrite for the next call.
 hipError_t launch_edges(const DevState& s, int cur, int dpar, int32_t n, int32_t m,
                         const int32_t* winner, const int32_t* second,
                         const uint8_t* accepted, int32_t max_age, int64_t half_cap,
-                        hipStream_t st);
+                        hipStream_t st, int32_t* taken = nullptr);
 // Greedy lock-set resolve (resolve_greedy.hip): rounds of claims over L_j = {b, s} + N(b),
 // grid_rounds grid-wide, the rest in one workgroup.  Uses lock, extra (as the taken marks),
 // pend (signal states), rem and list.
+// claimed: the find's merge made the first round's claims and set the signal states (the
+// lock words are all ones and the taken marks zero between calls, so there is no set-up
+// launch).
 hipError_t launch_resolve_greedy(const DevState& s, int cur, int32_t n, int32_t m,
                                  const int32_t* winner, const int32_t* second, const float* d1,
                                  uint8_t* accepted, int key_mode, int grid_rounds,
-                                 hipStream_t st);
+                                 hipStream_t st, bool claimed = false);
 
 // The sequential-survivor update (update_winner.hip), all enqueued without a host sync:
 // the slack copy of the CSR in buffer cur ^ 1, grid_rounds grid-wide rounds, the remaining

@@ -216,6 +216,9 @@ __global__ __launch_bounds__(kTailBlock) void rg_tail(GreedyArgs a, uint8_t* acc
     atomicAdd(&a.acc64[kA64Resolved], static_cast<unsigned long long>(a.m));
     if (s_acc != 0) atomicAdd(&a.acc64[kA64Accepted], static_cast<unsigned long long>(s_acc));
   }
+  // round 0's pending count starts at zero in the next call, whose first claims the find's
+  // merge may make (then no launch of this call's kind clears it)
+  spread_clear(a.rem + rm_round(0), tid);
 }
 
 }  // namespace
@@ -223,13 +226,15 @@ __global__ __launch_bounds__(kTailBlock) void rg_tail(GreedyArgs a, uint8_t* acc
 hipError_t launch_resolve_greedy(const DevState& s, int cur, int32_t n, int32_t m,
                                  const int32_t* winner, const int32_t* second, const float* d1,
                                  uint8_t* accepted, int key_mode, int grid_rounds,
-                                 hipStream_t st) {
+                                 hipStream_t st, bool claimed) {
   GreedyArgs a{m, n, winner, second, d1, key_mode, s.rp[cur], s.col[cur], s.lock,
                s.extra, s.pend, s.rem, s.list, s.status, s.acc64};
-  rg_init<<<blocks(std::max(n, m)), kBlock, 0, st>>>(a);
+  if (!claimed) rg_init<<<blocks(std::max(n, m)), kBlock, 0, st>>>(a);
   const int g = static_cast<int>((m + kRoundBlock - 1) / kRoundBlock);
   for (int32_t t = 0; t < grid_rounds; ++t) {
-    rg_claim<<<g, kRoundBlock, 0, st>>>(a, t);
+    // (round 0's claims may come from the find's merge; the tail of the previous call left
+    // round 0's pending count at zero)
+    if (t > 0 || !claimed) rg_claim<<<g, kRoundBlock, 0, st>>>(a, t);
     rg_check<<<g, kRoundBlock, 0, st>>>(a, t);
   }
   rg_tail<<<1, kTailBlock, 0, st>>>(a, accepted);

@@ -573,7 +573,9 @@ __global__ __launch_bounds__(kBlock) void st_merge(const unsigned long long* __r
   const unsigned long long ka = sa[0][c];
   const int32_t bw = static_cast<int32_t>(static_cast<uint32_t>(ka));
   const int32_t sw = static_cast<int32_t>(static_cast<uint32_t>(sb[0][c]));
-  if (!pair_ok(bw, sw, claim.n)) {
+  const bool ok = pair_ok(bw, sw, claim.n);
+  if (claim.pend && g == 0) claim.pend[sj[c]] = ok ? 1 : 0;
+  if (!ok) {
     if (g == 0) raise_error(claim.status, GSN_E_INVAL);
     return;
   }

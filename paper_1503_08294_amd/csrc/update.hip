@@ -544,11 +544,12 @@ __global__ void ed_write(int32_t n, const int32_t* __restrict__ rp,
                          const int32_t* __restrict__ bsum, int32_t* __restrict__ rp_new,
                          int32_t* __restrict__ col_new, int32_t* __restrict__ age_new,
                          int32_t* __restrict__ status, int fold, int32_t nb, int64_t cap,
-                         int32_t* __restrict__ out_total) {
+                         int32_t* __restrict__ out_total, int32_t* __restrict__ taken) {
   __shared__ int32_t wt[kBlock / 64];
   __shared__ int32_t red[2 * kBlock / 64];
   const int32_t u = blockIdx.x * kBlock + threadIdx.x;
   const int32_t c = u < n ? cnt[u] : 0;
+  if (taken && u < n) taken[u] = 0;  // the greedy resolve's marks, clear for the next call
   int32_t boff, abort;
   if (fold) {
     int32_t total;
@@ -623,7 +624,7 @@ __global__ void ed_rewrite(int32_t n, const int32_t* __restrict__ rp,
                            int32_t* __restrict__ status, int32_t nb, int64_t cap,
                            float* __restrict__ err, float beta,
                            const int32_t* __restrict__ apart, int32_t napart,
-                           unsigned long long* __restrict__ acc) {
+                           unsigned long long* __restrict__ acc, int32_t* __restrict__ taken) {
   __shared__ int32_t wt[kBlock / 64];
   __shared__ int32_t wa[kBlock / 64];
   __shared__ int32_t red[2 * kBlock / 64];
@@ -633,6 +634,7 @@ __global__ void ed_rewrite(int32_t n, const int32_t* __restrict__ rp,
   // start of the block, all loaded before any is waited for
   const int32_t r0 = in ? rp[u] : 0, r1 = in ? rp[u + 1] : 0, l = r1 - r0;
   const int32_t extra = in ? ins[u] : -1;
+  if (taken && in) taken[u] = 0;  // the greedy resolve's marks, clear for the next call
   const float e = in && err ? err[u] : 0.0f;
   const int32_t base = rp[blockIdx.x * kBlock];
   int32_t cv[kShortRow], gv[kShortRow];
@@ -800,7 +802,7 @@ hipError_t launch_adapt(const DevState& s, int cur, int32_t n, const float* sig,
 hipError_t launch_edges(const DevState& s, int cur, int dpar, int32_t n, int32_t m,
                         const int32_t* winner, const int32_t* second,
                         const uint8_t* accepted, int32_t max_age, int64_t half_cap,
-                        hipStream_t st) {
+                        hipStream_t st, int32_t* taken) {
   const int nxt = cur ^ 1;
   int32_t* bd = s.bdelta[dpar];
   int32_t* bd_next = s.bdelta[dpar ^ 1];
@@ -813,7 +815,7 @@ hipError_t launch_edges(const DevState& s, int cur, int dpar, int32_t n, int32_t
   if (nb <= kFoldBlocks) {
     ed_rewrite<<<nb, kBlock, 0, st>>>(n, s.rp[cur], s.col[cur], s.age[cur], s.ins, bd, bd_next,
                                       s.rp[nxt], s.col[nxt], s.age[nxt], s.status, nb, half_cap,
-                                      nullptr, 1.0f, nullptr, 0, nullptr);
+                                      nullptr, 1.0f, nullptr, 0, nullptr, taken);
     return hipGetLastError();
   }
   ed_count<<<nb, kBlock, 0, st>>>(n, s.rp[cur], s.age[cur], s.ins, s.cnt, s.bsum, nullptr,
@@ -821,7 +823,7 @@ hipError_t launch_edges(const DevState& s, int cur, int dpar, int32_t n, int32_t
   scan_blocks<<<1, 1024, 0, st>>>(s.bsum, nb, half_cap, s.rp[nxt] + n, s.status, -1);
   ed_write<<<nb, kBlock, 0, st>>>(n, s.rp[cur], s.col[cur], s.age[cur], s.ins, s.cnt, s.bsum,
                                   s.rp[nxt], s.col[nxt], s.age[nxt], s.status, 0, nb, half_cap,
-                                  s.rp[nxt] + n);
+                                  s.rp[nxt] + n, taken);
   return hipGetLastError();
 }
 
@@ -837,6 +839,8 @@ hipError_t launch_iterate_set(const DevState& s, int cur, int dpar, int32_t n, c
   const int gb = blocks(static_cast<int64_t>(m) * kGroup);
   // the accepted counts go to the statistics unless the resolve that decided them counted
   const int32_t* apart = m > 0 && !given ? s.apart : nullptr;
+  // after the greedy resolve its taken marks are cleared for the next call
+  int32_t* taken = given ? s.extra : nullptr;
   if (m > 0) {
     if (!claimed && !given)
       fu_claim<<<gb, kBlock, 0, st>>>(m, n, winner, second, d1, s.rp[cur], s.col[cur], s.lock,
@@ -853,7 +857,7 @@ hipError_t launch_iterate_set(const DevState& s, int cur, int dpar, int32_t n, c
   if (nb <= kFoldBlocks) {
     ed_rewrite<<<nb, kBlock, 0, st>>>(n, s.rp[cur], s.col[cur], s.age[cur], s.ins, bd, bd_next,
                                       s.rp[nxt], s.col[nxt], s.age[nxt], s.status, nb, half_cap,
-                                      s.err, beta, apart, gb, s.acc64 + kA64Accepted);
+                                      s.err, beta, apart, gb, s.acc64 + kA64Accepted, taken);
     return hipGetLastError();
   }
   ed_count<<<nb, kBlock, 0, st>>>(n, s.rp[cur], s.age[cur], s.ins, s.cnt, s.bsum, s.err, beta,
@@ -861,7 +865,7 @@ hipError_t launch_iterate_set(const DevState& s, int cur, int dpar, int32_t n, c
   scan_blocks<<<1, 1024, 0, st>>>(s.bsum, nb, half_cap, s.rp[nxt] + n, s.status, -1);
   ed_write<<<nb, kBlock, 0, st>>>(n, s.rp[cur], s.col[cur], s.age[cur], s.ins, s.cnt, s.bsum,
                                   s.rp[nxt], s.col[nxt], s.age[nxt], s.status, 0, nb, half_cap,
-                                  s.rp[nxt] + n);
+                                  s.rp[nxt] + n, taken);
   return hipGetLastError();
 }
 
